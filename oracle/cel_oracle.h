@@ -1,0 +1,87 @@
+/*
+ * CPU oracle for the Celeritas placement hot path -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, single-threaded C implementation of what the GPU library
+ * computes, written from the paper's definitions (Xu et al., "Celeritas: Fast
+ * Optimizer for Large Dataflow Graphs", arXiv 2208.00184).  Only the tests, the
+ * package's smoke check and the benchmark's CPU-baseline leg may call it.  It
+ * shares no header, source, table or helper with the GPU library.
+ *
+ * Conventions: every pointer is host memory owned by the caller; all times are
+ * int64 nanoseconds and all sizes int64 bytes; a node's communication cost is
+ * c[v] = ceil(ob[v] / bw) + lat (the linear fit t = k d + b of Section 4.2.1 in
+ * integer form), paid once per consumer edge.
+ */
+#ifndef CEL_ORACLE_H
+#define CEL_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  ORC_OK = 0,
+  ORC_E_ARG = -1,      /* bad sizes, ranges or pointers */
+  ORC_E_CYCLE = -2,    /* graph is not a DAG */
+  ORC_E_OVERFLOW = -3, /* sum w + sum over edges c[src] >= 2^62 */
+  ORC_E_ORDER = -6     /* order not a topological permutation / clusters not ordered */
+};
+
+enum { ORC_COMM_OFF = 1 };                 /* orc_blevel: comm costs treated as 0 */
+enum { ORC_DP = 0, ORC_GREEDY = 1, ORC_DP_DIRECT = 2 }; /* orc_cluster modes */
+
+typedef struct {
+  int32_t n, m;
+  const int32_t *out_ptr, *out_idx; /* successors, CSR  [n+1], [m] */
+  const int32_t *in_ptr, *in_idx;   /* predecessors, CSC [n+1], [m] */
+  const int64_t *w;                 /* compute time (ns), >= 0 */
+  const int64_t *mem;               /* memory (bytes), >= 0 */
+  const int64_t *ob;                /* output tensor bytes, >= 0 */
+} orc_graph;
+
+typedef struct {
+  int32_t D;          /* 1..255 modelled devices */
+  const int64_t *cap; /* [D] memory caps (bytes) */
+  int64_t bw;         /* link bytes per ns, > 0 */
+  int64_t lat;        /* link latency ns, >= 0 */
+} orc_devices;
+
+/* Kahn levels (Section 4.2.2): level[v] = 0 for sources, else 1 + max level of
+ * predecessors.  order_id = ids sorted by (level, id); level_ptr[0..L] bucket
+ * offsets (capacity n+1); *n_levels = L. */
+int orc_topo_levels(const orc_graph *g, int32_t *level, int32_t *order_id,
+                    int32_t *level_ptr, int32_t *n_levels);
+
+/* b-level (eq. 3), t-level (eq. 2), critical path = max b-level, and the
+ * priority order sorted by (level asc, b-level desc, id asc).  tlevel and
+ * prio_order may be NULL. */
+int orc_blevel(const orc_graph *g, const orc_devices *d, const int32_t *level,
+               const int32_t *order_id, int32_t flags, int64_t *blevel,
+               int64_t *tlevel, int32_t *prio_order, int64_t *cp);
+
+/* Contiguous clustering of a topological order (Section 5.1.3, eq. 4-6):
+ * DP over breakpoints minimising inter-cluster comm with cluster length <= R
+ * and cluster memory <= M (a single node may exceed M).  M = -1 selects
+ * floor(min cap / 4). */
+int orc_cluster(const orc_graph *g, const orc_devices *d, const int32_t *order,
+                int32_t R, int64_t M, int32_t mode, int32_t *cluster_id,
+                int32_t *n_clusters, int64_t *cut_cost);
+
+/* Coarse graph + Adjusting Placement (Section 5.2, eq. 7-9, Algorithm 2).
+ * cluster_fin ([C] finish time of each cluster) may be NULL. */
+int orc_place(const orc_graph *g, const orc_devices *d, const int32_t *cluster_id,
+              int32_t n_clusters, uint8_t *cluster_dev, uint8_t *node_dev,
+              int64_t *cluster_fin, int64_t *coarse_makespan, int32_t *best_effort_count);
+
+/* Makespan of K placements (node_dev is [K][n]): nodes taken in `order`, each
+ * device runs its nodes first-in first-out, comm (eq. 7's indicator) paid only
+ * across devices.  start/finish ([K][n], by node id) may be NULL. */
+int orc_makespan(const orc_graph *g, const orc_devices *d, const int32_t *order,
+                 int32_t K, const uint8_t *node_dev, int64_t *start, int64_t *finish,
+                 int64_t *makespan);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,486 @@
+"""Pins for the CPU oracle: hand-traced fixtures, brute force, closed forms and
+invariants.  CPU only; the GPU path is not involved."""
+from __future__ import annotations
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from tests import brute as B
+from workloads import from_edges, make_config, make_random_dag
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def load(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+def hand6(D=2, cap=(60, 60)):
+    g = load("hand6.json")["graph"]
+    return from_edges(g["n"], g["edges"], g["w"], g["ob"], D, cap, g["bw"], g["lat"],
+                      mem=g["mem"])
+
+
+def small_dags(count=40, n_lo=1, n_hi=11):
+    for s in range(count):
+        n = n_lo + s % (n_hi - n_lo + 1)
+        yield make_random_dag(s, n, p_edge=0.25 + 0.05 * (s % 5), D=2 + s % 3,
+                              multi=(s % 4 == 0), zero_frac=0.2 if s % 6 == 0 else 0.0)
+
+
+# ------------------------------------------------------------------ fixtures
+
+
+def test_hand6_levels_blevel():
+    gd = load("hand6.json")
+    wl = hand6()
+    assert list(O.comm(wl)) == gd["comm"]
+    lev, oid, lp, L = O.topo_levels(wl)
+    e = gd["levels"]
+    assert list(lev) == e["level"] and list(oid) == e["order_id"]
+    assert list(lp) == e["level_ptr"] and L == e["L"]
+    bl, tl, pr, cp = O.blevel(wl, lev, oid)
+    e = gd["blevel"]
+    assert list(bl) == e["blevel"] and list(tl) == e["tlevel"] and cp == e["cp"]
+    assert list(pr) == e["prio_order"]
+    bl0, _, _, cp0 = O.blevel(wl, lev, oid, comm_off=True)
+    assert list(bl0) == e["blevel_comm_off"] and cp0 == e["cp0"]
+
+
+def test_hand6_cluster():
+    e = load("hand6.json")["cluster"]
+    wl = hand6()
+    for mode in (O.DP, O.DP_DIRECT):
+        cid, C, cut = O.cluster(wl, e["order"], e["R"], e["M"], mode)
+        assert list(cid) == e["cluster_id"] and C == e["n_clusters"] and cut == e["cut_cost"]
+    cid, C, cut = O.cluster(wl, e["order"], e["R"], e["M"], O.GREEDY)
+    assert list(cid) == e["greedy_cluster_id"] and cut == e["greedy_cut_cost"]
+
+
+def test_hand6_place():
+    gd = load("hand6.json")
+    e = gd["place"]
+    wl = hand6(e["D"], e["cap"])
+    cdev, ndev, span, be, fin = O.place(wl, gd["cluster"]["cluster_id"], 3, want_fin=True)
+    assert list(cdev) == e["cluster_dev"] and list(ndev) == e["node_dev"]
+    assert list(fin) == e["cluster_fin"] and span == e["coarse_makespan"]
+    assert be == e["best_effort_count"]
+
+
+def test_hand6_makespan():
+    e = load("hand6.json")["makespan"]
+    for case in e["cases"]:
+        wl = hand6(case["D"], [10 ** 6] * case["D"])
+        ms, st, fi = O.makespan(wl, e["order"], np.array(case["node_dev"], np.uint8))
+        assert ms[0] == case["makespan"], case["derivation"]
+        assert list(st[0]) == case["start"] and list(fi[0]) == case["finish"]
+
+
+@pytest.mark.parametrize("case", load("place_hand.json")["cases"], ids=lambda c: c["name"])
+def test_place_hand_cases(case):
+    n = case["n"]
+    wl = from_edges(n, case["edges"], case["w"], case["ob"], case["D"], case["cap"],
+                    case["bw"], case["lat"], mem=case["mem"])
+    cid = np.array(case.get("cluster_id", range(n)), np.int32)
+    C = int(cid.max()) + 1
+    cdev, ndev, span, be, fin = O.place(wl, cid, C, want_fin=True)
+    assert list(cdev) == case["cluster_dev"], case["derivation"]
+    assert list(fin) == case["cluster_fin"]
+    assert span == case["coarse_makespan"] and be == case["best_effort_count"]
+
+
+# ------------------------------------------------------------------- levels
+
+
+def check_level_characterisation(wl, lev, oid, lp, L):
+    """The three properties that determine the level function uniquely."""
+    n = wl.n
+    src, dst = wl.edges()
+    assert np.all(lev[src] < lev[dst])
+    indeg = np.diff(wl.in_ptr)
+    assert np.array_equal(lev == 0, indeg == 0)
+    # every node above level 0 has a predecessor exactly one level below
+    has = np.zeros(n, bool)
+    np.logical_or.at(has, dst, lev[src] == lev[dst] - 1)
+    assert np.all(has[lev > 0])
+    # order_id = ids sorted by (level, id); level_ptr = bucket offsets
+    assert np.array_equal(oid, np.lexsort((np.arange(n), lev)))
+    assert L == (int(lev.max()) + 1 if n else 0)
+    assert np.array_equal(lp, np.concatenate([[0], np.cumsum(np.bincount(lev, minlength=L))]))
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_levels_configs(cfg):
+    wl = make_config(cfg, 0)
+    check_level_characterisation(wl, *O.topo_levels(wl))
+
+
+def test_levels_brute():
+    for wl in small_dags():
+        lev, oid, lp, L = O.topo_levels(wl)
+        assert list(lev) == B.hop_levels(wl)
+        check_level_characterisation(wl, lev, oid, lp, L)
+
+
+def test_levels_degenerate():
+    wl = from_edges(0, [], [], [], 1, [1], 1, 0)
+    lev, oid, lp, L = O.topo_levels(wl)
+    assert L == 0 and list(lp) == [0]
+    wl = from_edges(1, [], [5], [3], 1, [1], 1, 0)
+    lev, oid, lp, L = O.topo_levels(wl)
+    assert L == 1 and list(lev) == [0] and list(lp) == [0, 1]
+
+
+@pytest.mark.parametrize("edges", [[(0, 0)], [(0, 1), (1, 0)], [(0, 1), (1, 2), (2, 1)]])
+def test_levels_cycle(edges):
+    n = 1 + max(max(e) for e in edges)
+    wl = from_edges(n, edges, [1] * n, [1] * n, 1, [1], 1, 0)
+    with pytest.raises(O.OracleError) as ei:
+        O.topo_levels(wl)
+    assert ei.value.code == O.E_CYCLE
+
+
+def test_bad_graph_rejected():
+    wl = hand6()
+    wl.in_idx = wl.in_idx.copy()
+    wl.in_idx[0] = (wl.in_idx[0] + 1) % wl.n  # CSC no longer matches CSR
+    with pytest.raises(O.OracleError) as ei:
+        O.topo_levels(wl)
+    assert ei.value.code == O.E_ARG
+    wl = hand6()
+    wl.w = wl.w.copy(); wl.w[2] = -1
+    with pytest.raises(O.OracleError):
+        O.topo_levels(wl)
+
+
+def test_overflow_rejected():
+    wl = from_edges(2, [(0, 1)], [5, 6], [2 ** 62 - 10, 0], 1, [1], 1, 0, mem=[1, 1])
+    lev, oid, _, _ = O.topo_levels(wl)
+    with pytest.raises(O.OracleError) as ei:
+        O.blevel(wl, lev, oid)
+    assert ei.value.code == O.E_OVERFLOW
+
+
+# ------------------------------------------------------------ b/t-level, CP
+
+
+def test_blevel_brute():
+    for wl in small_dags():
+        lev, oid, _, _ = O.topo_levels(wl)
+        bl, tl, pr, cp = O.blevel(wl, lev, oid)
+        assert list(bl) == B.blevel_brute(wl)
+        assert list(tl) == B.tlevel_brute(wl)
+        assert cp == (max(bl) if wl.n else 0)
+        bl0, _, _, cp0 = O.blevel(wl, lev, oid, comm_off=True)
+        assert list(bl0) == B.blevel_brute(wl, comm_off=True)
+        if wl.n:  # longest path through any node equals the critical path
+            assert int(np.max(tl + bl)) == cp
+
+
+def test_blevel_chain_closed_form():
+    n = 7
+    w = [5, 1, 8, 2, 9, 3, 4]
+    ob = [10, 0, 33, 7, 1, 2, 50]
+    wl = from_edges(n, [(i, i + 1) for i in range(n - 1)], w, ob, 1, [1], 4, 6)
+    lev, oid, _, _ = O.topo_levels(wl)
+    bl, tl, pr, cp = O.blevel(wl, lev, oid)
+    c = [math.ceil(o / 4) + 6 for o in ob]
+    assert cp == sum(w) + sum(c[:-1])
+    assert tl[-1] == sum(w[:-1]) + sum(c[:-1])
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_prio_order_properties(cfg):
+    wl = make_config(cfg, 1)
+    lev, oid, _, _ = O.topo_levels(wl)
+    bl, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=False)
+    assert np.array_equal(np.sort(pr), np.arange(wl.n))
+    key = np.lexsort((pr, -bl[pr], lev[pr]))  # already sorted iff identity
+    assert np.array_equal(key, np.arange(wl.n))
+    assert np.all(np.diff(lev[pr]) >= 0)
+
+
+# ---------------------------------------------------------------- clustering
+
+
+def test_cluster_brute_force():
+    rng = np.random.default_rng(7)
+    for s in range(30):
+        n = 2 + s % 11
+        wl = make_random_dag(100 + s, n, p_edge=0.35, D=2, multi=(s % 3 == 0))
+        lev, oid, _, _ = O.topo_levels(wl)
+        _, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=False)
+        R = int(rng.integers(1, n + 1))
+        tot = int(wl.mem.sum())
+        M = int(rng.integers(0, tot + 1))
+        c = B.comm(wl)
+        cid, C, cut = O.cluster(wl, pr, R, M, O.DP)
+        best = min(B.cut_of(wl, pr, bps, c) for bps in B.interval_partitions(n)
+                   if B.feasible(wl, pr, bps, R, M))
+        assert cut == best
+        # the returned partition is contiguous in the order, feasible, and attains S(n)
+        seq = cid[pr]
+        assert seq[0] == 0 and np.all(np.diff(seq) >= 0) and np.all(np.diff(seq) <= 1)
+        bps = [0] + list(np.nonzero(np.diff(seq))[0] + 1) + [n]
+        assert B.feasible(wl, pr, bps, R, M) and B.cut_of(wl, pr, bps, c) == cut
+        assert C == len(bps) - 1
+        # tie reading: each cluster [a, b) starts at the smallest i for which
+        # S(i) + cost(i, b) = S(b), with S from brute force over prefixes
+        pos = np.empty(n, np.int64); pos[pr] = np.arange(n)
+
+        def leave(a, b):  # eq. 4: comm leaving [a, b) for positions >= b
+            return sum(c[pr[p]] for p in range(a, b)
+                       for v in wl.out_idx[wl.out_ptr[pr[p]]:wl.out_ptr[pr[p] + 1]]
+                       if pos[v] >= b)
+
+        S = {0: 0}
+        for j in range(1, n + 1):
+            vals = [S[bp[-2]] + leave(bp[-2], j) for bp in ([i, j] for i in range(j))
+                    if B.feasible(wl, pr, bp, R, M)]
+            S[j] = min(vals)
+        assert S[n] == cut
+        for a, b in zip(bps[:-1], bps[1:]):
+            cands = [i for i in range(max(0, b - R), b)
+                     if B.feasible(wl, pr, [i, b], R, M) and S[i] + leave(i, b) == S[b]]
+            assert a == min(cands)
+
+
+def test_cluster_paths_agree():
+    """eq. 4 evaluated directly vs the eq. 5 recursion."""
+    for s in range(25):
+        wl = make_random_dag(300 + s, 4 + s % 20, p_edge=0.3, D=3, multi=(s % 2 == 0))
+        lev, oid, _, _ = O.topo_levels(wl)
+        _, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=False)
+        for R, M in ((3, -1), (7, int(wl.mem.sum()) // 3), (50, 10 ** 12)):
+            a = O.cluster(wl, pr, R, M, O.DP)
+            b = O.cluster(wl, pr, R, M, O.DP_DIRECT)
+            assert np.array_equal(a[0], b[0]) and a[1:] == b[1:]
+
+
+def test_cluster_special_cases():
+    wl = make_random_dag(5, 12, p_edge=0.4, D=2)
+    lev, oid, _, _ = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=False)
+    c = O.comm(wl)
+    src, _ = wl.edges()
+    cid, C, cut = O.cluster(wl, pr, 1, 10 ** 15, O.DP)
+    assert C == wl.n and cut == int(c[src].sum())
+    cid, C, cut = O.cluster(wl, pr, wl.n, int(wl.mem.sum()), O.DP)
+    assert C == 1 and cut == 0 and np.all(cid == 0)
+    cid, C, cut = O.cluster(wl, pr, 5, 0, O.DP)  # M = 0: singletons unless mem is 0
+    assert C == wl.n or np.any(wl.mem == 0)
+
+
+def check_cluster_invariants(wl, order, cid, C, cut, R, M):
+    seq = cid[order]
+    assert seq[0] == 0 and seq[-1] == C - 1
+    assert np.all(np.diff(seq) >= 0) and np.all(np.diff(seq) <= 1)
+    sizes = np.bincount(seq, minlength=C)
+    memsum = np.bincount(seq, weights=wl.mem[order].astype(np.float64), minlength=C)
+    assert sizes.max() <= R
+    assert np.all((memsum <= M) | (sizes == 1))
+    src, dst = wl.edges()
+    crossing = cid[src] != cid[dst]
+    assert cut == int(O.comm(wl)[src[crossing]].sum())
+    assert np.all(cid[src[crossing]] < cid[dst[crossing]])  # coarse graph is a DAG
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+@pytest.mark.parametrize("mode", [O.DP, O.GREEDY])
+def test_cluster_invariants_configs(cfg, mode):
+    wl = make_config(cfg, 0)
+    lev, oid, _, _ = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=False)
+    M = int(wl.cap.min()) // 4
+    cid, C, cut = O.cluster(wl, pr, 200, -1, mode)
+    check_cluster_invariants(wl, pr, cid, C, cut, 200, M)
+    if mode == O.GREEDY:  # every greedy cluster is maximal
+        seq = cid[pr]
+        ends = np.nonzero(np.diff(seq))[0] + 1
+        PM = np.concatenate([[0], np.cumsum(wl.mem[pr])])
+        starts = np.concatenate([[0], ends])
+        for a, b in zip(starts[:-1], ends):
+            assert b + 1 - a > 200 or PM[b + 1] - PM[a] > M
+
+
+def test_cluster_rejects_bad_order():
+    wl = hand6()
+    with pytest.raises(O.OracleError) as ei:
+        O.cluster(wl, [4, 0, 1, 2, 3, 5], 3, 40)
+    assert ei.value.code == O.E_ORDER
+    with pytest.raises(O.OracleError) as ei:
+        O.cluster(wl, [0, 0, 1, 2, 3, 5], 3, 40)
+    assert ei.value.code == O.E_ORDER
+
+
+# ----------------------------------------------------------------- placement
+
+
+def coarse_edges(wl, cid):
+    c = O.comm(wl)
+    src, dst = wl.edges()
+    a, b = cid[src], cid[dst]
+    keep = a != b
+    d = {}
+    for x, y, cc in zip(a[keep], b[keep], c[src[keep]]):
+        d[(int(x), int(y))] = d.get((int(x), int(y)), 0) + int(cc)
+    return d
+
+
+def check_schedule(wl, cid, C, cdev, fin, be):
+    W = np.bincount(cid, weights=wl.w.astype(np.float64), minlength=C).astype(np.int64)
+    MEM = np.bincount(cid, weights=wl.mem.astype(np.float64), minlength=C).astype(np.int64)
+    start = fin - W
+    assert np.all(start >= 0)
+    for (a, b), cc in coarse_edges(wl, cid).items():  # precedence + comm (eq. 7)
+        assert start[b] >= fin[a] + (cc if cdev[a] != cdev[b] else 0)
+    for d in range(wl.D):  # a device runs one cluster at a time
+        on = np.nonzero((cdev == d) & (W > 0))[0]
+        iv = sorted(zip(start[on], fin[on]))
+        for (s0, f0), (s1, f1) in zip(iv[:-1], iv[1:]):
+            assert f0 <= s1
+        if be == 0:  # memory caps respected
+            assert MEM[cdev == d].sum() <= wl.cap[d]
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_place_invariants_configs(cfg):
+    wl = make_config(cfg, 2)
+    lev, oid, _, _ = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=False)
+    cid, C, _ = O.cluster(wl, pr, 200, -1)
+    cdev, ndev, span, be, fin = O.place(wl, cid, C, want_fin=True)
+    check_schedule(wl, cid, C, cdev, fin, be)
+    assert span == fin.max()
+    assert np.array_equal(ndev, cdev[cid])
+
+
+def test_place_random_invariants():
+    for s in range(30):
+        wl = make_random_dag(500 + s, 6 + s % 25, p_edge=0.3, D=1 + s % 4,
+                             cap_frac=(1, 1 + s % 5), multi=(s % 3 == 0),
+                             zero_frac=0.25 if s % 5 == 0 else 0.0)
+        cid = np.arange(wl.n, dtype=np.int32)
+        # cluster ids must follow a topological order: use the levels order
+        lev, oid, _, _ = O.topo_levels(wl)
+        cid[oid] = np.arange(wl.n)
+        cdev, ndev, span, be, fin = O.place(wl, cid, wl.n, want_fin=True)
+        check_schedule(wl, cid, wl.n, cdev, fin, be)
+
+
+def test_place_single_device_closed_form():
+    wl = make_config(1, 0)
+    wl.D = 1; wl.cap = np.array([10 ** 15], np.int64)
+    lev, oid, _, _ = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=False)
+    cid, C, _ = O.cluster(wl, pr, 50, -1)
+    cdev, ndev, span, be, fin = O.place(wl, cid, C, want_fin=True)
+    assert np.all(cdev == 0) and span == int(wl.w.sum()) and be == 0
+
+
+def test_place_no_move_when_comm_dominates():
+    """With huge link latency every move test fails, so nothing leaves device 0."""
+    wl = make_config(1, 3)
+    wl.lat = 10 ** 12
+    wl.cap = np.full(wl.D, 10 ** 15, np.int64)
+    lev, oid, _, _ = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=False)
+    cid, C, _ = O.cluster(wl, pr, 30, -1)
+    cdev, _, span, be, _ = O.place(wl, cid, C, want_fin=True)
+    src, dst = wl.edges()
+    linked = set(cid[src[cid[src] != cid[dst]]]) | set(cid[dst[cid[src] != cid[dst]]])
+    assert be == 0 and all(cdev[t] == 0 for t in linked)
+
+
+def test_place_graham_bound_independent_tasks():
+    """No edges and no comm: Adjusting Placement is a list schedule, so the
+    makespan obeys Graham's bound sum(W)/D + (1 - 1/D) max(W)."""
+    rng = np.random.default_rng(11)
+    for s in range(20):
+        n = int(rng.integers(1, 60)); D = int(rng.integers(1, 6))
+        w = rng.integers(0, 100, n)
+        wl = from_edges(n, [], w, np.zeros(n, np.int64), D, [10 ** 9] * D, 1, 0)
+        cdev, _, span, be, fin = O.place(wl, np.arange(n, dtype=np.int32), n, want_fin=True)
+        assert span * D <= int(w.sum()) + (D - 1) * int(w.max())
+        # every task starts at the earliest time some device is free (list schedule)
+        assert be == 0
+
+
+# ------------------------------------------------------------------ makespan
+
+
+def lower_upper(wl, ndev):
+    lev, oid, _, _ = O.topo_levels(wl)
+    _, _, _, cp0 = O.blevel(wl, lev, oid, comm_off=True, want_tlevel=False, want_prio=False)
+    sw = int(wl.w.sum())
+    lb = max(cp0, -(-sw // wl.D))
+    src, dst = wl.edges()
+    ub = sw + int(O.comm(wl)[src[ndev[src] != ndev[dst]]].sum())
+    return lb, ub
+
+
+def test_makespan_augmented_and_bounds():
+    rng = np.random.default_rng(3)
+    for wl in small_dags(60, 1, 40):
+        lev, oid, _, _ = O.topo_levels(wl)
+        _, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=False)
+        for _ in range(3):
+            ndev = rng.integers(0, wl.D, wl.n).astype(np.uint8)
+            ms, st, fi = O.makespan(wl, pr, ndev)
+            ref, f = B.makespan_augmented(wl, pr, ndev)
+            assert ms[0] == ref and list(fi[0]) == f
+            assert np.array_equal(st[0], fi[0] - wl.w)
+            lb, ub = lower_upper(wl, ndev)
+            assert lb <= ms[0] <= ub
+
+
+def test_makespan_closed_forms():
+    for wl in small_dags(30, 2, 30):
+        lev, oid, _, _ = O.topo_levels(wl)
+        bl, tl, pr, cp = O.blevel(wl, lev, oid)
+        ms, _, _ = O.makespan(wl, pr, np.zeros(wl.n, np.uint8))
+        assert ms[0] == int(wl.w.sum())  # one device: no comm, no idle time
+        if wl.n <= 255:  # every op on its own device: the critical path
+            wl.D = wl.n; wl.cap = np.full(wl.n, 10 ** 12, np.int64)
+            ms, st, fi = O.makespan(wl, pr, np.arange(wl.n, dtype=np.uint8))
+            assert ms[0] == cp and np.array_equal(fi[0], tl + wl.w)
+
+
+def test_makespan_alternating_chain():
+    n = 9
+    w = np.arange(1, n + 1) * 3
+    ob = np.arange(n) * 11
+    wl = from_edges(n, [(i, i + 1) for i in range(n - 1)], w, ob, 2, [1, 1], 5, 2)
+    ms, _, _ = O.makespan(wl, np.arange(n), (np.arange(n) % 2).astype(np.uint8))
+    c = -(-ob // 5) + 2
+    assert ms[0] == w.sum() + c[:-1].sum()
+
+
+def test_makespan_brute_force_opt_bound():
+    for s in range(12):
+        n = 3 + s % 5
+        wl = make_random_dag(700 + s, n, p_edge=0.4, D=2 + s % 2)
+        lev, oid, _, _ = O.topo_levels(wl)
+        _, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=False)
+        P = np.array(list(B.all_placements(n, wl.D)), np.uint8)
+        ms, _, _ = O.makespan(wl, pr, P, want_times=False)
+        lb = lower_upper(wl, P[0])[0]
+        assert ms.min() >= lb
+        for k in range(0, len(P), max(1, len(P) // 7)):  # batched row == single call
+            assert O.makespan(wl, pr, P[k], want_times=False)[0][0] == ms[k]
+        cid = np.empty(n, np.int32); cid[pr] = np.arange(n)
+        _, ndev, _, _ = O.place(wl, cid, n)
+        assert ms.min() <= O.makespan(wl, pr, ndev, want_times=False)[0][0]
+
+
+def test_makespan_rejects_bad_device():
+    wl = hand6()
+    with pytest.raises(O.OracleError) as ei:
+        O.makespan(wl, [1, 0, 3, 2, 4, 5], np.array([0, 1, 2, 0, 0, 0], np.uint8))
+    assert ei.value.code == O.E_ARG
