@@ -1,0 +1,159 @@
+/*
+ * libcel -- MI355X (gfx950) implementation of the data-parallel hot path of
+ * Celeritas's placement optimiser (Xu, Liao, Xie, Zhou, "Celeritas: Fast
+ * Optimizer for Large Dataflow Graphs", arXiv 2208.00184):
+ *
+ *   cel_topo_levels  level-synchronous topological ordering      (Section 4.2.2)
+ *   cel_blevel       b-level / t-level / critical path, priority  (Section 5.1.3, eq. 2-3)
+ *   cel_cluster      memory-capped contiguous clustering (DP)     (Section 5.1.3, eq. 4-6)
+ *   cel_place        coarse graph + Adjusting Placement           (Section 5.2, eq. 7-9, Alg. 2)
+ *   cel_makespan     makespan of one or K placements              (Section 5.2, eq. 7)
+ *
+ * Conventions (all entry points):
+ *  - Arrays are DEVICE pointers owned by the caller unless marked (host).  The
+ *    library never frees or keeps a caller pointer after it returns.
+ *  - Work is enqueued on `stream`; every call returns after its results are
+ *    complete (it synchronises `stream` once to read its status and scalar
+ *    outputs).  Scratch memory is taken from the device's stream-ordered pool
+ *    and returned before the call ends.
+ *  - Times are int64 nanoseconds, sizes int64 bytes, indices int32.  A node's
+ *    communication time is c[v] = ceil(ob[v] / bw) + lat (the paper's linear
+ *    fit t = k*d + b, Section 4.2.1, in integer form), paid once per consumer
+ *    edge: always in b-/t-levels, only between different devices in EST and
+ *    makespan (eq. 7).  All results are exact integers, hence deterministic.
+ *  - Return value: CEL_OK or a negative CEL_E_* code; cel_last_error() gives a
+ *    message for the calling thread.  Outputs are unspecified after an error.
+ *  - Calls on the same device may run concurrently on different streams.
+ */
+#ifndef CEL_H
+#define CEL_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *hipStream_t; /* HIP's stream handle (NULL = default stream) */
+
+enum {
+  CEL_OK = 0,
+  CEL_E_ARG = -1,      /* NULL pointer, bad size or range, malformed CSR/CSC, negative w/mem/ob */
+  CEL_E_CYCLE = -2,    /* the graph has a cycle (self-loops included) */
+  CEL_E_OVERFLOW = -3, /* sum(w) + sum over edges of c[src] >= 2^62 */
+  CEL_E_HIP = -4,      /* a HIP runtime call failed */
+  CEL_E_NOMEM = -5,    /* scratch allocation failed */
+  CEL_E_ORDER = -6     /* an order/level/cluster argument is inconsistent with the graph */
+};
+
+/* cel_blevel flags */
+enum { CEL_COMM_OFF = 1 /* treat every c[v] as 0 (compute-only critical path) */ };
+
+/* cel_cluster modes */
+enum { CEL_CLUSTER_DP = 0, CEL_CLUSTER_GREEDY = 1 };
+
+/* Operator DAG, device pointers, read-only (Section 4.1: nodes are operations,
+ * edges are data transfers).  Multi-edges are allowed and counted separately. */
+typedef struct {
+  int32_t n, m;                       /* nodes, edges (both >= 0) */
+  const int32_t *out_ptr, *out_idx;   /* successors (CSR): [n+1], [m] */
+  const int32_t *in_ptr, *in_idx;     /* predecessors (CSC): [n+1], [m], same edges */
+  const int64_t *w;                   /* [n] compute time, ns, >= 0 */
+  const int64_t *mem;                 /* [n] memory, bytes, >= 0 */
+  const int64_t *ob;                  /* [n] output tensor bytes, >= 0 */
+} cel_graph;
+
+/* Modelled target devices (Section 4.1: devices with memory limits). */
+typedef struct {
+  int32_t D;                          /* 1..255 */
+  const int64_t *cap;                 /* (host) [D] memory caps, bytes, >= 0 */
+  int64_t bw;                         /* link bytes per ns, > 0 */
+  int64_t lat;                        /* link latency, ns, >= 0 */
+} cel_devices;
+
+/* Level-synchronous Kahn ordering (Section 4.2.2: repeatedly remove the nodes
+ * of indegree 0; one level = one round).  level[v] = 0 for a source, else
+ * 1 + max level of its predecessors.  order_id lists the ids sorted by
+ * (level, id); level_ptr[l] is the first position of level l in order_id
+ * (capacity n+1; entries 0..L are written, level_ptr[L] = n).
+ * Outputs: level [n], order_id [n], level_ptr [n+1], n_levels (host) = L.
+ * Errors: CEL_E_ARG, CEL_E_CYCLE, CEL_E_HIP, CEL_E_NOMEM. */
+int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *order_id,
+                    int32_t *level_ptr, int32_t *n_levels, hipStream_t stream);
+
+/* b-level (eq. 3): blevel[v] = w[v] for a sink, else w[v] + c[v] + max over
+ * successors s of blevel[s]; t-level (eq. 2): tlevel[v] = 0 for a source,
+ * else max over predecessors p of tlevel[p] + w[p] + c[p]; cp (host) = the
+ * critical path = max blevel (Section 5.1.3).  prio_order lists the ids sorted
+ * by (level ascending, blevel descending, id ascending): a level-monotone
+ * topological order that visits longer critical paths first.
+ * Inputs: level, level_ptr, order_id, n_levels as produced by cel_topo_levels
+ * (any order_id that lists each level's nodes contiguously is accepted).
+ * Outputs: blevel [n]; tlevel [n] or NULL; prio_order [n] or NULL; cp (host).
+ * flags: CEL_COMM_OFF.  Errors: CEL_E_ARG, CEL_E_ORDER, CEL_E_OVERFLOW,
+ * CEL_E_HIP, CEL_E_NOMEM. */
+int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_t *level,
+               const int32_t *level_ptr, const int32_t *order_id, int32_t n_levels,
+               int32_t flags, int64_t *blevel, int64_t *tlevel, int32_t *prio_order,
+               int64_t *cp, hipStream_t stream);
+
+/* Contiguous clustering of a topological order (Section 5.1.3, eq. 4-6;
+ * clusters are runs of consecutive positions, which keeps the coarse graph
+ * acyclic by Lemma 1).  DP mode minimises the total comm of edges between
+ * clusters, S(j) = min over i of S(i) + cost(i, j), subject to j - i <= R and
+ * the cluster's summed memory <= M (a single node may exceed M); among equal
+ * totals the smaller i (longer cluster) wins.  GREEDY mode grows each cluster
+ * while both limits hold.  M = -1 selects floor(min cap / 4).
+ * Inputs: order [n] any topological order (permutation with pos[u] < pos[v]
+ * on every edge); 1 <= R <= 4096; M >= -1.
+ * Outputs: cluster_id [n] (cluster 0 holds order[0]); n_clusters (host);
+ * cut_cost (host) = sum of c[u] over edges u->v in different clusters.
+ * Errors: CEL_E_ARG, CEL_E_ORDER, CEL_E_OVERFLOW, CEL_E_HIP, CEL_E_NOMEM. */
+int cel_cluster(const cel_graph *g, const cel_devices *d, const int32_t *order,
+                int32_t R, int64_t M, int32_t mode, int32_t *cluster_id,
+                int32_t *n_clusters, int64_t *cut_cost, hipStream_t stream);
+
+/* Coarse graph and Adjusting Placement (Section 5.2, Algorithm 2).  Cluster t
+ * has W = sum of its members' w, MEM = sum of their mem; the coarse edge a->b
+ * carries the sum of c[u] over edges u->v with u in a, v in b.  Clusters are
+ * visited in index order; for each device the start time is the earliest
+ * first-fit slot at or after pre_t (eq. 7), or infinite when the device's
+ * remaining memory is below MEM; the cluster stays on the previous cluster's
+ * device (device 0 for the first) unless EST(prev) - EST(best) > back_cost,
+ * the max comm to a successor (eq. 8-9); if every device is full it goes to the
+ * device with the most remaining memory (best effort).  Ties go to the lowest
+ * device id.  Nodes inherit their cluster's device.
+ * Inputs: cluster_id [n] with values in [0, n_clusters) and cluster_id[u] <=
+ * cluster_id[v] on every edge.
+ * Outputs: cluster_dev [C] uint8; node_dev [n] uint8; cluster_fin [C] or NULL;
+ * coarse_makespan (host) = max finish; best_effort_count (host).
+ * Errors: CEL_E_ARG, CEL_E_ORDER, CEL_E_OVERFLOW, CEL_E_HIP, CEL_E_NOMEM. */
+int cel_place(const cel_graph *g, const cel_devices *d, const int32_t *cluster_id,
+              int32_t n_clusters, uint8_t *cluster_dev, uint8_t *node_dev,
+              int64_t *cluster_fin, int64_t *coarse_makespan, int32_t *best_effort_count,
+              hipStream_t stream);
+
+/* Makespan of K placements (eq. 7 without insertion): nodes are taken in
+ * `order`; a node is ready when every predecessor p has finished, plus c[p]
+ * when p sits on another device; it starts at the later of ready and the end
+ * of the previous node placed on its device; makespan = latest finish.
+ * Inputs: order [n] level-monotone (level[order[k]] non-decreasing and
+ * level_ptr[l] <= k < level_ptr[l+1] for level l), e.g. prio_order from
+ * cel_blevel with level/level_ptr/n_levels from cel_topo_levels; K >= 1;
+ * node_dev [K][n] uint8 device per node id, each < D.
+ * Outputs: start, finish [K][n] by node id, or NULL; makespan [K] (device).
+ * Errors: CEL_E_ARG, CEL_E_ORDER, CEL_E_OVERFLOW, CEL_E_HIP, CEL_E_NOMEM. */
+int cel_makespan(const cel_graph *g, const cel_devices *d, const int32_t *order,
+                 const int32_t *level, const int32_t *level_ptr, int32_t n_levels,
+                 int32_t K, const uint8_t *node_dev, int64_t *start, int64_t *finish,
+                 int64_t *makespan, hipStream_t stream);
+
+/* Message describing the calling thread's last error ("" if none). */
+const char *cel_last_error(void);
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int cel_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

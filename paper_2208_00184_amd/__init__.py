@@ -1,0 +1,12 @@
+"""MI355X (gfx950) implementation of the Celeritas placement hot path.
+
+The computation lives in libcel.so (HIP kernels behind the C ABI of
+include/cel.h); this package is its thin Python binding.
+"""
+from ._binding import (CelError, Devices, Graph, blevel, cluster, lib, makespan, place,
+                       topo_levels, version, CLUSTER_DP, CLUSTER_GREEDY, COMM_OFF, EXPORTS,
+                       LIB_PATH)
+
+__all__ = ["CelError", "Devices", "Graph", "blevel", "cluster", "lib", "makespan", "place",
+           "topo_levels", "version", "CLUSTER_DP", "CLUSTER_GREEDY", "COMM_OFF", "EXPORTS",
+           "LIB_PATH"]

@@ -1,0 +1,206 @@
+// cel_blevel: b-level (eq. 3), t-level (eq. 2), critical path and the
+// priority order (Section 5.1.3).
+//
+// Nodes are first relabelled into the positions of the level order, so each
+// level is a contiguous range and per-node data is read coalesced.  The sweep
+// over levels runs in one workgroup (a level is a dependent step; workgroup
+// barriers cost tens of ns where a grid barrier costs microseconds).  Inside a
+// level every node pulls the values of its successors (b-level, reverse
+// sweep) or predecessors (t-level, forward sweep): no atomics, so the result
+// is exact and independent of scheduling.
+#include "cel_internal.h"
+
+namespace cel {
+
+constexpr int kSweepB = 1024;
+constexpr int kSweepHeavy = 64;  // degree above which a node is reduced by the whole block
+
+// per position: w and w + c (c = 0 with CEL_COMM_OFF)
+__global__ void k_node_costs(int32_t n, const int32_t *order, const int64_t *w, const int64_t *ob,
+                             int64_t bw, int64_t lat, int comm_off, int64_t *wp, int64_t *wcp,
+                             const Status *st) {
+  if (failed(st)) return;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t v = order[p];
+    const int64_t wv = w[v];
+    wp[p] = wv;
+    wcp[p] = comm_off ? wv : wv + comm_of(ob[v], bw, lat);
+  }
+}
+
+__device__ inline int64_t block_max_1024(int64_t x, int64_t *red) {
+  for (int off = 32; off > 0; off >>= 1) {
+    int64_t y = __shfl_xor(x, off);
+    x = y > x ? y : x;
+  }
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (lane == 0) red[wv] = x;
+  __syncthreads();
+  int64_t r = red[0];
+  for (int i = 1; i < (int)(blockDim.x >> 6); i++) r = red[i] > r ? red[i] : r;
+  __syncthreads();
+  return r;
+}
+
+// REVERSE = true:  val[p] = wp[p] for a sink, else wcp[p] + max val[successor]   (eq. 3)
+// REVERSE = false: val[p] = 0 for a source, else max (val[pred] + wcp[pred])       (eq. 2)
+template <bool REVERSE>
+__global__ void __launch_bounds__(kSweepB)
+    k_level_sweep(int32_t L, const int32_t *lp, const int32_t *rptr, const int32_t *ridx,
+                  const int64_t *wp, const int64_t *wcp, int64_t *val, const Status *st) {
+  __shared__ int32_t s_nheavy;
+  __shared__ int32_t s_heavy[kSweepB];
+  __shared__ int64_t s_red[kSweepB / 64];
+  if (failed(st)) return;
+  for (int32_t step = 0; step < L; step++) {
+    const int32_t l = REVERSE ? L - 1 - step : step;
+    const int32_t b = lp[l], e = lp[l + 1];
+    for (int32_t base = b; base < e; base += kSweepB) {
+      if (threadIdx.x == 0) s_nheavy = 0;
+      __syncthreads();  // also orders the previous level's writes before these reads
+      const int32_t p = base + threadIdx.x;
+      if (p < e) {
+        const int32_t k0 = rptr[p], k1 = rptr[p + 1];
+        if (k1 - k0 > kSweepHeavy) {
+          s_heavy[atomicAdd(&s_nheavy, 1)] = p;
+        } else if (REVERSE) {
+          if (k0 == k1) {
+            val[p] = wp[p];
+          } else {
+            int64_t mx = val[ridx[k0]];
+            for (int32_t k = k0 + 1; k < k1; k++) {
+              const int64_t x = val[ridx[k]];
+              mx = x > mx ? x : mx;
+            }
+            val[p] = wcp[p] + mx;
+          }
+        } else {
+          int64_t mx = 0;
+          for (int32_t k = k0; k < k1; k++) {
+            const int32_t q = ridx[k];
+            const int64_t x = val[q] + wcp[q];
+            mx = x > mx ? x : mx;
+          }
+          val[p] = mx;
+        }
+      }
+      __syncthreads();
+      const int32_t nh = s_nheavy;
+      for (int32_t h = 0; h < nh; h++) {
+        const int32_t q = s_heavy[h];
+        const int32_t k0 = rptr[q], k1 = rptr[q + 1];
+        int64_t mx = 0;  // all values are >= 0 and the node has > 64 neighbours
+        for (int32_t k = k0 + threadIdx.x; k < k1; k += kSweepB) {
+          const int32_t r = ridx[k];
+          const int64_t x = REVERSE ? val[r] : val[r] + wcp[r];
+          mx = x > mx ? x : mx;
+        }
+        mx = block_max_1024(mx, s_red);
+        if (threadIdx.x == 0) val[q] = REVERSE ? wcp[q] + mx : mx;
+      }
+    }
+  }
+}
+
+// out[order[p]] = val[p] (out may be NULL); *maxout = max val
+__global__ void k_scatter_max(int32_t n, const int32_t *order, const int64_t *val, int64_t *out,
+                              const Status *st, int64_t *maxout) {
+  __shared__ int64_t red[4];
+  if (failed(st)) return;
+  int64_t mx = 0;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t x = val[p];
+    if (out) out[order[p]] = x;
+    mx = x > mx ? x : mx;
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    int64_t y = __shfl_xor(mx, off);
+    mx = y > mx ? y : mx;
+  }
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t r = red[0];
+    for (int i = 1; i < (int)(blockDim.x >> 6); i++) r = red[i] > r ? red[i] : r;
+    atomicMax((unsigned long long *)maxout, (unsigned long long)r);
+  }
+}
+
+// priority keys: larger b-level first, then id
+__global__ void k_prio_keys(int32_t n, const int32_t *order, const int64_t *blp, uint64_t *keys,
+                            uint32_t *ids, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    keys[p] = (uint64_t)(INT64_MAX - blp[p]);
+    ids[p] = (uint32_t)order[p];
+  }
+}
+
+}  // namespace cel
+
+using namespace cel;
+
+extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_t *level,
+                          const int32_t *level_ptr, const int32_t *order_id, int32_t L,
+                          int32_t flags, int64_t *blevel, int64_t *tlevel, int32_t *prio_order,
+                          int64_t *cp, hipStream_t s) {
+  const char *fn = "cel_blevel";
+  CEL_TRY(check_host_graph(g, fn));
+  CEL_TRY(check_host_devices(d, fn));
+  const int32_t n = g->n;
+  if (!cp || !level_ptr || (n > 0 && (!level || !order_id || !blevel)))
+    return set_error(CEL_E_ARG, "%s: NULL argument", fn);
+  if (L < 0 || L > n || (n > 0 && L == 0)) return set_error(CEL_E_ARG, "%s: n_levels out of range", fn);
+  if (flags & ~CEL_COMM_OFF) return set_error(CEL_E_ARG, "%s: unknown flags", fn);
+  Scratch sc(s);
+  Status *st;
+  int32_t *tmp, *pos, *sptr, *sidx;
+  int64_t *wp, *wcp, *blp;
+  CEL_TRY(sc.get(&st, 1));
+  CEL_TRY(sc.get(&tmp, n));
+  CEL_TRY(sc.get(&pos, n));
+  CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
+  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, s));
+  CEL_TRY(check_level_order(g, order_id, level, level_ptr, L, pos, st, s));
+  CEL_TRY(sc.get(&sptr, (int64_t)n + 1));
+  CEL_TRY(sc.get(&sidx, g->m));
+  CEL_TRY(sc.get(&wp, n));
+  CEL_TRY(sc.get(&wcp, n));
+  CEL_TRY(sc.get(&blp, n));
+  CEL_TRY(relabel_csr(n, order_id, pos, g->out_ptr, g->out_idx, sptr, sidx, sc, s, st));
+  k_node_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order_id, g->w, g->ob, d->bw, d->lat,
+                                                     (flags & CEL_COMM_OFF) ? 1 : 0, wp, wcp, st);
+  k_level_sweep<true><<<1, kSweepB, 0, s>>>(L, level_ptr, sptr, sidx, wp, wcp, blp, st);
+  k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, blp, blevel, st, &st->s0);
+  if (tlevel && n > 0) {
+    int32_t *pptr, *pidx;
+    int64_t *tlp;
+    CEL_TRY(sc.get(&pptr, (int64_t)n + 1));
+    CEL_TRY(sc.get(&pidx, g->m));
+    CEL_TRY(sc.get(&tlp, n));
+    CEL_TRY(relabel_csr(n, order_id, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
+    k_level_sweep<false><<<1, kSweepB, 0, s>>>(L, level_ptr, pptr, pidx, wp, wcp, tlp, st);
+    k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, tlp, tlevel, st, &st->s1);
+  }
+  CEL_HIP(hipGetLastError());
+  Status h;
+  CEL_TRY(read_status(st, &h, s));
+  if (h.err) return status_error(h, fn);
+  *cp = h.s0;
+  if (prio_order && n > 0) {
+    std::vector<int32_t> lp(L + 1);
+    CEL_HIP(hipMemcpyAsync(lp.data(), level_ptr, sizeof(int32_t) * (L + 1), hipMemcpyDeviceToHost, s));
+    CEL_HIP(hipStreamSynchronize(s));
+    std::vector<int64_t> seg(lp.begin(), lp.end());
+    uint64_t *keys;
+    CEL_TRY(sc.get(&keys, n));
+    uint32_t *ids = reinterpret_cast<uint32_t *>(prio_order);
+    k_prio_keys<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order_id, blp, keys, ids, st);
+    CEL_TRY(segmented_sort(keys, ids, seg, sc, s));
+  }
+  CEL_HIP(hipStreamSynchronize(s));
+  return CEL_OK;
+}

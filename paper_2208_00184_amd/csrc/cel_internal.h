@@ -1,0 +1,130 @@
+// Internal declarations shared by the libcel translation units.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <vector>
+
+#include "cel.h"
+
+namespace cel {
+
+constexpr int64_t kLim = int64_t(1) << 62;  // every sum the path forms stays below this
+constexpr int64_t kInf = INT64_MAX;         // comparison sentinel only
+constexpr int kMaxD = 255;
+
+// error bits raised by device-side checks (Status::err)
+enum : uint32_t { EB_ARG = 1u, EB_CYCLE = 2u, EB_OVERFLOW = 4u, EB_ORDER = 8u };
+
+// Per-call device status block.  Kernels after a failed check read `err` and
+// return without touching data addressed by unchecked indices.
+struct Status {
+  uint32_t err;
+  uint32_t pad;
+  uint64_t total;      // saturating sum(w) + sum over edges c[src]
+  int64_t s0, s1, s2;  // call-specific scalar results
+  int32_t i0, i1, i2, i3;
+};
+
+__host__ __device__ inline int64_t comm_of(int64_t ob, int64_t bw, int64_t lat) {
+  return ob / bw + (ob % bw != 0 ? 1 : 0) + lat;
+}
+
+__device__ inline void raise_err(Status *st, uint32_t bits) { atomicOr(&st->err, bits); }
+
+__device__ inline bool failed(const Status *st) {
+  return __atomic_load_n(&st->err, __ATOMIC_RELAXED) != 0u;
+}
+
+// ---------------------------------------------------------------- host side
+
+int set_error(int code, const char *fmt, ...);
+
+#define CEL_HIP(call)                                                              \
+  do {                                                                             \
+    hipError_t e_ = (call);                                                        \
+    if (e_ != hipSuccess)                                                          \
+      return ::cel::set_error(CEL_E_HIP, "%s failed: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+#define CEL_TRY(expr)          \
+  do {                         \
+    int rc_ = (expr);          \
+    if (rc_ != CEL_OK) return rc_; \
+  } while (0)
+
+// Stream-ordered scratch allocations, all returned when the object dies.
+class Scratch {
+ public:
+  explicit Scratch(hipStream_t s) : s_(s) {}
+  ~Scratch();
+  Scratch(const Scratch &) = delete;
+  Scratch &operator=(const Scratch &) = delete;
+  // allocate `count` elements of T (count may be 0: a 1-element block is taken)
+  template <class T>
+  int get(T **out, int64_t count) {
+    return raw(reinterpret_cast<void **>(out), sizeof(T) * (size_t)(count > 0 ? count : 1));
+  }
+  int raw(void **out, size_t bytes);
+
+ private:
+  hipStream_t s_;
+  std::vector<void *> ptrs_;
+};
+
+// Launch-configuration helpers
+inline int grid_for(int64_t work, int block, int cap = 65535 * 4) {
+  int64_t g = (work + block - 1) / block;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return (int)g;
+}
+
+// Host-side argument checks (NULLs, sizes, device parameters).
+int check_host_graph(const cel_graph *g, const char *fn);
+int check_host_devices(const cel_devices *d, const char *fn);
+
+// ----------------------------------------------------------- common kernels
+// (launchers; defined in common.hip)
+
+// Validates the graph arrays and, when `bound` is set, the overflow bound
+// sum(w) + sum over edges of c[src] < 2^62.  Fills indeg_scratch (n ints)
+// with in-degrees counted from the CSR.  Raises EB_ARG / EB_OVERFLOW in st.
+int check_graph(const cel_graph *g, int64_t bw, int64_t lat, bool bound, Status *st,
+                int32_t *indeg_scratch, hipStream_t s);
+
+// Checks that `order` is a permutation of 0..n-1 consistent with level /
+// level_ptr (level-monotone) and that level[u] < level[v] on every edge.
+// Fills pos (inverse permutation).  Raises EB_ORDER.
+int check_level_order(const cel_graph *g, const int32_t *order, const int32_t *level,
+                      const int32_t *level_ptr, int32_t L, int32_t *pos, Status *st,
+                      hipStream_t s);
+
+// Checks that `order` is a permutation with pos[u] < pos[v] on every edge.
+int check_topo_order(const cel_graph *g, const int32_t *order, int32_t *pos, Status *st,
+                     hipStream_t s);
+
+// out[0] = 0, out[i+1] = out[i] + in[i] for i < n (n+1 outputs).
+int exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, Scratch &sc, hipStream_t s);
+int exclusive_scan_i64(const int64_t *in, int64_t *out, int64_t n, Scratch &sc, hipStream_t s);
+
+// Relabels a CSR (ptr/idx over node ids) into position space of `order`:
+// row p lists pos[idx[k]] for the edges of node order[p].
+int relabel_csr(int32_t n, const int32_t *order, const int32_t *pos, const int32_t *ptr,
+                const int32_t *idx, int32_t *pptr, int32_t *pidx, Scratch &sc, hipStream_t s,
+                const Status *st);
+
+// Sorts each segment [seg[i], seg[i+1]) of (key, id) pairs by (key, id), both
+// ascending; (key, id) pairs must be distinct.  seg_host is a host copy of the
+// nseg+1 offsets.  Results land in keys/ids (in place).
+int segmented_sort(uint64_t *keys, uint32_t *ids, const std::vector<int64_t> &seg_host,
+                   Scratch &sc, hipStream_t s);
+
+// Copies the status block to the host (synchronising the stream).
+int read_status(const Status *dst, Status *host, hipStream_t s);
+
+// Translates device error bits into an API error code with a message.
+int status_error(const Status &h, const char *fn);
+
+}  // namespace cel

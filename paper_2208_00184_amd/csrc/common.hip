@@ -1,0 +1,665 @@
+// Shared pieces of libcel: error state, scratch memory, input validation,
+// prefix scans, CSR relabelling into position space and a segmented sort.
+#include <cstdarg>
+#include <cstring>
+#include <mutex>
+
+#include "cel_internal.h"
+
+namespace cel {
+
+// ------------------------------------------------------------------ errors
+
+static thread_local char g_msg[512] = "";
+
+int set_error(int code, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_msg, sizeof g_msg, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+const char *last_error_text() { return g_msg; }
+
+int status_error(const Status &h, const char *fn) {
+  if (h.err & EB_ARG) return set_error(CEL_E_ARG, "%s: malformed graph or argument arrays", fn);
+  if (h.err & EB_CYCLE) return set_error(CEL_E_CYCLE, "%s: the graph has a cycle", fn);
+  if (h.err & EB_OVERFLOW)
+    return set_error(CEL_E_OVERFLOW, "%s: sum(w) + sum over edges of c[src] reaches 2^62", fn);
+  if (h.err & EB_ORDER)
+    return set_error(CEL_E_ORDER, "%s: order/level/cluster arrays inconsistent with the graph", fn);
+  return CEL_OK;
+}
+
+int check_host_graph(const cel_graph *g, const char *fn) {
+  if (!g) return set_error(CEL_E_ARG, "%s: graph is NULL", fn);
+  if (g->n < 0 || g->m < 0) return set_error(CEL_E_ARG, "%s: negative n or m", fn);
+  if (!g->out_ptr || !g->in_ptr || (g->m > 0 && (!g->out_idx || !g->in_idx)) ||
+      (g->n > 0 && (!g->w || !g->mem || !g->ob)))
+    return set_error(CEL_E_ARG, "%s: NULL graph array", fn);
+  return CEL_OK;
+}
+
+int check_host_devices(const cel_devices *d, const char *fn) {
+  if (!d || !d->cap) return set_error(CEL_E_ARG, "%s: devices or caps NULL", fn);
+  if (d->D < 1 || d->D > kMaxD) return set_error(CEL_E_ARG, "%s: D = %d not in [1, 255]", fn, d->D);
+  if (d->bw <= 0 || d->lat < 0 || d->lat >= kLim)
+    return set_error(CEL_E_ARG, "%s: need bw > 0 and 0 <= lat < 2^62", fn);
+  for (int i = 0; i < d->D; i++)
+    if (d->cap[i] < 0) return set_error(CEL_E_ARG, "%s: negative memory cap", fn);
+  return CEL_OK;
+}
+
+// ----------------------------------------------------------------- scratch
+
+static void keep_pool_warm(int dev) {
+  static std::mutex mu;
+  static bool done[64] = {};
+  std::lock_guard<std::mutex> lk(mu);
+  if (dev < 0 || dev >= 64 || done[dev]) return;
+  hipMemPool_t pool;
+  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+    uint64_t thr = UINT64_MAX;  // keep freed blocks in the pool between calls
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+  }
+  done[dev] = true;
+}
+
+int Scratch::raw(void **out, size_t bytes) {
+  int dev = 0;
+  CEL_HIP(hipGetDevice(&dev));
+  keep_pool_warm(dev);
+  void *p = nullptr;
+  hipError_t e = hipMallocAsync(&p, bytes, s_);
+  if (e != hipSuccess || !p)
+    return set_error(CEL_E_NOMEM, "scratch allocation of %zu bytes failed: %s", bytes,
+                     hipGetErrorString(e));
+  ptrs_.push_back(p);
+  *out = p;
+  return CEL_OK;
+}
+
+Scratch::~Scratch() {
+  for (void *p : ptrs_) (void)hipFreeAsync(p, s_);
+}
+
+int read_status(const Status *dst, Status *host, hipStream_t s) {
+  CEL_HIP(hipMemcpyAsync(host, dst, sizeof(Status), hipMemcpyDeviceToHost, s));
+  CEL_HIP(hipStreamSynchronize(s));
+  return CEL_OK;
+}
+
+// ------------------------------------------------------------- validation
+
+// saturating add for the overflow bound
+__device__ inline uint64_t sat_add(uint64_t a, uint64_t b) {
+  uint64_t r = a + b;
+  return (r < a || r > (uint64_t)kLim) ? (uint64_t)kLim : r;
+}
+
+__device__ inline void atomic_sat_add(uint64_t *p, uint64_t v) {
+  uint64_t old = __atomic_load_n(p, __ATOMIC_RELAXED);
+  while (old < (uint64_t)kLim) {
+    uint64_t nv = sat_add(old, v);
+    if (atomicCAS((unsigned long long *)p, (unsigned long long)old, (unsigned long long)nv) == old)
+      break;
+    old = __atomic_load_n(p, __ATOMIC_RELAXED);
+  }
+}
+
+__global__ void k_check_nodes(cel_graph g, int64_t bw, int64_t lat, Status *st) {
+  __shared__ uint64_t part[4];
+  const int32_t n = g.n, m = g.m;
+  uint64_t acc = 0;
+  uint32_t bad = 0;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v <= n;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    if (v == 0 && (g.out_ptr[0] != 0 || g.in_ptr[0] != 0)) bad |= EB_ARG;
+    if (v == n) {
+      if (g.out_ptr[n] != m || g.in_ptr[n] != m) bad |= EB_ARG;
+      continue;
+    }
+    int32_t o0 = g.out_ptr[v], o1 = g.out_ptr[v + 1], i0 = g.in_ptr[v], i1 = g.in_ptr[v + 1];
+    if (o1 < o0 || i1 < i0) bad |= EB_ARG;
+    int64_t w = g.w[v], mem = g.mem[v], ob = g.ob[v];
+    if (w < 0 || mem < 0 || ob < 0) {
+      bad |= EB_ARG;
+      continue;
+    }
+    int64_t deg = o1 > o0 ? (int64_t)o1 - o0 : 0;
+    int64_t c = comm_of(ob, bw, lat);  // ob >= 0, bw >= 1, lat < 2^62: no overflow
+    uint64_t t = (uint64_t)w;
+    if (deg > 0) t = (c >= kLim / deg) ? (uint64_t)kLim : sat_add(t, (uint64_t)(c * deg));
+    acc = sat_add(acc, t);
+  }
+  // wave reduce (saturating) then block
+  for (int off = 32; off > 0; off >>= 1) {
+    uint64_t o = __shfl_down(acc, off);
+    acc = sat_add(acc, o);
+  }
+  int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (lane == 0) part[wv] = acc;
+  if (bad) raise_err(st, bad);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t tot = 0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); i++) tot = sat_add(tot, part[i]);
+    atomic_sat_add(&st->total, tot);
+  }
+}
+
+__device__ inline uint64_t mix64(uint64_t x) {  // SplitMix64 finaliser
+  x += 0x9E3779B97F4A7C15ull;
+  x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+  x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+  return x ^ (x >> 31);
+}
+
+// CSR pass: one block per 256 consecutive sources; the block's edges form one
+// contiguous range and are spread over all threads (owner by binary search).
+// Counts in-degrees and a per-target sum of hashed source ids.
+__global__ void k_check_csr(cel_graph g, Status *st, int32_t *indeg, uint64_t *hsum) {
+  __shared__ int32_t ptr[257];
+  if (failed(st)) return;  // row pointers not validated
+  const int32_t n = g.n;
+  const int64_t u0 = (int64_t)blockIdx.x * 256;
+  for (int i = threadIdx.x; i <= 256; i += blockDim.x) {
+    const int64_t u = u0 + i < n ? u0 + i : n;
+    ptr[i] = g.out_ptr[u];
+  }
+  __syncthreads();
+  uint32_t bad = 0;
+  const int32_t e0 = ptr[0], e1 = ptr[256];
+  for (int32_t e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
+    int lo = 0, hi = 255;  // source row: last i with ptr[i] <= e
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (ptr[mid] <= e) lo = mid;
+      else hi = mid - 1;
+    }
+    const int32_t t = g.out_idx[e];
+    if (t < 0 || t >= n) {
+      bad |= EB_ARG;
+      continue;
+    }
+    atomicAdd(&indeg[t], 1);
+    atomicAdd((unsigned long long *)&hsum[t], (unsigned long long)mix64((uint64_t)(u0 + lo)));
+  }
+  if (bad) raise_err(st, bad);
+}
+
+// CSC pass: in-degree and hashed-source sum of every node must match the CSR's
+// (equal edge multisets give equal sums; a mismatch is caught with
+// overwhelming probability).
+__global__ void k_check_csc(cel_graph g, Status *st, const int32_t *indeg, const uint64_t *hsum) {
+  if (failed(st)) return;
+  uint32_t bad = 0;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < g.n;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t k0 = g.in_ptr[v], k1 = g.in_ptr[v + 1];
+    if (indeg[v] != k1 - k0) {
+      bad |= EB_ARG;
+      continue;
+    }
+    uint64_t h = 0;
+    for (int32_t k = k0; k < k1; k++) {
+      const int32_t s = g.in_idx[k];
+      if (s < 0 || s >= g.n) {
+        bad |= EB_ARG;
+        break;
+      }
+      h += mix64((uint64_t)s);
+    }
+    if (h != hsum[v]) bad |= EB_ARG;
+  }
+  if (bad) raise_err(st, bad);
+}
+
+__global__ void k_finish_overflow(Status *st) {
+  if (threadIdx.x == 0 && st->total >= (uint64_t)kLim) raise_err(st, EB_OVERFLOW);
+}
+
+int check_graph(const cel_graph *g, int64_t bw, int64_t lat, bool bound, Status *st,
+                int32_t *indeg, hipStream_t s) {
+  const int B = 256;
+  k_check_nodes<<<grid_for(g->n + 1, B, 2048), B, 0, s>>>(*g, bw, lat, st);
+  if (g->n > 0) {
+    uint64_t *hsum;
+    CEL_HIP(hipMallocAsync((void **)&hsum, sizeof(uint64_t) * (size_t)g->n, s));
+    CEL_HIP(hipMemsetAsync(indeg, 0, sizeof(int32_t) * (size_t)g->n, s));
+    CEL_HIP(hipMemsetAsync(hsum, 0, sizeof(uint64_t) * (size_t)g->n, s));
+    k_check_csr<<<(unsigned)((g->n + 255) / 256), B, 0, s>>>(*g, st, indeg, hsum);
+    k_check_csc<<<grid_for(g->n, B, 4096), B, 0, s>>>(*g, st, indeg, hsum);
+    CEL_HIP(hipFreeAsync(hsum, s));
+  }
+  if (bound) k_finish_overflow<<<1, 64, 0, s>>>(st);
+  CEL_HIP(hipGetLastError());
+  return CEL_OK;
+}
+
+__global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+// pos[order[p]] = p, duplicates and out-of-range ids raise EB_ORDER
+__global__ void k_inverse_perm(int32_t n, const int32_t *order, int32_t *pos, Status *st) {
+  uint32_t bad = 0;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    int32_t v = order[p];
+    if (v < 0 || v >= n) {
+      bad |= EB_ORDER;
+      continue;
+    }
+    if (atomicCAS(&pos[v], -1, (int32_t)p) != -1) bad |= EB_ORDER;
+  }
+  if (bad) raise_err(st, bad);
+}
+
+__global__ void k_check_levels_nodes(int32_t n, const int32_t *order, const int32_t *level,
+                                     const int32_t *lp, int32_t L, Status *st) {
+  uint32_t bad = 0;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p <= n;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    if (p <= L) {  // level_ptr: 0 at the front, n at the back, non-decreasing
+      int32_t a = lp[p];
+      if (p == 0 && a != 0) bad |= EB_ORDER;
+      if (p == L && a != n) bad |= EB_ORDER;
+      if (p < L && lp[p + 1] < a) bad |= EB_ORDER;
+    }
+    if (p == n) continue;
+    int32_t v = order[p];
+    if (v < 0 || v >= n) {
+      bad |= EB_ORDER;
+      continue;
+    }
+    int32_t l = level[v];
+    if (l < 0 || l >= L) {
+      bad |= EB_ORDER;
+      continue;
+    }
+    if (p < lp[l] || p >= lp[l + 1]) bad |= EB_ORDER;
+  }
+  if (bad) raise_err(st, bad);
+}
+
+// level[u] < level[v] on every edge (needs level values in range: checked above)
+__global__ void k_check_levels_edges(cel_graph g, const int32_t *level, int32_t L, Status *st) {
+  if (failed(st)) return;  // edge indices or level values not validated
+  uint32_t bad = 0;
+  for (int64_t u = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; u < g.n;
+       u += (int64_t)gridDim.x * blockDim.x) {
+    int32_t lu = level[u];
+    for (int32_t e = g.out_ptr[u]; e < g.out_ptr[u + 1]; e++) {
+      int32_t v = g.out_idx[e];
+      if (level[v] <= lu) bad |= EB_ORDER;
+    }
+  }
+  if (bad) raise_err(st, bad);
+}
+
+// pos[u] < pos[v] on every edge (pos must be a complete permutation: checked)
+__global__ void k_check_topo_edges(cel_graph g, const int32_t *pos, Status *st) {
+  if (failed(st)) return;
+  uint32_t bad = 0;
+  for (int64_t u = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; u < g.n;
+       u += (int64_t)gridDim.x * blockDim.x) {
+    int32_t pu = pos[u];
+    for (int32_t e = g.out_ptr[u]; e < g.out_ptr[u + 1]; e++)
+      if (pos[g.out_idx[e]] <= pu) bad |= EB_ORDER;
+  }
+  if (bad) raise_err(st, bad);
+}
+
+int check_level_order(const cel_graph *g, const int32_t *order, const int32_t *level,
+                      const int32_t *level_ptr, int32_t L, int32_t *pos, Status *st,
+                      hipStream_t s) {
+  const int B = 256;
+  const int32_t n = g->n;
+  if (n > 0) {
+    k_fill_i32<<<grid_for(n, B, 4096), B, 0, s>>>(pos, n, -1);
+    k_inverse_perm<<<grid_for(n, B, 4096), B, 0, s>>>(n, order, pos, st);
+  }
+  k_check_levels_nodes<<<grid_for((int64_t)n + 1, B, 4096), B, 0, s>>>(n, order, level, level_ptr,
+                                                                       L, st);
+  if (n > 0) k_check_levels_edges<<<grid_for(n, B, 4096), B, 0, s>>>(*g, level, L, st);
+  CEL_HIP(hipGetLastError());
+  return CEL_OK;
+}
+
+int check_topo_order(const cel_graph *g, const int32_t *order, int32_t *pos, Status *st,
+                     hipStream_t s) {
+  const int B = 256;
+  const int32_t n = g->n;
+  if (n > 0) {
+    k_fill_i32<<<grid_for(n, B, 4096), B, 0, s>>>(pos, n, -1);
+    k_inverse_perm<<<grid_for(n, B, 4096), B, 0, s>>>(n, order, pos, st);
+    k_check_topo_edges<<<grid_for(n, B, 4096), B, 0, s>>>(*g, pos, st);
+  }
+  CEL_HIP(hipGetLastError());
+  return CEL_OK;
+}
+
+// ------------------------------------------------------------------- scans
+
+constexpr int kScanB = 256, kScanItems = 16, kScanTile = kScanB * kScanItems;
+
+template <class T>
+__device__ T block_exclusive_scan(T x, T *wsum, T *total) {
+  // 256 threads = 4 waves of 64
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  T inc = x;
+  for (int off = 1; off < 64; off <<= 1) {
+    T y = __shfl_up(inc, off);
+    if (lane >= off) inc += y;
+  }
+  if (lane == 63) wsum[wv] = inc;
+  __syncthreads();
+  T base = 0, tot = 0;
+  for (int i = 0; i < kScanB / 64; i++) {
+    if (i < wv) base += wsum[i];
+    tot += wsum[i];
+  }
+  __syncthreads();
+  *total = tot;
+  return base + inc - x;
+}
+
+template <class T>
+__global__ void k_scan_reduce(const T *in, int64_t n, T *bsum) {
+  __shared__ T wsum[kScanB / 64];
+  int64_t base = (int64_t)blockIdx.x * kScanTile;
+  T acc = 0;
+  for (int i = threadIdx.x; i < kScanTile; i += kScanB) {
+    int64_t k = base + i;
+    if (k < n) acc += in[k];
+  }
+  T tot;
+  (void)block_exclusive_scan<T>(acc, wsum, &tot);
+  if (threadIdx.x == 0) bsum[blockIdx.x] = tot;
+}
+
+template <class T>
+__global__ void k_scan_apply(const T *in, T *out, int64_t n, const T *boff) {
+  __shared__ T buf[kScanTile];
+  __shared__ T wsum[kScanB / 64];
+  int64_t base = (int64_t)blockIdx.x * kScanTile;
+  for (int i = threadIdx.x; i < kScanTile; i += kScanB) {
+    int64_t k = base + i;
+    buf[i] = k < n ? in[k] : (T)0;
+  }
+  __syncthreads();
+  T loc = 0;
+  for (int k = 0; k < kScanItems; k++) loc += buf[threadIdx.x * kScanItems + k];
+  T tot;
+  T run = block_exclusive_scan<T>(loc, wsum, &tot) + (boff ? boff[blockIdx.x] : (T)0);
+  for (int k = 0; k < kScanItems; k++) {
+    run += buf[threadIdx.x * kScanItems + k];
+    buf[threadIdx.x * kScanItems + k] = run;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < kScanTile; i += kScanB) {
+    int64_t k = base + i;
+    if (k < n) out[k + 1] = buf[i];
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) out[0] = 0;
+}
+
+template <class T>
+static int exclusive_scan(const T *in, T *out, int64_t n, Scratch &sc, hipStream_t s) {
+  if (n <= 0) {
+    CEL_HIP(hipMemsetAsync(out, 0, sizeof(T), s));
+    return CEL_OK;
+  }
+  int64_t nb = (n + kScanTile - 1) / kScanTile;
+  if (nb == 1) {
+    k_scan_apply<T><<<1, kScanB, 0, s>>>(in, out, n, nullptr);
+    CEL_HIP(hipGetLastError());
+    return CEL_OK;
+  }
+  T *bsum, *boff;
+  CEL_TRY(sc.get(&bsum, nb));
+  CEL_TRY(sc.get(&boff, nb + 1));
+  k_scan_reduce<T><<<(unsigned)nb, kScanB, 0, s>>>(in, n, bsum);
+  CEL_TRY(exclusive_scan<T>(bsum, boff, nb, sc, s));
+  k_scan_apply<T><<<(unsigned)nb, kScanB, 0, s>>>(in, out, n, boff);
+  CEL_HIP(hipGetLastError());
+  return CEL_OK;
+}
+
+int exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, Scratch &sc, hipStream_t s) {
+  return exclusive_scan<int32_t>(in, out, n, sc, s);
+}
+int exclusive_scan_i64(const int64_t *in, int64_t *out, int64_t n, Scratch &sc, hipStream_t s) {
+  return exclusive_scan<int64_t>(in, out, n, sc, s);
+}
+
+// ---------------------------------------------------------------- relabel
+
+__global__ void k_row_deg(int32_t n, const int32_t *order, const int32_t *ptr, int32_t *deg,
+                          const Status *st) {
+  if (failed(st)) return;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    int32_t v = order[p];
+    deg[p] = ptr[v + 1] - ptr[v];
+  }
+}
+
+// One block per 256 consecutive positions: the block's edges are spread over
+// all threads (owner found by binary search), so a node of huge degree does
+// not serialise on one thread.
+__global__ void k_relabel_rows(int32_t n, const int32_t *order, const int32_t *pos,
+                               const int32_t *ptr, const int32_t *idx, const int32_t *pptr,
+                               int32_t *pidx, const Status *st) {
+  __shared__ int32_t off[257];
+  __shared__ int32_t beg[256];
+  __shared__ int32_t wsum[4];
+  if (failed(st)) return;
+  const int64_t p0 = (int64_t)blockIdx.x * 256;
+  const int64_t p = p0 + threadIdx.x;
+  int32_t d = 0, b = 0;
+  if (p < n) {
+    int32_t v = order[p];
+    b = ptr[v];
+    d = ptr[v + 1] - b;
+  }
+  int32_t tot;
+  int32_t ex = block_exclusive_scan<int32_t>(d, wsum, &tot);
+  off[threadIdx.x] = ex;
+  beg[threadIdx.x] = b;
+  if (threadIdx.x == 0) off[256] = tot;
+  __syncthreads();
+  const int32_t outbase = pptr[p0];
+  for (int32_t j = threadIdx.x; j < tot; j += 256) {
+    int lo = 0, hi = 255;  // owner: last row with off[row] <= j
+    while (lo < hi) {
+      int mid = (lo + hi + 1) >> 1;
+      if (off[mid] <= j) lo = mid;
+      else hi = mid - 1;
+    }
+    int32_t k = j - off[lo];
+    pidx[outbase + j] = pos[idx[beg[lo] + k]];
+  }
+}
+
+int relabel_csr(int32_t n, const int32_t *order, const int32_t *pos, const int32_t *ptr,
+                const int32_t *idx, int32_t *pptr, int32_t *pidx, Scratch &sc, hipStream_t s,
+                const Status *st) {
+  if (n <= 0) {
+    CEL_HIP(hipMemsetAsync(pptr, 0, sizeof(int32_t), s));
+    return CEL_OK;
+  }
+  int32_t *deg;
+  CEL_TRY(sc.get(&deg, n));
+  k_row_deg<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, ptr, deg, st);
+  CEL_TRY(exclusive_scan_i32(deg, pptr, n, sc, s));
+  k_relabel_rows<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(n, order, pos, ptr, idx, pptr, pidx,
+                                                              st);
+  CEL_HIP(hipGetLastError());
+  return CEL_OK;
+}
+
+// ------------------------------------------------------- segmented sort
+
+constexpr int kSortTile = 2048;
+
+struct Tile {
+  int32_t start, len;
+};
+
+__device__ inline bool kless(uint64_t ka, uint32_t ia, uint64_t kb, uint32_t ib) {
+  return ka < kb || (ka == kb && ia < ib);
+}
+
+// Bitonic sort of one tile (<= kSortTile elements) in LDS.
+__global__ void __launch_bounds__(256) k_sort_tiles(uint64_t *keys, uint32_t *ids,
+                                                    const Tile *tiles) {
+  __shared__ uint64_t sk[kSortTile];
+  __shared__ uint32_t si[kSortTile];
+  const Tile t = tiles[blockIdx.x];
+  int P = 2;
+  while (P < t.len) P <<= 1;
+  for (int i = threadIdx.x; i < P; i += blockDim.x) {
+    if (i < t.len) {
+      sk[i] = keys[t.start + i];
+      si[i] = ids[t.start + i];
+    } else {
+      sk[i] = ~0ull;
+      si[i] = ~0u;
+    }
+  }
+  __syncthreads();
+  for (int size = 2; size <= P; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = threadIdx.x; i < (P >> 1); i += blockDim.x) {
+        int lo = 2 * stride * (i / stride) + (i % stride), hi = lo + stride;
+        bool up = (lo & size) == 0;
+        uint64_t ka = sk[lo], kb = sk[hi];
+        uint32_t ia = si[lo], ib = si[hi];
+        if (kless(kb, ib, ka, ia) == up) {
+          sk[lo] = kb; sk[hi] = ka;
+          si[lo] = ib; si[hi] = ia;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int i = threadIdx.x; i < t.len; i += blockDim.x) {
+    keys[t.start + i] = sk[i];
+    ids[t.start + i] = si[i];
+  }
+}
+
+// One merge round over every large segment: runs of `width` are merged in
+// pairs; each element finds its output slot by counting the smaller elements
+// of the partner run (binary search).  (key, id) pairs are distinct.
+__global__ void k_merge_pass(const uint64_t *kin, const uint32_t *iin, uint64_t *kout,
+                             uint32_t *iout, const int64_t *seg_start, const int64_t *seg_off,
+                             int nseg, int64_t width, int64_t total) {
+  for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g < total;
+       g += (int64_t)gridDim.x * blockDim.x) {
+    int lo = 0, hi = nseg - 1;  // segment: last s with seg_off[s] <= g
+    while (lo < hi) {
+      int mid = (lo + hi + 1) >> 1;
+      if (seg_off[mid] <= g) lo = mid;
+      else hi = mid - 1;
+    }
+    const int64_t base = seg_start[lo], len = seg_off[lo + 1] - seg_off[lo];
+    const int64_t off = g - seg_off[lo];
+    const int64_t a0 = (off / (2 * width)) * (2 * width);
+    const int64_t a1 = a0 + width < len ? a0 + width : len;
+    const int64_t b1 = a0 + 2 * width < len ? a0 + 2 * width : len;
+    const uint64_t k = kin[base + off];
+    const uint32_t id = iin[base + off];
+    int64_t r0, r1, own;
+    if (off < a1) {
+      r0 = a1; r1 = b1; own = off - a0;
+    } else {
+      r0 = a0; r1 = a1; own = off - a1;
+    }
+    int64_t l = r0, h = r1;  // count of partner elements smaller than (k, id)
+    while (l < h) {
+      int64_t mid = (l + h) >> 1;
+      if (kless(kin[base + mid], iin[base + mid], k, id)) l = mid + 1;
+      else h = mid;
+    }
+    const int64_t dst = a0 + own + (l - r0);
+    kout[base + dst] = k;
+    iout[base + dst] = id;
+  }
+}
+
+int segmented_sort(uint64_t *keys, uint32_t *ids, const std::vector<int64_t> &seg,
+                   Scratch &sc, hipStream_t s) {
+  const int64_t nseg = (int64_t)seg.size() - 1;
+  std::vector<Tile> tiles;
+  std::vector<int64_t> big_start, big_off{0};
+  int64_t maxlen = 0;
+  for (int64_t i = 0; i < nseg; i++) {
+    int64_t a = seg[i], len = seg[i + 1] - seg[i];
+    if (len <= 1) continue;
+    for (int64_t t = 0; t < len; t += kSortTile)
+      tiles.push_back(Tile{(int32_t)(a + t), (int32_t)(len - t < kSortTile ? len - t : kSortTile)});
+    if (len > kSortTile) {
+      big_start.push_back(a);
+      big_off.push_back(big_off.back() + len);
+      if (len > maxlen) maxlen = len;
+    }
+  }
+  if (tiles.empty()) return CEL_OK;
+  Tile *dtiles;
+  CEL_TRY(sc.get(&dtiles, (int64_t)tiles.size()));
+  CEL_HIP(hipMemcpyAsync(dtiles, tiles.data(), sizeof(Tile) * tiles.size(), hipMemcpyHostToDevice,
+                         s));
+  // one launch per 65535 tiles (grid x limit kept modest)
+  for (size_t t0 = 0; t0 < tiles.size(); t0 += 65535) {
+    size_t cnt = tiles.size() - t0 < 65535 ? tiles.size() - t0 : 65535;
+    k_sort_tiles<<<(unsigned)cnt, 256, 0, s>>>(keys, ids, dtiles + t0);
+  }
+  CEL_HIP(hipGetLastError());
+  if (big_start.empty()) {
+    // the host vectors must outlive the async copies: synchronise before return
+    CEL_HIP(hipStreamSynchronize(s));
+    return CEL_OK;
+  }
+  const int nb = (int)big_start.size();
+  const int64_t total = big_off.back();
+  int64_t *dstart, *doff;
+  CEL_TRY(sc.get(&dstart, nb));
+  CEL_TRY(sc.get(&doff, nb + 1));
+  CEL_HIP(hipMemcpyAsync(dstart, big_start.data(), sizeof(int64_t) * nb, hipMemcpyHostToDevice, s));
+  CEL_HIP(hipMemcpyAsync(doff, big_off.data(), sizeof(int64_t) * (nb + 1), hipMemcpyHostToDevice,
+                         s));
+  // ping-pong buffers addressed like the input (only large segments are used)
+  int64_t span = seg.back();
+  uint64_t *k2;
+  uint32_t *i2;
+  CEL_TRY(sc.get(&k2, span));
+  CEL_TRY(sc.get(&i2, span));
+  uint64_t *ka = keys, *kb = k2;
+  uint32_t *ia = ids, *ib = i2;
+  int passes = 0;
+  for (int64_t width = kSortTile; width < maxlen; width *= 2) {
+    k_merge_pass<<<grid_for(total, 256, 8192), 256, 0, s>>>(ka, ia, kb, ib, dstart, doff, nb,
+                                                            width, total);
+    std::swap(ka, kb);
+    std::swap(ia, ib);
+    passes++;
+  }
+  CEL_HIP(hipGetLastError());
+  if (passes & 1) {  // result sits in the scratch copy: bring large segments back
+    for (int i = 0; i < nb; i++) {
+      int64_t a = big_start[i], len = big_off[i + 1] - big_off[i];
+      CEL_HIP(hipMemcpyAsync(keys + a, k2 + a, sizeof(uint64_t) * len, hipMemcpyDeviceToDevice, s));
+      CEL_HIP(hipMemcpyAsync(ids + a, i2 + a, sizeof(uint32_t) * len, hipMemcpyDeviceToDevice, s));
+    }
+  }
+  CEL_HIP(hipStreamSynchronize(s));
+  return CEL_OK;
+}
+
+}  // namespace cel

@@ -1,0 +1,119 @@
+// cel_topo_levels: level-synchronous Kahn ordering (Section 4.2.2).
+//
+// One workgroup runs all levels: a level costs a few dependent L2 round trips
+// (frontier id -> adjacency -> in-degree atomic), so keeping the whole loop in
+// one workgroup with workgroup barriers is far cheaper than one launch or one
+// grid-wide barrier per level.  Frontiers are appended to the caller's
+// order_id buffer; each level's slice is then sorted by id.
+#include "cel_internal.h"
+
+namespace cel {
+
+constexpr int kKahnB = 1024;
+constexpr int kKahnHeavy = 64;  // out-degree above which the whole block shares a node
+
+__device__ inline void kahn_release(const cel_graph &g, int32_t *cnt, int32_t *F,
+                                    int32_t *s_tail, int32_t e) {
+  const int32_t v = g.out_idx[e];
+  if (atomicSub(&cnt[v], 1) == 1) {  // last in-edge removed: v joins the next frontier
+    const int32_t k = atomicAdd(s_tail, 1);
+    F[k] = v;
+  }
+}
+
+__global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, int32_t *F,
+                                                 int32_t *level, int32_t *lstart, Status *st) {
+  __shared__ int32_t s_tail, s_nheavy;
+  __shared__ int32_t s_heavy[kKahnB];
+  if (failed(st)) return;
+  const int tid = threadIdx.x;
+  const int32_t n = g.n;
+  if (tid == 0) s_tail = 0;
+  __syncthreads();
+  for (int32_t v = tid; v < n; v += kKahnB)
+    if (cnt[v] == 0) F[atomicAdd(&s_tail, 1)] = v;
+  __syncthreads();
+  int32_t fb = 0, fe = s_tail, lvl = 0;
+  while (fb < fe) {
+    if (tid == 0) lstart[lvl] = fb;
+    for (int32_t base = fb; base < fe; base += kKahnB) {
+      if (tid == 0) s_nheavy = 0;
+      __syncthreads();
+      const int32_t i = base + tid;
+      if (i < fe) {
+        const int32_t u = F[i];
+        level[u] = lvl;
+        const int32_t e0 = g.out_ptr[u], e1 = g.out_ptr[u + 1];
+        if (e1 - e0 > kKahnHeavy) {
+          s_heavy[atomicAdd(&s_nheavy, 1)] = u;
+        } else {
+          for (int32_t e = e0; e < e1; e++) kahn_release(g, cnt, F, &s_tail, e);
+        }
+      }
+      __syncthreads();
+      const int32_t nh = s_nheavy;
+      for (int32_t h = 0; h < nh; h++) {
+        const int32_t u = s_heavy[h];
+        for (int32_t e = g.out_ptr[u] + tid; e < g.out_ptr[u + 1]; e += kKahnB)
+          kahn_release(g, cnt, F, &s_tail, e);
+      }
+      __syncthreads();
+    }
+    fb = fe;
+    fe = s_tail;
+    lvl++;
+    __syncthreads();  // everyone has read s_tail before the next level appends
+  }
+  if (tid == 0) {
+    st->i0 = lvl;     // number of levels
+    st->i1 = s_tail;  // nodes taken; < n means a cycle
+    lstart[lvl] = s_tail;
+  }
+}
+
+__global__ void k_zero_u64(uint64_t *p, int64_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0;
+}
+
+}  // namespace cel
+
+using namespace cel;
+
+extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *order_id,
+                               int32_t *level_ptr, int32_t *n_levels, hipStream_t s) {
+  if (!g || !n_levels || !level_ptr) return set_error(CEL_E_ARG, "cel_topo_levels: NULL argument");
+  if (g->n < 0 || g->m < 0) return set_error(CEL_E_ARG, "cel_topo_levels: negative size");
+  if (!g->out_ptr || !g->in_ptr || (g->m > 0 && (!g->out_idx || !g->in_idx)) ||
+      (g->n > 0 && (!g->w || !g->mem || !g->ob || !level || !order_id)))
+    return set_error(CEL_E_ARG, "cel_topo_levels: NULL array");
+  const int32_t n = g->n;
+  Scratch sc(s);
+  Status *st;
+  int32_t *cnt;
+  CEL_TRY(sc.get(&st, 1));
+  CEL_TRY(sc.get(&cnt, n));
+  CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
+  CEL_TRY(check_graph(g, 1, 0, /*bound=*/false, st, cnt, s));
+  k_kahn<<<1, kKahnB, 0, s>>>(*g, cnt, order_id, level, level_ptr, st);
+  CEL_HIP(hipGetLastError());
+  Status h;
+  CEL_TRY(read_status(st, &h, s));
+  if (h.err) return status_error(h, "cel_topo_levels");
+  if (h.i1 != n) return set_error(CEL_E_CYCLE, "cel_topo_levels: the graph has a cycle (%d of %d nodes ordered)", h.i1, n);
+  const int32_t L = h.i0;
+  *n_levels = L;
+  if (n == 0) return CEL_OK;
+  // sort each level's frontier slice by id
+  std::vector<int32_t> lp(L + 1);
+  CEL_HIP(hipMemcpyAsync(lp.data(), level_ptr, sizeof(int32_t) * (L + 1), hipMemcpyDeviceToHost, s));
+  CEL_HIP(hipStreamSynchronize(s));
+  std::vector<int64_t> seg(lp.begin(), lp.end());
+  uint64_t *keys;
+  CEL_TRY(sc.get(&keys, n));
+  k_zero_u64<<<grid_for(n, 256, 4096), 256, 0, s>>>(keys, n);
+  CEL_TRY(segmented_sort(keys, reinterpret_cast<uint32_t *>(order_id), seg, sc, s));
+  CEL_HIP(hipStreamSynchronize(s));
+  return CEL_OK;
+}
