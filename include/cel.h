@@ -147,6 +147,16 @@ int cel_makespan(const cel_graph *g, const cel_devices *d, const int32_t *order,
                  int32_t K, const uint8_t *node_dev, int64_t *start, int64_t *finish,
                  int64_t *makespan, hipStream_t stream);
 
+/* Diagnostics: per-kernel device time.  After cel_timing(1), every call
+ * records a pair of HIP events on its stream around each of its main kernel
+ * launches; the elapsed times are added to process-wide totals when the call
+ * completes.  cel_kernel_stats writes one line per kernel, "name launches
+ * total_ms\n", into buf (NUL-terminated, truncated to buflen), returns the
+ * number of kernels listed, and clears the totals when reset != 0.
+ * cel_timing returns the previous setting. */
+int cel_timing(int enable);
+int cel_kernel_stats(char *buf, int buflen, int reset);
+
 /* Message describing the calling thread's last error ("" if none). */
 const char *cel_last_error(void);
 

@@ -21,7 +21,7 @@ COMM_OFF = 1
 CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
 EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cluster", "cel_place", "cel_makespan",
-           "cel_last_error", "cel_version")
+           "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
 class CelError(RuntimeError):
@@ -65,12 +65,32 @@ def lib() -> C.CDLL:
             getattr(L, f).restype = C.c_int
         L.cel_last_error.argtypes = []
         L.cel_last_error.restype = C.c_char_p
+        L.cel_timing.argtypes = [C.c_int]
+        L.cel_timing.restype = C.c_int
+        L.cel_kernel_stats.argtypes = [C.c_char_p, C.c_int, C.c_int]
+        L.cel_kernel_stats.restype = C.c_int
         _lib = L
     return _lib
 
 
 def version() -> int:
     return lib().cel_version()
+
+
+def timing(enable: bool) -> bool:
+    """Turn per-kernel event timing on/off; returns the previous setting."""
+    return bool(lib().cel_timing(1 if enable else 0))
+
+
+def kernel_stats(reset: bool = False) -> dict:
+    """{kernel name: (launches, total_ms)} accumulated since the last reset."""
+    buf = C.create_string_buffer(1 << 16)
+    lib().cel_kernel_stats(buf, len(buf), 1 if reset else 0)
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, cnt, ms = line.split()
+        out[name] = (int(cnt), float(ms))
+    return out
 
 
 def _check(rc: int):

@@ -173,7 +173,10 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
   CEL_TRY(relabel_csr(n, order_id, pos, g->out_ptr, g->out_idx, sptr, sidx, sc, s, st));
   k_node_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order_id, g->w, g->ob, d->bw, d->lat,
                                                      (flags & CEL_COMM_OFF) ? 1 : 0, wp, wcp, st);
-  k_level_sweep<true><<<1, kSweepB, 0, s>>>(L, level_ptr, sptr, sidx, wp, wcp, blp, st);
+  {
+    KTimer kt(s, "k_blevel_sweep");
+    k_level_sweep<true><<<1, kSweepB, 0, s>>>(L, level_ptr, sptr, sidx, wp, wcp, blp, st);
+  }
   k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, blp, blevel, st, &st->s0);
   if (tlevel && n > 0) {
     int32_t *pptr, *pidx;
@@ -182,7 +185,10 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
     CEL_TRY(sc.get(&pidx, g->m));
     CEL_TRY(sc.get(&tlp, n));
     CEL_TRY(relabel_csr(n, order_id, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
-    k_level_sweep<false><<<1, kSweepB, 0, s>>>(L, level_ptr, pptr, pidx, wp, wcp, tlp, st);
+    {
+      KTimer kt(s, "k_tlevel_sweep");
+      k_level_sweep<false><<<1, kSweepB, 0, s>>>(L, level_ptr, pptr, pidx, wp, wcp, tlp, st);
+    }
     k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, tlp, tlevel, st, &st->s1);
   }
   CEL_HIP(hipGetLastError());
@@ -202,5 +208,6 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
     CEL_TRY(segmented_sort(keys, ids, seg, sc, s));
   }
   CEL_HIP(hipStreamSynchronize(s));
+  timing_collect();
   return CEL_OK;
 }

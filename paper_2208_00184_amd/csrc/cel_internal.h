@@ -81,6 +81,23 @@ inline int grid_for(int64_t work, int block, int cap = 65535 * 4) {
   return (int)g;
 }
 
+// Optional per-kernel timing: records HIP events around one launch when
+// cel_timing(1) is on.  Pending pairs are resolved by timing_collect(), which
+// read_status() calls after its stream synchronisation.
+class KTimer {
+ public:
+  KTimer(hipStream_t s, const char *name);
+  ~KTimer();
+  KTimer(const KTimer &) = delete;
+  KTimer &operator=(const KTimer &) = delete;
+
+ private:
+  hipStream_t s_;
+  const char *name_;
+  hipEvent_t a_ = nullptr, b_ = nullptr;
+};
+void timing_collect();
+
 // Host-side argument checks (NULLs, sizes, device parameters).
 int check_host_graph(const cel_graph *g, const char *fn);
 int check_host_devices(const cel_devices *d, const char *fn);

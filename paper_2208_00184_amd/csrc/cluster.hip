@@ -252,6 +252,7 @@ template <int SL>
 static void launch_dp(int32_t n, int32_t R, const int32_t *lo, const int32_t *pptr,
                       const int32_t *pidx, const int64_t *cq, const int64_t *PO, int32_t *P,
                       Status *st, hipStream_t s) {
+  KTimer kt(s, "k_cluster_dp");
   k_cluster_dp<SL><<<1, 64, 0, s>>>(n, R, lo, pptr, pidx, cq, PO, P, st);
 }
 

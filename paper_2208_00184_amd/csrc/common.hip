@@ -87,6 +87,7 @@ Scratch::~Scratch() {
 int read_status(const Status *dst, Status *host, hipStream_t s) {
   CEL_HIP(hipMemcpyAsync(host, dst, sizeof(Status), hipMemcpyDeviceToHost, s));
   CEL_HIP(hipStreamSynchronize(s));
+  timing_collect();
   return CEL_OK;
 }
 
@@ -497,6 +498,7 @@ int relabel_csr(int32_t n, const int32_t *order, const int32_t *pos, const int32
   CEL_TRY(sc.get(&deg, n));
   k_row_deg<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, ptr, deg, st);
   CEL_TRY(exclusive_scan_i32(deg, pptr, n, sc, s));
+  KTimer kt(s, "k_relabel_rows");
   k_relabel_rows<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(n, order, pos, ptr, idx, pptr, pidx,
                                                               st);
   CEL_HIP(hipGetLastError());
@@ -618,12 +620,14 @@ int segmented_sort(uint64_t *keys, uint32_t *ids, const std::vector<int64_t> &se
   // one launch per 65535 tiles (grid x limit kept modest)
   for (size_t t0 = 0; t0 < tiles.size(); t0 += 65535) {
     size_t cnt = tiles.size() - t0 < 65535 ? tiles.size() - t0 : 65535;
+    KTimer kt(s, "k_sort_tiles");
     k_sort_tiles<<<(unsigned)cnt, 256, 0, s>>>(keys, ids, dtiles + t0);
   }
   CEL_HIP(hipGetLastError());
   if (big_start.empty()) {
     // the host vectors must outlive the async copies: synchronise before return
     CEL_HIP(hipStreamSynchronize(s));
+    timing_collect();
     return CEL_OK;
   }
   const int nb = (int)big_start.size();
@@ -644,6 +648,7 @@ int segmented_sort(uint64_t *keys, uint32_t *ids, const std::vector<int64_t> &se
   uint32_t *ia = ids, *ib = i2;
   int passes = 0;
   for (int64_t width = kSortTile; width < maxlen; width *= 2) {
+    KTimer kt(s, "k_merge_pass");
     k_merge_pass<<<grid_for(total, 256, 8192), 256, 0, s>>>(ka, ia, kb, ib, dstart, doff, nb,
                                                             width, total);
     std::swap(ka, kb);
@@ -659,6 +664,7 @@ int segmented_sort(uint64_t *keys, uint32_t *ids, const std::vector<int64_t> &se
     }
   }
   CEL_HIP(hipStreamSynchronize(s));
+  timing_collect();
   return CEL_OK;
 }
 

@@ -262,12 +262,15 @@ extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int3
                                                     st);
   k_dev_gather<<<grid_for((int64_t)K * n, 256, 8192), 256, 0, s>>>(K, n, order, node_dev, d->D,
                                                                   devp, st);
-  if (K == 1)
+  if (K == 1) {
+    KTimer kt(s, "k_makespan_sweep");
     k_makespan_sweep<1024><<<1, 1024, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq, devp, finp,
                                               makespan, st);
-  else
+  } else {
+    KTimer kt(s, "k_makespan_batch");
     k_makespan_sweep<256><<<(unsigned)K, 256, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq, devp,
                                                       finp, makespan, st);
+  }
   if (start || finish)
     k_makespan_out<<<grid_for((int64_t)K * n, 256, 8192), 256, 0, s>>>(K, n, order, finp, wp, start,
                                                                       finish, st);

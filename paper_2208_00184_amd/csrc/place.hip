@@ -403,8 +403,11 @@ extern "C" int cel_place(const cel_graph *g, const cel_devices *d, const int32_t
   CEL_TRY(segmented_sort(keys, ids, seg, sc, s));
   k_place_combine<<<grid_for(C, 256, 4096), 256, 0, s>>>(C, boff, keys, ids, ecost, ca, cc, ncp,
                                                         back, st);
-  k_place<<<1, kPlaceB, 0, s>>>(C, d->D, dcap, W, MEM, boff, ncp, ca, cc, back, cluster_dev, Fin,
-                                bs, bf, (int32_t)bcap, st);
+  {
+    KTimer kt(s, "k_place");
+    k_place<<<1, kPlaceB, 0, s>>>(C, d->D, dcap, W, MEM, boff, ncp, ca, cc, back, cluster_dev,
+                                  Fin, bs, bf, (int32_t)bcap, st);
+  }
   k_place_out<<<grid_for(n > C ? n : C, 256, 4096), 256, 0, s>>>(n, C, cluster_id, cluster_dev,
                                                                 node_dev, Fin, cluster_fin, st);
   CEL_HIP(hipGetLastError());

@@ -96,7 +96,10 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
   CEL_TRY(sc.get(&cnt, n));
   CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
   CEL_TRY(check_graph(g, 1, 0, /*bound=*/false, st, cnt, s));
-  k_kahn<<<1, kKahnB, 0, s>>>(*g, cnt, order_id, level, level_ptr, st);
+  {
+    KTimer kt(s, "k_kahn");
+    k_kahn<<<1, kKahnB, 0, s>>>(*g, cnt, order_id, level, level_ptr, st);
+  }
   CEL_HIP(hipGetLastError());
   Status h;
   CEL_TRY(read_status(st, &h, s));
@@ -115,5 +118,6 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
   k_zero_u64<<<grid_for(n, 256, 4096), 256, 0, s>>>(keys, n);
   CEL_TRY(segmented_sort(keys, reinterpret_cast<uint32_t *>(order_id), seg, sc, s));
   CEL_HIP(hipStreamSynchronize(s));
+  timing_collect();
   return CEL_OK;
 }
