@@ -71,6 +71,7 @@ void timing_collect() {
 
 }  // namespace cel
 
+
 extern "C" const char *cel_last_error(void) { return cel::last_error_text(); }
 
 extern "C" int cel_version(void) { return 100; /* 0.1.0 */ }

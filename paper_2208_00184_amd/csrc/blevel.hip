@@ -13,7 +13,6 @@
 namespace cel {
 
 constexpr int kSweepB = 1024;
-constexpr int kSweepHeavy = 64;  // degree above which a node is reduced by the whole block
 
 // per position: w and w + c (c = 0 with CEL_COMM_OFF)
 __global__ void k_node_costs(int32_t n, const int32_t *order, const int64_t *w, const int64_t *ob,
@@ -43,63 +42,261 @@ __device__ inline int64_t block_max_1024(int64_t x, int64_t *red) {
   return r;
 }
 
+// Windowed level sweep.
+//
 // REVERSE = true:  val[p] = wp[p] for a sink, else wcp[p] + max val[successor]   (eq. 3)
 // REVERSE = false: val[p] = 0 for a source, else max (val[pred] + wcp[pred])       (eq. 2)
+//
+// Positions are processed in windows of at most kWinN consecutive positions
+// (kWinE edges, kWinL levels), from the top for REVERSE, from the bottom
+// otherwise.  Staging a window reads its rows, edge targets and -- for every
+// neighbour outside the window, whose value is already final -- that value,
+// folding those values into a per-node partial maximum in LDS, all in one
+// parallel pass; it also records each edge's owner node.  Processing then
+// walks the window level by level touching LDS only (neighbours inside the
+// window belong to earlier-processed levels of the same window): the level's
+// edges are spread over the threads (atomic max into the owner's partial, so
+// a node of high degree costs no more than one of degree one), then every
+// node forms its value.  A level with at most 64 nodes and 256 edges is run
+// by wave 0 alone with no workgroup barrier (a wave sees its own LDS writes in
+// order); wider levels use the whole block with two barriers.  A single node
+// with more than kWinE edges forms a window of its own, reduced from global
+// memory by the whole block.
+constexpr int kWinN = 2048, kWinE = 8192, kWinL = 256;
+
 template <bool REVERSE>
 __global__ void __launch_bounds__(kSweepB)
-    k_level_sweep(int32_t L, const int32_t *lp, const int32_t *rptr, const int32_t *ridx,
-                  const int64_t *wp, const int64_t *wcp, int64_t *val, const Status *st) {
-  __shared__ int32_t s_nheavy;
-  __shared__ int32_t s_heavy[kSweepB];
+    k_level_sweep(int32_t n, int32_t L, const int32_t *lp, const int32_t *rptr,
+                  const int32_t *ridx, const int64_t *wp, const int64_t *wcp, int64_t *val,
+                  const Status *st) {
+  __shared__ int32_t s_lv[kWinL + 2];  // level boundaries near the cursor
+  __shared__ int32_t s_rp[kWinN + 1];  // rows of the candidate window (absolute edge offsets)
+  __shared__ int32_t s_tgt[kWinE];     // neighbour positions of the window's edges
+  __shared__ int16_t s_own[kWinE];     // owner (window-relative node) of each edge
+  __shared__ int64_t s_pm[kWinN];      // running max over neighbours, -1 if none yet
+  __shared__ int64_t s_v[kWinN];       // values computed in this window
+  __shared__ int64_t s_wc[kWinN];      // wcp (w for a sink in REVERSE) of the window's nodes
+  __shared__ int32_t s_la[kWinL], s_lb[kWinL], s_lea[kWinL], s_leb[kWinL], s_lend[kWinL];
   __shared__ int64_t s_red[kSweepB / 64];
+  __shared__ int32_t s_cut;
   if (failed(st)) return;
-  for (int32_t step = 0; step < L; step++) {
-    const int32_t l = REVERSE ? L - 1 - step : step;
-    const int32_t b = lp[l], e = lp[l + 1];
-    for (int32_t base = b; base < e; base += kSweepB) {
-      if (threadIdx.x == 0) s_nheavy = 0;
-      __syncthreads();  // also orders the previous level's writes before these reads
-      const int32_t p = base + threadIdx.x;
-      if (p < e) {
-        const int32_t k0 = rptr[p], k1 = rptr[p + 1];
-        if (k1 - k0 > kSweepHeavy) {
-          s_heavy[atomicAdd(&s_nheavy, 1)] = p;
-        } else if (REVERSE) {
-          if (k0 == k1) {
-            val[p] = wp[p];
-          } else {
-            int64_t mx = val[ridx[k0]];
-            for (int32_t k = k0 + 1; k < k1; k++) {
-              const int64_t x = val[ridx[k]];
-              mx = x > mx ? x : mx;
-            }
-            val[p] = wcp[p] + mx;
-          }
-        } else {
-          int64_t mx = 0;
-          for (int32_t k = k0; k < k1; k++) {
-            const int32_t q = ridx[k];
-            const int64_t x = val[q] + wcp[q];
-            mx = x > mx ? x : mx;
-          }
-          val[p] = mx;
+  const int tid = threadIdx.x;
+  const bool wave0 = tid < 64;
+  int32_t edge_lo = REVERSE ? n : 0;   // boundary of the processed region
+  int32_t lcur = REVERSE ? L - 1 : 0;  // level holding the next position to process
+  while (REVERSE ? edge_lo > 0 : edge_lo < n) {
+    CEL_TSTAMP(t0);
+    CEL_TCOUNT(REVERSE ? 6 : 16 + 6);
+    const int32_t Pc0 = REVERSE ? (edge_lo - kWinN > 0 ? edge_lo - kWinN : 0) : edge_lo;
+    const int32_t Pc1 = REVERSE ? edge_lo : (edge_lo + kWinN < n ? edge_lo + kWinN : n);
+    for (int t = tid; t <= Pc1 - Pc0; t += kSweepB) s_rp[t] = rptr[Pc0 + t];
+    for (int k = tid; k <= kWinL + 1; k += kSweepB) {
+      // REVERSE: s_lv[k] = lp[lcur + 1 - k], so level lcur - k is [s_lv[k+1], s_lv[k]);
+      // forward: s_lv[k] = lp[lcur + k], so level lcur + k is [s_lv[k], s_lv[k+1])
+      const int32_t l = REVERSE ? lcur + 1 - k : lcur + k;
+      s_lv[k] = lp[l < 0 ? 0 : (l > L ? L : l)];
+    }
+    if (tid == 0) s_cut = 0;
+    __syncthreads();
+    // window bounds: edge cap (counted from the boundary) and level cap
+    int32_t cnt = 0;
+    for (int t = tid; t < Pc1 - Pc0; t += kSweepB) {
+      if (REVERSE) cnt += (s_rp[Pc1 - Pc0] - s_rp[t] > kWinE) ? 1 : 0;  // too far below P1
+      else cnt += (s_rp[t + 1] - s_rp[0] <= kWinE) ? 1 : 0;            // fits above P0
+    }
+    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
+    if ((tid & 63) == 0 && cnt) atomicAdd(&s_cut, cnt);
+    __syncthreads();
+    int32_t P0, P1;
+    if (REVERSE) {
+      P1 = Pc1;
+      P0 = Pc0 + s_cut;
+      const int32_t lvcap = (lcur - kWinL + 1 > 0) ? s_lv[kWinL] : 0;  // start of level lcur-kWinL+1
+      if (P0 < lvcap) P0 = lvcap;
+    } else {
+      P0 = Pc0;
+      P1 = Pc0 + s_cut;
+      const int32_t lvcap = (lcur + kWinL < L) ? s_lv[kWinL] : n;  // end of level lcur+kWinL-1
+      if (P1 > lvcap) P1 = lvcap;
+    }
+    const bool heavy = (P0 == P1);  // one node with more than kWinE edges
+    if (heavy) {
+      if (REVERSE) P0 = P1 - 1;
+      else P1 = P0 + 1;
+    }
+    const int32_t E0 = s_rp[P0 - Pc0], E1 = s_rp[P1 - Pc0];
+    CEL_TSTAMP(t1);
+    CEL_TADD(REVERSE ? 0 : 16 + 0, t0, t1);
+    if (heavy) {
+      const int32_t p = P0;
+      int64_t mx = 0;  // values are >= 0; the node has > kWinE neighbours
+      for (int32_t k = E0 + tid; k < E1; k += kSweepB) {
+        const int32_t r = ridx[k];
+        const int64_t x = REVERSE ? val[r] : val[r] + wcp[r];
+        mx = x > mx ? x : mx;
+      }
+      mx = block_max_1024(mx, s_red);
+      if (tid == 0) val[p] = REVERSE ? wcp[p] + mx : mx;
+    } else {
+      const int32_t R0 = P0 - Pc0;  // row of P0 in s_rp
+      // stage nodes: costs, partials (0 for a REVERSE sink: its value is w),
+      // edge owners
+      for (int32_t i = tid; i < P1 - P0; i += kSweepB) {
+        const int32_t k0 = s_rp[R0 + i] - E0, k1 = s_rp[R0 + i + 1] - E0;
+        const bool sink = k0 == k1;
+        s_pm[i] = (REVERSE && sink) ? 0 : -1;
+        s_wc[i] = (REVERSE && sink) ? wp[P0 + i] : wcp[P0 + i];
+        for (int32_t q = k0; q < k1; q++) s_own[q] = (int16_t)i;
+      }
+      // per-level ranges of the window: nodes [a, b), edges [ea, eb) (window-relative)
+      for (int32_t k = tid; k < kWinL; k += kSweepB) {
+        const int32_t lb = REVERSE ? s_lv[k + 1] : s_lv[k];
+        const int32_t le = REVERSE ? s_lv[k] : s_lv[k + 1];
+        // clamp to the window: levels outside it become empty ranges at its edge
+        int32_t a = lb < P0 ? P0 : (lb > P1 ? P1 : lb);
+        const int32_t b = le < P0 ? P0 : (le > P1 ? P1 : le);
+        if (a > b) a = b;
+        s_la[k] = a - P0;
+        s_lb[k] = b - P0;
+        s_lea[k] = s_rp[a - Pc0] - E0;
+        s_leb[k] = s_rp[b - Pc0] - E0;
+        s_lend[k] = REVERSE ? (lb <= P0) : (le >= P1);
+      }
+      __syncthreads();
+      CEL_TSTAMP(t2);
+      CEL_TADD(REVERSE ? 1 : 16 + 1, t1, t2);
+      // stage edges: neighbours outside the window are final
+      for (int32_t e = E0 + tid; e < E1; e += kSweepB) {
+        const int32_t r = ridx[e];
+        s_tgt[e - E0] = r;
+        if (REVERSE ? (r >= P1) : (r < P0)) {
+          const int64_t x = REVERSE ? val[r] : val[r] + wcp[r];
+          atomicMax((long long *)&s_pm[s_own[e - E0]], (long long)x);
         }
       }
       __syncthreads();
-      const int32_t nh = s_nheavy;
-      for (int32_t h = 0; h < nh; h++) {
-        const int32_t q = s_heavy[h];
-        const int32_t k0 = rptr[q], k1 = rptr[q + 1];
-        int64_t mx = 0;  // all values are >= 0 and the node has > 64 neighbours
-        for (int32_t k = k0 + threadIdx.x; k < k1; k += kSweepB) {
-          const int32_t r = ridx[k];
-          const int64_t x = REVERSE ? val[r] : val[r] + wcp[r];
-          mx = x > mx ? x : mx;
+      CEL_TSTAMP(t3);
+      CEL_TADD(REVERSE ? 2 : 16 + 2, t2, t3);
+      // level metadata in registers: lane l holds levels l, l+64, l+128, l+192
+      int32_t ma[4], mb[4], mea[4], meb[4], mend[4];
+#pragma unroll
+      for (int u = 0; u < 4; u++) {
+        const int k = (tid & 63) + 64 * u;
+        ma[u] = s_la[k];
+        mb[u] = s_lb[k];
+        mea[u] = s_lea[k];
+        meb[u] = s_leb[k];
+        mend[u] = s_lend[k];
+      }
+      bool synced = true;  // every wave has seen all LDS writes made so far
+      for (int32_t k = 0; k < kWinL; k++) {
+        const int u = k >> 6, ln = k & 63;
+        int32_t a, b, ea, eb, stop;
+        switch (u) {  // uniform: pick the register set, then read lane ln
+          case 0: a = ma[0]; b = mb[0]; ea = mea[0]; eb = meb[0]; stop = mend[0]; break;
+          case 1: a = ma[1]; b = mb[1]; ea = mea[1]; eb = meb[1]; stop = mend[1]; break;
+          case 2: a = ma[2]; b = mb[2]; ea = mea[2]; eb = meb[2]; stop = mend[2]; break;
+          default: a = ma[3]; b = mb[3]; ea = mea[3]; eb = meb[3]; stop = mend[3]; break;
         }
-        mx = block_max_1024(mx, s_red);
-        if (threadIdx.x == 0) val[q] = REVERSE ? wcp[q] + mx : mx;
+        a = __builtin_amdgcn_readlane(a, ln);
+        b = __builtin_amdgcn_readlane(b, ln);
+        ea = __builtin_amdgcn_readlane(ea, ln);
+        eb = __builtin_amdgcn_readlane(eb, ln);
+        stop = __builtin_amdgcn_readlane(stop, ln);
+        if (a < b) {
+          const bool narrow = (b - a <= 256) && (eb - ea <= 512);
+          CEL_TSTAMP(tl0);
+          if (narrow) {
+            CEL_TCOUNT(REVERSE ? 4 : 16 + 4);
+            if (wave0) {
+              // neighbours inside the window, 8 edges per lane, loads batched
+              int32_t r[8];
+#pragma unroll
+              for (int q = 0; q < 8; q++) {
+                const int32_t e = ea + tid + 64 * q;
+                r[q] = e < eb ? s_tgt[e] : (REVERSE ? P1 : -1);
+              }
+              int64_t x[8];
+              int32_t ow[8];
+#pragma unroll
+              for (int q = 0; q < 8; q++) {
+                const bool in = REVERSE ? (r[q] < P1) : (r[q] >= P0);
+                const int32_t j = in ? r[q] - P0 : 0;
+                ow[q] = in ? s_own[ea + tid + 64 * q] : -1;
+                x[q] = REVERSE ? s_v[j] : s_v[j] + s_wc[j];
+              }
+#pragma unroll
+              for (int q = 0; q < 8; q++)
+                if (ow[q] >= 0) atomicMax((long long *)&s_pm[ow[q]], (long long)x[q]);
+              wave_lds_sync();
+#pragma unroll
+              for (int q = 0; q < 4; q++) {
+                const int32_t i = a + tid + 64 * q;
+                if (i < b) {
+                  const int64_t pm = s_pm[i];
+                  const int64_t v = REVERSE ? s_wc[i] + pm : (pm > 0 ? pm : 0);
+                  s_v[i] = v;
+                  val[P0 + i] = v;
+                }
+              }
+              wave_lds_sync();
+            }
+            synced = false;
+            CEL_TSTAMP(tl1);
+            CEL_TADD(REVERSE ? 7 : 16 + 7, tl0, tl1);
+          } else {
+            CEL_TCOUNT(REVERSE ? 5 : 16 + 5);
+            if (!synced) __syncthreads();
+            for (int32_t e = ea + tid; e < eb; e += kSweepB) {
+              const int32_t r = s_tgt[e];
+              if (REVERSE ? (r < P1) : (r >= P0)) {
+                const int32_t j = r - P0;
+                const int64_t x = REVERSE ? s_v[j] : s_v[j] + s_wc[j];
+                atomicMax((long long *)&s_pm[s_own[e]], (long long)x);
+              }
+            }
+            __syncthreads();
+            for (int32_t i = a + tid; i < b; i += kSweepB) {
+              const int64_t pm = s_pm[i];
+              const int64_t v = REVERSE ? s_wc[i] + pm : (pm > 0 ? pm : 0);
+              s_v[i] = v;
+              val[P0 + i] = v;
+            }
+            __syncthreads();
+            synced = true;
+            CEL_TSTAMP(tl1);
+            CEL_TADD(REVERSE ? 8 : 16 + 8, tl0, tl1);
+          }
+        }
+        if (stop) break;  // the window ends inside this level
+      }
+      CEL_TSTAMP(t4);
+      CEL_TADD(REVERSE ? 3 : 16 + 3, t3, t4);
+    }
+    // advance the cursor to the level holding the next unprocessed position
+    // (s_lv still covers every level the window touched)
+    if (REVERSE) {
+      edge_lo = P0;
+      if (P0 > 0) {
+        int32_t k = 1;  // smallest k >= 1 with start(lcur + 1 - k) <= P0 - 1
+        while (k <= kWinL + 1 && s_lv[k] > P0 - 1) k++;
+        if (k <= kWinL + 1) {
+          lcur = lcur + 1 - k;
+        } else {  // only past a run of empty levels
+          int32_t l = lcur - kWinL - 1;
+          while (l > 0 && lp[l] > P0 - 1) l--;
+          lcur = l;
+        }
+      }
+    } else {
+      edge_lo = P1;
+      if (P1 < n) {
+        int32_t k = 0;  // largest k with start(lcur + k) <= P1
+        while (k < kWinL && lcur + k + 1 < L && s_lv[k + 1] <= P1) k++;
+        lcur = lcur + k;
       }
     }
+    __syncthreads();
   }
 }
 
@@ -143,6 +340,8 @@ __global__ void k_prio_keys(int32_t n, const int32_t *order, const int64_t *blp,
 
 using namespace cel;
 
+CEL_PHASE_READER(cel_debug_phases_blevel)
+
 extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_t *level,
                           const int32_t *level_ptr, const int32_t *order_id, int32_t L,
                           int32_t flags, int64_t *blevel, int64_t *tlevel, int32_t *prio_order,
@@ -175,7 +374,7 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
                                                      (flags & CEL_COMM_OFF) ? 1 : 0, wp, wcp, st);
   {
     KTimer kt(s, "k_blevel_sweep");
-    k_level_sweep<true><<<1, kSweepB, 0, s>>>(L, level_ptr, sptr, sidx, wp, wcp, blp, st);
+    k_level_sweep<true><<<1, kSweepB, 0, s>>>(n, L, level_ptr, sptr, sidx, wp, wcp, blp, st);
   }
   k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, blp, blevel, st, &st->s0);
   if (tlevel && n > 0) {
@@ -187,7 +386,7 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
     CEL_TRY(relabel_csr(n, order_id, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
     {
       KTimer kt(s, "k_tlevel_sweep");
-      k_level_sweep<false><<<1, kSweepB, 0, s>>>(L, level_ptr, pptr, pidx, wp, wcp, tlp, st);
+      k_level_sweep<false><<<1, kSweepB, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, wcp, tlp, st);
     }
     k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, tlp, tlevel, st, &st->s1);
   }

@@ -37,6 +37,105 @@ __device__ inline bool failed(const Status *st) {
   return __atomic_load_n(&st->err, __ATOMIC_RELAXED) != 0u;
 }
 
+// Orders a wave's own LDS accesses: every LDS write or atomic issued before it
+// by any lane of this wave is visible to every lane after it.  (Compiler
+// fence plus a wait for the wave's outstanding LDS operations.)
+__device__ inline void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0), vmcnt/expcnt untouched
+  __builtin_amdgcn_wave_barrier();
+}
+
+// ------------------------------------------------ wave-level scans with DPP
+// DPP moves read another lane's register inside the VALU (no LDS round trip).
+// Lanes whose source is outside the allowed rows keep `old`.
+template <int CTRL, int ROWMASK>
+__device__ inline int32_t dpp32(int32_t src, int32_t old) {
+  return __builtin_amdgcn_update_dpp(old, src, CTRL, ROWMASK, 0xF, false);
+}
+template <int CTRL, int ROWMASK>
+__device__ inline int64_t dpp64(int64_t src, int64_t old) {
+  const int32_t lo = dpp32<CTRL, ROWMASK>((int32_t)src, (int32_t)old);
+  const int32_t hi = dpp32<CTRL, ROWMASK>((int32_t)(src >> 32), (int32_t)(old >> 32));
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// One Hillis-Steele step of the segmented scan of max-plus maps x -> max(a,
+// x + b): combine with the lane selected by CTRL unless this lane already
+// starts its segment; the identity (kNeg, 0, no start) fills missing lanes.
+constexpr int64_t kNeg = -(int64_t(1) << 62);
+template <int CTRL, int ROWMASK>
+__device__ inline void seg_step(int64_t &a, int64_t &b, int32_t &f) {
+  const int64_t ua = dpp64<CTRL, ROWMASK>(a, kNeg);
+  const int64_t ub = dpp64<CTRL, ROWMASK>(b, 0);
+  const int32_t uf = dpp32<CTRL, ROWMASK>(f, 0);
+  if (!f) {
+    const int64_t c = ua + b;
+    a = c > a ? c : a;
+    b = ub + b;
+    f = uf;
+  }
+}
+
+// Inclusive segmented scan over the 64 lanes of a wave: rows of 16 by right
+// shifts 1, 2, 4, 8, then row 0 -> 1 and 2 -> 3 (broadcast of lane 15 of the
+// row below), then rows 0-1 -> 2-3 (broadcast of lane 31).  f = 1 marks a
+// segment start and, on return, whether the segment began at or before the
+// lane.  a values must lie in [kNeg, 2^62), b in [0, 2^62).
+__device__ inline void wave_seg_scan_dpp(int64_t &a, int64_t &b, int32_t &f) {
+  seg_step<0x111, 0xF>(a, b, f);  // row_shr:1
+  seg_step<0x112, 0xF>(a, b, f);  // row_shr:2
+  seg_step<0x114, 0xF>(a, b, f);  // row_shr:4
+  seg_step<0x118, 0xF>(a, b, f);  // row_shr:8
+  seg_step<0x142, 0xA>(a, b, f);  // row_bcast:15 into rows 1 and 3
+  seg_step<0x143, 0xC>(a, b, f);  // row_bcast:31 into rows 2 and 3
+}
+
+// Calls f(u, e) for every CSR edge e whose source u lies in the 256 sources
+// [blockIdx.x * 256, + 256).  The block's edges form one contiguous range and
+// are spread over all threads (source found by binary search), so a node of
+// huge out-degree does not serialise on one thread.  `ptr` is a 257-entry
+// shared array; row pointers must already be validated.
+template <class F>
+__device__ inline void for_block_edges(const int32_t *out_ptr, int32_t n, int32_t *ptr, F f) {
+  const int64_t u0 = (int64_t)blockIdx.x * 256;
+  for (int i = threadIdx.x; i <= 256; i += blockDim.x) ptr[i] = out_ptr[u0 + i < n ? u0 + i : n];
+  __syncthreads();
+  for (int32_t e = ptr[0] + threadIdx.x; e < ptr[256]; e += blockDim.x) {
+    int lo = 0, hi = 255;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (ptr[mid] <= e) lo = mid;
+      else hi = mid - 1;
+    }
+    f((int32_t)(u0 + lo), e);
+  }
+}
+
+// Phase timers for tuning builds (-DCEL_PHASE_TIMERS): thread 0 of each
+// workgroup adds wall-clock intervals (100 MHz ticks) to a device array that
+// cel_debug_phases() reads back.  Compiled out otherwise.
+#ifdef CEL_PHASE_TIMERS
+static __device__ unsigned long long g_cel_phase[32];  // one copy per translation unit
+#define CEL_PHASE_READER(name)                                                          \
+  extern "C" int name(unsigned long long *out) {                                       \
+    unsigned long long z[32] = {};                                                     \
+    if (hipMemcpyFromSymbol(out, HIP_SYMBOL(cel::g_cel_phase), sizeof z) != hipSuccess) \
+      return -1;                                                                       \
+    return hipMemcpyToSymbol(HIP_SYMBOL(cel::g_cel_phase), z, sizeof z) == hipSuccess ? 0 : -1; \
+  }
+#define CEL_TSTAMP(v) const unsigned long long v = wall_clock64()
+#define CEL_TADD(i, a, b) \
+  do { if (threadIdx.x == 0) atomicAdd(&g_cel_phase[i], (b) - (a)); } while (0)
+#define CEL_TCOUNT(i) \
+  do { if (threadIdx.x == 0) atomicAdd(&g_cel_phase[i], 1ull); } while (0)
+#else
+#define CEL_PHASE_READER(name)
+#define CEL_TSTAMP(v) ((void)0)
+#define CEL_TADD(i, a, b) ((void)0)
+#define CEL_TCOUNT(i) ((void)0)
+#endif
+
 // ---------------------------------------------------------------- host side
 
 int set_error(int code, const char *fmt, ...);

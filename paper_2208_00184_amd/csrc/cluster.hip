@@ -224,21 +224,10 @@ __global__ void k_cut_cost(cel_graph g, int64_t bw, int64_t lat, const int32_t *
   __shared__ int32_t ptr[257];
   __shared__ int64_t red[4];
   if (failed(st)) return;
-  const int32_t n = g.n;
-  const int64_t u0 = (int64_t)blockIdx.x * 256;
-  for (int i = threadIdx.x; i <= 256; i += blockDim.x) ptr[i] = g.out_ptr[u0 + i < n ? u0 + i : n];
-  __syncthreads();
   int64_t acc = 0;
-  for (int32_t e = ptr[0] + threadIdx.x; e < ptr[256]; e += blockDim.x) {
-    int lo = 0, hi = 255;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (ptr[mid] <= e) lo = mid;
-      else hi = mid - 1;
-    }
-    const int32_t u = (int32_t)(u0 + lo);
+  for_block_edges(g.out_ptr, g.n, ptr, [&](int32_t u, int32_t e) {
     if (cid[u] != cid[g.out_idx[e]]) acc += comm_of(g.ob[u], bw, lat);
-  }
+  });
   for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
   __syncthreads();

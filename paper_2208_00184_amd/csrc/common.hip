@@ -99,17 +99,7 @@ __device__ inline uint64_t sat_add(uint64_t a, uint64_t b) {
   return (r < a || r > (uint64_t)kLim) ? (uint64_t)kLim : r;
 }
 
-__device__ inline void atomic_sat_add(uint64_t *p, uint64_t v) {
-  uint64_t old = __atomic_load_n(p, __ATOMIC_RELAXED);
-  while (old < (uint64_t)kLim) {
-    uint64_t nv = sat_add(old, v);
-    if (atomicCAS((unsigned long long *)p, (unsigned long long)old, (unsigned long long)nv) == old)
-      break;
-    old = __atomic_load_n(p, __ATOMIC_RELAXED);
-  }
-}
-
-__global__ void k_check_nodes(cel_graph g, int64_t bw, int64_t lat, Status *st) {
+__global__ void k_check_nodes(cel_graph g, int64_t bw, int64_t lat, Status *st, uint64_t *part_out) {
   __shared__ uint64_t part[4];
   const int32_t n = g.n, m = g.m;
   uint64_t acc = 0;
@@ -146,7 +136,7 @@ __global__ void k_check_nodes(cel_graph g, int64_t bw, int64_t lat, Status *st) 
   if (threadIdx.x == 0) {
     uint64_t tot = 0;
     for (int i = 0; i < (int)(blockDim.x >> 6); i++) tot = sat_add(tot, part[i]);
-    atomic_sat_add(&st->total, tot);
+    part_out[blockIdx.x] = tot;
   }
 }
 
@@ -164,29 +154,16 @@ __global__ void k_check_csr(cel_graph g, Status *st, int32_t *indeg, uint64_t *h
   __shared__ int32_t ptr[257];
   if (failed(st)) return;  // row pointers not validated
   const int32_t n = g.n;
-  const int64_t u0 = (int64_t)blockIdx.x * 256;
-  for (int i = threadIdx.x; i <= 256; i += blockDim.x) {
-    const int64_t u = u0 + i < n ? u0 + i : n;
-    ptr[i] = g.out_ptr[u];
-  }
-  __syncthreads();
   uint32_t bad = 0;
-  const int32_t e0 = ptr[0], e1 = ptr[256];
-  for (int32_t e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
-    int lo = 0, hi = 255;  // source row: last i with ptr[i] <= e
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (ptr[mid] <= e) lo = mid;
-      else hi = mid - 1;
-    }
+  for_block_edges(g.out_ptr, n, ptr, [&](int32_t u, int32_t e) {
     const int32_t t = g.out_idx[e];
     if (t < 0 || t >= n) {
       bad |= EB_ARG;
-      continue;
+      return;
     }
     atomicAdd(&indeg[t], 1);
-    atomicAdd((unsigned long long *)&hsum[t], (unsigned long long)mix64((uint64_t)(u0 + lo)));
-  }
+    atomicAdd((unsigned long long *)&hsum[t], (unsigned long long)mix64((uint64_t)u));
+  });
   if (bad) raise_err(st, bad);
 }
 
@@ -217,14 +194,29 @@ __global__ void k_check_csc(cel_graph g, Status *st, const int32_t *indeg, const
   if (bad) raise_err(st, bad);
 }
 
-__global__ void k_finish_overflow(Status *st) {
-  if (threadIdx.x == 0 && st->total >= (uint64_t)kLim) raise_err(st, EB_OVERFLOW);
+// one block: saturating sum of the per-block partials
+__global__ void k_finish_overflow(const uint64_t *part, int np, Status *st) {
+  __shared__ uint64_t red[4];
+  uint64_t acc = 0;
+  for (int i = threadIdx.x; i < np; i += blockDim.x) acc = sat_add(acc, part[i]);
+  for (int off = 32; off > 0; off >>= 1) acc = sat_add(acc, __shfl_down(acc, off));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t t = 0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); i++) t = sat_add(t, red[i]);
+    st->total = t;
+    if (t >= (uint64_t)kLim) raise_err(st, EB_OVERFLOW);
+  }
 }
 
 int check_graph(const cel_graph *g, int64_t bw, int64_t lat, bool bound, Status *st,
                 int32_t *indeg, hipStream_t s) {
   const int B = 256;
-  k_check_nodes<<<grid_for(g->n + 1, B, 2048), B, 0, s>>>(*g, bw, lat, st);
+  const int nbk = grid_for((int64_t)g->n + 1, B, 2048);
+  uint64_t *part;
+  CEL_HIP(hipMallocAsync((void **)&part, sizeof(uint64_t) * nbk, s));
+  k_check_nodes<<<nbk, B, 0, s>>>(*g, bw, lat, st, part);
   if (g->n > 0) {
     uint64_t *hsum;
     CEL_HIP(hipMallocAsync((void **)&hsum, sizeof(uint64_t) * (size_t)g->n, s));
@@ -234,7 +226,8 @@ int check_graph(const cel_graph *g, int64_t bw, int64_t lat, bool bound, Status 
     k_check_csc<<<grid_for(g->n, B, 4096), B, 0, s>>>(*g, st, indeg, hsum);
     CEL_HIP(hipFreeAsync(hsum, s));
   }
-  if (bound) k_finish_overflow<<<1, 64, 0, s>>>(st);
+  if (bound) k_finish_overflow<<<1, B, 0, s>>>(part, nbk, st);
+  CEL_HIP(hipFreeAsync(part, s));
   CEL_HIP(hipGetLastError());
   return CEL_OK;
 }
@@ -289,29 +282,23 @@ __global__ void k_check_levels_nodes(int32_t n, const int32_t *order, const int3
 
 // level[u] < level[v] on every edge (needs level values in range: checked above)
 __global__ void k_check_levels_edges(cel_graph g, const int32_t *level, int32_t L, Status *st) {
+  __shared__ int32_t ptr[257];
   if (failed(st)) return;  // edge indices or level values not validated
   uint32_t bad = 0;
-  for (int64_t u = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; u < g.n;
-       u += (int64_t)gridDim.x * blockDim.x) {
-    int32_t lu = level[u];
-    for (int32_t e = g.out_ptr[u]; e < g.out_ptr[u + 1]; e++) {
-      int32_t v = g.out_idx[e];
-      if (level[v] <= lu) bad |= EB_ORDER;
-    }
-  }
+  for_block_edges(g.out_ptr, g.n, ptr, [&](int32_t u, int32_t e) {
+    if (level[g.out_idx[e]] <= level[u]) bad |= EB_ORDER;
+  });
   if (bad) raise_err(st, bad);
 }
 
 // pos[u] < pos[v] on every edge (pos must be a complete permutation: checked)
 __global__ void k_check_topo_edges(cel_graph g, const int32_t *pos, Status *st) {
+  __shared__ int32_t ptr[257];
   if (failed(st)) return;
   uint32_t bad = 0;
-  for (int64_t u = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; u < g.n;
-       u += (int64_t)gridDim.x * blockDim.x) {
-    int32_t pu = pos[u];
-    for (int32_t e = g.out_ptr[u]; e < g.out_ptr[u + 1]; e++)
-      if (pos[g.out_idx[e]] <= pu) bad |= EB_ORDER;
-  }
+  for_block_edges(g.out_ptr, g.n, ptr, [&](int32_t u, int32_t e) {
+    if (pos[g.out_idx[e]] <= pos[u]) bad |= EB_ORDER;
+  });
   if (bad) raise_err(st, bad);
 }
 
@@ -326,7 +313,7 @@ int check_level_order(const cel_graph *g, const int32_t *order, const int32_t *l
   }
   k_check_levels_nodes<<<grid_for((int64_t)n + 1, B, 4096), B, 0, s>>>(n, order, level, level_ptr,
                                                                        L, st);
-  if (n > 0) k_check_levels_edges<<<grid_for(n, B, 4096), B, 0, s>>>(*g, level, L, st);
+  if (n > 0) k_check_levels_edges<<<(unsigned)((n + 255) / 256), B, 0, s>>>(*g, level, L, st);
   CEL_HIP(hipGetLastError());
   return CEL_OK;
 }
@@ -338,7 +325,7 @@ int check_topo_order(const cel_graph *g, const int32_t *order, int32_t *pos, Sta
   if (n > 0) {
     k_fill_i32<<<grid_for(n, B, 4096), B, 0, s>>>(pos, n, -1);
     k_inverse_perm<<<grid_for(n, B, 4096), B, 0, s>>>(n, order, pos, st);
-    k_check_topo_edges<<<grid_for(n, B, 4096), B, 0, s>>>(*g, pos, st);
+    k_check_topo_edges<<<(unsigned)((n + 255) / 256), B, 0, s>>>(*g, pos, st);
   }
   CEL_HIP(hipGetLastError());
   return CEL_OK;

@@ -48,13 +48,36 @@ __global__ void k_pos_costs(int32_t n, const int32_t *order, const int64_t *w, c
   }
 }
 
-template <int B>
+// Windowed sweep, one workgroup per placement.  Positions are taken in
+// windows of at most NC consecutive positions (EC in-edges, kMsL levels).
+// Staging folds every predecessor outside the window (its finish time is
+// final) into a partial ready time per node, records each edge's owner and
+// the owner's device, keeps the window's costs and devices in LDS and the
+// per-level ranges in registers (lane l holds levels l, l+64, ...).  Each
+// level of the window is then evaluated from LDS only: predecessors inside
+// the window edge-parallel (atomic max into the owner's ready time), then the
+// device-FIFO chains as a segmented max-plus scan over the level's nodes in
+// device-grouped order.  A level of at most 256 nodes and 512 edges is run by
+// wave 0 alone in rows of 64, without workgroup barriers; wider levels use
+// the whole block.  A node with more than EC predecessors forms a window of
+// its own.
+constexpr int kMsL = 256;
+
+template <int B, int NC, int EC>
 __global__ void __launch_bounds__(B)
     k_makespan_sweep(int32_t n, int32_t L, const int32_t *lp, const int32_t *pptr,
                      const int32_t *pidx, const int64_t *wp, const int64_t *cq,
                      const uint8_t *devp, int64_t *finp, int64_t *makespan, const Status *st) {
   constexpr int NW = B / 64;
   static_assert(B >= 256, "device partition uses 256 threads");
+  __shared__ int32_t s_lv[kMsL + 2];
+  __shared__ int32_t s_rp[NC + 1];
+  __shared__ int32_t s_tgt[EC];
+  __shared__ int16_t s_own[EC];
+  __shared__ uint8_t s_edv[EC];
+  __shared__ int64_t s_pm[NC], s_f[NC], s_w[NC], s_c[NC];
+  __shared__ uint8_t s_dv[NC];
+  __shared__ int32_t s_la[kMsL], s_lb[kMsL], s_lea[kMsL], s_leb[kMsL], s_lend[kMsL];
   __shared__ int64_t s_avail[256];
   __shared__ int32_t s_wcnt[NW][256];
   __shared__ int32_t s_dbase[256];
@@ -65,124 +88,302 @@ __global__ void __launch_bounds__(B)
   __shared__ int64_t s_wa[NW], s_wb[NW];
   __shared__ int32_t s_wf[NW];
   __shared__ int64_t s_red[NW];
+  __shared__ int32_t s_cut;
   if (failed(st)) return;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const bool wave0 = tid < 64;
+  const uint64_t lanemask_lt = (1ull << lane) - 1ull;
   const int64_t koff = (int64_t)blockIdx.x * n;
   const uint8_t *dk = devp + koff;
   int64_t *fk = finp + koff;
   for (int i = tid; i < 256; i += B) s_avail[i] = 0;
   int64_t mk = 0;
-  for (int32_t l = 0; l < L; l++) {
-    const int32_t b = lp[l], e = lp[l + 1];
-    for (int32_t base = b; base < e; base += B) {
-      const int32_t cnt = e - base < B ? e - base : B;
-      const bool act = tid < cnt;
-      const int32_t p = base + tid;
-      for (int i = tid; i < NW * 256; i += B) (&s_wcnt[0][0])[i] = 0;
-      __syncthreads();  // earlier finishes and free times visible; counters clear
-      // ready time of every node of the chunk (independent within a level)
-      int dv = 255;
-      int64_t a = 0, w = 0;
-      if (act) {
-        dv = dk[p];
-        int64_t ready = 0;
-        const int32_t k1 = pptr[p + 1];
-        for (int32_t k = pptr[p]; k < k1; k++) {
-          const int32_t q = pidx[k];
-          const int64_t f = fk[q] + (dk[q] != dv ? cq[q] : 0);
-          ready = f > ready ? f : ready;
-        }
-        w = wp[p];
-        a = ready + w;
-      }
-      // stable partition by device: rank among same-device lanes of the wave
-      uint64_t eq = ~0ull;
-      for (int bit = 0; bit < 8; bit++) {
-        const int on = (dv >> bit) & 1;
-        const uint64_t bb = __ballot(on);
-        eq &= on ? bb : ~bb;
-      }
-      const int rank = __popcll(eq & ((1ull << lane) - 1ull));
-      if (act && rank == 0) s_wcnt[wv][dv] = __popcll(eq);
-      __syncthreads();
-      int32_t tot = 0;
-      if (tid < 256) {
-        for (int w2 = 0; w2 < NW; w2++) {
-          const int32_t c = s_wcnt[w2][tid];
-          s_wcnt[w2][tid] = tot;
-          tot += c;
-        }
-      }
-      int32_t inc = tot;
-      for (int off = 1; off < 64; off <<= 1) {
-        const int32_t y = __shfl_up(inc, off);
-        if (lane >= off) inc += y;
-      }
-      if (tid < 256 && lane == 63) s_dsum[wv] = inc;
-      __syncthreads();
-      if (tid < 256) {
-        int32_t bv = inc - tot;
-        for (int w2 = 0; w2 < wv; w2++) bv += s_dsum[w2];
-        s_dbase[tid] = bv;
-      }
-      __syncthreads();
-      if (act) {
-        const int q = s_dbase[dv] + s_wcnt[wv][dv] + rank;
-        s_a[q] = a;
-        s_b[q] = w;
-        s_pos[q] = p;
-        s_dev[q] = (uint8_t)dv;
-      }
-      __syncthreads();
-      // segmented scan of (a, b) in device-grouped order
-      const bool aq = tid < cnt;
-      int64_t sa = 0, sb = 0;
-      int dq = 255;
-      bool f = true;
-      if (aq) {
-        sa = s_a[tid];
-        sb = s_b[tid];
-        dq = s_dev[tid];
-        f = (tid == 0) || (s_dev[tid - 1] != dq);
-      }
-      for (int off = 1; off < 64; off <<= 1) {
-        const int64_t ua = __shfl_up(sa, off), ub = __shfl_up(sb, off);
-        const int uf = __shfl_up((int)f, off);
-        if (lane >= off && !f) {
-          sa = (ua + sb) > sa ? ua + sb : sa;
-          sb = ub + sb;
-          f = uf != 0;
-        }
-      }
-      if (lane == 63) {
-        s_wa[wv] = sa;
-        s_wb[wv] = sb;
-        s_wf[wv] = f ? 1 : 0;
-      }
-      __syncthreads();
-      if (aq && !f && wv > 0) {  // segment began in an earlier wave: prepend their totals
-        int64_t ca = s_wa[wv - 1], cb = s_wb[wv - 1];
-        bool done = s_wf[wv - 1] != 0;
-        for (int w2 = wv - 2; w2 >= 0 && !done; w2--) {
-          ca = (s_wa[w2] + cb) > ca ? s_wa[w2] + cb : ca;
-          cb = s_wb[w2] + cb;
-          done = s_wf[w2] != 0;
-        }
-        sa = (ca + sb) > sa ? ca + sb : sa;
-        sb = cb + sb;
-      }
-      int64_t fin = 0;
-      bool last = false;
-      if (aq) {
-        const int64_t viafree = s_avail[dq] + sb;
-        fin = viafree > sa ? viafree : sa;
-        fk[s_pos[tid]] = fin;
-        mk = fin > mk ? fin : mk;
-        last = (tid + 1 == cnt) || (s_dev[tid + 1] != dq);
-      }
-      __syncthreads();  // every read of s_avail is done
-      if (last) s_avail[dq] = fin;
+  int32_t P0 = 0, lcur = 0;
+  while (P0 < n) {
+    const int32_t Pc1 = P0 + NC < n ? P0 + NC : n;
+    for (int t = tid; t <= Pc1 - P0; t += B) s_rp[t] = pptr[P0 + t];
+    for (int k = tid; k <= kMsL + 1; k += B) {
+      const int32_t l = lcur + k;  // level lcur + k is [s_lv[k], s_lv[k+1])
+      s_lv[k] = lp[l > L ? L : l];
     }
+    if (tid == 0) s_cut = 0;
+    __syncthreads();
+    int32_t cnt = 0;
+    for (int t = tid; t < Pc1 - P0; t += B) cnt += (s_rp[t + 1] - s_rp[0] <= EC) ? 1 : 0;
+    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
+    if (lane == 0 && cnt) atomicAdd(&s_cut, cnt);
+    __syncthreads();
+    int32_t P1 = P0 + s_cut;
+    const int32_t lvcap = (lcur + kMsL < L) ? s_lv[kMsL] : n;
+    if (P1 > lvcap) P1 = lvcap;
+    const bool heavy = (P1 == P0);  // one node with more than EC predecessors
+    if (heavy) P1 = P0 + 1;
+    const int32_t E0 = s_rp[0], E1 = s_rp[P1 - P0];
+    for (int32_t i = tid; i < P1 - P0; i += B) {
+      const uint8_t dv = dk[P0 + i];
+      s_pm[i] = 0;
+      s_w[i] = wp[P0 + i];
+      s_c[i] = cq[P0 + i];
+      s_dv[i] = dv;
+      if (!heavy)
+        for (int32_t q = s_rp[i] - E0; q < s_rp[i + 1] - E0; q++) {
+          s_own[q] = (int16_t)i;
+          s_edv[q] = dv;
+        }
+    }
+    for (int32_t k = tid; k < kMsL; k += B) {
+      const int32_t lb = s_lv[k], le = s_lv[k + 1];
+      int32_t a = lb < P0 ? P0 : (lb > P1 ? P1 : lb);
+      const int32_t b = le < P0 ? P0 : (le > P1 ? P1 : le);
+      if (a > b) a = b;
+      s_la[k] = a - P0;
+      s_lb[k] = b - P0;
+      s_lea[k] = heavy ? 0 : s_rp[a - P0] - E0;
+      s_leb[k] = heavy ? 0 : s_rp[b - P0] - E0;
+      s_lend[k] = le >= P1;
+    }
+    __syncthreads();
+    // predecessors before the window are final: fold them into s_pm
+    for (int32_t e = E0 + tid; e < E1; e += B) {
+      const int32_t q = pidx[e];
+      const int32_t own = heavy ? 0 : s_own[e - E0];
+      if (!heavy) s_tgt[e - E0] = q;
+      if (q < P0) {
+        const int64_t x = fk[q] + (dk[q] != s_dv[own] ? cq[q] : 0);
+        atomicMax((long long *)&s_pm[own], (long long)x);
+      }
+    }
+    __syncthreads();
+    int32_t ma[4], mb[4], mea[4], meb[4], mend[4];
+#pragma unroll
+    for (int u = 0; u < 4; u++) {
+      const int k = lane + 64 * u;
+      ma[u] = s_la[k];
+      mb[u] = s_lb[k];
+      mea[u] = s_lea[k];
+      meb[u] = s_leb[k];
+      mend[u] = s_lend[k];
+    }
+    bool synced = true;
+    for (int32_t k = 0; k < kMsL; k++) {
+      const int u = k >> 6, ln = k & 63;
+      int32_t a0, b0, ea, eb, stop;
+      switch (u) {
+        case 0: a0 = ma[0]; b0 = mb[0]; ea = mea[0]; eb = meb[0]; stop = mend[0]; break;
+        case 1: a0 = ma[1]; b0 = mb[1]; ea = mea[1]; eb = meb[1]; stop = mend[1]; break;
+        case 2: a0 = ma[2]; b0 = mb[2]; ea = mea[2]; eb = meb[2]; stop = mend[2]; break;
+        default: a0 = ma[3]; b0 = mb[3]; ea = mea[3]; eb = meb[3]; stop = mend[3]; break;
+      }
+      a0 = __builtin_amdgcn_readlane(a0, ln);
+      b0 = __builtin_amdgcn_readlane(b0, ln);
+      ea = __builtin_amdgcn_readlane(ea, ln);
+      eb = __builtin_amdgcn_readlane(eb, ln);
+      stop = __builtin_amdgcn_readlane(stop, ln);
+      if (a0 < b0) {
+        const bool narrow = (b0 - a0 <= 256) && (eb - ea <= 512);
+        if (narrow) {
+          if (wave0) {
+            // predecessors inside the window: 8 edges per lane, loads batched
+            int32_t r[8];
+#pragma unroll
+            for (int q = 0; q < 8; q++) {
+              const int32_t e = ea + lane + 64 * q;
+              r[q] = e < eb ? s_tgt[e] : -1;
+            }
+            int64_t x[8];
+            int32_t ow[8];
+#pragma unroll
+            for (int q = 0; q < 8; q++) {
+              const int32_t e = ea + lane + 64 * q;
+              const bool in = r[q] >= P0;
+              const int32_t j = in ? r[q] - P0 : 0;
+              ow[q] = in ? s_own[e] : -1;
+              const uint8_t od = in ? s_edv[e] : 0;
+              x[q] = s_f[j] + (s_dv[j] != od ? s_c[j] : 0);
+            }
+#pragma unroll
+            for (int q = 0; q < 8; q++)
+              if (ow[q] >= 0) atomicMax((long long *)&s_pm[ow[q]], (long long)x[q]);
+            wave_lds_sync();
+            for (int32_t row = a0; row < b0; row += 64) {
+              const int32_t cnt2 = b0 - row < 64 ? b0 - row : 64;
+              const bool act = lane < cnt2;
+              const int32_t i = row + lane;
+              int dv = 0;
+              int64_t aa = 0, ww = 0;
+              if (act) {
+                dv = s_dv[i];
+                ww = s_w[i];
+                aa = s_pm[i] + ww;
+              }
+              // slot in device-grouped order: devices ascending, positions ascending
+              const uint64_t actm = __ballot(act);
+              uint64_t eq = actm, lt = 0;
+              for (int bit = 7; bit >= 0; bit--) {
+                const int on = (dv >> bit) & 1;
+                const uint64_t bb = __ballot(on) & actm;
+                if (on) {
+                  lt |= eq & ~bb;
+                  eq &= bb;
+                } else {
+                  eq &= ~bb;
+                }
+              }
+              if (act) {
+                const int q = __popcll(lt) + __popcll(eq & lanemask_lt);
+                s_a[q] = aa;
+                s_b[q] = ww;
+                s_pos[q] = i;
+                s_dev[q] = (uint8_t)dv;
+              }
+              wave_lds_sync();
+              int64_t sa = kNeg, sb = 0;
+              int dq = 0;
+              int32_t f = 1;
+              if (act) {
+                sa = s_a[lane];
+                sb = s_b[lane];
+                dq = s_dev[lane];
+                f = (lane == 0) || (s_dev[lane - 1] != dq);
+              }
+              wave_seg_scan_dpp(sa, sb, f);
+              int64_t fin = 0;
+              bool last = false;
+              if (act) {
+                const int64_t viafree = s_avail[dq] + sb;
+                fin = viafree > sa ? viafree : sa;
+                const int32_t j = s_pos[lane];
+                s_f[j] = fin;
+                fk[P0 + j] = fin;
+                mk = fin > mk ? fin : mk;
+                last = (lane + 1 == cnt2) || (s_dev[lane + 1] != dq);
+              }
+              wave_lds_sync();
+              if (last) s_avail[dq] = fin;
+              wave_lds_sync();
+            }
+          }
+          synced = false;
+        } else {
+          if (!synced) __syncthreads();
+          for (int32_t e = ea + tid; e < eb; e += B) {
+            const int32_t r = s_tgt[e];
+            if (r >= P0) {
+              const int32_t j = r - P0;
+              const int64_t x = s_f[j] + (s_dv[j] != s_edv[e] ? s_c[j] : 0);
+              atomicMax((long long *)&s_pm[s_own[e]], (long long)x);
+            }
+          }
+          __syncthreads();
+          for (int32_t base = a0; base < b0; base += B) {
+            const int32_t cnt2 = b0 - base < B ? b0 - base : B;
+            const bool act = tid < cnt2;
+            const int32_t i = base + tid;
+            for (int x = tid; x < NW * 256; x += B) (&s_wcnt[0][0])[x] = 0;
+            __syncthreads();
+            int dv = 255;
+            int64_t aa = 0, ww = 0;
+            if (act) {
+              dv = s_dv[i];
+              ww = s_w[i];
+              aa = s_pm[i] + ww;
+            }
+            // stable partition by device: rank among same-device lanes of the wave
+            uint64_t eq = ~0ull;
+            for (int bit = 0; bit < 8; bit++) {
+              const int on = (dv >> bit) & 1;
+              const uint64_t bb = __ballot(on);
+              eq &= on ? bb : ~bb;
+            }
+            const int rank = __popcll(eq & lanemask_lt);
+            if (act && rank == 0) s_wcnt[wv][dv] = __popcll(eq);
+            __syncthreads();
+            int32_t tot = 0;
+            if (tid < 256) {
+              for (int w2 = 0; w2 < NW; w2++) {
+                const int32_t c = s_wcnt[w2][tid];
+                s_wcnt[w2][tid] = tot;
+                tot += c;
+              }
+            }
+            int32_t inc = tot;
+            for (int off = 1; off < 64; off <<= 1) {
+              const int32_t y = __shfl_up(inc, off);
+              if (lane >= off) inc += y;
+            }
+            if (tid < 256 && lane == 63) s_dsum[wv] = inc;
+            __syncthreads();
+            if (tid < 256) {
+              int32_t bv = inc - tot;
+              for (int w2 = 0; w2 < wv; w2++) bv += s_dsum[w2];
+              s_dbase[tid] = bv;
+            }
+            __syncthreads();
+            if (act) {
+              const int q = s_dbase[dv] + s_wcnt[wv][dv] + rank;
+              s_a[q] = aa;
+              s_b[q] = ww;
+              s_pos[q] = i;
+              s_dev[q] = (uint8_t)dv;
+            }
+            __syncthreads();
+            // segmented scan of (a, b) in device-grouped order
+            const bool aq = tid < cnt2;
+            int64_t sa = kNeg, sb = 0;
+            int dq = 255;
+            int32_t f = 1;
+            if (aq) {
+              sa = s_a[tid];
+              sb = s_b[tid];
+              dq = s_dev[tid];
+              f = (tid == 0) || (s_dev[tid - 1] != dq);
+            }
+            wave_seg_scan_dpp(sa, sb, f);
+            if (lane == 63) {
+              s_wa[wv] = sa;
+              s_wb[wv] = sb;
+              s_wf[wv] = f;
+            }
+            __syncthreads();
+            if (aq && !f && wv > 0) {  // segment began in an earlier wave: prepend their totals
+              int64_t ca = s_wa[wv - 1], cb = s_wb[wv - 1];
+              bool done = s_wf[wv - 1] != 0;
+              for (int w2 = wv - 2; w2 >= 0 && !done; w2--) {
+                ca = (s_wa[w2] + cb) > ca ? s_wa[w2] + cb : ca;
+                cb = s_wb[w2] + cb;
+                done = s_wf[w2] != 0;
+              }
+              sa = (ca + sb) > sa ? ca + sb : sa;
+              sb = cb + sb;
+            }
+            int64_t fin = 0;
+            bool last = false;
+            if (aq) {
+              const int64_t viafree = s_avail[dq] + sb;
+              fin = viafree > sa ? viafree : sa;
+              const int32_t j = s_pos[tid];
+              s_f[j] = fin;
+              fk[P0 + j] = fin;
+              mk = fin > mk ? fin : mk;
+              last = (tid + 1 == cnt2) || (s_dev[tid + 1] != dq);
+            }
+            __syncthreads();  // every read of s_avail is done
+            if (last) s_avail[dq] = fin;
+            __syncthreads();
+          }
+          synced = true;
+        }
+      }
+      if (stop) break;  // the window ends inside this level
+    }
+    // next window starts at P1; move the level cursor to the level holding P1
+    if (P1 < n) {
+      int32_t k = 0;
+      while (k < kMsL && lcur + k + 1 < L && s_lv[k + 1] <= P1) k++;
+      lcur += k;
+    }
+    P0 = P1;
+    __syncthreads();
   }
   for (int off = 32; off > 0; off >>= 1) {
     const int64_t y = __shfl_xor(mk, off);
@@ -222,6 +423,8 @@ __global__ void k_fill_i64(int64_t *p, int64_t n, int64_t v) {
 }  // namespace cel
 
 using namespace cel;
+
+CEL_PHASE_READER(cel_debug_phases_makespan)
 
 extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int32_t *order,
                             const int32_t *level, const int32_t *level_ptr, int32_t L, int32_t K,
@@ -264,12 +467,12 @@ extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int3
                                                                   devp, st);
   if (K == 1) {
     KTimer kt(s, "k_makespan_sweep");
-    k_makespan_sweep<1024><<<1, 1024, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq, devp, finp,
-                                              makespan, st);
+    k_makespan_sweep<1024, 1536, 6144><<<1, 1024, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq,
+                                                          devp, finp, makespan, st);
   } else {
     KTimer kt(s, "k_makespan_batch");
-    k_makespan_sweep<256><<<(unsigned)K, 256, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq, devp,
-                                                      finp, makespan, st);
+    k_makespan_sweep<256, 1024, 4096><<<(unsigned)K, 256, 0, s>>>(n, L, level_ptr, pptr, pidx, wp,
+                                                                  cq, devp, finp, makespan, st);
   }
   if (start || finish)
     k_makespan_out<<<grid_for((int64_t)K * n, 256, 8192), 256, 0, s>>>(K, n, order, finp, wp, start,

@@ -44,24 +44,13 @@ __global__ void k_place_edges(cel_graph g, int64_t bw, int64_t lat, const int32_
                               int64_t *ecost, Status *st) {
   __shared__ int32_t ptr[257];
   if (failed(st)) return;
-  const int32_t n = g.n;
-  const int64_t u0 = (int64_t)blockIdx.x * 256;
-  for (int i = threadIdx.x; i <= 256; i += blockDim.x) ptr[i] = g.out_ptr[u0 + i < n ? u0 + i : n];
-  __syncthreads();
   uint32_t bad = 0;
-  for (int32_t e = ptr[0] + threadIdx.x; e < ptr[256]; e += blockDim.x) {
-    int lo = 0, hi = 255;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (ptr[mid] <= e) lo = mid;
-      else hi = mid - 1;
-    }
-    const int32_t u = (int32_t)(u0 + lo);
+  for_block_edges(g.out_ptr, g.n, ptr, [&](int32_t u, int32_t e) {
     const int32_t a = cid[u], b = cid[g.out_idx[e]];
-    if (a == b) continue;
+    if (a == b) return;
     if (a > b) {
       bad |= EB_ORDER;
-      continue;
+      return;
     }
     if (PASS == 0) {
       atomicAdd(&cnt[b], 1);
@@ -71,7 +60,7 @@ __global__ void k_place_edges(cel_graph g, int64_t bw, int64_t lat, const int32_
       ids[slot] = (uint32_t)e;
       ecost[e] = comm_of(g.ob[u], bw, lat);
     }
-  }
+  });
   if (bad) raise_err(st, bad);
 }
 
