@@ -4,15 +4,28 @@
 // With PO the prefix sum of each node's out-going comm (outdeg * c) and
 // Int(i, j) the comm of edges with both ends inside positions [i, j),
 //   cost(i, j) = PO[j] - PO[i] - Int(i, j)            (eq. 4 rewritten)
-//   S(j)      = PO[j] + min_i V_j(i),   V_j(i) = S(i) - PO[i] - Int(i, j).
-// Moving from j to j+1 only adds the in-edges of the node at position j, each
-// lowering V(i) for every i at or before its source (eq. 5's subtracted sum).
-// The recurrence is sequential in j, so one wave runs it with the window of
-// the last R candidates held 64 lanes wide in registers: per step, a few
-// predicated subtractions and one wave-wide (min value, min index) reduction.
-// The in-edge lists are staged through LDS in blocks so that no step waits on
-// a global load.  The memory bound lo(j) comes from a prefix sum of the
-// memory in order (binary search), the greedy mode from the same prefix sums.
+//   S(j)      = PO[j] + min_i V_j(i),   V_j(i) = S(i) - PO[i] - Int(i, j),
+// over lo(j) <= i < j (window R, memory cap M); ties go to the smallest i.
+//
+// The recurrence is sequential in j.  One workgroup runs it in blocks of 64
+// targets, one lane per target:
+//  * the candidates below the block ("old" ones, at most R) are split in
+//    chunks of 64 over waves 1..NW-1; each wave sweeps its candidates in
+//    descending order, merging the block's edge list (sorted by source,
+//    descending), so that every lane keeps the running Int of its own target
+//    and a running (min, argmin); per-wave offsets are added afterwards;
+//  * wave 0 meanwhile gathers, in registers, Int(i, j) for the candidates and
+//    targets inside the block, then runs the 64 in-block steps (one lane
+//    broadcast per step).
+// H(i) = V_{j0}(i) for the old candidates lives in an LDS ring and moves to
+// the next block by subtracting the comm of the block's edges whose source is
+// at or after i.  Only edges whose source lies in the window can change a
+// candidate, so each block's list holds only those; it is built and sorted by
+// a parallel pass and staged one block ahead.  Graphs whose blocks exceed the
+// staging sizes take a step-wise kernel that keeps the window in registers.
+//
+// The memory bound lo(j) comes from a prefix sum of the memory in order
+// (binary search), the greedy mode from the same prefix sums.
 #include "cel_internal.h"
 
 namespace cel {
@@ -72,12 +85,16 @@ __global__ void k_cluster_bounds(int32_t n, int32_t R, int64_t M, const int64_t 
   }
 }
 
+// ---------------------------------------------------- step-wise DP (fallback)
+// One wave; the window of the last R candidates is held 64 lanes wide in
+// registers: per step a few predicated subtractions and one wave-wide
+// (min value, min index) reduction.  In-edge lists are staged through LDS.
 constexpr int kDpBlk = 256;    // DP steps staged per block
 constexpr int kDpEcap = 6144;  // in-edges staged per block
 
 template <int SL>
 __global__ void __launch_bounds__(64)
-    k_cluster_dp(int32_t n, int32_t R, const int32_t *lo, const int32_t *pptr,
+    k_cluster_dp_step(int32_t n, int32_t R, const int32_t *lo, const int32_t *pptr,
                  const int32_t *pidx, const int64_t *cq, const int64_t *PO, int32_t *P,
                  Status *st) {
   constexpr int RW = 64 * SL;
@@ -182,6 +199,563 @@ __global__ void __launch_bounds__(64)
   if (lane == 0) st->s0 = PO[n] + G;  // S(n): the total inter-cluster comm
 }
 
+// ------------------------------------------------------------ blocked DP
+constexpr int kRing = 8192;  // LDS ring of H over positions (window R + 64 <= 4160)
+constexpr int kEC = 1024;    // staged edges of one block
+constexpr int kPF = 4;       // prefetched edges per thread of waves 1..NW-1
+constexpr int kMaxW = 7;     // candidate waves
+
+__device__ inline int32_t rl32(int32_t v, int32_t l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ inline int64_t rl64(int64_t v, int32_t l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int32_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int32_t)(v >> 32), l);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+__device__ inline int rmod(int32_t p) { return p & (kRing - 1); }
+
+// first k in [0, cnt) with q[k] <= thr (q descending), cnt if none; wave-uniform
+__device__ inline int32_t first_le(const int32_t *q, int32_t cnt, int32_t thr, int lane) {
+  for (int32_t base = 0; base < cnt; base += 64) {
+    const int32_t k = base + lane;
+    const uint64_t m = __ballot(k < cnt && q[k] <= thr);
+    if (m) return base + (int32_t)__builtin_ctzll(m);
+  }
+  return cnt;
+}
+
+// Per block of 64 targets (block b: j in [64b, 64b + 64)): the number of
+// in-edges of positions [64b, min(64b + 64, n)) whose source is at or after
+// lo(64b), and the largest such count.  One wave per block.
+__global__ void k_dp_count(int32_t n, int32_t nb, const int32_t *pptr, const int32_t *pidx,
+                           const int32_t *lo, int32_t *cnt, int32_t *mx, const Status *st) {
+  if (failed(st)) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t b = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6; b < nb; b += nw) {
+    const int32_t j0 = (int32_t)b * 64, pe = j0 + 64 < n ? j0 + 64 : n;
+    const int32_t lo0 = b == 0 ? 0 : lo[j0];
+    const int32_t e1 = pptr[pe];
+    int32_t c = 0;
+    for (int32_t e = pptr[j0] + lane; e < e1; e += 64) c += pidx[e] >= lo0;
+    for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+    if (lane == 0) {
+      cnt[b] = c;
+      atomicMax(mx, c);
+    }
+  }
+}
+
+// Builds each block's edge list: (source position q, target offset t) sorted
+// by q descending then t ascending, the source's comm c and the exclusive
+// prefix sum E of c along the list.  One workgroup per block, rank sort in
+// LDS.  Blocks above kEC edges are skipped (the step-wise kernel runs then).
+__global__ void __launch_bounds__(256)
+    k_dp_fill(int32_t n, int32_t nb, const int32_t *pptr, const int32_t *pidx, const int32_t *lo,
+              const int64_t *cq, const int32_t *boff, int32_t *eq, int32_t *et, int64_t *ec,
+              int64_t *eE, const Status *st) {
+  __shared__ int32_t s_ptr[65];
+  __shared__ int32_t s_q[kEC];
+  __shared__ int32_t s_t[kEC];
+  __shared__ int64_t s_c[kEC];
+  __shared__ int32_t s_n;
+  if (failed(st)) return;
+  const int lane = threadIdx.x & 63;
+  for (int32_t b = blockIdx.x; b < nb; b += gridDim.x) {
+    const int32_t o = boff[b], c = boff[b + 1] - o;
+    if (c > kEC) continue;
+    const int32_t j0 = b * 64, pe = j0 + 64 < n ? j0 + 64 : n, rows = pe - j0;
+    const int32_t lo0 = b == 0 ? 0 : lo[j0];
+    for (int t = threadIdx.x; t <= rows; t += blockDim.x) s_ptr[t] = pptr[j0 + t];
+    if (threadIdx.x == 0) s_n = 0;
+    __syncthreads();
+    for (int32_t e = s_ptr[0] + threadIdx.x; e < s_ptr[rows]; e += blockDim.x) {
+      const int32_t q = pidx[e];
+      if (q >= lo0) {
+        int r = 0, h = rows - 1;  // target row: last r with s_ptr[r] <= e
+        while (r < h) {
+          const int mid = (r + h + 1) >> 1;
+          if (s_ptr[mid] <= e) r = mid;
+          else h = mid - 1;
+        }
+        const int32_t k = atomicAdd(&s_n, 1);
+        if (k < kEC) {
+          s_q[k] = q;
+          s_t[k] = r;
+        }
+      }
+    }
+    __syncthreads();
+    for (int32_t k = threadIdx.x; k < c; k += blockDim.x) {
+      const int32_t q = s_q[k], t = s_t[k];
+      int32_t r = 0;
+      for (int32_t k2 = 0; k2 < c; k2++) {
+        const int32_t q2 = s_q[k2], t2 = s_t[k2];
+        r += (q2 > q) || (q2 == q && (t2 < t || (t2 == t && k2 < k)));
+      }
+      eq[o + r] = q;
+      et[o + r] = t;
+      s_c[r] = cq[q];
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) {
+      int64_t run = 0;
+      for (int32_t base = 0; base < c; base += 64) {
+        const int32_t k = base + lane;
+        const int64_t v = k < c ? s_c[k] : 0;
+        int64_t x = v;
+        for (int d = 1; d < 64; d <<= 1) {
+          const int64_t y = __shfl_up(x, d);
+          if (lane >= d) x += y;
+        }
+        if (k < c) {
+          ec[o + k] = v;
+          eE[o + k] = run + x - v;
+        }
+        run += __shfl(x, 63);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Candidate keys: (V << 13) + (i - base), base = j0 - kBaseOff, so that one
+// signed 64-bit minimum picks the smallest V and, among equal V, the smallest
+// i.  Valid while every |V| stays below 2^48 (the host checks the total comm
+// PO[n] against kPackLim).
+constexpr int kIdxBits = 13;
+constexpr int64_t kIdxMask = (int64_t(1) << kIdxBits) - 1;
+constexpr int32_t kBaseOff = 4160;
+constexpr int64_t kKeyInf = int64_t(1) << 62;
+constexpr int64_t kPackLim = int64_t(1) << 46;
+constexpr int kMaxRuns = 12;  // in-block runs handled by scans (more: one step per target)
+
+// One Hillis-Steele step of a segmented inclusive min-scan (f = 1 starts a
+// segment); lanes without a source combine with the identity.
+template <int CTRL, int ROWMASK>
+__device__ inline void segmin_step(int64_t &x, int32_t &f) {
+  const int64_t ux = dpp64<CTRL, ROWMASK>(x, kKeyInf);
+  const int32_t uf = dpp32<CTRL, ROWMASK>(f, 0);
+  if (!f) {
+    x = ux < x ? ux : x;
+    f = uf;
+  }
+}
+__device__ inline void wave_segmin(int64_t &x, int32_t f) {
+  segmin_step<0x111, 0xF>(x, f);
+  segmin_step<0x112, 0xF>(x, f);
+  segmin_step<0x114, 0xF>(x, f);
+  segmin_step<0x118, 0xF>(x, f);
+  segmin_step<0x142, 0xA>(x, f);
+  segmin_step<0x143, 0xC>(x, f);
+}
+// inclusive prefix sums over the wave
+__device__ inline int32_t wave_incl_sum32(int32_t x) {
+  x += dpp32<0x111, 0xF>(x, 0);
+  x += dpp32<0x112, 0xF>(x, 0);
+  x += dpp32<0x114, 0xF>(x, 0);
+  x += dpp32<0x118, 0xF>(x, 0);
+  x += dpp32<0x142, 0xA>(x, 0);
+  x += dpp32<0x143, 0xC>(x, 0);
+  return x;
+}
+__device__ inline int64_t wave_incl_sum64(int64_t x) {
+  x += dpp64<0x111, 0xF>(x, 0);
+  x += dpp64<0x112, 0xF>(x, 0);
+  x += dpp64<0x114, 0xF>(x, 0);
+  x += dpp64<0x118, 0xF>(x, 0);
+  x += dpp64<0x142, 0xA>(x, 0);
+  x += dpp64<0x143, 0xC>(x, 0);
+  return x;
+}
+
+__device__ inline int64_t wave_prefix_min(int64_t x) {
+  int64_t y;
+  y = dpp64<0x111, 0xF>(x, kKeyInf);
+  x = y < x ? y : x;
+  y = dpp64<0x112, 0xF>(x, kKeyInf);
+  x = y < x ? y : x;
+  y = dpp64<0x114, 0xF>(x, kKeyInf);
+  x = y < x ? y : x;
+  y = dpp64<0x118, 0xF>(x, kKeyInf);
+  x = y < x ? y : x;
+  y = dpp64<0x142, 0xA>(x, kKeyInf);
+  x = y < x ? y : x;
+  y = dpp64<0x143, 0xC>(x, kKeyInf);
+  x = y < x ? y : x;
+  return x;
+}
+
+// Key of candidate position j0 + s carrying value G (the index field replaced).
+__device__ inline int64_t relabel(int64_t key, int32_t s) {
+  return (key & ~kIdxMask) | (int64_t)(s + kBaseOff);
+}
+
+// One chunk of candidates [cb, ct] (at most 64, lane l <-> i = ct - l) for
+// the 64 targets of the block.  The chunk's edges split its candidates into
+// segments (a segment starts at each candidate with edges); inside one the
+// lane's running comm accS is constant, so a segmented min-scan gives every
+// segment's best key.  The loop then walks the edges in order (sources
+// descending): add the edge to the lanes above its target, evaluate its
+// segment.  A segment evaluated before its last edge only overestimates.
+// H moves to the next block.  FULL: every target may use every candidate.
+template <bool FULL>
+__device__ inline void dp_chunk(int32_t ct, int32_t cb, int32_t base, int32_t lo_t, int32_t *hist,
+                                int64_t *H, const int32_t *Q, const int32_t *T, const int64_t *C,
+                                const int64_t *E, int32_t cnt, int32_t &kk, int64_t &best,
+                                int64_t &accS, int lane) {
+  const int32_t nc = ct - cb + 1;
+  const int32_t k0 = kk;
+  int32_t k1 = k0;
+  for (;;) {  // edges of the chunk: [k0, k1); per-candidate counts in LDS
+    const int32_t e = k1 + lane;
+    const bool in = e < cnt && Q[e] >= cb;
+    const uint64_t m = __ballot(in);
+    if (in) atomicAdd(&hist[ct - Q[e]], 1);
+    k1 += __popcll(m);
+    if (m != ~0ull) break;
+  }
+  wave_lds_sync();
+  const int32_t ecnt = hist[lane];
+  hist[lane] = 0;
+  const int32_t i = ct - lane;
+  const int64_t h = lane < nc ? H[rmod(i)] : 0;
+  int64_t sx = lane < nc ? (int64_t)((uint64_t)h << kIdxBits) + (i - base) : kKeyInf;
+  const uint64_t F = __ballot(ecnt > 0) | 1ull;
+  wave_segmin(sx, (int32_t)((F >> lane) & 1));
+  const uint64_t above = lane == 63 ? 0ull : F & ~((2ull << lane) - 1);
+  const int32_t en_l = above ? (int32_t)__builtin_ctzll(above) - 1 : nc - 1;  // segment end
+  int32_t lmax = 63;
+  int64_t Pt = 0;
+  if (!FULL) {
+    lmax = ct - lo_t < nc - 1 ? ct - lo_t : nc - 1;  // last candidate lane valid for the target
+    Pt = __shfl(sx, lmax < 0 ? 0 : lmax);
+  }
+  {  // segment of lane 0 before the chunk's edges
+    const int32_t en0 = rl32(en_l, 0);
+    const int64_t sk = rl64(sx, en0);
+    if (FULL) {
+      const int64_t kv = sk - accS;
+      best = kv < best ? kv : best;
+    } else {
+      const int64_t kv = (lmax >= en0 ? sk : Pt) - accS;
+      if (lmax >= 0 && kv < best) best = kv;
+    }
+  }
+  for (int32_t kb0 = k0; kb0 < k1; kb0 += 64) {
+    const int32_t nE = k1 - kb0 < 64 ? k1 - kb0 : 64;
+    const bool v = lane < nE;
+    const int32_t x = v ? kb0 + lane : k0;
+    const int32_t stx = v ? ct - Q[x] : 0;
+    const int32_t tx = v ? T[x] : 64;
+    const int64_t cx = v ? (int64_t)((uint64_t)C[x] << kIdxBits) : 0;
+    const int32_t enx = __shfl(en_l, stx);
+    const int64_t skx = __shfl(sx, enx);
+#pragma unroll 4
+    for (int32_t y = 0; y < nE; y++) {
+      const int32_t tk = rl32(tx, y);
+      const int64_t ck = rl64(cx, y);
+      const int64_t sk = rl64(skx, y);
+      accS += lane > tk ? ck : 0;
+      if (FULL) {
+        const int64_t kv = sk - accS;
+        best = kv < best ? kv : best;
+      } else {
+        const int32_t st = rl32(stx, y), en = rl32(enx, y);
+        const int64_t kv = (lmax >= en ? sk : Pt) - accS;
+        if (lmax >= st && kv < best) best = kv;
+      }
+    }
+  }
+  kk = k1;
+  // H(i) for the next block: minus the comm of the block's edges with source >= i
+  const int32_t kl = k0 + wave_incl_sum32(ecnt);
+  if (lane < nc) H[rmod(i)] = h - E[kl];
+}
+
+// In-block steps, one target at a time: lane t takes candidate j0 + s at step
+// s (s < t, and j0 + s >= lo when GEN); RS holds the lane's Int(j0 + s, j0 +
+// t) shifted, reduced past each in-block source.
+template <bool GEN>
+__device__ inline void dp_inblock(int64_t &best, int64_t RS, int32_t smin, int32_t j0, int32_t ein,
+                                  const int32_t *Q, const int32_t *T, const int64_t *C, int lane) {
+  int32_t kbase = ein - 64 > 0 ? ein - 64 : 0;
+  int32_t qb = kbase + lane < ein ? Q[kbase + lane] : -1;
+  int32_t tb = kbase + lane < ein ? T[kbase + lane] : 0;
+  int64_t cb = kbase + lane < ein ? C[kbase + lane] : 0;
+  int32_t ke = ein - 1;
+  int32_t nsrc = ke >= 0 ? rl32(qb, ke - kbase) - j0 : 64;
+  int32_t lv = lane;
+  asm volatile("" : "+v"(lv));  // keeps the per-step lane tests inside the loop
+  const uint32_t len = (uint32_t)(lv - smin);
+#pragma unroll
+  for (int s = 0; s < 64; s++) {
+    const int64_t Gs = relabel(rl64(best, s), s);
+    const int64_t kv = Gs - RS;
+    const bool valid = GEN ? ((uint32_t)(s - smin) < len) : (lv > s);
+    if (valid && kv < best) best = kv;
+    while (nsrc == s) {
+      const int32_t tk = rl32(tb, ke - kbase);
+      const int64_t ck = rl64(cb, ke - kbase) << kIdxBits;
+      if (lane > tk) RS -= ck;
+      ke--;
+      if (ke >= 0 && ke < kbase) {
+        kbase = ke - 63 > 0 ? ke - 63 : 0;
+        qb = Q[kbase + lane < ein ? kbase + lane : 0];
+        tb = T[kbase + lane < ein ? kbase + lane : 0];
+        cb = C[kbase + lane < ein ? kbase + lane : 0];
+      }
+      nsrc = ke >= 0 ? rl32(qb, ke - kbase) - j0 : 64;
+    }
+  }
+}
+
+// In-block steps by runs: the targets between two consecutive in-block edge
+// targets form a run.  Inside a run no in-block edge lies within [s, t) for
+// candidates s of the run, so the run's targets take, besides their own best
+// key U_t, either the best earlier candidate K (one reduction) or the best
+// candidate s in [start, t) of the run, whose value is the prefix minimum of
+// U: one exclusive prefix-min scan.  Y holds the finished candidates' keys as
+// seen by the current run.  Requires ein <= 64 and no memory bound in-block.
+__device__ inline void dp_inblock_runs(int64_t &best, uint64_t runs, int32_t j0, int32_t ein,
+                                       const int32_t *Q, const int32_t *T, const int64_t *C,
+                                       int lane) {
+  const bool v = lane < ein;
+  const int32_t se = v ? Q[lane] - j0 : 0;
+  const int32_t te = v ? T[lane] : -2;
+  const int64_t ce = v ? (int64_t)((uint64_t)C[lane] << kIdxBits) : 0;
+  int64_t Y = kKeyInf;
+  while (runs) {
+    const int32_t ta = (int32_t)__builtin_ctzll(runs);
+    runs &= runs - 1;
+    const int32_t tb = runs ? (int32_t)__builtin_ctzll(runs) : 64;
+    int64_t K = kKeyInf;
+    if (ta > 0) {
+      for (uint64_t m = __ballot(te == ta - 1); m; m &= m - 1) {  // edges now inside [s, t)
+        const int32_t x = (int32_t)__builtin_ctzll(m);
+        const int32_t sx = rl32(se, x);
+        const int64_t cx = rl64(ce, x);
+        if (lane <= sx) Y -= cx;
+      }
+      K = rl64(wave_prefix_min(Y), 63);
+    }
+    const bool in = lane >= ta && lane < tb;
+    const int64_t U = K < best ? K : best;
+    const int64_t W = in ? relabel(U, lane) : kKeyInf;
+    const int64_t inc = wave_prefix_min(W);
+    const int64_t X0 = __shfl(inc, lane > 0 ? lane - 1 : 0);
+    const int64_t X = lane > 0 ? X0 : kKeyInf;
+    const int64_t G = X < U ? X : U;
+    if (in) {
+      best = G;
+      Y = relabel(G, lane);
+    }
+  }
+}
+
+// The blocked DP.  blockDim = 64 * NW: wave 0 runs the in-block steps, waves
+// 1..NW-1 the candidates below the block.
+__global__ void __launch_bounds__(512)
+    k_cluster_dp(int32_t n, int32_t nb, const int32_t *lo, const int32_t *boff, const int32_t *eq,
+                 const int32_t *et, const int64_t *ec, const int64_t *eE, const int64_t *PO,
+                 int32_t *P, Status *st) {
+  __shared__ int64_t s_h[kRing];
+  __shared__ int32_t s_eq[2][kEC];
+  __shared__ int32_t s_et[2][kEC];
+  __shared__ int64_t s_ec[2][kEC];
+  __shared__ int64_t s_eE[2][kEC + 1];
+  __shared__ int32_t s_lo[2][64];
+  __shared__ int64_t s_wb[kMaxW][64];  // per wave: min key relative to the wave's offset
+  __shared__ int64_t s_wa[kMaxW][64];  // per wave: comm (shifted) of its edges counted by the lane
+  __shared__ int32_t s_hist[kMaxW + 1][64];
+  __shared__ int64_t s_hc[64];
+  if (failed(st)) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int W = (int)(blockDim.x >> 6) - 1, NT = W * 64;
+
+  // block 0 staged by everyone; histograms cleared
+  int32_t o0 = 0, o1 = boff[1 < nb ? 1 : nb], o2 = boff[2 < nb ? 2 : nb];
+  {
+    const int32_t c0 = o1;
+    for (int32_t k = tid; k < c0; k += blockDim.x) {
+      s_eq[0][k] = eq[k];
+      s_et[0][k] = et[k];
+      s_ec[0][k] = ec[k];
+      s_eE[0][k] = eE[k];
+      if (k == c0 - 1) s_eE[0][c0] = eE[k] + ec[k];
+    }
+    if (tid == 0 && c0 == 0) s_eE[0][0] = 0;
+    if (tid < 64) s_lo[0][tid] = tid == 0 ? 0 : lo[tid <= n ? tid : n];
+    for (int k = tid; k < (kMaxW + 1) * 64; k += blockDim.x) (&s_hist[0][0])[k] = 0;
+    if (tid < 64) s_hc[tid] = 0;
+  }
+
+#ifdef CEL_PHASE_TIMERS
+  unsigned long long tp_prev = wall_clock64();
+#endif
+  for (int32_t b = 0; b < nb; b++) {
+    __syncthreads();  // staging of block b and H of block b - 1 visible
+    CEL_TSTAMP(tp_a);
+#ifdef CEL_PHASE_TIMERS
+    if (tid == 0) {
+      atomicAdd(&g_cel_phase[3], tp_a - tp_prev);
+      atomicAdd(&g_cel_phase[6], 1ull);
+    }
+#endif
+    const int buf = b & 1;
+    const int32_t j0 = b * 64, base = j0 - kBaseOff;
+    const int32_t cnt = o1 - o0;
+    const int32_t o3 = boff[b + 3 < nb ? b + 3 : nb];
+    const bool more = b + 1 < nb;
+    const int32_t *Q = s_eq[buf];
+    const int32_t *T = s_et[buf];
+    const int64_t *Cc = s_ec[buf];
+    const int64_t *E = s_eE[buf];
+    const int32_t lo_t = s_lo[buf][lane];
+    const int32_t lo_hi = s_lo[buf][63];  // lo is nondecreasing: the block's largest
+
+    // prefetch of block b + 1 into registers (waves 1..W)
+    int32_t pq[kPF], pt[kPF], plo = 0;
+    int64_t pc[kPF], pE[kPF];
+#pragma unroll
+    for (int r = 0; r < kPF; r++) {
+      pq[r] = pt[r] = 0;
+      pc[r] = pE[r] = 0;
+    }
+    if (wave >= 1 && more) {
+      const int x = tid - 64;
+#pragma unroll
+      for (int r = 0; r < kPF; r++) {
+        const int32_t e = o1 + x + r * NT;
+        if (e < o2) {
+          pq[r] = eq[e];
+          pt[r] = et[e];
+          pc[r] = ec[e];
+          pE[r] = eE[e];
+        }
+      }
+      if (x < 64) {
+        const int32_t jj = j0 + 64 + x;
+        plo = lo[jj <= n ? jj : n];
+      }
+    }
+
+    int32_t ein = 0;
+    int64_t XS = 0, Nt = 0;
+    uint64_t runs = 1;
+    if (wave == 0) {
+      // in-block edges: per-source counts and per-target comm
+      ein = first_le(Q, cnt, j0 - 1, lane);
+      for (int32_t k = lane; k < ein; k += 64) {
+        atomicAdd(&s_hist[kMaxW][Q[k] - j0], 1);
+        atomicAdd((unsigned long long *)&s_hc[T[k]], (unsigned long long)Cc[k]);
+      }
+      wave_lds_sync();
+      const int32_t sc = s_hist[kMaxW][lane];
+      const int64_t hc = s_hc[lane];
+      s_hist[kMaxW][lane] = 0;
+      s_hc[lane] = 0;
+      XS = (int64_t)((uint64_t)(wave_incl_sum64(hc) - hc) << kIdxBits);  // edges with t_e < t
+      const int32_t ks = ein - (wave_incl_sum32(sc) - sc);                 // edges with q >= j0 + t
+      Nt = E[ks];
+      runs = (__ballot(hc > 0) << 1) | 1ull;  // a run starts after each in-block edge target
+    } else {
+      // candidates below the block: chunks [ka, kb) of 64, descending
+      const int w = wave - 1;
+      int64_t best = kKeyInf, accS = 0;
+      if (j0 > 0) {
+        const int32_t lo0 = s_lo[buf][0];
+        const int32_t K = (j0 - lo0 + 63) >> 6;
+        const int32_t ka = w * K / W, kb = (w + 1) * K / W;
+        if (ka < kb) {
+          const int32_t top = j0 - 1 - 64 * ka;
+          const int32_t bot = j0 - 64 * kb > lo0 ? j0 - 64 * kb : lo0;
+          int32_t kk = first_le(Q, cnt, top, lane);
+          for (int32_t ct = top; ct >= bot; ct -= 64) {
+            const int32_t cb = ct - 63 > bot ? ct - 63 : bot;
+            if (lo_hi <= cb)
+              dp_chunk<true>(ct, cb, base, lo_t, s_hist[w], s_h, Q, T, Cc, E, cnt, kk, best, accS,
+                             lane);
+            else
+              dp_chunk<false>(ct, cb, base, lo_t, s_hist[w], s_h, Q, T, Cc, E, cnt, kk, best, accS,
+                              lane);
+          }
+        }
+      }
+      s_wb[w][lane] = best;
+      s_wa[w][lane] = accS;
+    }
+#ifdef CEL_PHASE_TIMERS
+    {
+      const unsigned long long t = wall_clock64();
+      if (lane == 0 && wave < 6) atomicAdd(&g_cel_phase[8 + wave], t - tp_a);
+    }
+#endif
+    __syncthreads();  // wave results visible
+    CEL_TSTAMP(tp_b);
+#ifdef CEL_PHASE_TIMERS
+    if (tid == 0) atomicAdd(&g_cel_phase[1], tp_b - tp_a);
+#endif
+
+    if (wave == 0) {
+      const int32_t j = j0 + lane;
+      int64_t best = j == 0 ? (int64_t)kBaseOff : kKeyInf;  // S(0) = 0
+      int64_t off = XS;
+      for (int w = 0; w < W; w++) {
+        const int64_t kv = s_wb[w][lane] - off;
+        best = kv < best ? kv : best;
+        off += s_wa[w][lane];
+      }
+      const int32_t smin = lo_t - j0 > 0 ? lo_t - j0 : 0;
+      if (lo_hi > j0) dp_inblock<true>(best, XS, smin, j0, ein, Q, T, Cc, lane);
+      else if (ein <= 64 && __popcll(runs) <= kMaxRuns)
+        dp_inblock_runs(best, runs, j0, ein, Q, T, Cc, lane);
+      else dp_inblock<false>(best, XS, smin, j0, ein, Q, T, Cc, lane);
+      const int64_t G = best >> kIdxBits;
+      if (j >= 1 && j <= n) P[j] = (int32_t)(best & kIdxMask) + base;
+      if (j < n) s_h[rmod(j)] = G - Nt;
+      if (j == n) st->s0 = PO[n] + G;
+    } else if (more) {
+      // stage block b + 1
+      const int nbuf = buf ^ 1;
+      const int x = tid - 64;
+      const int32_t c1 = o2 - o1;
+#pragma unroll
+      for (int r = 0; r < kPF; r++) {
+        const int32_t k = x + r * NT;
+        if (k < c1) {
+          s_eq[nbuf][k] = pq[r];
+          s_et[nbuf][k] = pt[r];
+          s_ec[nbuf][k] = pc[r];
+          s_eE[nbuf][k] = pE[r];
+          if (k == c1 - 1) s_eE[nbuf][c1] = pE[r] + pc[r];
+        }
+      }
+      for (int32_t k = x + kPF * NT; k < c1; k += NT) {
+        const int32_t e = o1 + k;
+        s_eq[nbuf][k] = eq[e];
+        s_et[nbuf][k] = et[e];
+        s_ec[nbuf][k] = ec[e];
+        s_eE[nbuf][k] = eE[e];
+        if (k == c1 - 1) s_eE[nbuf][c1] = eE[e] + ec[e];
+      }
+      if (x == 0 && c1 == 0) s_eE[nbuf][0] = 0;
+      if (x < 64) s_lo[nbuf][x] = plo;
+    }
+#ifdef CEL_PHASE_TIMERS
+    {
+      const unsigned long long t = wall_clock64();
+      if (tid == 0) atomicAdd(&g_cel_phase[2], t - tp_b);
+      if (tid == 64) atomicAdd(&g_cel_phase[5], t - tp_b);
+      tp_prev = t;
+    }
+#endif
+    o0 = o1;
+    o1 = o2;
+    o2 = o3;
+  }
+}
+
 // breakpoints: follow P from n down to 0, flagging cluster starts
 __global__ void k_backtrack(int32_t n, const int32_t *P, int32_t *flag, Status *st) {
   if (failed(st)) return;
@@ -241,9 +815,58 @@ template <int SL>
 static void launch_dp(int32_t n, int32_t R, const int32_t *lo, const int32_t *pptr,
                       const int32_t *pidx, const int64_t *cq, const int64_t *PO, int32_t *P,
                       Status *st, hipStream_t s) {
-  KTimer kt(s, "k_cluster_dp");
-  k_cluster_dp<SL><<<1, 64, 0, s>>>(n, R, lo, pptr, pidx, cq, PO, P, st);
+  KTimer kt(s, "k_cluster_dp_step");
+  k_cluster_dp_step<SL><<<1, 64, 0, s>>>(n, R, lo, pptr, pidx, cq, PO, P, st);
 }
+
+// Blocked DP when every block fits the staging sizes (sets *done), else
+// leaves the step-wise kernel to the caller.
+static int dp_blocked(int32_t n, int32_t m, int32_t R, const int32_t *lo, const int32_t *pptr,
+                      const int32_t *pidx, const int64_t *cq, const int64_t *PO, int32_t *P,
+                      Status *st, Scratch &sc, hipStream_t s, bool *done) {
+  *done = false;
+  const int32_t nb = n / 64 + 1;
+  int32_t *bcnt, *boff, *mx;
+  CEL_TRY(sc.get(&bcnt, nb));
+  CEL_TRY(sc.get(&boff, (int64_t)nb + 1));
+  CEL_TRY(sc.get(&mx, 1));
+  CEL_HIP(hipMemsetAsync(mx, 0, sizeof(int32_t), s));
+  {
+    KTimer kt(s, "k_dp_count");
+    k_dp_count<<<grid_for((int64_t)nb * 64, 256, 4096), 256, 0, s>>>(n, nb, pptr, pidx, lo, bcnt,
+                                                                     mx, st);
+  }
+  CEL_TRY(exclusive_scan_i32(bcnt, boff, nb, sc, s));
+  int32_t hm[1] = {0};
+  int64_t total = 0;
+  CEL_HIP(hipMemcpyAsync(hm, mx, sizeof hm, hipMemcpyDeviceToHost, s));
+  CEL_HIP(hipMemcpyAsync(&total, PO + n, sizeof total, hipMemcpyDeviceToHost, s));
+  CEL_HIP(hipStreamSynchronize(s));
+  timing_collect();
+  if (hm[0] > kEC || total >= kPackLim) return CEL_OK;  // step-wise kernel
+  int32_t *eq, *et;
+  int64_t *ec, *eE;
+  CEL_TRY(sc.get(&eq, m));
+  CEL_TRY(sc.get(&et, m));
+  CEL_TRY(sc.get(&ec, m));
+  CEL_TRY(sc.get(&eE, m));
+  {
+    KTimer kt(s, "k_dp_fill");
+    k_dp_fill<<<nb < 65535 ? nb : 65535, 256, 0, s>>>(n, nb, pptr, pidx, lo, cq, boff, eq, et, ec,
+                                                      eE, st);
+  }
+  const int32_t K = (R + 63) / 64;
+  const int NW = 1 + (K < kMaxW ? K : kMaxW);
+  {
+    KTimer kt(s, "k_cluster_dp");
+    k_cluster_dp<<<1, 64 * NW, 0, s>>>(n, nb, lo, boff, eq, et, ec, eE, PO, P, st);
+  }
+  CEL_HIP(hipGetLastError());
+  *done = true;
+  return CEL_OK;
+}
+
+CEL_PHASE_READER(cel_debug_phases_cluster)
 
 }  // namespace cel
 
@@ -307,7 +930,10 @@ extern "C" int cel_cluster(const cel_graph *g, const cel_devices *d, const int32
     CEL_TRY(sc.get(&P, (int64_t)n + 1));
     CEL_TRY(exclusive_scan_i64(outc, PO, n, sc, s));
     CEL_TRY(relabel_csr(n, order, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
-    if (R <= 64) launch_dp<1>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
+    bool blocked = false;
+    CEL_TRY(dp_blocked(n, g->m, R, lo, pptr, pidx, cq, PO, P, st, sc, s, &blocked));
+    if (blocked) {
+    } else if (R <= 64) launch_dp<1>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
     else if (R <= 128) launch_dp<2>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
     else if (R <= 256) launch_dp<4>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
     else if (R <= 512) launch_dp<8>(n, R, lo, pptr, pidx, cq, PO, P, st, s);

@@ -280,6 +280,80 @@ def test_cluster_window_sizes_and_orders():
                 (s, R, M, mode)
 
 
+def _cluster_with_kernels(wl, order, R, M):
+    """GPU clustering plus the names of the DP kernels it launched."""
+    cel.timing(True)
+    cel.kernel_stats(reset=True)
+    try:
+        got = gpu_cluster(wl, order, R, M, 0)
+        ks = cel.kernel_stats(reset=True)
+    finally:
+        cel.timing(False)
+    return got, {k for k in ks if k.startswith("k_cluster_dp")}
+
+
+# (seed, n, p_edge, max fan-in, R, M, DP kernel): dense local structure on both
+# sides of the blocked kernel's staging size (1024 window edges per block of 64
+# targets): many edges per candidate and inside one block, several edge
+# batches, the prefetch remainder (R <= 64: one candidate wave), and blocks too
+# dense for staging (step-wise kernel).
+DENSE_CASES = [
+    (4, 600, 0.12, 20, 130, -1, "k_cluster_dp"),
+    (6, 2000, 0.02, 30, 1000, -1, "k_cluster_dp"),
+    (7, 800, 0.1, 12, 60, -1, "k_cluster_dp"),
+    (6, 2000, 0.02, 30, 1000, 10 ** 15, "k_cluster_dp_step"),
+    (1, 400, 0.5, 400, 200, -1, "k_cluster_dp_step"),
+    (8, 800, 0.2, 16, 40, -1, "k_cluster_dp"),
+    (10, 1000, 0.3, 10, 30, -1, "k_cluster_dp"),
+]
+
+
+@pytest.mark.parametrize("case", DENSE_CASES, ids=[f"s{c[0]}-R{c[4]}-{c[6]}" for c in DENSE_CASES])
+def test_cluster_dense_blocks(case):
+    seed, n, p, fan, R, M, kern = case
+    wl = make_random_dag(seed, n, p, D=3, max_fanin=fan)
+    lev, oid, _, _ = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    for k, order in enumerate((pr, random_topo_order(wl, np.random.default_rng(seed)))):
+        ref = O.cluster(wl, order, R, M)
+        got, used = _cluster_with_kernels(wl, order, R, M)
+        assert got[1] == ref[1] and got[2] == ref[2] and np.array_equal(got[0], ref[0]), k
+        if k == 0:  # the priority order is the one the case was sized on
+            assert used == {kern}
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_cluster_memory_bound_windows(seed):
+    """Memory caps that end windows inside a block of 64 targets: targets of one
+    block see different first candidates (some none below the block)."""
+    n = 400 + 230 * seed
+    wl = make_random_dag(4000 + seed, n, min(0.5, 5.0 / n), D=3, multi=seed % 2 == 1)
+    lev, oid, _, _ = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    avg = int(wl.mem.sum()) // n
+    for width in (20, 45, 70, 120):
+        for R in (64, 200):
+            M = avg * width
+            ref = O.cluster(wl, pr, R, M)
+            got, used = _cluster_with_kernels(wl, pr, R, M)
+            assert got[1] == ref[1] and got[2] == ref[2] and np.array_equal(got[0], ref[0]), \
+                (width, R)
+            assert used == {"k_cluster_dp"}
+
+
+def test_cluster_huge_comm_takes_step_kernel():
+    """Total comm at or above 2^46 ns: the step-wise kernel, same results."""
+    for seed, n in ((11, 300), (12, 90)):
+        wl = make_random_dag(seed, n, min(0.5, 6.0 / n), D=3, ob_max=1 << 45, bw=1, lat=5)
+        lev, oid, _, _ = O.topo_levels(wl)
+        _, _, pr, _ = O.blevel(wl, lev, oid)
+        for R in (200, 17):
+            ref = O.cluster(wl, pr, R, -1)
+            got, used = _cluster_with_kernels(wl, pr, R, -1)
+            assert got[1] == ref[1] and got[2] == ref[2] and np.array_equal(got[0], ref[0])
+            assert used == {"k_cluster_dp_step"}
+
+
 def random_topo_order(wl, rng):
     import heapq
     indeg = np.diff(wl.in_ptr).copy()
