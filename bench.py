@@ -1,19 +1,23 @@
 """Benchmark of the placement hot path on one MI355X.
 
 A step is one pass of the whole path over the 1.07M-node transformer training
-graph (96 blocks, hidden 8192, micro-op granularity): Kahn levels -> b-level,
-t-level and priority order -> DP clustering (R = 200) -> Adjusting Placement
--> makespan of the resulting placement -> makespan of a batch of 64 perturbed
+graph (96 blocks, hidden 8192, micro-op granularity): Kahn levels -> b-level
+and priority order -> DP clustering (R = 200) -> Adjusting Placement ->
+makespan of the resulting placement -> makespan of a batch of 64 perturbed
 placements (5% of the clusters moved to a random device).  Inputs are
 device-resident before timing starts.
 
 Headline: DAG edges/s of the b-level + makespan evaluation (m divided by the
 time of the b-level call plus the single-placement makespan call).  Also
 reported: placement-generation ms (levels + b-level + clustering +
-placement), per-stage and per-kernel times, the roofline of the dominant
-kernel and the CPU oracle (one core) on the same graph.
+placement), per-stage and per-kernel times with algorithmic-byte rooflines,
+the per-level latency of the level sweeps (a single placement of a graph
+10^4 levels deep is bound by it, not by HBM), the t-level pass (an optional
+output, timed apart), batched scoring of 1,024 perturbed placements of the
+200k-node layered DAG in one call (the bandwidth-bound regime), and the CPU
+oracle (one core) on the same 1.07M-node graph.
 
-Usage: python bench.py [--gpus 1] [--steps 5] [--warmup 2] [--no-cpu]
+Usage: python bench.py [--gpus 1] [--steps 5] [--warmup 2] [--no-cpu] [--no-batch]
 """
 from __future__ import annotations
 
@@ -33,6 +37,7 @@ METRIC = "DAG edges/sec for b-level+makespan eval (1M-node graph); placement-gen
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
 VALU_I32_PEAK = 256 * 4 * 16 * 2.4e9  # lane-ops/s: 256 CUs x 4 SIMD16 x 2.4 GHz
 BATCH = 64
+BATCH5 = 1024  # candidates of the 200k-node batched-scoring row
 
 
 def algorithmic_bytes(kernel: str, n: int, m: int, K: int) -> float | None:
@@ -48,6 +53,50 @@ def algorithmic_bytes(kernel: str, n: int, m: int, K: int) -> float | None:
     return None
 
 
+def batched_row(cel, torch, dev, args):
+    """1,024 perturbed placements of the 200k-node layered DAG scored in one call."""
+    from workloads import make_config, perturb_placements
+    wl = make_config(5, args.seed)
+    g = cel.Graph.from_arrays(wl, dev)
+    d = cel.Devices.from_arrays(wl)
+    lev, oid, lp, L = cel.topo_levels(g)
+    _, _, pr, _ = cel.blevel(g, d, lev, lp, oid, L)
+    cid, C, _ = cel.cluster(g, d, pr, 200, -1)
+    cdev, ndev, _, _ = cel.place(g, d, cid, C)
+    cand = perturb_placements(cdev.cpu().numpy(), wl.D, BATCH5, args.seed)
+    nd = torch.gather(torch.from_numpy(cand).to(dev), 1,
+                      cid.long().unsqueeze(0).expand(BATCH5, -1)).contiguous()
+    del cand
+    stream = torch.cuda.current_stream()
+    cel.makespan(g, d, pr, lev, lp, L, nd)  # warm-up
+    torch.cuda.synchronize()
+    cel.kernel_stats(reset=True)
+    cel.timing(True)
+    times = []
+    for _ in range(max(1, args.steps)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        ms, _, _ = cel.makespan(g, d, pr, lev, lp, L, nd)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    cel.timing(False)
+    ks = cel.kernel_stats(reset=True)
+    c_, t_ = ks["k_makespan_batch"]
+    kms = t_ / c_
+    B = algorithmic_bytes("k_makespan_batch", wl.n, wl.m, BATCH5)
+    call_ms = float(np.mean(times))
+    print(f"[bench] 200k-node scoring of {BATCH5} placements: {call_ms:.2f} ms per call",
+          file=sys.stderr, flush=True)
+    return {"workload": f"layered-200k: 400 x 500 layered DAG, {BATCH5} placements (5% of the "
+                        f"clusters of the Adjusting Placement moved at random)",
+            "n": wl.n, "m": wl.m, "levels": L, "K": BATCH5, "call_ms": call_ms,
+            "edges_per_s": BATCH5 * wl.m / (call_ms * 1e-3), "kernel_ms": kms,
+            "algorithmic_bytes": B, "achieved_GBs": round(B / (kms * 1e-3) / 1e9, 2),
+            "frac": round(B / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS, 5),
+            "makespan_min_ns": int(ms.min().item()), "makespan_max_ns": int(ms.max().item())}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -55,6 +104,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-batch", action="store_true",
+                    help="skip the 1,024-candidate scoring row on the 200k-node DAG")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this benchmark runs on one GPU only (got --gpus {args.gpus}); the "
@@ -84,7 +135,7 @@ def main() -> int:
         ev[0].record(stream)
         lev, oid, lp, L = cel.topo_levels(g)
         ev[1].record(stream)
-        bl, tl, pr, cp = cel.blevel(g, d, lev, lp, oid, L, want_tlevel=True)
+        bl, _, pr, cp = cel.blevel(g, d, lev, lp, oid, L)
         ev[2].record(stream)
         cid, C, cut = cel.cluster(g, d, pr, 200, -1)
         ev[3].record(stream)
@@ -126,6 +177,23 @@ def main() -> int:
     cel.timing(False)
     kstats = cel.kernel_stats(reset=True)
 
+    # t-level (optional output of the b-level call): the extra time it costs
+    lev, oid, lp, L = cel.topo_levels(g)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    cel.kernel_stats(reset=True)
+    cel.timing(True)
+    e0.record(stream)
+    cel.blevel(g, d, lev, lp, oid, L, want_tlevel=True)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    cel.timing(False)
+    ks_t = cel.kernel_stats(reset=True)
+    tlevel_row = {"blevel_with_tlevel_ms": e0.elapsed_time(e1),
+                  "k_tlevel_sweep_ms": ks_t.get("k_tlevel_sweep", (1, float("nan")))[1]}
+
+    batch5 = None if args.no_batch else batched_row(cel, torch, dev, args)
+
     stages = {k: float(np.mean(v)) for k, v in rec.items()}
     eval_ms = stages["blevel"] + stages["makespan"]
     value = m / (eval_ms * 1e-3)
@@ -144,6 +212,15 @@ def main() -> int:
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
                 "traffic": None, "algorithmic_bytes": B,
                 "ns_per_level": round(t_dom * 1e9 / L, 1)}
+    # the level sweeps are chains of L dependent levels: per-level latency
+    per_level = {k: round(kernels[k]["avg_ms"] * 1e6 / L, 1)
+                 for k in ("k_kahn", "k_blevel_sweep", "k_makespan_sweep", "k_makespan_batch")
+                 if k in kernels}
+    for k, v in kernels.items():
+        b_ = algorithmic_bytes(k, n, m, BATCH if k == "k_makespan_batch" else 1)
+        if b_ is not None:
+            v["achieved_GBs"] = round(b_ / (v["avg_ms"] * 1e-3) / 1e9, 3)
+            v["hbm_frac"] = round(b_ / (v["avg_ms"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 6)
     Bk = algorithmic_bytes("k_makespan_batch", n, m, BATCH)
     tk = kernels["k_makespan_batch"]["avg_ms"] * 1e-3
     batched = {"K": BATCH, "edges_per_s": BATCH * m / (stages["makespan_batch"] * 1e-3),
@@ -157,13 +234,13 @@ def main() -> int:
         reps, t_cpu = 0, 0.0
         while t_cpu < 10.0 and reps < 5:
             a = time.perf_counter()
-            _, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=True)
+            _, _, pr, _ = O.blevel(wl, lev, oid)
             O.makespan(wl, pr, np.zeros(n, np.uint8), want_times=False)
             t_cpu += time.perf_counter() - a
             reps += 1
         cpu = {"value": m / (t_cpu / reps), "unit": "edges/s", "cores": 1, "kind": "oracle",
-               "sample": f"b-level (with t-level and priority order) + single-placement "
-                         f"makespan on the full {n}-node graph, {reps} reps, single-threaded C"}
+               "sample": f"b-level (with priority order) + single-placement makespan on the "
+                         f"full {n}-node graph, {reps} reps, single-threaded C"}
         print(f"[bench] cpu oracle {t_cpu / reps * 1e3:.0f} ms per pass", file=sys.stderr,
               flush=True)
 
@@ -180,7 +257,10 @@ def main() -> int:
         "stages_ms": stages,
         "kernels": kernels,
         "roofline": roofline,
+        "ns_per_level": per_level,
+        "tlevel": tlevel_row,
         "batched_makespan": batched,
+        "batched_scoring_200k": batch5,
         "cpu_baseline": cpu,
         "results": {"critical_path_ns": state["cp"], "clusters": state["C"],
                     "cut_cost_ns": state["cut"], "coarse_makespan_ns": state["cms"],
