@@ -91,24 +91,69 @@ __device__ inline void wave_seg_scan_dpp(int64_t &a, int64_t &b, int32_t &f) {
   seg_step<0x143, 0xC>(a, b, f);  // row_bcast:31 into rows 2 and 3
 }
 
-// Calls f(u, e) for every CSR edge e whose source u lies in the 256 sources
-// [blockIdx.x * 256, + 256).  The block's edges form one contiguous range and
-// are spread over all threads (source found by binary search), so a node of
-// huge out-degree does not serialise on one thread.  `ptr` is a 257-entry
-// shared array; row pointers must already be validated.
+// Edge-balanced CSR traversal: block b takes edges [b * kEdgesPB, +kEdgesPB)
+// whatever their sources, so a node of huge out-degree is spread over many
+// blocks.  Wave 0 finds the rows of the slice's first and last edge by a
+// 64-way search over out_ptr; the slice's row pointers are staged in LDS
+// (kRowsPB at most, else the per-edge search reads out_ptr).  Row pointers must
+// already be validated (non-decreasing, out_ptr[0] = 0, out_ptr[n] = m).
+constexpr int kEdgesPB = 2048;
+constexpr int kRowsPB = 1024;
+
+inline unsigned edge_blocks(int32_t m) {
+  return m > 0 ? (unsigned)((m + kEdgesPB - 1) / kEdgesPB) : 1u;
+}
+
+// last u in [0, n) with out_ptr[u] <= x, for 0 <= x < m; wave-uniform result
+__device__ inline int32_t wave_row_of(const int32_t *out_ptr, int32_t n, int32_t x, int lane) {
+  int32_t lo = 0, hi = n - 1;  // out_ptr[lo] <= x; the answer lies in [lo, hi]
+  while (lo < hi) {
+    const int64_t span = (int64_t)hi - lo;
+    const int32_t probe = lo + (int32_t)((span * (lane + 1) + 63) / 64);  // lane 63 probes hi
+    const uint64_t le = __ballot(out_ptr[probe] <= x);  // a prefix of the lanes
+    if (le == 0) {
+      hi = __builtin_amdgcn_readlane(probe, 0) - 1;
+    } else {
+      const int k = 63 - __builtin_clzll(le);
+      const int32_t pk = __builtin_amdgcn_readlane(probe, k);
+      if (k < 63) hi = __builtin_amdgcn_readlane(probe, k + 1) - 1;
+      lo = pk;
+    }
+  }
+  return lo;
+}
+
+// Calls f(u, e) for every edge e of the block's slice, u its source.  s_ptr
+// holds kRowsPB + 1 ints, s_u two.
 template <class F>
-__device__ inline void for_block_edges(const int32_t *out_ptr, int32_t n, int32_t *ptr, F f) {
-  const int64_t u0 = (int64_t)blockIdx.x * 256;
-  for (int i = threadIdx.x; i <= 256; i += blockDim.x) ptr[i] = out_ptr[u0 + i < n ? u0 + i : n];
+__device__ inline void for_edges_balanced(const int32_t *out_ptr, int32_t n, int32_t m,
+                                          int32_t *s_ptr, int32_t *s_u, F f) {
+  const int64_t e0 = (int64_t)blockIdx.x * kEdgesPB;
+  if (e0 >= m) return;  // uniform over the block
+  const int32_t e1 = e0 + kEdgesPB < m ? (int32_t)(e0 + kEdgesPB) : m;
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    const int32_t u0 = wave_row_of(out_ptr, n, (int32_t)e0, lane);
+    const int32_t u1 = wave_row_of(out_ptr, n, e1 - 1, lane);
+    if (lane == 0) {
+      s_u[0] = u0;
+      s_u[1] = u1;
+    }
+  }
   __syncthreads();
-  for (int32_t e = ptr[0] + threadIdx.x; e < ptr[256]; e += blockDim.x) {
-    int lo = 0, hi = 255;
+  const int32_t u0 = s_u[0], nr = s_u[1] - u0 + 1;
+  const bool staged = nr <= kRowsPB;
+  if (staged)
+    for (int t = threadIdx.x; t <= nr; t += blockDim.x) s_ptr[t] = out_ptr[u0 + t];
+  __syncthreads();
+  for (int32_t e = (int32_t)e0 + threadIdx.x; e < e1; e += blockDim.x) {
+    int32_t lo = 0, hi = nr - 1;  // last row r with ptr[u0 + r] <= e
     while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (ptr[mid] <= e) lo = mid;
+      const int32_t mid = (lo + hi + 1) >> 1;
+      if ((staged ? s_ptr[mid] : out_ptr[u0 + mid]) <= e) lo = mid;
       else hi = mid - 1;
     }
-    f((int32_t)(u0 + lo), e);
+    f(u0 + lo, e);
   }
 }
 

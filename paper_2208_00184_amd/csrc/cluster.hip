@@ -450,7 +450,6 @@ __device__ inline void dp_chunk(int32_t ct, int32_t cb, int32_t base, int32_t lo
     const int64_t cx = v ? (int64_t)((uint64_t)C[x] << kIdxBits) : 0;
     const int32_t enx = __shfl(en_l, stx);
     const int64_t skx = __shfl(sx, enx);
-#pragma unroll 4
     for (int32_t y = 0; y < nE; y++) {
       const int32_t tk = rl32(tx, y);
       const int64_t ck = rl64(cx, y);
@@ -793,13 +792,13 @@ __global__ void k_label(int32_t n, const int32_t *order, const int32_t *incl, in
     cid[order[p]] = incl[p + 1] - 1;
 }
 
-// sum of c[u] over edges u -> v in different clusters (block per 256 sources)
+// sum of c[u] over edges u -> v in different clusters (edge-balanced blocks)
 __global__ void k_cut_cost(cel_graph g, int64_t bw, int64_t lat, const int32_t *cid, Status *st) {
-  __shared__ int32_t ptr[257];
+  __shared__ int32_t ptr[kRowsPB + 1], su[2];
   __shared__ int64_t red[4];
   if (failed(st)) return;
   int64_t acc = 0;
-  for_block_edges(g.out_ptr, g.n, ptr, [&](int32_t u, int32_t e) {
+  for_edges_balanced(g.out_ptr, g.n, g.m, ptr, su, [&](int32_t u, int32_t e) {
     if (cid[u] != cid[g.out_idx[e]]) acc += comm_of(g.ob[u], bw, lat);
   });
   for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
@@ -947,7 +946,7 @@ extern "C" int cel_cluster(const cel_graph *g, const cel_devices *d, const int32
   CEL_TRY(exclusive_scan_i32(flag, incl, n, sc, s));
   k_label<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, incl, cluster_id, st);
   if (mode == CEL_CLUSTER_GREEDY)
-    k_cut_cost<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(*g, d->bw, d->lat, cluster_id, st);
+    k_cut_cost<<<edge_blocks(g->m), 256, 0, s>>>(*g, d->bw, d->lat, cluster_id, st);
   CEL_HIP(hipGetLastError());
   Status h;
   CEL_TRY(read_status(st, &h, s));

@@ -147,15 +147,14 @@ __device__ inline uint64_t mix64(uint64_t x) {  // SplitMix64 finaliser
   return x ^ (x >> 31);
 }
 
-// CSR pass: one block per 256 consecutive sources; the block's edges form one
-// contiguous range and are spread over all threads (owner by binary search).
-// Counts in-degrees and a per-target sum of hashed source ids.
+// CSR pass over edge-balanced blocks: counts in-degrees and a per-target sum
+// of hashed source ids.
 __global__ void k_check_csr(cel_graph g, Status *st, int32_t *indeg, uint64_t *hsum) {
-  __shared__ int32_t ptr[257];
+  __shared__ int32_t ptr[kRowsPB + 1], su[2];
   if (failed(st)) return;  // row pointers not validated
   const int32_t n = g.n;
   uint32_t bad = 0;
-  for_block_edges(g.out_ptr, n, ptr, [&](int32_t u, int32_t e) {
+  for_edges_balanced(g.out_ptr, n, g.m, ptr, su, [&](int32_t u, int32_t e) {
     const int32_t t = g.out_idx[e];
     if (t < 0 || t >= n) {
       bad |= EB_ARG;
@@ -222,7 +221,7 @@ int check_graph(const cel_graph *g, int64_t bw, int64_t lat, bool bound, Status 
     CEL_HIP(hipMallocAsync((void **)&hsum, sizeof(uint64_t) * (size_t)g->n, s));
     CEL_HIP(hipMemsetAsync(indeg, 0, sizeof(int32_t) * (size_t)g->n, s));
     CEL_HIP(hipMemsetAsync(hsum, 0, sizeof(uint64_t) * (size_t)g->n, s));
-    k_check_csr<<<(unsigned)((g->n + 255) / 256), B, 0, s>>>(*g, st, indeg, hsum);
+    k_check_csr<<<edge_blocks(g->m), B, 0, s>>>(*g, st, indeg, hsum);
     k_check_csc<<<grid_for(g->n, B, 4096), B, 0, s>>>(*g, st, indeg, hsum);
     CEL_HIP(hipFreeAsync(hsum, s));
   }
@@ -282,10 +281,10 @@ __global__ void k_check_levels_nodes(int32_t n, const int32_t *order, const int3
 
 // level[u] < level[v] on every edge (needs level values in range: checked above)
 __global__ void k_check_levels_edges(cel_graph g, const int32_t *level, int32_t L, Status *st) {
-  __shared__ int32_t ptr[257];
+  __shared__ int32_t ptr[kRowsPB + 1], su[2];
   if (failed(st)) return;  // edge indices or level values not validated
   uint32_t bad = 0;
-  for_block_edges(g.out_ptr, g.n, ptr, [&](int32_t u, int32_t e) {
+  for_edges_balanced(g.out_ptr, g.n, g.m, ptr, su, [&](int32_t u, int32_t e) {
     if (level[g.out_idx[e]] <= level[u]) bad |= EB_ORDER;
   });
   if (bad) raise_err(st, bad);
@@ -293,10 +292,10 @@ __global__ void k_check_levels_edges(cel_graph g, const int32_t *level, int32_t 
 
 // pos[u] < pos[v] on every edge (pos must be a complete permutation: checked)
 __global__ void k_check_topo_edges(cel_graph g, const int32_t *pos, Status *st) {
-  __shared__ int32_t ptr[257];
+  __shared__ int32_t ptr[kRowsPB + 1], su[2];
   if (failed(st)) return;
   uint32_t bad = 0;
-  for_block_edges(g.out_ptr, g.n, ptr, [&](int32_t u, int32_t e) {
+  for_edges_balanced(g.out_ptr, g.n, g.m, ptr, su, [&](int32_t u, int32_t e) {
     if (pos[g.out_idx[e]] <= pos[u]) bad |= EB_ORDER;
   });
   if (bad) raise_err(st, bad);
@@ -313,7 +312,7 @@ int check_level_order(const cel_graph *g, const int32_t *order, const int32_t *l
   }
   k_check_levels_nodes<<<grid_for((int64_t)n + 1, B, 4096), B, 0, s>>>(n, order, level, level_ptr,
                                                                        L, st);
-  if (n > 0) k_check_levels_edges<<<(unsigned)((n + 255) / 256), B, 0, s>>>(*g, level, L, st);
+  if (n > 0) k_check_levels_edges<<<edge_blocks(g->m), B, 0, s>>>(*g, level, L, st);
   CEL_HIP(hipGetLastError());
   return CEL_OK;
 }
@@ -325,7 +324,7 @@ int check_topo_order(const cel_graph *g, const int32_t *order, int32_t *pos, Sta
   if (n > 0) {
     k_fill_i32<<<grid_for(n, B, 4096), B, 0, s>>>(pos, n, -1);
     k_inverse_perm<<<grid_for(n, B, 4096), B, 0, s>>>(n, order, pos, st);
-    k_check_topo_edges<<<(unsigned)((n + 255) / 256), B, 0, s>>>(*g, pos, st);
+    k_check_topo_edges<<<edge_blocks(g->m), B, 0, s>>>(*g, pos, st);
   }
   CEL_HIP(hipGetLastError());
   return CEL_OK;

@@ -21,18 +21,19 @@
 
 namespace cel {
 
-// device per position, with range check (devp[k][p] = node_dev[k][order[p]])
+// device per position, with range check (devp[k][p] = node_dev[k][order[p]]);
+// x runs over positions, y over placements
 __global__ void k_dev_gather(int32_t K, int32_t n, const int32_t *order, const uint8_t *node_dev,
                              int32_t D, uint8_t *devp, Status *st) {
   if (failed(st)) return;
   uint32_t bad = 0;
-  const int64_t tot = (int64_t)K * n;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < tot;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t k = i / n, p = i - k * n;
-    const uint8_t dv = node_dev[k * n + order[p]];
-    if (dv >= D) bad |= EB_ARG;
-    devp[i] = dv;
+  for (int32_t p = blockIdx.x * blockDim.x + threadIdx.x; p < n; p += gridDim.x * blockDim.x) {
+    const int32_t v = order[p];
+    for (int32_t k = blockIdx.y; k < K; k += gridDim.y) {
+      const uint8_t dv = node_dev[(int64_t)k * n + v];
+      if (dv >= D) bad |= EB_ARG;
+      devp[(int64_t)k * n + p] = dv;
+    }
   }
   if (bad) raise_err(st, bad);
 }
@@ -62,6 +63,7 @@ __global__ void k_pos_costs(int32_t n, const int32_t *order, const int64_t *w, c
 // the whole block.  A node with more than EC predecessors forms a window of
 // its own.
 constexpr int kMsL = 256;
+constexpr int kBatchWide = 384;  // batches up to this size get one CU-sized window per placement
 
 template <int B, int NC, int EC>
 __global__ void __launch_bounds__(B)
@@ -463,16 +465,26 @@ extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int3
   CEL_TRY(relabel_csr(n, order, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
   k_pos_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, g->w, g->ob, d->bw, d->lat, wp, cq,
                                                     st);
-  k_dev_gather<<<grid_for((int64_t)K * n, 256, 8192), 256, 0, s>>>(K, n, order, node_dev, d->D,
-                                                                  devp, st);
+  {
+    const int gx = grid_for(n, 256, 1024);
+    const int gy = K < 1024 ? K : 1024;
+    KTimer kt(s, "k_dev_gather");
+    k_dev_gather<<<dim3(gx, gy), 256, 0, s>>>(K, n, order, node_dev, d->D, devp, st);
+  }
   if (K == 1) {
     KTimer kt(s, "k_makespan_sweep");
     k_makespan_sweep<1024, 1536, 6144><<<1, 1024, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq,
                                                           devp, finp, makespan, st);
-  } else {
+  } else if (K <= kBatchWide) {
     KTimer kt(s, "k_makespan_batch");
     k_makespan_sweep<256, 1024, 4096><<<(unsigned)K, 256, 0, s>>>(n, L, level_ptr, pptr, pidx, wp,
                                                                   cq, devp, finp, makespan, st);
+  } else {
+    // more placements than CUs: small windows (about 35 KB of LDS) so that
+    // several placements share a CU and hide each other's memory latency
+    KTimer kt(s, "k_makespan_batch");
+    k_makespan_sweep<256, 256, 1024><<<(unsigned)K, 256, 0, s>>>(n, L, level_ptr, pptr, pidx, wp,
+                                                                 cq, devp, finp, makespan, st);
   }
   if (start || finish)
     k_makespan_out<<<grid_for((int64_t)K * n, 256, 8192), 256, 0, s>>>(K, n, order, finp, wp, start,

@@ -35,17 +35,17 @@ __global__ void k_place_nodes(int32_t n, int32_t C, const int32_t *cid, const in
   if (bad) raise_err(st, bad);
 }
 
-// Edges between clusters, one block per 256 consecutive sources.  PASS 0
+// Edges between clusters, edge-balanced blocks.  PASS 0
 // counts per target cluster (and checks cid[u] <= cid[v]); PASS 1 writes
 // (source cluster, edge id) into the target's bucket and the edge's comm.
 template <int PASS>
 __global__ void k_place_edges(cel_graph g, int64_t bw, int64_t lat, const int32_t *cid,
                               int32_t *cnt, const int32_t *boff, uint64_t *keys, uint32_t *ids,
                               int64_t *ecost, Status *st) {
-  __shared__ int32_t ptr[257];
+  __shared__ int32_t ptr[kRowsPB + 1], su[2];
   if (failed(st)) return;
   uint32_t bad = 0;
-  for_block_edges(g.out_ptr, g.n, ptr, [&](int32_t u, int32_t e) {
+  for_edges_balanced(g.out_ptr, g.n, g.m, ptr, su, [&](int32_t u, int32_t e) {
     const int32_t a = cid[u], b = cid[g.out_idx[e]];
     if (a == b) return;
     if (a > b) {
@@ -369,7 +369,7 @@ extern "C" int cel_place(const cel_graph *g, const cel_devices *d, const int32_t
   CEL_HIP(hipMemsetAsync(cnt, 0, sizeof(int32_t) * C, s));
   CEL_HIP(hipMemcpyAsync(dcap, d->cap, sizeof(int64_t) * d->D, hipMemcpyHostToDevice, s));
   k_place_nodes<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, C, cluster_id, g->w, g->mem, W, MEM, st);
-  const unsigned eb = (unsigned)((n + 255) / 256);
+  const unsigned eb = edge_blocks(g->m);
   k_place_edges<0><<<eb, 256, 0, s>>>(*g, d->bw, d->lat, cluster_id, cnt, nullptr, nullptr,
                                       nullptr, nullptr, st);
   CEL_TRY(exclusive_scan_i32(cnt, boff, C, sc, s));

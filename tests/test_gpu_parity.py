@@ -14,7 +14,7 @@ if not torch.cuda.is_available():  # collected on CPU, skipped there
 
 import paper_2208_00184_amd as cel  # noqa: E402
 from oracle import oracle as O  # noqa: E402
-from workloads import from_edges, make_config, make_random_dag  # noqa: E402
+from workloads import from_edges, make_config, make_random_dag, perturb_placements  # noqa: E402
 
 DEV = "cuda:0"
 
@@ -113,6 +113,35 @@ def test_makespan_configs(cfg, seed):
         ms1, st1, fi1 = cel.makespan(g, d, *args, tt(P[k], np.uint8), want_times=True)
         assert np_(ms1)[0] == ref_ms[k]
         assert np.array_equal(np_(fi1)[0], ref_fi[k])
+
+
+def test_makespan_large_batches():
+    """Batches larger than the CU count take the small-window kernel: every row
+    of a 400-placement batch on config 1, and sampled rows of the 1,024 perturbed
+    placements of config 5 (the batched-scoring workload)."""
+    wl, rt, rb = config(1, 1)
+    lev, oid, lp, L = rt
+    pr = rb[2]
+    P = random_placements(wl, 400, 7)
+    ref_ms, _, ref_fi = O.makespan(wl, pr, P)
+    g, d = up(wl)
+    args = (tt(pr, np.int32), tt(lev, np.int32), tt(lp, np.int32), L)
+    ms, st, fi = cel.makespan(g, d, *args, tt(P, np.uint8), want_times=True)
+    assert np.array_equal(np_(ms), ref_ms) and np.array_equal(np_(fi), ref_fi)
+
+    wl5 = make_config(5, 0)
+    lev5, oid5, lp5, L5 = O.topo_levels(wl5)
+    _, _, pr5, _ = O.blevel(wl5, lev5, oid5)
+    cid5, C5, _ = O.cluster(wl5, pr5, 200, -1)
+    cdev5, _, _, _ = O.place(wl5, cid5, C5)
+    P5 = perturb_placements(cdev5, wl5.D, 1024, 0)[:, cid5]
+    g5, d5 = up(wl5)
+    ms5, _, _ = cel.makespan(g5, d5, tt(pr5, np.int32), tt(lev5, np.int32), tt(lp5, np.int32), L5,
+                             tt(P5, np.uint8))
+    ms5 = np_(ms5)
+    rows = [0, 1, 511, 777, 1022, 1023]
+    ref5, _, _ = O.makespan(wl5, pr5, P5[rows], want_times=False)
+    assert np.array_equal(ms5[rows], ref5)
 
 
 # ---------------------------------------------------------- random small DAGs
