@@ -12,6 +12,16 @@
 
 namespace cel {
 
+// packed edge words of edges [ea, eb) (at most 512 of them), 8 per lane
+__device__ inline void load_pk8(int32_t (&pk)[8], const int32_t *w, int32_t ea, int32_t eb,
+                                int lane) {
+#pragma unroll
+  for (int q = 0; q < 8; q++) {
+    const int32_t e = ea + lane + 64 * q;
+    pk[q] = (ea + 64 * q < eb && e < eb) ? w[e] : 0;
+  }
+}
+
 constexpr int kSweepB = 1024;
 
 // per position: w and w + c (c = 0 with CEL_COMM_OFF)
@@ -71,7 +81,7 @@ __global__ void __launch_bounds__(kSweepB)
                   const Status *st) {
   __shared__ int32_t s_lv[kWinL + 2];  // level boundaries near the cursor
   __shared__ int32_t s_rp[kWinN + 1];  // rows of the candidate window (absolute edge offsets)
-  __shared__ int32_t s_tgt[kWinE];     // neighbour positions of the window's edges
+  __shared__ int32_t s_epk[kWinE];     // per edge: neighbour slot + 1 (0: outside) | owner << 16
   __shared__ int16_t s_own[kWinE];     // owner (window-relative node) of each edge
   __shared__ int64_t s_pm[kWinN];      // running max over neighbours, -1 if none yet
   __shared__ int64_t s_v[kWinN];       // values computed in this window
@@ -168,10 +178,12 @@ __global__ void __launch_bounds__(kSweepB)
       // stage edges: neighbours outside the window are final
       for (int32_t e = E0 + tid; e < E1; e += kSweepB) {
         const int32_t r = ridx[e];
-        s_tgt[e - E0] = r;
-        if (REVERSE ? (r >= P1) : (r < P0)) {
+        const int32_t own = s_own[e - E0];
+        const bool in = REVERSE ? (r < P1) : (r >= P0);
+        s_epk[e - E0] = (in ? r - P0 + 1 : 0) | (own << 16);
+        if (!in) {
           const int64_t x = REVERSE ? val[r] : val[r] + wcp[r];
-          atomicMax((long long *)&s_pm[s_own[e - E0]], (long long)x);
+          atomicMax((long long *)&s_pm[own], (long long)x);
         }
       }
       __syncthreads();
@@ -209,37 +221,39 @@ __global__ void __launch_bounds__(kSweepB)
           if (narrow) {
             CEL_TCOUNT(REVERSE ? 4 : 16 + 4);
             if (wave0) {
-              // neighbours inside the window, 8 edges per lane, loads batched
-              int32_t r[8];
-#pragma unroll
-              for (int q = 0; q < 8; q++) {
-                const int32_t e = ea + tid + 64 * q;
-                r[q] = e < eb ? s_tgt[e] : (REVERSE ? P1 : -1);
-              }
+              // neighbours inside the window, up to 8 edges per lane (one packed
+              // word each: neighbour slot and owner)
+              int32_t pk[8];
+              load_pk8(pk, s_epk, ea, eb, tid);
               int64_t x[8];
               int32_t ow[8];
 #pragma unroll
               for (int q = 0; q < 8; q++) {
-                const bool in = REVERSE ? (r[q] < P1) : (r[q] >= P0);
-                const int32_t j = in ? r[q] - P0 : 0;
-                ow[q] = in ? s_own[ea + tid + 64 * q] : -1;
-                x[q] = REVERSE ? s_v[j] : s_v[j] + s_wc[j];
+                ow[q] = -1;
+                x[q] = 0;
+                if (ea + 64 * q < eb) {
+                  const int32_t jp = pk[q] & 0xFFFF;
+                  const int32_t j = jp ? jp - 1 : 0;
+                  ow[q] = jp ? pk[q] >> 16 : -1;
+                  x[q] = REVERSE ? s_v[j] : s_v[j] + s_wc[j];
+                }
               }
 #pragma unroll
               for (int q = 0; q < 8; q++)
                 if (ow[q] >= 0) atomicMax((long long *)&s_pm[ow[q]], (long long)x[q]);
-              wave_lds_sync();
+              // a wave's LDS operations complete in issue order: no wait needed
+              lds_order();
 #pragma unroll
               for (int q = 0; q < 4; q++) {
                 const int32_t i = a + tid + 64 * q;
-                if (i < b) {
+                if (a + 64 * q < b && i < b) {
                   const int64_t pm = s_pm[i];
                   const int64_t v = REVERSE ? s_wc[i] + pm : (pm > 0 ? pm : 0);
                   s_v[i] = v;
                   val[P0 + i] = v;
                 }
               }
-              wave_lds_sync();
+              lds_order();
             }
             synced = false;
             CEL_TSTAMP(tl1);
@@ -248,11 +262,12 @@ __global__ void __launch_bounds__(kSweepB)
             CEL_TCOUNT(REVERSE ? 5 : 16 + 5);
             if (!synced) __syncthreads();
             for (int32_t e = ea + tid; e < eb; e += kSweepB) {
-              const int32_t r = s_tgt[e];
-              if (REVERSE ? (r < P1) : (r >= P0)) {
-                const int32_t j = r - P0;
+              const int32_t wd = s_epk[e];
+              const int32_t jp = wd & 0xFFFF;
+              if (jp) {
+                const int32_t j = jp - 1;
                 const int64_t x = REVERSE ? s_v[j] : s_v[j] + s_wc[j];
-                atomicMax((long long *)&s_pm[s_own[e]], (long long)x);
+                atomicMax((long long *)&s_pm[wd >> 16], (long long)x);
               }
             }
             __syncthreads();

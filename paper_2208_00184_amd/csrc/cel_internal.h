@@ -46,6 +46,12 @@ __device__ inline void wave_lds_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
+// Compiler-only ordering of LDS accesses inside one wave.  A wave's LDS
+// operations complete in issue order, so a lane reads what another lane of
+// the same wave wrote earlier without a wait; the compiler must merely keep
+// the accesses in program order.
+__device__ inline void lds_order() { asm volatile("" ::: "memory"); }
+
 // ------------------------------------------------ wave-level scans with DPP
 // DPP moves read another lane's register inside the VALU (no LDS round trip).
 // Lanes whose source is outside the allowed rows keep `old`.

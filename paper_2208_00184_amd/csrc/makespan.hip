@@ -63,20 +63,58 @@ __global__ void k_pos_costs(int32_t n, const int32_t *order, const int64_t *w, c
 // the whole block.  A node with more than EC predecessors forms a window of
 // its own.
 constexpr int kMsL = 256;
+constexpr int64_t kShift = int64_t(1) << 62;
+
+// packed in-edge words of edges [ea, eb) (at most 512), 8 per lane
+__device__ inline void load_epk(int32_t (&pk)[8], const int32_t *s_epk, int32_t ea, int32_t eb,
+                                int lane) {
+#pragma unroll
+  for (int q = 0; q < 8; q++) {
+    const int32_t e = ea + lane + 64 * q;
+    pk[q] = (ea + 64 * q < eb && e < eb) ? s_epk[e] : 0;
+  }
+}
+
+// One step of the segmented scan of max-plus maps x -> max(a, x + b) with a
+// shifted by +2^62, so that the identity (a, b, no start) is all zero and DPP
+// may zero-fill: combine with the lane selected by CTRL unless this lane
+// already starts its segment.
+template <int CTRL, int ROWMASK>
+__device__ inline void segz_step(int64_t &a, int64_t &b, int32_t &f) {
+  const int32_t alo = __builtin_amdgcn_update_dpp(0, (int32_t)a, CTRL, ROWMASK, 0xF, true);
+  const int32_t ahi = __builtin_amdgcn_update_dpp(0, (int32_t)(a >> 32), CTRL, ROWMASK, 0xF, true);
+  const int32_t blo = __builtin_amdgcn_update_dpp(0, (int32_t)b, CTRL, ROWMASK, 0xF, true);
+  const int32_t bhi = __builtin_amdgcn_update_dpp(0, (int32_t)(b >> 32), CTRL, ROWMASK, 0xF, true);
+  const int32_t uf = __builtin_amdgcn_update_dpp(0, f, CTRL, ROWMASK, 0xF, true);
+  const int64_t ua = (int64_t)(((uint64_t)(uint32_t)ahi << 32) | (uint32_t)alo);
+  const int64_t ub = (int64_t)(((uint64_t)(uint32_t)bhi << 32) | (uint32_t)blo);
+  const bool keep = f != 0;
+  const int64_t c = ua + b;
+  a = (keep || c <= a) ? a : c;
+  b = keep ? b : ub + b;
+  f = keep ? f : uf;
+}
+__device__ inline void wave_seg_scan_maxplus_z(int64_t &a, int64_t &b, int32_t &f) {
+  segz_step<0x111, 0xF>(a, b, f);  // row_shr:1
+  segz_step<0x112, 0xF>(a, b, f);  // row_shr:2
+  segz_step<0x114, 0xF>(a, b, f);  // row_shr:4
+  segz_step<0x118, 0xF>(a, b, f);  // row_shr:8
+  segz_step<0x142, 0xA>(a, b, f);  // row_bcast:15 into rows 1 and 3
+  segz_step<0x143, 0xC>(a, b, f);  // row_bcast:31 into rows 2 and 3
+}
 constexpr int kBatchWide = 384;  // batches up to this size get one CU-sized window per placement
 
 template <int B, int NC, int EC>
 __global__ void __launch_bounds__(B)
-    k_makespan_sweep(int32_t n, int32_t L, const int32_t *lp, const int32_t *pptr,
+    k_makespan_sweep(int32_t n, int32_t L, int32_t dbits, const int32_t *lp, const int32_t *pptr,
                      const int32_t *pidx, const int64_t *wp, const int64_t *cq,
                      const uint8_t *devp, int64_t *finp, int64_t *makespan, const Status *st) {
   constexpr int NW = B / 64;
   static_assert(B >= 256, "device partition uses 256 threads");
   __shared__ int32_t s_lv[kMsL + 2];
   __shared__ int32_t s_rp[NC + 1];
-  __shared__ int32_t s_tgt[EC];
+  __shared__ int32_t s_epk[EC];  // per in-edge: pred slot + 1 (0: before the window), owner, owner's device
   __shared__ int16_t s_own[EC];
-  __shared__ uint8_t s_edv[EC];
   __shared__ int64_t s_pm[NC], s_f[NC], s_w[NC], s_c[NC];
   __shared__ uint8_t s_dv[NC];
   __shared__ int32_t s_la[kMsL], s_lb[kMsL], s_lea[kMsL], s_leb[kMsL], s_lend[kMsL];
@@ -102,6 +140,8 @@ __global__ void __launch_bounds__(B)
   int64_t mk = 0;
   int32_t P0 = 0, lcur = 0;
   while (P0 < n) {
+    CEL_TSTAMP(t0);
+    CEL_TCOUNT(6);
     const int32_t Pc1 = P0 + NC < n ? P0 + NC : n;
     for (int t = tid; t <= Pc1 - P0; t += B) s_rp[t] = pptr[P0 + t];
     for (int k = tid; k <= kMsL + 1; k += B) {
@@ -128,10 +168,7 @@ __global__ void __launch_bounds__(B)
       s_c[i] = cq[P0 + i];
       s_dv[i] = dv;
       if (!heavy)
-        for (int32_t q = s_rp[i] - E0; q < s_rp[i + 1] - E0; q++) {
-          s_own[q] = (int16_t)i;
-          s_edv[q] = dv;
-        }
+        for (int32_t q = s_rp[i] - E0; q < s_rp[i + 1] - E0; q++) s_own[q] = (int16_t)i;
     }
     for (int32_t k = tid; k < kMsL; k += B) {
       const int32_t lb = s_lv[k], le = s_lv[k + 1];
@@ -145,17 +182,22 @@ __global__ void __launch_bounds__(B)
       s_lend[k] = le >= P1;
     }
     __syncthreads();
+    CEL_TSTAMP(t1);
+    CEL_TADD(0, t0, t1);
     // predecessors before the window are final: fold them into s_pm
     for (int32_t e = E0 + tid; e < E1; e += B) {
       const int32_t q = pidx[e];
       const int32_t own = heavy ? 0 : s_own[e - E0];
-      if (!heavy) s_tgt[e - E0] = q;
+      if (!heavy)
+        s_epk[e - E0] = (q >= P0 ? q - P0 + 1 : 0) | (own << 12) | ((int32_t)s_dv[own] << 24);
       if (q < P0) {
         const int64_t x = fk[q] + (dk[q] != s_dv[own] ? cq[q] : 0);
         atomicMax((long long *)&s_pm[own], (long long)x);
       }
     }
     __syncthreads();
+    CEL_TSTAMP(t2);
+    CEL_TADD(1, t1, t2);
     int32_t ma[4], mb[4], mea[4], meb[4], mend[4];
 #pragma unroll
     for (int u = 0; u < 4; u++) {
@@ -167,6 +209,8 @@ __global__ void __launch_bounds__(B)
       mend[u] = s_lend[k];
     }
     bool synced = true;
+    CEL_TSTAMP(t3);
+    CEL_TADD(2, t2, t3);
     for (int32_t k = 0; k < kMsL; k++) {
       const int u = k >> 6, ln = k & 63;
       int32_t a0, b0, ea, eb, stop;
@@ -183,31 +227,37 @@ __global__ void __launch_bounds__(B)
       stop = __builtin_amdgcn_readlane(stop, ln);
       if (a0 < b0) {
         const bool narrow = (b0 - a0 <= 256) && (eb - ea <= 512);
+        CEL_TSTAMP(tl0);
         if (narrow) {
           if (wave0) {
-            // predecessors inside the window: 8 edges per lane, loads batched
-            int32_t r[8];
-#pragma unroll
-            for (int q = 0; q < 8; q++) {
-              const int32_t e = ea + lane + 64 * q;
-              r[q] = e < eb ? s_tgt[e] : -1;
-            }
+            // predecessors inside the window: up to 8 edges per lane (one
+            // packed word each: predecessor slot, owner, owner's device)
+            int32_t pk[8];
+            load_epk(pk, s_epk, ea, eb, lane);
             int64_t x[8];
             int32_t ow[8];
 #pragma unroll
             for (int q = 0; q < 8; q++) {
-              const int32_t e = ea + lane + 64 * q;
-              const bool in = r[q] >= P0;
-              const int32_t j = in ? r[q] - P0 : 0;
-              ow[q] = in ? s_own[e] : -1;
-              const uint8_t od = in ? s_edv[e] : 0;
-              x[q] = s_f[j] + (s_dv[j] != od ? s_c[j] : 0);
+              ow[q] = -1;
+              x[q] = 0;
+              if (ea + 64 * q < eb) {
+                const int32_t wd = pk[q];
+                const int32_t jp = wd & 0xFFF;
+                const int32_t j = jp ? jp - 1 : 0;
+                ow[q] = jp ? (wd >> 12) & 0xFFF : -1;
+                x[q] = s_f[j] + (s_dv[j] != ((wd >> 24) & 255) ? s_c[j] : 0);
+              }
             }
 #pragma unroll
             for (int q = 0; q < 8; q++)
               if (ow[q] >= 0) atomicMax((long long *)&s_pm[ow[q]], (long long)x[q]);
-            wave_lds_sync();
+            // One wave's LDS operations complete in issue order, so the rows
+            // below see these updates; only the compiler must not reorder.
+            lds_order();
+            CEL_TSTAMP(te);
+            CEL_TADD(9, tl0, te);
             for (int32_t row = a0; row < b0; row += 64) {
+              CEL_TCOUNT(11);
               const int32_t cnt2 = b0 - row < 64 ? b0 - row : 64;
               const bool act = lane < cnt2;
               const int32_t i = row + lane;
@@ -218,62 +268,69 @@ __global__ void __launch_bounds__(B)
                 ww = s_w[i];
                 aa = s_pm[i] + ww;
               }
-              // slot in device-grouped order: devices ascending, positions ascending
+              // slot in device-grouped order (devices ascending, positions
+              // ascending): ballots over the device id's bits, high to low
               const uint64_t actm = __ballot(act);
-              uint64_t eq = actm, lt = 0;
-              for (int bit = 7; bit >= 0; bit--) {
-                const int on = (dv >> bit) & 1;
+              uint32_t eql = (uint32_t)actm, eqh = (uint32_t)(actm >> 32), ltl = 0, lth = 0;
+              for (int bit = dbits - 1; bit >= 0; bit--) {
+                const uint32_t on = (dv >> bit) & 1;
                 const uint64_t bb = __ballot(on) & actm;
-                if (on) {
-                  lt |= eq & ~bb;
-                  eq &= bb;
-                } else {
-                  eq &= ~bb;
-                }
+                const uint32_t bl = (uint32_t)bb, bh = (uint32_t)(bb >> 32);
+                const uint32_t keep0 = on - 1u;  // ~0 when the bit is 0, else 0
+                ltl |= (eql & ~bl) & ~keep0;     // equal so far, bit 0 there, 1 here
+                lth |= (eqh & ~bh) & ~keep0;
+                eql &= bl ^ keep0;
+                eqh &= bh ^ keep0;
               }
-              if (act) {
-                const int q = __popcll(lt) + __popcll(eq & lanemask_lt);
-                s_a[q] = aa;
-                s_b[q] = ww;
-                s_pos[q] = i;
-                s_dev[q] = (uint8_t)dv;
-              }
-              wave_lds_sync();
-              int64_t sa = kNeg, sb = 0;
-              int dq = 0;
-              int32_t f = 1;
-              if (act) {
-                sa = s_a[lane];
-                sb = s_b[lane];
-                dq = s_dev[lane];
-                f = (lane == 0) || (s_dev[lane - 1] != dq);
-              }
-              wave_seg_scan_dpp(sa, sb, f);
-              int64_t fin = 0;
-              bool last = false;
-              if (act) {
+              const uint64_t eq = ((uint64_t)eqh << 32) | eql;
+              const int below = __popcll(eq & lanemask_lt);
+              const int q = act ? __popc(ltl) + __popc(lth) + below : lane;  // a permutation
+              const int head = act && below == 0;                // first of its device
+              const int tail = act && (eq >> lane) == 1ull;      // last of its device
+              const int addr = q << 2;
+              const int64_t ash = aa + kShift;  // shifted: the scan identity is all zero
+              const int32_t meta = dv | (head << 8) | (tail << 9) | ((int)act << 10);
+              const int32_t pa_lo = __builtin_amdgcn_ds_permute(addr, (int32_t)ash);
+              const int32_t pa_hi = __builtin_amdgcn_ds_permute(addr, (int32_t)(ash >> 32));
+              const int32_t pb_lo = __builtin_amdgcn_ds_permute(addr, (int32_t)ww);
+              const int32_t pb_hi = __builtin_amdgcn_ds_permute(addr, (int32_t)(ww >> 32));
+              const int32_t pm = __builtin_amdgcn_ds_permute(addr, meta);
+              const int32_t pj = __builtin_amdgcn_ds_permute(addr, i);
+              const bool pact = (pm >> 10) & 1;
+              const int dq = pm & 255;
+              int64_t sa = pact ? (int64_t)(((uint64_t)(uint32_t)pa_hi << 32) | (uint32_t)pa_lo) : 0;
+              int64_t sb = pact ? (int64_t)(((uint64_t)(uint32_t)pb_hi << 32) | (uint32_t)pb_lo) : 0;
+              int32_t f = pact ? ((pm >> 8) & 1) : 1;
+              wave_seg_scan_maxplus_z(sa, sb, f);
+              sa -= kShift;
+              if (pact) {
                 const int64_t viafree = s_avail[dq] + sb;
-                fin = viafree > sa ? viafree : sa;
-                const int32_t j = s_pos[lane];
-                s_f[j] = fin;
-                fk[P0 + j] = fin;
+                const int64_t fin = viafree > sa ? viafree : sa;
+                s_f[pj] = fin;
+                fk[P0 + pj] = fin;
                 mk = fin > mk ? fin : mk;
-                last = (lane + 1 == cnt2) || (s_dev[lane + 1] != dq);
+                lds_order();  // every lane's read of s_avail precedes the update
+                if ((pm >> 9) & 1) s_avail[dq] = fin;
               }
-              wave_lds_sync();
-              if (last) s_avail[dq] = fin;
-              wave_lds_sync();
+              lds_order();
             }
+            CEL_TSTAMP(tr);
+            CEL_TADD(10, te, tr);
           }
           synced = false;
+          CEL_TSTAMP(tl1);
+          CEL_TADD(7, tl0, tl1);
+
+          CEL_TCOUNT(4);
         } else {
           if (!synced) __syncthreads();
           for (int32_t e = ea + tid; e < eb; e += B) {
-            const int32_t r = s_tgt[e];
-            if (r >= P0) {
-              const int32_t j = r - P0;
-              const int64_t x = s_f[j] + (s_dv[j] != s_edv[e] ? s_c[j] : 0);
-              atomicMax((long long *)&s_pm[s_own[e]], (long long)x);
+            const int32_t wd = s_epk[e];
+            const int32_t jp = wd & 0xFFF;
+            if (jp) {
+              const int32_t j = jp - 1;
+              const int64_t x = s_f[j] + (s_dv[j] != ((wd >> 24) & 255) ? s_c[j] : 0);
+              atomicMax((long long *)&s_pm[(wd >> 12) & 0xFFF], (long long)x);
             }
           }
           __syncthreads();
@@ -374,10 +431,15 @@ __global__ void __launch_bounds__(B)
             __syncthreads();
           }
           synced = true;
+          CEL_TSTAMP(tl1);
+          CEL_TADD(8, tl0, tl1);
+          CEL_TCOUNT(5);
         }
       }
       if (stop) break;  // the window ends inside this level
     }
+    CEL_TSTAMP(t4);
+    CEL_TADD(3, t3, t4);
     // next window starts at P1; move the level cursor to the level holding P1
     if (P1 < n) {
       int32_t k = 0;
@@ -471,19 +533,21 @@ extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int3
     KTimer kt(s, "k_dev_gather");
     k_dev_gather<<<dim3(gx, gy), 256, 0, s>>>(K, n, order, node_dev, d->D, devp, st);
   }
+  int dbits = 0;  // bits of the largest device id
+  while ((1 << dbits) < d->D) dbits++;
   if (K == 1) {
     KTimer kt(s, "k_makespan_sweep");
-    k_makespan_sweep<1024, 1536, 6144><<<1, 1024, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq,
+    k_makespan_sweep<1024, 1536, 6144><<<1, 1024, 0, s>>>(n, L, dbits, level_ptr, pptr, pidx, wp, cq,
                                                           devp, finp, makespan, st);
   } else if (K <= kBatchWide) {
     KTimer kt(s, "k_makespan_batch");
-    k_makespan_sweep<256, 1024, 4096><<<(unsigned)K, 256, 0, s>>>(n, L, level_ptr, pptr, pidx, wp,
+    k_makespan_sweep<256, 1024, 4096><<<(unsigned)K, 256, 0, s>>>(n, L, dbits, level_ptr, pptr, pidx, wp,
                                                                   cq, devp, finp, makespan, st);
   } else {
     // more placements than CUs: small windows (about 35 KB of LDS) so that
     // several placements share a CU and hide each other's memory latency
     KTimer kt(s, "k_makespan_batch");
-    k_makespan_sweep<256, 256, 1024><<<(unsigned)K, 256, 0, s>>>(n, L, level_ptr, pptr, pidx, wp,
+    k_makespan_sweep<256, 256, 1024><<<(unsigned)K, 256, 0, s>>>(n, L, dbits, level_ptr, pptr, pidx, wp,
                                                                  cq, devp, finp, makespan, st);
   }
   if (start || finish)
