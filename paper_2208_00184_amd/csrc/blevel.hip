@@ -384,7 +384,7 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
   CEL_TRY(sc.get(&wp, n));
   CEL_TRY(sc.get(&wcp, n));
   CEL_TRY(sc.get(&blp, n));
-  CEL_TRY(relabel_csr(n, order_id, pos, g->out_ptr, g->out_idx, sptr, sidx, sc, s, st));
+  CEL_TRY(relabel_csr(n, g->m, order_id, pos, g->out_ptr, g->out_idx, sptr, sidx, sc, s, st));
   k_node_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order_id, g->w, g->ob, d->bw, d->lat,
                                                      (flags & CEL_COMM_OFF) ? 1 : 0, wp, wcp, st);
   {
@@ -398,30 +398,24 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
     CEL_TRY(sc.get(&pptr, (int64_t)n + 1));
     CEL_TRY(sc.get(&pidx, g->m));
     CEL_TRY(sc.get(&tlp, n));
-    CEL_TRY(relabel_csr(n, order_id, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
+    CEL_TRY(relabel_csr(n, g->m, order_id, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
     {
       KTimer kt(s, "k_tlevel_sweep");
       k_level_sweep<false><<<1, kSweepB, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, wcp, tlp, st);
     }
     k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, tlp, tlevel, st, &st->s1);
   }
+  if (prio_order && n > 0) {
+    uint64_t *keys;
+    CEL_TRY(sc.get(&keys, n));
+    uint32_t *ids = reinterpret_cast<uint32_t *>(prio_order);
+    k_prio_keys<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order_id, blp, keys, ids, st);
+    CEL_TRY(segmented_sort(keys, ids, level_ptr, L, n, sc, s, st));
+  }
   CEL_HIP(hipGetLastError());
   Status h;
   CEL_TRY(read_status(st, &h, s));
   if (h.err) return status_error(h, fn);
   *cp = h.s0;
-  if (prio_order && n > 0) {
-    std::vector<int32_t> lp(L + 1);
-    CEL_HIP(hipMemcpyAsync(lp.data(), level_ptr, sizeof(int32_t) * (L + 1), hipMemcpyDeviceToHost, s));
-    CEL_HIP(hipStreamSynchronize(s));
-    std::vector<int64_t> seg(lp.begin(), lp.end());
-    uint64_t *keys;
-    CEL_TRY(sc.get(&keys, n));
-    uint32_t *ids = reinterpret_cast<uint32_t *>(prio_order);
-    k_prio_keys<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order_id, blp, keys, ids, st);
-    CEL_TRY(segmented_sort(keys, ids, seg, sc, s));
-  }
-  CEL_HIP(hipStreamSynchronize(s));
-  timing_collect();
   return CEL_OK;
 }

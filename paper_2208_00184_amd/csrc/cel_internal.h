@@ -276,17 +276,18 @@ int check_topo_order(const cel_graph *g, const int32_t *order, int32_t *pos, Sta
 int exclusive_scan_i32(const int32_t *in, int32_t *out, int64_t n, Scratch &sc, hipStream_t s);
 int exclusive_scan_i64(const int64_t *in, int64_t *out, int64_t n, Scratch &sc, hipStream_t s);
 
-// Relabels a CSR (ptr/idx over node ids) into position space of `order`:
-// row p lists pos[idx[k]] for the edges of node order[p].
-int relabel_csr(int32_t n, const int32_t *order, const int32_t *pos, const int32_t *ptr,
-                const int32_t *idx, int32_t *pptr, int32_t *pidx, Scratch &sc, hipStream_t s,
-                const Status *st);
+// Relabels a CSR (ptr/idx over node ids, m edges, validated) into position
+// space of `order`: row p lists pos[idx[k]] for the edges of node order[p].
+int relabel_csr(int32_t n, int32_t m, const int32_t *order, const int32_t *pos,
+                const int32_t *ptr, const int32_t *idx, int32_t *pptr, int32_t *pidx, Scratch &sc,
+                hipStream_t s, const Status *st);
 
 // Sorts each segment [seg[i], seg[i+1]) of (key, id) pairs by (key, id), both
-// ascending; (key, id) pairs must be distinct.  seg_host is a host copy of the
-// nseg+1 offsets.  Results land in keys/ids (in place).
-int segmented_sort(uint64_t *keys, uint32_t *ids, const std::vector<int64_t> &seg_host,
-                   Scratch &sc, hipStream_t s);
+// ascending; (key, id) pairs must be distinct.  seg is a device array of
+// nseg + 1 offsets covering [0, n), trusted only while st holds no error (the
+// kernels return early otherwise).  Stream-ordered: no host synchronisation.
+int segmented_sort(uint64_t *keys, uint32_t *ids, const int32_t *seg, int32_t nseg, int64_t n,
+                   Scratch &sc, hipStream_t s, const Status *st);
 
 // Copies the status block to the host (synchronising the stream).
 int read_status(const Status *dst, Status *host, hipStream_t s);

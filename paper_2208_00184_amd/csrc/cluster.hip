@@ -928,7 +928,7 @@ extern "C" int cel_cluster(const cel_graph *g, const cel_devices *d, const int32
     CEL_TRY(sc.get(&pidx, g->m));
     CEL_TRY(sc.get(&P, (int64_t)n + 1));
     CEL_TRY(exclusive_scan_i64(outc, PO, n, sc, s));
-    CEL_TRY(relabel_csr(n, order, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
+    CEL_TRY(relabel_csr(n, g->m, order, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
     bool blocked = false;
     CEL_TRY(dp_blocked(n, g->m, R, lo, pptr, pidx, cq, PO, P, st, sc, s, &blocked));
     if (blocked) {

@@ -436,46 +436,22 @@ __global__ void k_row_deg(int32_t n, const int32_t *order, const int32_t *ptr, i
   }
 }
 
-// One block per 256 consecutive positions: the block's edges are spread over
-// all threads (owner found by binary search), so a node of huge degree does
-// not serialise on one thread.
-__global__ void k_relabel_rows(int32_t n, const int32_t *order, const int32_t *pos,
+// Output edges in edge-balanced blocks: slot k of row p (position p) takes
+// edge k - pptr[p] of node order[p], so a row of huge degree is spread over
+// many blocks.
+__global__ void k_relabel_rows(int32_t n, int32_t m, const int32_t *order, const int32_t *pos,
                                const int32_t *ptr, const int32_t *idx, const int32_t *pptr,
                                int32_t *pidx, const Status *st) {
-  __shared__ int32_t off[257];
-  __shared__ int32_t beg[256];
-  __shared__ int32_t wsum[4];
+  __shared__ int32_t rp[kRowsPB + 1], su[2];
   if (failed(st)) return;
-  const int64_t p0 = (int64_t)blockIdx.x * 256;
-  const int64_t p = p0 + threadIdx.x;
-  int32_t d = 0, b = 0;
-  if (p < n) {
-    int32_t v = order[p];
-    b = ptr[v];
-    d = ptr[v + 1] - b;
-  }
-  int32_t tot;
-  int32_t ex = block_exclusive_scan<int32_t>(d, wsum, &tot);
-  off[threadIdx.x] = ex;
-  beg[threadIdx.x] = b;
-  if (threadIdx.x == 0) off[256] = tot;
-  __syncthreads();
-  const int32_t outbase = pptr[p0];
-  for (int32_t j = threadIdx.x; j < tot; j += 256) {
-    int lo = 0, hi = 255;  // owner: last row with off[row] <= j
-    while (lo < hi) {
-      int mid = (lo + hi + 1) >> 1;
-      if (off[mid] <= j) lo = mid;
-      else hi = mid - 1;
-    }
-    int32_t k = j - off[lo];
-    pidx[outbase + j] = pos[idx[beg[lo] + k]];
-  }
+  for_edges_balanced(pptr, n, m, rp, su, [&](int32_t p, int32_t k) {
+    pidx[k] = pos[idx[ptr[order[p]] + (k - pptr[p])]];
+  });
 }
 
-int relabel_csr(int32_t n, const int32_t *order, const int32_t *pos, const int32_t *ptr,
-                const int32_t *idx, int32_t *pptr, int32_t *pidx, Scratch &sc, hipStream_t s,
-                const Status *st) {
+int relabel_csr(int32_t n, int32_t m, const int32_t *order, const int32_t *pos,
+                const int32_t *ptr, const int32_t *idx, int32_t *pptr, int32_t *pidx, Scratch &sc,
+                hipStream_t s, const Status *st) {
   if (n <= 0) {
     CEL_HIP(hipMemsetAsync(pptr, 0, sizeof(int32_t), s));
     return CEL_OK;
@@ -485,13 +461,17 @@ int relabel_csr(int32_t n, const int32_t *order, const int32_t *pos, const int32
   k_row_deg<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, ptr, deg, st);
   CEL_TRY(exclusive_scan_i32(deg, pptr, n, sc, s));
   KTimer kt(s, "k_relabel_rows");
-  k_relabel_rows<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(n, order, pos, ptr, idx, pptr, pidx,
-                                                              st);
+  k_relabel_rows<<<edge_blocks(m), 256, 0, s>>>(n, m, order, pos, ptr, idx, pptr, pidx, st);
   CEL_HIP(hipGetLastError());
   return CEL_OK;
 }
 
 // ------------------------------------------------------- segmented sort
+//
+// Device-only: tiles of at most kSortTile elements are bitonic-sorted in LDS,
+// then segments longer than a tile are merged in passes of doubling run
+// width.  Tile lists and pass counts come from device data and host-known
+// upper bounds, so no host synchronisation is needed.
 
 constexpr int kSortTile = 2048;
 
@@ -503,11 +483,36 @@ __device__ inline bool kless(uint64_t ka, uint32_t ia, uint64_t kb, uint32_t ib)
   return ka < kb || (ka == kb && ia < ib);
 }
 
-// Bitonic sort of one tile (<= kSortTile elements) in LDS.
+__global__ void k_tile_count(const int32_t *seg, int32_t nseg, int32_t *tcnt, const Status *st) {
+  if (failed(st)) return;  // offsets not validated
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nseg;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t len = seg[i + 1] - seg[i];
+    tcnt[i] = len > 1 ? (len + kSortTile - 1) / kSortTile : 0;
+  }
+}
+
+__global__ void k_tile_fill(const int32_t *seg, int32_t nseg, const int32_t *toff, Tile *tiles,
+                            const Status *st) {
+  if (failed(st)) return;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nseg;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t a = seg[i], len = seg[i + 1] - a;
+    if (len <= 1) continue;
+    int32_t t = toff[i];
+    for (int32_t o = 0; o < len; o += kSortTile, t++)
+      tiles[t] = Tile{a + o, len - o < kSortTile ? len - o : kSortTile};
+  }
+}
+
+// Bitonic sort of one tile (<= kSortTile elements) in LDS; blocks past the
+// tile count (ntiles, on the device) exit.
 __global__ void __launch_bounds__(256) k_sort_tiles(uint64_t *keys, uint32_t *ids,
-                                                    const Tile *tiles) {
+                                                    const Tile *tiles, const int32_t *ntiles,
+                                                    const Status *st) {
   __shared__ uint64_t sk[kSortTile];
   __shared__ uint32_t si[kSortTile];
+  if (failed(st) || (int32_t)blockIdx.x >= *ntiles) return;
   const Tile t = tiles[blockIdx.x];
   int P = 2;
   while (P < t.len) P <<= 1;
@@ -542,36 +547,54 @@ __global__ void __launch_bounds__(256) k_sort_tiles(uint64_t *keys, uint32_t *id
   }
 }
 
-// One merge round over every large segment: runs of `width` are merged in
-// pairs; each element finds its output slot by counting the smaller elements
-// of the partner run (binary search).  (key, id) pairs are distinct.
-__global__ void k_merge_pass(const uint64_t *kin, const uint32_t *iin, uint64_t *kout,
-                             uint32_t *iout, const int64_t *seg_start, const int64_t *seg_off,
-                             int nseg, int64_t width, int64_t total) {
-  for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g < total;
-       g += (int64_t)gridDim.x * blockDim.x) {
-    int lo = 0, hi = nseg - 1;  // segment: last s with seg_off[s] <= g
+// segment of every element: last s with seg[s] <= i
+__global__ void k_seg_of(const int32_t *seg, int32_t nseg, int64_t n, int32_t *sid,
+                         const Status *st) {
+  if (failed(st)) return;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    int32_t lo = 0, hi = nseg - 1;
     while (lo < hi) {
-      int mid = (lo + hi + 1) >> 1;
-      if (seg_off[mid] <= g) lo = mid;
+      const int32_t mid = (lo + hi + 1) >> 1;
+      if (seg[mid] <= i) lo = mid;
       else hi = mid - 1;
     }
-    const int64_t base = seg_start[lo], len = seg_off[lo + 1] - seg_off[lo];
-    const int64_t off = g - seg_off[lo];
+    sid[i] = lo;
+  }
+}
+
+// One merge round over the segments longer than a tile: runs of `width` are
+// merged in pairs (each element finds its slot by counting the smaller
+// elements of the partner run); segments already one run are copied.
+__global__ void k_merge_pass(const uint64_t *kin, const uint32_t *iin, uint64_t *kout,
+                             uint32_t *iout, const int32_t *seg, const int32_t *sid, int64_t n,
+                             int64_t width, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g < n;
+       g += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t s = sid[g];
+    const int64_t base = seg[s], len = seg[s + 1] - base;
+    if (len <= kSortTile) continue;  // sorted by its tile, never moves
+    const uint64_t k = kin[g];
+    const uint32_t id = iin[g];
+    if (len <= width) {
+      kout[g] = k;
+      iout[g] = id;
+      continue;
+    }
+    const int64_t off = g - base;
     const int64_t a0 = (off / (2 * width)) * (2 * width);
     const int64_t a1 = a0 + width < len ? a0 + width : len;
     const int64_t b1 = a0 + 2 * width < len ? a0 + 2 * width : len;
-    const uint64_t k = kin[base + off];
-    const uint32_t id = iin[base + off];
     int64_t r0, r1, own;
     if (off < a1) {
       r0 = a1; r1 = b1; own = off - a0;
     } else {
       r0 = a0; r1 = a1; own = off - a1;
     }
-    int64_t l = r0, h = r1;  // count of partner elements smaller than (k, id)
+    int64_t l = r0, h = r1;  // partner elements smaller than (k, id)
     while (l < h) {
-      int64_t mid = (l + h) >> 1;
+      const int64_t mid = (l + h) >> 1;
       if (kless(kin[base + mid], iin[base + mid], k, id)) l = mid + 1;
       else h = mid;
     }
@@ -581,76 +604,59 @@ __global__ void k_merge_pass(const uint64_t *kin, const uint32_t *iin, uint64_t 
   }
 }
 
-int segmented_sort(uint64_t *keys, uint32_t *ids, const std::vector<int64_t> &seg,
-                   Scratch &sc, hipStream_t s) {
-  const int64_t nseg = (int64_t)seg.size() - 1;
-  std::vector<Tile> tiles;
-  std::vector<int64_t> big_start, big_off{0};
-  int64_t maxlen = 0;
-  for (int64_t i = 0; i < nseg; i++) {
-    int64_t a = seg[i], len = seg[i + 1] - seg[i];
-    if (len <= 1) continue;
-    for (int64_t t = 0; t < len; t += kSortTile)
-      tiles.push_back(Tile{(int32_t)(a + t), (int32_t)(len - t < kSortTile ? len - t : kSortTile)});
-    if (len > kSortTile) {
-      big_start.push_back(a);
-      big_off.push_back(big_off.back() + len);
-      if (len > maxlen) maxlen = len;
-    }
+// elements of segments longer than a tile: copy back from the scratch copy
+__global__ void k_copy_big(const uint64_t *kin, const uint32_t *iin, uint64_t *kout,
+                           uint32_t *iout, const int32_t *seg, const int32_t *sid, int64_t n,
+                           const Status *st) {
+  if (failed(st)) return;
+  for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g < n;
+       g += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t s = sid[g];
+    if (seg[s + 1] - seg[s] <= kSortTile) continue;
+    kout[g] = kin[g];
+    iout[g] = iin[g];
   }
-  if (tiles.empty()) return CEL_OK;
-  Tile *dtiles;
-  CEL_TRY(sc.get(&dtiles, (int64_t)tiles.size()));
-  CEL_HIP(hipMemcpyAsync(dtiles, tiles.data(), sizeof(Tile) * tiles.size(), hipMemcpyHostToDevice,
-                         s));
-  // one launch per 65535 tiles (grid x limit kept modest)
-  for (size_t t0 = 0; t0 < tiles.size(); t0 += 65535) {
-    size_t cnt = tiles.size() - t0 < 65535 ? tiles.size() - t0 : 65535;
+}
+
+int segmented_sort(uint64_t *keys, uint32_t *ids, const int32_t *seg, int32_t nseg, int64_t n,
+                   Scratch &sc, hipStream_t s, const Status *st) {
+  if (nseg <= 0 || n <= 1) return CEL_OK;
+  int32_t *tcnt, *toff;
+  Tile *tiles;
+  const int64_t maxtiles = (int64_t)nseg + n / kSortTile + 1;
+  CEL_TRY(sc.get(&tcnt, nseg));
+  CEL_TRY(sc.get(&toff, (int64_t)nseg + 1));
+  CEL_TRY(sc.get(&tiles, maxtiles));
+  k_tile_count<<<grid_for(nseg, 256, 4096), 256, 0, s>>>(seg, nseg, tcnt, st);
+  CEL_TRY(exclusive_scan_i32(tcnt, toff, nseg, sc, s));
+  k_tile_fill<<<grid_for(nseg, 256, 4096), 256, 0, s>>>(seg, nseg, toff, tiles, st);
+  {
     KTimer kt(s, "k_sort_tiles");
-    k_sort_tiles<<<(unsigned)cnt, 256, 0, s>>>(keys, ids, dtiles + t0);
+    k_sort_tiles<<<(unsigned)maxtiles, 256, 0, s>>>(keys, ids, tiles, toff + nseg, st);
   }
-  CEL_HIP(hipGetLastError());
-  if (big_start.empty()) {
-    // the host vectors must outlive the async copies: synchronise before return
-    CEL_HIP(hipStreamSynchronize(s));
-    timing_collect();
-    return CEL_OK;
-  }
-  const int nb = (int)big_start.size();
-  const int64_t total = big_off.back();
-  int64_t *dstart, *doff;
-  CEL_TRY(sc.get(&dstart, nb));
-  CEL_TRY(sc.get(&doff, nb + 1));
-  CEL_HIP(hipMemcpyAsync(dstart, big_start.data(), sizeof(int64_t) * nb, hipMemcpyHostToDevice, s));
-  CEL_HIP(hipMemcpyAsync(doff, big_off.data(), sizeof(int64_t) * (nb + 1), hipMemcpyHostToDevice,
-                         s));
-  // ping-pong buffers addressed like the input (only large segments are used)
-  int64_t span = seg.back();
-  uint64_t *k2;
-  uint32_t *i2;
-  CEL_TRY(sc.get(&k2, span));
-  CEL_TRY(sc.get(&i2, span));
-  uint64_t *ka = keys, *kb = k2;
-  uint32_t *ia = ids, *ib = i2;
-  int passes = 0;
-  for (int64_t width = kSortTile; width < maxlen; width *= 2) {
-    KTimer kt(s, "k_merge_pass");
-    k_merge_pass<<<grid_for(total, 256, 8192), 256, 0, s>>>(ka, ia, kb, ib, dstart, doff, nb,
-                                                            width, total);
-    std::swap(ka, kb);
-    std::swap(ia, ib);
-    passes++;
-  }
-  CEL_HIP(hipGetLastError());
-  if (passes & 1) {  // result sits in the scratch copy: bring large segments back
-    for (int i = 0; i < nb; i++) {
-      int64_t a = big_start[i], len = big_off[i + 1] - big_off[i];
-      CEL_HIP(hipMemcpyAsync(keys + a, k2 + a, sizeof(uint64_t) * len, hipMemcpyDeviceToDevice, s));
-      CEL_HIP(hipMemcpyAsync(ids + a, i2 + a, sizeof(uint32_t) * len, hipMemcpyDeviceToDevice, s));
+  int passes = 0;  // enough for the longest possible segment (n)
+  while (((int64_t)kSortTile << passes) < n) passes++;
+  if (passes > 0) {
+    int32_t *sid;
+    uint64_t *k2;
+    uint32_t *i2;
+    CEL_TRY(sc.get(&sid, n));
+    CEL_TRY(sc.get(&k2, n));
+    CEL_TRY(sc.get(&i2, n));
+    k_seg_of<<<grid_for(n, 256, 8192), 256, 0, s>>>(seg, nseg, n, sid, st);
+    uint64_t *ka = keys, *kb = k2;
+    uint32_t *ia = ids, *ib = i2;
+    for (int p = 0; p < passes; p++) {
+      KTimer kt(s, "k_merge_pass");
+      k_merge_pass<<<grid_for(n, 256, 8192), 256, 0, s>>>(ka, ia, kb, ib, seg, sid, n,
+                                                           (int64_t)kSortTile << p, st);
+      std::swap(ka, kb);
+      std::swap(ia, ib);
     }
+    if (passes & 1)
+      k_copy_big<<<grid_for(n, 256, 8192), 256, 0, s>>>(k2, i2, keys, ids, seg, sid, n, st);
   }
-  CEL_HIP(hipStreamSynchronize(s));
-  timing_collect();
+  CEL_HIP(hipGetLastError());
   return CEL_OK;
 }
 

@@ -524,7 +524,7 @@ extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int3
   CEL_TRY(sc.get(&cq, n));
   CEL_TRY(sc.get(&devp, (int64_t)K * n));
   CEL_TRY(sc.get(&finp, (int64_t)K * n));
-  CEL_TRY(relabel_csr(n, order, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
+  CEL_TRY(relabel_csr(n, g->m, order, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
   k_pos_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, g->w, g->ob, d->bw, d->lat, wp, cq,
                                                     st);
   {

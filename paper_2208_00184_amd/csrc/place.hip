@@ -388,8 +388,7 @@ extern "C" int cel_place(const cel_graph *g, const cel_devices *d, const int32_t
   CEL_HIP(hipMemsetAsync(cnt, 0, sizeof(int32_t) * C, s));
   k_place_edges<1><<<eb, 256, 0, s>>>(*g, d->bw, d->lat, cluster_id, cnt, boff, keys, ids, ecost,
                                       st);
-  std::vector<int64_t> seg(hb.begin(), hb.end());
-  CEL_TRY(segmented_sort(keys, ids, seg, sc, s));
+  CEL_TRY(segmented_sort(keys, ids, boff, C, ncross, sc, s, st));
   k_place_combine<<<grid_for(C, 256, 4096), 256, 0, s>>>(C, boff, keys, ids, ecost, ca, cc, ncp,
                                                         back, st);
   {

@@ -109,14 +109,10 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
   *n_levels = L;
   if (n == 0) return CEL_OK;
   // sort each level's frontier slice by id
-  std::vector<int32_t> lp(L + 1);
-  CEL_HIP(hipMemcpyAsync(lp.data(), level_ptr, sizeof(int32_t) * (L + 1), hipMemcpyDeviceToHost, s));
-  CEL_HIP(hipStreamSynchronize(s));
-  std::vector<int64_t> seg(lp.begin(), lp.end());
   uint64_t *keys;
   CEL_TRY(sc.get(&keys, n));
   k_zero_u64<<<grid_for(n, 256, 4096), 256, 0, s>>>(keys, n);
-  CEL_TRY(segmented_sort(keys, reinterpret_cast<uint32_t *>(order_id), seg, sc, s));
+  CEL_TRY(segmented_sort(keys, reinterpret_cast<uint32_t *>(order_id), level_ptr, L, n, sc, s, st));
   CEL_HIP(hipStreamSynchronize(s));
   timing_collect();
   return CEL_OK;
