@@ -25,23 +25,41 @@ struct Pending {
   const char *name;
   hipEvent_t a, b;
 };
-thread_local std::vector<Pending> t_pending;
-thread_local std::vector<hipEvent_t> t_pool;
+// Event pairs of timed launches, resolved lazily (when statistics are read or
+// when many are pending) so that a timed call pays only for recording them.
+std::vector<Pending> g_pending;
+std::vector<hipEvent_t> g_pool;
+constexpr size_t kMaxPending = 4096;
 
-hipEvent_t take_event() {
-  if (!t_pool.empty()) {
-    hipEvent_t e = t_pool.back();
-    t_pool.pop_back();
+hipEvent_t take_event() {  // g_mu held
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
     return e;
   }
   hipEvent_t e = nullptr;
   if (hipEventCreate(&e) != hipSuccess) return nullptr;
   return e;
 }
+
+void collect_locked() {
+  for (const Pending &p : g_pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(p.b) == hipSuccess && hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
+      Tot &t = totals()[p.name];
+      t.launches++;
+      t.ms += ms;
+    }
+    g_pool.push_back(p.a);
+    g_pool.push_back(p.b);
+  }
+  g_pending.clear();
+}
 }  // namespace
 
 KTimer::KTimer(hipStream_t s, const char *name) : s_(s), name_(name) {
   if (!g_timing.load(std::memory_order_relaxed)) return;
+  std::lock_guard<std::mutex> lk(g_mu);
   a_ = take_event();
   b_ = take_event();
   if (a_ && b_) (void)hipEventRecord(a_, s_);
@@ -50,23 +68,9 @@ KTimer::KTimer(hipStream_t s, const char *name) : s_(s), name_(name) {
 KTimer::~KTimer() {
   if (!a_ || !b_) return;
   (void)hipEventRecord(b_, s_);
-  t_pending.push_back(Pending{name_, a_, b_});
-}
-
-void timing_collect() {
-  if (t_pending.empty()) return;
   std::lock_guard<std::mutex> lk(g_mu);
-  for (const Pending &p : t_pending) {
-    float ms = 0.f;
-    if (hipEventSynchronize(p.b) == hipSuccess && hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
-      Tot &t = totals()[p.name];
-      t.launches++;
-      t.ms += ms;
-    }
-    t_pool.push_back(p.a);
-    t_pool.push_back(p.b);
-  }
-  t_pending.clear();
+  g_pending.push_back(Pending{name_, a_, b_});
+  if (g_pending.size() >= kMaxPending) collect_locked();
 }
 
 }  // namespace cel
@@ -80,6 +84,7 @@ extern "C" int cel_timing(int enable) { return cel::g_timing.exchange(enable ? 1
 
 extern "C" int cel_kernel_stats(char *buf, int buflen, int reset) {
   std::lock_guard<std::mutex> lk(cel::g_mu);
+  cel::collect_locked();
   std::string out;
   int count = 0;
   for (auto &kv : cel::totals()) {

@@ -232,8 +232,8 @@ inline int grid_for(int64_t work, int block, int cap = 65535 * 4) {
 }
 
 // Optional per-kernel timing: records HIP events around one launch when
-// cel_timing(1) is on.  Pending pairs are resolved by timing_collect(), which
-// read_status() calls after its stream synchronisation.
+// cel_timing(1) is on.  Pending pairs are resolved lazily, by
+// cel_kernel_stats() or once many are pending.
 class KTimer {
  public:
   KTimer(hipStream_t s, const char *name);
@@ -246,7 +246,6 @@ class KTimer {
   const char *name_;
   hipEvent_t a_ = nullptr, b_ = nullptr;
 };
-void timing_collect();
 
 // Host-side argument checks (NULLs, sizes, device parameters).
 int check_host_graph(const cel_graph *g, const char *fn);

@@ -706,10 +706,23 @@ __global__ void __launch_bounds__(512)
         off += s_wa[w][lane];
       }
       const int32_t smin = lo_t - j0 > 0 ? lo_t - j0 : 0;
-      if (lo_hi > j0) dp_inblock<true>(best, XS, smin, j0, ein, Q, T, Cc, lane);
-      else if (ein <= 64 && __popcll(runs) <= kMaxRuns)
+      CEL_TSTAMP(tq0);
+      if (lo_hi > j0) {
+        dp_inblock<true>(best, XS, smin, j0, ein, Q, T, Cc, lane);
+        CEL_TSTAMP(tq1);
+        CEL_TADD(14, tq0, tq1);
+        CEL_TCOUNT(15);
+      } else if (ein <= 64 && __popcll(runs) <= kMaxRuns) {
         dp_inblock_runs(best, runs, j0, ein, Q, T, Cc, lane);
-      else dp_inblock<false>(best, XS, smin, j0, ein, Q, T, Cc, lane);
+        CEL_TSTAMP(tq1);
+        CEL_TADD(16, tq0, tq1);
+        CEL_TCOUNT(17);
+      } else {
+        dp_inblock<false>(best, XS, smin, j0, ein, Q, T, Cc, lane);
+        CEL_TSTAMP(tq1);
+        CEL_TADD(18, tq0, tq1);
+        CEL_TCOUNT(19);
+      }
       const int64_t G = best >> kIdxBits;
       if (j >= 1 && j <= n) P[j] = (int32_t)(best & kIdxMask) + base;
       if (j < n) s_h[rmod(j)] = G - Nt;
@@ -831,7 +844,6 @@ static int dp_blocked(int32_t n, int32_t m, int32_t R, const int32_t *lo, const 
   CEL_TRY(sc.get(&mx, 1));
   CEL_HIP(hipMemsetAsync(mx, 0, sizeof(int32_t), s));
   {
-    KTimer kt(s, "k_dp_count");
     k_dp_count<<<grid_for((int64_t)nb * 64, 256, 4096), 256, 0, s>>>(n, nb, pptr, pidx, lo, bcnt,
                                                                      mx, st);
   }
@@ -841,7 +853,6 @@ static int dp_blocked(int32_t n, int32_t m, int32_t R, const int32_t *lo, const 
   CEL_HIP(hipMemcpyAsync(hm, mx, sizeof hm, hipMemcpyDeviceToHost, s));
   CEL_HIP(hipMemcpyAsync(&total, PO + n, sizeof total, hipMemcpyDeviceToHost, s));
   CEL_HIP(hipStreamSynchronize(s));
-  timing_collect();
   if (hm[0] > kEC || total >= kPackLim) return CEL_OK;  // step-wise kernel
   int32_t *eq, *et;
   int64_t *ec, *eE;
@@ -850,7 +861,6 @@ static int dp_blocked(int32_t n, int32_t m, int32_t R, const int32_t *lo, const 
   CEL_TRY(sc.get(&ec, m));
   CEL_TRY(sc.get(&eE, m));
   {
-    KTimer kt(s, "k_dp_fill");
     k_dp_fill<<<nb < 65535 ? nb : 65535, 256, 0, s>>>(n, nb, pptr, pidx, lo, cq, boff, eq, et, ec,
                                                       eE, st);
   }

@@ -87,7 +87,6 @@ Scratch::~Scratch() {
 int read_status(const Status *dst, Status *host, hipStream_t s) {
   CEL_HIP(hipMemcpyAsync(host, dst, sizeof(Status), hipMemcpyDeviceToHost, s));
   CEL_HIP(hipStreamSynchronize(s));
-  timing_collect();
   return CEL_OK;
 }
 
@@ -460,7 +459,6 @@ int relabel_csr(int32_t n, int32_t m, const int32_t *order, const int32_t *pos,
   CEL_TRY(sc.get(&deg, n));
   k_row_deg<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, ptr, deg, st);
   CEL_TRY(exclusive_scan_i32(deg, pptr, n, sc, s));
-  KTimer kt(s, "k_relabel_rows");
   k_relabel_rows<<<edge_blocks(m), 256, 0, s>>>(n, m, order, pos, ptr, idx, pptr, pidx, st);
   CEL_HIP(hipGetLastError());
   return CEL_OK;
@@ -631,7 +629,6 @@ int segmented_sort(uint64_t *keys, uint32_t *ids, const int32_t *seg, int32_t ns
   CEL_TRY(exclusive_scan_i32(tcnt, toff, nseg, sc, s));
   k_tile_fill<<<grid_for(nseg, 256, 4096), 256, 0, s>>>(seg, nseg, toff, tiles, st);
   {
-    KTimer kt(s, "k_sort_tiles");
     k_sort_tiles<<<(unsigned)maxtiles, 256, 0, s>>>(keys, ids, tiles, toff + nseg, st);
   }
   int passes = 0;  // enough for the longest possible segment (n)
@@ -647,7 +644,6 @@ int segmented_sort(uint64_t *keys, uint32_t *ids, const int32_t *seg, int32_t ns
     uint64_t *ka = keys, *kb = k2;
     uint32_t *ia = ids, *ib = i2;
     for (int p = 0; p < passes; p++) {
-      KTimer kt(s, "k_merge_pass");
       k_merge_pass<<<grid_for(n, 256, 8192), 256, 0, s>>>(ka, ia, kb, ib, seg, sid, n,
                                                            (int64_t)kSortTile << p, st);
       std::swap(ka, kb);

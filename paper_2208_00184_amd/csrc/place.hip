@@ -64,30 +64,75 @@ __global__ void k_place_edges(cel_graph g, int64_t bw, int64_t lat, const int32_
   if (bad) raise_err(st, bad);
 }
 
-// Per target cluster: sum runs of equal source cluster into coarse in-edges
-// (written in place at the bucket's front) and raise back_cost of the source.
+// Per target cluster (one wave each): sum runs of equal source cluster into
+// coarse in-edges, written in order at the bucket's front, and raise the
+// source's back_cost.  64 bucket entries at a time: run heads from the
+// neighbouring key, a segmented sum over the wave, run tails compacted by a
+// ballot; a run that reaches the end of a batch carries into the next.
 __global__ void k_place_combine(int32_t C, const int32_t *boff, const uint64_t *keys,
                                 const uint32_t *ids, const int64_t *ecost, int32_t *ca,
                                 int64_t *cc, int32_t *ncp, uint64_t *back, const Status *st) {
   if (failed(st)) return;
-  for (int64_t b = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; b < C;
-       b += (int64_t)gridDim.x * blockDim.x) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t lt = (1ull << lane) - 1ull;
+  const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t b = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6; b < C; b += nw) {
     const int32_t k0 = boff[b], k1 = boff[b + 1];
     int32_t out = k0;
-    int32_t k = k0;
-    while (k < k1) {
-      const uint64_t a = keys[k];
-      int64_t sum = 0;
-      while (k < k1 && keys[k] == a) {
-        sum += ecost[ids[k]];
-        k++;
+    uint64_t ckey = ~0ull;  // run carried from the previous batch (none: ~0)
+    int64_t csum = 0;
+    for (int32_t base = k0; base < k1; base += 64) {
+      const int32_t k = base + lane;
+      const bool v = k < k1;
+      const uint64_t key = v ? keys[k] : ~0ull;
+      const int64_t c = v ? ecost[ids[k]] : 0;
+      const uint64_t first = __shfl(key, 0);
+      if (ckey != ~0ull && first != ckey) {  // the carried run ended with the last batch
+        if (lane == 0) {
+          ca[out] = (int32_t)ckey;
+          cc[out] = csum;
+          atomicMax((unsigned long long *)&back[ckey], (unsigned long long)csum);
+        }
+        out++;
+        ckey = ~0ull;
+        csum = 0;
       }
-      ca[out] = (int32_t)a;
-      cc[out] = sum;
-      out++;
-      atomicMax((unsigned long long *)&back[a], (unsigned long long)sum);
+      const uint64_t prev = __shfl_up(key, 1);
+      const uint64_t pk = lane == 0 ? ckey : prev;
+      const int32_t head = v && key != pk;
+      // segmented inclusive sum (segments start at heads)
+      int64_t x = c;
+      int32_t f = head;
+      for (int d = 1; d < 64; d <<= 1) {
+        const int64_t y = __shfl_up(x, d);
+        const int32_t g = __shfl_up(f, d);
+        if (lane >= d && !f) {
+          x += y;
+          f = g;
+        }
+      }
+      if (!f) x += csum;  // still in the run carried into this batch
+      const uint64_t next = __shfl_down(key, 1);
+      const bool last_valid = k1 - base <= 64 ? lane == k1 - base - 1 : lane == 63;
+      const bool more = k1 - base > 64;  // the batch's last run may continue
+      const bool tail = v && (last_valid ? !more : next != key);
+      const uint64_t tm = __ballot(tail);
+      if (tail) {
+        const int32_t o = out + __popcll(tm & lt);
+        ca[o] = (int32_t)key;
+        cc[o] = x;
+        atomicMax((unsigned long long *)&back[key], (unsigned long long)x);
+      }
+      out += __popcll(tm);
+      // carry: the run open at the end of the batch
+      const int src = k1 - base < 64 ? k1 - base - 1 : 63;
+      ckey = __shfl(key, src);
+      const int64_t xs = __shfl(x, src);
+      const bool open = more && !__shfl((int)tail, src);
+      csum = open ? xs : 0;
+      if (!open) ckey = ~0ull;
     }
-    ncp[b] = out - k0;
+    if (lane == 0) ncp[b] = out - k0;
   }
 }
 
@@ -389,8 +434,8 @@ extern "C" int cel_place(const cel_graph *g, const cel_devices *d, const int32_t
   k_place_edges<1><<<eb, 256, 0, s>>>(*g, d->bw, d->lat, cluster_id, cnt, boff, keys, ids, ecost,
                                       st);
   CEL_TRY(segmented_sort(keys, ids, boff, C, ncross, sc, s, st));
-  k_place_combine<<<grid_for(C, 256, 4096), 256, 0, s>>>(C, boff, keys, ids, ecost, ca, cc, ncp,
-                                                        back, st);
+  k_place_combine<<<grid_for((int64_t)C * 64, 256, 8192), 256, 0, s>>>(C, boff, keys, ids, ecost,
+                                                                      ca, cc, ncp, back, st);
   {
     KTimer kt(s, "k_place");
     k_place<<<1, kPlaceB, 0, s>>>(C, d->D, dcap, W, MEM, boff, ncp, ca, cc, back, cluster_dev,

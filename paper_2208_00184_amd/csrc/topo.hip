@@ -114,6 +114,5 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
   k_zero_u64<<<grid_for(n, 256, 4096), 256, 0, s>>>(keys, n);
   CEL_TRY(segmented_sort(keys, reinterpret_cast<uint32_t *>(order_id), level_ptr, L, n, sc, s, st));
   CEL_HIP(hipStreamSynchronize(s));
-  timing_collect();
   return CEL_OK;
 }
