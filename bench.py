@@ -106,6 +106,9 @@ def main() -> int:
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-batch", action="store_true",
                     help="skip the 1,024-candidate scoring row on the 200k-node DAG")
+    ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
+                    help="first copy MIB MiB device-to-device once: the reference dispatch "
+                         "that scales rocprofv3 FETCH_SIZE / WRITE_SIZE into bytes")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this benchmark runs on one GPU only (got --gpus {args.gpus}); the "
@@ -119,6 +122,15 @@ def main() -> int:
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.calib_copy > 0:
+        nb = args.calib_copy << 20
+        src = torch.ones(nb // 8, dtype=torch.int64, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] calibration copy of {args.calib_copy} MiB done", file=sys.stderr, flush=True)
+        del src, dst
     t0 = time.time()
     wl = make_config(4, args.seed)
     print(f"[bench] generated {wl.name}: n={wl.n} m={wl.m} in {time.time() - t0:.1f}s",

@@ -12,16 +12,6 @@
 
 namespace cel {
 
-// packed edge words of edges [ea, eb) (at most 512 of them), 8 per lane
-__device__ inline void load_pk8(int32_t (&pk)[8], const int32_t *w, int32_t ea, int32_t eb,
-                                int lane) {
-#pragma unroll
-  for (int q = 0; q < 8; q++) {
-    const int32_t e = ea + lane + 64 * q;
-    pk[q] = (ea + 64 * q < eb && e < eb) ? w[e] : 0;
-  }
-}
-
 constexpr int kSweepB = 1024;
 
 // per position: w and w + c (c = 0 with CEL_COMM_OFF)
@@ -38,20 +28,6 @@ __global__ void k_node_costs(int32_t n, const int32_t *order, const int64_t *w, 
   }
 }
 
-__device__ inline int64_t block_max_1024(int64_t x, int64_t *red) {
-  for (int off = 32; off > 0; off >>= 1) {
-    int64_t y = __shfl_xor(x, off);
-    x = y > x ? y : x;
-  }
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  if (lane == 0) red[wv] = x;
-  __syncthreads();
-  int64_t r = red[0];
-  for (int i = 1; i < (int)(blockDim.x >> 6); i++) r = red[i] > r ? red[i] : r;
-  __syncthreads();
-  return r;
-}
-
 // Windowed level sweep.
 //
 // REVERSE = true:  val[p] = wp[p] for a sink, else wcp[p] + max val[successor]   (eq. 3)
@@ -59,39 +35,84 @@ __device__ inline int64_t block_max_1024(int64_t x, int64_t *red) {
 //
 // Positions are processed in windows of at most kWinN consecutive positions
 // (kWinE edges, kWinL levels), from the top for REVERSE, from the bottom
-// otherwise.  Staging a window reads its rows, edge targets and -- for every
-// neighbour outside the window, whose value is already final -- that value,
-// folding those values into a per-node partial maximum in LDS, all in one
-// parallel pass; it also records each edge's owner node.  Processing then
-// walks the window level by level touching LDS only (neighbours inside the
-// window belong to earlier-processed levels of the same window): the level's
-// edges are spread over the threads (atomic max into the owner's partial, so
-// a node of high degree costs no more than one of degree one), then every
-// node forms its value.  A level with at most 64 nodes and 256 edges is run
-// by wave 0 alone with no workgroup barrier (a wave sees its own LDS writes in
-// order); wider levels use the whole block with two barriers.  A single node
-// with more than kWinE edges forms a window of its own, reduced from global
-// memory by the whole block.
-constexpr int kWinN = 2048, kWinE = 8192, kWinL = 256;
+// otherwise.  Staging a window reads its rows and edge targets.  A neighbour
+// outside the window already has its final value, which is folded into the
+// node's partial maximum in LDS right away.  Neighbours inside the window are
+// counted per node with an LDS atomic: the first kPullB of them form the
+// node's pull list (window slots), the rest (rare) become packed overflow
+// words (neighbour | owner << 16) that a per-level edge-parallel atomic max
+// applies first.  A node's value is then a few independent LDS gathers and a
+// max, unrolled to the largest pull count in its wave.  A level of at most
+// kNarrowB nodes is run by wave 0 alone in rows of 64 with no workgroup
+// barrier (a wave sees its own LDS writes in order); wider levels use the
+// whole block.  A node with more than kWinE edges forms a window of its own,
+// all of whose neighbours lie outside it.
+constexpr int kWinN = 1536, kWinE = 6144, kWinL = 256, kPullB = 6, kNarrowB = 256;
+
+template <bool REVERSE, int K>
+__device__ inline int64_t pull_max(int64_t r, const int16_t (*pw)[kWinN + 1], int32_t si,
+                                   const int64_t *s_v, const int64_t *s_wc) {
+  int32_t j[K];
+#pragma unroll
+  for (int k = 0; k < K; k++) j[k] = pw[k][si];
+#pragma unroll
+  for (int k = 0; k < K; k++) {
+    const int64_t x = REVERSE ? s_v[j[k]] : s_v[j[k]] + s_wc[j[k]];
+    r = x > r ? x : r;
+  }
+  return r;
+}
+
+// value of slot si (wave-uniform control flow; si = kWinN for idle lanes)
+template <bool REVERSE>
+__device__ inline int64_t slot_val(int32_t si, const int16_t (*pw)[kWinN + 1], const int32_t *s_pc,
+                                   const int64_t *s_pm, const int64_t *s_v, const int64_t *s_wc) {
+  const int32_t pc = s_pc[si];
+  const int64_t pm = s_pm[si], wc = s_wc[si];
+  const int32_t c = pc < kPullB ? pc : kPullB;
+  int kmax = 0;
+  while (kmax < kPullB && __ballot(c > kmax)) kmax++;
+  int64_t r;
+  switch (kmax) {
+    case 0: r = pm; break;
+    case 1: r = pull_max<REVERSE, 1>(pm, pw, si, s_v, s_wc); break;
+    case 2: r = pull_max<REVERSE, 2>(pm, pw, si, s_v, s_wc); break;
+    case 3: r = pull_max<REVERSE, 3>(pm, pw, si, s_v, s_wc); break;
+    case 4: r = pull_max<REVERSE, 4>(pm, pw, si, s_v, s_wc); break;
+    case 5: r = pull_max<REVERSE, 5>(pm, pw, si, s_v, s_wc); break;
+    default: r = pull_max<REVERSE, 6>(pm, pw, si, s_v, s_wc); break;
+  }
+  return REVERSE ? wc + r : (r > 0 ? r : 0);
+}
 
 template <bool REVERSE>
 __global__ void __launch_bounds__(kSweepB)
     k_level_sweep(int32_t n, int32_t L, const int32_t *lp, const int32_t *rptr,
                   const int32_t *ridx, const int64_t *wp, const int64_t *wcp, int64_t *val,
                   const Status *st) {
+  constexpr int32_t kNoop = (kWinN << 16) | kWinN;  // overflow word that changes nothing
   __shared__ int32_t s_lv[kWinL + 2];  // level boundaries near the cursor
   __shared__ int32_t s_rp[kWinN + 1];  // rows of the candidate window (absolute edge offsets)
-  __shared__ int32_t s_epk[kWinE];     // per edge: neighbour slot + 1 (0: outside) | owner << 16
-  __shared__ int16_t s_own[kWinE];     // owner (window-relative node) of each edge
-  __shared__ int64_t s_pm[kWinN];      // running max over neighbours, -1 if none yet
-  __shared__ int64_t s_v[kWinN];       // values computed in this window
-  __shared__ int64_t s_wc[kWinN];      // wcp (w for a sink in REVERSE) of the window's nodes
+  __shared__ int32_t s_epk[kWinE];     // overflow words (kNoop for the other edges)
+  __shared__ int16_t s_own[kWinE];     // owner (window slot) of each edge
+  __shared__ int16_t s_pw[kPullB][kWinN + 1];  // pull lists
+  __shared__ int32_t s_pc[kWinN + 1];  // in-window neighbours per slot
+  __shared__ int64_t s_pm[kWinN + 1];  // partial max over neighbours, -1 if none yet
+  __shared__ int64_t s_v[kWinN + 1];   // values computed in this window (-1 at the dummy)
+  __shared__ int64_t s_wc[kWinN + 1];  // wcp (w for a sink in REVERSE) of the window's nodes
   __shared__ int32_t s_la[kWinL], s_lb[kWinL], s_lea[kWinL], s_leb[kWinL], s_lend[kWinL];
-  __shared__ int64_t s_red[kSweepB / 64];
+  __shared__ int32_t s_lov[kWinL];
   __shared__ int32_t s_cut;
   if (failed(st)) return;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
   const bool wave0 = tid < 64;
+  if (tid == 0) {
+    s_pc[kWinN] = 0;
+    s_pm[kWinN] = -1;
+    s_v[kWinN] = -1;
+    s_wc[kWinN] = 0;
+  }
+  if (tid < kPullB) s_pw[tid][kWinN] = kWinN;
   int32_t edge_lo = REVERSE ? n : 0;   // boundary of the processed region
   int32_t lcur = REVERSE ? L - 1 : 0;  // level holding the next position to process
   while (REVERSE ? edge_lo > 0 : edge_lo < n) {
@@ -134,160 +155,160 @@ __global__ void __launch_bounds__(kSweepB)
       if (REVERSE) P0 = P1 - 1;
       else P1 = P0 + 1;
     }
-    const int32_t E0 = s_rp[P0 - Pc0], E1 = s_rp[P1 - Pc0];
+    const int32_t NN = P1 - P0;
+    const int32_t R0 = P0 - Pc0;  // row of P0 in s_rp
+    const int32_t E0 = s_rp[R0], E1 = s_rp[R0 + NN];
     CEL_TSTAMP(t1);
     CEL_TADD(REVERSE ? 0 : 16 + 0, t0, t1);
-    if (heavy) {
-      const int32_t p = P0;
-      int64_t mx = 0;  // values are >= 0; the node has > kWinE neighbours
-      for (int32_t k = E0 + tid; k < E1; k += kSweepB) {
-        const int32_t r = ridx[k];
-        const int64_t x = REVERSE ? val[r] : val[r] + wcp[r];
-        mx = x > mx ? x : mx;
-      }
-      mx = block_max_1024(mx, s_red);
-      if (tid == 0) val[p] = REVERSE ? wcp[p] + mx : mx;
-    } else {
-      const int32_t R0 = P0 - Pc0;  // row of P0 in s_rp
-      // stage nodes: costs, partials (0 for a REVERSE sink: its value is w),
-      // edge owners
-      for (int32_t i = tid; i < P1 - P0; i += kSweepB) {
-        const int32_t k0 = s_rp[R0 + i] - E0, k1 = s_rp[R0 + i + 1] - E0;
-        const bool sink = k0 == k1;
-        s_pm[i] = (REVERSE && sink) ? 0 : -1;
-        s_wc[i] = (REVERSE && sink) ? wp[P0 + i] : wcp[P0 + i];
+    // stage nodes: costs, partials (0 for a REVERSE sink: its value is w),
+    // pull counters, edge owners
+    for (int32_t i = tid; i < NN; i += kSweepB) {
+      const int32_t k0 = s_rp[R0 + i] - E0, k1 = s_rp[R0 + i + 1] - E0;
+      const bool sink = k0 == k1;
+      s_pm[i] = (REVERSE && sink) ? 0 : -1;
+      s_wc[i] = (REVERSE && sink) ? wp[P0 + i] : wcp[P0 + i];
+      s_pc[i] = 0;
+#pragma unroll
+      for (int k = 0; k < kPullB; k++) s_pw[k][i] = kWinN;  // rows gather past a short list
+      if (!heavy)
         for (int32_t q = k0; q < k1; q++) s_own[q] = (int16_t)i;
-      }
-      // per-level ranges of the window: nodes [a, b), edges [ea, eb) (window-relative)
-      for (int32_t k = tid; k < kWinL; k += kSweepB) {
-        const int32_t lb = REVERSE ? s_lv[k + 1] : s_lv[k];
-        const int32_t le = REVERSE ? s_lv[k] : s_lv[k + 1];
-        // clamp to the window: levels outside it become empty ranges at its edge
-        int32_t a = lb < P0 ? P0 : (lb > P1 ? P1 : lb);
-        const int32_t b = le < P0 ? P0 : (le > P1 ? P1 : le);
-        if (a > b) a = b;
-        s_la[k] = a - P0;
-        s_lb[k] = b - P0;
-        s_lea[k] = s_rp[a - Pc0] - E0;
-        s_leb[k] = s_rp[b - Pc0] - E0;
-        s_lend[k] = REVERSE ? (lb <= P0) : (le >= P1);
-      }
-      __syncthreads();
-      CEL_TSTAMP(t2);
-      CEL_TADD(REVERSE ? 1 : 16 + 1, t1, t2);
-      // stage edges: neighbours outside the window are final
-      for (int32_t e = E0 + tid; e < E1; e += kSweepB) {
-        const int32_t r = ridx[e];
-        const int32_t own = s_own[e - E0];
-        const bool in = REVERSE ? (r < P1) : (r >= P0);
-        s_epk[e - E0] = (in ? r - P0 + 1 : 0) | (own << 16);
-        if (!in) {
-          const int64_t x = REVERSE ? val[r] : val[r] + wcp[r];
-          atomicMax((long long *)&s_pm[own], (long long)x);
-        }
-      }
-      __syncthreads();
-      CEL_TSTAMP(t3);
-      CEL_TADD(REVERSE ? 2 : 16 + 2, t2, t3);
-      // level metadata in registers: lane l holds levels l, l+64, l+128, l+192
-      int32_t ma[4], mb[4], mea[4], meb[4], mend[4];
-#pragma unroll
-      for (int u = 0; u < 4; u++) {
-        const int k = (tid & 63) + 64 * u;
-        ma[u] = s_la[k];
-        mb[u] = s_lb[k];
-        mea[u] = s_lea[k];
-        meb[u] = s_leb[k];
-        mend[u] = s_lend[k];
-      }
-      bool synced = true;  // every wave has seen all LDS writes made so far
-      for (int32_t k = 0; k < kWinL; k++) {
-        const int u = k >> 6, ln = k & 63;
-        int32_t a, b, ea, eb, stop;
-        switch (u) {  // uniform: pick the register set, then read lane ln
-          case 0: a = ma[0]; b = mb[0]; ea = mea[0]; eb = meb[0]; stop = mend[0]; break;
-          case 1: a = ma[1]; b = mb[1]; ea = mea[1]; eb = meb[1]; stop = mend[1]; break;
-          case 2: a = ma[2]; b = mb[2]; ea = mea[2]; eb = meb[2]; stop = mend[2]; break;
-          default: a = ma[3]; b = mb[3]; ea = mea[3]; eb = meb[3]; stop = mend[3]; break;
-        }
-        a = __builtin_amdgcn_readlane(a, ln);
-        b = __builtin_amdgcn_readlane(b, ln);
-        ea = __builtin_amdgcn_readlane(ea, ln);
-        eb = __builtin_amdgcn_readlane(eb, ln);
-        stop = __builtin_amdgcn_readlane(stop, ln);
-        if (a < b) {
-          const bool narrow = (b - a <= 256) && (eb - ea <= 512);
-          CEL_TSTAMP(tl0);
-          if (narrow) {
-            CEL_TCOUNT(REVERSE ? 4 : 16 + 4);
-            if (wave0) {
-              // neighbours inside the window, up to 8 edges per lane (one packed
-              // word each: neighbour slot and owner)
-              int32_t pk[8];
-              load_pk8(pk, s_epk, ea, eb, tid);
-              int64_t x[8];
-              int32_t ow[8];
-#pragma unroll
-              for (int q = 0; q < 8; q++) {
-                ow[q] = -1;
-                x[q] = 0;
-                if (ea + 64 * q < eb) {
-                  const int32_t jp = pk[q] & 0xFFFF;
-                  const int32_t j = jp ? jp - 1 : 0;
-                  ow[q] = jp ? pk[q] >> 16 : -1;
-                  x[q] = REVERSE ? s_v[j] : s_v[j] + s_wc[j];
-                }
-              }
-#pragma unroll
-              for (int q = 0; q < 8; q++)
-                if (ow[q] >= 0) atomicMax((long long *)&s_pm[ow[q]], (long long)x[q]);
-              // a wave's LDS operations complete in issue order: no wait needed
-              lds_order();
-#pragma unroll
-              for (int q = 0; q < 4; q++) {
-                const int32_t i = a + tid + 64 * q;
-                if (a + 64 * q < b && i < b) {
-                  const int64_t pm = s_pm[i];
-                  const int64_t v = REVERSE ? s_wc[i] + pm : (pm > 0 ? pm : 0);
-                  s_v[i] = v;
-                  val[P0 + i] = v;
-                }
-              }
-              lds_order();
+    }
+    // per-level ranges of the window: nodes [a, b), edges [ea, eb) (window-relative)
+    for (int32_t k = tid; k < kWinL; k += kSweepB) {
+      const int32_t lb = REVERSE ? s_lv[k + 1] : s_lv[k];
+      const int32_t le = REVERSE ? s_lv[k] : s_lv[k + 1];
+      // clamp to the window: levels outside it become empty ranges at its edge
+      int32_t a = lb < P0 ? P0 : (lb > P1 ? P1 : lb);
+      const int32_t b = le < P0 ? P0 : (le > P1 ? P1 : le);
+      if (a > b) a = b;
+      s_la[k] = a - P0;
+      s_lb[k] = b - P0;
+      s_lea[k] = heavy ? 0 : s_rp[a - Pc0] - E0;
+      s_leb[k] = heavy ? 0 : s_rp[b - Pc0] - E0;
+      s_lend[k] = REVERSE ? (lb <= P0) : (le >= P1);
+      s_lov[k] = 0;
+    }
+    __syncthreads();
+    CEL_TSTAMP(t2);
+    CEL_TADD(REVERSE ? 1 : 16 + 1, t1, t2);
+    // stage edges: neighbours outside the window are final
+    for (int32_t e = E0 + tid; e < E1; e += kSweepB) {
+      const int32_t r = ridx[e];
+      const int32_t own = heavy ? 0 : s_own[e - E0];
+      const bool in = REVERSE ? (r < P1) : (r >= P0);
+      int32_t word = kNoop;
+      if (in) {
+        const int32_t j = r - P0;
+        const int32_t kk = atomicAdd(&s_pc[own], 1);
+        if (kk < kPullB) {
+          s_pw[kk][own] = (int16_t)j;
+        } else {
+          word = j | (own << 16);
+          // the owner's level: REVERSE levels run down the table, forward up
+          int32_t lo = 0, hi = kWinL - 1;
+          while (lo < hi) {
+            if (REVERSE) {
+              const int32_t mid = (lo + hi) >> 1;
+              if (s_la[mid] <= own) hi = mid;
+              else lo = mid + 1;
+            } else {
+              const int32_t mid = (lo + hi + 1) >> 1;
+              if (s_la[mid] <= own) lo = mid;
+              else hi = mid - 1;
             }
-            synced = false;
-            CEL_TSTAMP(tl1);
-            CEL_TADD(REVERSE ? 7 : 16 + 7, tl0, tl1);
-          } else {
-            CEL_TCOUNT(REVERSE ? 5 : 16 + 5);
-            if (!synced) __syncthreads();
-            for (int32_t e = ea + tid; e < eb; e += kSweepB) {
-              const int32_t wd = s_epk[e];
-              const int32_t jp = wd & 0xFFFF;
-              if (jp) {
-                const int32_t j = jp - 1;
+          }
+          s_lov[lo] = 1;
+        }
+      } else {
+        const int64_t x = REVERSE ? val[r] : val[r] + wcp[r];
+        atomicMax((long long *)&s_pm[own], (long long)x);
+      }
+      if (!heavy) s_epk[e - E0] = word;
+    }
+    __syncthreads();
+    CEL_TSTAMP(t3);
+    CEL_TADD(REVERSE ? 2 : 16 + 2, t2, t3);
+    // level metadata in registers: lane l holds levels l, l+64, l+128, l+192
+    int32_t ma[4], mb[4], mea[4], meb[4], mend[4];
+#pragma unroll
+    for (int u = 0; u < 4; u++) {
+      const int k = (tid & 63) + 64 * u;
+      ma[u] = s_la[k];
+      mb[u] = s_lb[k];
+      mea[u] = s_lea[k];
+      meb[u] = s_leb[k];
+      mend[u] = s_lend[k] | (s_lov[k] << 1);
+    }
+    bool synced = true;  // every wave has seen all LDS writes made so far
+    for (int32_t k = 0; k < kWinL; k++) {
+      const int u = k >> 6, ln = k & 63;
+      int32_t a, b, ea, eb, fl;
+      switch (u) {  // uniform: pick the register set, then read lane ln
+        case 0: a = ma[0]; b = mb[0]; ea = mea[0]; eb = meb[0]; fl = mend[0]; break;
+        case 1: a = ma[1]; b = mb[1]; ea = mea[1]; eb = meb[1]; fl = mend[1]; break;
+        case 2: a = ma[2]; b = mb[2]; ea = mea[2]; eb = meb[2]; fl = mend[2]; break;
+        default: a = ma[3]; b = mb[3]; ea = mea[3]; eb = meb[3]; fl = mend[3]; break;
+      }
+      a = __builtin_amdgcn_readlane(a, ln);
+      b = __builtin_amdgcn_readlane(b, ln);
+      ea = __builtin_amdgcn_readlane(ea, ln);
+      eb = __builtin_amdgcn_readlane(eb, ln);
+      fl = __builtin_amdgcn_readlane(fl, ln);
+      if (a < b) {
+        CEL_TSTAMP(tl0);
+        if (b - a <= kNarrowB) {
+          CEL_TCOUNT(REVERSE ? 4 : 16 + 4);
+          if (wave0) {
+            if (fl & 2) {  // in-window neighbours past the pull lists
+              for (int32_t e = ea + lane; e < eb; e += 64) {
+                const int32_t wd = s_epk[e];
+                const int32_t j = wd & 0xFFFF;
                 const int64_t x = REVERSE ? s_v[j] : s_v[j] + s_wc[j];
                 atomicMax((long long *)&s_pm[wd >> 16], (long long)x);
               }
+              lds_order();
             }
-            __syncthreads();
-            for (int32_t i = a + tid; i < b; i += kSweepB) {
-              const int64_t pm = s_pm[i];
-              const int64_t v = REVERSE ? s_wc[i] + pm : (pm > 0 ? pm : 0);
-              s_v[i] = v;
-              val[P0 + i] = v;
+            for (int32_t r0 = a; r0 < b; r0 += 64) {
+              const int32_t s = r0 + lane;
+              const bool act = s < b;
+              const int64_t v = slot_val<REVERSE>(act ? s : kWinN, s_pw, s_pc, s_pm, s_v, s_wc);
+              if (act) {
+                s_v[s] = v;
+                val[P0 + s] = v;
+              }
+              lds_order();
             }
-            __syncthreads();
-            synced = true;
-            CEL_TSTAMP(tl1);
-            CEL_TADD(REVERSE ? 8 : 16 + 8, tl0, tl1);
           }
+          synced = false;
+          CEL_TSTAMP(tl1);
+          CEL_TADD(REVERSE ? 7 : 16 + 7, tl0, tl1);
+        } else {
+          CEL_TCOUNT(REVERSE ? 5 : 16 + 5);
+          if (!synced) __syncthreads();
+          if (fl & 2) {
+            for (int32_t e = ea + tid; e < eb; e += kSweepB) {
+              const int32_t wd = s_epk[e];
+              const int32_t j = wd & 0xFFFF;
+              const int64_t x = REVERSE ? s_v[j] : s_v[j] + s_wc[j];
+              atomicMax((long long *)&s_pm[wd >> 16], (long long)x);
+            }
+            __syncthreads();
+          }
+          for (int32_t i = a + tid; i < b; i += kSweepB) {
+            const int64_t v = slot_val<REVERSE>(i, s_pw, s_pc, s_pm, s_v, s_wc);
+            s_v[i] = v;
+            val[P0 + i] = v;
+          }
+          __syncthreads();
+          synced = true;
+          CEL_TSTAMP(tl1);
+          CEL_TADD(REVERSE ? 8 : 16 + 8, tl0, tl1);
         }
-        if (stop) break;  // the window ends inside this level
       }
-      CEL_TSTAMP(t4);
-      CEL_TADD(REVERSE ? 3 : 16 + 3, t3, t4);
+      if (fl & 1) break;  // the window ends inside this level
     }
+    CEL_TSTAMP(t4);
+    CEL_TADD(REVERSE ? 3 : 16 + 3, t3, t4);
     // advance the cursor to the level holding the next unprocessed position
     // (s_lv still covers every level the window touched)
     if (REVERSE) {
@@ -377,7 +398,7 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
   CEL_TRY(sc.get(&tmp, n));
   CEL_TRY(sc.get(&pos, n));
   CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
-  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, s));
+  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, sc, s));
   CEL_TRY(check_level_order(g, order_id, level, level_ptr, L, pos, st, s));
   CEL_TRY(sc.get(&sptr, (int64_t)n + 1));
   CEL_TRY(sc.get(&sidx, g->m));

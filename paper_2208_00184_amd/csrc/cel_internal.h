@@ -204,10 +204,16 @@ int set_error(int code, const char *fmt, ...);
     if (rc_ != CEL_OK) return rc_; \
   } while (0)
 
-// Stream-ordered scratch allocations, all returned when the object dies.
+// Scratch memory of one call: sub-allocations from a per-(device, stream)
+// arena of device blocks that persist across calls, so a call costs no
+// allocator round trip once the arena has grown to its working size.  The
+// arena is held for the object's lifetime, so calls on one stream from
+// several host threads take turns; calls on different streams use different
+// arenas.  Pointers stay valid until the object dies.
+struct Arena;
 class Scratch {
  public:
-  explicit Scratch(hipStream_t s) : s_(s) {}
+  explicit Scratch(hipStream_t s);
   ~Scratch();
   Scratch(const Scratch &) = delete;
   Scratch &operator=(const Scratch &) = delete;
@@ -220,7 +226,8 @@ class Scratch {
 
  private:
   hipStream_t s_;
-  std::vector<void *> ptrs_;
+  Arena *a_ = nullptr;
+  int err_ = CEL_OK;
 };
 
 // Launch-configuration helpers
@@ -258,7 +265,7 @@ int check_host_devices(const cel_devices *d, const char *fn);
 // sum(w) + sum over edges of c[src] < 2^62.  Fills indeg_scratch (n ints)
 // with in-degrees counted from the CSR.  Raises EB_ARG / EB_OVERFLOW in st.
 int check_graph(const cel_graph *g, int64_t bw, int64_t lat, bool bound, Status *st,
-                int32_t *indeg_scratch, hipStream_t s);
+                int32_t *indeg_scratch, Scratch &sc, hipStream_t s);
 
 // Checks that `order` is a permutation of 0..n-1 consistent with level /
 // level_ptr (level-monotone) and that level[u] < level[v] on every edge.

@@ -906,7 +906,7 @@ extern "C" int cel_cluster(const cel_graph *g, const cel_devices *d, const int32
   CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
   CEL_TRY(sc.get(&tmp, n));
   CEL_TRY(sc.get(&pos, n));
-  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, s));
+  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, sc, s));
   CEL_TRY(check_topo_order(g, order, pos, st, s));
   if (n == 0) {
     Status h;

@@ -2,7 +2,10 @@
 // prefix scans, CSR relabelling into position space and a segmented sort.
 #include <cstdarg>
 #include <cstring>
+#include <map>
 #include <mutex>
+#include <utility>
+#include <vector>
 
 #include "cel_internal.h"
 
@@ -53,35 +56,78 @@ int check_host_devices(const cel_devices *d, const char *fn) {
 
 // ----------------------------------------------------------------- scratch
 
-static void keep_pool_warm(int dev) {
-  static std::mutex mu;
-  static bool done[64] = {};
-  std::lock_guard<std::mutex> lk(mu);
-  if (dev < 0 || dev >= 64 || done[dev]) return;
-  hipMemPool_t pool;
-  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
-    uint64_t thr = UINT64_MAX;  // keep freed blocks in the pool between calls
-    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+struct Arena {
+  std::mutex mu;  // held by the Scratch object of the running call
+  std::vector<std::pair<char *, size_t>> blocks;
+  size_t blk = 0, off = 0;  // bump position of the running call
+  size_t need = 0;          // bytes the running call asked for in total
+  size_t grow_to = 0;       // one block of this size replaces the chain at the next call
+};
+
+static std::mutex g_arenas_mu;
+static std::map<std::pair<int, hipStream_t>, Arena *> g_arenas;
+constexpr size_t kAlign = 256;
+constexpr size_t kMinBlock = size_t(8) << 20;
+
+Scratch::Scratch(hipStream_t s) : s_(s) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    err_ = set_error(CEL_E_HIP, "hipGetDevice failed");
+    return;
   }
-  done[dev] = true;
+  {
+    std::lock_guard<std::mutex> lk(g_arenas_mu);
+    Arena *&a = g_arenas[{dev, s}];
+    if (!a) a = new Arena();  // kept until the process ends
+    a_ = a;
+  }
+  a_->mu.lock();
+  a_->blk = a_->off = a_->need = 0;
+  if (a_->grow_to > 0) {
+    // the last call spilled into several blocks: replace them by one that
+    // fits it, once the stream has drained (earlier kernels may use them)
+    if (hipStreamSynchronize(s_) != hipSuccess) {
+      err_ = set_error(CEL_E_HIP, "hipStreamSynchronize failed");
+      return;
+    }
+    for (auto &b : a_->blocks) (void)hipFree(b.first);
+    a_->blocks.clear();
+    void *p = nullptr;
+    if (hipMalloc(&p, a_->grow_to) != hipSuccess || !p) {
+      err_ = set_error(CEL_E_NOMEM, "scratch arena of %zu bytes: allocation failed", a_->grow_to);
+      a_->grow_to = 0;
+      return;
+    }
+    a_->blocks.push_back({(char *)p, a_->grow_to});
+    a_->grow_to = 0;
+  }
 }
 
 int Scratch::raw(void **out, size_t bytes) {
-  int dev = 0;
-  CEL_HIP(hipGetDevice(&dev));
-  keep_pool_warm(dev);
-  void *p = nullptr;
-  hipError_t e = hipMallocAsync(&p, bytes, s_);
-  if (e != hipSuccess || !p)
-    return set_error(CEL_E_NOMEM, "scratch allocation of %zu bytes failed: %s", bytes,
-                     hipGetErrorString(e));
-  ptrs_.push_back(p);
-  *out = p;
+  if (err_ != CEL_OK) return err_;
+  const size_t sz = (bytes + kAlign - 1) / kAlign * kAlign;
+  a_->need += sz;
+  while (a_->blk < a_->blocks.size() && a_->off + sz > a_->blocks[a_->blk].second) {
+    a_->blk++;
+    a_->off = 0;
+  }
+  if (a_->blk == a_->blocks.size()) {  // grow: a new block at the end of the chain
+    const size_t bsz = sz > kMinBlock ? sz : kMinBlock;
+    void *p = nullptr;
+    if (hipMalloc(&p, bsz) != hipSuccess || !p)
+      return err_ = set_error(CEL_E_NOMEM, "scratch allocation of %zu bytes failed", bytes);
+    a_->blocks.push_back({(char *)p, bsz});
+    a_->off = 0;
+  }
+  *out = a_->blocks[a_->blk].first + a_->off;
+  a_->off += sz;
   return CEL_OK;
 }
 
 Scratch::~Scratch() {
-  for (void *p : ptrs_) (void)hipFreeAsync(p, s_);
+  if (!a_) return;
+  if (a_->blocks.size() > 1) a_->grow_to = a_->need;
+  a_->mu.unlock();
 }
 
 int read_status(const Status *dst, Status *host, hipStream_t s) {
@@ -209,23 +255,21 @@ __global__ void k_finish_overflow(const uint64_t *part, int np, Status *st) {
 }
 
 int check_graph(const cel_graph *g, int64_t bw, int64_t lat, bool bound, Status *st,
-                int32_t *indeg, hipStream_t s) {
+                int32_t *indeg, Scratch &sc, hipStream_t s) {
   const int B = 256;
   const int nbk = grid_for((int64_t)g->n + 1, B, 2048);
   uint64_t *part;
-  CEL_HIP(hipMallocAsync((void **)&part, sizeof(uint64_t) * nbk, s));
+  CEL_TRY(sc.get(&part, nbk));
   k_check_nodes<<<nbk, B, 0, s>>>(*g, bw, lat, st, part);
   if (g->n > 0) {
     uint64_t *hsum;
-    CEL_HIP(hipMallocAsync((void **)&hsum, sizeof(uint64_t) * (size_t)g->n, s));
+    CEL_TRY(sc.get(&hsum, g->n));
     CEL_HIP(hipMemsetAsync(indeg, 0, sizeof(int32_t) * (size_t)g->n, s));
     CEL_HIP(hipMemsetAsync(hsum, 0, sizeof(uint64_t) * (size_t)g->n, s));
     k_check_csr<<<edge_blocks(g->m), B, 0, s>>>(*g, st, indeg, hsum);
     k_check_csc<<<grid_for(g->n, B, 4096), B, 0, s>>>(*g, st, indeg, hsum);
-    CEL_HIP(hipFreeAsync(hsum, s));
   }
   if (bound) k_finish_overflow<<<1, B, 0, s>>>(part, nbk, st);
-  CEL_HIP(hipFreeAsync(part, s));
   CEL_HIP(hipGetLastError());
   return CEL_OK;
 }

@@ -462,6 +462,423 @@ __global__ void __launch_bounds__(B)
   }
 }
 
+// ---------------------------------------------------------------------------
+// Single placement (K = 1) over the device-grouped order.
+//
+// Inside every level the nodes are sorted by device, priority order kept
+// within a device, so each device's FIFO chain in a level is one run of
+// consecutive slots.  With S(i) the sum of w over the run up to and including
+// slot i and Sx(i) = S(i) - w(i), the chain x -> max(ready + w, x + w)
+// unrolls to
+//   fin(i) = S(i) + max(free(d) - Sx(h), max over h <= j <= i of (ready(j) - Sx(j)))
+// where h is the run's first slot in the window and free(d) the device's
+// free time before it: a segmented prefix maximum.  k_runs precomputes Sx,
+// the distance from each slot to its run's first slot and the run ends, so
+// the sweep needs neither a partition nor a scan of maps.
+//
+// Windows of up to NC consecutive slots (EC in-edges, kMsL levels) are staged
+// into LDS.  Predecessors before the window are final and are folded into a
+// partial ready time per slot.  Predecessors inside the window are counted
+// per slot with an LDS atomic: the first kPull form the slot's pull list
+// (predecessor slot, bit 12 = devices differ), so ready() is a few
+// independent LDS gathers and a max, unrolled to the largest pull count of
+// the row; the rest (rare) are applied per level beforehand by an
+// edge-parallel atomic max.  A level part of at most kNarrow slots is run
+// by wave 0 in rows of 64 without workgroup barriers, the prefix maximum of a
+// run that crosses rows carried in from lane 63; wider parts use the block.
+constexpr int kPull = 6;
+constexpr int kNarrow = 256;
+
+// One step of the segmented prefix max: take the value of the lane selected
+// by CTRL when `ok` (that lane lies in the same run); lanes the DPP move does
+// not reach read the identity.
+template <int CTRL, int ROWMASK>
+__device__ inline void pmax_step(int64_t &y, bool ok) {
+  const int32_t lo = __builtin_amdgcn_update_dpp((int32_t)kNeg, (int32_t)y, CTRL, ROWMASK, 0xF, false);
+  const int32_t hi =
+      __builtin_amdgcn_update_dpp((int32_t)(kNeg >> 32), (int32_t)(y >> 32), CTRL, ROWMASK, 0xF, false);
+  const int64_t u = (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+  y = (ok && u > y) ? u : y;
+}
+
+// Inclusive prefix max over the run of every lane inside the wave's 64 lanes;
+// hd = distance from the lane's slot to its run's first slot.
+__device__ inline int64_t wave_seg_pmax(int64_t y, int32_t hd, int lane) {
+  pmax_step<0x111, 0xF>(y, hd >= 1);               // row_shr:1
+  pmax_step<0x112, 0xF>(y, hd >= 2);               // row_shr:2
+  pmax_step<0x114, 0xF>(y, hd >= 4);               // row_shr:4
+  pmax_step<0x118, 0xF>(y, hd >= 8);               // row_shr:8
+  pmax_step<0x142, 0xA>(y, hd >= (lane & 15) + 1);  // row_bcast:15 into rows 1 and 3
+  pmax_step<0x143, 0xC>(y, hd >= lane - 31);        // row_bcast:31 into rows 2 and 3
+  return y;
+}
+
+// max of r and the first K pull gathers of slot si (finish + comm if the
+// devices differ)
+template <int NC, int K>
+__device__ inline int64_t ms_pull(int64_t r, const int16_t (*pw)[NC + 1], int32_t si,
+                                  const int64_t *s_f, const int64_t *s_c) {
+  int32_t wd[K];
+#pragma unroll
+  for (int k = 0; k < K; k++) wd[k] = pw[k][si];
+#pragma unroll
+  for (int k = 0; k < K; k++) {
+    const int32_t j = wd[k] & 0xFFF;
+    const int64_t f = s_f[j], c = s_c[j];
+    const int64_t x = f + (((wd[k] >> 12) & 1) ? c : 0);
+    r = x > r ? x : r;
+  }
+  return r;
+}
+
+__device__ inline int64_t readlane64(int64_t v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int32_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int32_t)(v >> 32), l);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Run structure of the device-grouped order, per slot s: sx = exclusive sum
+// of w over the slot's run, meta = device | run ends here << 8 |
+// min(distance to the run's first slot, 32767) << 16.
+__global__ void k_runs(int32_t n, const int32_t *lp, const int32_t *level, const int32_t *gorder,
+                       const uint8_t *gdev, const int64_t *wx, int64_t *sx, int32_t *meta,
+                       const Status *st) {
+  if (failed(st)) return;
+  for (int32_t s = blockIdx.x * blockDim.x + threadIdx.x; s < n; s += gridDim.x * blockDim.x) {
+    const int32_t l = level[gorder[s]];
+    const int32_t lo = lp[l], hi = lp[l + 1];
+    const int d = gdev[s];
+    int32_t a = lo, b = s;  // first slot of the level with device d (devices ascend)
+    while (a < b) {
+      const int32_t mid = (a + b) >> 1;
+      if (gdev[mid] < d) a = mid + 1;
+      else b = mid;
+    }
+    sx[s] = wx[s] - wx[a];
+    const int32_t hd = s - a < 32767 ? s - a : 32767;
+    const int tl = (s + 1 == hi) || gdev[s + 1] != d;
+    meta[s] = d | (tl << 8) | (hd << 16);
+  }
+}
+
+template <int B, int NC, int EC>
+__global__ void __launch_bounds__(B)
+    k_makespan_one(int32_t n, int32_t L, const int32_t *lp, const int32_t *pptr,
+                   const int32_t *pidx, const int64_t *wp, const int64_t *cq, const uint8_t *devp,
+                   const int64_t *sxp, const int32_t *metap, int64_t *finp, int64_t *makespan,
+                   const Status *st) {
+  constexpr int NW = B / 64;
+  constexpr int F = kPull;
+  static_assert(NC < 4095 && EC < 32768, "slot fields are 12 bits");
+  constexpr int32_t kNoop = (NC << 16) | NC;  // overflow word that changes nothing
+  __shared__ int32_t s_lv[kMsL + 2];
+  __shared__ int32_t s_rp[NC + 1];
+  __shared__ int32_t s_epk[EC + 1];
+  __shared__ int16_t s_own[EC];
+  __shared__ int64_t s_pm[NC + 1], s_f[NC + 1], s_w[NC + 1], s_c[NC + 1], s_sx[NC + 1];
+  __shared__ int32_t s_meta[NC + 1];
+  __shared__ int16_t s_pw[F][NC + 1];
+  __shared__ int32_t s_pc[NC + 1];
+  __shared__ int32_t s_la[kMsL], s_lb[kMsL], s_lea[kMsL], s_leb[kMsL], s_lend[kMsL];
+  __shared__ int32_t s_lov[kMsL];
+  __shared__ int64_t s_avail[256];
+  __shared__ int64_t s_wy[2][NW], s_cy[2];
+  __shared__ int64_t s_red[NW];
+  __shared__ int32_t s_cut;
+  if (failed(st)) return;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const bool wave0 = tid < 64;
+  for (int i = tid; i < 256; i += B) s_avail[i] = 0;
+  if (tid == 0) {
+    s_epk[EC] = kNoop;
+    s_pm[NC] = 0;
+    s_f[NC] = 0;
+    s_w[NC] = 0;
+    s_c[NC] = 0;
+    s_sx[NC] = 0;
+    s_meta[NC] = 0;
+    s_pc[NC] = 0;
+    for (int k = 0; k < F; k++) s_pw[k][NC] = NC;
+  }
+  // ready() of a slot: partial from before the window, pull gathers; the
+  // value y = ready - Sx of the prefix max (with the device's free time at a
+  // run's first slot), and base = Sx + w
+  auto slot_value = [&](int32_t si, int64_t &y, int32_t &meta, int64_t &base) {
+    const int64_t pm = s_pm[si], w = s_w[si], sx = s_sx[si];
+    meta = s_meta[si];
+    const int32_t pc = s_pc[si];
+    const int64_t av = s_avail[meta & 255];
+    const int32_t cpc = pc < F ? pc : F;
+    int kmax = 0;
+    while (kmax < F && __ballot(cpc > kmax)) kmax++;
+    int64_t r;
+    switch (kmax) {
+      case 0: r = pm; break;
+      case 1: r = ms_pull<NC, 1>(pm, s_pw, si, s_f, s_c); break;
+      case 2: r = ms_pull<NC, 2>(pm, s_pw, si, s_f, s_c); break;
+      case 3: r = ms_pull<NC, 3>(pm, s_pw, si, s_f, s_c); break;
+      case 4: r = ms_pull<NC, 4>(pm, s_pw, si, s_f, s_c); break;
+      case 5: r = ms_pull<NC, 5>(pm, s_pw, si, s_f, s_c); break;
+      default: r = ms_pull<NC, 6>(pm, s_pw, si, s_f, s_c); break;
+    }
+    y = r - sx;
+    const int64_t viafree = av - sx;
+    if ((meta >> 16) == 0 && viafree > y) y = viafree;
+    base = sx + w;
+    asm volatile("" : "+v"(base));  // formed here, off the dependent chain after the scan
+  };
+  int64_t mk = 0;
+  int32_t P0 = 0, lcur = 0;
+  while (P0 < n) {
+    CEL_TSTAMP(t0);
+    CEL_TCOUNT(6);
+    const int32_t Pc1 = P0 + NC < n ? P0 + NC : n;
+    for (int t = tid; t <= Pc1 - P0; t += B) s_rp[t] = pptr[P0 + t];
+    for (int k = tid; k <= kMsL + 1; k += B) {
+      const int32_t l = lcur + k;  // level lcur + k is [s_lv[k], s_lv[k+1])
+      s_lv[k] = lp[l > L ? L : l];
+    }
+    if (tid == 0) s_cut = 0;
+    __syncthreads();
+    int32_t cnt = 0;
+    for (int t = tid; t < Pc1 - P0; t += B) cnt += (s_rp[t + 1] - s_rp[0] <= EC) ? 1 : 0;
+    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
+    if (lane == 0 && cnt) atomicAdd(&s_cut, cnt);
+    __syncthreads();
+    int32_t P1 = P0 + s_cut;
+    const int32_t lvcap = (lcur + kMsL < L) ? s_lv[kMsL] : n;
+    if (P1 > lvcap) P1 = lvcap;
+    const bool heavy = (P1 == P0);  // one node with more than EC predecessors
+    if (heavy) P1 = P0 + 1;
+    const int32_t NN = P1 - P0;
+    const int32_t E0 = s_rp[0], E1 = s_rp[NN];
+    for (int32_t i = tid; i < NN; i += B) {
+      const int32_t p = P0 + i;
+      const int32_t mt = metap[p];
+      int32_t hd = mt >> 16;
+      hd = hd < i ? hd : i;  // the window's first slot starts a run part ...
+      const int32_t tl = ((mt >> 8) & 1) | (i == NN - 1);  // ... and its last slot ends one
+      s_meta[i] = (mt & 255) | (tl << 8) | (hd << 16);
+      s_w[i] = wp[p];
+      s_c[i] = cq[p];
+      s_sx[i] = sxp[p];
+      s_pm[i] = 0;
+      s_pc[i] = 0;
+#pragma unroll
+      for (int k = 0; k < F; k++) s_pw[k][i] = NC;  // rows gather past a short list
+      if (!heavy)
+        for (int32_t q = s_rp[i] - E0; q < s_rp[i + 1] - E0; q++) s_own[q] = (int16_t)i;
+    }
+    for (int32_t k = tid; k < kMsL; k += B) {
+      const int32_t lb = s_lv[k], le = s_lv[k + 1];
+      int32_t a = lb < P0 ? P0 : (lb > P1 ? P1 : lb);
+      const int32_t b = le < P0 ? P0 : (le > P1 ? P1 : le);
+      if (a > b) a = b;
+      s_la[k] = a - P0;
+      s_lb[k] = b - P0;
+      s_lea[k] = heavy ? 0 : s_rp[a - P0] - E0;
+      s_leb[k] = heavy ? 0 : s_rp[b - P0] - E0;
+      s_lend[k] = le >= P1;
+      s_lov[k] = 0;
+    }
+    __syncthreads();
+    CEL_TSTAMP(t1);
+    CEL_TADD(0, t0, t1);
+    // in-edges: pull lists and overflow words; predecessors before the window
+    // are final and are folded into the owner's partial ready time
+    for (int32_t e = E0 + tid; e < E1; e += B) {
+      const int32_t q = pidx[e];
+      const int32_t own = heavy ? 0 : s_own[e - E0];
+      const int dvo = s_meta[own] & 255;
+      int32_t word = kNoop;
+      if (q >= P0) {  // never for a heavy window: its predecessors all precede it
+        const int32_t j = q - P0;
+        const int32_t pwd = j | ((int32_t)((s_meta[j] & 255) != dvo) << 12);
+        const int32_t kk = atomicAdd(&s_pc[own], 1);
+        if (kk < F) {
+          s_pw[kk][own] = (int16_t)pwd;
+        } else {
+          word = pwd | (own << 16);
+          int32_t lo = 0, hi = kMsL - 1;  // the owner's level: last k with s_lv[k] <= P0 + own
+          while (lo < hi) {
+            const int32_t mid = (lo + hi + 1) >> 1;
+            if (s_lv[mid] <= P0 + own) lo = mid;
+            else hi = mid - 1;
+          }
+          s_lov[lo] = 1;
+        }
+      } else {
+        const int64_t x = finp[q] + (devp[q] != dvo ? cq[q] : 0);
+        atomicMax((long long *)&s_pm[own], (long long)x);
+      }
+      if (!heavy) s_epk[e - E0] = word;
+    }
+    __syncthreads();
+    CEL_TSTAMP(t2);
+    CEL_TADD(1, t1, t2);
+    int32_t ma[4], mb[4], mea[4], meb[4], mend[4];
+#pragma unroll
+    for (int u = 0; u < 4; u++) {
+      const int k = lane + 64 * u;
+      ma[u] = s_la[k];
+      mb[u] = s_lb[k];
+      mea[u] = s_lea[k];
+      meb[u] = s_leb[k];
+      mend[u] = s_lend[k] | (s_lov[k] << 1);
+    }
+    bool synced = true;
+    CEL_TSTAMP(t3);
+    CEL_TADD(2, t2, t3);
+    for (int32_t k = 0; k < kMsL; k++) {
+      const int u = k >> 6, ln = k & 63;
+      int32_t a0, b0, ea, eb, fl;
+      switch (u) {
+        case 0: a0 = ma[0]; b0 = mb[0]; ea = mea[0]; eb = meb[0]; fl = mend[0]; break;
+        case 1: a0 = ma[1]; b0 = mb[1]; ea = mea[1]; eb = meb[1]; fl = mend[1]; break;
+        case 2: a0 = ma[2]; b0 = mb[2]; ea = mea[2]; eb = meb[2]; fl = mend[2]; break;
+        default: a0 = ma[3]; b0 = mb[3]; ea = mea[3]; eb = meb[3]; fl = mend[3]; break;
+      }
+      a0 = __builtin_amdgcn_readlane(a0, ln);
+      b0 = __builtin_amdgcn_readlane(b0, ln);
+      ea = __builtin_amdgcn_readlane(ea, ln);
+      eb = __builtin_amdgcn_readlane(eb, ln);
+      fl = __builtin_amdgcn_readlane(fl, ln);
+      if (a0 < b0) {
+        CEL_TSTAMP(tl0);
+        if (b0 - a0 <= kNarrow) {
+          if (wave0) {
+            if (fl & 2) {  // in-edges past the pull lists
+              for (int32_t e = ea + lane; e < eb; e += 64) {
+                const int32_t wd = s_epk[e];
+                const int32_t j = wd & 0xFFF;
+                const int64_t x = s_f[j] + (((wd >> 12) & 1) ? s_c[j] : 0);
+                atomicMax((long long *)&s_pm[(wd >> 16) & 0xFFF], (long long)x);
+              }
+              lds_order();
+            }
+            int64_t carry = kNeg;
+            for (int32_t r0 = a0; r0 < b0; r0 += 64) {
+              CEL_TCOUNT(11);
+              const int32_t s = r0 + lane;
+              const bool act = s < b0;
+              int64_t y, base;
+              int32_t meta;
+              slot_value(act ? s : NC, y, meta, base);
+              const int32_t hd = meta >> 16;
+              y = wave_seg_pmax(y, hd, lane);
+              if (hd > lane && carry > y) y = carry;  // the run began in an earlier row
+              const int64_t fin = base + y;
+              if (act) {
+                s_f[s] = fin;
+                finp[P0 + s] = fin;
+                mk = fin > mk ? fin : mk;
+                if (meta & 256) s_avail[meta & 255] = fin;
+              }
+              carry = readlane64(y, 63);
+              lds_order();
+            }
+          }
+          synced = false;
+          CEL_TSTAMP(tl1);
+          CEL_TADD(7, tl0, tl1);
+          CEL_TCOUNT(4);
+        } else {
+          if (!synced) __syncthreads();
+          if (fl & 2) {
+            for (int32_t e = ea + tid; e < eb; e += B) {
+              const int32_t wd = s_epk[e];
+              const int32_t j = wd & 0xFFF;
+              const int64_t x = s_f[j] + (((wd >> 12) & 1) ? s_c[j] : 0);
+              atomicMax((long long *)&s_pm[(wd >> 16) & 0xFFF], (long long)x);
+            }
+            __syncthreads();
+          }
+          if (tid == 0) s_cy[0] = kNeg;
+          int par = 0;
+          for (int32_t base0 = a0; base0 < b0; base0 += B) {
+            const int32_t s = base0 + tid;
+            const bool act = s < b0;
+            int64_t y, base;
+            int32_t meta;
+            slot_value(act ? s : NC, y, meta, base);
+            const int32_t hd = meta >> 16;
+            y = wave_seg_pmax(y, hd, lane);
+            if (lane == 63) s_wy[par][wv] = y;
+            __syncthreads();
+            if (hd > lane) {  // the run began before this wave's row
+              const int32_t hs = s - hd;
+              int64_t cy = kNeg;
+              for (int w2 = wv - 1; w2 >= 0 && base0 + 64 * w2 + 63 >= hs; w2--)
+                cy = s_wy[par][w2] > cy ? s_wy[par][w2] : cy;
+              if (hs < base0 && s_cy[par] > cy) cy = s_cy[par];
+              y = cy > y ? cy : y;
+            }
+            const int64_t fin = base + y;
+            if (act) {
+              s_f[s] = fin;
+              finp[P0 + s] = fin;
+              mk = fin > mk ? fin : mk;
+              if (meta & 256) s_avail[meta & 255] = fin;
+              if (tid == B - 1) s_cy[par ^ 1] = y;
+            }
+            par ^= 1;
+          }
+          __syncthreads();
+          synced = true;
+          CEL_TSTAMP(tl1);
+          CEL_TADD(8, tl0, tl1);
+          CEL_TCOUNT(5);
+        }
+      }
+      if (fl & 1) break;  // the window ends inside this level
+    }
+    CEL_TSTAMP(t4);
+    CEL_TADD(3, t3, t4);
+    if (P1 < n) {
+      int32_t k = 0;
+      while (k < kMsL && lcur + k + 1 < L && s_lv[k + 1] <= P1) k++;
+      lcur += k;
+    }
+    P0 = P1;
+    __syncthreads();
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const int64_t y = __shfl_xor(mk, off);
+    mk = y > mk ? y : mk;
+  }
+  if (lane == 0) s_red[wv] = mk;
+  __syncthreads();
+  if (tid == 0) {
+    int64_t r = s_red[0];
+    for (int i = 1; i < NW; i++) r = s_red[i] > r ? s_red[i] : r;
+    makespan[0] = r;
+  }
+}
+
+// keys for the device-grouped order: device of each position, id = position
+__global__ void k_dev_keys(int32_t n, const uint8_t *devp, uint64_t *keys, uint32_t *ids,
+                           const Status *st) {
+  if (failed(st)) return;
+  for (int32_t p = blockIdx.x * blockDim.x + threadIdx.x; p < n; p += gridDim.x * blockDim.x) {
+    keys[p] = devp[p];
+    ids[p] = (uint32_t)p;
+  }
+}
+
+// grouped order: node, device and inverse position of every slot
+__global__ void k_grouped(int32_t n, const int32_t *order, const uint32_t *sig,
+                          const uint8_t *devp, int32_t *gorder, int32_t *gpos, uint8_t *gdev,
+                          const Status *st) {
+  if (failed(st)) return;
+  for (int32_t s = blockIdx.x * blockDim.x + threadIdx.x; s < n; s += gridDim.x * blockDim.x) {
+    const uint32_t p = sig[s];
+    const int32_t v = order[p];
+    gorder[s] = v;
+    gpos[v] = s;
+    gdev[s] = devp[p];
+  }
+}
+
 // finish/start by node id from position-space finishes
 __global__ void k_makespan_out(int32_t K, int32_t n, const int32_t *order, const int64_t *finp,
                                const int64_t *wp, int64_t *start, int64_t *finish,
@@ -516,7 +933,7 @@ extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int3
   }
   CEL_TRY(sc.get(&tmp, n));
   CEL_TRY(sc.get(&pos, n));
-  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, s));
+  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, sc, s));
   CEL_TRY(check_level_order(g, order, level, level_ptr, L, pos, st, s));
   CEL_TRY(sc.get(&pptr, (int64_t)n + 1));
   CEL_TRY(sc.get(&pidx, g->m));
@@ -524,35 +941,72 @@ extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int3
   CEL_TRY(sc.get(&cq, n));
   CEL_TRY(sc.get(&devp, (int64_t)K * n));
   CEL_TRY(sc.get(&finp, (int64_t)K * n));
-  CEL_TRY(relabel_csr(n, g->m, order, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
-  k_pos_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, g->w, g->ob, d->bw, d->lat, wp, cq,
-                                                    st);
-  {
-    const int gx = grid_for(n, 256, 1024);
-    const int gy = K < 1024 ? K : 1024;
-    KTimer kt(s, "k_dev_gather");
-    k_dev_gather<<<dim3(gx, gy), 256, 0, s>>>(K, n, order, node_dev, d->D, devp, st);
-  }
-  int dbits = 0;  // bits of the largest device id
-  while ((1 << dbits) < d->D) dbits++;
+  const int gx = grid_for(n, 256, 1024);
   if (K == 1) {
-    KTimer kt(s, "k_makespan_sweep");
-    k_makespan_sweep<1024, 1536, 6144><<<1, 1024, 0, s>>>(n, L, dbits, level_ptr, pptr, pidx, wp, cq,
-                                                          devp, finp, makespan, st);
-  } else if (K <= kBatchWide) {
-    KTimer kt(s, "k_makespan_batch");
-    k_makespan_sweep<256, 1024, 4096><<<(unsigned)K, 256, 0, s>>>(n, L, dbits, level_ptr, pptr, pidx, wp,
-                                                                  cq, devp, finp, makespan, st);
+    // Device-grouped order: inside each level, nodes sorted by (device,
+    // position in `order`).  Every device keeps its FIFO order, so the
+    // makespan is unchanged, and each device's chain in a level is one run.
+    uint8_t *dev0;
+    uint64_t *keys;
+    uint32_t *sig;
+    int32_t *gorder, *meta;
+    int64_t *wx, *sx;
+    CEL_TRY(sc.get(&dev0, n));
+    CEL_TRY(sc.get(&keys, n));
+    CEL_TRY(sc.get(&sig, n));
+    CEL_TRY(sc.get(&gorder, n));
+    CEL_TRY(sc.get(&meta, n));
+    CEL_TRY(sc.get(&wx, (int64_t)n + 1));
+    CEL_TRY(sc.get(&sx, n));
+    {
+      KTimer kt(s, "k_dev_gather");
+      k_dev_gather<<<dim3(gx, 1), 256, 0, s>>>(1, n, order, node_dev, d->D, dev0, st);
+    }
+    k_dev_keys<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, dev0, keys, sig, st);
+    CEL_TRY(segmented_sort(keys, sig, level_ptr, L, n, sc, s, st));
+    k_grouped<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, sig, dev0, gorder, pos, devp, st);
+    CEL_TRY(relabel_csr(n, g->m, gorder, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
+    k_pos_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, gorder, g->w, g->ob, d->bw, d->lat, wp,
+                                                      cq, st);
+    CEL_TRY(exclusive_scan_i64(wp, wx, n, sc, s));
+    k_runs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, level_ptr, level, gorder, devp, wx, sx, meta,
+                                                 st);
+    {
+      KTimer kt(s, "k_makespan_sweep");
+      k_makespan_one<1024, 1536, 5120><<<1, 1024, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq, devp,
+                                                          sx, meta, finp, makespan, st);
+    }
+    if (start || finish)
+      k_makespan_out<<<grid_for(n, 256, 8192), 256, 0, s>>>(1, n, gorder, finp, wp, start, finish,
+                                                            st);
   } else {
-    // more placements than CUs: small windows (about 35 KB of LDS) so that
-    // several placements share a CU and hide each other's memory latency
-    KTimer kt(s, "k_makespan_batch");
-    k_makespan_sweep<256, 256, 1024><<<(unsigned)K, 256, 0, s>>>(n, L, dbits, level_ptr, pptr, pidx, wp,
-                                                                 cq, devp, finp, makespan, st);
+    CEL_TRY(relabel_csr(n, g->m, order, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
+    k_pos_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, g->w, g->ob, d->bw, d->lat, wp,
+                                                      cq, st);
+    {
+      const int gy = K < 1024 ? K : 1024;
+      KTimer kt(s, "k_dev_gather");
+      k_dev_gather<<<dim3(gx, gy), 256, 0, s>>>(K, n, order, node_dev, d->D, devp, st);
+    }
+    int dbits = 0;  // bits of the largest device id
+    while ((1 << dbits) < d->D) dbits++;
+    if (K <= kBatchWide) {
+      KTimer kt(s, "k_makespan_batch");
+      k_makespan_sweep<256, 1024, 4096><<<(unsigned)K, 256, 0, s>>>(n, L, dbits, level_ptr, pptr,
+                                                                    pidx, wp, cq, devp, finp,
+                                                                    makespan, st);
+    } else {
+      // more placements than CUs: small windows (about 35 KB of LDS) so that
+      // several placements share a CU and hide each other's memory latency
+      KTimer kt(s, "k_makespan_batch");
+      k_makespan_sweep<256, 256, 1024><<<(unsigned)K, 256, 0, s>>>(n, L, dbits, level_ptr, pptr,
+                                                                   pidx, wp, cq, devp, finp,
+                                                                   makespan, st);
+    }
+    if (start || finish)
+      k_makespan_out<<<grid_for((int64_t)K * n, 256, 8192), 256, 0, s>>>(K, n, order, finp, wp,
+                                                                        start, finish, st);
   }
-  if (start || finish)
-    k_makespan_out<<<grid_for((int64_t)K * n, 256, 8192), 256, 0, s>>>(K, n, order, finp, wp, start,
-                                                                      finish, st);
   CEL_HIP(hipGetLastError());
   Status h;
   CEL_TRY(read_status(st, &h, s));

@@ -384,7 +384,7 @@ extern "C" int cel_place(const cel_graph *g, const cel_devices *d, const int32_t
   CEL_TRY(sc.get(&st, 1));
   CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
   CEL_TRY(sc.get(&tmp, n));
-  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, s));
+  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, sc, s));
   if (C == 0) {
     Status h;
     CEL_TRY(read_status(st, &h, s));

@@ -95,7 +95,7 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
   CEL_TRY(sc.get(&st, 1));
   CEL_TRY(sc.get(&cnt, n));
   CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
-  CEL_TRY(check_graph(g, 1, 0, /*bound=*/false, st, cnt, s));
+  CEL_TRY(check_graph(g, 1, 0, /*bound=*/false, st, cnt, sc, s));
   {
     KTimer kt(s, "k_kahn");
     k_kahn<<<1, kKahnB, 0, s>>>(*g, cnt, order_id, level, level_ptr, st);
