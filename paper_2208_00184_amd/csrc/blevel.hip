@@ -55,9 +55,18 @@ __device__ inline int64_t pull_max(int64_t r, const int16_t (*pw)[kWinN + 1], in
   int32_t j[K];
 #pragma unroll
   for (int k = 0; k < K; k++) j[k] = pw[k][si];
+  int64_t v[K], c[K];
 #pragma unroll
   for (int k = 0; k < K; k++) {
-    const int64_t x = REVERSE ? s_v[j[k]] : s_v[j[k]] + s_wc[j[k]];
+    v[k] = s_v[j[k]];
+    c[k] = REVERSE ? 0 : s_wc[j[k]];
+  }
+  // every gather is issued before the first use (the compiler would
+  // otherwise chain the cases of the caller's switch into serial round trips)
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int k = 0; k < K; k++) {
+    const int64_t x = v[k] + c[k];
     r = x > r ? x : r;
   }
   return r;
@@ -191,39 +200,59 @@ __global__ void __launch_bounds__(kSweepB)
     __syncthreads();
     CEL_TSTAMP(t2);
     CEL_TADD(REVERSE ? 1 : 16 + 1, t1, t2);
-    // stage edges: neighbours outside the window are final
-    for (int32_t e = E0 + tid; e < E1; e += kSweepB) {
-      const int32_t r = ridx[e];
-      const int32_t own = heavy ? 0 : s_own[e - E0];
-      const bool in = REVERSE ? (r < P1) : (r >= P0);
-      int32_t word = kNoop;
-      if (in) {
-        const int32_t j = r - P0;
-        const int32_t kk = atomicAdd(&s_pc[own], 1);
-        if (kk < kPullB) {
-          s_pw[kk][own] = (int16_t)j;
-        } else {
-          word = j | (own << 16);
-          // the owner's level: REVERSE levels run down the table, forward up
-          int32_t lo = 0, hi = kWinL - 1;
-          while (lo < hi) {
-            if (REVERSE) {
-              const int32_t mid = (lo + hi) >> 1;
-              if (s_la[mid] <= own) hi = mid;
-              else lo = mid + 1;
-            } else {
-              const int32_t mid = (lo + hi + 1) >> 1;
-              if (s_la[mid] <= own) lo = mid;
-              else hi = mid - 1;
-            }
-          }
-          s_lov[lo] = 1;
-        }
-      } else {
-        const int64_t x = REVERSE ? val[r] : val[r] + wcp[r];
-        atomicMax((long long *)&s_pm[own], (long long)x);
+    // stage edges: neighbours outside the window are final (each thread takes
+    // EU edges per pass: all index loads, then all value gathers, in flight
+    // together)
+    constexpr int EU = (kWinE + kSweepB - 1) / kSweepB;
+    for (int32_t e0 = E0 + tid; e0 < E1; e0 += EU * kSweepB) {
+      int32_t rr[EU];
+#pragma unroll
+      for (int u = 0; u < EU; u++) {
+        const int32_t e = e0 + u * kSweepB;
+        rr[u] = e < E1 ? ridx[e] : P0;
       }
-      if (!heavy) s_epk[e - E0] = word;
+      int64_t xv[EU];
+#pragma unroll
+      for (int u = 0; u < EU; u++) {  // unconditional: in-window neighbours read a final slot
+        const bool in = REVERSE ? (rr[u] < P1) : (rr[u] >= P0);
+        const int32_t rs = in ? 0 : rr[u];
+        xv[u] = REVERSE ? val[rs] : val[rs] + wcp[rs];
+      }
+#pragma unroll
+      for (int u = 0; u < EU; u++) {
+        const int32_t e = e0 + u * kSweepB;
+        if (e >= E1) break;
+        const int32_t r = rr[u];
+        const int32_t own = heavy ? 0 : s_own[e - E0];
+        const bool in = REVERSE ? (r < P1) : (r >= P0);
+        int32_t word = kNoop;
+        if (in) {
+          const int32_t j = r - P0;
+          const int32_t kk = atomicAdd(&s_pc[own], 1);
+          if (kk < kPullB) {
+            s_pw[kk][own] = (int16_t)j;
+          } else {
+            word = j | (own << 16);
+            // the owner's level: REVERSE levels run down the table, forward up
+            int32_t lo = 0, hi = kWinL - 1;
+            while (lo < hi) {
+              if (REVERSE) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (s_la[mid] <= own) hi = mid;
+                else lo = mid + 1;
+              } else {
+                const int32_t mid = (lo + hi + 1) >> 1;
+                if (s_la[mid] <= own) lo = mid;
+                else hi = mid - 1;
+              }
+            }
+            s_lov[lo] = 1;
+          }
+        } else {
+          atomicMax((long long *)&s_pm[own], (long long)xv[u]);
+        }
+        if (!heavy) s_epk[e - E0] = word;
+      }
     }
     __syncthreads();
     CEL_TSTAMP(t3);

@@ -513,19 +513,23 @@ __device__ inline int64_t wave_seg_pmax(int64_t y, int32_t hd, int lane) {
   return y;
 }
 
-// max of r and the first K pull gathers of slot si (finish + comm if the
-// devices differ)
-template <int NC, int K>
-__device__ inline int64_t ms_pull(int64_t r, const int16_t (*pw)[NC + 1], int32_t si,
-                                  const int64_t *s_f, const int64_t *s_c) {
-  int32_t wd[K];
-#pragma unroll
-  for (int k = 0; k < K; k++) wd[k] = pw[k][si];
+// max of r and the first K pull gathers (finish + comm if the devices differ)
+template <int K>
+__device__ inline int64_t ms_pull(int64_t r, const int32_t *pw, const int64_t *s_f,
+                                  const int64_t *s_c) {
+  int64_t f[K], c[K];
 #pragma unroll
   for (int k = 0; k < K; k++) {
-    const int32_t j = wd[k] & 0xFFF;
-    const int64_t f = s_f[j], c = s_c[j];
-    const int64_t x = f + (((wd[k] >> 12) & 1) ? c : 0);
+    const int32_t j = pw[k] & 0xFFF;
+    f[k] = s_f[j];
+    c[k] = s_c[j];
+  }
+  // every gather is issued before the first use (the compiler would
+  // otherwise chain the cases of the caller's switch into serial round trips)
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int k = 0; k < K; k++) {
+    const int64_t x = f[k] + (((pw[k] >> 12) & 1) ? c[k] : 0);
     r = x > r ? x : r;
   }
   return r;
@@ -600,32 +604,46 @@ __global__ void __launch_bounds__(B)
     s_pc[NC] = 0;
     for (int k = 0; k < F; k++) s_pw[k][NC] = NC;
   }
-  // ready() of a slot: partial from before the window, pull gathers; the
-  // value y = ready - Sx of the prefix max (with the device's free time at a
-  // run's first slot), and base = Sx + w
-  auto slot_value = [&](int32_t si, int64_t &y, int32_t &meta, int64_t &base) {
-    const int64_t pm = s_pm[si], w = s_w[si], sx = s_sx[si];
-    meta = s_meta[si];
-    const int32_t pc = s_pc[si];
-    const int64_t av = s_avail[meta & 255];
-    const int32_t cpc = pc < F ? pc : F;
+  // a row's structure: costs, run data, pull list
+  struct RowPre {
+    int64_t w, sx;
+    int32_t meta, pc;
+    int32_t pw[F];
+  };
+  auto row_pre = [&](int32_t si) {
+    RowPre p;
+    p.w = s_w[si];
+    p.sx = s_sx[si];
+    p.meta = s_meta[si];
+    p.pc = s_pc[si];
+#pragma unroll
+    for (int k = 0; k < F; k++) p.pw[k] = s_pw[k][si];
+    return p;
+  };
+  // ready() of a slot: partial from before the window, then the pull
+  // gathers, unrolled to the row's largest pull count; returns the value
+  // ready - Sx of the prefix max (the device's free time folded in at a
+  // run's first slot)
+  auto row_value = [&](int32_t si, const RowPre &p) {
+    const int64_t pm = s_pm[si];
+    const int64_t av = s_avail[p.meta & 255];
+    const int32_t cpc = p.pc < F ? p.pc : F;
     int kmax = 0;
     while (kmax < F && __ballot(cpc > kmax)) kmax++;
     int64_t r;
     switch (kmax) {
       case 0: r = pm; break;
-      case 1: r = ms_pull<NC, 1>(pm, s_pw, si, s_f, s_c); break;
-      case 2: r = ms_pull<NC, 2>(pm, s_pw, si, s_f, s_c); break;
-      case 3: r = ms_pull<NC, 3>(pm, s_pw, si, s_f, s_c); break;
-      case 4: r = ms_pull<NC, 4>(pm, s_pw, si, s_f, s_c); break;
-      case 5: r = ms_pull<NC, 5>(pm, s_pw, si, s_f, s_c); break;
-      default: r = ms_pull<NC, 6>(pm, s_pw, si, s_f, s_c); break;
+      case 1: r = ms_pull<1>(pm, p.pw, s_f, s_c); break;
+      case 2: r = ms_pull<2>(pm, p.pw, s_f, s_c); break;
+      case 3: r = ms_pull<3>(pm, p.pw, s_f, s_c); break;
+      case 4: r = ms_pull<4>(pm, p.pw, s_f, s_c); break;
+      case 5: r = ms_pull<5>(pm, p.pw, s_f, s_c); break;
+      default: r = ms_pull<6>(pm, p.pw, s_f, s_c); break;
     }
-    y = r - sx;
-    const int64_t viafree = av - sx;
-    if ((meta >> 16) == 0 && viafree > y) y = viafree;
-    base = sx + w;
-    asm volatile("" : "+v"(base));  // formed here, off the dependent chain after the scan
+    int64_t y = r - p.sx;
+    const int64_t viafree = av - p.sx;
+    if ((p.meta >> 16) == 0 && viafree > y) y = viafree;
+    return y;
   };
   int64_t mk = 0;
   int32_t P0 = 0, lcur = 0;
@@ -686,32 +704,55 @@ __global__ void __launch_bounds__(B)
     CEL_TADD(0, t0, t1);
     // in-edges: pull lists and overflow words; predecessors before the window
     // are final and are folded into the owner's partial ready time
-    for (int32_t e = E0 + tid; e < E1; e += B) {
-      const int32_t q = pidx[e];
-      const int32_t own = heavy ? 0 : s_own[e - E0];
-      const int dvo = s_meta[own] & 255;
-      int32_t word = kNoop;
-      if (q >= P0) {  // never for a heavy window: its predecessors all precede it
-        const int32_t j = q - P0;
-        const int32_t pwd = j | ((int32_t)((s_meta[j] & 255) != dvo) << 12);
-        const int32_t kk = atomicAdd(&s_pc[own], 1);
-        if (kk < F) {
-          s_pw[kk][own] = (int16_t)pwd;
-        } else {
-          word = pwd | (own << 16);
-          int32_t lo = 0, hi = kMsL - 1;  // the owner's level: last k with s_lv[k] <= P0 + own
-          while (lo < hi) {
-            const int32_t mid = (lo + hi + 1) >> 1;
-            if (s_lv[mid] <= P0 + own) lo = mid;
-            else hi = mid - 1;
-          }
-          s_lov[lo] = 1;
-        }
-      } else {
-        const int64_t x = finp[q] + (devp[q] != dvo ? cq[q] : 0);
-        atomicMax((long long *)&s_pm[own], (long long)x);
+    // (each thread takes EU edges per pass: all index loads, then all
+    // predecessor gathers, are in flight together)
+    constexpr int EU = (EC + B - 1) / B;
+    for (int32_t e0 = E0 + tid; e0 < E1; e0 += EU * B) {
+      int32_t qq[EU];
+#pragma unroll
+      for (int u = 0; u < EU; u++) {
+        const int32_t e = e0 + u * B;
+        qq[u] = e < E1 ? pidx[e] : P0;
       }
-      if (!heavy) s_epk[e - E0] = word;
+      int64_t fq[EU], cqq[EU];
+      int32_t dq[EU];
+#pragma unroll
+      for (int u = 0; u < EU; u++) {  // unconditional: in-window predecessors read a final slot
+        const int32_t qs = qq[u] < P0 ? qq[u] : 0;
+        fq[u] = finp[qs];
+        dq[u] = devp[qs];
+        cqq[u] = cq[qs];
+      }
+#pragma unroll
+      for (int u = 0; u < EU; u++) {
+        const int32_t e = e0 + u * B;
+        if (e >= E1) break;
+        const int32_t q = qq[u];
+        const int32_t own = heavy ? 0 : s_own[e - E0];
+        const int dvo = s_meta[own] & 255;
+        int32_t word = kNoop;
+        if (q >= P0) {  // never for a heavy window: its predecessors all precede it
+          const int32_t j = q - P0;
+          const int32_t pwd = j | ((int32_t)((s_meta[j] & 255) != dvo) << 12);
+          const int32_t kk = atomicAdd(&s_pc[own], 1);
+          if (kk < F) {
+            s_pw[kk][own] = (int16_t)pwd;
+          } else {
+            word = pwd | (own << 16);
+            int32_t lo = 0, hi = kMsL - 1;  // the owner's level: last k with s_lv[k] <= P0 + own
+            while (lo < hi) {
+              const int32_t mid = (lo + hi + 1) >> 1;
+              if (s_lv[mid] <= P0 + own) lo = mid;
+              else hi = mid - 1;
+            }
+            s_lov[lo] = 1;
+          }
+        } else {
+          const int64_t x = fq[u] + (dq[u] != dvo ? cqq[u] : 0);
+          atomicMax((long long *)&s_pm[own], (long long)x);
+        }
+        if (!heavy) s_epk[e - E0] = word;
+      }
     }
     __syncthreads();
     CEL_TSTAMP(t2);
@@ -761,18 +802,18 @@ __global__ void __launch_bounds__(B)
               CEL_TCOUNT(11);
               const int32_t s = r0 + lane;
               const bool act = s < b0;
-              int64_t y, base;
-              int32_t meta;
-              slot_value(act ? s : NC, y, meta, base);
-              const int32_t hd = meta >> 16;
+              const int32_t si = act ? s : NC;
+              const RowPre cur = row_pre(si);
+              int64_t y = row_value(si, cur);
+              const int32_t hd = cur.meta >> 16;
               y = wave_seg_pmax(y, hd, lane);
               if (hd > lane && carry > y) y = carry;  // the run began in an earlier row
-              const int64_t fin = base + y;
+              const int64_t fin = cur.sx + cur.w + y;
               if (act) {
                 s_f[s] = fin;
                 finp[P0 + s] = fin;
                 mk = fin > mk ? fin : mk;
-                if (meta & 256) s_avail[meta & 255] = fin;
+                if (cur.meta & 256) s_avail[cur.meta & 255] = fin;
               }
               carry = readlane64(y, 63);
               lds_order();
@@ -798,9 +839,11 @@ __global__ void __launch_bounds__(B)
           for (int32_t base0 = a0; base0 < b0; base0 += B) {
             const int32_t s = base0 + tid;
             const bool act = s < b0;
-            int64_t y, base;
-            int32_t meta;
-            slot_value(act ? s : NC, y, meta, base);
+            const int32_t si = act ? s : NC;
+            const RowPre cur = row_pre(si);
+            int64_t y = row_value(si, cur);
+            const int32_t meta = cur.meta;
+            const int64_t base = cur.sx + cur.w;
             const int32_t hd = meta >> 16;
             y = wave_seg_pmax(y, hd, lane);
             if (lane == 63) s_wy[par][wv] = y;
