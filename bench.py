@@ -53,6 +53,94 @@ def algorithmic_bytes(kernel: str, n: int, m: int, K: int) -> float | None:
     return None
 
 
+# rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE of one bench step (see --pmc-summary)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_transformer96_step.md")
+CSRC = os.path.join(ROOT, "paper_2208_00184_amd", "csrc")
+# kernels the bench names, their symbols in rocprofv3 output and their sources
+PMC_KERNELS = {
+    "k_makespan_sweep": ("cel::k_makespan_one<", ["makespan.hip", "cel_internal.h"]),
+    "k_blevel_sweep": ("cel::k_level_sweep<true>", ["blevel.hip", "cel_internal.h"]),
+    "k_tlevel_sweep": ("cel::k_level_sweep<false>", ["blevel.hip", "cel_internal.h"]),
+    "k_makespan_batch": ("cel::k_makespan_sweep<256, 1024, 4096>", ["makespan.hip", "cel_internal.h"]),
+    "k_kahn": ("cel::k_kahn(", ["topo.hip", "cel_internal.h"]),
+    "k_cluster_dp": ("cel::k_cluster_dp(", ["cluster.hip", "cel_internal.h"]),
+    "k_place": ("cel::k_place(", ["place.hip", "cel_internal.h"]),
+}
+
+
+def source_hash(files) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def pmc_summary(fetch_csv: str, write_csv: str, calib_mib: int, extra_csvs=()) -> str:
+    """Markdown summary of rocprofv3 counter CSVs: per-kernel mean per dispatch,
+    FETCH_SIZE / WRITE_SIZE scaled by what they read for a plain copy of
+    calib_mib MiB (the largest __amd_rocclr_copyBuffer dispatch)."""
+    import csv
+    from collections import defaultdict
+
+    vals = defaultdict(lambda: defaultdict(list))
+    for path in (fetch_csv, write_csv, *extra_csvs):
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                vals[r["Kernel_Name"]][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    copy = [v for k, v in vals.items() if k.startswith("__amd_rocclr_copyBuffer")]
+    cf = max(x for v in copy for x in v.get("FETCH_SIZE", [0]))
+    cw = max(x for v in copy for x in v.get("WRITE_SIZE", [0]))
+    kib = calib_mib * 1024.0
+    ff, fw = kib / cf, kib / cw
+    lines = [f"copy calibration: {calib_mib} MiB copied; FETCH_SIZE read {cf:.1f} KiB, "
+             f"WRITE_SIZE {cw:.1f} KiB; factors fetch {ff:.4f} write {fw:.4f}", "",
+             "| kernel | source | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes (scaled) |"
+             " other counters (mean per dispatch) |",
+             "|---|---|---:|---:|---:|---:|---|"]
+    for name, (sym, files) in PMC_KERNELS.items():
+        hits = [v for k, v in vals.items() if k.removeprefix("void ").startswith(sym)]
+        if not hits:
+            continue
+        v = hits[0]
+        f = sum(v["FETCH_SIZE"]) / len(v["FETCH_SIZE"])
+        w = sum(v["WRITE_SIZE"]) / len(v["WRITE_SIZE"])
+        other = ", ".join(f"{c} {sum(x) / len(x):.0f}" for c, x in sorted(v.items())
+                          if c not in ("FETCH_SIZE", "WRITE_SIZE"))
+        lines.append(f"| {name} | {source_hash(files)} | {len(v['FETCH_SIZE'])} | {f:.1f} | "
+                     f"{w:.1f} | {(f * ff + w * fw) * 1024:.0f} | {other} |")
+    return "\n".join(lines)
+
+
+def stats_summary(stats_csv: str, top: int = 40) -> str:
+    """Markdown table of a rocprofv3 --stats kernel_stats CSV (largest total first)."""
+    import csv
+    rows = []
+    with open(stats_csv) as fh:
+        for r in csv.DictReader(fh):
+            rows.append((r["Name"].split("(")[0][:70], int(r["Calls"]),
+                         float(r["TotalDurationNs"]) / 1e6, float(r["AverageNs"]) / 1e3))
+    rows.sort(key=lambda x: -x[2])
+    out = ["| kernel | calls | total ms | avg us |", "|---|---:|---:|---:|"]
+    out += [f"| {n} | {c} | {t:.3f} | {a:.1f} |" for n, c, t, a in rows[:top]]
+    return "\n".join(out)
+
+
+def load_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or
+    None when the summary is missing or the kernel's sources changed since."""
+    if not os.path.exists(TRAFFIC_FILE) or kernel not in PMC_KERNELS:
+        return None
+    want = source_hash(PMC_KERNELS[kernel][1])
+    with open(TRAFFIC_FILE) as fh:
+        for line in fh:
+            cells = [c.strip() for c in line.strip().strip("|").split("|")]
+            if len(cells) >= 6 and cells[0] == kernel:
+                return float(cells[5]) if cells[1] == want else None
+    return None
+
+
 def batched_row(cel, torch, dev, args):
     """1,024 perturbed placements of the 200k-node layered DAG scored in one call."""
     from workloads import make_config, perturb_placements
@@ -109,7 +197,24 @@ def main() -> int:
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="first copy MIB MiB device-to-device once: the reference dispatch "
                          "that scales rocprofv3 FETCH_SIZE / WRITE_SIZE into bytes")
+    ap.add_argument("--pmc-summary", nargs="+", metavar="CSV",
+                    help="print the counter summary of rocprofv3 counter_collection CSVs "
+                         "(FETCH_SIZE run, WRITE_SIZE run, then any others) and exit; "
+                         "--calib-copy gives the copy size of those runs")
+    ap.add_argument("--stats-summary", metavar="CSV",
+                    help="print a rocprofv3 --stats kernel_stats CSV as a table and exit")
     args = ap.parse_args()
+    if args.stats_summary:
+        print(stats_summary(args.stats_summary))
+        return 0
+    if args.pmc_summary:
+        if len(args.pmc_summary) < 2 or args.calib_copy <= 0:
+            print("--pmc-summary needs the FETCH_SIZE and WRITE_SIZE CSVs and --calib-copy",
+                  file=sys.stderr)
+            return 2
+        print(pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.calib_copy,
+                          args.pmc_summary[2:]))
+        return 0
     if args.gpus != 1:
         print(f"bench.py: this benchmark runs on one GPU only (got --gpus {args.gpus}); the "
               "placement path has no multi-GPU mode", file=sys.stderr)
@@ -222,7 +327,7 @@ def main() -> int:
     L = state["L"]
     roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 3),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
-                "traffic": None, "algorithmic_bytes": B,
+                "traffic": load_traffic(dom), "algorithmic_bytes": B,
                 "ns_per_level": round(t_dom * 1e9 / L, 1)}
     # the level sweeps are chains of L dependent levels: per-level latency
     per_level = {k: round(kernels[k]["avg_ms"] * 1e6 / L, 1)

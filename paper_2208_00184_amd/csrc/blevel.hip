@@ -102,8 +102,8 @@ __global__ void __launch_bounds__(kSweepB)
   constexpr int32_t kNoop = (kWinN << 16) | kWinN;  // overflow word that changes nothing
   __shared__ int32_t s_lv[kWinL + 2];  // level boundaries near the cursor
   __shared__ int32_t s_rp[kWinN + 1];  // rows of the candidate window (absolute edge offsets)
+  __shared__ int16_t s_own[kWinE];     // owner slot of each edge (-1: past kOwnFill of its row)
   __shared__ int32_t s_epk[kWinE];     // overflow words (kNoop for the other edges)
-  __shared__ int16_t s_own[kWinE];     // owner (window slot) of each edge
   __shared__ int16_t s_pw[kPullB][kWinN + 1];  // pull lists
   __shared__ int32_t s_pc[kWinN + 1];  // in-window neighbours per slot
   __shared__ int64_t s_pm[kWinN + 1];  // partial max over neighbours, -1 if none yet
@@ -130,6 +130,7 @@ __global__ void __launch_bounds__(kSweepB)
     const int32_t Pc0 = REVERSE ? (edge_lo - kWinN > 0 ? edge_lo - kWinN : 0) : edge_lo;
     const int32_t Pc1 = REVERSE ? edge_lo : (edge_lo + kWinN < n ? edge_lo + kWinN : n);
     for (int t = tid; t <= Pc1 - Pc0; t += kSweepB) s_rp[t] = rptr[Pc0 + t];
+    for (int t = tid; t < kWinE; t += kSweepB) s_own[t] = -1;
     for (int k = tid; k <= kWinL + 1; k += kSweepB) {
       // REVERSE: s_lv[k] = lp[lcur + 1 - k], so level lcur - k is [s_lv[k+1], s_lv[k]);
       // forward: s_lv[k] = lp[lcur + k], so level lcur + k is [s_lv[k], s_lv[k+1])
@@ -170,17 +171,19 @@ __global__ void __launch_bounds__(kSweepB)
     CEL_TSTAMP(t1);
     CEL_TADD(REVERSE ? 0 : 16 + 0, t0, t1);
     // stage nodes: costs, partials (0 for a REVERSE sink: its value is w),
-    // pull counters, edge owners
+    // pull counters and lists
     for (int32_t i = tid; i < NN; i += kSweepB) {
-      const int32_t k0 = s_rp[R0 + i] - E0, k1 = s_rp[R0 + i + 1] - E0;
-      const bool sink = k0 == k1;
+      const bool sink = s_rp[R0 + i] == s_rp[R0 + i + 1];
       s_pm[i] = (REVERSE && sink) ? 0 : -1;
       s_wc[i] = (REVERSE && sink) ? wp[P0 + i] : wcp[P0 + i];
       s_pc[i] = 0;
 #pragma unroll
       for (int k = 0; k < kPullB; k++) s_pw[k][i] = kWinN;  // rows gather past a short list
-      if (!heavy)
-        for (int32_t q = k0; q < k1; q++) s_own[q] = (int16_t)i;
+      if (!heavy) {  // owners of the row's first kOwnFill edges
+        const int32_t k0 = s_rp[R0 + i] - E0, k1 = s_rp[R0 + i + 1] - E0;
+        const int32_t kc = k1 - k0 < kOwnFill ? k1 : k0 + kOwnFill;
+        for (int32_t q = k0; q < kc; q++) s_own[q] = (int16_t)i;
+      }
     }
     // per-level ranges of the window: nodes [a, b), edges [ea, eb) (window-relative)
     for (int32_t k = tid; k < kWinL; k += kSweepB) {
@@ -223,7 +226,7 @@ __global__ void __launch_bounds__(kSweepB)
         const int32_t e = e0 + u * kSweepB;
         if (e >= E1) break;
         const int32_t r = rr[u];
-        const int32_t own = heavy ? 0 : s_own[e - E0];
+        const int32_t own = heavy ? 0 : owner_of(&s_rp[R0], NN, s_own[e - E0], e);
         const bool in = REVERSE ? (r < P1) : (r >= P0);
         int32_t word = kNoop;
         if (in) {
@@ -268,8 +271,12 @@ __global__ void __launch_bounds__(kSweepB)
       meb[u] = s_leb[k];
       mend[u] = s_lend[k] | (s_lov[k] << 1);
     }
-    bool synced = true;  // every wave has seen all LDS writes made so far
-    for (int32_t k = 0; k < kWinL; k++) {
+    uint64_t vis[4];  // levels the whole block visits: wide ones and the window's end
+#pragma unroll
+    for (int u = 0; u < 4; u++)
+      vis[u] = __ballot((mb[u] - ma[u] > kNarrowB) || (mend[u] & 1));
+    for (int32_t k = wave0 ? 0 : next_marked(vis, 0); k < kWinL;
+         k = wave0 ? k + 1 : next_marked(vis, k + 1)) {
       const int u = k >> 6, ln = k & 63;
       int32_t a, b, ea, eb, fl;
       switch (u) {  // uniform: pick the register set, then read lane ln
@@ -308,12 +315,11 @@ __global__ void __launch_bounds__(kSweepB)
               lds_order();
             }
           }
-          synced = false;
           CEL_TSTAMP(tl1);
           CEL_TADD(REVERSE ? 7 : 16 + 7, tl0, tl1);
         } else {
           CEL_TCOUNT(REVERSE ? 5 : 16 + 5);
-          if (!synced) __syncthreads();
+          __syncthreads();  // wave 0's narrow levels before this one
           if (fl & 2) {
             for (int32_t e = ea + tid; e < eb; e += kSweepB) {
               const int32_t wd = s_epk[e];
@@ -329,7 +335,6 @@ __global__ void __launch_bounds__(kSweepB)
             val[P0 + i] = v;
           }
           __syncthreads();
-          synced = true;
           CEL_TSTAMP(tl1);
           CEL_TADD(REVERSE ? 8 : 16 + 8, tl0, tl1);
         }

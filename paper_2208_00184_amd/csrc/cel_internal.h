@@ -97,6 +97,36 @@ __device__ inline void wave_seg_scan_dpp(int64_t &a, int64_t &b, int32_t &f) {
   seg_step<0x143, 0xC>(a, b, f);  // row_bcast:31 into rows 2 and 3
 }
 
+// Level loops of the window sweeps: only wave 0 runs narrow levels, so the
+// other waves jump from one level the whole block must visit to the next.
+// Bit (k & 63) of m[k >> 6] marks level k; returns the first marked level at
+// or after k, or 256 when there is none.
+__device__ inline int32_t next_marked(const uint64_t (&m)[4], int32_t k) {
+  while (k < 256) {
+    const int u = k >> 6;
+    const uint64_t r = m[u] >> (k & 63);
+    if (r) return k + (int32_t)__builtin_ctzll(r);
+    k = (u + 1) << 6;
+  }
+  return 256;
+}
+
+// Window staging records the owner slot of each edge for the first kOwnFill
+// edges of every row (one thread per row); an edge past that (rows of very
+// high degree only) finds its owner by binary search over the row starts:
+// the last row i in [0, nrows) with rp[i] <= e.
+constexpr int kOwnFill = 32;
+__device__ inline int32_t owner_of(const int32_t *rp, int32_t nrows, int32_t recorded, int32_t e) {
+  if (recorded >= 0) return recorded;
+  int32_t lo = 0, hi = nrows - 1;
+  while (lo < hi) {
+    const int32_t mid = (lo + hi + 1) >> 1;
+    if (rp[mid] <= e) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
 // Edge-balanced CSR traversal: block b takes edges [b * kEdgesPB, +kEdgesPB)
 // whatever their sources, so a node of huge out-degree is spread over many
 // blocks.  Wave 0 finds the rows of the slice's first and last edge by a

@@ -486,7 +486,7 @@ __global__ void __launch_bounds__(B)
 // edge-parallel atomic max.  A level part of at most kNarrow slots is run
 // by wave 0 in rows of 64 without workgroup barriers, the prefix maximum of a
 // run that crosses rows carried in from lane 63; wider parts use the block.
-constexpr int kPull = 6;
+constexpr int kPull = 8;
 constexpr int kNarrow = 256;
 
 // One step of the segmented prefix max: take the value of the lane selected
@@ -513,14 +513,15 @@ __device__ inline int64_t wave_seg_pmax(int64_t y, int32_t hd, int lane) {
   return y;
 }
 
-// max of r and the first K pull gathers (finish + comm if the devices differ)
+// max of r and the first K pull gathers (finish + comm if the devices differ);
+// pw holds 8 16-bit words, two per register
 template <int K>
-__device__ inline int64_t ms_pull(int64_t r, const int32_t *pw, const int64_t *s_f,
+__device__ inline int64_t ms_pull(int64_t r, const uint32_t (&pw)[4], const int64_t *s_f,
                                   const int64_t *s_c) {
   int64_t f[K], c[K];
 #pragma unroll
   for (int k = 0; k < K; k++) {
-    const int32_t j = pw[k] & 0xFFF;
+    const int32_t j = (pw[k >> 1] >> (16 * (k & 1))) & 0xFFF;
     f[k] = s_f[j];
     c[k] = s_c[j];
   }
@@ -529,7 +530,8 @@ __device__ inline int64_t ms_pull(int64_t r, const int32_t *pw, const int64_t *s
   asm volatile("" ::: "memory");
 #pragma unroll
   for (int k = 0; k < K; k++) {
-    const int64_t x = f[k] + (((pw[k] >> 12) & 1) ? c[k] : 0);
+    const bool cross = (pw[k >> 1] >> (16 * (k & 1) + 12)) & 1;
+    const int64_t x = f[k] + (cross ? c[k] : 0);
     r = x > r ? x : r;
   }
   return r;
@@ -575,13 +577,15 @@ __global__ void __launch_bounds__(B)
   constexpr int F = kPull;
   static_assert(NC < 4095 && EC < 32768, "slot fields are 12 bits");
   constexpr int32_t kNoop = (NC << 16) | NC;  // overflow word that changes nothing
+  constexpr uint32_t kPw2 = ((uint32_t)NC << 16) | NC;  // two dummy pull words
+  static_assert(kPull == 8, "a pull list is one 16-byte LDS word");
   __shared__ int32_t s_lv[kMsL + 2];
   __shared__ int32_t s_rp[NC + 1];
+  __shared__ int16_t s_own[EC];  // owner slot of each edge (-1: past kOwnFill of its row)
   __shared__ int32_t s_epk[EC + 1];
-  __shared__ int16_t s_own[EC];
   __shared__ int64_t s_pm[NC + 1], s_f[NC + 1], s_w[NC + 1], s_c[NC + 1], s_sx[NC + 1];
   __shared__ int32_t s_meta[NC + 1];
-  __shared__ int16_t s_pw[F][NC + 1];
+  __shared__ uint4 s_pw[NC + 1];  // pull lists: F = 8 words of 16 bits per slot
   __shared__ int32_t s_pc[NC + 1];
   __shared__ int32_t s_la[kMsL], s_lb[kMsL], s_lea[kMsL], s_leb[kMsL], s_lend[kMsL];
   __shared__ int32_t s_lov[kMsL];
@@ -602,13 +606,13 @@ __global__ void __launch_bounds__(B)
     s_sx[NC] = 0;
     s_meta[NC] = 0;
     s_pc[NC] = 0;
-    for (int k = 0; k < F; k++) s_pw[k][NC] = NC;
+    s_pw[NC] = make_uint4(kPw2, kPw2, kPw2, kPw2);
   }
-  // a row's structure: costs, run data, pull list
+  // a row's structure: costs, run data, in-window predecessor count, pull list
   struct RowPre {
     int64_t w, sx;
     int32_t meta, pc;
-    int32_t pw[F];
+    uint32_t pw[4];
   };
   auto row_pre = [&](int32_t si) {
     RowPre p;
@@ -616,20 +620,26 @@ __global__ void __launch_bounds__(B)
     p.sx = s_sx[si];
     p.meta = s_meta[si];
     p.pc = s_pc[si];
-#pragma unroll
-    for (int k = 0; k < F; k++) p.pw[k] = s_pw[k][si];
+    const uint4 q = s_pw[si];
+    p.pw[0] = q.x;
+    p.pw[1] = q.y;
+    p.pw[2] = q.z;
+    p.pw[3] = q.w;
     return p;
   };
+  // the largest pull count of the wave's lanes (wave-uniform)
+  auto row_kmax = [&](int32_t pc) {
+    const int32_t c = pc < F ? pc : F;
+    int kmax = 0;
+    while (kmax < F && __ballot(c > kmax)) kmax++;
+    return kmax;
+  };
   // ready() of a slot: partial from before the window, then the pull
-  // gathers, unrolled to the row's largest pull count; returns the value
-  // ready - Sx of the prefix max (the device's free time folded in at a
-  // run's first slot)
-  auto row_value = [&](int32_t si, const RowPre &p) {
+  // gathers; returns the value ready - Sx of the prefix max (the device's
+  // free time folded in at a run's first slot)
+  auto row_value = [&](int32_t si, const RowPre &p, int kmax) {
     const int64_t pm = s_pm[si];
     const int64_t av = s_avail[p.meta & 255];
-    const int32_t cpc = p.pc < F ? p.pc : F;
-    int kmax = 0;
-    while (kmax < F && __ballot(cpc > kmax)) kmax++;
     int64_t r;
     switch (kmax) {
       case 0: r = pm; break;
@@ -638,7 +648,9 @@ __global__ void __launch_bounds__(B)
       case 3: r = ms_pull<3>(pm, p.pw, s_f, s_c); break;
       case 4: r = ms_pull<4>(pm, p.pw, s_f, s_c); break;
       case 5: r = ms_pull<5>(pm, p.pw, s_f, s_c); break;
-      default: r = ms_pull<6>(pm, p.pw, s_f, s_c); break;
+      case 6: r = ms_pull<6>(pm, p.pw, s_f, s_c); break;
+      case 7: r = ms_pull<7>(pm, p.pw, s_f, s_c); break;
+      default: r = ms_pull<8>(pm, p.pw, s_f, s_c); break;
     }
     int64_t y = r - p.sx;
     const int64_t viafree = av - p.sx;
@@ -652,6 +664,7 @@ __global__ void __launch_bounds__(B)
     CEL_TCOUNT(6);
     const int32_t Pc1 = P0 + NC < n ? P0 + NC : n;
     for (int t = tid; t <= Pc1 - P0; t += B) s_rp[t] = pptr[P0 + t];
+    for (int t = tid; t < EC; t += B) s_own[t] = -1;
     for (int k = tid; k <= kMsL + 1; k += B) {
       const int32_t l = lcur + k;  // level lcur + k is [s_lv[k], s_lv[k+1])
       s_lv[k] = lp[l > L ? L : l];
@@ -682,10 +695,12 @@ __global__ void __launch_bounds__(B)
       s_sx[i] = sxp[p];
       s_pm[i] = 0;
       s_pc[i] = 0;
-#pragma unroll
-      for (int k = 0; k < F; k++) s_pw[k][i] = NC;  // rows gather past a short list
-      if (!heavy)
-        for (int32_t q = s_rp[i] - E0; q < s_rp[i + 1] - E0; q++) s_own[q] = (int16_t)i;
+      s_pw[i] = make_uint4(kPw2, kPw2, kPw2, kPw2);  // rows gather past a short list
+      if (!heavy) {  // owners of the row's first kOwnFill edges
+        const int32_t k0 = s_rp[i] - E0, k1 = s_rp[i + 1] - E0;
+        const int32_t kc = k1 - k0 < kOwnFill ? k1 : k0 + kOwnFill;
+        for (int32_t q = k0; q < kc; q++) s_own[q] = (int16_t)i;
+      }
     }
     for (int32_t k = tid; k < kMsL; k += B) {
       const int32_t lb = s_lv[k], le = s_lv[k + 1];
@@ -728,7 +743,7 @@ __global__ void __launch_bounds__(B)
         const int32_t e = e0 + u * B;
         if (e >= E1) break;
         const int32_t q = qq[u];
-        const int32_t own = heavy ? 0 : s_own[e - E0];
+        const int32_t own = heavy ? 0 : owner_of(s_rp, NN, s_own[e - E0], e);
         const int dvo = s_meta[own] & 255;
         int32_t word = kNoop;
         if (q >= P0) {  // never for a heavy window: its predecessors all precede it
@@ -736,7 +751,7 @@ __global__ void __launch_bounds__(B)
           const int32_t pwd = j | ((int32_t)((s_meta[j] & 255) != dvo) << 12);
           const int32_t kk = atomicAdd(&s_pc[own], 1);
           if (kk < F) {
-            s_pw[kk][own] = (int16_t)pwd;
+            reinterpret_cast<uint16_t *>(&s_pw[own])[kk] = (uint16_t)pwd;
           } else {
             word = pwd | (own << 16);
             int32_t lo = 0, hi = kMsL - 1;  // the owner's level: last k with s_lv[k] <= P0 + own
@@ -757,34 +772,36 @@ __global__ void __launch_bounds__(B)
     __syncthreads();
     CEL_TSTAMP(t2);
     CEL_TADD(1, t1, t2);
-    int32_t ma[4], mb[4], mea[4], meb[4], mend[4];
+    // level descriptors in registers, lane l holding levels l, l+64, ...:
+    // first slot | end slot << 12 | window ends here << 24 | overflow << 25
+    int32_t lvm[4];
 #pragma unroll
     for (int u = 0; u < 4; u++) {
       const int k = lane + 64 * u;
-      ma[u] = s_la[k];
-      mb[u] = s_lb[k];
-      mea[u] = s_lea[k];
-      meb[u] = s_leb[k];
-      mend[u] = s_lend[k] | (s_lov[k] << 1);
+      lvm[u] = s_la[k] | (s_lb[k] << 12) | (s_lend[k] << 24) | (s_lov[k] << 25);
     }
-    bool synced = true;
+    auto level_desc = [&](int32_t kk) {
+      int32_t t;
+      switch (kk >> 6) {  // uniform: pick the register, then read lane kk & 63
+        case 0: t = lvm[0]; break;
+        case 1: t = lvm[1]; break;
+        case 2: t = lvm[2]; break;
+        default: t = lvm[3]; break;
+      }
+      return __builtin_amdgcn_readlane(t, kk & 63);
+    };
+    uint64_t vis[4];  // levels the whole block visits: wide ones and the window's end
+#pragma unroll
+    for (int u = 0; u < 4; u++)
+      vis[u] = __ballot((((lvm[u] >> 12) & 0xFFF) - (lvm[u] & 0xFFF) > kNarrow) || ((lvm[u] >> 24) & 1));
     CEL_TSTAMP(t3);
     CEL_TADD(2, t2, t3);
-    for (int32_t k = 0; k < kMsL; k++) {
-      const int u = k >> 6, ln = k & 63;
-      int32_t a0, b0, ea, eb, fl;
-      switch (u) {
-        case 0: a0 = ma[0]; b0 = mb[0]; ea = mea[0]; eb = meb[0]; fl = mend[0]; break;
-        case 1: a0 = ma[1]; b0 = mb[1]; ea = mea[1]; eb = meb[1]; fl = mend[1]; break;
-        case 2: a0 = ma[2]; b0 = mb[2]; ea = mea[2]; eb = meb[2]; fl = mend[2]; break;
-        default: a0 = ma[3]; b0 = mb[3]; ea = mea[3]; eb = meb[3]; fl = mend[3]; break;
-      }
-      a0 = __builtin_amdgcn_readlane(a0, ln);
-      b0 = __builtin_amdgcn_readlane(b0, ln);
-      ea = __builtin_amdgcn_readlane(ea, ln);
-      eb = __builtin_amdgcn_readlane(eb, ln);
-      fl = __builtin_amdgcn_readlane(fl, ln);
+    for (int32_t k = wave0 ? 0 : next_marked(vis, 0); k < kMsL;
+         k = wave0 ? k + 1 : next_marked(vis, k + 1)) {
+      const int32_t dsc = level_desc(k);
+      const int32_t a0 = dsc & 0xFFF, b0 = (dsc >> 12) & 0xFFF, fl = dsc >> 24;
       if (a0 < b0) {
+        const int32_t ea = (fl & 2) ? s_lea[k] : 0, eb = (fl & 2) ? s_leb[k] : 0;
         CEL_TSTAMP(tl0);
         if (b0 - a0 <= kNarrow) {
           if (wave0) {
@@ -804,7 +821,7 @@ __global__ void __launch_bounds__(B)
               const bool act = s < b0;
               const int32_t si = act ? s : NC;
               const RowPre cur = row_pre(si);
-              int64_t y = row_value(si, cur);
+              int64_t y = row_value(si, cur, row_kmax(cur.pc));
               const int32_t hd = cur.meta >> 16;
               y = wave_seg_pmax(y, hd, lane);
               if (hd > lane && carry > y) y = carry;  // the run began in an earlier row
@@ -815,16 +832,15 @@ __global__ void __launch_bounds__(B)
                 mk = fin > mk ? fin : mk;
                 if (cur.meta & 256) s_avail[cur.meta & 255] = fin;
               }
-              carry = readlane64(y, 63);
+              if (r0 + 64 < b0) carry = readlane64(y, 63);
               lds_order();
             }
           }
-          synced = false;
           CEL_TSTAMP(tl1);
           CEL_TADD(7, tl0, tl1);
           CEL_TCOUNT(4);
         } else {
-          if (!synced) __syncthreads();
+          __syncthreads();  // wave 0's narrow levels before this one
           if (fl & 2) {
             for (int32_t e = ea + tid; e < eb; e += B) {
               const int32_t wd = s_epk[e];
@@ -841,7 +857,7 @@ __global__ void __launch_bounds__(B)
             const bool act = s < b0;
             const int32_t si = act ? s : NC;
             const RowPre cur = row_pre(si);
-            int64_t y = row_value(si, cur);
+            int64_t y = row_value(si, cur, row_kmax(cur.pc));
             const int32_t meta = cur.meta;
             const int64_t base = cur.sx + cur.w;
             const int32_t hd = meta >> 16;
@@ -867,7 +883,6 @@ __global__ void __launch_bounds__(B)
             par ^= 1;
           }
           __syncthreads();
-          synced = true;
           CEL_TSTAMP(tl1);
           CEL_TADD(8, tl0, tl1);
           CEL_TCOUNT(5);
