@@ -103,6 +103,7 @@ __device__ inline void wave_seg_scan_maxplus_z(int64_t &a, int64_t &b, int32_t &
   segz_step<0x143, 0xC>(a, b, f);  // row_bcast:31 into rows 2 and 3
 }
 constexpr int kBatchWide = 384;  // batches up to this size get one CU-sized window per placement
+constexpr int kWideLevels = 256;  // mean level width from which batches skip the windows
 
 template <int B, int NC, int EC>
 __global__ void __launch_bounds__(B)
@@ -937,6 +938,204 @@ __global__ void k_grouped(int32_t n, const int32_t *order, const uint32_t *sig,
   }
 }
 
+// ---------------------------------------------------------------------------
+// Batches over graphs with wide levels: one workgroup of B threads per
+// placement walks the levels in order with no LDS window.  Predecessors of a
+// level all lie in earlier levels, whose finish times this workgroup already
+// wrote to global memory, so every ready() of a level is gathered at once:
+// each thread takes PT nodes per pass, loads their first kRnd in-edge indices,
+// then all predecessor finish, device and comm values, in flight together (a
+// node with more in-edges finishes in a loop).  Each chunk of B nodes is then
+// partitioned by device (stable: ballots per wave, per-wave device counts in
+// LDS) and scanned as max-plus maps per device run, seeded with the device's
+// free time, which the run's last node updates.
+template <int B, int PT, int kRnd>
+__global__ void __launch_bounds__(B)
+    k_makespan_levels(int32_t n, int32_t L, int32_t dbits, const int32_t *lp, const int32_t *pptr,
+                      const int32_t *pidx, const int64_t *wp, const int64_t *cq,
+                      const uint8_t *devp, int64_t *finp, int64_t *makespan, const Status *st) {
+  constexpr int NW = B / 64;
+  static_assert(B >= 256 && B % 64 == 0, "the device prefix uses one thread per device id");
+  __shared__ int64_t s_avail[256];
+  __shared__ int32_t s_wcnt[NW][256];
+  __shared__ int32_t s_dbase[256];
+  __shared__ int32_t s_dsum[4];
+  __shared__ int64_t s_a[B], s_b[B];
+  __shared__ int32_t s_pos[B];
+  __shared__ uint8_t s_dev[B];
+  __shared__ int64_t s_wa[NW], s_wb[NW];
+  __shared__ int32_t s_wf[NW];
+  __shared__ int64_t s_red[NW];
+  if (failed(st)) return;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const uint64_t lanemask_lt = (1ull << lane) - 1ull;
+  const int64_t koff = (int64_t)blockIdx.x * n;
+  const uint8_t *dk = devp + koff;
+  int64_t *fk = finp + koff;
+  const bool dlane = tid < 256;  // threads that own a device id in the prefix steps
+  if (dlane) {
+    s_avail[tid] = 0;
+    for (int w2 = 0; w2 < NW; w2++) s_wcnt[w2][tid] = 0;
+  }
+  __syncthreads();
+  int64_t mk = 0;
+  for (int32_t l = 0; l < L; l++) {
+    const int32_t a = lp[l], b = lp[l + 1];
+    for (int32_t base = a; base < b; base += B * PT) {
+      // ---- gather: a = ready + w and w of PT nodes per thread
+      int32_t dv[PT], e0[PT], e1[PT];
+      int64_t w[PT], rdy[PT];
+#pragma unroll
+      for (int j = 0; j < PT; j++) {
+        const int32_t p = base + j * B + tid;
+        const bool act = p < b;
+        const int32_t ps = act ? p : a;
+        dv[j] = act ? dk[ps] : 255;
+        w[j] = wp[ps];
+        e0[j] = pptr[ps];
+        e1[j] = act ? pptr[ps + 1] : e0[j];
+        rdy[j] = 0;
+      }
+      int32_t q[PT][kRnd];
+#pragma unroll
+      for (int j = 0; j < PT; j++)
+#pragma unroll
+        for (int r = 0; r < kRnd; r++) {
+          const bool ok = e0[j] + r < e1[j];
+          const int32_t v = pidx[ok ? e0[j] + r : 0];  // pidx holds at least one element
+          q[j][r] = ok ? v : 0;                         // node 0 stands in for absent edges
+        }
+      int64_t fq[PT][kRnd], cc[PT][kRnd];
+      int32_t dq[PT][kRnd];
+#pragma unroll
+      for (int j = 0; j < PT; j++)
+#pragma unroll
+        for (int r = 0; r < kRnd; r++) {
+          fq[j][r] = fk[q[j][r]];
+          dq[j][r] = dk[q[j][r]];
+          cc[j][r] = cq[q[j][r]];
+        }
+#pragma unroll
+      for (int j = 0; j < PT; j++) {
+#pragma unroll
+        for (int r = 0; r < kRnd; r++) {
+          if (e0[j] + r < e1[j]) {
+            const int64_t x = fq[j][r] + (dq[j][r] != dv[j] ? cc[j][r] : 0);
+            rdy[j] = x > rdy[j] ? x : rdy[j];
+          }
+        }
+        for (int32_t e = e0[j] + kRnd; e < e1[j]; e++) {  // in-edges past the first kRnd
+          const int32_t qq = pidx[e];
+          const int64_t x = fk[qq] + (dk[qq] != dv[j] ? cq[qq] : 0);
+          rdy[j] = x > rdy[j] ? x : rdy[j];
+        }
+      }
+      // ---- per chunk of B nodes: stable partition by device, then scan
+#pragma unroll
+      for (int j = 0; j < PT; j++) {
+        const int32_t cbase = base + j * B;
+        if (cbase >= b) break;  // uniform
+        const int32_t cnt = b - cbase < B ? b - cbase : B;
+        const bool act = tid < cnt;
+        const int d = dv[j];
+        const uint64_t actm = __ballot(act);
+        uint64_t eq = actm;
+        for (int bit = 0; bit < dbits; bit++) {
+          const int on = (d >> bit) & 1;
+          const uint64_t bb = __ballot(on);
+          eq &= on ? bb : ~bb;
+        }
+        const int rank = __popcll(eq & lanemask_lt);
+        if (act && rank == 0) s_wcnt[wv][d] = __popcll(eq);
+        __syncthreads();
+        // per device: exclusive bases over the waves, then over the devices
+        int32_t tot = 0;
+        if (dlane)
+          for (int w2 = 0; w2 < NW; w2++) {
+            const int32_t c = s_wcnt[w2][tid];
+            s_wcnt[w2][tid] = tot;
+            tot += c;
+          }
+        int32_t inc = tot;
+        for (int off = 1; off < 64; off <<= 1) {
+          const int32_t y = __shfl_up(inc, off);
+          if (lane >= off) inc += y;
+        }
+        if (dlane && lane == 63) s_dsum[wv] = inc;
+        __syncthreads();
+        if (dlane) {
+          int32_t bv = inc - tot;
+          for (int w2 = 0; w2 < wv; w2++) bv += s_dsum[w2];
+          s_dbase[tid] = bv;
+        }
+        __syncthreads();
+        if (act) {
+          const int slot = s_dbase[d] + s_wcnt[wv][d] + rank;
+          s_a[slot] = rdy[j] + w[j];
+          s_b[slot] = w[j];
+          s_pos[slot] = cbase + tid;
+          s_dev[slot] = (uint8_t)d;
+        }
+        __syncthreads();
+        if (dlane)
+          for (int w2 = 0; w2 < NW; w2++) s_wcnt[w2][tid] = 0;  // ready for the next chunk
+        // segmented scan of (a, b) over the device runs
+        int64_t sa = kNeg, sb = 0;
+        int dq2 = 0;
+        int32_t f = 1;
+        if (act) {
+          sa = s_a[tid];
+          sb = s_b[tid];
+          dq2 = s_dev[tid];
+          f = (tid == 0) || (s_dev[tid - 1] != dq2);
+        }
+        wave_seg_scan_dpp(sa, sb, f);
+        if (lane == 63) {
+          s_wa[wv] = sa;
+          s_wb[wv] = sb;
+          s_wf[wv] = f;
+        }
+        __syncthreads();
+        if (act && !f && wv > 0) {  // the run began in an earlier wave: prepend their totals
+          int64_t ca = s_wa[wv - 1], cb = s_wb[wv - 1];
+          bool done = s_wf[wv - 1] != 0;
+          for (int w2 = wv - 2; w2 >= 0 && !done; w2--) {
+            ca = (s_wa[w2] + cb) > ca ? s_wa[w2] + cb : ca;
+            cb = s_wb[w2] + cb;
+            done = s_wf[w2] != 0;
+          }
+          sa = (ca + sb) > sa ? ca + sb : sa;
+          sb = cb + sb;
+        }
+        int64_t fin = 0;
+        bool last = false;
+        if (act) {
+          const int64_t viafree = s_avail[dq2] + sb;
+          fin = viafree > sa ? viafree : sa;
+          fk[s_pos[tid]] = fin;
+          mk = fin > mk ? fin : mk;
+          last = (tid + 1 == cnt) || (s_dev[tid + 1] != dq2);
+        }
+        __syncthreads();  // every read of s_avail, s_a, s_b, s_dev is done
+        if (last) s_avail[dq2] = fin;
+      }
+    }
+    // the next level gathers these finish times from global memory
+    __syncthreads();
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const int64_t y = __shfl_xor(mk, off);
+    mk = y > mk ? y : mk;
+  }
+  if (lane == 0) s_red[wv] = mk;
+  __syncthreads();
+  if (tid == 0) {
+    int64_t r = s_red[0];
+    for (int i = 1; i < NW; i++) r = s_red[i] > r ? s_red[i] : r;
+    makespan[blockIdx.x] = r;
+  }
+}
+
 // finish/start by node id from position-space finishes
 __global__ void k_makespan_out(int32_t K, int32_t n, const int32_t *order, const int64_t *finp,
                                const int64_t *wp, int64_t *start, int64_t *finish,
@@ -1046,9 +1245,14 @@ extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int3
       KTimer kt(s, "k_dev_gather");
       k_dev_gather<<<dim3(gx, gy), 256, 0, s>>>(K, n, order, node_dev, d->D, devp, st);
     }
+    const bool wide = (int64_t)n >= (int64_t)kWideLevels * L;  // gathers from global memory
     int dbits = 0;  // bits of the largest device id
     while ((1 << dbits) < d->D) dbits++;
-    if (K <= kBatchWide) {
+    if (wide) {
+      KTimer kt(s, "k_makespan_batch");
+      k_makespan_levels<512, 1, 3><<<(unsigned)K, 512, 0, s>>>(n, L, dbits, level_ptr, pptr, pidx,
+                                                              wp, cq, devp, finp, makespan, st);
+    } else if (K <= kBatchWide) {
       KTimer kt(s, "k_makespan_batch");
       k_makespan_sweep<256, 1024, 4096><<<(unsigned)K, 256, 0, s>>>(n, L, dbits, level_ptr, pptr,
                                                                     pidx, wp, cq, devp, finp,

@@ -144,6 +144,63 @@ def test_makespan_large_batches():
     assert np.array_equal(ms5[rows], ref5)
 
 
+def _wide_layered(seed, widths, max_fanin, D):
+    """Layered DAG with the given level widths; each node draws 1..max_fanin
+    parents (with repeats: multi-edges) from the previous level."""
+    rng = np.random.default_rng([91, seed])
+    starts = np.concatenate([[0], np.cumsum(widths)])
+    n = int(starts[-1])
+    edges = []
+    for li in range(1, len(widths)):
+        for v in range(int(starts[li]), int(starts[li + 1])):
+            k = int(rng.integers(1, max_fanin + 1))
+            for u in rng.integers(starts[li - 1], starts[li], k):
+                edges.append((int(u), v))
+    w = rng.integers(1, 5000, n)
+    ob = rng.integers(0, 1 << 20, n)
+    return from_edges(n, edges, w, ob, D, np.full(D, 1 << 40), 7, 300, name="wide-layered")
+
+
+@pytest.mark.parametrize("widths,fanin,D,K", [
+    ([700, 1300, 900], 10, 200, 3),     # passes of 512 nodes, tail in-edges, 8-bit devices
+    ([257, 513, 1025, 300], 3, 16, 5),  # ragged chunks
+    ([600, 600], 1, 1, 2),              # one device
+])
+def test_makespan_wide_levels_batch(widths, fanin, D, K):
+    """Batches on graphs with wide levels run without LDS windows."""
+    wl = _wide_layered(len(widths) * 100 + fanin, widths, fanin, D)
+    lev, oid, lp, L = O.topo_levels(wl)
+    assert wl.n >= 256 * L  # the window-free kernel's regime
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    P = random_placements(wl, K, D)
+    ref_ms, ref_st, ref_fi = O.makespan(wl, pr, P)
+    g, d = up(wl)
+    ms, st, fi = cel.makespan(g, d, tt(pr, np.int32), tt(lev, np.int32), tt(lp, np.int32), L,
+                              tt(P, np.uint8), want_times=True)
+    assert np.array_equal(np_(ms), ref_ms)
+    assert np.array_equal(np_(st), ref_st) and np.array_equal(np_(fi), ref_fi)
+
+
+def test_makespan_wide_no_edges_batch():
+    """Sources only: one level of 3,000 isolated nodes, 4 placements."""
+    n, D = 3000, 5
+    rng = np.random.default_rng(5)
+    wl = from_edges(n, [], rng.integers(1, 100, n), rng.integers(0, 1000, n), D,
+                    np.full(D, 1 << 40), 3, 10)
+    lev, oid, lp, L = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    P = random_placements(wl, 4, 1)
+    ref_ms, _, ref_fi = O.makespan(wl, pr, P)
+    g, d = up(wl)
+    ms, _, fi = cel.makespan(g, d, tt(pr, np.int32), tt(lev, np.int32), tt(lp, np.int32), L,
+                             tt(P, np.uint8), want_times=True)
+    assert np.array_equal(np_(ms), ref_ms) and np.array_equal(np_(fi), ref_fi)
+    P[2, 1234] = D  # a device id out of range is rejected on this path too
+    with pytest.raises(cel.CelError):
+        cel.makespan(g, d, tt(pr, np.int32), tt(lev, np.int32), tt(lp, np.int32), L,
+                     tt(P, np.uint8))
+
+
 # ---------------------------------------------------------- random small DAGs
 
 
