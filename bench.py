@@ -53,8 +53,10 @@ def algorithmic_bytes(kernel: str, n: int, m: int, K: int) -> float | None:
     return None
 
 
-# rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE of one bench step (see --pmc-summary)
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_transformer96_step.md")
+# rocprofv3 --pmc summaries (see --pmc-summary): one bench step on the
+# transformer graph, and the 1,024-placement scoring row
+TRAFFIC_FILES = [os.path.join(ROOT, "profiles", f) for f in
+                 ("pmc_transformer96_step.md", "pmc_layered200k_batch1024.md")]
 CSRC = os.path.join(ROOT, "paper_2208_00184_amd", "csrc")
 # kernels the bench names, their symbols in rocprofv3 output and their sources
 PMC_KERNELS = {
@@ -62,6 +64,7 @@ PMC_KERNELS = {
     "k_blevel_sweep": ("cel::k_level_sweep<true>", ["blevel.hip", "cel_internal.h"]),
     "k_tlevel_sweep": ("cel::k_level_sweep<false>", ["blevel.hip", "cel_internal.h"]),
     "k_makespan_batch": ("cel::k_makespan_sweep<256, 1024, 4096>", ["makespan.hip", "cel_internal.h"]),
+    "k_makespan_batch_wide": ("cel::k_makespan_levels<", ["makespan.hip", "cel_internal.h"]),
     "k_kahn": ("cel::k_kahn(", ["topo.hip", "cel_internal.h"]),
     "k_cluster_dp": ("cel::k_cluster_dp(", ["cluster.hip", "cel_internal.h"]),
     "k_place": ("cel::k_place(", ["place.hip", "cel_internal.h"]),
@@ -77,7 +80,7 @@ def source_hash(files) -> str:
     return h.hexdigest()[:16]
 
 
-def pmc_summary(fetch_csv: str, write_csv: str, calib_mib: int, extra_csvs=()) -> str:
+def pmc_summary(fetch_csv: str, write_csv: str, calib_mib: int, extra_csvs=(), only=None) -> str:
     """Markdown summary of rocprofv3 counter CSVs: per-kernel mean per dispatch,
     FETCH_SIZE / WRITE_SIZE scaled by what they read for a plain copy of
     calib_mib MiB (the largest __amd_rocclr_copyBuffer dispatch)."""
@@ -100,6 +103,8 @@ def pmc_summary(fetch_csv: str, write_csv: str, calib_mib: int, extra_csvs=()) -
              " other counters (mean per dispatch) |",
              "|---|---|---:|---:|---:|---:|---|"]
     for name, (sym, files) in PMC_KERNELS.items():
+        if only and name not in only:
+            continue
         hits = [v for k, v in vals.items() if k.removeprefix("void ").startswith(sym)]
         if not hits:
             continue
@@ -130,14 +135,17 @@ def stats_summary(stats_csv: str, top: int = 40) -> str:
 def load_traffic(kernel: str):
     """HBM bytes per launch of `kernel` from the committed counter summary, or
     None when the summary is missing or the kernel's sources changed since."""
-    if not os.path.exists(TRAFFIC_FILE) or kernel not in PMC_KERNELS:
+    if kernel not in PMC_KERNELS:
         return None
     want = source_hash(PMC_KERNELS[kernel][1])
-    with open(TRAFFIC_FILE) as fh:
-        for line in fh:
-            cells = [c.strip() for c in line.strip().strip("|").split("|")]
-            if len(cells) >= 6 and cells[0] == kernel:
-                return float(cells[5]) if cells[1] == want else None
+    for path in TRAFFIC_FILES:
+        if not os.path.exists(path):
+            continue
+        with open(path) as fh:
+            for line in fh:
+                cells = [c.strip() for c in line.strip().strip("|").split("|")]
+                if len(cells) >= 6 and cells[0] == kernel:
+                    return float(cells[5]) if cells[1] == want else None
     return None
 
 
@@ -182,6 +190,7 @@ def batched_row(cel, torch, dev, args):
             "edges_per_s": BATCH5 * wl.m / (call_ms * 1e-3), "kernel_ms": kms,
             "algorithmic_bytes": B, "achieved_GBs": round(B / (kms * 1e-3) / 1e9, 2),
             "frac": round(B / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS, 5),
+            "traffic": load_traffic("k_makespan_batch_wide"),
             "makespan_min_ns": int(ms.min().item()), "makespan_max_ns": int(ms.max().item())}
 
 
@@ -201,6 +210,8 @@ def main() -> int:
                     help="print the counter summary of rocprofv3 counter_collection CSVs "
                          "(FETCH_SIZE run, WRITE_SIZE run, then any others) and exit; "
                          "--calib-copy gives the copy size of those runs")
+    ap.add_argument("--pmc-kernels", nargs="+", metavar="NAME",
+                    help="restrict --pmc-summary to these kernels")
     ap.add_argument("--stats-summary", metavar="CSV",
                     help="print a rocprofv3 --stats kernel_stats CSV as a table and exit")
     args = ap.parse_args()
@@ -213,7 +224,7 @@ def main() -> int:
                   file=sys.stderr)
             return 2
         print(pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.calib_copy,
-                          args.pmc_summary[2:]))
+                          args.pmc_summary[2:], args.pmc_kernels))
         return 0
     if args.gpus != 1:
         print(f"bench.py: this benchmark runs on one GPU only (got --gpus {args.gpus}); the "

@@ -14,8 +14,10 @@
  *    library never frees or keeps a caller pointer after it returns.
  *  - Work is enqueued on `stream`; every call returns after its results are
  *    complete (it synchronises `stream` once to read its status and scalar
- *    outputs).  Scratch memory is taken from the device's stream-ordered pool
- *    and returned before the call ends.
+ *    outputs).  Scratch memory comes from a library-owned arena per (device,
+ *    stream): device blocks that grow to the largest call's needs and are
+ *    kept until the process ends, so repeated calls allocate nothing.  Calls
+ *    on one stream from several host threads take turns on its arena.
  *  - Times are int64 nanoseconds, sizes int64 bytes, indices int32.  A node's
  *    communication time is c[v] = ceil(ob[v] / bw) + lat (the paper's linear
  *    fit t = k*d + b, Section 4.2.1, in integer form), paid once per consumer
