@@ -10,58 +10,76 @@
 namespace cel {
 
 constexpr int kKahnB = 1024;
-constexpr int kKahnHeavy = 64;  // out-degree above which the whole block shares a node
+constexpr int kKahnHeavy = 64;    // out-degree above which the whole block shares a node
+constexpr int kKahnFront = 8192;  // frontier entries mirrored in LDS
+constexpr int kKahnE = 4;         // out-edges per node whose loads and atomics go out together
 
-__device__ inline void kahn_release(const cel_graph &g, int32_t *cnt, int32_t *F,
-                                    int32_t *s_tail, int32_t e) {
-  const int32_t v = g.out_idx[e];
-  if (atomicSub(&cnt[v], 1) == 1) {  // last in-edge removed: v joins the next frontier
-    const int32_t k = atomicAdd(s_tail, 1);
-    F[k] = v;
-  }
+// Removes edge e's target's in-edge; the node that removes the last one
+// appends the target to the next frontier (global order, and the LDS mirror
+// while it has room).
+__device__ inline void kahn_append(int32_t *F, int32_t *s_front, int32_t *s_tail, int32_t fe,
+                                   int32_t v) {
+  const int32_t k = atomicAdd(s_tail, 1);
+  F[k] = v;
+  if (k - fe < kKahnFront) s_front[k - fe] = v;
 }
 
 __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, int32_t *F,
                                                  int32_t *level, int32_t *lstart, Status *st) {
   __shared__ int32_t s_tail, s_nheavy;
   __shared__ int32_t s_heavy[kKahnB];
+  __shared__ int32_t s_front[2][kKahnFront];  // the frontier being read, the one being built
   if (failed(st)) return;
   const int tid = threadIdx.x;
   const int32_t n = g.n;
   if (tid == 0) s_tail = 0;
   __syncthreads();
   for (int32_t v = tid; v < n; v += kKahnB)
-    if (cnt[v] == 0) F[atomicAdd(&s_tail, 1)] = v;
+    if (cnt[v] == 0) kahn_append(F, s_front[0], &s_tail, 0, v);
   __syncthreads();
-  int32_t fb = 0, fe = s_tail, lvl = 0;
+  int32_t fb = 0, fe = s_tail, lvl = 0, cur = 0;
   while (fb < fe) {
     if (tid == 0) lstart[lvl] = fb;
+    const int32_t *front = s_front[cur];
+    int32_t *next = s_front[cur ^ 1];
     for (int32_t base = fb; base < fe; base += kKahnB) {
       if (tid == 0) s_nheavy = 0;
       __syncthreads();
       const int32_t i = base + tid;
       if (i < fe) {
-        const int32_t u = F[i];
+        const int32_t u = i - fb < kKahnFront ? front[i - fb] : F[i];
         level[u] = lvl;
         const int32_t e0 = g.out_ptr[u], e1 = g.out_ptr[u + 1];
         if (e1 - e0 > kKahnHeavy) {
           s_heavy[atomicAdd(&s_nheavy, 1)] = u;
         } else {
-          for (int32_t e = e0; e < e1; e++) kahn_release(g, cnt, F, &s_tail, e);
+          for (int32_t eb = e0; eb < e1; eb += kKahnE) {
+            int32_t v[kKahnE], c[kKahnE];
+#pragma unroll
+            for (int q = 0; q < kKahnE; q++) v[q] = eb + q < e1 ? g.out_idx[eb + q] : -1;
+#pragma unroll
+            for (int q = 0; q < kKahnE; q++) c[q] = v[q] >= 0 ? atomicSub(&cnt[v[q]], 1) : 0;
+#pragma unroll
+            for (int q = 0; q < kKahnE; q++)
+              if (c[q] == 1) kahn_append(F, next, &s_tail, fe, v[q]);  // last in-edge removed
+          }
         }
       }
       __syncthreads();
       const int32_t nh = s_nheavy;
       for (int32_t h = 0; h < nh; h++) {
         const int32_t u = s_heavy[h];
-        for (int32_t e = g.out_ptr[u] + tid; e < g.out_ptr[u + 1]; e += kKahnB)
-          kahn_release(g, cnt, F, &s_tail, e);
+        for (int32_t e = g.out_ptr[u] + tid; e < g.out_ptr[u + 1]; e += kKahnB) {
+          const int32_t v = g.out_idx[e];
+          if (atomicSub(&cnt[v], 1) == 1) kahn_append(F, next, &s_tail, fe, v);
+        }
       }
       __syncthreads();
     }
     fb = fe;
     fe = s_tail;
     lvl++;
+    cur ^= 1;
     __syncthreads();  // everyone has read s_tail before the next level appends
   }
   if (tid == 0) {
