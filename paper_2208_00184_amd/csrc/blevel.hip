@@ -47,7 +47,7 @@ __global__ void k_node_costs(int32_t n, const int32_t *order, const int64_t *w, 
 // barrier (a wave sees its own LDS writes in order); wider levels use the
 // whole block.  A node with more than kWinE edges forms a window of its own,
 // all of whose neighbours lie outside it.
-constexpr int kWinN = 1536, kWinE = 6144, kWinL = 256, kPullB = 6, kNarrowB = 256;
+constexpr int kWinN = 2048, kWinE = 8192, kWinL = 256, kPullB = 6, kNarrowB = 256;
 
 template <bool REVERSE, int K>
 __device__ inline int64_t pull_max(int64_t r, const int16_t (*pw)[kWinN + 1], int32_t si,
