@@ -1230,7 +1230,7 @@ extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int3
                                                  st);
     {
       KTimer kt(s, "k_makespan_sweep");
-      k_makespan_one<1024, 1536, 5120><<<1, 1024, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq, devp,
+      k_makespan_one<1024, 1792, 5120><<<1, 1024, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq, devp,
                                                           sx, meta, finp, makespan, st);
     }
     if (start || finish)
