@@ -49,49 +49,94 @@ __global__ void k_node_costs(int32_t n, const int32_t *order, const int64_t *w, 
 // all of whose neighbours lie outside it.
 constexpr int kWinN = 2048, kWinE = 8192, kWinL = 256, kPullB = 6, kNarrowB = 256;
 
-template <bool REVERSE, int K>
-__device__ inline int64_t pull_max(int64_t r, const int16_t (*pw)[kWinN + 1], int32_t si,
-                                   const int64_t *s_v, const int64_t *s_wc) {
-  int32_t j[K];
+// Gathered value of a window slot: s_x[j] = val(j) (REVERSE) or val(j) +
+// wcp(j) (forward), what a neighbour's pull needs; -1 at the dummy slot.
+//
+// Pull maxima of NR rows of 64 slots at once (slot si[u] of row u; kWinN for
+// idle lanes), K gathers per slot: every gather of the rows is issued before
+// the first use (the compiler would otherwise chain the cases of the caller's
+// switch into serial round trips).
+template <int NR, int K, int K0 = 0>
+__device__ inline void rows_pull(int64_t (&r)[NR], const int32_t (&si)[NR],
+                                 const int16_t (*pw)[kWinN + 1], const int64_t *s_x) {
+  int32_t j[NR][K];
 #pragma unroll
-  for (int k = 0; k < K; k++) j[k] = pw[k][si];
-  int64_t v[K], c[K];
+  for (int u = 0; u < NR; u++)
 #pragma unroll
-  for (int k = 0; k < K; k++) {
-    v[k] = s_v[j[k]];
-    c[k] = REVERSE ? 0 : s_wc[j[k]];
-  }
-  // every gather is issued before the first use (the compiler would
-  // otherwise chain the cases of the caller's switch into serial round trips)
+    for (int k = 0; k < K; k++) j[u][k] = pw[K0 + k][si[u]];
+  int64_t x[NR][K];
+#pragma unroll
+  for (int u = 0; u < NR; u++)
+#pragma unroll
+    for (int k = 0; k < K; k++) x[u][k] = s_x[j[u][k]];
   asm volatile("" ::: "memory");
 #pragma unroll
-  for (int k = 0; k < K; k++) {
-    const int64_t x = v[k] + c[k];
-    r = x > r ? x : r;
-  }
-  return r;
+  for (int u = 0; u < NR; u++)
+#pragma unroll
+    for (int k = 0; k < K; k++) r[u] = x[u][k] > r[u] ? x[u][k] : r[u];
 }
 
-// value of slot si (wave-uniform control flow; si = kWinN for idle lanes)
-template <bool REVERSE>
-__device__ inline int64_t slot_val(int32_t si, const int16_t (*pw)[kWinN + 1], const int32_t *s_pc,
-                                   const int64_t *s_pm, const int64_t *s_v, const int64_t *s_wc) {
-  const int32_t pc = s_pc[si];
-  const int64_t pm = s_pm[si], wc = s_wc[si];
-  const int32_t c = pc < kPullB ? pc : kPullB;
+// Values of the NR rows of slots starting at a (slots past b idle); the
+// gathers are unrolled to the largest pull count among the rows' lanes.
+// Returns the values; the caller stores them.
+template <bool REVERSE, int NR>
+__device__ inline void rows_val(int32_t a, int32_t b, int lane, const int16_t (*pw)[kWinN + 1],
+                                const int32_t *s_pc, const int64_t *s_pm, const int64_t *s_x,
+                                const int64_t *s_wc, int64_t (&v)[NR], int64_t (&wc)[NR]) {
+  int32_t si[NR];
+  int64_t r[NR];
+  int32_t c = 0;
+#pragma unroll
+  for (int u = 0; u < NR; u++) {
+    const int32_t s = a + lane + 64 * u;
+    si[u] = s < b ? s : kWinN;
+    const int32_t pc = s_pc[si[u]];
+    r[u] = s_pm[si[u]];
+    wc[u] = s_wc[si[u]];
+    c = pc > c ? pc : c;
+  }
+  c = c < kPullB ? c : kPullB;
   int kmax = 0;
   while (kmax < kPullB && __ballot(c > kmax)) kmax++;
-  int64_t r;
+  // one batch holds at most 12 gathers per lane (registers); more take two
+  constexpr int KB = 12 / NR < kPullB ? 12 / NR : kPullB;
   switch (kmax) {
-    case 0: r = pm; break;
-    case 1: r = pull_max<REVERSE, 1>(pm, pw, si, s_v, s_wc); break;
-    case 2: r = pull_max<REVERSE, 2>(pm, pw, si, s_v, s_wc); break;
-    case 3: r = pull_max<REVERSE, 3>(pm, pw, si, s_v, s_wc); break;
-    case 4: r = pull_max<REVERSE, 4>(pm, pw, si, s_v, s_wc); break;
-    case 5: r = pull_max<REVERSE, 5>(pm, pw, si, s_v, s_wc); break;
-    default: r = pull_max<REVERSE, 6>(pm, pw, si, s_v, s_wc); break;
+    case 0: break;
+    case 1: rows_pull<NR, 1>(r, si, pw, s_x); break;
+    case 2: rows_pull<NR, 2>(r, si, pw, s_x); break;
+    case 3: rows_pull<NR, (3 < KB ? 3 : KB)>(r, si, pw, s_x);
+      if constexpr (KB < 3) rows_pull<NR, 3 - KB, KB>(r, si, pw, s_x);
+      break;
+    case 4: rows_pull<NR, (4 < KB ? 4 : KB)>(r, si, pw, s_x);
+      if constexpr (KB < 4) rows_pull<NR, 4 - KB, KB>(r, si, pw, s_x);
+      break;
+    case 5: rows_pull<NR, (5 < KB ? 5 : KB)>(r, si, pw, s_x);
+      if constexpr (KB < 5) rows_pull<NR, 5 - KB, KB>(r, si, pw, s_x);
+      break;
+    default: rows_pull<NR, (6 < KB ? 6 : KB)>(r, si, pw, s_x);
+      if constexpr (KB < 6) rows_pull<NR, 6 - KB, KB>(r, si, pw, s_x);
+      break;
   }
-  return REVERSE ? wc + r : (r > 0 ? r : 0);
+#pragma unroll
+  for (int u = 0; u < NR; u++) v[u] = REVERSE ? wc[u] + r[u] : (r[u] > 0 ? r[u] : 0);
+}
+
+// Narrow level [a, b) of at most 4 rows, run by one wave: values, then the
+// window copy (the pull value) and the global output
+template <bool REVERSE, int NR>
+__device__ inline void narrow_level(int32_t a, int32_t b, int lane, const int16_t (*pw)[kWinN + 1],
+                                    const int32_t *s_pc, const int64_t *s_pm, int64_t *s_x,
+                                    const int64_t *s_wc, int64_t *valP0) {
+  int64_t v[NR], wc[NR];
+  rows_val<REVERSE, NR>(a, b, lane, pw, s_pc, s_pm, s_x, s_wc, v, wc);
+#pragma unroll
+  for (int u = 0; u < NR; u++) {
+    const int32_t s = a + lane + 64 * u;
+    if (s < b) {
+      s_x[s] = REVERSE ? v[u] : v[u] + wc[u];
+      valP0[s] = v[u];
+    }
+  }
 }
 
 template <bool REVERSE>
@@ -107,7 +152,7 @@ __global__ void __launch_bounds__(kSweepB)
   __shared__ int16_t s_pw[kPullB][kWinN + 1];  // pull lists
   __shared__ int32_t s_pc[kWinN + 1];  // in-window neighbours per slot
   __shared__ int64_t s_pm[kWinN + 1];  // partial max over neighbours, -1 if none yet
-  __shared__ int64_t s_v[kWinN + 1];   // values computed in this window (-1 at the dummy)
+  __shared__ int64_t s_x[kWinN + 1];   // pull values of this window's slots (-1 at the dummy)
   __shared__ int64_t s_wc[kWinN + 1];  // wcp (w for a sink in REVERSE) of the window's nodes
   __shared__ int32_t s_la[kWinL], s_lb[kWinL], s_lea[kWinL], s_leb[kWinL], s_lend[kWinL];
   __shared__ int32_t s_lov[kWinL];
@@ -118,7 +163,7 @@ __global__ void __launch_bounds__(kSweepB)
   if (tid == 0) {
     s_pc[kWinN] = 0;
     s_pm[kWinN] = -1;
-    s_v[kWinN] = -1;
+    s_x[kWinN] = -1;
     s_wc[kWinN] = 0;
   }
   if (tid < kPullB) s_pw[tid][kWinN] = kWinN;
@@ -298,22 +343,18 @@ __global__ void __launch_bounds__(kSweepB)
             if (fl & 2) {  // in-window neighbours past the pull lists
               for (int32_t e = ea + lane; e < eb; e += 64) {
                 const int32_t wd = s_epk[e];
-                const int32_t j = wd & 0xFFFF;
-                const int64_t x = REVERSE ? s_v[j] : s_v[j] + s_wc[j];
-                atomicMax((long long *)&s_pm[wd >> 16], (long long)x);
+                atomicMax((long long *)&s_pm[wd >> 16], (long long)s_x[wd & 0xFFFF]);
               }
               lds_order();
             }
-            for (int32_t r0 = a; r0 < b; r0 += 64) {
-              const int32_t s = r0 + lane;
-              const bool act = s < b;
-              const int64_t v = slot_val<REVERSE>(act ? s : kWinN, s_pw, s_pc, s_pm, s_v, s_wc);
-              if (act) {
-                s_v[s] = v;
-                val[P0 + s] = v;
-              }
-              lds_order();
+            // all rows of the level at once: their gathers share round trips
+            switch ((b - a + 63) >> 6) {
+              case 1: narrow_level<REVERSE, 1>(a, b, lane, s_pw, s_pc, s_pm, s_x, s_wc, val + P0); break;
+              case 2: narrow_level<REVERSE, 2>(a, b, lane, s_pw, s_pc, s_pm, s_x, s_wc, val + P0); break;
+              case 3: narrow_level<REVERSE, 3>(a, b, lane, s_pw, s_pc, s_pm, s_x, s_wc, val + P0); break;
+              default: narrow_level<REVERSE, 4>(a, b, lane, s_pw, s_pc, s_pm, s_x, s_wc, val + P0); break;
             }
+            lds_order();
           }
           CEL_TSTAMP(tl1);
           CEL_TADD(REVERSE ? 7 : 16 + 7, tl0, tl1);
@@ -323,16 +364,18 @@ __global__ void __launch_bounds__(kSweepB)
           if (fl & 2) {
             for (int32_t e = ea + tid; e < eb; e += kSweepB) {
               const int32_t wd = s_epk[e];
-              const int32_t j = wd & 0xFFFF;
-              const int64_t x = REVERSE ? s_v[j] : s_v[j] + s_wc[j];
-              atomicMax((long long *)&s_pm[wd >> 16], (long long)x);
+              atomicMax((long long *)&s_pm[wd >> 16], (long long)s_x[wd & 0xFFFF]);
             }
             __syncthreads();
           }
-          for (int32_t i = a + tid; i < b; i += kSweepB) {
-            const int64_t v = slot_val<REVERSE>(i, s_pw, s_pc, s_pm, s_v, s_wc);
-            s_v[i] = v;
-            val[P0 + i] = v;
+          for (int32_t i0 = a + (tid & ~63); i0 < b; i0 += kSweepB) {  // a row per wave
+            int64_t v[1], wc[1];
+            rows_val<REVERSE, 1>(i0, b, lane, s_pw, s_pc, s_pm, s_x, s_wc, v, wc);
+            const int32_t i = i0 + lane;
+            if (i < b) {
+              s_x[i] = REVERSE ? v[0] : v[0] + wc[0];
+              val[P0 + i] = v[0];
+            }
           }
           __syncthreads();
           CEL_TSTAMP(tl1);
