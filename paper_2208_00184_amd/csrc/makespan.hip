@@ -17,6 +17,8 @@
 //
 // One workgroup evaluates one placement; a batch of K placements runs K
 // independent workgroups that share the graph structure through L2/MALL.
+#include <type_traits>
+
 #include "cel_internal.h"
 
 namespace cel {
@@ -538,6 +540,58 @@ __device__ inline int64_t ms_pull(int64_t r, const uint32_t (&pw)[4], const int6
   return r;
 }
 
+// Rows form of ms_pull: pulls K0 .. K0 + K - 1 of NR rows (row u's packed
+// list in cur[u].pw), all gathers issued before the first use.
+template <int NR, int K, int K0, class RP>
+__device__ inline void ms_pull_rows(int64_t (&r)[NR], const RP (&cur)[NR], const int64_t *s_f,
+                                    const int64_t *s_c) {
+  int64_t f[NR][K], c[NR][K];
+#pragma unroll
+  for (int u = 0; u < NR; u++)
+#pragma unroll
+    for (int k = 0; k < K; k++) {
+      const int kk = K0 + k;
+      const int32_t j = (cur[u].pw[kk >> 1] >> (16 * (kk & 1))) & 0xFFF;
+      f[u][k] = s_f[j];
+      c[u][k] = s_c[j];
+    }
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int u = 0; u < NR; u++)
+#pragma unroll
+    for (int k = 0; k < K; k++) {
+      const int kk = K0 + k;
+      const bool cross = (cur[u].pw[kk >> 1] >> (16 * (kk & 1) + 12)) & 1;
+      const int64_t x = f[u][k] + (cross ? c[u][k] : 0);
+      r[u] = x > r[u] ? x : r[u];
+    }
+}
+
+// Pulls K0 .. kmax - 1 of NR rows in batches small enough for the registers.
+template <int NR, int K0, class RP>
+__device__ inline void ms_pull_from(int kmax, int64_t (&r)[NR], const RP (&cur)[NR],
+                                    const int64_t *s_f, const int64_t *s_c) {
+  constexpr int KB = NR == 1 ? 8 : 4;
+  if constexpr (K0 < 8) {
+    const int left = kmax - K0;
+    if (left <= 0) return;
+    if (left >= KB) {
+      ms_pull_rows<NR, KB, K0>(r, cur, s_f, s_c);
+      ms_pull_from<NR, K0 + KB>(kmax, r, cur, s_f, s_c);
+      return;
+    }
+    switch (left) {
+      case 1: ms_pull_rows<NR, 1, K0>(r, cur, s_f, s_c); break;
+      case 2: if constexpr (KB > 2) ms_pull_rows<NR, 2, K0>(r, cur, s_f, s_c); break;
+      case 3: if constexpr (KB > 3) ms_pull_rows<NR, 3, K0>(r, cur, s_f, s_c); break;
+      case 4: if constexpr (KB > 4) ms_pull_rows<NR, 4, K0>(r, cur, s_f, s_c); break;
+      case 5: if constexpr (KB > 5) ms_pull_rows<NR, 5, K0>(r, cur, s_f, s_c); break;
+      case 6: if constexpr (KB > 6) ms_pull_rows<NR, 6, K0>(r, cur, s_f, s_c); break;
+      default: if constexpr (KB > 7) ms_pull_rows<NR, 7, K0>(r, cur, s_f, s_c); break;
+    }
+  }
+}
+
 __device__ inline int64_t readlane64(int64_t v, int l) {
   const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int32_t)v, l);
   const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int32_t)(v >> 32), l);
@@ -660,6 +714,53 @@ __global__ void __launch_bounds__(B)
   };
   int64_t mk = 0;
   int32_t P0 = 0, lcur = 0;
+  // NR (1 or 2) rows of a narrow level starting at slot r0 (slots from b0
+  // idle), run by wave 0; carry: the run value at the end of the previous row
+  auto narrow_rows = [&](auto nrc, int32_t r0, int32_t b0, int64_t &carry) {
+    constexpr int NR = decltype(nrc)::value;
+    RowPre cur[NR];
+    int32_t si[NR];
+    int32_t cmax = 0;
+#pragma unroll
+    for (int u = 0; u < NR; u++) {
+      const int32_t s = r0 + lane + 64 * u;
+      si[u] = s < b0 ? s : NC;
+      cur[u] = row_pre(si[u]);
+      cmax = cur[u].pc > cmax ? cur[u].pc : cmax;
+    }
+    const int kmax = row_kmax(cmax);
+    int64_t r[NR], av[NR];
+#pragma unroll
+    for (int u = 0; u < NR; u++) {
+      r[u] = s_pm[si[u]];
+      av[u] = s_avail[cur[u].meta & 255];  // free times as of the level's start
+    }
+    ms_pull_from<NR, 0>(kmax, r, cur, s_f, s_c);
+    int64_t y[NR];
+#pragma unroll
+    for (int u = 0; u < NR; u++) {
+      y[u] = r[u] - cur[u].sx;
+      const int64_t viafree = av[u] - cur[u].sx;
+      if ((cur[u].meta >> 16) == 0 && viafree > y[u]) y[u] = viafree;
+      y[u] = wave_seg_pmax(y[u], cur[u].meta >> 16, lane);
+    }
+#pragma unroll
+    for (int u = 0; u < NR; u++) {  // a run that began in an earlier row
+      if ((cur[u].meta >> 16) > lane && carry > y[u]) y[u] = carry;
+      if (u + 1 < NR || r0 + 64 * NR < b0) carry = readlane64(y[u], 63);
+    }
+#pragma unroll
+    for (int u = 0; u < NR; u++) {
+      const int32_t s = r0 + lane + 64 * u;
+      if (s < b0) {
+        const int64_t fin = cur[u].sx + cur[u].w + y[u];
+        s_f[s] = fin;
+        finp[P0 + s] = fin;
+        mk = fin > mk ? fin : mk;
+        if (cur[u].meta & 256) s_avail[cur[u].meta & 255] = fin;
+      }
+    }
+  };
   while (P0 < n) {
     CEL_TSTAMP(t0);
     CEL_TCOUNT(6);
@@ -815,25 +916,12 @@ __global__ void __launch_bounds__(B)
               }
               lds_order();
             }
+            // rows in pairs: gathers and scans of the two rows are
+            // independent; only the carry chains the rows
             int64_t carry = kNeg;
-            for (int32_t r0 = a0; r0 < b0; r0 += 64) {
-              CEL_TCOUNT(11);
-              const int32_t s = r0 + lane;
-              const bool act = s < b0;
-              const int32_t si = act ? s : NC;
-              const RowPre cur = row_pre(si);
-              int64_t y = row_value(si, cur, row_kmax(cur.pc));
-              const int32_t hd = cur.meta >> 16;
-              y = wave_seg_pmax(y, hd, lane);
-              if (hd > lane && carry > y) y = carry;  // the run began in an earlier row
-              const int64_t fin = cur.sx + cur.w + y;
-              if (act) {
-                s_f[s] = fin;
-                finp[P0 + s] = fin;
-                mk = fin > mk ? fin : mk;
-                if (cur.meta & 256) s_avail[cur.meta & 255] = fin;
-              }
-              if (r0 + 64 < b0) carry = readlane64(y, 63);
+            for (int32_t r0 = a0; r0 < b0; r0 += 128) {
+              if (b0 - r0 > 64) narrow_rows(std::integral_constant<int, 2>(), r0, b0, carry);
+              else narrow_rows(std::integral_constant<int, 1>(), r0, b0, carry);
               lds_order();
             }
           }
