@@ -251,8 +251,14 @@ __global__ void __launch_bounds__(kSweepB)
     // stage edges: neighbours outside the window are final (each thread takes
     // EU edges per pass: all index loads, then all value gathers, in flight
     // together)
+    if (heavy) {  // a single node with more than kWinE edges, all outside the window
+      const int64_t mx = heavy_max<kHeavyU, kSweepB>(
+          E0, E1, tid, [&](int32_t e) { return ridx[e]; },
+          [&](int32_t r) { return REVERSE ? val[r] : val[r] + wcp[r]; });
+      if ((tid & 63) == 0 && mx >= 0) atomicMax((long long *)&s_pm[0], (long long)mx);
+    }
     constexpr int EU = (kWinE + kSweepB - 1) / kSweepB;
-    for (int32_t e0 = E0 + tid; e0 < E1; e0 += EU * kSweepB) {
+    for (int32_t e0 = E0 + tid; !heavy && e0 < E1; e0 += EU * kSweepB) {
       int32_t rr[EU];
 #pragma unroll
       for (int u = 0; u < EU; u++) {

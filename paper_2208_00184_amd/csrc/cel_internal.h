@@ -127,6 +127,43 @@ __device__ inline int32_t owner_of(const int32_t *rp, int32_t nrows, int32_t rec
   return lo;
 }
 
+// Maximum of value(index(e)) over the edges [e0, e1) of a node with too many
+// neighbours for a sweep window, taken by the whole block: thread tid takes
+// every B-th edge, keeping U index loads and then U value loads in flight
+// (the next group's indices are requested before this group's values), and
+// the lanes of each wave then combine theirs.  Values are >= 0; the result
+// (-1 when the wave saw no edge) is the same in every lane of a wave.
+constexpr int kHeavyU = 8;
+template <int U, int B, class IndexF, class ValueF>
+__device__ inline int64_t heavy_max(int32_t e0, int32_t e1, int tid, IndexF index, ValueF value) {
+  int64_t mx = -1;
+  int32_t rn[U];
+#pragma unroll
+  for (int u = 0; u < U; u++) {
+    const int64_t e = (int64_t)e0 + tid + (int64_t)u * B;
+    rn[u] = e < e1 ? index((int32_t)e) : -1;
+  }
+  for (int64_t base = e0; base < e1; base += (int64_t)U * B) {
+    int32_t r[U];
+#pragma unroll
+    for (int u = 0; u < U; u++) {
+      r[u] = rn[u];
+      const int64_t e = base + (int64_t)U * B + tid + (int64_t)u * B;
+      rn[u] = e < e1 ? index((int32_t)e) : -1;
+    }
+    int64_t x[U];
+#pragma unroll
+    for (int u = 0; u < U; u++) x[u] = r[u] >= 0 ? value(r[u]) : -1;
+#pragma unroll
+    for (int u = 0; u < U; u++) mx = x[u] > mx ? x[u] : mx;
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const int64_t o = __shfl_xor((long long)mx, off);
+    mx = o > mx ? o : mx;
+  }
+  return mx;
+}
+
 // Edge-balanced CSR traversal: block b takes edges [b * kEdgesPB, +kEdgesPB)
 // whatever their sources, so a node of huge out-degree is spread over many
 // blocks.  Wave 0 finds the rows of the slice's first and last edge by a

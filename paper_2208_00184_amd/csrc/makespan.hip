@@ -642,8 +642,10 @@ __global__ void __launch_bounds__(B)
   __shared__ int32_t s_meta[NC + 1];
   __shared__ uint4 s_pw[NC + 1];  // pull lists: F = 8 words of 16 bits per slot
   __shared__ int32_t s_pc[NC + 1];
-  __shared__ int32_t s_la[kMsL], s_lb[kMsL], s_lea[kMsL], s_leb[kMsL], s_lend[kMsL];
-  __shared__ int32_t s_lov[kMsL];
+  // per level of the window: first slot | end slot << 12 | window ends in
+  // it << 24 | has overflow words << 25, and its in-edge range ea | eb << 15
+  __shared__ int32_t s_ld[kMsL], s_le[kMsL];
+  static_assert(EC < 32768, "edge range fields are 15 bits");
   __shared__ int64_t s_avail[256];
   __shared__ int64_t s_wy[2][NW], s_cy[2];
   __shared__ int64_t s_red[NW];
@@ -714,6 +716,11 @@ __global__ void __launch_bounds__(B)
   };
   int64_t mk = 0;
   int32_t P0 = 0, lcur = 0;
+  int32_t E0 = 0;                       // edge offset of P0, pptr[P0]
+  int32_t prev_lo = 0;                  // the previous window [prev_lo, P0), still in LDS
+  const int32_t m = pptr[n];
+  constexpr int NU = (NC + B - 1) / B;  // candidate positions per thread
+  constexpr int EU = (EC + B - 1) / B;  // candidate edges per thread
   // NR (1 or 2) rows of a narrow level starting at slot r0 (slots from b0
   // idle), run by wave 0; carry: the run value at the end of the previous row
   auto narrow_rows = [&](auto nrc, int32_t r0, int32_t b0, int64_t &carry) {
@@ -765,13 +772,76 @@ __global__ void __launch_bounds__(B)
     CEL_TSTAMP(t0);
     CEL_TCOUNT(6);
     const int32_t Pc1 = P0 + NC < n ? P0 + NC : n;
-    for (int t = tid; t <= Pc1 - P0; t += B) s_rp[t] = pptr[P0 + t];
-    for (int t = tid; t < EC; t += B) s_own[t] = -1;
-    for (int k = tid; k <= kMsL + 1; k += B) {
-      const int32_t l = lcur + k;  // level lcur + k is [s_lv[k], s_lv[k+1])
-      s_lv[k] = lp[l > L ? L : l];
+    // P0 and its edge offset are fixed, so every global load the staging
+    // needs that does not depend on the cut is issued before the first wait:
+    // the candidate positions [P0, Pc1) and the candidate edges
+    // [E0, E0 + EC), which hold the edges of any window that is not a single
+    // heavy node
+    const int32_t efar = pptr[Pc1];  // uniform
+    constexpr int NRW = (NC + 1 + B - 1) / B;
+    int32_t rpv[NRW];
+#pragma unroll
+    for (int k = 0; k < NRW; k++) {
+      const int32_t t = tid + k * B;
+      rpv[k] = t <= Pc1 - P0 ? pptr[P0 + t] : 0;
     }
+    const int32_t Elim = E0 + EC < m ? E0 + EC : m;
+    int32_t qq[EU];
+#pragma unroll
+    for (int u = 0; u < EU; u++) {
+      const int32_t e = E0 + tid + u * B;
+      qq[u] = (u * B + tid < EC && e < Elim) ? pidx[e] : P0;  // P0: in-window, nothing gathered
+    }
+    int32_t cmt[NU];
+    int64_t cwv[NU], ccv[NU], csx[NU];
+#pragma unroll
+    for (int k = 0; k < NU; k++) {
+      const int32_t p = P0 + tid + k * B;
+      const bool ok = k * B + tid < NC && p < Pc1;
+      cmt[k] = ok ? metap[p] : 0;
+      cwv[k] = ok ? wp[p] : 0;
+      ccv[k] = ok ? cq[p] : 0;
+      csx[k] = ok ? sxp[p] : 0;
+    }
+    static_assert(kMsL + 2 <= B, "one level bound per thread");
+    int32_t lvv = 0;
+    if (tid <= kMsL + 1) {
+      const int32_t l = lcur + tid;  // level lcur + k is [s_lv[k], s_lv[k+1])
+      lvv = lp[l > L ? L : l];
+    }
+    for (int t = tid; t < EC; t += B) s_own[t] = -1;
     if (tid == 0) s_cut = 0;
+#pragma unroll
+    for (int k = 0; k < NRW; k++) {
+      const int32_t t = tid + k * B;
+      if (t <= Pc1 - P0) s_rp[t] = rpv[k];
+    }
+    if (tid <= kMsL + 1) s_lv[tid] = lvv;
+    // predecessors before the window are final: finish time, device and
+    // transfer cost of those in the previous window are read from its LDS
+    // copy before the node staging below overwrites it; older ones are
+    // gathered, in flight across the barriers (edges past the candidate
+    // positions' own, e >= efar, are skipped)
+    int64_t fq[EU], cqq[EU];
+    int32_t dq[EU];
+#pragma unroll
+    for (int u = 0; u < EU; u++) {
+      const int32_t q = qq[u];
+      const bool cand = E0 + tid + u * B < efar;
+      fq[u] = 0;
+      dq[u] = 0;
+      cqq[u] = 0;
+      if (cand && q < prev_lo) {
+        fq[u] = finp[q];
+        dq[u] = devp[q];
+        cqq[u] = cq[q];
+      } else if (cand && q < P0) {
+        const int32_t j = q - prev_lo;
+        fq[u] = s_f[j];
+        dq[u] = s_meta[j] & 255;
+        cqq[u] = s_c[j];
+      }
+    }
     __syncthreads();
     int32_t cnt = 0;
     for (int t = tid; t < Pc1 - P0; t += B) cnt += (s_rp[t + 1] - s_rp[0] <= EC) ? 1 : 0;
@@ -784,17 +854,19 @@ __global__ void __launch_bounds__(B)
     const bool heavy = (P1 == P0);  // one node with more than EC predecessors
     if (heavy) P1 = P0 + 1;
     const int32_t NN = P1 - P0;
-    const int32_t E0 = s_rp[0], E1 = s_rp[NN];
-    for (int32_t i = tid; i < NN; i += B) {
-      const int32_t p = P0 + i;
-      const int32_t mt = metap[p];
+    const int32_t E1 = s_rp[NN];
+#pragma unroll
+    for (int k = 0; k < NU; k++) {
+      const int32_t i = tid + k * B;
+      if (i >= NN) continue;
+      const int32_t mt = cmt[k];
       int32_t hd = mt >> 16;
       hd = hd < i ? hd : i;  // the window's first slot starts a run part ...
       const int32_t tl = ((mt >> 8) & 1) | (i == NN - 1);  // ... and its last slot ends one
       s_meta[i] = (mt & 255) | (tl << 8) | (hd << 16);
-      s_w[i] = wp[p];
-      s_c[i] = cq[p];
-      s_sx[i] = sxp[p];
+      s_w[i] = cwv[k];
+      s_c[i] = ccv[k];
+      s_sx[i] = csx[k];
       s_pm[i] = 0;
       s_pc[i] = 0;
       s_pw[i] = make_uint4(kPw2, kPw2, kPw2, kPw2);  // rows gather past a short list
@@ -809,46 +881,20 @@ __global__ void __launch_bounds__(B)
       int32_t a = lb < P0 ? P0 : (lb > P1 ? P1 : lb);
       const int32_t b = le < P0 ? P0 : (le > P1 ? P1 : le);
       if (a > b) a = b;
-      s_la[k] = a - P0;
-      s_lb[k] = b - P0;
-      s_lea[k] = heavy ? 0 : s_rp[a - P0] - E0;
-      s_leb[k] = heavy ? 0 : s_rp[b - P0] - E0;
-      s_lend[k] = le >= P1;
-      s_lov[k] = 0;
+      s_ld[k] = (a - P0) | ((b - P0) << 12) | ((int32_t)(le >= P1) << 24);
+      s_le[k] = heavy ? 0 : (s_rp[a - P0] - E0) | ((s_rp[b - P0] - E0) << 15);
     }
     __syncthreads();
     CEL_TSTAMP(t1);
     CEL_TADD(0, t0, t1);
     // in-edges: pull lists and overflow words; predecessors before the window
     // are final and are folded into the owner's partial ready time
-    // (each thread takes EU edges per pass: all index loads, then all
-    // predecessor gathers, are in flight together)
-    constexpr int EU = (EC + B - 1) / B;
-    for (int32_t e0 = E0 + tid; e0 < E1; e0 += EU * B) {
-      int32_t qq[EU];
-#pragma unroll
-      for (int u = 0; u < EU; u++) {
-        const int32_t e = e0 + u * B;
-        qq[u] = e < E1 ? pidx[e] : P0;
-      }
-      int64_t fq[EU], cqq[EU];
-      int32_t dq[EU];
-#pragma unroll
-      for (int u = 0; u < EU; u++) {  // unconditional: in-window predecessors read a final slot
-        const int32_t qs = qq[u] < P0 ? qq[u] : 0;
-        fq[u] = finp[qs];
-        dq[u] = devp[qs];
-        cqq[u] = cq[qs];
-      }
-#pragma unroll
-      for (int u = 0; u < EU; u++) {
-        const int32_t e = e0 + u * B;
-        if (e >= E1) break;
-        const int32_t q = qq[u];
-        const int32_t own = heavy ? 0 : owner_of(s_rp, NN, s_own[e - E0], e);
+    if (!heavy) {
+      auto stage_edge = [&](int32_t e, int32_t q, int64_t fqv, int32_t dqv, int64_t cqv) {
+        const int32_t own = owner_of(s_rp, NN, s_own[e - E0], e);
         const int dvo = s_meta[own] & 255;
         int32_t word = kNoop;
-        if (q >= P0) {  // never for a heavy window: its predecessors all precede it
+        if (q >= P0) {
           const int32_t j = q - P0;
           const int32_t pwd = j | ((int32_t)((s_meta[j] & 255) != dvo) << 12);
           const int32_t kk = atomicAdd(&s_pc[own], 1);
@@ -862,14 +908,25 @@ __global__ void __launch_bounds__(B)
               if (s_lv[mid] <= P0 + own) lo = mid;
               else hi = mid - 1;
             }
-            s_lov[lo] = 1;
+            atomicOr(&s_ld[lo], 1 << 25);
           }
         } else {
-          const int64_t x = fq[u] + (dq[u] != dvo ? cqq[u] : 0);
+          const int64_t x = fqv + (dqv != dvo ? cqv : 0);
           atomicMax((long long *)&s_pm[own], (long long)x);
         }
-        if (!heavy) s_epk[e - E0] = word;
+        s_epk[e - E0] = word;
+      };
+#pragma unroll
+      for (int u = 0; u < EU; u++) {
+        const int32_t e = E0 + tid + u * B;
+        if (u * B + tid < EC && e < E1) stage_edge(e, qq[u], fq[u], dq[u], cqq[u]);
       }
+    } else {  // a single node with more than EC predecessors, all before it
+      const int dv0 = s_meta[0] & 255;
+      const int64_t mx = heavy_max<kHeavyU, B>(
+          E0, E1, tid, [&](int32_t e) { return pidx[e]; },
+          [&](int32_t q) { return finp[q] + (devp[q] != dv0 ? cq[q] : 0); });
+      if (lane == 0 && mx >= 0) atomicMax((long long *)&s_pm[0], (long long)mx);
     }
     __syncthreads();
     CEL_TSTAMP(t2);
@@ -880,7 +937,7 @@ __global__ void __launch_bounds__(B)
 #pragma unroll
     for (int u = 0; u < 4; u++) {
       const int k = lane + 64 * u;
-      lvm[u] = s_la[k] | (s_lb[k] << 12) | (s_lend[k] << 24) | (s_lov[k] << 25);
+      lvm[u] = s_ld[k];
     }
     auto level_desc = [&](int32_t kk) {
       int32_t t;
@@ -903,7 +960,7 @@ __global__ void __launch_bounds__(B)
       const int32_t dsc = level_desc(k);
       const int32_t a0 = dsc & 0xFFF, b0 = (dsc >> 12) & 0xFFF, fl = dsc >> 24;
       if (a0 < b0) {
-        const int32_t ea = (fl & 2) ? s_lea[k] : 0, eb = (fl & 2) ? s_leb[k] : 0;
+        const int32_t le = (fl & 2) ? s_le[k] : 0, ea = le & 0x7FFF, eb = le >> 15;
         CEL_TSTAMP(tl0);
         if (b0 - a0 <= kNarrow) {
           if (wave0) {
@@ -986,7 +1043,9 @@ __global__ void __launch_bounds__(B)
       while (k < kMsL && lcur + k + 1 < L && s_lv[k + 1] <= P1) k++;
       lcur += k;
     }
+    prev_lo = P0;
     P0 = P1;
+    E0 = E1;
     __syncthreads();
   }
   for (int off = 32; off > 0; off >>= 1) {

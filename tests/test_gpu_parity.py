@@ -256,6 +256,35 @@ def test_heavy_fanout_node():
     assert_topo_blevel(wl, rt, rb, gt, gb)
 
 
+def test_heavy_window_nodes():
+    """Nodes with more neighbours than a sweep window holds edges: a source with
+    9,999 successors (b-level), a sink with 10,000 predecessors (t-level and
+    makespan), both between ordinary levels, for every sweep and both
+    makespan paths."""
+    n = 24000
+    rng = np.random.default_rng(13)
+    edges = [(0, j) for j in range(1, 10000)]
+    edges += [(j, 23999) for j in range(10000, 20000)]
+    edges += [(j, 10000 + int(rng.integers(0, 10000))) for j in range(1, 10000)]
+    edges += [(20000 + (j % 3999), 20001 + (j % 3998)) for j in range(0, 3998)]
+    edges += [(j, 20000 + int(rng.integers(0, 3999))) for j in range(10000, 20000, 7)]
+    edges = sorted(set((u, v) for u, v in edges if u < v))
+    wl = from_edges(n, edges, rng.integers(1, 50, n), rng.integers(0, 900, n), 5,
+                    [10 ** 12] * 5, 4, 2)
+    rt = O.topo_levels(wl)
+    rb = O.blevel(wl, rt[0], rt[1])
+    g, d, gt, gb = run_topo_blevel(wl)
+    assert_topo_blevel(wl, rt, rb, gt, gb)
+    lev, oid, lp, L = rt
+    P = random_placements(wl, 3, 5)
+    ref_ms, _, ref_fi = O.makespan(wl, rb[2], P)
+    args = (tt(rb[2], np.int32), tt(lev, np.int32), tt(lp, np.int32), L)
+    ms, _, fi = cel.makespan(g, d, *args, tt(P, np.uint8), want_times=True)
+    assert np.array_equal(np_(ms), ref_ms) and np.array_equal(np_(fi), ref_fi)
+    ms1, _, fi1 = cel.makespan(g, d, *args, tt(P[1], np.uint8), want_times=True)
+    assert np_(ms1)[0] == ref_ms[1] and np.array_equal(np_(fi1)[0], ref_fi[1])
+
+
 # -------------------------------------------------------------- edge cases
 
 
