@@ -1,80 +1,197 @@
 // cel_topo_levels: level-synchronous Kahn ordering (Section 4.2.2).
 //
-// One workgroup runs all levels: a level costs a few dependent L2 round trips
-// (frontier id -> adjacency -> in-degree atomic), so keeping the whole loop in
-// one workgroup with workgroup barriers is far cheaper than one launch or one
-// grid-wide barrier per level.  Frontiers are appended to the caller's
+// One workgroup runs all levels: a level costs dependent L2 round trips, so
+// keeping the whole loop in one workgroup with workgroup barriers is far
+// cheaper than one launch or one grid-wide barrier per level.  Frontier
+// entries carry their node's adjacency, which leaves one round trip (the
+// in-degree atomics) per level for nodes of small degree.  Frontiers are appended to the caller's
 // order_id buffer; each level's slice is then sorted by id.
 #include "cel_internal.h"
 
 namespace cel {
 
 constexpr int kKahnB = 1024;
-constexpr int kKahnHeavy = 64;    // out-degree above which the whole block shares a node
-constexpr int kKahnFront = 8192;  // frontier entries mirrored in LDS
-constexpr int kKahnE = 4;         // out-edges per node whose loads and atomics go out together
+constexpr int kKahnNW = kKahnB / 64;
+constexpr int kKahnA = 4;         // successors carried with a frontier entry
+constexpr int kKahnCap = 2048;    // frontier entries mirrored in LDS
+constexpr int kKahnE = 4;         // edges per thread whose loads and atomics go out together
 
-// Removes edge e's target's in-edge; the node that removes the last one
-// appends the target to the next frontier (global order, and the LDS mirror
-// while it has room).
-__device__ inline void kahn_append(int32_t *F, int32_t *s_front, int32_t *s_tail, int32_t fe,
-                                   int32_t v) {
-  const int32_t k = atomicAdd(s_tail, 1);
-  F[k] = v;
-  if (k - fe < kKahnFront) s_front[k - fe] = v;
+// Per node: out-degree and its first kKahnA successors (-1 past the end), so
+// that a node that becomes ready brings its adjacency along with it.
+__global__ void k_kahn_prep(int32_t n, const int32_t *out_ptr, const int32_t *out_idx,
+                            int32_t *deg, int4 *adj, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t e0 = out_ptr[v], d = out_ptr[v + 1] - e0;
+    deg[v] = d;
+    adj[v] = make_int4(d > 0 ? out_idx[e0] : -1, d > 1 ? out_idx[e0 + 1] : -1,
+                       d > 2 ? out_idx[e0 + 2] : -1, d > 3 ? out_idx[e0 + 3] : -1);
+  }
 }
 
-__global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, int32_t *F,
-                                                 int32_t *level, int32_t *lstart, Status *st) {
-  __shared__ int32_t s_tail, s_nheavy;
-  __shared__ int32_t s_heavy[kKahnB];
-  __shared__ int32_t s_front[2][kKahnFront];  // the frontier being read, the one being built
+__device__ inline int32_t int4_at(const int4 &a, int q) {
+  return q == 0 ? a.x : (q == 1 ? a.y : (q == 2 ? a.z : a.w));
+}
+
+// Appends v (with its degree and first successors) to the frontier being
+// built, for the lanes with want set: one LDS atomic per wave reserves the
+// wave's slots.  F holds every frontier in order; the LDS mirror holds the
+// first kKahnCap entries of the one being built (fe: its first index).
+__device__ inline void kahn_append(bool want, int32_t v, int32_t d, const int4 &a, int32_t *F,
+                                   int32_t *s_tail, int32_t fe, int32_t *s_fv, int32_t *s_fd,
+                                   int4 *s_fa) {
+  const uint64_t m = __ballot(want);
+  if (m == 0) return;
+  const int leader = __builtin_ctzll(m);
+  int32_t base = 0;
+  if ((int)(threadIdx.x & 63) == leader) base = atomicAdd(s_tail, __popcll(m));
+  base = __shfl(base, leader);
+  if (!want) return;
+  const int32_t k =
+      base + (int32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+  F[k] = v;
+  if (k - fe < kKahnCap) {
+    s_fv[k - fe] = v;
+    s_fd[k - fe] = d;
+    s_fa[k - fe] = a;
+  }
+}
+
+// Level-synchronous Kahn in one workgroup.  A frontier node of degree at most
+// kKahnA removes its in-edge from each successor with a global atomic; the
+// successor's degree and first successors are loaded in the same round, so
+// the node that the last removal makes ready joins the next frontier with its
+// adjacency.  Nodes of higher degree are listed and their edges then spread
+// over the whole block (flattened by a prefix sum of the degrees).
+__global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, const int32_t *deg,
+                                                 const int4 *adj, int32_t *F, int32_t *level,
+                                                 int32_t *lstart, Status *st) {
+  __shared__ int32_t s_tail, s_nh;
+  __shared__ int32_t s_fv[2][kKahnCap], s_fd[2][kKahnCap];
+  __shared__ int4 s_fa[2][kKahnCap];
+  __shared__ int32_t s_hv[kKahnB], s_hd[kKahnB], s_he[kKahnB], s_hp[kKahnB + 1];
+  __shared__ int32_t s_wt[kKahnNW];
   if (failed(st)) return;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t n = g.n;
   if (tid == 0) s_tail = 0;
   __syncthreads();
-  for (int32_t v = tid; v < n; v += kKahnB)
-    if (cnt[v] == 0) kahn_append(F, s_front[0], &s_tail, 0, v);
+  for (int32_t v0 = 0; v0 < n; v0 += kKahnB) {  // sources
+    const int32_t v = v0 + tid;
+    const bool src = v < n && cnt[v] == 0;
+    const int32_t d = src ? deg[v] : 0;
+    const int4 a = src ? adj[v] : make_int4(-1, -1, -1, -1);
+    kahn_append(src, v, d, a, F, &s_tail, 0, s_fv[0], s_fd[0], s_fa[0]);
+  }
   __syncthreads();
   int32_t fb = 0, fe = s_tail, lvl = 0, cur = 0;
   while (fb < fe) {
     if (tid == 0) lstart[lvl] = fb;
-    const int32_t *front = s_front[cur];
-    int32_t *next = s_front[cur ^ 1];
+    int32_t *nv = s_fv[cur ^ 1], *nd = s_fd[cur ^ 1];
+    int4 *na = s_fa[cur ^ 1];
     for (int32_t base = fb; base < fe; base += kKahnB) {
-      if (tid == 0) s_nheavy = 0;
+      if (tid == 0) s_nh = 0;
       __syncthreads();
       const int32_t i = base + tid;
+      bool light = false;
+      int32_t d = 0;
+      int4 a = make_int4(-1, -1, -1, -1);
       if (i < fe) {
-        const int32_t u = i - fb < kKahnFront ? front[i - fb] : F[i];
-        level[u] = lvl;
-        const int32_t e0 = g.out_ptr[u], e1 = g.out_ptr[u + 1];
-        if (e1 - e0 > kKahnHeavy) {
-          s_heavy[atomicAdd(&s_nheavy, 1)] = u;
+        int32_t u;
+        if (i - fb < kKahnCap) {
+          u = s_fv[cur][i - fb];
+          d = s_fd[cur][i - fb];
+          a = s_fa[cur][i - fb];
         } else {
-          for (int32_t eb = e0; eb < e1; eb += kKahnE) {
-            int32_t v[kKahnE], c[kKahnE];
+          u = F[i];
+          d = deg[u];
+          a = adj[u];
+        }
+        level[u] = lvl;
+        light = d <= kKahnA;
+        if (!light) {
+          const int32_t j = atomicAdd(&s_nh, 1);
+          s_hv[j] = u;
+          s_hd[j] = d;
+          s_he[j] = g.out_ptr[u];
+        }
+      }
+      {  // light nodes: every removal and the successors' adjacency in one round
+        int32_t c[kKahnA], td[kKahnA];
+        int4 ta[kKahnA];
 #pragma unroll
-            for (int q = 0; q < kKahnE; q++) v[q] = eb + q < e1 ? g.out_idx[eb + q] : -1;
-#pragma unroll
-            for (int q = 0; q < kKahnE; q++) c[q] = v[q] >= 0 ? atomicSub(&cnt[v[q]], 1) : 0;
-#pragma unroll
-            for (int q = 0; q < kKahnE; q++)
-              if (c[q] == 1) kahn_append(F, next, &s_tail, fe, v[q]);  // last in-edge removed
+        for (int q = 0; q < kKahnA; q++) {
+          const int32_t t = int4_at(a, q);
+          c[q] = 0;
+          td[q] = 0;
+          ta[q] = make_int4(-1, -1, -1, -1);
+          if (light && q < d) {
+            c[q] = atomicSub(&cnt[t], 1);
+            td[q] = deg[t];
+            ta[q] = adj[t];
           }
         }
+#pragma unroll
+        for (int q = 0; q < kKahnA; q++)
+          kahn_append(c[q] == 1, int4_at(a, q), td[q], ta[q], F, &s_tail, fe, nv, nd, na);
       }
       __syncthreads();
-      const int32_t nh = s_nheavy;
-      for (int32_t h = 0; h < nh; h++) {
-        const int32_t u = s_heavy[h];
-        for (int32_t e = g.out_ptr[u] + tid; e < g.out_ptr[u + 1]; e += kKahnB) {
-          const int32_t v = g.out_idx[e];
-          if (atomicSub(&cnt[v], 1) == 1) kahn_append(F, next, &s_tail, fe, v);
+      const int32_t nh = s_nh;
+      if (nh > 0) {
+        // exclusive prefix of the listed nodes' degrees
+        const int32_t dj = tid < nh ? s_hd[tid] : 0;
+        int32_t x = dj;
+        for (int o = 1; o < 64; o <<= 1) {
+          const int32_t y = __shfl_up(x, o);
+          if (lane >= o) x += y;
         }
+        if (lane == 63) s_wt[wave] = x;
+        __syncthreads();
+        int32_t off = 0;
+        for (int w = 0; w < wave; w++) off += s_wt[w];
+        if (tid < nh) s_hp[tid] = off + x - dj;
+        if (tid == nh - 1) s_hp[nh] = off + x;
+        __syncthreads();
+        const int32_t tot = s_hp[nh];
+        int32_t h = 0;  // listed node of the thread's current edge (edges only move forward)
+        for (int32_t t0 = tid; t0 < tot; t0 += kKahnE * kKahnB) {
+          int32_t v[kKahnE];
+#pragma unroll
+          for (int q = 0; q < kKahnE; q++) {
+            const int32_t t = t0 + q * kKahnB;
+            v[q] = -1;
+            if (t < tot) {
+              int32_t lo = h, hi = nh - 1;  // last listed node whose edges start at or before t
+              while (lo < hi) {
+                const int32_t mid = (lo + hi + 1) >> 1;
+                if (s_hp[mid] <= t) lo = mid;
+                else hi = mid - 1;
+              }
+              h = lo;
+              v[q] = g.out_idx[s_he[h] + (t - s_hp[h])];
+            }
+          }
+          int32_t c[kKahnE], td[kKahnE];
+          int4 ta[kKahnE];
+#pragma unroll
+          for (int q = 0; q < kKahnE; q++) {
+            c[q] = 0;
+            td[q] = 0;
+            ta[q] = make_int4(-1, -1, -1, -1);
+            if (v[q] >= 0) {
+              c[q] = atomicSub(&cnt[v[q]], 1);
+              td[q] = deg[v[q]];
+              ta[q] = adj[v[q]];
+            }
+          }
+#pragma unroll
+          for (int q = 0; q < kKahnE; q++)
+            kahn_append(c[q] == 1, v[q], td[q], ta[q], F, &s_tail, fe, nv, nd, na);
+        }
+        __syncthreads();
       }
-      __syncthreads();
     }
     fb = fe;
     fe = s_tail;
@@ -114,9 +231,15 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
   CEL_TRY(sc.get(&cnt, n));
   CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
   CEL_TRY(check_graph(g, 1, 0, /*bound=*/false, st, cnt, sc, s));
+  int32_t *deg;
+  int4 *adj;
+  CEL_TRY(sc.get(&deg, n));
+  CEL_TRY(sc.get(&adj, n));
+  if (n > 0)
+    k_kahn_prep<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, g->out_ptr, g->out_idx, deg, adj, st);
   {
     KTimer kt(s, "k_kahn");
-    k_kahn<<<1, kKahnB, 0, s>>>(*g, cnt, order_id, level, level_ptr, st);
+    k_kahn<<<1, kKahnB, 0, s>>>(*g, cnt, deg, adj, order_id, level, level_ptr, st);
   }
   CEL_HIP(hipGetLastError());
   Status h;
