@@ -16,15 +16,16 @@ constexpr int kKahnA = 4;         // successors carried with a frontier entry
 constexpr int kKahnCap = 2048;    // frontier entries mirrored in LDS
 constexpr int kKahnE = 4;         // edges per thread whose loads and atomics go out together
 
-// Per node: out-degree and its first kKahnA successors (-1 past the end), so
-// that a node that becomes ready brings its adjacency along with it.
+// Per node: first out-edge and out-degree, and its first kKahnA successors
+// (-1 past the end), so that a node that becomes ready brings its adjacency
+// along with it.
 __global__ void k_kahn_prep(int32_t n, const int32_t *out_ptr, const int32_t *out_idx,
-                            int32_t *deg, int4 *adj, const Status *st) {
+                            int2 *deg, int4 *adj, const Status *st) {
   if (failed(st)) return;
   for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
        v += (int64_t)gridDim.x * blockDim.x) {
     const int32_t e0 = out_ptr[v], d = out_ptr[v + 1] - e0;
-    deg[v] = d;
+    deg[v] = make_int2(e0, d);
     adj[v] = make_int4(d > 0 ? out_idx[e0] : -1, d > 1 ? out_idx[e0 + 1] : -1,
                        d > 2 ? out_idx[e0 + 2] : -1, d > 3 ? out_idx[e0 + 3] : -1);
   }
@@ -38,8 +39,8 @@ __device__ inline int32_t int4_at(const int4 &a, int q) {
 // built, for the lanes with want set: one LDS atomic per wave reserves the
 // wave's slots.  F holds every frontier in order; the LDS mirror holds the
 // first kKahnCap entries of the one being built (fe: its first index).
-__device__ inline void kahn_append(bool want, int32_t v, int32_t d, const int4 &a, int32_t *F,
-                                   int32_t *s_tail, int32_t fe, int32_t *s_fv, int32_t *s_fd,
+__device__ inline void kahn_append(bool want, int32_t v, const int2 &d, const int4 &a, int32_t *F,
+                                   int32_t *s_tail, int32_t fe, int32_t *s_fv, int2 *s_fd,
                                    int4 *s_fa) {
   const uint64_t m = __ballot(want);
   if (m == 0) return;
@@ -65,38 +66,41 @@ __device__ inline void kahn_append(bool want, int32_t v, int32_t d, const int4 &
 // the node that the last removal makes ready joins the next frontier with its
 // adjacency.  Nodes of higher degree are listed and their edges then spread
 // over the whole block (flattened by a prefix sum of the degrees).
-__global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, const int32_t *deg,
+__global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, const int2 *deg,
                                                  const int4 *adj, int32_t *F, int32_t *level,
                                                  int32_t *lstart, Status *st) {
-  __shared__ int32_t s_tail, s_nh;
-  __shared__ int32_t s_fv[2][kKahnCap], s_fd[2][kKahnCap];
+  __shared__ int32_t s_tail, s_nh[3];  // s_nh: listed nodes, counters used by passes in turn
+  __shared__ int32_t s_fv[2][kKahnCap];
+  __shared__ int2 s_fd[2][kKahnCap];  // first out-edge, out-degree
   __shared__ int4 s_fa[2][kKahnCap];
-  __shared__ int32_t s_hv[kKahnB], s_hd[kKahnB], s_he[kKahnB], s_hp[kKahnB + 1];
+  __shared__ int32_t s_hd[kKahnB], s_he[kKahnB], s_hp[kKahnB + 1];
   __shared__ int32_t s_wt[kKahnNW];
   if (failed(st)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t n = g.n;
-  if (tid == 0) s_tail = 0;
+  if (tid == 0) {
+    s_tail = 0;
+    s_nh[0] = s_nh[1] = s_nh[2] = 0;
+  }
   __syncthreads();
   for (int32_t v0 = 0; v0 < n; v0 += kKahnB) {  // sources
     const int32_t v = v0 + tid;
     const bool src = v < n && cnt[v] == 0;
-    const int32_t d = src ? deg[v] : 0;
+    const int2 d = src ? deg[v] : make_int2(0, 0);
     const int4 a = src ? adj[v] : make_int4(-1, -1, -1, -1);
     kahn_append(src, v, d, a, F, &s_tail, 0, s_fv[0], s_fd[0], s_fa[0]);
   }
   __syncthreads();
-  int32_t fb = 0, fe = s_tail, lvl = 0, cur = 0;
+  int32_t fb = 0, fe = s_tail, lvl = 0, cur = 0, pp = 0;
   while (fb < fe) {
     if (tid == 0) lstart[lvl] = fb;
-    int32_t *nv = s_fv[cur ^ 1], *nd = s_fd[cur ^ 1];
+    int32_t *nv = s_fv[cur ^ 1];
+    int2 *nd = s_fd[cur ^ 1];
     int4 *na = s_fa[cur ^ 1];
-    for (int32_t base = fb; base < fe; base += kKahnB) {
-      if (tid == 0) s_nh = 0;
-      __syncthreads();
+    for (int32_t base = fb; base < fe; base += kKahnB, pp = pp == 2 ? 0 : pp + 1) {
       const int32_t i = base + tid;
       bool light = false;
-      int32_t d = 0;
+      int2 d = make_int2(0, 0);
       int4 a = make_int4(-1, -1, -1, -1);
       if (i < fe) {
         int32_t u;
@@ -110,24 +114,24 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
           a = adj[u];
         }
         level[u] = lvl;
-        light = d <= kKahnA;
+        light = d.y <= kKahnA;
         if (!light) {
-          const int32_t j = atomicAdd(&s_nh, 1);
-          s_hv[j] = u;
-          s_hd[j] = d;
-          s_he[j] = g.out_ptr[u];
+          const int32_t j = atomicAdd(&s_nh[pp], 1);
+          s_hd[j] = d.y;
+          s_he[j] = d.x;
         }
       }
       {  // light nodes: every removal and the successors' adjacency in one round
-        int32_t c[kKahnA], td[kKahnA];
+        int32_t c[kKahnA];
+        int2 td[kKahnA];
         int4 ta[kKahnA];
 #pragma unroll
         for (int q = 0; q < kKahnA; q++) {
           const int32_t t = int4_at(a, q);
           c[q] = 0;
-          td[q] = 0;
+          td[q] = make_int2(0, 0);
           ta[q] = make_int4(-1, -1, -1, -1);
-          if (light && q < d) {
+          if (light && q < d.y) {
             c[q] = atomicSub(&cnt[t], 1);
             td[q] = deg[t];
             ta[q] = adj[t];
@@ -138,19 +142,26 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
           kahn_append(c[q] == 1, int4_at(a, q), td[q], ta[q], F, &s_tail, fe, nv, nd, na);
       }
       __syncthreads();
-      const int32_t nh = s_nh;
+      const int32_t nh = s_nh[pp];
+      // the counter of the pass after next: last read in the previous pass,
+      // before this pass's barrier, and next counted after the next pass's
+      if (tid == 0) s_nh[pp == 0 ? 2 : pp - 1] = 0;
       if (nh > 0) {
-        // exclusive prefix of the listed nodes' degrees
+        // exclusive prefix of the listed nodes' degrees (by wave 0 alone when
+        // they fit one wave)
         const int32_t dj = tid < nh ? s_hd[tid] : 0;
         int32_t x = dj;
-        for (int o = 1; o < 64; o <<= 1) {
-          const int32_t y = __shfl_up(x, o);
-          if (lane >= o) x += y;
-        }
-        if (lane == 63) s_wt[wave] = x;
-        __syncthreads();
+        if (nh > 64 || wave == 0)
+          for (int o = 1; o < 64; o <<= 1) {
+            const int32_t y = __shfl_up(x, o);
+            if (lane >= o) x += y;
+          }
         int32_t off = 0;
-        for (int w = 0; w < wave; w++) off += s_wt[w];
+        if (nh > 64) {
+          if (lane == 63) s_wt[wave] = x;
+          __syncthreads();
+          for (int w = 0; w < wave; w++) off += s_wt[w];
+        }
         if (tid < nh) s_hp[tid] = off + x - dj;
         if (tid == nh - 1) s_hp[nh] = off + x;
         __syncthreads();
@@ -173,12 +184,13 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
               v[q] = g.out_idx[s_he[h] + (t - s_hp[h])];
             }
           }
-          int32_t c[kKahnE], td[kKahnE];
+          int32_t c[kKahnE];
+          int2 td[kKahnE];
           int4 ta[kKahnE];
 #pragma unroll
           for (int q = 0; q < kKahnE; q++) {
             c[q] = 0;
-            td[q] = 0;
+            td[q] = make_int2(0, 0);
             ta[q] = make_int4(-1, -1, -1, -1);
             if (v[q] >= 0) {
               c[q] = atomicSub(&cnt[v[q]], 1);
@@ -231,7 +243,7 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
   CEL_TRY(sc.get(&cnt, n));
   CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
   CEL_TRY(check_graph(g, 1, 0, /*bound=*/false, st, cnt, sc, s));
-  int32_t *deg;
+  int2 *deg;
   int4 *adj;
   CEL_TRY(sc.get(&deg, n));
   CEL_TRY(sc.get(&adj, n));
