@@ -111,6 +111,13 @@ __device__ inline int32_t next_marked(const uint64_t (&m)[4], int32_t k) {
   return 256;
 }
 
+// Lane l's value of a 64-bit register, for a uniform l.
+__device__ inline int64_t readlane64(int64_t v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int32_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int32_t)(v >> 32), l);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 // Window staging records the owner slot of each edge for the first kOwnFill
 // edges of every row (one thread per row); an edge past that (rows of very
 // high degree only) finds its owner by binary search over the row starts:

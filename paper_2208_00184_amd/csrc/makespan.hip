@@ -592,12 +592,6 @@ __device__ inline void ms_pull_from(int kmax, int64_t (&r)[NR], const RP (&cur)[
   }
 }
 
-__device__ inline int64_t readlane64(int64_t v, int l) {
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int32_t)v, l);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int32_t)(v >> 32), l);
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
 // Run structure of the device-grouped order, per slot s: sx = exclusive sum
 // of w over the slot's run, meta = device | run ends here << 8 |
 // min(distance to the run's first slot, 32767) << 16.

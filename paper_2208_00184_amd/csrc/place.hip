@@ -6,14 +6,13 @@
 // (source cluster, edge id) and runs of equal source cluster summed, which
 // gives each cluster its list of coarse in-edges (pred, comm) in a fixed order.
 //
-// Placement (sequential over clusters, as the algorithm is): one workgroup.
-// For cluster t, pre_t on device x is max over preds of Fin[p] + I(dev p != x)
-// cc; it is evaluated for all devices at once from two block reductions:
-// per-device max of Fin over same-device preds, and the largest and
-// second-largest (on another device) values of Fin + cc.  Lane x then finds
-// the first-fit start on device x in that device's sorted list of busy
-// blocks (touching intervals are merged, so the list holds one block per
-// idle gap), and a block argmin picks the device.
+// Placement (sequential over clusters, as the algorithm is): one wave.  For
+// cluster t, pre_t on device x is max over preds of Fin[p] + I(dev p != x)
+// cc; it is evaluated for all devices at once from per-device maxima of Fin
+// and of Fin + cc over the preds, and the best and second-best devices of
+// the latter.  Lane x then finds the first-fit start on device x in that
+// device's sorted list of busy blocks (touching intervals are merged, so the
+// list holds one block per idle gap), and a wave argmin picks the device.
 #include "cel_internal.h"
 
 namespace cel {
@@ -136,22 +135,12 @@ __global__ void k_place_combine(int32_t C, const int32_t *boff, const uint64_t *
   }
 }
 
-constexpr int kPlaceB = 256;
-
-__device__ inline void argmin_i64(int64_t &v, int32_t &i) {  // wave: smallest v, then smallest i
-  for (int off = 32; off > 0; off >>= 1) {
-    const int64_t ov = __shfl_xor(v, off);
-    const int32_t oi = __shfl_xor(i, off);
-    if (ov < v || (ov == v && oi < i)) {
-      v = ov;
-      i = oi;
-    }
-  }
-}
+constexpr int kPlaceBlk = 5120;  // busy blocks held in LDS, shared evenly by the devices
+constexpr int kPlaceLds = 6144;  // clusters whose Fin and device are kept in LDS too
 
 __device__ inline void argmax_i64(int64_t &v, int32_t &i) {  // wave: largest v, then smallest i
   for (int off = 32; off > 0; off >>= 1) {
-    const int64_t ov = __shfl_xor(v, off);
+    const int64_t ov = __shfl_xor((long long)v, off);
     const int32_t oi = __shfl_xor(i, off);
     if (ov > v || (ov == v && oi < i)) {
       v = ov;
@@ -160,187 +149,309 @@ __device__ inline void argmax_i64(int64_t &v, int32_t &i) {  // wave: largest v,
   }
 }
 
-__global__ void __launch_bounds__(kPlaceB)
+// Number of blocks of a sorted busy list (ends xf[0..nb)) that end at or
+// before s, searched from the end: ready times mostly fall near the end of
+// the list, so a galloping step back brackets them in a few reads.
+__device__ inline int32_t blocks_ending_by(const int64_t *xf, int32_t nb, int64_t s) {
+  int32_t hi = nb, step = 1;
+  while (hi > 0 && xf[hi - 1] > s) {  // xf[hi - 1] > s: the answer is below hi
+    const int32_t lo = hi - step > 0 ? hi - step : 0;
+    if (xf[lo] <= s) {  // answer in (lo, hi): binary search
+      int32_t a = lo + 1, b = hi - 1;  // first index in [a, b] ending after s, else b + 1
+      while (a <= b) {
+        const int32_t mid = (a + b) >> 1;
+        if (xf[mid] <= s) a = mid + 1;
+        else b = mid - 1;
+      }
+      return a;
+    }
+    hi = lo;
+    step <<= 1;
+  }
+  return hi;
+}
+
+// Inserts [s0, f) into a sorted list of merged busy blocks (xs, xf, nb of
+// them, room for cap): touching blocks merge, so the list keeps one block
+// per idle gap.  Returns the end of the last block.
+__device__ inline int64_t busy_insert(int64_t *xs, int64_t *xf, int32_t &nb, int32_t cap,
+                                      int64_t s0, int64_t f, Status *st) {
+  const int32_t k = blocks_ending_by(xf, nb, s0);
+  const bool left = k > 0 && xf[k - 1] == s0;
+  const bool right = k < nb && xs[k] == f;
+  if (left && right) {
+    xf[k - 1] = xf[k];
+    for (int32_t q = k; q + 1 < nb; q++) {
+      xs[q] = xs[q + 1];
+      xf[q] = xf[q + 1];
+    }
+    nb--;
+  } else if (left) {
+    xf[k - 1] = f;
+  } else if (right) {
+    xs[k] = s0;
+  } else if (nb < cap) {
+    for (int32_t q = nb; q > k; q--) {
+      xs[q] = xs[q - 1];
+      xf[q] = xf[q - 1];
+    }
+    xs[k] = s0;
+    xf[k] = f;
+    nb++;
+  } else {
+    raise_err(st, EB_ARG);  // cannot happen: the list moves out of LDS when full
+  }
+  return nb > 0 ? xf[nb - 1] : 0;
+}
+
+// Placement, one wave (its LDS accesses are in program order, so no barrier
+// is needed).  For cluster t, one pass over its coarse preds leaves per device
+// y the largest Fin and the largest Fin + cc of the preds on y; pre_t on
+// device x is then max(0, the first at x, the largest second over devices
+// other than x), from the best and second-best devices.  Device x's free
+// memory and busy-list state sit in the registers of lane x mod 64; values
+// every lane needs are read from LDS in unrolled groups, all requests out
+// before the first use.  Each device's busy list lives in LDS
+// (kPlaceBlk / D blocks) until it outgrows that share; it then moves to its
+// global list.  LDSF keeps every cluster's Fin and device in LDS as well
+// (C <= kPlaceLds).
+template <bool LDSF>
+__global__ void __launch_bounds__(64)
     k_place(int32_t C, int32_t D, const int64_t *cap, const uint64_t *W, const uint64_t *MEM,
             const int32_t *boff, const int32_t *ncp, const int32_t *ca, const int64_t *cc,
             const uint64_t *back, uint8_t *cdev, int64_t *Fin, int64_t *bs, int64_t *bf,
             int32_t bcap, Status *st) {
-  __shared__ int64_t s_ava[256], s_devmax[256], s_est[256], s_slot[256], s_last[256];
-  __shared__ int32_t s_nb[256];
-  __shared__ int64_t s_rv[4];
-  __shared__ int32_t s_ri[4];
-  __shared__ int64_t s_m1, s_m2;
-  __shared__ int32_t s_d1;
+  constexpr int G = 16;  // devices per group of LDS reads
+  __shared__ int64_t s_bs[kPlaceBlk], s_bf[kPlaceBlk];
+  __shared__ int64_t s_fin[LDSF ? kPlaceLds : 1];
+  __shared__ uint8_t s_cd[LDSF ? kPlaceLds : 1];
+  // per device: max Fin and max Fin + cc of the preds on it (-1: none), EST
+  // (kInf past D)
+  __shared__ int64_t s_dm[256], s_dmc[256], s_est[256];
   if (failed(st)) return;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  for (int x = tid; x < 256; x += kPlaceB) {
-    s_ava[x] = x < D ? cap[x] : 0;
-    s_nb[x] = 0;
-    s_last[x] = 0;
+  const int lane = threadIdx.x;
+  const int32_t capL = kPlaceBlk / D;
+  int64_t ava[4], last[4];  // device lane + 64 i: free memory, end of its last busy block
+  int32_t nbl[4], glob[4];  // its busy-block count; list moved to global memory
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const int x = lane + 64 * i;
+    ava[i] = x < D ? cap[x] : 0;
+    last[i] = 0;
+    nbl[i] = 0;
+    glob[i] = 0;
+    s_dm[x] = -1;
+    s_dmc[x] = -1;
+    s_est[x] = kInf;
   }
   int32_t prev = 0, be = 0;
   int64_t span = 0;
-  __syncthreads();
+  // Loads run ahead of their use: the sizes of 64 clusters at a time, one per
+  // lane, a block of 64 ahead (read back with readlane), and the first 64
+  // preds of a cluster kPD steps ahead; their Fin and device come from LDS
+  // (LDSF), else from global memory at the step.
+  constexpr int kPD = 3;
+  auto bulk = [&](int32_t t0, int32_t &zb, int32_t &zn, int64_t &zw, int64_t &zm, int64_t &zk) {
+    const int32_t t = t0 + lane;
+    zb = t < C ? boff[t] : 0;
+    zn = t < C ? ncp[t] : 0;
+    zw = t < C ? (int64_t)W[t] : 0;
+    zm = t < C ? (int64_t)MEM[t] : 0;
+    zk = t < C ? (int64_t)back[t] : 0;
+  };
+  int32_t ub, un, vb, vn;  // sizes of clusters [T, T + 64) (u*) and [T + 64, T + 128) (v*)
+  int64_t uw, um, uk, vw, vm, vk;
+  bulk(0, ub, un, uw, um, uk);
+  bulk(64, vb, vn, vw, vm, vk);
+  // first preds of the cluster t' (t' < T + 128), by lane
+  auto preds = [&](int32_t tp, int32_t T, int32_t &pa, int64_t &pc) {
+    pa = 0;
+    pc = 0;
+    if (tp >= C) return;
+    const bool in_u = tp - T < 64;
+    const int l = (tp - T) & 63;
+    const int32_t b = __builtin_amdgcn_readlane(in_u ? ub : vb, l);
+    const int32_t nn = __builtin_amdgcn_readlane(in_u ? un : vn, l);
+    if (lane < nn) {
+      pa = ca[b + lane];
+      pc = cc[b + lane];
+    }
+  };
+  int32_t pa[kPD];
+  int64_t pcv[kPD];
+#pragma unroll
+  for (int q = 0; q < kPD; q++) preds(q, 0, pa[q], pcv[q]);
   for (int32_t t = 0; t < C; t++) {
-    const int32_t b0 = boff[t], np = ncp[t];
-    const int64_t Wt = (int64_t)W[t], Mt = (int64_t)MEM[t], bk = (int64_t)back[t];
-    for (int x = tid; x < D; x += kPlaceB) s_devmax[x] = -1;
-    __syncthreads();
-    // largest Fin + cc over all preds (device of the best, lowest id on ties)
-    int64_t v1 = -1;
+    const int32_t T = t & ~63;
+    if (t > 0 && (t & 63) == 0) {  // next block of sizes
+      ub = vb;
+      un = vn;
+      uw = vw;
+      um = vm;
+      uk = vk;
+      bulk(t + 64, vb, vn, vw, vm, vk);
+    }
+    const int l = t & 63;
+    const int32_t b0 = __builtin_amdgcn_readlane(ub, l), np = __builtin_amdgcn_readlane(un, l);
+    const int64_t Wt = readlane64(uw, l), Mt = readlane64(um, l), bk = readlane64(uk, l);
+    int32_t a0 = pa[0];
+    int64_t c0 = pcv[0];
+#pragma unroll
+    for (int q = 0; q + 1 < kPD; q++) {
+      pa[q] = pa[q + 1];
+      pcv[q] = pcv[q + 1];
+    }
+    preds(t + kPD, T, pa[kPD - 1], pcv[kPD - 1]);
+    // per-device maxima over the preds
+    for (int32_t k0 = 0; k0 < np; k0 += 64) {
+      if (k0 > 0) {
+        a0 = k0 + lane < np ? ca[b0 + k0 + lane] : 0;
+        c0 = k0 + lane < np ? cc[b0 + k0 + lane] : 0;
+      }
+      if (k0 + lane < np) {
+        const int64_t f0 = LDSF ? s_fin[a0] : Fin[a0];
+        const int32_t d0 = LDSF ? s_cd[a0] : cdev[a0];
+        atomicMax((long long *)&s_dm[d0], (long long)f0);
+        atomicMax((long long *)&s_dmc[d0], (long long)(f0 + c0));
+      }
+    }
+    // best device by Fin + cc (lowest id on ties) and the best of the others,
+    // by every lane
+    int64_t m1 = -1, m2 = -1;
     int32_t d1 = INT32_MAX;
-    for (int32_t k = tid; k < np; k += kPlaceB) {
-      const int32_t a = ca[b0 + k];
-      const int64_t fa = Fin[a];
-      const int32_t da = cdev[a];
-      atomicMax((long long *)&s_devmax[da], (long long)fa);
-      const int64_t x = fa + cc[b0 + k];
-      if (x > v1 || (x == v1 && da < d1)) {
-        v1 = x;
-        d1 = da;
+    for (int32_t x0 = 0; x0 < D; x0 += G) {
+      int64_t v[G];
+#pragma unroll
+      for (int q = 0; q < G; q++) v[q] = s_dmc[x0 + q];
+#pragma unroll
+      for (int q = 0; q < G; q++) {
+        if (v[q] > m1) {
+          m2 = m1;
+          m1 = v[q];
+          d1 = x0 + q;
+        } else if (v[q] > m2) {
+          m2 = v[q];
+        }
       }
     }
-    argmax_i64(v1, d1);
-    if (lane == 0) {
-      s_rv[wv] = v1;
-      s_ri[wv] = d1;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      int64_t bv = s_rv[0];
-      int32_t bd = s_ri[0];
-      for (int i = 1; i < kPlaceB / 64; i++)
-        if (s_rv[i] > bv || (s_rv[i] == bv && s_ri[i] < bd)) {
-          bv = s_rv[i];
-          bd = s_ri[i];
+    // device x: pre_t, first-fit slot and EST (eq. 7)
+    int64_t slot[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      slot[i] = 0;
+      const int x = lane + 64 * i;
+      if (64 * i >= D) continue;  // uniform
+      if (x < D) {
+        int64_t pre = 0;
+        const int64_t other = x != d1 ? m1 : m2;
+        pre = other > pre ? other : pre;
+        pre = s_dm[x] > pre ? s_dm[x] : pre;
+        int64_t sv = pre;
+        const int32_t nb = nbl[i];
+        if (Wt > 0 && nb > 0 && sv < last[i]) {  // LDS and global lists in separate code
+          if (!glob[i]) {
+            const int64_t *xs = s_bs + x * capL, *xf = s_bf + x * capL;
+            for (int32_t k = blocks_ending_by(xf, nb, sv); k < nb && xs[k] < sv + Wt; k++)
+              sv = xf[k];
+          } else {
+            const int64_t *xs = bs + (int64_t)x * bcap, *xf = bf + (int64_t)x * bcap;
+            for (int32_t k = blocks_ending_by(xf, nb, sv); k < nb && xs[k] < sv + Wt; k++)
+              sv = xf[k];
+          }
         }
-      s_m1 = bv;
-      s_d1 = bd;
-    }
-    __syncthreads();
-    // largest Fin + cc over preds on another device than the best one
-    const int32_t D1 = s_d1;
-    int64_t v2 = -1;
-    int32_t dummy = 0;
-    for (int32_t k = tid; k < np; k += kPlaceB) {
-      const int32_t a = ca[b0 + k];
-      if ((int32_t)cdev[a] == D1) continue;
-      const int64_t x = Fin[a] + cc[b0 + k];
-      v2 = x > v2 ? x : v2;
-    }
-    argmax_i64(v2, dummy);
-    if (lane == 0) s_rv[wv] = v2;
-    __syncthreads();
-    if (tid == 0) {
-      int64_t bv = s_rv[0];
-      for (int i = 1; i < kPlaceB / 64; i++) bv = s_rv[i] > bv ? s_rv[i] : bv;
-      s_m2 = bv;
-    }
-    __syncthreads();
-    // lane x: pre_t, first-fit slot and EST on device x  (eq. 7)
-    const int64_t M1 = s_m1, M2 = s_m2;
-    for (int x = tid; x < D; x += kPlaceB) {
-      int64_t pre = 0;
-      const int64_t other = (x != D1) ? M1 : M2;
-      pre = other > pre ? other : pre;
-      pre = s_devmax[x] > pre ? s_devmax[x] : pre;
-      int64_t s = pre;
-      const int32_t nb = s_nb[x];
-      if (Wt > 0 && nb > 0 && s < s_last[x]) {
-        const int64_t *xs = bs + (int64_t)x * bcap, *xf = bf + (int64_t)x * bcap;
-        int32_t lo = 0, hi = nb;  // first block ending after s
-        while (lo < hi) {
-          const int32_t mid = (lo + hi) >> 1;
-          if (xf[mid] <= s) lo = mid + 1;
-          else hi = mid;
-        }
-        for (int32_t k = lo; k < nb && xs[k] < s + Wt; k++) s = xf[k];
+        slot[i] = sv;
+        s_est[x] = ava[i] < Mt ? kInf : sv;
+        s_dm[x] = -1;  // cleared for the next cluster
+        s_dmc[x] = -1;
       }
-      s_slot[x] = s;
-      s_est[x] = s_ava[x] < Mt ? kInf : s;
     }
-    __syncthreads();
-    // device of smallest EST (lowest id on ties)
+    // device of smallest EST (lowest id on ties), by every lane
     int64_t ev = kInf;
     int32_t ei = INT32_MAX;
-    for (int x = tid; x < D; x += kPlaceB)
-      if (s_est[x] < ev || (s_est[x] == ev && x < ei)) {
-        ev = s_est[x];
-        ei = x;
-      }
-    argmin_i64(ev, ei);
-    if (lane == 0) {
-      s_rv[wv] = ev;
-      s_ri[wv] = ei;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      int64_t e1 = s_rv[0];
-      int32_t dd = s_ri[0];
-      for (int i = 1; i < kPlaceB / 64; i++)
-        if (s_rv[i] < e1 || (s_rv[i] == e1 && s_ri[i] < dd)) {
-          e1 = s_rv[i];
-          dd = s_ri[i];
+    for (int32_t x0 = 0; x0 < D; x0 += G) {
+      int64_t v[G];
+#pragma unroll
+      for (int q = 0; q < G; q++) v[q] = s_est[x0 + q];
+#pragma unroll
+      for (int q = 0; q < G; q++)
+        if (v[q] < ev) {
+          ev = v[q];
+          ei = x0 + q;
         }
-      const int32_t dk = t == 0 ? 0 : prev;
-      int32_t pick;
-      if (e1 == kInf) {  // every device full: most remaining memory (best effort)
-        pick = 0;
-        for (int x = 1; x < D; x++)
-          if (s_ava[x] > s_ava[pick]) pick = x;
-        be++;
-      } else if (s_est[dk] == kInf || s_est[dk] - e1 > bk) {  // eq. 9
-        pick = dd;
-      } else {
-        pick = dk;
+    }
+    // the choice (eq. 8-9), uniform over the wave
+    const int32_t dk = t == 0 ? 0 : prev;
+    const int64_t edk = s_est[dk];
+    int32_t pick;
+    if (ev == kInf) {  // every device full: most remaining memory (best effort)
+      int64_t av = INT64_MIN;  // free memory can be negative after best-effort picks
+      int32_t ai = INT32_MAX;
+#pragma unroll
+      for (int i = 0; i < 4; i++)
+        if (lane + 64 * i < D && ava[i] > av) {
+          av = ava[i];
+          ai = lane + 64 * i;
+        }
+      argmax_i64(av, ai);
+      pick = ai;
+      be++;
+    } else if (edk == kInf || edk - ev > bk) {
+      pick = ei;
+    } else {
+      pick = dk;
+    }
+    const int ip = pick >> 6, lp = pick & 63;
+    int64_t slp = 0;
+    int32_t nb = 0, gl = 0;
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+      if (i == ip) {
+        slp = slot[i];
+        nb = nbl[i];
+        gl = glob[i];
       }
-      const int64_t s0 = s_slot[pick], f = s0 + Wt;
+    const int64_t s0 = readlane64(slp, lp), f = s0 + Wt;
+    nb = __builtin_amdgcn_readlane(nb, lp);
+    gl = __builtin_amdgcn_readlane(gl, lp);
+    span = f > span ? f : span;
+    prev = pick;
+    if (Wt > 0) {  // insert [s0, f) into the device's merged busy blocks
+      if (!gl && nb == capL) {  // the LDS share is full: move the list out
+        for (int32_t q = lane; q < nb; q += 64) {
+          bs[(int64_t)pick * bcap + q] = s_bs[pick * capL + q];
+          bf[(int64_t)pick * bcap + q] = s_bf[pick * capL + q];
+        }
+        gl = 1;
+      }
+      int64_t lastv = 0;
+      if (lane == 0) {
+        if (!gl) lastv = busy_insert(s_bs + pick * capL, s_bf + pick * capL, nb, capL, s0, f, st);
+        else lastv = busy_insert(bs + (int64_t)pick * bcap, bf + (int64_t)pick * bcap, nb, bcap,
+                                 s0, f, st);
+      }
+      nb = __builtin_amdgcn_readlane(nb, 0);
+      lastv = readlane64(lastv, 0);
+#pragma unroll
+      for (int i = 0; i < 4; i++)
+        if (i == ip && lane == lp) {
+          nbl[i] = nb;
+          last[i] = lastv;
+          glob[i] = gl;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+      if (i == ip && lane == lp) ava[i] -= Mt;
+    if (lane == 0) {  // later steps of this wave read these back, in program order
       cdev[t] = (uint8_t)pick;
       Fin[t] = f;
-      span = f > span ? f : span;
-      s_ava[pick] -= Mt;
-      prev = pick;
-      if (Wt > 0) {  // insert [s0, f) into the device's merged busy blocks
-        int64_t *xs = bs + (int64_t)pick * bcap, *xf = bf + (int64_t)pick * bcap;
-        int32_t nb = s_nb[pick];
-        int32_t lo = 0, hi = nb;  // k = number of blocks ending at or before s0
-        while (lo < hi) {
-          const int32_t mid = (lo + hi) >> 1;
-          if (xf[mid] <= s0) lo = mid + 1;
-          else hi = mid;
-        }
-        const int32_t k = lo;
-        const bool left = k > 0 && xf[k - 1] == s0;
-        const bool right = k < nb && xs[k] == f;
-        if (left && right) {
-          xf[k - 1] = xf[k];
-          for (int32_t q = k; q + 1 < nb; q++) {
-            xs[q] = xs[q + 1];
-            xf[q] = xf[q + 1];
-          }
-          nb--;
-        } else if (left) {
-          xf[k - 1] = f;
-        } else if (right) {
-          xs[k] = s0;
-        } else if (nb < bcap) {
-          for (int32_t q = nb; q > k; q--) {
-            xs[q] = xs[q - 1];
-            xf[q] = xf[q - 1];
-          }
-          xs[k] = s0;
-          xf[k] = f;
-          nb++;
-        } else {
-          raise_err(st, EB_ARG);  // cannot happen: one block per placed cluster at most
-        }
-        s_nb[pick] = nb;
-        s_last[pick] = nb > 0 ? xf[nb - 1] : 0;
+      if (LDSF) {
+        s_fin[t] = f;
+        s_cd[t] = (uint8_t)pick;
       }
     }
-    __syncthreads();
   }
-  if (tid == 0) {
+  if (lane == 0) {
     st->s0 = span;
     st->i0 = be;
   }
@@ -438,8 +549,12 @@ extern "C" int cel_place(const cel_graph *g, const cel_devices *d, const int32_t
                                                                       ca, cc, ncp, back, st);
   {
     KTimer kt(s, "k_place");
-    k_place<<<1, kPlaceB, 0, s>>>(C, d->D, dcap, W, MEM, boff, ncp, ca, cc, back, cluster_dev,
-                                  Fin, bs, bf, (int32_t)bcap, st);
+    if (C <= kPlaceLds)
+      k_place<true><<<1, 64, 0, s>>>(C, d->D, dcap, W, MEM, boff, ncp, ca, cc, back, cluster_dev,
+                                     Fin, bs, bf, (int32_t)bcap, st);
+    else
+      k_place<false><<<1, 64, 0, s>>>(C, d->D, dcap, W, MEM, boff, ncp, ca, cc, back,
+                                      cluster_dev, Fin, bs, bf, (int32_t)bcap, st);
   }
   k_place_out<<<grid_for(n > C ? n : C, 256, 4096), 256, 0, s>>>(n, C, cluster_id, cluster_dev,
                                                                 node_dev, Fin, cluster_fin, st);

@@ -550,6 +550,22 @@ def test_place_random():
         check_place(wl, cid, C)
 
 
+def test_place_many_clusters_and_devices():
+    """More clusters than the placement keeps in LDS (config 3, R = 4: 14,429
+    clusters), and 80 or 200 devices, where the busy lists outgrow their LDS
+    share and the device choice takes the wave reductions."""
+    wl, rt, rb = config(3, 0)
+    cid, C, _ = O.cluster(wl, rb[2], 4, -1)
+    assert C > 6144
+    check_place(wl, cid, C)
+    for D in (80, 200):
+        wl2 = make_random_dag(77 + D, 3000, p_edge=4.0 / 3000, D=D, cap_frac=(1, 3))
+        lev2, oid2, lp2, L2 = O.topo_levels(wl2)
+        _, _, pr2, _ = O.blevel(wl2, lev2, oid2)
+        cid2, C2, _ = O.cluster(wl2, pr2, 2, -1)
+        check_place(wl2, cid2, C2)
+
+
 def test_place_rejects_bad_clusters():
     wl, rt, rb = config(1, 0)
     cid, C, _ = O.cluster(wl, rb[2], 200, -1)
