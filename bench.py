@@ -67,7 +67,7 @@ PMC_KERNELS = {
     "k_makespan_batch_wide": ("cel::k_makespan_levels<", ["makespan.hip", "cel_internal.h"]),
     "k_kahn": ("cel::k_kahn(", ["topo.hip", "cel_internal.h"]),
     "k_cluster_dp": ("cel::k_cluster_dp(", ["cluster.hip", "cel_internal.h"]),
-    "k_place": ("cel::k_place(", ["place.hip", "cel_internal.h"]),
+    "k_place": ("cel::k_place<", ["place.hip", "cel_internal.h"]),
 }
 
 
