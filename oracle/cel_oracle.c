@@ -238,6 +238,70 @@ int orc_blevel(const orc_graph *g, const orc_devices *d, const int32_t *level,
   return ORC_OK;
 }
 
+/* ---------------------------------------------------------------- CPD-TOPO */
+
+typedef struct {
+  int64_t cpath;
+  int32_t id;
+} cp_key;
+
+/* increasing cpath, and among equal cpath the higher id first: pushed in this
+ * order, the top of the stack is the largest cpath with the lowest id */
+static int cmp_push(const void *a, const void *b) {
+  const cp_key *x = a, *y = b;
+  if (x->cpath != y->cpath) return x->cpath < y->cpath ? -1 : 1;
+  return (y->id > x->id) - (y->id < x->id);
+}
+
+/* Algorithm 1 (CPD_Topo), Section 5.1.3: the queue Q has the sources in
+ * decreasing cpath order; the head node is dequeued and numbered, its
+ * children sorted by increasing cpath, its out-edges deleted, and each child
+ * left with in-degree 0 is put at the head of Q.  Q is a stack here (the head
+ * is the top).  A child reached by several edges from the node is counted
+ * once: it becomes free when its last in-edge goes. */
+int orc_cpd_topo(const orc_graph *g, const int64_t *blevel, const int64_t *tlevel,
+                 int32_t *cpd_order) {
+  int rc = check_graph(g);
+  if (rc) return rc;
+  int32_t n = g->n;
+  if (n > 0 && (!blevel || !tlevel || !cpd_order)) return ORC_E_ARG;
+  int32_t *indeg = calloc((size_t)n + 1, sizeof(int32_t));
+  int32_t *stack = malloc(sizeof(int32_t) * ((size_t)n + 1));
+  cp_key *tmp = malloc(sizeof(cp_key) * ((size_t)n + 1));
+  for (int32_t e = 0; e < g->m; e++) indeg[g->out_idx[e]]++;
+  /* sources, pushed so that the largest cpath (lowest id on ties) is on top */
+  int32_t ns = 0;
+  for (int32_t v = 0; v < n; v++)
+    if (indeg[v] == 0) {
+      tmp[ns].cpath = tlevel[v] + blevel[v];
+      tmp[ns].id = v;
+      ns++;
+    }
+  qsort(tmp, (size_t)ns, sizeof(cp_key), cmp_push);
+  int32_t top = 0;
+  for (int32_t k = 0; k < ns; k++) stack[top++] = tmp[k].id;
+  int32_t out = 0;
+  while (top > 0) {
+    int32_t v = stack[--top];
+    cpd_order[out++] = v;
+    int32_t nr = 0;
+    for (int32_t e = g->out_ptr[v]; e < g->out_ptr[v + 1]; e++) {
+      int32_t s = g->out_idx[e];
+      if (--indeg[s] == 0) {
+        tmp[nr].cpath = tlevel[s] + blevel[s];
+        tmp[nr].id = s;
+        nr++;
+      }
+    }
+    qsort(tmp, (size_t)nr, sizeof(cp_key), cmp_push);
+    for (int32_t k = 0; k < nr; k++) stack[top++] = tmp[k].id;
+  }
+  free(indeg);
+  free(stack);
+  free(tmp);
+  return out == n ? ORC_OK : ORC_E_CYCLE;
+}
+
 /* ------------------------------------------------------------- clustering */
 
 /* eq. 4 evaluated literally: the comm time of every edge that leaves the node

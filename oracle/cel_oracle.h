@@ -60,6 +60,15 @@ int orc_blevel(const orc_graph *g, const orc_devices *d, const int32_t *level,
                const int32_t *order_id, int32_t flags, int64_t *blevel,
                int64_t *tlevel, int32_t *prio_order, int64_t *cp);
 
+/* CPD-TOPO order (Section 5.1.3, Algorithm 1): with cpath(v) = tlevel(v) +
+ * blevel(v) (eq. 2-3, as given), a stack starts with the sources, the largest
+ * cpath on top; repeatedly the top node is popped and output, its out-edges
+ * are removed, and the successors left with no in-edge are pushed in
+ * increasing cpath order, so the most critical one is popped next.  Equal
+ * cpath: the lower id is output first.  cpd_order[k] = k-th node output. */
+int orc_cpd_topo(const orc_graph *g, const int64_t *blevel, const int64_t *tlevel,
+                 int32_t *cpd_order);
+
 /* Contiguous clustering of a topological order (Section 5.1.3, eq. 4-6):
  * DP over breakpoints minimising inter-cluster comm with cluster length <= R
  * and cluster memory <= M (a single node may exceed M).  M = -1 selects

@@ -57,7 +57,9 @@ def lib():
                                 _PU8, _PU8, _P64, _P64, _P32]
         L.orc_makespan.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), _P32, C.c_int32,
                                    _PU8, _P64, _P64, _P64]
-        for f in (L.orc_topo_levels, L.orc_blevel, L.orc_cluster, L.orc_place, L.orc_makespan):
+        L.orc_cpd_topo.argtypes = [C.POINTER(_Graph), _P64, _P64, _P32]
+        for f in (L.orc_topo_levels, L.orc_blevel, L.orc_cluster, L.orc_place, L.orc_makespan,
+                  L.orc_cpd_topo):
             f.restype = C.c_int
         _lib = L
     return _lib
@@ -121,6 +123,18 @@ def blevel(wl, level, order_id, comm_off=False, want_tlevel=True, want_prio=True
                             COMM_OFF if comm_off else 0, _ptr(bl, _P64), _ptr(tl, _P64),
                             _ptr(pr, _P32), C.byref(cp)), "orc_blevel")
     return (bl[:n], None if tl is None else tl[:n], None if pr is None else pr[:n], cp.value)
+
+
+def cpd_topo(wl, blevel, tlevel):
+    """CPD-TOPO order (Algorithm 1) from the given b-/t-levels -> int32[n] node ids."""
+    k = _Keep(wl)
+    n = int(wl.n)
+    bl = np.ascontiguousarray(blevel, np.int64)
+    tl = np.ascontiguousarray(tlevel, np.int64)
+    out = np.zeros(max(n, 1), np.int32)
+    _check(lib().orc_cpd_topo(C.byref(k.g), _ptr(bl, _P64), _ptr(tl, _P64), _ptr(out, _P32)),
+           "orc_cpd_topo")
+    return out[:n]
 
 
 def cluster(wl, order, R=200, M=-1, mode=DP):

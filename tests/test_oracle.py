@@ -484,3 +484,93 @@ def test_makespan_rejects_bad_device():
     with pytest.raises(O.OracleError) as ei:
         O.makespan(wl, [1, 0, 3, 2, 4, 5], np.array([0, 1, 2, 0, 0, 0], np.uint8))
     assert ei.value.code == O.E_ARG
+
+
+# ------------------------------------------------------------- CPD-TOPO order
+
+
+def cpd_of(wl):
+    lev, oid, lp, L = O.topo_levels(wl)
+    bl, tl, _, _ = O.blevel(wl, lev, oid, want_prio=False)
+    return O.cpd_topo(wl, bl, tl), bl + tl
+
+
+def test_hand6_cpd():
+    gd = load("hand6.json")
+    order, cpath = cpd_of(hand6())
+    assert list(cpath) == [17, 18, 16, 18, 18, 15]
+    assert list(order) == gd["cpd"]["cpd_order"]
+
+
+def test_cpd_two_chains_and_ties():
+    # one source, two chains; the heavier chain (cpath 11) is finished first
+    wl = from_edges(5, [(0, 1), (1, 2), (0, 3), (3, 4)], [1, 1, 1, 5, 5], [0] * 5, 2,
+                    [10 ** 9] * 2, 1, 0)
+    assert list(cpd_of(wl)[0]) == [0, 3, 4, 1, 2]
+    # equal chains: the lower id goes first, depth first
+    wl = from_edges(5, [(0, 1), (1, 3), (0, 2), (2, 4)], [1] * 5, [0] * 5, 2, [10 ** 9] * 2, 1, 0)
+    assert list(cpd_of(wl)[0]) == [0, 1, 3, 2, 4]
+    # sources by decreasing cpath, each followed by what it frees
+    wl = from_edges(4, [(0, 2), (1, 3)], [1, 4, 1, 1], [0] * 4, 2, [10 ** 9] * 2, 1, 0)
+    assert list(cpd_of(wl)[0]) == [1, 3, 0, 2]
+
+
+def preorder(wl, cpath):
+    """Textbook recursive preorder DFS of a forest (every node has at most one
+    parent), children visited by decreasing cpath, then increasing id."""
+    kids = [[] for _ in range(wl.n)]
+    has_parent = np.zeros(wl.n, bool)
+    for u, v in zip(*wl.edges()):
+        kids[int(u)].append(int(v))
+        has_parent[v] = True
+    key = lambda v: (-int(cpath[v]), v)  # noqa: E731
+    out = []
+
+    def visit(v):
+        out.append(v)
+        for c in sorted(kids[v], key=key):
+            visit(c)
+
+    for r in sorted((v for v in range(wl.n) if not has_parent[v]), key=key):
+        visit(r)
+    return out
+
+
+def test_cpd_forest_is_preorder_dfs():
+    """On a forest, CPD-TOPO reduces to a preorder depth-first traversal."""
+    rng = np.random.default_rng(21)
+    for s in range(30):
+        n = 1 + int(rng.integers(1, 300))
+        parent = [-1 if (v == 0 or rng.random() < 0.1) else int(rng.integers(0, v))
+                  for v in range(n)]
+        edges = [(p, v) for v, p in enumerate(parent) if p >= 0]
+        w = rng.integers(0, 30, n) if s % 3 else np.ones(n, np.int64)  # ties in some cases
+        wl = from_edges(n, edges, w, rng.integers(0, 60, n), 2, [10 ** 12] * 2, 7, 3)
+        order, cpath = cpd_of(wl)
+        assert list(order) == preorder(wl, cpath)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_cpd_topological_configs(cfg):
+    wl = make_config(cfg, 0)
+    order, _ = cpd_of(wl)
+    pos = np.empty(wl.n, np.int64)
+    pos[order] = np.arange(wl.n)
+    assert sorted(order.tolist()) == list(range(wl.n))
+    src = np.repeat(np.arange(wl.n), np.diff(np.asarray(wl.out_ptr)))
+    assert np.all(pos[src] < pos[np.asarray(wl.out_idx)])
+
+
+def test_cpd_small_dags_and_edge_cases():
+    for wl in small_dags():
+        order, _ = cpd_of(wl)
+        pos = {v: k for k, v in enumerate(order)}
+        assert sorted(order.tolist()) == list(range(wl.n))
+        assert all(pos[int(u)] < pos[int(v)] for u, v in zip(*wl.edges()))
+    wl = from_edges(0, [], [], [], 2, [5, 5], 3, 1)
+    assert len(cpd_of(wl)[0]) == 0
+    wl = from_edges(6, [(k, k + 1) for k in range(5)], [2] * 6, [1] * 6, 2, [50, 50], 1, 1)
+    assert list(cpd_of(wl)[0]) == list(range(6))  # a chain stays a chain
+    wl = from_edges(3, [(0, 1), (1, 2), (2, 0)], [1] * 3, [0] * 3, 2, [5, 5], 1, 0)
+    with pytest.raises(O.OracleError):
+        O.cpd_topo(wl, np.zeros(3, np.int64), np.zeros(3, np.int64))
