@@ -194,6 +194,27 @@ def batched_row(cel, torch, dev, args):
             "makespan_min_ns": int(ms.min().item()), "makespan_max_ns": int(ms.max().item())}
 
 
+def cpd_compare(cel, torch, g, d, bl, tl, prio, lev, lp, L):
+    """CPD-TOPO order (host walk over GPU b-/t-levels) and what it changes
+    downstream: DP clustering (R = 200) and Adjusting Placement on it, against
+    the level-monotone priority order."""
+    ts = []
+    for _ in range(3):
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        cpd = cel.cpd_order(g, bl, tl)
+        torch.cuda.synchronize()
+        ts.append((time.perf_counter() - a) * 1e3)
+    row = {"cpd_order_ms": float(np.median(ts))}
+    for name, order in (("priority", prio), ("cpd", cpd)):
+        cid, C, cut = cel.cluster(g, d, order, 200, -1)
+        _, ndev, cms, be = cel.place(g, d, cid, C)
+        ms, _, _ = cel.makespan(g, d, prio, lev, lp, L, ndev)
+        row[name] = {"clusters": C, "cut_cost_ns": cut, "coarse_makespan_ns": cms,
+                     "best_effort": be, "makespan_ns": int(ms[0].item())}
+    return row
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -312,13 +333,15 @@ def main() -> int:
     cel.kernel_stats(reset=True)
     cel.timing(True)
     e0.record(stream)
-    cel.blevel(g, d, lev, lp, oid, L, want_tlevel=True)
+    bl_t, tl_t, pr_t, _ = cel.blevel(g, d, lev, lp, oid, L, want_tlevel=True)
     e1.record(stream)
     torch.cuda.synchronize()
     cel.timing(False)
     ks_t = cel.kernel_stats(reset=True)
     tlevel_row = {"blevel_with_tlevel_ms": e0.elapsed_time(e1),
                   "k_tlevel_sweep_ms": ks_t.get("k_tlevel_sweep", (1, float("nan")))[1]}
+
+    cpd_row = cpd_compare(cel, torch, g, d, bl_t, tl_t, pr_t, lev, lp, L)
 
     batch5 = None if args.no_batch else batched_row(cel, torch, dev, args)
 
@@ -387,6 +410,7 @@ def main() -> int:
         "roofline": roofline,
         "ns_per_level": per_level,
         "tlevel": tlevel_row,
+        "cpd_topo": cpd_row,
         "batched_makespan": batched,
         "batched_scoring_200k": batch5,
         "cpu_baseline": cpu,

@@ -5,6 +5,7 @@
  *
  *   cel_topo_levels  level-synchronous topological ordering      (Section 4.2.2)
  *   cel_blevel       b-level / t-level / critical path, priority  (Section 5.1.3, eq. 2-3)
+ *   cel_cpd_order    CPD-TOPO critical-path depth-first order    (Section 5.1.3, Algorithm 1)
  *   cel_cluster      memory-capped contiguous clustering (DP)     (Section 5.1.3, eq. 4-6)
  *   cel_place        coarse graph + Adjusting Placement           (Section 5.2, eq. 7-9, Alg. 2)
  *   cel_makespan     makespan of one or K placements              (Section 5.2, eq. 7)
@@ -97,6 +98,22 @@ int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_t *level,
                const int32_t *level_ptr, const int32_t *order_id, int32_t n_levels,
                int32_t flags, int64_t *blevel, int64_t *tlevel, int32_t *prio_order,
                int64_t *cp, hipStream_t stream);
+
+/* CPD-TOPO order (Section 5.1.3, Algorithm 1), the critical-path depth-first
+ * topological order that the paper feeds to the clustering.  With cpath[v] =
+ * tlevel[v] + blevel[v], a stack starts with the sources (largest cpath on
+ * top); the top node is popped and output, its out-edges removed, and the
+ * successors left with no in-edge are pushed in increasing cpath order, so
+ * the most critical one comes next.  Equal cpath: the lower id first.
+ * Inputs: blevel [n] and tlevel [n] as produced by cel_blevel (with or
+ * without CEL_COMM_OFF); only the CSR half of the graph is read.
+ * Output: cpd_order [n], the node ids in CPD-TOPO order (a topological order,
+ * which cel_cluster accepts).  The walk is one dependent step per node, so
+ * it runs on the host over a copy of the successor lists; the call
+ * synchronises `stream` first.
+ * Errors: CEL_E_ARG (NULL or a malformed CSR), CEL_E_CYCLE, CEL_E_HIP. */
+int cel_cpd_order(const cel_graph *g, const int64_t *blevel, const int64_t *tlevel,
+                  int32_t *cpd_order, hipStream_t stream);
 
 /* Contiguous clustering of a topological order (Section 5.1.3, eq. 4-6;
  * clusters are runs of consecutive positions, which keeps the coarse graph

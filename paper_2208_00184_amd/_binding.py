@@ -20,7 +20,7 @@ OK, E_ARG, E_CYCLE, E_OVERFLOW, E_HIP, E_NOMEM, E_ORDER = 0, -1, -2, -3, -4, -5,
 COMM_OFF = 1
 CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
-EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cluster", "cel_place", "cel_makespan",
+EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_cluster", "cel_place", "cel_makespan",
            "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
@@ -60,8 +60,9 @@ def lib() -> C.CDLL:
         L.cel_cluster.argtypes = [G, Dv, vp, i32, i64, i32, vp, C.POINTER(i32), C.POINTER(i64), vp]
         L.cel_place.argtypes = [G, Dv, vp, i32, vp, vp, vp, C.POINTER(i64), C.POINTER(i32), vp]
         L.cel_makespan.argtypes = [G, Dv, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]
+        L.cel_cpd_order.argtypes = [G, vp, vp, vp, vp]
         for f in ("cel_topo_levels", "cel_blevel", "cel_cluster", "cel_place", "cel_makespan",
-                  "cel_version"):
+                  "cel_cpd_order", "cel_version"):
             getattr(L, f).restype = C.c_int
         L.cel_last_error.argtypes = []
         L.cel_last_error.restype = C.c_char_p
@@ -187,6 +188,15 @@ def blevel(g: Graph, d: Devices, level, level_ptr, order_id, n_levels, comm_off=
                             C.byref(cp), _stream()))
     return bl[:n], (tl[:n] if tl is not None else None), (pr[:n] if pr is not None else None), \
         cp.value
+
+
+def cpd_order(g: Graph, blevel_, tlevel_):
+    """CPD-TOPO order (Algorithm 1) from b-/t-levels -> int32[n] node ids."""
+    n = g.n
+    out = _empty(n, torch.int32, g.device)
+    gc = g._c()
+    _check(lib().cel_cpd_order(C.byref(gc), _p(blevel_), _p(tlevel_), _p(out), _stream()))
+    return out[:n]
 
 
 def cluster(g: Graph, d: Devices, order, R=200, M=-1, mode=CLUSTER_DP):

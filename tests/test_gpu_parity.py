@@ -602,3 +602,65 @@ def test_full_path_large(cfg):
     assert np.array_equal(np_(ms), rm[0]) and np.array_equal(np_(fi), rm[2])
     ms1, _, _ = cel.makespan(g, d, gb[2], gt[0], gt[2], gt[3], ndev)
     assert np_(ms1)[0] == rm[0][0]
+
+
+# ------------------------------------------------------------- CPD-TOPO order
+
+
+def gpu_cpd(g, d, comm_off=False):
+    lev, oid, lp, L = cel.topo_levels(g)
+    bl, tl, _, _ = cel.blevel(g, d, lev, lp, oid, L, comm_off=comm_off, want_tlevel=True,
+                              want_prio=False)
+    return cel.cpd_order(g, bl, tl)
+
+
+def oracle_cpd(wl, comm_off=False):
+    lev, oid, lp, L = O.topo_levels(wl)
+    bl, tl, _, _ = O.blevel(wl, lev, oid, comm_off=comm_off, want_prio=False)
+    return O.cpd_topo(wl, bl, tl)
+
+
+@pytest.mark.parametrize("cfg,comm_off", [(1, False), (1, True), (2, False), (3, False),
+                                          (5, False)])
+def test_cpd_order_configs(cfg, comm_off):
+    wl, _, _ = config(cfg, 0)
+    g, d = up(wl)
+    got = np_(gpu_cpd(g, d, comm_off))
+    assert np.array_equal(got, oracle_cpd(wl, comm_off))
+
+
+def test_cpd_order_transformer96():
+    wl = make_config(4, 0)
+    g, d = up(wl)
+    assert np.array_equal(np_(gpu_cpd(g, d)), oracle_cpd(wl))
+
+
+def test_cpd_order_random_and_edge_cases():
+    for s in range(12):
+        wl = make_random_dag(500 + s, 20 + 37 * s, p_edge=min(0.5, 3.0 / (20 + 37 * s)),
+                             D=2 + s % 4, multi=(s % 2 == 0), zero_frac=0.2 if s % 3 == 0 else 0)
+        g, d = up(wl)
+        assert np.array_equal(np_(gpu_cpd(g, d)), oracle_cpd(wl)), s
+    wl = from_edges(0, [], [], [], 2, [5, 5], 3, 1)
+    g, d = up(wl)
+    assert np_(gpu_cpd(g, d)).size == 0
+    wl = from_edges(1, [], [7], [100], 2, [5, 5], 3, 1)
+    g, d = up(wl)
+    assert np_(gpu_cpd(g, d)).tolist() == [0]
+    wl = from_edges(3, [(0, 1), (1, 2), (2, 0)], [1] * 3, [0] * 3, 2, [5, 5], 1, 0)
+    g, d = up(wl)
+    z = torch.zeros(3, dtype=torch.int64, device=DEV)
+    with pytest.raises(cel.CelError) as ei:
+        cel.cpd_order(g, z, z)
+    assert ei.value.code == -2
+
+
+@pytest.mark.parametrize("cfg", [1, 3])
+def test_cluster_on_cpd_order(cfg):
+    wl, _, _ = config(cfg, 0)
+    g, d = up(wl)
+    order = gpu_cpd(g, d)
+    ref = O.cluster(wl, oracle_cpd(wl), 200, -1)
+    cid, C, cut = cel.cluster(g, d, order, 200, -1)
+    assert C == ref[1] and cut == ref[2]
+    assert np.array_equal(np_(cid), ref[0])
