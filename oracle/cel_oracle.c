@@ -302,6 +302,61 @@ int orc_cpd_topo(const orc_graph *g, const int64_t *blevel, const int64_t *tleve
   return out == n ? ORC_OK : ORC_E_CYCLE;
 }
 
+/* ------------------------------------------------- CCR and Order-Place */
+
+/* eq. 1: CCR = sum over edges of c_{i,j} / sum over nodes of w_i; fusion keeps
+ * the total compute and drops the edges inside clusters (Section 5.1.1). */
+int orc_comm_sums(const orc_graph *g, const orc_devices *d, const int32_t *cluster_id,
+                  int64_t *edge_comm, int64_t *w_sum) {
+  int rc = check_graph(g);
+  if (rc) return rc;
+  if ((rc = check_devices(d))) return rc;
+  if ((rc = check_overflow(g, d))) return rc;
+  if (!edge_comm || !w_sum) return ORC_E_ARG;
+  int64_t ec = 0, ws = 0;
+  for (int32_t u = 0; u < g->n; u++) {
+    ws += g->w[u];
+    int64_t cu = comm_of(g->ob[u], d->bw, d->lat);
+    for (int32_t e = g->out_ptr[u]; e < g->out_ptr[u + 1]; e++)
+      if (!cluster_id || cluster_id[u] != cluster_id[g->out_idx[e]]) ec += cu;
+  }
+  *edge_comm = ec;
+  *w_sum = ws;
+  return ORC_OK;
+}
+
+/* Order-Place, Section 6: the coarse nodes in order, one device until its
+ * memory is used up, then the next. */
+int orc_order_place(const orc_graph *g, const orc_devices *d, const int32_t *cluster_id,
+                    int32_t n_clusters, uint8_t *cluster_dev, uint8_t *node_dev,
+                    int32_t *best_effort_count) {
+  int rc = check_graph(g);
+  if (rc) return rc;
+  if ((rc = check_devices(d))) return rc;
+  int32_t n = g->n, C = n_clusters;
+  if (C < 0 || !best_effort_count) return ORC_E_ARG;
+  if ((n > 0 && (!cluster_id || !node_dev || C < 1)) || (C > 0 && !cluster_dev)) return ORC_E_ARG;
+  for (int32_t v = 0; v < n; v++)
+    if (cluster_id[v] < 0 || cluster_id[v] >= C) return ORC_E_ARG;
+  int64_t *MEM = calloc((size_t)C + 1, sizeof(int64_t));
+  for (int32_t v = 0; v < n; v++) MEM[cluster_id[v]] += g->mem[v];
+  int32_t dev = 0, be = 0;
+  int64_t used = 0;
+  for (int32_t t = 0; t < C; t++) {
+    while (used + MEM[t] > d->cap[dev] && dev + 1 < d->D) {  /* full: the next device */
+      dev++;
+      used = 0;
+    }
+    if (used + MEM[t] > d->cap[dev]) be++;  /* the last device, over its cap */
+    cluster_dev[t] = (uint8_t)dev;
+    used += MEM[t];
+  }
+  for (int32_t v = 0; v < n; v++) node_dev[v] = cluster_dev[cluster_id[v]];
+  *best_effort_count = be;
+  free(MEM);
+  return ORC_OK;
+}
+
 /* ------------------------------------------------------------- clustering */
 
 /* eq. 4 evaluated literally: the comm time of every edge that leaves the node

@@ -83,6 +83,20 @@ int orc_place(const orc_graph *g, const orc_devices *d, const int32_t *cluster_i
               int32_t n_clusters, uint8_t *cluster_dev, uint8_t *node_dev,
               int64_t *cluster_fin, int64_t *coarse_makespan, int32_t *best_effort_count);
 
+/* CCR (eq. 1) parts: *edge_comm = sum over edges u->v of c[u] (with a
+ * cluster_id, only edges between different clusters: the coarse graph's
+ * edges), *w_sum = sum of w (unchanged by fusion).  cluster_id may be NULL. */
+int orc_comm_sums(const orc_graph *g, const orc_devices *d, const int32_t *cluster_id,
+                  int64_t *edge_comm, int64_t *w_sum);
+
+/* Order-Place (the baseline of Section 6, built on the coarse graph of
+ * Section 5.2): clusters in index order fill device 0 and move on to the next
+ * device when the next cluster does not fit the current one's remaining
+ * memory; the last device takes whatever is left (best effort, counted). */
+int orc_order_place(const orc_graph *g, const orc_devices *d, const int32_t *cluster_id,
+                    int32_t n_clusters, uint8_t *cluster_dev, uint8_t *node_dev,
+                    int32_t *best_effort_count);
+
 /* Makespan of K placements (node_dev is [K][n]): nodes taken in `order`, each
  * device runs its nodes first-in first-out, comm (eq. 7's indicator) paid only
  * across devices.  start/finish ([K][n], by node id) may be NULL. */

@@ -58,8 +58,12 @@ def lib():
         L.orc_makespan.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), _P32, C.c_int32,
                                    _PU8, _P64, _P64, _P64]
         L.orc_cpd_topo.argtypes = [C.POINTER(_Graph), _P64, _P64, _P32]
+        L.orc_comm_sums.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), _P32,
+                                    C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
+        L.orc_order_place.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), _P32, C.c_int32,
+                                      _PU8, _PU8, C.POINTER(C.c_int32)]
         for f in (L.orc_topo_levels, L.orc_blevel, L.orc_cluster, L.orc_place, L.orc_makespan,
-                  L.orc_cpd_topo):
+                  L.orc_cpd_topo, L.orc_comm_sums, L.orc_order_place):
             f.restype = C.c_int
         _lib = L
     return _lib
@@ -135,6 +139,29 @@ def cpd_topo(wl, blevel, tlevel):
     _check(lib().orc_cpd_topo(C.byref(k.g), _ptr(bl, _P64), _ptr(tl, _P64), _ptr(out, _P32)),
            "orc_cpd_topo")
     return out[:n]
+
+
+def comm_sums(wl, cluster_id=None):
+    """CCR parts (eq. 1) -> (edge comm, total w); with cluster_id only edges between clusters."""
+    k = _Keep(wl)
+    cid = None if cluster_id is None else np.ascontiguousarray(cluster_id, np.int32)
+    ec, ws = C.c_int64(0), C.c_int64(0)
+    _check(lib().orc_comm_sums(C.byref(k.g), C.byref(k.d), _ptr(cid, _P32), C.byref(ec),
+                               C.byref(ws)), "orc_comm_sums")
+    return ec.value, ws.value
+
+
+def order_place(wl, cluster_id, n_clusters):
+    """Order-Place -> (cluster_dev uint8[C], node_dev uint8[n], best_effort_count)."""
+    k = _Keep(wl)
+    n = int(wl.n)
+    cid = np.ascontiguousarray(cluster_id, np.int32)
+    cdev = np.zeros(max(n_clusters, 1), np.uint8)
+    ndev = np.zeros(max(n, 1), np.uint8)
+    be = C.c_int32(0)
+    _check(lib().orc_order_place(C.byref(k.g), C.byref(k.d), _ptr(cid, _P32), int(n_clusters),
+                                 _ptr(cdev, _PU8), _ptr(ndev, _PU8), C.byref(be)), "orc_order_place")
+    return cdev[:n_clusters], ndev[:n], be.value
 
 
 def cluster(wl, order, R=200, M=-1, mode=DP):

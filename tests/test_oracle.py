@@ -574,3 +574,61 @@ def test_cpd_small_dags_and_edge_cases():
     wl = from_edges(3, [(0, 1), (1, 2), (2, 0)], [1] * 3, [0] * 3, 2, [5, 5], 1, 0)
     with pytest.raises(O.OracleError):
         O.cpd_topo(wl, np.zeros(3, np.int64), np.zeros(3, np.int64))
+
+
+# ------------------------------------------------------- CCR and Order-Place
+
+
+def test_hand6_ccr_and_order_place():
+    gd = load("hand6.json")
+    wl = hand6()
+    e = gd["ccr"]
+    assert O.comm_sums(wl) == (e["edge_comm"], e["w_sum"])
+    cid = np.array(gd["order_place"]["cluster_id"], np.int32)
+    assert O.comm_sums(wl, cid) == (e["edge_comm_clustered"], e["w_sum"])
+    for caps, key in (((60, 60), "caps_60"), ((30, 30), "caps_30")):
+        cdev, ndev, be = O.order_place(hand6(cap=caps), cid, 3)
+        assert cdev.tolist() == gd["order_place"][key]["cluster_dev"]
+        assert be == gd["order_place"][key]["best_effort"]
+        assert ndev.tolist() == [int(cdev[c]) for c in cid]
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_ccr_sums_configs(cfg):
+    """Unclustered: sum over nodes of out-degree x c (closed form); clustered by
+    the DP: equal to the DP's own cut cost S(n)."""
+    wl = make_config(cfg, 0)
+    c = np.asarray(O.comm(wl), np.int64)
+    outdeg = np.diff(np.asarray(wl.out_ptr)).astype(np.int64)
+    assert O.comm_sums(wl) == (int((outdeg * c).sum()), int(np.asarray(wl.w).sum()))
+    lev, oid, lp, L = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    cid, C, cut = O.cluster(wl, pr, 200, -1)
+    assert O.comm_sums(wl, cid)[0] == cut
+
+
+def test_order_place_properties():
+    rng = np.random.default_rng(8)
+    for s in range(40):
+        wl = make_random_dag(900 + s, 5 + s * 7, p_edge=0.1, D=1 + s % 6, cap_frac=(1, 1 + s % 4))
+        order = O.topo_levels(wl)[1]
+        cid, C, _ = O.cluster(wl, order, int(rng.integers(1, 12)), -1, s % 2)
+        cdev, ndev, be = O.order_place(wl, cid, C)
+        mem = np.zeros(C, np.int64)
+        np.add.at(mem, cid, np.asarray(wl.mem, np.int64))
+        cap = np.asarray(wl.cap, np.int64)
+        assert np.all(np.diff(cdev.astype(int)) >= 0)           # devices in cluster order
+        assert np.array_equal(ndev, cdev[cid])
+        used = np.zeros(wl.D, np.int64)
+        np.add.at(used, cdev.astype(int), mem)
+        if be == 0:
+            assert np.all(used <= cap)
+        for t in range(1, C):                                    # a move only when forced
+            if cdev[t] != cdev[t - 1]:
+                prev = cdev[t - 1]
+                filled = mem[:t][cdev[:t] == prev].sum()
+                assert filled + mem[t] > cap[prev]
+    wl = make_random_dag(7, 30, p_edge=0.2, D=1)
+    cid = np.arange(30, dtype=np.int32)
+    cdev, _, _ = O.order_place(wl, cid, 30)
+    assert not cdev.any()                                        # one device takes all
