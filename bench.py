@@ -194,24 +194,37 @@ def batched_row(cel, torch, dev, args):
             "makespan_min_ns": int(ms.min().item()), "makespan_max_ns": int(ms.max().item())}
 
 
-def cpd_compare(cel, torch, g, d, bl, tl, prio, lev, lp, L):
-    """CPD-TOPO order (host walk over GPU b-/t-levels) and what it changes
-    downstream: DP clustering (R = 200) and Adjusting Placement on it, against
-    the level-monotone priority order."""
-    ts = []
-    for _ in range(3):
+def _timed(torch, f, reps=3):
+    ts, out = [], None
+    for _ in range(reps):
         torch.cuda.synchronize()
         a = time.perf_counter()
-        cpd = cel.cpd_order(g, bl, tl)
+        out = f()
         torch.cuda.synchronize()
         ts.append((time.perf_counter() - a) * 1e3)
-    row = {"cpd_order_ms": float(np.median(ts))}
+    return out, float(np.median(ts))
+
+
+def cpd_compare(cel, torch, g, d, bl, tl, prio, lev, lp, L):
+    """CPD-TOPO order (host walk over GPU b-/t-levels) and what it changes
+    downstream: DP clustering (R = 200) on it against the level-monotone
+    priority order; for each, the CCR before and after fusion (eq. 1, as in
+    the paper's CCR table) and the makespan of Order-Place against Adjusting
+    Placement on the same clusters (as in its placement comparison)."""
+    cpd, cpd_ms = _timed(torch, lambda: cel.cpd_order(g, bl, tl))
+    (ec0, ws), ccr_ms = _timed(torch, lambda: cel.comm_sums(g, d))
+    row = {"cpd_order_ms": cpd_ms, "comm_sums_ms": ccr_ms, "n": g.n, "ccr": ec0 / ws}
     for name, order in (("priority", prio), ("cpd", cpd)):
         cid, C, cut = cel.cluster(g, d, order, 200, -1)
+        ec, _ = cel.comm_sums(g, d, cid)
         _, ndev, cms, be = cel.place(g, d, cid, C)
         ms, _, _ = cel.makespan(g, d, prio, lev, lp, L, ndev)
-        row[name] = {"clusters": C, "cut_cost_ns": cut, "coarse_makespan_ns": cms,
-                     "best_effort": be, "makespan_ns": int(ms[0].item())}
+        (_, ndev_o, be_o), op_ms = _timed(torch, lambda: cel.order_place(g, d, cid, C))
+        ms_o, _, _ = cel.makespan(g, d, prio, lev, lp, L, ndev_o)
+        row[name] = {"clusters": C, "cut_cost_ns": cut, "ccr_fused": ec / ws,
+                     "coarse_makespan_ns": cms, "best_effort": be, "makespan_ns": int(ms[0].item()),
+                     "order_place": {"makespan_ns": int(ms_o[0].item()), "best_effort": be_o,
+                                     "ms": op_ms}}
     return row
 
 

@@ -9,6 +9,8 @@
  *   cel_cluster      memory-capped contiguous clustering (DP)     (Section 5.1.3, eq. 4-6)
  *   cel_place        coarse graph + Adjusting Placement           (Section 5.2, eq. 7-9, Alg. 2)
  *   cel_makespan     makespan of one or K placements              (Section 5.2, eq. 7)
+ *   cel_order_place  Order-Place baseline placement               (Section 5.2, 6.2.2)
+ *   cel_comm_sums    the parts of the comm/compute ratio CCR      (Section 5.1.1, eq. 1)
  *
  * Conventions (all entry points):
  *  - Arrays are DEVICE pointers owned by the caller unless marked (host).  The
@@ -150,6 +152,31 @@ int cel_place(const cel_graph *g, const cel_devices *d, const int32_t *cluster_i
               int32_t n_clusters, uint8_t *cluster_dev, uint8_t *node_dev,
               int64_t *cluster_fin, int64_t *coarse_makespan, int32_t *best_effort_count,
               hipStream_t stream);
+
+/* Order-Place, the baseline placement of Sections 5.2 and 6.2.2: clusters are taken in
+ * index order and filled onto device 0 until the next cluster's MEM (sum of
+ * its members' mem) no longer fits that device's remaining cap, then onto
+ * device 1, and so on; once the last device is reached every remaining
+ * cluster goes there, and each one that does not fit it counts as best
+ * effort.  Nodes inherit their cluster's device.  Clusters may be empty.
+ * Inputs: cluster_id [n] with values in [0, n_clusters); n_clusters >= 1
+ * when n > 0; the total mem must stay below 2^63.
+ * Outputs: cluster_dev [C] uint8; node_dev [n] uint8; best_effort_count
+ * (host).
+ * Errors: CEL_E_ARG, CEL_E_HIP, CEL_E_NOMEM. */
+int cel_order_place(const cel_graph *g, const cel_devices *d, const int32_t *cluster_id,
+                    int32_t n_clusters, uint8_t *cluster_dev, uint8_t *node_dev,
+                    int32_t *best_effort_count, hipStream_t stream);
+
+/* The two parts of the communication-to-computation ratio CCR (Section 5.1.1, eq. 1): edge_comm
+ * = sum over edges u->v of c[u] (only the edges whose ends sit in different
+ * clusters when cluster_id is given), w_sum = sum of w; CCR = edge_comm /
+ * w_sum is left to the caller.
+ * Inputs: cluster_id [n] or NULL for the whole graph.
+ * Outputs: edge_comm, w_sum (host).
+ * Errors: CEL_E_ARG, CEL_E_OVERFLOW, CEL_E_HIP, CEL_E_NOMEM. */
+int cel_comm_sums(const cel_graph *g, const cel_devices *d, const int32_t *cluster_id,
+                  int64_t *edge_comm, int64_t *w_sum, hipStream_t stream);
 
 /* Makespan of K placements (eq. 7 without insertion): nodes are taken in
  * `order`; a node is ready when every predecessor p has finished, plus c[p]

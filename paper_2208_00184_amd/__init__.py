@@ -3,10 +3,10 @@
 The computation lives in libcel.so (HIP kernels behind the C ABI of
 include/cel.h); this package is its thin Python binding.
 """
-from ._binding import (CelError, Devices, Graph, blevel, cluster, cpd_order, kernel_stats, lib, makespan,
-                       place, timing, topo_levels, version, CLUSTER_DP, CLUSTER_GREEDY,
+from ._binding import (CelError, Devices, Graph, blevel, cluster, comm_sums, cpd_order, kernel_stats, lib,
+                       makespan, order_place, place, timing, topo_levels, version, CLUSTER_DP, CLUSTER_GREEDY,
                        COMM_OFF, EXPORTS, LIB_PATH)
 
-__all__ = ["CelError", "Devices", "Graph", "blevel", "cluster", "cpd_order", "kernel_stats", "lib", "makespan",
-           "place", "timing", "topo_levels", "version", "CLUSTER_DP", "CLUSTER_GREEDY", "COMM_OFF", "EXPORTS",
+__all__ = ["CelError", "Devices", "Graph", "blevel", "cluster", "comm_sums", "cpd_order", "kernel_stats", "lib",
+           "makespan", "order_place", "place", "timing", "topo_levels", "version", "CLUSTER_DP", "CLUSTER_GREEDY", "COMM_OFF", "EXPORTS",
            "LIB_PATH"]

@@ -21,7 +21,7 @@ COMM_OFF = 1
 CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
 EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_cluster", "cel_place", "cel_makespan",
-           "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
+           "cel_order_place", "cel_comm_sums", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
 class CelError(RuntimeError):
@@ -61,8 +61,10 @@ def lib() -> C.CDLL:
         L.cel_place.argtypes = [G, Dv, vp, i32, vp, vp, vp, C.POINTER(i64), C.POINTER(i32), vp]
         L.cel_makespan.argtypes = [G, Dv, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]
         L.cel_cpd_order.argtypes = [G, vp, vp, vp, vp]
+        L.cel_order_place.argtypes = [G, Dv, vp, i32, vp, vp, C.POINTER(i32), vp]
+        L.cel_comm_sums.argtypes = [G, Dv, vp, C.POINTER(i64), C.POINTER(i64), vp]
         for f in ("cel_topo_levels", "cel_blevel", "cel_cluster", "cel_place", "cel_makespan",
-                  "cel_cpd_order", "cel_version"):
+                  "cel_cpd_order", "cel_order_place", "cel_comm_sums", "cel_version"):
             getattr(L, f).restype = C.c_int
         L.cel_last_error.argtypes = []
         L.cel_last_error.restype = C.c_char_p
@@ -225,6 +227,28 @@ def place(g: Graph, d: Devices, cluster_id, n_clusters, want_fin=False):
                            _p(ndev), _p(fin), C.byref(span), C.byref(be), _stream()))
     out = (cdev[:n_clusters], ndev[:n], span.value, be.value)
     return out + (fin[:n_clusters],) if want_fin else out
+
+
+def order_place(g: Graph, d: Devices, cluster_id, n_clusters):
+    """Order-Place -> (cluster_dev uint8[C], node_dev uint8[n], best_effort_count)"""
+    n = g.n
+    cdev = _empty(n_clusters, torch.uint8, g.device)
+    ndev = _empty(n, torch.uint8, g.device)
+    be = C.c_int32(0)
+    gc, dc = g._c(), d._c()
+    _check(lib().cel_order_place(C.byref(gc), C.byref(dc), _p(cluster_id), int(n_clusters), _p(cdev),
+                                 _p(ndev), C.byref(be), _stream()))
+    return cdev[:n_clusters], ndev[:n], be.value
+
+
+def comm_sums(g: Graph, d: Devices, cluster_id=None):
+    """CCR parts (eq. 1) -> (edge comm, total w); with cluster_id only edges between clusters."""
+    ec = C.c_int64(0)
+    ws = C.c_int64(0)
+    gc, dc = g._c(), d._c()
+    _check(lib().cel_comm_sums(C.byref(gc), C.byref(dc), _p(cluster_id), C.byref(ec), C.byref(ws),
+                               _stream()))
+    return ec.value, ws.value
 
 
 def makespan(g: Graph, d: Devices, order, level, level_ptr, n_levels, node_dev, want_times=False):

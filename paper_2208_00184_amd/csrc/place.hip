@@ -1,5 +1,6 @@
 // cel_place: coarse graph + Adjusting Placement (Section 5.2, eq. 7-9,
-// Algorithm 2).
+// Algorithm 2); also the Order-Place baseline (Sections 5.2, 6.2.2) and the
+// CCR parts (Section 5.1.1, eq. 1) used to compare them.
 //
 // Coarse graph (data-parallel): cluster sums by atomics; every edge between
 // two clusters is bucketed by its target cluster, each bucket sorted by
@@ -469,6 +470,63 @@ __global__ void k_place_out(int32_t n, int32_t C, const int32_t *cid, const uint
   }
 }
 
+// CCR parts (Section 5.1.1, eq. 1): the comm of the edges (only between clusters when cid is
+// given) and the total compute; edge-balanced blocks, block sums in LDS, one
+// atomic per block.
+__global__ void k_comm_sums(cel_graph g, int64_t bw, int64_t lat, const int32_t *cid,
+                            unsigned long long *sums, const Status *st) {
+  __shared__ int32_t ptr[kRowsPB + 1], su[2];
+  __shared__ unsigned long long s_e, s_w;
+  if (failed(st)) return;
+  if (threadIdx.x == 0) s_e = s_w = 0;
+  __syncthreads();
+  unsigned long long ec = 0, ws = 0;
+  for_edges_balanced(g.out_ptr, g.n, g.m, ptr, su, [&](int32_t u, int32_t e) {
+    if (!cid || cid[u] != cid[g.out_idx[e]]) ec += (unsigned long long)comm_of(g.ob[u], bw, lat);
+  });
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < g.n;
+       v += (int64_t)gridDim.x * blockDim.x)
+    ws += (unsigned long long)g.w[v];
+  if (ec) atomicAdd(&s_e, ec);
+  if (ws) atomicAdd(&s_w, ws);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    atomicAdd(&sums[0], s_e);
+    atomicAdd(&sums[1], s_w);
+  }
+}
+
+// Order-Place (the baseline of Sections 5.2, 6.2.2): clusters in index order fill one
+// device until the next cluster does not fit its remaining memory, then the
+// next device; the last device takes the rest (best effort, counted).  One
+// wave: the fill state is uniform, cluster sizes come 64 at a time.
+__global__ void __launch_bounds__(64)
+    k_order_place(int32_t C, int32_t D, const int64_t *cap, const uint64_t *MEM, uint8_t *cdev,
+                  Status *st) {
+  if (failed(st)) return;
+  const int lane = threadIdx.x;
+  int32_t dev = 0, be = 0;
+  int64_t used = 0, capd = cap[0];
+  for (int32_t t0 = 0; t0 < C; t0 += 64) {
+    const int64_t mv = t0 + lane < C ? (int64_t)MEM[t0 + lane] : 0;
+    const int nt = C - t0 < 64 ? C - t0 : 64;
+    int32_t mine = 0;
+    for (int l = 0; l < nt; l++) {
+      const int64_t mt = readlane64(mv, l);
+      while (used + mt > capd && dev + 1 < D) {  // full: the next device
+        dev++;
+        used = 0;
+        capd = cap[dev];
+      }
+      if (used + mt > capd) be++;  // the last device, over its cap
+      used += mt;
+      if (lane == l) mine = dev;
+    }
+    if (t0 + lane < C) cdev[t0 + lane] = (uint8_t)mine;
+  }
+  if (lane == 0) st->i0 = be;
+}
+
 }  // namespace cel
 
 using namespace cel;
@@ -562,6 +620,79 @@ extern "C" int cel_place(const cel_graph *g, const cel_devices *d, const int32_t
   CEL_TRY(read_status(st, &h, s));
   if (h.err) return status_error(h, fn);
   *coarse_makespan = h.s0;
+  *best_effort_count = h.i0;
+  return CEL_OK;
+}
+
+extern "C" int cel_comm_sums(const cel_graph *g, const cel_devices *d, const int32_t *cluster_id,
+                             int64_t *edge_comm, int64_t *w_sum, hipStream_t s) {
+  const char *fn = "cel_comm_sums";
+  CEL_TRY(check_host_graph(g, fn));
+  CEL_TRY(check_host_devices(d, fn));
+  if (!edge_comm || !w_sum) return set_error(CEL_E_ARG, "%s: NULL argument", fn);
+  Scratch sc(s);
+  Status *st;
+  int32_t *tmp;
+  unsigned long long *sums;
+  CEL_TRY(sc.get(&st, 1));
+  CEL_TRY(sc.get(&tmp, g->n));
+  CEL_TRY(sc.get(&sums, 2));
+  CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
+  CEL_HIP(hipMemsetAsync(sums, 0, 2 * sizeof(unsigned long long), s));
+  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, sc, s));
+  k_comm_sums<<<edge_blocks(g->m), 256, 0, s>>>(*g, d->bw, d->lat, cluster_id, sums, st);
+  CEL_HIP(hipGetLastError());
+  unsigned long long h2[2] = {0, 0};
+  CEL_HIP(hipMemcpyAsync(h2, sums, sizeof h2, hipMemcpyDeviceToHost, s));
+  Status h;
+  CEL_TRY(read_status(st, &h, s));
+  if (h.err) return status_error(h, fn);
+  *edge_comm = (int64_t)h2[0];
+  *w_sum = (int64_t)h2[1];
+  return CEL_OK;
+}
+
+extern "C" int cel_order_place(const cel_graph *g, const cel_devices *d, const int32_t *cluster_id,
+                               int32_t C, uint8_t *cluster_dev, uint8_t *node_dev,
+                               int32_t *best_effort_count, hipStream_t s) {
+  const char *fn = "cel_order_place";
+  CEL_TRY(check_host_graph(g, fn));
+  CEL_TRY(check_host_devices(d, fn));
+  const int32_t n = g->n;
+  if (!best_effort_count || (n > 0 && (!cluster_id || !node_dev)) || (C > 0 && !cluster_dev))
+    return set_error(CEL_E_ARG, "%s: NULL argument", fn);
+  if (C < 0 || (n > 0 && C < 1))
+    return set_error(CEL_E_ARG, "%s: n_clusters = %d out of range", fn, C);
+  Scratch sc(s);
+  Status *st;
+  int32_t *tmp;
+  CEL_TRY(sc.get(&st, 1));
+  CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
+  CEL_TRY(sc.get(&tmp, n));
+  CEL_TRY(check_graph(g, d->bw, d->lat, false, st, tmp, sc, s));
+  if (C == 0) {
+    Status h;
+    CEL_TRY(read_status(st, &h, s));
+    if (h.err) return status_error(h, fn);
+    *best_effort_count = 0;
+    return CEL_OK;
+  }
+  uint64_t *W, *MEM;
+  int64_t *dcap;
+  CEL_TRY(sc.get(&W, C));
+  CEL_TRY(sc.get(&MEM, C));
+  CEL_TRY(sc.get(&dcap, d->D));
+  CEL_HIP(hipMemsetAsync(W, 0, sizeof(uint64_t) * C, s));
+  CEL_HIP(hipMemsetAsync(MEM, 0, sizeof(uint64_t) * C, s));
+  CEL_HIP(hipMemcpyAsync(dcap, d->cap, sizeof(int64_t) * d->D, hipMemcpyHostToDevice, s));
+  k_place_nodes<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, C, cluster_id, g->w, g->mem, W, MEM, st);
+  k_order_place<<<1, 64, 0, s>>>(C, d->D, dcap, MEM, cluster_dev, st);
+  k_place_out<<<grid_for(n > C ? n : C, 256, 4096), 256, 0, s>>>(n, C, cluster_id, cluster_dev,
+                                                                node_dev, nullptr, nullptr, st);
+  CEL_HIP(hipGetLastError());
+  Status h;
+  CEL_TRY(read_status(st, &h, s));
+  if (h.err) return status_error(h, fn);
   *best_effort_count = h.i0;
   return CEL_OK;
 }

@@ -664,3 +664,112 @@ def test_cluster_on_cpd_order(cfg):
     cid, C, cut = cel.cluster(g, d, order, 200, -1)
     assert C == ref[1] and cut == ref[2]
     assert np.array_equal(np_(cid), ref[0])
+
+
+# ----------------------------------------- Order-Place and the CCR parts
+
+
+def check_order_place(wl, cid, C):
+    ref = O.order_place(wl, cid, C)
+    g, d = up(wl)
+    cdev, ndev, be = cel.order_place(g, d, tt(cid, np.int32), C)
+    assert be == ref[2]
+    assert np.array_equal(np_(cdev), ref[0])
+    assert np.array_equal(np_(ndev), ref[1])
+    return ref
+
+
+def check_comm_sums(wl, cid=None):
+    ref = O.comm_sums(wl, cid)
+    g, d = up(wl)
+    got = cel.comm_sums(g, d, None if cid is None else tt(cid, np.int32))
+    assert got == ref
+    return ref
+
+
+def test_order_place_and_ccr_hand6():
+    import json
+    import os
+    gd = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "hand6.json")))
+    g6 = gd["graph"]
+    cid = np.array(gd["order_place"]["cluster_id"], np.int32)
+    for caps, key in (((60, 60), "caps_60"), ((30, 30), "caps_30")):
+        wl = from_edges(g6["n"], g6["edges"], g6["w"], g6["ob"], 2, caps, g6["bw"], g6["lat"],
+                        mem=g6["mem"])
+        g, d = up(wl)
+        cdev, ndev, be = cel.order_place(g, d, tt(cid, np.int32), 3)
+        assert np_(cdev).tolist() == gd["order_place"][key]["cluster_dev"]
+        assert be == gd["order_place"][key]["best_effort"]
+        assert np_(ndev).tolist() == [np_(cdev)[c] for c in cid]
+    assert cel.comm_sums(g, d) == (gd["ccr"]["edge_comm"], gd["ccr"]["w_sum"])
+    assert cel.comm_sums(g, d, tt(cid, np.int32))[0] == gd["ccr"]["edge_comm_clustered"]
+
+
+@pytest.mark.parametrize("cfg,seed", [(1, 0), (2, 0), (3, 0), (5, 0)])
+def test_order_place_and_ccr_configs(cfg, seed):
+    """The priority- and CPD-order clusterings of each config, at its own caps and
+    at caps tight enough to move across devices and end in best effort."""
+    import dataclasses
+    wl, rt, rb = config(cfg, seed)
+    check_comm_sums(wl)
+    for order in (rb[2], oracle_cpd(wl)):
+        for R, mode in ((200, O.DP), (40, O.GREEDY)):
+            cid, C, cut = O.cluster(wl, order, R, -1, mode)
+            ec, ws = check_comm_sums(wl, cid)
+            assert ec == cut
+            for frac in (None, 8, 64):
+                w2 = wl if frac is None else dataclasses.replace(
+                    wl, cap=np.full(wl.D, int(wl.mem.sum()) // frac, np.int64))
+                check_order_place(w2, cid, C)
+
+
+def test_order_place_random_and_edge_cases():
+    import dataclasses
+    rng = np.random.default_rng(9)
+    for s in range(24):
+        n = 2 + (s * 53) % 700
+        wl = make_random_dag(900 + s, n, p_edge=min(0.5, 4.0 / n), D=1 + s % 7,
+                             cap_frac=(1, 1 + s % 9), multi=(s % 3 == 0),
+                             zero_frac=0.2 if s % 4 == 0 else 0.0)
+        check_comm_sums(wl)
+        order = random_topo_order(wl, rng)
+        cid, C, _ = O.cluster(wl, order, int(rng.integers(1, 30)), -1, s % 2)
+        check_comm_sums(wl, cid)
+        check_order_place(wl, cid, C)
+        # caps that differ per device (some zero), and empty clusters past the used ids
+        w2 = dataclasses.replace(wl, cap=rng.integers(0, max(2, int(wl.mem.sum()) // 2),
+                                                      wl.D).astype(np.int64))
+        check_order_place(w2, cid, C + 1 + s % 70)
+    wl = from_edges(0, [], [], [], 2, [5, 5], 3, 1)
+    g, d = up(wl)
+    assert cel.comm_sums(g, d) == (0, 0)
+    z = torch.zeros(0, dtype=torch.int32, device=DEV)
+    cdev, ndev, be = cel.order_place(g, d, z, 0)
+    assert np_(cdev).size == 0 and np_(ndev).size == 0 and be == 0
+    check_order_place(wl, np.zeros(0, np.int32), 3)
+    wl = from_edges(3, [(0, 1), (1, 2)], [1, 2, 3], [4, 5, 6], 3, [10, 0, 3], 2, 1)
+    check_order_place(wl, np.array([0, 1, 2], np.int32), 3)  # mem 8, 10, 12
+    check_order_place(wl, np.array([0, 0, 0], np.int32), 1)
+    g, d = up(wl)
+    with pytest.raises(cel.CelError) as ei:  # id out of range
+        cel.order_place(g, d, tt(np.array([0, 1, 3], np.int32), np.int32), 3)
+    assert ei.value.code == -1
+    with pytest.raises(cel.CelError) as ei:  # no clusters for three nodes
+        cel.order_place(g, d, tt(np.zeros(3, np.int32), np.int32), 0)
+    assert ei.value.code == -1
+    wl = from_edges(2, [(0, 1)], [1, 1], [2 ** 62, 0], 2, [5, 5], 1, 0, mem=[0, 0])
+    g, d = up(wl)
+    with pytest.raises(cel.CelError) as ei:
+        cel.comm_sums(g, d)
+    assert ei.value.code == -3
+
+
+def test_order_place_and_ccr_transformer96():
+    """Full size: 1.07M nodes, the CPD-order clustering of Section 5.1.3."""
+    wl = make_config(4, 0)
+    g, d = up(wl)
+    ocpd = oracle_cpd(wl)
+    cid, C, cut = O.cluster(wl, ocpd, 200, -1)
+    assert check_comm_sums(wl, cid)[0] == cut
+    check_comm_sums(wl)
+    check_order_place(wl, cid, C)
