@@ -696,3 +696,119 @@ int orc_makespan(const orc_graph *g, const orc_devices *d, const int32_t *order,
   free(c); free(fin); free(avail);
   return ORC_OK;
 }
+
+/* Makespan under the richer device models (node_dev is [K][n], model a set of
+ * ORC_MODEL_* bits; model 0 is orc_makespan's schedule).
+ *
+ * ORC_MODEL_INSERT: the device slot rule of eq. 7 applied to single nodes.  A
+ *   node starts at the earliest time >= ready at which it fits between the
+ *   tasks already placed on its device (first fit over that device's busy
+ *   intervals), instead of after the device's last task.  A node with w = 0
+ *   starts at ready and occupies nothing.
+ * ORC_MODEL_COMM_TASKS: a transfer is a task of its own (the runtime model of
+ *   Section 6.1).  After node u finishes on device a, one transfer of its
+ *   output goes to each other device b that holds a successor of u, in
+ *   increasing b; it takes c[u] and occupies a's send channel and b's receive
+ *   channel together, each channel serving its transfers one at a time in the
+ *   order they are issued: start = max(fin[u], send free[a], receive free[b]).
+ *   A successor on b is ready for u's output when that transfer ends; outputs
+ *   consumed on their own device need no transfer.  Compute never waits for a
+ *   channel other than through its inputs. */
+int orc_makespan_model(const orc_graph *g, const orc_devices *d, const int32_t *order,
+                       int32_t K, const uint8_t *node_dev, int32_t model, int64_t *start,
+                       int64_t *finish, int64_t *makespan) {
+  int rc = check_graph(g);
+  if (rc) return rc;
+  if ((rc = check_devices(d))) return rc;
+  if ((rc = check_overflow(g, d))) return rc;
+  int32_t n = g->n, D = d->D;
+  if (K < 1 || !makespan || (n > 0 && !node_dev) || (model & ~3)) return ORC_E_ARG;
+  for (int64_t i = 0; i < (int64_t)K * n; i++)
+    if (node_dev[i] >= D) return ORC_E_ARG;
+  int32_t *pos = malloc(sizeof(int32_t) * (size_t)(n + 1));
+  rc = check_order(g, order, pos);
+  free(pos);
+  if (rc) return rc;
+  const int insert = model & ORC_MODEL_INSERT, tasks = model & ORC_MODEL_COMM_TASKS;
+  int64_t *c = malloc(sizeof(int64_t) * (size_t)(n + 1));
+  for (int32_t v = 0; v < n; v++) c[v] = comm_of(g->ob[v], d->bw, d->lat);
+  int64_t *fin = malloc(sizeof(int64_t) * (size_t)(n + 1));
+  int64_t *avail = malloc(sizeof(int64_t) * (size_t)D);
+  int64_t *snd = malloc(sizeof(int64_t) * (size_t)D), *rcv = malloc(sizeof(int64_t) * (size_t)D);
+  /* arrival of u's output on device b (transfers only) */
+  int64_t *arr = tasks ? malloc(sizeof(int64_t) * ((size_t)n * D + 1)) : NULL;
+  char *wants = malloc((size_t)D);
+  /* busy intervals per device, sorted by start (insertion only) */
+  int64_t *bs = insert ? malloc(sizeof(int64_t) * ((size_t)n + 1)) : NULL;
+  int64_t *bf = insert ? malloc(sizeof(int64_t) * ((size_t)n + 1)) : NULL;
+  int32_t *boff = malloc(sizeof(int32_t) * (size_t)(D + 1)), *nb = malloc(sizeof(int32_t) * (size_t)D);
+  for (int32_t k = 0; k < K; k++) {
+    const uint8_t *dev = node_dev + (int64_t)k * n;
+    for (int32_t x = 0; x < D; x++) avail[x] = snd[x] = rcv[x] = 0, nb[x] = 0;
+    /* device x's busy list lives in bs/bf[boff[x] .. boff[x] + its node count) */
+    for (int32_t x = 0; x <= D; x++) boff[x] = 0;
+    for (int32_t v = 0; v < n; v++) boff[dev[v] + 1]++;
+    for (int32_t x = 0; x < D; x++) boff[x + 1] += boff[x];
+    int64_t span = 0;
+    for (int32_t p = 0; p < n; p++) {
+      int32_t v = order[p], dv = dev[v];
+      int64_t ready = 0;
+      for (int32_t e = g->in_ptr[v]; e < g->in_ptr[v + 1]; e++) {
+        int32_t u = g->in_idx[e];
+        int64_t r;
+        if (dev[u] == dv) r = fin[u];
+        else if (tasks) r = arr[(int64_t)u * D + dv];
+        else r = fin[u] + c[u];
+        if (r > ready) ready = r;
+      }
+      int64_t s, w = g->w[v];
+      if (!insert) {
+        s = ready > avail[dv] ? ready : avail[dv];
+        avail[dv] = s + w;
+      } else {
+        int64_t *xs = bs + boff[dv], *xf = bf + boff[dv];
+        int32_t cnt = nb[dv];
+        s = ready;
+        if (w > 0) {
+          /* intervals ending at or before ready cannot overlap [s, s + w):
+           * skip them by bisection (the intervals are disjoint, so their ends
+           * are sorted too), then take the first gap that holds w */
+          int32_t lo = 0, hi = cnt;
+          while (lo < hi) {
+            int32_t mid = lo + (hi - lo) / 2;
+            if (xf[mid] <= s) lo = mid + 1; else hi = mid;
+          }
+          int32_t q = lo;
+          for (; q < cnt; q++) {
+            if (xs[q] < s + w) s = xf[q];
+            else break;
+          }
+          for (int32_t i = cnt; i > q; i--) xs[i] = xs[i - 1], xf[i] = xf[i - 1];
+          xs[q] = s;
+          xf[q] = s + w;
+          nb[dv] = cnt + 1;
+        }
+      }
+      fin[v] = s + w;
+      if (fin[v] > span) span = fin[v];
+      if (start) start[(int64_t)k * n + v] = s;
+      if (tasks) {
+        for (int32_t x = 0; x < D; x++) wants[x] = 0;
+        for (int32_t e = g->out_ptr[v]; e < g->out_ptr[v + 1]; e++) wants[dev[g->out_idx[e]]] = 1;
+        for (int32_t b = 0; b < D; b++) {
+          if (b == dv || !wants[b]) continue;
+          int64_t t0 = fin[v];
+          if (snd[dv] > t0) t0 = snd[dv];
+          if (rcv[b] > t0) t0 = rcv[b];
+          arr[(int64_t)v * D + b] = t0 + c[v];
+          snd[dv] = rcv[b] = t0 + c[v];
+        }
+      }
+    }
+    if (finish) memcpy(finish + (int64_t)k * n, fin, sizeof(int64_t) * (size_t)n);
+    makespan[k] = span;
+  }
+  free(c); free(fin); free(avail); free(snd); free(rcv); free(arr); free(wants);
+  free(bs); free(bf); free(boff); free(nb);
+  return ORC_OK;
+}

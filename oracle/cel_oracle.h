@@ -104,6 +104,18 @@ int orc_makespan(const orc_graph *g, const orc_devices *d, const int32_t *order,
                  int32_t K, const uint8_t *node_dev, int64_t *start, int64_t *finish,
                  int64_t *makespan);
 
+/* Makespan under richer device models: model is a set of ORC_MODEL_* bits
+ * (0 gives orc_makespan's schedule).  INSERT: first-fit insertion of each
+ * node into its device's busy intervals (eq. 7's slot rule at node level).
+ * COMM_TASKS: transfers are tasks on per-device send and receive channels,
+ * one per (producer, other device holding a successor), issued in increasing
+ * device order (Section 6.1's runtime model).  `order` is any topological
+ * order; start/finish ([K][n], by node id) may be NULL. */
+enum { ORC_MODEL_INSERT = 1, ORC_MODEL_COMM_TASKS = 2 };
+int orc_makespan_model(const orc_graph *g, const orc_devices *d, const int32_t *order,
+                       int32_t K, const uint8_t *node_dev, int32_t model, int64_t *start,
+                       int64_t *finish, int64_t *makespan);
+
 #ifdef __cplusplus
 }
 #endif

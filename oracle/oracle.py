@@ -62,8 +62,10 @@ def lib():
                                     C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
         L.orc_order_place.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), _P32, C.c_int32,
                                       _PU8, _PU8, C.POINTER(C.c_int32)]
+        L.orc_makespan_model.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), _P32, C.c_int32,
+                                         _PU8, C.c_int32, _P64, _P64, _P64]
         for f in (L.orc_topo_levels, L.orc_blevel, L.orc_cluster, L.orc_place, L.orc_makespan,
-                  L.orc_cpd_topo, L.orc_comm_sums, L.orc_order_place):
+                  L.orc_cpd_topo, L.orc_comm_sums, L.orc_order_place, L.orc_makespan_model):
             f.restype = C.c_int
         _lib = L
     return _lib
@@ -209,6 +211,29 @@ def makespan(wl, order, node_dev, want_times=True):
     ms = np.zeros(K, np.int64)
     _check(lib().orc_makespan(C.byref(k.g), C.byref(k.d), _ptr(order, _P32), K, _ptr(nd, _PU8),
                               _ptr(st, _P64), _ptr(fi, _P64), _ptr(ms, _P64)), "orc_makespan")
+    if want_times:
+        st, fi = st[:, :n], fi[:, :n]
+    return ms, st, fi
+
+
+MODEL_INSERT, MODEL_COMM_TASKS = 1, 2
+
+
+def makespan_model(wl, order, node_dev, model, want_times=True):
+    """Makespan under the device models (bits MODEL_INSERT, MODEL_COMM_TASKS; 0 is
+    makespan()'s schedule) -> (makespan int64[K], start, finish) ([K, n] or None)"""
+    k = _Keep(wl)
+    n = int(wl.n)
+    nd = np.ascontiguousarray(node_dev, np.uint8)
+    K = 1 if nd.ndim == 1 else nd.shape[0]
+    nd = nd.reshape(K, n) if n > 0 else np.zeros((K, 1), np.uint8)
+    order = np.ascontiguousarray(order, np.int32)
+    st = np.zeros((K, max(n, 1)), np.int64) if want_times else None
+    fi = np.zeros((K, max(n, 1)), np.int64) if want_times else None
+    ms = np.zeros(K, np.int64)
+    _check(lib().orc_makespan_model(C.byref(k.g), C.byref(k.d), _ptr(order, _P32), K,
+                                    _ptr(nd, _PU8), int(model), _ptr(st, _P64), _ptr(fi, _P64),
+                                    _ptr(ms, _P64)), "orc_makespan_model")
     if want_times:
         st, fi = st[:, :n], fi[:, :n]
     return ms, st, fi

@@ -632,3 +632,142 @@ def test_order_place_properties():
     cid = np.arange(30, dtype=np.int32)
     cdev, _, _ = O.order_place(wl, cid, 30)
     assert not cdev.any()                                        # one device takes all
+
+
+# --------------------------------------------- makespan under device models
+
+
+def _rand_topo(wl, rng):
+    """A random topological order (Kahn with a random pick among the ready)."""
+    indeg = np.diff(np.asarray(wl.in_ptr)).astype(np.int64)
+    ready = [v for v in range(wl.n) if indeg[v] == 0]
+    out = []
+    while ready:
+        v = ready.pop(int(rng.integers(len(ready))))
+        out.append(v)
+        for e in range(wl.out_ptr[v], wl.out_ptr[v + 1]):
+            t = int(wl.out_idx[e])
+            indeg[t] -= 1
+            if indeg[t] == 0:
+                ready.append(t)
+    return np.array(out, np.int32)
+
+
+def _ready_times(wl, dev, fin, c):
+    """Contention-free ready time of every node from its predecessors' finish."""
+    rdy = np.zeros(wl.n, np.int64)
+    for u, v in zip(*wl.edges()):
+        r = fin[u] + (c[u] if dev[u] != dev[v] else 0)
+        rdy[v] = max(rdy[v], r)
+    return rdy
+
+
+def test_model_hand_fixtures():
+    for case in load("model_hand.json")["cases"]:
+        wl = from_edges(case["n"], case["edges"], case["w"], case["ob"], case["D"], case["cap"],
+                        case["bw"], case["lat"])
+        for m, e in case["models"].items():
+            ms, st, fi = O.makespan_model(wl, np.array(case["order"], np.int32),
+                                          np.array(case["dev"], np.uint8), int(m))
+            assert st[0].tolist() == e["start"], (case["name"], m)
+            assert fi[0].tolist() == e["finish"] and int(ms[0]) == e["makespan"], (case["name"], m)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_model0_is_fifo_makespan(cfg):
+    """Model 0 must give orc_makespan's schedule node by node."""
+    wl = make_config(cfg, 0)
+    lev, oid, lp, L = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    rng = np.random.default_rng(cfg)
+    P = rng.integers(0, wl.D, (3, wl.n)).astype(np.uint8)
+    a = O.makespan(wl, pr, P)
+    b = O.makespan_model(wl, pr, P, 0)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_model_insert_is_first_fit():
+    """Each node with w > 0 starts at the smallest t >= its ready time at which
+    [t, t + w) overlaps none of the intervals of the nodes placed before it (in
+    the order) on its device -- the definition of first fit, checked by brute
+    force over the candidates {ready} and those nodes' finish times.  Also: the
+    schedule respects every edge, devices never overlap, and no node starts
+    later than under FIFO devices (insertion only ever adds free slots)."""
+    rng = np.random.default_rng(31)
+    for s in range(40):
+        n = 2 + s % 23
+        wl = make_random_dag(4000 + s, n, p_edge=0.15 + 0.02 * (s % 5), D=1 + s % 4,
+                             multi=(s % 5 == 0), zero_frac=0.25 if s % 3 == 0 else 0.0)
+        order = _rand_topo(wl, rng)
+        dev = rng.integers(0, wl.D, n).astype(np.uint8)
+        _, st, fi = O.makespan_model(wl, order, dev, O.MODEL_INSERT)
+        st, fi = st[0], fi[0]
+        c = np.asarray(O.comm(wl), np.int64)
+        w = np.asarray(wl.w, np.int64)
+        assert np.array_equal(fi, st + w)
+        rdy = _ready_times(wl, dev, fi, c)
+        _, st0, _ = O.makespan(wl, order, dev)
+        assert np.all(st <= st0[0]), s
+        for i, v in enumerate(order):
+            assert st[v] >= rdy[v]
+            if w[v] == 0:
+                assert st[v] == rdy[v]
+                continue
+            before = [u for u in order[:i] if dev[u] == dev[v] and w[u] > 0]
+
+            def free(t):
+                return all(t + w[v] <= st[u] or t >= fi[u] for u in before)
+
+            cands = sorted({int(rdy[v])} | {int(fi[u]) for u in before if fi[u] >= rdy[v]})
+            first = next((t for t in cands if free(t)), None)
+            if first is None:  # after everything placed so far
+                first = max([int(rdy[v])] + [int(fi[u]) for u in before])
+            assert st[v] == first, (s, v)
+        for x in range(wl.D):
+            iv = sorted((st[v], fi[v]) for v in range(n) if dev[v] == x and w[v] > 0)
+            assert all(a[1] <= b[0] for a, b in zip(iv, iv[1:]))
+
+
+def test_model_comm_tasks_properties():
+    """Transfers as tasks: one device (no transfers) gives the model without
+    them; a chain alternating two devices has no contention (sum of w and c);
+    every node starts no earlier than with contention-free comm; per device,
+    FIFO order is kept."""
+    rng = np.random.default_rng(5)
+    for s in range(30):
+        n = 2 + s * 5
+        wl = make_random_dag(5000 + s, n, p_edge=min(0.5, 3.0 / n), D=2 + s % 5,
+                             multi=(s % 4 == 0), zero_frac=0.2 if s % 3 == 0 else 0.0)
+        order = _rand_topo(wl, rng)
+        dev = rng.integers(0, wl.D, n).astype(np.uint8)
+        _, st2, _ = O.makespan_model(wl, order, dev, O.MODEL_COMM_TASKS)
+        _, st0, _ = O.makespan_model(wl, order, dev, 0)
+        assert np.all(st2[0] >= st0[0]), s
+        pos = np.empty(n, np.int64)
+        pos[order] = np.arange(n)
+        for x in range(wl.D):
+            on = sorted((pos[v], v) for v in range(n) if dev[v] == x)
+            assert all(st2[0][a[1]] + wl.w[a[1]] <= st2[0][b[1]] for a, b in zip(on, on[1:]))
+        one = np.zeros(n, np.uint8)
+        for m in (0, 1):
+            a = O.makespan_model(wl, order, one, m)
+            b = O.makespan_model(wl, order, one, m | O.MODEL_COMM_TASKS)
+            assert all(np.array_equal(x, y) for x, y in zip(a, b))
+    n = 9
+    wl = from_edges(n, [(i, i + 1) for i in range(n - 1)], list(range(1, n + 1)), [3] * n, 2,
+                    [100, 100], 2, 1)
+    dev = np.array([i % 2 for i in range(n)], np.uint8)
+    ms, _, _ = O.makespan_model(wl, np.arange(n, dtype=np.int32), dev, O.MODEL_COMM_TASKS)
+    assert int(ms[0]) == sum(range(1, n + 1)) + (n - 1) * (2 + 1)  # c = ceil(3/2) + 1
+
+
+def test_model_rejects_bad_inputs():
+    wl = from_edges(3, [(0, 1), (1, 2)], [1, 1, 1], [0, 0, 0], 2, [5, 5], 1, 0)
+    dev = np.zeros(3, np.uint8)
+    with pytest.raises(RuntimeError):
+        O.makespan_model(wl, np.array([0, 1, 2], np.int32), dev, 4)
+    with pytest.raises(RuntimeError):
+        O.makespan_model(wl, np.array([1, 0, 2], np.int32), dev, 1)
+    with pytest.raises(RuntimeError):
+        O.makespan_model(wl, np.array([0, 1, 2], np.int32), np.array([0, 2, 0], np.uint8), 2)
