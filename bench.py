@@ -225,6 +225,37 @@ def cpd_compare(cel, torch, g, d, bl, tl, prio, lev, lp, L):
                      "coarse_makespan_ns": cms, "best_effort": be, "makespan_ns": int(ms[0].item()),
                      "order_place": {"makespan_ns": int(ms_o[0].item()), "best_effort": be_o,
                                      "ms": op_ms}}
+    return row, ndev
+
+
+MODEL_NAMES = {0: "fifo", 1: "insert", 2: "comm_tasks", 3: "insert+comm_tasks"}
+
+
+def models_row(cel, torch, g, d, prio, ndev, seed, K=64):
+    """The makespan under each device model (first-fit insertion, transfers as
+    tasks) of Adjusting Placement's placement (K = 1) and of K placements in one
+    call (that one first, the rest random), on the priority order."""
+    n, m = g.n, g.m
+    rng = np.random.default_rng([seed, 17])
+    PK = torch.from_numpy(rng.integers(0, d.D, (K, n)).astype(np.uint8)).to(ndev.device)
+    PK[0] = ndev
+    row = {}
+    for model, name in MODEL_NAMES.items():
+        r = {}
+        for k, P in ((1, ndev), (K, PK)):
+            cel.kernel_stats(reset=True)
+            cel.timing(True)
+            (ms, _, _), call_ms = _timed(torch, lambda: cel.makespan_model(g, d, prio, P, model),
+                                         reps=2)
+            cel.timing(False)
+            c_, t_ = cel.kernel_stats(reset=True).get("k_makespan_model", (1, float("nan")))
+            kms = t_ / c_
+            B = k * (29.0 * n + 21.0 * m)  # per placement: dev, w, c, ptr, fin write; per edge: idx, dev, c, fin
+            r[f"K{k}"] = {"call_ms": round(call_ms, 2), "kernel_ms": round(kms, 2),
+                          "edges_per_s": k * m / (call_ms * 1e-3),
+                          "achieved_GBs": round(B / (kms * 1e-3) / 1e9, 3),
+                          "makespan_ns": int(ms[0].item())}
+        row[name] = r
     return row
 
 
@@ -354,7 +385,9 @@ def main() -> int:
     tlevel_row = {"blevel_with_tlevel_ms": e0.elapsed_time(e1),
                   "k_tlevel_sweep_ms": ks_t.get("k_tlevel_sweep", (1, float("nan")))[1]}
 
-    cpd_row = cpd_compare(cel, torch, g, d, bl_t, tl_t, pr_t, lev, lp, L)
+    cpd_row, ndev_cpd = cpd_compare(cel, torch, g, d, bl_t, tl_t, pr_t, lev, lp, L)
+    print("[bench] device models", file=sys.stderr, flush=True)
+    model_row = models_row(cel, torch, g, d, pr_t, ndev_cpd, args.seed)
 
     batch5 = None if args.no_batch else batched_row(cel, torch, dev, args)
 
@@ -424,6 +457,7 @@ def main() -> int:
         "ns_per_level": per_level,
         "tlevel": tlevel_row,
         "cpd_topo": cpd_row,
+        "device_models": model_row,
         "batched_makespan": batched,
         "batched_scoring_200k": batch5,
         "cpu_baseline": cpu,

@@ -9,6 +9,7 @@
  *   cel_cluster      memory-capped contiguous clustering (DP)     (Section 5.1.3, eq. 4-6)
  *   cel_place        coarse graph + Adjusting Placement           (Section 5.2, eq. 7-9, Alg. 2)
  *   cel_makespan     makespan of one or K placements              (Section 5.2, eq. 7)
+ *   cel_makespan_model  makespan with insertion / transfer tasks  (Section 5.2 eq. 7, 6.1)
  *   cel_order_place  Order-Place baseline placement               (Section 5.2, 6.2.2)
  *   cel_comm_sums    the parts of the comm/compute ratio CCR      (Section 5.1.1, eq. 1)
  *
@@ -52,6 +53,12 @@ enum {
 
 /* cel_blevel flags */
 enum { CEL_COMM_OFF = 1 /* treat every c[v] as 0 (compute-only critical path) */ };
+
+/* cel_makespan_model model bits */
+enum {
+  CEL_MODEL_INSERT = 1,     /* first-fit insertion into each device's idle slots */
+  CEL_MODEL_COMM_TASKS = 2  /* transfers as tasks on per-device send/receive channels */
+};
 
 /* cel_cluster modes */
 enum { CEL_CLUSTER_DP = 0, CEL_CLUSTER_GREEDY = 1 };
@@ -192,6 +199,29 @@ int cel_makespan(const cel_graph *g, const cel_devices *d, const int32_t *order,
                  const int32_t *level, const int32_t *level_ptr, int32_t n_levels,
                  int32_t K, const uint8_t *node_dev, int64_t *start, int64_t *finish,
                  int64_t *makespan, hipStream_t stream);
+
+/* Makespan of K placements under richer device models (Section 5.2's slot
+ * rule, eq. 7, at node level; Section 6.1's transfers as tasks).  Nodes are
+ * taken in `order`; a node is ready when each input has arrived: a
+ * predecessor p on the same device at its finish, on another device at
+ * finish + c[p] or, with CEL_MODEL_COMM_TASKS, when p's transfer to this
+ * device ends.  Start: model without CEL_MODEL_INSERT, the later of ready and
+ * the end of the device's previous node (cel_makespan's FIFO schedule for
+ * model 0); with it, the earliest time >= ready at which the node fits
+ * between the nodes already placed on the device (w = 0: ready).
+ * CEL_MODEL_COMM_TASKS: after p finishes, one transfer per other device
+ * holding a successor of p, in increasing device order, each taking c[p] and
+ * holding p's device's send channel and the target's receive channel:
+ * start = max(finish of p, both channels' previous transfer end).
+ * Inputs: order [n] any topological order (permutation with pos[u] < pos[v]
+ * on every edge); K >= 1; node_dev [K][n] uint8, each < D; D <= 64; model a
+ * combination of the CEL_MODEL_* bits.
+ * Outputs: start, finish [K][n] by node id, or NULL; makespan [K] (device).
+ * Errors: CEL_E_ARG (also D > 64), CEL_E_ORDER, CEL_E_OVERFLOW, CEL_E_HIP,
+ * CEL_E_NOMEM. */
+int cel_makespan_model(const cel_graph *g, const cel_devices *d, const int32_t *order,
+                       int32_t K, const uint8_t *node_dev, int32_t model, int64_t *start,
+                       int64_t *finish, int64_t *makespan, hipStream_t stream);
 
 /* Diagnostics: per-kernel device time.  After cel_timing(1), every call
  * records a pair of HIP events on its stream around each of its main kernel

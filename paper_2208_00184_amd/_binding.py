@@ -21,7 +21,7 @@ COMM_OFF = 1
 CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
 EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_cluster", "cel_place", "cel_makespan",
-           "cel_order_place", "cel_comm_sums", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
+           "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
 class CelError(RuntimeError):
@@ -63,8 +63,10 @@ def lib() -> C.CDLL:
         L.cel_cpd_order.argtypes = [G, vp, vp, vp, vp]
         L.cel_order_place.argtypes = [G, Dv, vp, i32, vp, vp, C.POINTER(i32), vp]
         L.cel_comm_sums.argtypes = [G, Dv, vp, C.POINTER(i64), C.POINTER(i64), vp]
+        L.cel_makespan_model.argtypes = [G, Dv, vp, i32, vp, i32, vp, vp, vp, vp]
         for f in ("cel_topo_levels", "cel_blevel", "cel_cluster", "cel_place", "cel_makespan",
-                  "cel_cpd_order", "cel_order_place", "cel_comm_sums", "cel_version"):
+                  "cel_cpd_order", "cel_order_place", "cel_comm_sums", "cel_makespan_model",
+                  "cel_version"):
             getattr(L, f).restype = C.c_int
         L.cel_last_error.argtypes = []
         L.cel_last_error.restype = C.c_char_p
@@ -239,6 +241,26 @@ def order_place(g: Graph, d: Devices, cluster_id, n_clusters):
     _check(lib().cel_order_place(C.byref(gc), C.byref(dc), _p(cluster_id), int(n_clusters), _p(cdev),
                                  _p(ndev), C.byref(be), _stream()))
     return cdev[:n_clusters], ndev[:n], be.value
+
+
+MODEL_INSERT, MODEL_COMM_TASKS = 1, 2
+
+
+def makespan_model(g: Graph, d: Devices, order, node_dev, model, want_times=False):
+    """Makespan under the device models (MODEL_* bits; 0 = FIFO devices, contention-free
+    comm). node_dev uint8 [n] or [K, n] -> (makespan int64[K], start, finish) ([K, n] or None)"""
+    n = g.n
+    nd = node_dev.contiguous()
+    K = 1 if nd.dim() == 1 else nd.shape[0]
+    ms = torch.empty(K, dtype=torch.int64, device=g.device)
+    st = torch.empty((K, max(n, 1)), dtype=torch.int64, device=g.device) if want_times else None
+    fi = torch.empty((K, max(n, 1)), dtype=torch.int64, device=g.device) if want_times else None
+    gc, dc = g._c(), d._c()
+    _check(lib().cel_makespan_model(C.byref(gc), C.byref(dc), _p(order), int(K), _p(nd), int(model),
+                                    _p(st), _p(fi), _p(ms), _stream()))
+    if want_times:
+        st, fi = st[:, :n], fi[:, :n]
+    return ms, st, fi
 
 
 def comm_sums(g: Graph, d: Devices, cluster_id=None):

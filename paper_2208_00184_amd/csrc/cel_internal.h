@@ -369,6 +369,19 @@ int relabel_csr(int32_t n, int32_t m, const int32_t *order, const int32_t *pos,
 int segmented_sort(uint64_t *keys, uint32_t *ids, const int32_t *seg, int32_t nseg, int64_t n,
                    Scratch &sc, hipStream_t s, const Status *st);
 
+// Makespan helpers (makespan.hip), shared with the device-model variant.
+// devp[k][p] = node_dev[k][order[p]] (EB_ARG when >= D); wp/cq = w and c by
+// position; k_makespan_out scatters finish (and start = finish - w) by
+// position back to node ids; k_fill_i64 sets n values.
+__global__ void k_dev_gather(int32_t K, int32_t n, const int32_t *order, const uint8_t *node_dev,
+                             int32_t D, uint8_t *devp, Status *st);
+__global__ void k_pos_costs(int32_t n, const int32_t *order, const int64_t *w, const int64_t *ob,
+                            int64_t bw, int64_t lat, int64_t *wp, int64_t *cq, const Status *st);
+__global__ void k_makespan_out(int32_t K, int32_t n, const int32_t *order, const int64_t *finp,
+                               const int64_t *wp, int64_t *start, int64_t *finish,
+                               const Status *st);
+__global__ void k_fill_i64(int64_t *p, int64_t n, int64_t v);
+
 // Copies the status block to the host (synchronising the stream).
 int read_status(const Status *dst, Status *host, hipStream_t s);
 

@@ -1,0 +1,502 @@
+// cel_makespan_model: makespan of K placements under richer device models.
+// INSERT applies the slot rule of eq. 7 (Section 5.2) to single nodes: a node
+// starts in the first idle slot of its device, at or after its ready time,
+// that holds it.  COMM_TASKS makes every transfer a task (the runtime model of
+// Section 6.1): one transfer of a producer's output to each other device that
+// holds one of its successors, in increasing device order, occupying the
+// producer device's send channel and the target device's receive channel.
+//
+// Under either model a node's start depends on everything placed before it in
+// the order, so a placement is a sequential walk.  One wave walks one
+// placement, 64 consecutive positions (a window) at a time:
+//  A. lane j folds slot j's inputs from before the window (finish times, or
+//     arrivals of transfers: final by now) into a partial ready time, marks
+//     its in-window predecessors in a 64-bit mask, and loads its own w, c,
+//     device and destination-device mask.  Rows with many inputs are folded
+//     by the whole wave.
+//  B. the wave steps through the slots with uniform control flow: a slot's
+//     values and its in-window inputs come from other lanes by readlane;
+//     device d's state (free time or end of its last task, idle-gap count,
+//     channel free times) lives in lane d.  Only the gap search and the
+//     transfer arrivals touch memory.
+//  C. the window's finish times are stored.
+//
+// Idle gaps: device d keeps the idle intervals before its last task, sorted,
+// in its own segment of a per-placement array (a task adds at most one gap,
+// so the segment holds as many entries as d has nodes).  A node ready at or
+// after the last gap's end goes after the device's last task with no search;
+// otherwise the wave loads 64 gaps at a time, walking back from the end to the
+// first gap that ends after the ready time, and takes the first gap from
+// there that holds the node (ballot), then shrinks, splits or empties it.
+// Transfers: a producer's destination devices form a mask; its arrivals sit
+// in a pool at off[p] + (rank of the device in the mask).
+#include "cel_internal.h"
+
+namespace cel {
+
+constexpr int kMmLight = 16;  // rows with more inputs are folded by the whole wave
+
+struct MmArgs {
+  int32_t n, D;
+  const int32_t *iptr, *iidx;  // predecessors in position space
+  const int64_t *wp, *cq;      // w, c by position
+  const uint8_t *devp;         // [K][n] device by position
+  const uint64_t *dmask;       // [K][n] destination devices by position (transfers)
+  const int64_t *aoff;         // [K][n] arrival pool offsets (transfers)
+  int64_t *pool;               // arrivals (transfers)
+  const int64_t *goff;         // [K][D] start of each device's gap segment (insertion)
+  int64_t *ga, *gb;            // gap starts and ends (insertion)
+  int64_t *finp;               // [K][n] finish by position
+  int64_t *makespan;           // [K]
+};
+
+// Lane l of a register replaced by v (uniform l and v): a lane compare and a
+// select, no memory.
+template <class T>
+__device__ inline T setlane(T old, T v, int l) {
+  return (int)threadIdx.x == l ? v : old;
+}
+
+__device__ inline uint64_t below(int b) { return (uint64_t(1) << b) - 1; }
+
+// Ready-time contribution of the inputs iidx[e] for e = e0, e0 + step, ...
+// < e1 of a node on device dv: inputs before the window (position < P0) are
+// folded into ext, the others marked in msk (bit = position - P0).  An input
+// on another device contributes f + c (contention-free) or, with transfers,
+// the arrival of its output on dv: pool[off + rank of dv in its mask].
+template <bool TASKS>
+__device__ inline void fold_inputs(const MmArgs &a, const uint8_t *dev, const int64_t *fin,
+                                   const uint64_t *dm, const int64_t *of, int32_t P0, int32_t e0,
+                                   int32_t e1, int32_t step, int32_t dv, int64_t &ext,
+                                   uint64_t &msk, uint32_t &bad) {
+  for (int32_t e = e0; e < e1; e += 4 * step) {
+    int32_t q[4];
+#pragma unroll
+    for (int u = 0; u < 4; u++) q[u] = e + u * step < e1 ? a.iidx[e + u * step] : -1;
+    int64_t f[4], x[4];
+    int32_t dq[4];
+#pragma unroll
+    for (int u = 0; u < 4; u++) {  // first round: all loads that need only q
+      dq[u] = dv;
+      f[u] = x[u] = 0;
+      if (q[u] >= 0 && q[u] < P0) {
+        dq[u] = dev[q[u]];
+        f[u] = fin[q[u]];
+        if (TASKS) {  // -1: dv missing from the mask (CSR and CSC disagree)
+          const uint64_t mq = dm[q[u]];
+          x[u] = (mq >> dv) & 1 ? of[q[u]] + __builtin_popcountll(mq & below(dv)) : -1;
+        } else {
+          x[u] = a.cq[q[u]];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; u++) {  // second round: arrivals of transfers
+      if (q[u] < 0) continue;
+      if (q[u] >= P0) {
+        msk |= uint64_t(1) << (q[u] - P0);
+        continue;
+      }
+      int64_t t;
+      if (dq[u] == dv) {
+        t = f[u];
+      } else if (TASKS) {
+        if (x[u] < 0) {
+          bad |= EB_ARG;
+          continue;
+        }
+        t = a.pool[x[u]];
+      } else {
+        t = f[u] + x[u];
+      }
+      ext = t > ext ? t : ext;
+    }
+  }
+}
+
+// First-fit slot of a node (w > 0, ready r) on device dj, whose gap segment
+// starts at A / B; L, G, gl are the device's last end, gap count and last
+// gap end (uniform), updated in place.  Returns the start.
+__device__ inline int64_t insert_slot(int64_t *A, int64_t *B, int64_t r, int64_t w, int64_t &L,
+                                      int32_t &G, int64_t &gl, int lane) {
+  if (G == 0 || r >= gl) {  // no idle gap ends after r: go after the last task
+    const int64_t s = r > L ? r : L;
+    if (s > L) {
+      if (lane == 0) {
+        A[G] = L;
+        B[G] = s;
+      }
+      G++;
+      gl = s;
+    }
+    L = s + w;
+    return s;
+  }
+  // gaps stored by earlier steps must be visible to this wave's loads
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  // walk back to the chunk holding the first gap that ends after r
+  int32_t lo = G > 64 ? G - 64 : 0;
+  int64_t ca, cb;
+  for (;;) {
+    const int32_t i = lo + lane;
+    ca = cb = 0;
+    if (i < G) {
+      ca = A[i];
+      cb = B[i];
+    }
+    if (lo == 0 || !(__builtin_amdgcn_readfirstlane((int32_t)(cb > r)))) break;
+    lo = lo > 64 ? lo - 64 : 0;
+  }
+  // scan forward from there for the first gap that holds [max(start, r), + w)
+  int32_t q = -1;
+  int64_t qa = 0, qb = 0;
+  for (;;) {
+    const int32_t i = lo + lane;
+    const int64_t t = ca > r ? ca : r;
+    const uint64_t fit = __ballot(i < G && cb > r && t + w <= cb);
+    if (fit) {
+      const int l = __builtin_ctzll(fit);
+      q = lo + l;
+      qa = readlane64(ca, l);
+      qb = readlane64(cb, l);
+      break;
+    }
+    lo += 64;
+    if (lo >= G) break;
+    ca = cb = 0;
+    if (lo + lane < G) {
+      ca = A[lo + lane];
+      cb = B[lo + lane];
+    }
+  }
+  if (q < 0) {  // none holds it: after the last task (r < gl <= L)
+    const int64_t s = L;
+    L = s + w;
+    return s;
+  }
+  const int64_t s = qa > r ? qa : r, e = s + w;
+  const bool left = s > qa, right = e < qb;
+  if (left && right) {  // split: move gaps q+1 .. G-1 up by one, top chunk first
+    for (int32_t hi = G; hi > q + 1;) {
+      const int32_t l0 = hi - 64 > q + 1 ? hi - 64 : q + 1;
+      const int32_t i = l0 + lane;
+      int64_t xa = 0, xb = 0;
+      if (i < hi) {
+        xa = A[i];
+        xb = B[i];
+      }
+      if (i < hi) {
+        A[i + 1] = xa;
+        B[i + 1] = xb;
+      }
+      hi = l0;
+    }
+    if (lane == 0) {
+      B[q] = s;
+      A[q + 1] = e;
+      B[q + 1] = qb;
+    }
+    G++;
+  } else if (left) {  // the node ends the gap
+    if (lane == 0) B[q] = s;
+    if (q == G - 1) gl = s;
+  } else if (right) {  // the node starts the gap
+    if (lane == 0) A[q] = e;
+  } else {  // filled exactly: leave an empty gap [qb, qb)
+    if (lane == 0) A[q] = qb;
+  }
+  return s;
+}
+
+template <bool INS, bool TASKS>
+__global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
+  __shared__ int64_t s_T[TASKS ? 64 * 64 : 1];  // arrival of slot j's output on device b
+  if (failed(st)) return;
+  const int lane = threadIdx.x;
+  const int64_t k = blockIdx.x;
+  const int32_t n = a.n;
+  const uint8_t *dev = a.devp + k * n;
+  int64_t *fin = a.finp + k * n;
+  const uint64_t *dm = TASKS ? a.dmask + k * n : nullptr;
+  const int64_t *of = TASKS ? a.aoff + k * n : nullptr;
+  // device `lane`'s state
+  int64_t last = 0;   // free time (FIFO) or end of the last task (insertion)
+  int32_t gcnt = 0;   // idle gaps stored
+  int64_t glast = 0;  // end of the last stored gap
+  int64_t gbase = INS && lane < a.D ? a.goff[k * a.D + lane] : 0;
+  int64_t snd = 0, rcv = 0, tcur = 0;
+  int64_t span = 0;
+  uint32_t bad = 0;
+  for (int32_t P0 = 0; P0 < n; P0 += 64) {
+    const int32_t nw = n - P0 < 64 ? n - P0 : 64;
+    const int32_t p = P0 + lane;
+    const bool act = lane < nw;
+    int32_t dv = 0, i0 = 0, i1 = 0;
+    int64_t w = 0, c = 0, ext = 0, myoff = 0;
+    uint64_t msk = 0, mydm = 0;
+    if (act) {
+      dv = dev[p];
+      w = a.wp[p];
+      c = a.cq[p];
+      i0 = a.iptr[p];
+      i1 = a.iptr[p + 1];
+      if (TASKS) {
+        mydm = dm[p];
+        myoff = of[p];
+      }
+    }
+    // A: inputs from before the window
+    const bool heavy = i1 - i0 > kMmLight;
+    if (!heavy) fold_inputs<TASKS>(a, dev, fin, dm, of, P0, i0, i1, 1, dv, ext, msk, bad);
+    for (uint64_t hv = __ballot(heavy); hv; hv &= hv - 1) {
+      const int h = __builtin_ctzll(hv);
+      const int32_t e0 = __builtin_amdgcn_readlane(i0, h), e1 = __builtin_amdgcn_readlane(i1, h);
+      const int32_t dh = __builtin_amdgcn_readlane(dv, h);
+      int64_t mx = 0;
+      uint64_t mk = 0;
+      fold_inputs<TASKS>(a, dev, fin, dm, of, P0, e0 + lane, e1, 64, dh, mx, mk, bad);
+      for (int off = 32; off > 0; off >>= 1) {
+        const int64_t o = __shfl_xor(mx, off);
+        mx = o > mx ? o : mx;
+        mk |= __shfl_xor(mk, off);
+      }
+      if (lane == h) {
+        ext = mx;
+        msk = mk;
+      }
+    }
+    // B: the slots in order
+    int64_t finw = 0;
+    for (int j = 0; j < nw; j++) {
+      const int32_t dj = __builtin_amdgcn_readlane(dv, j);
+      const int64_t wj = readlane64(w, j);
+      int64_t r = readlane64(ext, j);
+      for (uint64_t mj = (uint64_t)readlane64((int64_t)msk, j); mj; mj &= mj - 1) {
+        const int q = __builtin_ctzll(mj);
+        const int32_t dq = __builtin_amdgcn_readlane(dv, q);
+        const int64_t fq = readlane64(finw, q);
+        int64_t t;
+        if (dq == dj) t = fq;
+        else if (TASKS) t = s_T[q * 64 + dj];
+        else t = fq + readlane64(c, q);
+        r = t > r ? t : r;
+      }
+      int64_t s;
+      if (!INS) {
+        const int64_t L = readlane64(last, dj);
+        s = r > L ? r : L;
+        last = setlane<int64_t>(last, s + wj, dj);
+      } else if (wj == 0) {
+        s = r;
+      } else {
+        int64_t L = readlane64(last, dj), gl = readlane64(glast, dj);
+        int32_t G = __builtin_amdgcn_readlane(gcnt, dj);
+        const int64_t base = readlane64(gbase, dj);
+        s = insert_slot(a.ga + base, a.gb + base, r, wj, L, G, gl, lane);
+        last = setlane<int64_t>(last, L, dj);
+        glast = setlane<int64_t>(glast, gl, dj);
+        gcnt = setlane<int32_t>(gcnt, G, dj);
+      }
+      const int64_t f = s + wj;
+      finw = setlane<int64_t>(finw, f, j);
+      span = f > span ? f : span;
+      if (TASKS) {
+        const uint64_t dmj = (uint64_t)readlane64((int64_t)mydm, j);
+        if (dmj) {
+          const int64_t cj = readlane64(c, j);
+          int64_t sf = readlane64(snd, dj);
+          for (uint64_t x = dmj; x; x &= x - 1) {
+            const int b = __builtin_ctzll(x);
+            const int64_t rb = readlane64(rcv, b);
+            int64_t t0 = f > sf ? f : sf;
+            t0 = rb > t0 ? rb : t0;
+            sf = t0 + cj;
+            rcv = setlane<int64_t>(rcv, sf, b);
+            tcur = setlane<int64_t>(tcur, sf, b);
+          }
+          snd = setlane<int64_t>(snd, sf, dj);
+          if ((dmj >> lane) & 1) {
+            s_T[j * 64 + lane] = tcur;
+            a.pool[readlane64(myoff, j) + __builtin_popcountll(dmj & below(lane))] = tcur;
+          }
+          lds_order();
+        }
+      }
+    }
+    // C: finish times of the window
+    if (act) fin[p] = finw;
+    // the next window reads these finish times and arrivals
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  }
+  if (lane == 0) a.makespan[k] = span;
+  if (bad) raise_err(st, bad);
+}
+
+// Per placement, nodes per device (gap segment sizes); blocks take chunks of
+// positions and add an LDS histogram into cnt[k][D].
+__global__ void k_mm_devcount(int32_t K, int32_t n, int32_t D, const uint8_t *devp, int32_t *cnt,
+                              const Status *st) {
+  __shared__ int32_t h[64];
+  if (failed(st)) return;
+  for (int64_t k = blockIdx.y; k < K; k += gridDim.y) {
+    if (threadIdx.x < 64) h[threadIdx.x] = 0;
+    __syncthreads();
+    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+         p += (int64_t)gridDim.x * blockDim.x)
+      atomicAdd(&h[devp[k * n + p]], 1);
+    __syncthreads();
+    if (threadIdx.x < D && h[threadIdx.x]) atomicAdd(&cnt[k * D + threadIdx.x], h[threadIdx.x]);
+    __syncthreads();
+  }
+}
+
+// goff[k][d] = k * n + nodes of placement k on devices below d.
+__global__ void k_mm_goff(int32_t K, int32_t n, int32_t D, const int32_t *cnt, int64_t *goff,
+                          const Status *st) {
+  if (failed(st)) return;
+  for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < K;
+       k += (int64_t)gridDim.x * blockDim.x) {
+    int64_t acc = k * n;
+    for (int32_t d = 0; d < D; d++) {
+      goff[k * D + d] = acc;
+      acc += cnt[k * D + d];
+    }
+  }
+}
+
+// Destination devices of every producer: for each edge u -> v and placement
+// k with v on another device, set that device's bit in u's mask (by u's
+// position); reading first keeps heavy rows from hammering one word.
+__global__ void k_mm_dmask(cel_graph g, int32_t K, const int32_t *pos, const uint8_t *node_dev,
+                           unsigned long long *dmask, const Status *st) {
+  __shared__ int32_t ptr[kRowsPB + 1], su[2];
+  if (failed(st)) return;
+  const int64_t n = g.n;
+  for_edges_balanced(g.out_ptr, g.n, g.m, ptr, su, [&](int32_t u, int32_t e) {
+    const int32_t v = g.out_idx[e];
+    const int64_t pu = pos[u];
+    for (int64_t k = blockIdx.y; k < K; k += gridDim.y) {
+      const int du = node_dev[k * n + u], dv = node_dev[k * n + v];
+      if (du == dv) continue;
+      const unsigned long long bit = 1ull << dv;
+      unsigned long long *x = &dmask[k * n + pu];
+      if (!(__atomic_load_n(x, __ATOMIC_RELAXED) & bit)) atomicOr(x, bit);
+    }
+  });
+}
+
+__global__ void k_mm_popc(int64_t N, const uint64_t *dmask, int64_t *cntv, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < N;
+       i += (int64_t)gridDim.x * blockDim.x)
+    cntv[i] = __builtin_popcountll(dmask[i]);
+}
+
+}  // namespace cel
+
+using namespace cel;
+
+extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, const int32_t *order,
+                                  int32_t K, const uint8_t *node_dev, int32_t model,
+                                  int64_t *start, int64_t *finish, int64_t *makespan,
+                                  hipStream_t s) {
+  const char *fn = "cel_makespan_model";
+  CEL_TRY(check_host_graph(g, fn));
+  CEL_TRY(check_host_devices(d, fn));
+  const int32_t n = g->n, D = d->D;
+  if (!makespan || K < 1 || (n > 0 && (!order || !node_dev)))
+    return set_error(CEL_E_ARG, "%s: NULL argument or K < 1", fn);
+  if (model & ~(CEL_MODEL_INSERT | CEL_MODEL_COMM_TASKS))
+    return set_error(CEL_E_ARG, "%s: unknown model bits 0x%x", fn, model);
+  if (D > 64) return set_error(CEL_E_ARG, "%s: D = %d above 64", fn, D);
+  const bool ins = model & CEL_MODEL_INSERT, tasks = model & CEL_MODEL_COMM_TASKS;
+  Scratch sc(s);
+  Status *st;
+  CEL_TRY(sc.get(&st, 1));
+  CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
+  if (n == 0) {
+    k_fill_i64<<<grid_for(K, 256, 1024), 256, 0, s>>>(makespan, K, 0);
+    CEL_HIP(hipGetLastError());
+    CEL_HIP(hipStreamSynchronize(s));
+    return CEL_OK;
+  }
+  int32_t *tmp, *pos, *iptr, *iidx;
+  int64_t *wp, *cq, *finp;
+  uint8_t *devp;
+  CEL_TRY(sc.get(&tmp, n));
+  CEL_TRY(sc.get(&pos, n));
+  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, sc, s));
+  CEL_TRY(check_topo_order(g, order, pos, st, s));
+  const int64_t Kn = (int64_t)K * n;
+  CEL_TRY(sc.get(&iptr, (int64_t)n + 1));
+  CEL_TRY(sc.get(&iidx, g->m));
+  CEL_TRY(sc.get(&wp, n));
+  CEL_TRY(sc.get(&cq, n));
+  CEL_TRY(sc.get(&devp, Kn));
+  CEL_TRY(sc.get(&finp, Kn));
+  CEL_TRY(relabel_csr(n, g->m, order, pos, g->in_ptr, g->in_idx, iptr, iidx, sc, s, st));
+  k_pos_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, g->w, g->ob, d->bw, d->lat, wp, cq,
+                                                    st);
+  const int gx = grid_for(n, 256, 1024), gy = K < 1024 ? K : 1024;
+  k_dev_gather<<<dim3(gx, gy), 256, 0, s>>>(K, n, order, node_dev, D, devp, st);
+  MmArgs a{};
+  a.n = n;
+  a.D = D;
+  a.iptr = iptr;
+  a.iidx = iidx;
+  a.wp = wp;
+  a.cq = cq;
+  a.devp = devp;
+  a.finp = finp;
+  a.makespan = makespan;
+  if (ins) {
+    int32_t *cnt;
+    int64_t *goff, *ga, *gb;
+    CEL_TRY(sc.get(&cnt, (int64_t)K * D));
+    CEL_TRY(sc.get(&goff, (int64_t)K * D));
+    CEL_TRY(sc.get(&ga, Kn));
+    CEL_TRY(sc.get(&gb, Kn));
+    CEL_HIP(hipMemsetAsync(cnt, 0, sizeof(int32_t) * K * D, s));
+    k_mm_devcount<<<dim3(grid_for(n, 256, 64), gy), 256, 0, s>>>(K, n, D, devp, cnt, st);
+    k_mm_goff<<<grid_for(K, 256, 1024), 256, 0, s>>>(K, n, D, cnt, goff, st);
+    a.goff = goff;
+    a.ga = ga;
+    a.gb = gb;
+  }
+  if (tasks) {
+    uint64_t *dmask;
+    int64_t *pc, *aoff, *pool;
+    CEL_TRY(sc.get(&dmask, Kn));
+    CEL_TRY(sc.get(&pc, Kn));
+    CEL_TRY(sc.get(&aoff, Kn + 1));
+    CEL_HIP(hipMemsetAsync(dmask, 0, sizeof(uint64_t) * Kn, s));
+    k_mm_dmask<<<dim3(edge_blocks(g->m), gy), 256, 0, s>>>(*g, K, pos, node_dev,
+                                                           (unsigned long long *)dmask, st);
+    k_mm_popc<<<grid_for(Kn, 256, 8192), 256, 0, s>>>(Kn, dmask, pc, st);
+    CEL_TRY(exclusive_scan_i64(pc, aoff, Kn, sc, s));
+    int64_t total = 0;  // transfers of all placements (valid once the checks passed)
+    CEL_HIP(hipMemcpyAsync(&total, aoff + Kn, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    Status h0;
+    CEL_TRY(read_status(st, &h0, s));
+    if (h0.err) return status_error(h0, fn);
+    CEL_TRY(sc.get(&pool, total > 0 ? total : 1));
+    a.dmask = dmask;
+    a.aoff = aoff;
+    a.pool = pool;
+  }
+  {
+    KTimer kt(s, "k_makespan_model");
+    if (!ins && !tasks) k_makespan_model<false, false><<<(unsigned)K, 64, 0, s>>>(a, st);
+    else if (ins && !tasks) k_makespan_model<true, false><<<(unsigned)K, 64, 0, s>>>(a, st);
+    else if (!ins) k_makespan_model<false, true><<<(unsigned)K, 64, 0, s>>>(a, st);
+    else k_makespan_model<true, true><<<(unsigned)K, 64, 0, s>>>(a, st);
+  }
+  if (start || finish)
+    k_makespan_out<<<grid_for(Kn, 256, 8192), 256, 0, s>>>(K, n, order, finp, wp, start, finish,
+                                                          st);
+  CEL_HIP(hipGetLastError());
+  Status h;
+  CEL_TRY(read_status(st, &h, s));
+  if (h.err) return status_error(h, fn);
+  return CEL_OK;
+}

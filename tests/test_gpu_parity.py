@@ -773,3 +773,148 @@ def test_order_place_and_ccr_transformer96():
     assert check_comm_sums(wl, cid)[0] == cut
     check_comm_sums(wl)
     check_order_place(wl, cid, C)
+
+
+# ------------------------------------ makespan under device models (insertion, transfers)
+
+MODELS = (0, cel.MODEL_INSERT, cel.MODEL_COMM_TASKS, cel.MODEL_INSERT | cel.MODEL_COMM_TASKS)
+
+
+def check_model(wl, order, P, models=MODELS):
+    g, d = up(wl)
+    o = tt(order, np.int32)
+    Pt = tt(P, np.uint8)
+    for m in models:
+        ref = O.makespan_model(wl, order, P, m)
+        print(f"[model] n={wl.n} D={wl.D} K={1 if P.ndim == 1 else P.shape[0]} model={m}", flush=True)
+        ms, st, fi = cel.makespan_model(g, d, o, Pt, m, want_times=True)
+        assert np.array_equal(np_(ms), ref[0]), m
+        assert np.array_equal(np_(fi), ref[2]), m
+        assert np.array_equal(np_(st), ref[1]), m
+
+
+def test_model_hand_fixtures():
+    import json
+    import os
+    gold = os.path.join(os.path.dirname(__file__), "golden", "model_hand.json")
+    for case in json.load(open(gold))["cases"]:
+        wl = from_edges(case["n"], case["edges"], case["w"], case["ob"], case["D"], case["cap"],
+                        case["bw"], case["lat"])
+        g, d = up(wl)
+        for m, e in case["models"].items():
+            ms, st, fi = cel.makespan_model(g, d, tt(case["order"], np.int32),
+                                            tt(case["dev"], np.uint8), int(m), want_times=True)
+            assert np_(st)[0].tolist() == e["start"], (case["name"], m)
+            assert np_(fi)[0].tolist() == e["finish"] and int(np_(ms)[0]) == e["makespan"]
+
+
+@pytest.mark.parametrize("cfg,seed", [(1, 0), (2, 0), (3, 0), (5, 0)])
+def test_model_configs(cfg, seed):
+    """Priority and CPD-TOPO orders; random placements and Adjusting Placement's."""
+    wl, rt, rb = config(cfg, seed)
+    P = random_placements(wl, 2, 9 + cfg)
+    cid, C, _ = O.cluster(wl, rb[2], 200, -1)
+    P = np.concatenate([O.place(wl, cid, C)[1][None, :], P])
+    check_model(wl, rb[2], P)
+    check_model(wl, oracle_cpd(wl), P[:1])
+    # model 0 is cel_makespan's schedule
+    g, d = up(wl)
+    ms0, _, _ = cel.makespan_model(g, d, tt(rb[2], np.int32), tt(P, np.uint8), 0)
+    ms1, _, _ = cel.makespan(g, d, tt(rb[2], np.int32), tt(rt[0], np.int32), tt(rt[2], np.int32),
+                             rt[3], tt(P, np.uint8))
+    assert np.array_equal(np_(ms0), np_(ms1))
+
+
+def test_model_random_dags():
+    """Random topological orders (not level-monotone), multi-edges, zero w,
+    1..64 devices, rows of many inputs (folded by the whole wave)."""
+    rng = np.random.default_rng(12)
+    for s in range(16):
+        n = 5 + (s * 131) % 1500
+        D = [1, 2, 3, 5, 8, 17, 64, 40][s % 8]
+        wl = make_random_dag(7000 + s, n, p_edge=min(0.6, (2.0 + 30.0 * (s % 3 == 0)) / n), D=D,
+                             multi=(s % 3 == 0), zero_frac=0.25 if s % 4 == 0 else 0.0)
+        order = random_topo_order(wl, rng)
+        P = rng.integers(0, D, (2, n)).astype(np.uint8)
+        check_model(wl, order, P)
+
+
+def test_model_heavy_rows():
+    """Rows with more inputs than one lane folds (16): a sink fed by every node,
+    a node fed by the 100 positions just before it (inputs inside and before
+    its window), and a source feeding everything (transfers to every device)."""
+    rng = np.random.default_rng(21)
+    n = 3000
+    edges = [(0, v) for v in range(1, n)]
+    edges += [(u, n - 1) for u in range(1, n - 1)]
+    edges += [(u, 1530) for u in range(1430, 1530)]
+    wl = from_edges(n, edges, rng.integers(0, 50, n), rng.integers(0, 200, n), 7,
+                    [10 ** 9] * 7, 3, 2)
+    order = np.arange(n, dtype=np.int32)
+    check_model(wl, order, rng.integers(0, 7, (2, n)).astype(np.uint8))
+
+
+def test_model_many_gaps():
+    """Hundreds of idle gaps on one device, filled late: chunked walk back over
+    the gap list, splits that shift the gaps above, exact fills."""
+    rng = np.random.default_rng(3)
+    A, edges, w, ob, dev = 300, [], [], [], []
+    for i in range(A):  # a_i (dev0, w 10) -> b_i (dev1, w 1), c = 5
+        edges.append((2 * i, 2 * i + 1))
+        if i:
+            edges.append((2 * i - 2, 2 * i))
+        w += [10, 1]
+        ob += [5, 0]
+        dev += [0, 1]
+    base = 2 * A
+    late = 400
+    for j in range(late):  # late nodes on dev1: no inputs, or an input from some a_i
+        w.append(int(rng.integers(1, 9)))
+        ob.append(0)
+        dev.append(1)
+        if j % 3 == 0:
+            edges.append((2 * int(rng.integers(0, A)), base + j))
+    n = base + late
+    wl = from_edges(n, edges, w, ob, 2, [10 ** 9, 10 ** 9], 1, 0)
+    order = np.arange(n, dtype=np.int32)
+    check_model(wl, order, np.array(dev, np.uint8))
+
+
+def test_model_edge_cases_and_errors():
+    wl = from_edges(0, [], [], [], 2, [5, 5], 3, 1)
+    g, d = up(wl)
+    z = torch.zeros((3, 0), dtype=torch.uint8, device=DEV)
+    ms, _, _ = cel.makespan_model(g, d, torch.zeros(0, dtype=torch.int32, device=DEV), z, 3)
+    assert np_(ms).tolist() == [0, 0, 0]
+    wl = from_edges(1, [], [7], [100], 3, [5, 5, 5], 3, 1)
+    check_model(wl, np.array([0], np.int32), np.array([2], np.uint8))
+    wl = from_edges(3, [(0, 1), (1, 2)], [1, 2, 3], [4, 5, 6], 2, [10, 10], 2, 1)
+    g, d = up(wl)
+    o = tt([0, 1, 2], np.int32)
+    with pytest.raises(cel.CelError) as ei:  # unknown model bit
+        cel.makespan_model(g, d, o, tt([0, 1, 0], np.uint8), 4)
+    assert ei.value.code == -1
+    with pytest.raises(cel.CelError) as ei:  # device out of range
+        cel.makespan_model(g, d, o, tt([0, 2, 0], np.uint8), 2)
+    assert ei.value.code == -1
+    with pytest.raises(cel.CelError) as ei:  # not topological
+        cel.makespan_model(g, d, tt([1, 0, 2], np.int32), tt([0, 1, 0], np.uint8), 1)
+    assert ei.value.code == -6
+    wl = make_random_dag(3, 50, p_edge=0.1, D=65)
+    g, d = up(wl)
+    with pytest.raises(cel.CelError) as ei:  # more than 64 devices
+        cel.makespan_model(g, d, tt(O.topo_levels(wl)[1], np.int32),
+                           torch.zeros(50, dtype=torch.uint8, device=DEV), 1)
+    assert ei.value.code == -1
+
+
+def test_model_transformer96():
+    """Full size (1.07M nodes): every model on Adjusting Placement's placement
+    of the CPD-TOPO clustering and on a random placement."""
+    wl = make_config(4, 0)
+    ocpd = oracle_cpd(wl)
+    cid, C, _ = O.cluster(wl, ocpd, 200, -1)
+    P = np.stack([O.place(wl, cid, C)[1], random_placements(wl, 1, 5)[0]])
+    lev, oid, lp, L = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    check_model(wl, pr, P)
