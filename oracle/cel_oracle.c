@@ -714,13 +714,74 @@ int orc_makespan(const orc_graph *g, const orc_devices *d, const int32_t *order,
  *   A successor on b is ready for u's output when that transfer ends; outputs
  *   consumed on their own device need no transfer.  Compute never waits for a
  *   channel other than through its inputs. */
-int orc_makespan_model(const orc_graph *g, const orc_devices *d, const int32_t *order,
-                       int32_t K, const uint8_t *node_dev, int32_t model, int64_t *start,
-                       int64_t *finish, int64_t *makespan) {
+/* Heterogeneous devices: node v takes ceil(w[v] * tmul[x] / 1024) on device x,
+ * and its output takes ceil(ob[v] / bw[a][b]) + lat[a][b] from device a to b.
+ * h == NULL, or a NULL member, means the homogeneous value (1024, d->bw,
+ * d->lat). */
+static int64_t dur_on(const orc_hetero *h, int64_t w, int32_t x) {
+  if (!h || !h->tmul) return w;
+  __int128 t = (__int128)w * h->tmul[x];
+  return (int64_t)((t + 1023) / 1024);
+}
+
+static int64_t link_comm(const orc_hetero *h, const orc_devices *d, int64_t ob, int32_t a,
+                         int32_t b) {
+  int64_t bw = h && h->bw ? h->bw[a * d->D + b] : d->bw;
+  int64_t lat = h && h->lat ? h->lat[a * d->D + b] : d->lat;
+  return comm_of(ob, bw, lat);
+}
+
+/* The overflow bound with the slowest device and the worst link. */
+static int check_hetero(const orc_graph *g, const orc_devices *d, const orc_hetero *h) {
+  if (!h) return check_overflow(g, d);
+  int32_t D = d->D;
+  int64_t tmax = 1024, bwmin = d->bw, latmax = d->lat;
+  if (h->tmul) {
+    tmax = 0;
+    for (int32_t x = 0; x < D; x++) {
+      if (h->tmul[x] < 1 || h->tmul[x] > 65536) return ORC_E_ARG;
+      if (h->tmul[x] > tmax) tmax = h->tmul[x];
+    }
+  }
+  if (h->bw) {
+    bwmin = INT64_MAX;
+    for (int32_t i = 0; i < D * D; i++) {
+      if (i / D == i % D) continue;
+      if (h->bw[i] < 1) return ORC_E_ARG;
+      if (h->bw[i] < bwmin) bwmin = h->bw[i];
+    }
+    if (D == 1) bwmin = 1;
+  }
+  if (h->lat) {
+    latmax = 0;
+    for (int32_t i = 0; i < D * D; i++) {
+      if (i / D == i % D) continue;
+      if (h->lat[i] < 0 || h->lat[i] >= ((int64_t)1 << 62)) return ORC_E_ARG;
+      if (h->lat[i] > latmax) latmax = h->lat[i];
+    }
+  }
+  orc_devices worst = *d;
+  worst.bw = bwmin;
+  worst.lat = latmax;
+  int rc = check_overflow(g, &worst);
+  if (rc) return rc;
+  /* every duration at most ceil(tmax / 1024) times w */
+  __int128 tot = 0, f = (tmax + 1023) / 1024;
+  for (int32_t v = 0; v < g->n; v++) {
+    tot += (__int128)g->w[v] * f;
+    int64_t c = comm_of(g->ob[v], bwmin, latmax);
+    tot += (__int128)c * (g->out_ptr[v + 1] - g->out_ptr[v]);
+  }
+  return tot >= ((__int128)1 << 62) ? ORC_E_OVERFLOW : ORC_OK;
+}
+
+int orc_makespan_model(const orc_graph *g, const orc_devices *d, const orc_hetero *h,
+                       const int32_t *order, int32_t K, const uint8_t *node_dev, int32_t model,
+                       int64_t *start, int64_t *finish, int64_t *makespan) {
   int rc = check_graph(g);
   if (rc) return rc;
   if ((rc = check_devices(d))) return rc;
-  if ((rc = check_overflow(g, d))) return rc;
+  if ((rc = check_hetero(g, d, h))) return rc;
   int32_t n = g->n, D = d->D;
   if (K < 1 || !makespan || (n > 0 && !node_dev) || (model & ~3)) return ORC_E_ARG;
   for (int64_t i = 0; i < (int64_t)K * n; i++)
@@ -758,10 +819,10 @@ int orc_makespan_model(const orc_graph *g, const orc_devices *d, const int32_t *
         int64_t r;
         if (dev[u] == dv) r = fin[u];
         else if (tasks) r = arr[(int64_t)u * D + dv];
-        else r = fin[u] + c[u];
+        else r = fin[u] + (h ? link_comm(h, d, g->ob[u], dev[u], dv) : c[u]);
         if (r > ready) ready = r;
       }
-      int64_t s, w = g->w[v];
+      int64_t s, w = dur_on(h, g->w[v], dv);
       if (!insert) {
         s = ready > avail[dv] ? ready : avail[dv];
         avail[dv] = s + w;
@@ -800,8 +861,9 @@ int orc_makespan_model(const orc_graph *g, const orc_devices *d, const int32_t *
           int64_t t0 = fin[v];
           if (snd[dv] > t0) t0 = snd[dv];
           if (rcv[b] > t0) t0 = rcv[b];
-          arr[(int64_t)v * D + b] = t0 + c[v];
-          snd[dv] = rcv[b] = t0 + c[v];
+          int64_t cv = h ? link_comm(h, d, g->ob[v], dv, b) : c[v];
+          arr[(int64_t)v * D + b] = t0 + cv;
+          snd[dv] = rcv[b] = t0 + cv;
         }
       }
     }
@@ -810,5 +872,35 @@ int orc_makespan_model(const orc_graph *g, const orc_devices *d, const int32_t *
   }
   free(c); free(fin); free(avail); free(snd); free(rcv); free(arr); free(wants);
   free(bs); free(bf); free(boff); free(nb);
+  return ORC_OK;
+}
+
+/* Co-location groups (Section 6.1, as in Baechi): every node of a group runs
+ * on the device of the group's first node in `order`; nodes with group -1
+ * keep theirs.  node_dev is [K][n], rewritten in place. */
+int orc_colocate(const orc_graph *g, const int32_t *order, const int32_t *group,
+                 int32_t n_groups, int32_t K, uint8_t *node_dev) {
+  int rc = check_graph(g);
+  if (rc) return rc;
+  int32_t n = g->n;
+  if (K < 1 || n_groups < 0 || (n > 0 && (!order || !group || !node_dev))) return ORC_E_ARG;
+  int32_t *pos = malloc(sizeof(int32_t) * (size_t)(n + 1));
+  rc = check_order(g, order, pos);
+  free(pos);
+  if (rc) return rc;
+  for (int32_t v = 0; v < n; v++)
+    if (group[v] < -1 || group[v] >= n_groups) return ORC_E_ARG;
+  int32_t *lead = malloc(sizeof(int32_t) * ((size_t)n_groups + 1));
+  for (int32_t x = 0; x < n_groups; x++) lead[x] = -1;
+  for (int32_t p = 0; p < n; p++) {  /* the first member in the order leads */
+    int32_t v = order[p];
+    if (group[v] >= 0 && lead[group[v]] < 0) lead[group[v]] = v;
+  }
+  for (int32_t k = 0; k < K; k++) {
+    uint8_t *dev = node_dev + (int64_t)k * n;
+    for (int32_t v = 0; v < n; v++)
+      if (group[v] >= 0) dev[v] = dev[lead[group[v]]];
+  }
+  free(lead);
   return ORC_OK;
 }

@@ -112,9 +112,23 @@ int orc_makespan(const orc_graph *g, const orc_devices *d, const int32_t *order,
  * device order (Section 6.1's runtime model).  `order` is any topological
  * order; start/finish ([K][n], by node id) may be NULL. */
 enum { ORC_MODEL_INSERT = 1, ORC_MODEL_COMM_TASKS = 2 };
-int orc_makespan_model(const orc_graph *g, const orc_devices *d, const int32_t *order,
-                       int32_t K, const uint8_t *node_dev, int32_t model, int64_t *start,
-                       int64_t *finish, int64_t *makespan);
+/* Heterogeneous devices (NULL members: homogeneous): tmul[D] scales compute
+ * time by tmul / 1024 (rounded up, 1 <= tmul <= 65536); bw[D*D], lat[D*D]
+ * give the link from device a to b at [a * D + b] (diagonal unused). */
+typedef struct {
+  const int64_t *tmul;
+  const int64_t *bw;
+  const int64_t *lat;
+} orc_hetero;
+int orc_makespan_model(const orc_graph *g, const orc_devices *d, const orc_hetero *h,
+                       const int32_t *order, int32_t K, const uint8_t *node_dev, int32_t model,
+                       int64_t *start, int64_t *finish, int64_t *makespan);
+
+/* Co-location groups: nodes with group[v] >= 0 take the device of their
+ * group's first node in `order` (a topological order); node_dev [K][n] in
+ * place. */
+int orc_colocate(const orc_graph *g, const int32_t *order, const int32_t *group,
+                 int32_t n_groups, int32_t K, uint8_t *node_dev);
 
 #ifdef __cplusplus
 }

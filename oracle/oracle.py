@@ -62,10 +62,13 @@ def lib():
                                     C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
         L.orc_order_place.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), _P32, C.c_int32,
                                       _PU8, _PU8, C.POINTER(C.c_int32)]
-        L.orc_makespan_model.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), _P32, C.c_int32,
-                                         _PU8, C.c_int32, _P64, _P64, _P64]
+        L.orc_makespan_model.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices),
+                                         C.POINTER(_Hetero), _P32, C.c_int32, _PU8, C.c_int32,
+                                         _P64, _P64, _P64]
+        L.orc_colocate.argtypes = [C.POINTER(_Graph), _P32, _P32, C.c_int32, C.c_int32, _PU8]
         for f in (L.orc_topo_levels, L.orc_blevel, L.orc_cluster, L.orc_place, L.orc_makespan,
-                  L.orc_cpd_topo, L.orc_comm_sums, L.orc_order_place, L.orc_makespan_model):
+                  L.orc_cpd_topo, L.orc_comm_sums, L.orc_order_place, L.orc_makespan_model,
+                  L.orc_colocate):
             f.restype = C.c_int
         _lib = L
     return _lib
@@ -219,10 +222,22 @@ def makespan(wl, order, node_dev, want_times=True):
 MODEL_INSERT, MODEL_COMM_TASKS = 1, 2
 
 
-def makespan_model(wl, order, node_dev, model, want_times=True):
+class _Hetero(C.Structure):
+    _fields_ = [("tmul", _P64), ("bw", _P64), ("lat", _P64)]
+
+
+def makespan_model(wl, order, node_dev, model, want_times=True, tmul=None, bw=None, lat=None):
     """Makespan under the device models (bits MODEL_INSERT, MODEL_COMM_TASKS; 0 is
-    makespan()'s schedule) -> (makespan int64[K], start, finish) ([K, n] or None)"""
+    makespan()'s schedule) -> (makespan int64[K], start, finish) ([K, n] or None).
+    tmul [D] (compute time x tmul / 1024), bw / lat [D, D] (link a -> b): heterogeneous
+    devices; all None = homogeneous."""
     k = _Keep(wl)
+    het = None
+    if tmul is not None or bw is not None or lat is not None:
+        arrs = [None if a is None else np.ascontiguousarray(a, np.int64).reshape(-1)
+                for a in (tmul, bw, lat)]
+        k.het_arrays = arrs
+        het = _Hetero(*[_ptr(a, _P64) for a in arrs])
     n = int(wl.n)
     nd = np.ascontiguousarray(node_dev, np.uint8)
     K = 1 if nd.ndim == 1 else nd.shape[0]
@@ -231,12 +246,29 @@ def makespan_model(wl, order, node_dev, model, want_times=True):
     st = np.zeros((K, max(n, 1)), np.int64) if want_times else None
     fi = np.zeros((K, max(n, 1)), np.int64) if want_times else None
     ms = np.zeros(K, np.int64)
-    _check(lib().orc_makespan_model(C.byref(k.g), C.byref(k.d), _ptr(order, _P32), K,
+    _check(lib().orc_makespan_model(C.byref(k.g), C.byref(k.d),
+                                    None if het is None else C.byref(het), _ptr(order, _P32), K,
                                     _ptr(nd, _PU8), int(model), _ptr(st, _P64), _ptr(fi, _P64),
                                     _ptr(ms, _P64)), "orc_makespan_model")
     if want_times:
         st, fi = st[:, :n], fi[:, :n]
     return ms, st, fi
+
+
+def colocate(wl, order, group, n_groups, node_dev):
+    """Co-location: returns node_dev ([n] or [K, n], a copy) with every group on its
+    first node's (in order) device."""
+    k = _Keep(wl)
+    n = int(wl.n)
+    nd = np.array(node_dev, np.uint8, copy=True)
+    shape = nd.shape
+    K = 1 if nd.ndim == 1 else nd.shape[0]
+    nd = np.ascontiguousarray(nd.reshape(K, n) if n > 0 else np.zeros((K, 1), np.uint8))
+    order = np.ascontiguousarray(order, np.int32)
+    grp = np.ascontiguousarray(group, np.int32)
+    _check(lib().orc_colocate(C.byref(k.g), _ptr(order, _P32), _ptr(grp, _P32), int(n_groups), K,
+                              _ptr(nd, _PU8)), "orc_colocate")
+    return nd[:, :n].reshape(shape) if n > 0 else nd[:, :0].reshape(shape)
 
 
 def comm(wl):

@@ -666,9 +666,10 @@ def test_model_hand_fixtures():
     for case in load("model_hand.json")["cases"]:
         wl = from_edges(case["n"], case["edges"], case["w"], case["ob"], case["D"], case["cap"],
                         case["bw"], case["lat"])
+        het = dict(tmul=case.get("tmul"), bw=case.get("bw_matrix"), lat=case.get("lat_matrix"))
         for m, e in case["models"].items():
             ms, st, fi = O.makespan_model(wl, np.array(case["order"], np.int32),
-                                          np.array(case["dev"], np.uint8), int(m))
+                                          np.array(case["dev"], np.uint8), int(m), **het)
             assert st[0].tolist() == e["start"], (case["name"], m)
             assert fi[0].tolist() == e["finish"] and int(ms[0]) == e["makespan"], (case["name"], m)
 
@@ -771,3 +772,137 @@ def test_model_rejects_bad_inputs():
         O.makespan_model(wl, np.array([1, 0, 2], np.int32), dev, 1)
     with pytest.raises(RuntimeError):
         O.makespan_model(wl, np.array([0, 1, 2], np.int32), np.array([0, 2, 0], np.uint8), 2)
+
+
+# ------------------------------------- heterogeneous devices, co-location
+
+
+def _rand_het(rng, D, wl):
+    tmul = rng.integers(256, 4096, D)
+    bw = rng.integers(1, 4 * int(wl.bw) + 2, (D, D))
+    lat = rng.integers(0, 3 * int(wl.lat) + 5, (D, D))
+    return tmul, bw, lat
+
+
+def test_hetero_uniform_is_homogeneous():
+    """A descriptor that repeats the homogeneous values changes nothing."""
+    rng = np.random.default_rng(41)
+    for s in range(12):
+        n = 3 + s * 17
+        wl = make_random_dag(6100 + s, n, p_edge=min(0.5, 3.0 / n), D=1 + s % 5,
+                             multi=(s % 3 == 0), zero_frac=0.2 if s % 2 else 0.0)
+        order = _rand_topo(wl, rng)
+        P = rng.integers(0, wl.D, (2, n)).astype(np.uint8)
+        D = wl.D
+        for m in range(4):
+            a = O.makespan_model(wl, order, P, m)
+            b = O.makespan_model(wl, order, P, m, tmul=[1024] * D, bw=np.full((D, D), wl.bw),
+                                 lat=np.full((D, D), wl.lat))
+            assert all(np.array_equal(x, y) for x, y in zip(a, b)), (s, m)
+
+
+def test_hetero_closed_forms():
+    """tmul = 2048 everywhere with no comm doubles every time (same as w x 2); one
+    device runs sum of ceil(w tmul / 1024); an alternating chain on two devices
+    with asymmetric links takes sum of durations plus the links crossed."""
+    rng = np.random.default_rng(42)
+    for s in range(10):
+        n = 5 + s * 23
+        wl = make_random_dag(6200 + s, n, p_edge=min(0.5, 3.0 / n), D=2 + s % 3)
+        wl.ob = np.zeros(n, np.int64)
+        wl.lat = 0
+        order = _rand_topo(wl, rng)
+        P = rng.integers(0, wl.D, (2, n)).astype(np.uint8)
+        w2 = from_edges(n, list(zip(*wl.edges())), 2 * np.asarray(wl.w), wl.ob, wl.D, wl.cap,
+                        wl.bw, 0)
+        for m in range(4):
+            a = O.makespan_model(wl, order, P, m, tmul=[2048] * wl.D)
+            b = O.makespan_model(w2, order, P, m)
+            assert all(np.array_equal(x, y) for x, y in zip(a, b)), (s, m)
+        t = int(rng.integers(100, 5000))
+        one = O.makespan_model(wl, order, np.zeros(n, np.uint8), s % 4, tmul=[t] * wl.D)
+        assert int(one[0][0]) == sum(-(-int(x) * t // 1024) for x in wl.w)
+    n = 11
+    w = list(range(3, 3 + n))
+    ob = [7 + i for i in range(n)]
+    wl = from_edges(n, [(i, i + 1) for i in range(n - 1)], w, ob, 2, [100, 100], 1, 0)
+    tm, bw, lat = [700, 1500], [[1, 3], [2, 1]], [[0, 4], [9, 0]]
+    dev = np.array([i % 2 for i in range(n)], np.uint8)
+    expect = sum(-(-w[i] * tm[i % 2] // 1024) for i in range(n))
+    expect += sum(-(-ob[i] // bw[i % 2][1 - i % 2]) + lat[i % 2][1 - i % 2] for i in range(n - 1))
+    for m in range(4):
+        ms, _, _ = O.makespan_model(wl, np.arange(n, dtype=np.int32), dev, m, tmul=tm, bw=bw,
+                                    lat=lat)
+        assert int(ms[0]) == expect
+
+
+def test_hetero_insert_is_first_fit():
+    """The first-fit definition with per-device durations and per-link comm."""
+    rng = np.random.default_rng(43)
+    for s in range(25):
+        n = 2 + s % 19
+        wl = make_random_dag(6300 + s, n, p_edge=0.2, D=2 + s % 3, zero_frac=0.2)
+        order = _rand_topo(wl, rng)
+        dev = rng.integers(0, wl.D, n).astype(np.uint8)
+        tm, bw, lat = _rand_het(rng, wl.D, wl)
+        _, st, fi = O.makespan_model(wl, order, dev, O.MODEL_INSERT, tmul=tm, bw=bw, lat=lat)
+        st, fi = st[0], fi[0]
+        dur = np.array([-(-int(wl.w[v]) * int(tm[dev[v]]) // 1024) for v in range(n)])
+        assert np.array_equal(fi - st, dur)
+        rdy = np.zeros(n, np.int64)
+        for u, v in zip(*wl.edges()):
+            a, b = dev[u], dev[v]
+            c = 0 if a == b else -(-int(wl.ob[u]) // int(bw[a][b])) + int(lat[a][b])
+            rdy[v] = max(rdy[v], fi[u] + c)
+        for i, v in enumerate(order):
+            if dur[v] == 0:
+                assert st[v] == rdy[v]
+                continue
+            before = [u for u in order[:i] if dev[u] == dev[v] and dur[u] > 0]
+            cands = sorted({int(rdy[v])} | {int(fi[u]) for u in before if fi[u] >= rdy[v]})
+            first = next(t for t in cands
+                         if all(t + dur[v] <= st[u] or t >= fi[u] for u in before))
+            assert st[v] == first, (s, v)
+
+
+def test_hetero_rejects_bad_descriptors():
+    wl = from_edges(3, [(0, 1), (1, 2)], [1, 1, 1], [1, 1, 1], 2, [5, 5], 1, 0)
+    o, dev = np.array([0, 1, 2], np.int32), np.array([0, 1, 0], np.uint8)
+    for kw in (dict(tmul=[0, 1024]), dict(tmul=[1024, 70000]), dict(bw=[[1, 0], [1, 1]]),
+               dict(lat=[[0, -1], [0, 0]])):
+        with pytest.raises(RuntimeError):
+            O.makespan_model(wl, o, dev, 0, **kw)
+
+
+def test_colocate_hand_and_properties():
+    case = load("colocate_hand.json")["cases"][0]
+    wl = from_edges(case["n"], case["edges"], [1] * case["n"], [0] * case["n"], 4, [9] * 4, 1, 0)
+    got = O.colocate(wl, case["order"], case["group"], case["n_groups"],
+                     np.array(case["dev_in"], np.uint8))
+    assert got.tolist() == case["dev_out"]
+    rng = np.random.default_rng(44)
+    for s in range(20):
+        n = 1 + s * 13
+        wl = make_random_dag(6400 + s, n, p_edge=min(0.5, 3.0 / n), D=1 + s % 6)
+        order = _rand_topo(wl, rng)
+        G = 1 + s % 7
+        grp = rng.integers(-1, G, n).astype(np.int32)
+        P = rng.integers(0, wl.D, (3, n)).astype(np.uint8)
+        out = O.colocate(wl, order, grp, G, P)
+        pos = np.empty(n, np.int64)
+        pos[order] = np.arange(n)
+        for k in range(3):
+            assert np.array_equal(out[k][grp < 0], P[k][grp < 0])
+            for x in range(G):
+                mem = np.nonzero(grp == x)[0]
+                if mem.size:
+                    lead = mem[np.argmin(pos[mem])]
+                    assert np.all(out[k][mem] == P[k][lead])
+        assert np.array_equal(O.colocate(wl, order, grp, G, out), out)  # idempotent
+        single = np.arange(n, dtype=np.int32)
+        assert np.array_equal(O.colocate(wl, order, single, n, P), P)
+    wl = from_edges(2, [(0, 1)], [1, 1], [0, 0], 2, [5, 5], 1, 0)
+    with pytest.raises(RuntimeError):
+        O.colocate(wl, [0, 1], [0, 2], 2, np.zeros(2, np.uint8))
+    with pytest.raises(RuntimeError):
+        O.colocate(wl, [1, 0], [0, 0], 1, np.zeros(2, np.uint8))
