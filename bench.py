@@ -256,6 +256,32 @@ def models_row(cel, torch, g, d, prio, ndev, seed, K=64):
                           "achieved_GBs": round(B / (kms * 1e-3) / 1e9, 3),
                           "makespan_ns": int(ms[0].item())}
         row[name] = r
+    # heterogeneous devices: the upper half of the devices twice as slow, links
+    # inside a pair of devices twice as fast with half the latency
+    D = d.D
+    het = dict(tmul=[1024 if x < D // 2 else 2048 for x in range(D)],
+               bw=[[2 * d.bw if x // 2 == y // 2 else d.bw for y in range(D)] for x in range(D)],
+               lat=[[d.lat // 2 if x // 2 == y // 2 else d.lat for y in range(D)] for x in range(D)])
+    row["hetero"] = {"devices": "tmul 1024 on devices 0..D/2-1, 2048 above; pairs (2i, 2i+1) "
+                                "linked at 2 x bw, lat / 2"}
+    for model, name in MODEL_NAMES.items():
+        (ms, _, _), call_ms = _timed(torch, lambda: cel.makespan_model(g, d, prio, ndev, model,
+                                                                        **het), reps=2)
+        row["hetero"][name] = {"call_ms": round(call_ms, 2), "makespan_ns": int(ms[0].item())}
+    # co-location: seeded groups of 4 over a tenth of the nodes, K placements
+    G = n // 40
+    grp = np.full(n, -1, np.int32)
+    pick = rng.permutation(n)[:4 * G]
+    grp[pick] = np.repeat(np.arange(G, dtype=np.int32), 4)
+    grp_t = torch.from_numpy(grp).to(ndev.device)
+    PK2 = PK.clone()
+    _, colo_ms = _timed(torch, lambda: cel.colocate(g, prio, grp_t, G, PK2), reps=3)
+    nd1 = ndev.clone()
+    cel.colocate(g, prio, grp_t, G, nd1)
+    (ms_c, _, _), _ = _timed(torch, lambda: cel.makespan_model(g, d, prio, nd1, 0), reps=1)
+    row["colocate"] = {"groups": G, "group_size": 4, "K": K, "call_ms": round(colo_ms, 2),
+                       "makespan_ns_after": int(ms_c[0].item()),
+                       "makespan_ns_before": row["fifo"]["K1"]["makespan_ns"]}
     return row
 
 

@@ -10,6 +10,7 @@
  *   cel_place        coarse graph + Adjusting Placement           (Section 5.2, eq. 7-9, Alg. 2)
  *   cel_makespan     makespan of one or K placements              (Section 5.2, eq. 7)
  *   cel_makespan_model  makespan with insertion / transfer tasks  (Section 5.2 eq. 7, 6.1)
+ *   cel_colocate     co-location groups follow their first node  (Section 6.1)
  *   cel_order_place  Order-Place baseline placement               (Section 5.2, 6.2.2)
  *   cel_comm_sums    the parts of the comm/compute ratio CCR      (Section 5.1.1, eq. 1)
  *
@@ -200,6 +201,17 @@ int cel_makespan(const cel_graph *g, const cel_devices *d, const int32_t *order,
                  int32_t K, const uint8_t *node_dev, int64_t *start, int64_t *finish,
                  int64_t *makespan, hipStream_t stream);
 
+/* Heterogeneous devices for cel_makespan_model (host arrays; a NULL member
+ * keeps the homogeneous value): device x runs a node of compute time w in
+ * ceil(w * tmul[x] / 1024) (1024 = the reference speed, 1 <= tmul <= 65536);
+ * node u's output takes ceil(ob[u] / bw[a*D + b]) + lat[a*D + b] from device
+ * a to device b (1 <= bw < 2^31, 0 <= lat < 2^31; the diagonal is unused). */
+typedef struct {
+  const int64_t *tmul; /* (host) [D] */
+  const int64_t *bw;   /* (host) [D*D] bytes per ns */
+  const int64_t *lat;  /* (host) [D*D] ns */
+} cel_hetero;
+
 /* Makespan of K placements under richer device models (Section 5.2's slot
  * rule, eq. 7, at node level; Section 6.1's transfers as tasks).  Nodes are
  * taken in `order`; a node is ready when each input has arrived: a
@@ -213,15 +225,26 @@ int cel_makespan(const cel_graph *g, const cel_devices *d, const int32_t *order,
  * holding a successor of p, in increasing device order, each taking c[p] and
  * holding p's device's send channel and the target's receive channel:
  * start = max(finish of p, both channels' previous transfer end).
+ * h: heterogeneous devices (cel_hetero; node durations and link costs follow
+ * it), or NULL.
  * Inputs: order [n] any topological order (permutation with pos[u] < pos[v]
  * on every edge); K >= 1; node_dev [K][n] uint8, each < D; D <= 64; model a
  * combination of the CEL_MODEL_* bits.
  * Outputs: start, finish [K][n] by node id, or NULL; makespan [K] (device).
  * Errors: CEL_E_ARG (also D > 64), CEL_E_ORDER, CEL_E_OVERFLOW, CEL_E_HIP,
  * CEL_E_NOMEM. */
-int cel_makespan_model(const cel_graph *g, const cel_devices *d, const int32_t *order,
-                       int32_t K, const uint8_t *node_dev, int32_t model, int64_t *start,
-                       int64_t *finish, int64_t *makespan, hipStream_t stream);
+int cel_makespan_model(const cel_graph *g, const cel_devices *d, const cel_hetero *h,
+                       const int32_t *order, int32_t K, const uint8_t *node_dev, int32_t model,
+                       int64_t *start, int64_t *finish, int64_t *makespan, hipStream_t stream);
+
+/* Co-location groups (Section 6.1): every node with group[v] >= 0 moves to the
+ * device of its group's first node in `order`; nodes with group -1 keep
+ * theirs.  Memory caps are not rechecked (the group's leader decides).
+ * Inputs: order [n] a topological order; group [n] in [-1, n_groups);
+ * node_dev [K][n] uint8, rewritten in place.
+ * Errors: CEL_E_ARG, CEL_E_ORDER, CEL_E_HIP, CEL_E_NOMEM. */
+int cel_colocate(const cel_graph *g, const int32_t *order, const int32_t *group,
+                 int32_t n_groups, int32_t K, uint8_t *node_dev, hipStream_t stream);
 
 /* Diagnostics: per-kernel device time.  After cel_timing(1), every call
  * records a pair of HIP events on its stream around each of its main kernel

@@ -21,7 +21,7 @@ COMM_OFF = 1
 CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
 EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_cluster", "cel_place", "cel_makespan",
-           "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
+           "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_colocate", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
 class CelError(RuntimeError):
@@ -35,6 +35,11 @@ class _Graph(C.Structure):
                 ("out_ptr", C.c_void_p), ("out_idx", C.c_void_p),
                 ("in_ptr", C.c_void_p), ("in_idx", C.c_void_p),
                 ("w", C.c_void_p), ("mem", C.c_void_p), ("ob", C.c_void_p)]
+
+
+class _Hetero(C.Structure):
+    _fields_ = [("tmul", C.POINTER(C.c_int64)), ("bw", C.POINTER(C.c_int64)),
+                ("lat", C.POINTER(C.c_int64))]
 
 
 class _Devices(C.Structure):
@@ -63,10 +68,11 @@ def lib() -> C.CDLL:
         L.cel_cpd_order.argtypes = [G, vp, vp, vp, vp]
         L.cel_order_place.argtypes = [G, Dv, vp, i32, vp, vp, C.POINTER(i32), vp]
         L.cel_comm_sums.argtypes = [G, Dv, vp, C.POINTER(i64), C.POINTER(i64), vp]
-        L.cel_makespan_model.argtypes = [G, Dv, vp, i32, vp, i32, vp, vp, vp, vp]
+        L.cel_makespan_model.argtypes = [G, Dv, C.POINTER(_Hetero), vp, i32, vp, i32, vp, vp, vp, vp]
+        L.cel_colocate.argtypes = [G, vp, vp, i32, i32, vp, vp]
         for f in ("cel_topo_levels", "cel_blevel", "cel_cluster", "cel_place", "cel_makespan",
                   "cel_cpd_order", "cel_order_place", "cel_comm_sums", "cel_makespan_model",
-                  "cel_version"):
+                  "cel_colocate", "cel_version"):
             getattr(L, f).restype = C.c_int
         L.cel_last_error.argtypes = []
         L.cel_last_error.restype = C.c_char_p
@@ -246,9 +252,22 @@ def order_place(g: Graph, d: Devices, cluster_id, n_clusters):
 MODEL_INSERT, MODEL_COMM_TASKS = 1, 2
 
 
-def makespan_model(g: Graph, d: Devices, order, node_dev, model, want_times=False):
+def makespan_model(g: Graph, d: Devices, order, node_dev, model, want_times=False, tmul=None,
+                   bw=None, lat=None):
     """Makespan under the device models (MODEL_* bits; 0 = FIFO devices, contention-free
-    comm). node_dev uint8 [n] or [K, n] -> (makespan int64[K], start, finish) ([K, n] or None)"""
+    comm). node_dev uint8 [n] or [K, n] -> (makespan int64[K], start, finish) ([K, n] or None).
+    tmul [D], bw / lat [D, D]: heterogeneous devices (host values, time x tmul / 1024)."""
+    het, keep = None, []
+    if tmul is not None or bw is not None or lat is not None:
+        ptrs = []
+        for a in (tmul, bw, lat):
+            if a is None:
+                ptrs.append(None)
+                continue
+            arr = (C.c_int64 * int(np.asarray(a).size))(*[int(x) for x in np.asarray(a).reshape(-1)])
+            keep.append(arr)
+            ptrs.append(C.cast(arr, C.POINTER(C.c_int64)))
+        het = _Hetero(*ptrs)
     n = g.n
     nd = node_dev.contiguous()
     K = 1 if nd.dim() == 1 else nd.shape[0]
@@ -256,11 +275,24 @@ def makespan_model(g: Graph, d: Devices, order, node_dev, model, want_times=Fals
     st = torch.empty((K, max(n, 1)), dtype=torch.int64, device=g.device) if want_times else None
     fi = torch.empty((K, max(n, 1)), dtype=torch.int64, device=g.device) if want_times else None
     gc, dc = g._c(), d._c()
-    _check(lib().cel_makespan_model(C.byref(gc), C.byref(dc), _p(order), int(K), _p(nd), int(model),
-                                    _p(st), _p(fi), _p(ms), _stream()))
+    _check(lib().cel_makespan_model(C.byref(gc), C.byref(dc), None if het is None else C.byref(het),
+                                    _p(order), int(K), _p(nd), int(model), _p(st), _p(fi), _p(ms),
+                                    _stream()))
     if want_times:
         st, fi = st[:, :n], fi[:, :n]
     return ms, st, fi
+
+
+def colocate(g: Graph, order, group, n_groups, node_dev):
+    """Co-location groups: node_dev (uint8 [n] or [K, n], device) rewritten in place so that
+    every group follows its first node in `order`; returns node_dev."""
+    nd = node_dev
+    assert nd.is_contiguous()
+    K = 1 if nd.dim() == 1 else nd.shape[0]
+    gc = g._c()
+    _check(lib().cel_colocate(C.byref(gc), _p(order), _p(group), int(n_groups), int(K), _p(nd),
+                              _stream()))
+    return nd
 
 
 def comm_sums(g: Graph, d: Devices, cluster_id=None):

@@ -381,6 +381,7 @@ __global__ void k_makespan_out(int32_t K, int32_t n, const int32_t *order, const
                                const int64_t *wp, int64_t *start, int64_t *finish,
                                const Status *st);
 __global__ void k_fill_i64(int64_t *p, int64_t n, int64_t v);
+__global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v);  // common.hip
 
 // Copies the status block to the host (synchronising the stream).
 int read_status(const Status *dst, Status *host, hipStream_t s);

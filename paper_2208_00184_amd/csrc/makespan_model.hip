@@ -30,6 +30,14 @@
 // there that holds the node (ballot), then shrinks, splits or empties it.
 // Transfers: a producer's destination devices form a mask; its arrivals sit
 // in a pool at off[p] + (rank of the device in the mask).
+// Heterogeneous devices (HET): device d runs a node of w in ceil(w tmul[d] /
+// 1024), computed as (w >> 10) tmul + ceil((w & 1023) tmul / 1024) so that
+// no product leaves 64 bits; a transfer from a to b takes ceil(ob / bw[a][b])
+// + lat[a][b], the link tables staged in LDS.
+//
+// cel_colocate (co-location groups, Section 6.1): the first member of each
+// group in the order (smallest position, by atomicMin) leads, and every
+// member takes its device.
 #include "cel_internal.h"
 
 namespace cel {
@@ -48,7 +56,21 @@ struct MmArgs {
   int64_t *ga, *gb;            // gap starts and ends (insertion)
   int64_t *finp;               // [K][n] finish by position
   int64_t *makespan;           // [K]
+  const int64_t *obp;          // ob by position (HET)
+  const int64_t *tmul;         // [D] time multipliers, 1/1024 (HET)
+  const int64_t *lbw, *llat;   // [D][D] links (HET)
 };
+
+constexpr int kHetD = 64;  // link table stride
+
+// ceil(w * tm / 1024) for w >= 0, 1 <= tm <= 65536, without a 128-bit product
+__device__ inline int64_t dur_on(int64_t w, int64_t tm) {
+  return (w >> 10) * tm + (((w & 1023) * tm + 1023) >> 10);
+}
+
+__device__ inline int64_t link_c(int64_t ob, int32_t bw, int32_t lat) {
+  return ob / bw + (ob % bw != 0 ? 1 : 0) + lat;
+}
 
 // Lane l of a register replaced by v (uniform l and v): a lane compare and a
 // select, no memory.
@@ -64,11 +86,12 @@ __device__ inline uint64_t below(int b) { return (uint64_t(1) << b) - 1; }
 // folded into ext, the others marked in msk (bit = position - P0).  An input
 // on another device contributes f + c (contention-free) or, with transfers,
 // the arrival of its output on dv: pool[off + rank of dv in its mask].
-template <bool TASKS>
+template <bool TASKS, bool HET>
 __device__ inline void fold_inputs(const MmArgs &a, const uint8_t *dev, const int64_t *fin,
-                                   const uint64_t *dm, const int64_t *of, int32_t P0, int32_t e0,
-                                   int32_t e1, int32_t step, int32_t dv, int64_t &ext,
-                                   uint64_t &msk, uint32_t &bad) {
+                                   const uint64_t *dm, const int64_t *of, const int32_t *s_bw,
+                                   const int32_t *s_lat, int32_t P0, int32_t e0, int32_t e1,
+                                   int32_t step, int32_t dv, int64_t &ext, uint64_t &msk,
+                                   uint32_t &bad) {
   for (int32_t e = e0; e < e1; e += 4 * step) {
     int32_t q[4];
 #pragma unroll
@@ -86,7 +109,7 @@ __device__ inline void fold_inputs(const MmArgs &a, const uint8_t *dev, const in
           const uint64_t mq = dm[q[u]];
           x[u] = (mq >> dv) & 1 ? of[q[u]] + __builtin_popcountll(mq & below(dv)) : -1;
         } else {
-          x[u] = a.cq[q[u]];
+          x[u] = HET ? a.obp[q[u]] : a.cq[q[u]];
         }
       }
     }
@@ -106,6 +129,8 @@ __device__ inline void fold_inputs(const MmArgs &a, const uint8_t *dev, const in
           continue;
         }
         t = a.pool[x[u]];
+      } else if (HET) {
+        t = f[u] + link_c(x[u], s_bw[dq[u] * kHetD + dv], s_lat[dq[u] * kHetD + dv]);
       } else {
         t = f[u] + x[u];
       }
@@ -208,11 +233,22 @@ __device__ inline int64_t insert_slot(int64_t *A, int64_t *B, int64_t r, int64_t
   return s;
 }
 
-template <bool INS, bool TASKS>
+template <bool INS, bool TASKS, bool HET>
 __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
   __shared__ int64_t s_T[TASKS ? 64 * 64 : 1];  // arrival of slot j's output on device b
+  __shared__ int32_t s_bw[HET ? kHetD * kHetD : 1], s_lat[HET ? kHetD * kHetD : 1];
   if (failed(st)) return;
   const int lane = threadIdx.x;
+  int64_t tmr = 1024;  // device `lane`'s time multiplier
+  if (HET) {
+    for (int i = lane; i < a.D * a.D; i += 64) {
+      const int x = i / a.D, y = i - x * a.D;
+      s_bw[x * kHetD + y] = (int32_t)a.lbw[i];
+      s_lat[x * kHetD + y] = (int32_t)a.llat[i];
+    }
+    if (lane < a.D) tmr = a.tmul[lane];
+    __syncthreads();
+  }
   const int64_t k = blockIdx.x;
   const int32_t n = a.n;
   const uint8_t *dev = a.devp + k * n;
@@ -237,7 +273,7 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
     if (act) {
       dv = dev[p];
       w = a.wp[p];
-      c = a.cq[p];
+      c = HET ? a.obp[p] : a.cq[p];  // ob under HET: the comm depends on the link
       i0 = a.iptr[p];
       i1 = a.iptr[p + 1];
       if (TASKS) {
@@ -247,14 +283,16 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
     }
     // A: inputs from before the window
     const bool heavy = i1 - i0 > kMmLight;
-    if (!heavy) fold_inputs<TASKS>(a, dev, fin, dm, of, P0, i0, i1, 1, dv, ext, msk, bad);
+    if (!heavy)
+      fold_inputs<TASKS, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, i0, i1, 1, dv, ext, msk, bad);
     for (uint64_t hv = __ballot(heavy); hv; hv &= hv - 1) {
       const int h = __builtin_ctzll(hv);
       const int32_t e0 = __builtin_amdgcn_readlane(i0, h), e1 = __builtin_amdgcn_readlane(i1, h);
       const int32_t dh = __builtin_amdgcn_readlane(dv, h);
       int64_t mx = 0;
       uint64_t mk = 0;
-      fold_inputs<TASKS>(a, dev, fin, dm, of, P0, e0 + lane, e1, 64, dh, mx, mk, bad);
+      fold_inputs<TASKS, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, e0 + lane, e1, 64, dh, mx, mk,
+                              bad);
       for (int off = 32; off > 0; off >>= 1) {
         const int64_t o = __shfl_xor(mx, off);
         mx = o > mx ? o : mx;
@@ -269,7 +307,7 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
     int64_t finw = 0;
     for (int j = 0; j < nw; j++) {
       const int32_t dj = __builtin_amdgcn_readlane(dv, j);
-      const int64_t wj = readlane64(w, j);
+      const int64_t wj = HET ? dur_on(readlane64(w, j), readlane64(tmr, dj)) : readlane64(w, j);
       int64_t r = readlane64(ext, j);
       for (uint64_t mj = (uint64_t)readlane64((int64_t)msk, j); mj; mj &= mj - 1) {
         const int q = __builtin_ctzll(mj);
@@ -278,6 +316,7 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
         int64_t t;
         if (dq == dj) t = fq;
         else if (TASKS) t = s_T[q * 64 + dj];
+        else if (HET) t = fq + link_c(readlane64(c, q), s_bw[dq * kHetD + dj], s_lat[dq * kHetD + dj]);
         else t = fq + readlane64(c, q);
         r = t > r ? t : r;
       }
@@ -310,7 +349,7 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
             const int64_t rb = readlane64(rcv, b);
             int64_t t0 = f > sf ? f : sf;
             t0 = rb > t0 ? rb : t0;
-            sf = t0 + cj;
+            sf = t0 + (HET ? link_c(cj, s_bw[dj * kHetD + b], s_lat[dj * kHetD + b]) : cj);
             rcv = setlane<int64_t>(rcv, sf, b);
             tcur = setlane<int64_t>(tcur, sf, b);
           }
@@ -392,14 +431,95 @@ __global__ void k_mm_popc(int64_t N, const uint64_t *dmask, int64_t *cntv, const
     cntv[i] = __builtin_popcountll(dmask[i]);
 }
 
+// Start and finish by node id: start = finish - the node's duration on its
+// device (w, or ceil(w tmul / 1024) with tmul).
+__global__ void k_mm_out(int32_t K, int32_t n, const int32_t *order, const int64_t *finp,
+                         const int64_t *wp, const uint8_t *devp, const int64_t *tmul,
+                         int64_t *start, int64_t *finish, const Status *st) {
+  if (failed(st)) return;
+  const int64_t tot = (int64_t)K * n;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < tot;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t k = i / n, p = i - k * n;
+    const int64_t v = k * n + order[p];
+    const int64_t f = finp[i];
+    if (finish) finish[v] = f;
+    if (start) start[v] = f - (tmul ? dur_on(wp[p], tmul[devp[i]]) : wp[p]);
+  }
+}
+
+// lead[g] = smallest position of a member of group g (INT32_MAX initially).
+__global__ void k_colo_lead(int32_t n, int32_t G, const int32_t *group, const int32_t *pos,
+                            int32_t *lead, Status *st) {
+  if (failed(st)) return;
+  uint32_t bad = 0;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t x = group[v];
+    if (x < -1 || x >= G) bad |= EB_ARG;
+    else if (x >= 0) atomicMin(&lead[x], pos[v]);
+  }
+  if (bad) raise_err(st, bad);
+}
+
+// Every member takes its group leader's device (the leader keeps its own).
+__global__ void k_colo_apply(int32_t K, int32_t n, const int32_t *group, const int32_t *lead,
+                             const int32_t *order, uint8_t *node_dev, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t x = group[v];
+    if (x < 0) continue;
+    const int32_t u = order[lead[x]];
+    if (u == v) continue;
+    for (int64_t k = blockIdx.y; k < K; k += gridDim.y)
+      node_dev[k * n + v] = node_dev[k * n + u];
+  }
+}
+
 }  // namespace cel
 
 using namespace cel;
 
-extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, const int32_t *order,
-                                  int32_t K, const uint8_t *node_dev, int32_t model,
-                                  int64_t *start, int64_t *finish, int64_t *makespan,
-                                  hipStream_t s) {
+// Host checks of a heterogeneous descriptor; fills the worst link (smallest
+// bandwidth, largest latency) and the largest multiplier.
+static int check_hetero(const cel_hetero *h, const cel_devices *d, const char *fn, int64_t *bwmin,
+                        int64_t *latmax, int64_t *tmax) {
+  const int32_t D = d->D;
+  *bwmin = d->bw;
+  *latmax = d->lat;
+  *tmax = 1024;
+  if (h->tmul) {
+    *tmax = 0;
+    for (int32_t x = 0; x < D; x++) {
+      if (h->tmul[x] < 1 || h->tmul[x] > 65536)
+        return set_error(CEL_E_ARG, "%s: tmul[%d] outside [1, 65536]", fn, x);
+      *tmax = h->tmul[x] > *tmax ? h->tmul[x] : *tmax;
+    }
+  }
+  if (h->bw) *bwmin = INT32_MAX;
+  if (h->lat) *latmax = 0;
+  for (int32_t i = 0; i < D * D; i++) {
+    if (i / D == i % D) continue;
+    if (h->bw) {
+      if (h->bw[i] < 1 || h->bw[i] > INT32_MAX)
+        return set_error(CEL_E_ARG, "%s: link bandwidth %d outside [1, 2^31)", fn, i);
+      *bwmin = h->bw[i] < *bwmin ? h->bw[i] : *bwmin;
+    }
+    if (h->lat) {
+      if (h->lat[i] < 0 || h->lat[i] > INT32_MAX)
+        return set_error(CEL_E_ARG, "%s: link latency %d outside [0, 2^31)", fn, i);
+      *latmax = h->lat[i] > *latmax ? h->lat[i] : *latmax;
+    }
+  }
+  if (D == 1) *bwmin = d->bw;
+  return CEL_OK;
+}
+
+extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, const cel_hetero *h,
+                                  const int32_t *order, int32_t K, const uint8_t *node_dev,
+                                  int32_t model, int64_t *start, int64_t *finish,
+                                  int64_t *makespan, hipStream_t s) {
   const char *fn = "cel_makespan_model";
   CEL_TRY(check_host_graph(g, fn));
   CEL_TRY(check_host_devices(d, fn));
@@ -410,6 +530,21 @@ extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, cons
     return set_error(CEL_E_ARG, "%s: unknown model bits 0x%x", fn, model);
   if (D > 64) return set_error(CEL_E_ARG, "%s: D = %d above 64", fn, D);
   const bool ins = model & CEL_MODEL_INSERT, tasks = model & CEL_MODEL_COMM_TASKS;
+  const bool het = h && (h->tmul || h->bw || h->lat);
+  int64_t bwmin = d->bw, latmax = d->lat, tmax = 1024;
+  if (het) {
+    CEL_TRY(check_hetero(h, d, fn, &bwmin, &latmax, &tmax));
+    // overflow bound with the slowest device and the worst link: every time
+    // is a sum of durations and transfers along one chain
+    cel_devices worst = *d;
+    worst.bw = bwmin;
+    worst.lat = latmax;
+    int64_t ec = 0, ws = 0;
+    CEL_TRY(cel_comm_sums(g, &worst, nullptr, &ec, &ws, s));
+    const __int128 tot = (__int128)ws * ((tmax + 1023) / 1024) + ec;
+    if (tot >= ((__int128)1 << 62))
+      return set_error(CEL_E_OVERFLOW, "%s: times could reach 2^62", fn);
+  }
   Scratch sc(s);
   Status *st;
   CEL_TRY(sc.get(&st, 1));
@@ -425,7 +560,7 @@ extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, cons
   uint8_t *devp;
   CEL_TRY(sc.get(&tmp, n));
   CEL_TRY(sc.get(&pos, n));
-  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, sc, s));
+  CEL_TRY(check_graph(g, bwmin, latmax, true, st, tmp, sc, s));
   CEL_TRY(check_topo_order(g, order, pos, st, s));
   const int64_t Kn = (int64_t)K * n;
   CEL_TRY(sc.get(&iptr, (int64_t)n + 1));
@@ -435,8 +570,9 @@ extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, cons
   CEL_TRY(sc.get(&devp, Kn));
   CEL_TRY(sc.get(&finp, Kn));
   CEL_TRY(relabel_csr(n, g->m, order, pos, g->in_ptr, g->in_idx, iptr, iidx, sc, s, st));
-  k_pos_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, g->w, g->ob, d->bw, d->lat, wp, cq,
-                                                    st);
+  // under HET cq holds ob (bandwidth 1, latency 0): the link decides the comm
+  k_pos_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, g->w, g->ob, het ? 1 : d->bw,
+                                                    het ? 0 : d->lat, wp, cq, st);
   const int gx = grid_for(n, 256, 1024), gy = K < 1024 ? K : 1024;
   k_dev_gather<<<dim3(gx, gy), 256, 0, s>>>(K, n, order, node_dev, D, devp, st);
   MmArgs a{};
@@ -449,6 +585,29 @@ extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, cons
   a.devp = devp;
   a.finp = finp;
   a.makespan = makespan;
+  int64_t *tmul_d = nullptr;
+  if (het) {
+    int64_t *lbw, *llat;
+    CEL_TRY(sc.get(&tmul_d, D));
+    CEL_TRY(sc.get(&lbw, (int64_t)D * D));
+    CEL_TRY(sc.get(&llat, (int64_t)D * D));
+    std::vector<int64_t> ht(D), hb((size_t)D * D), hl((size_t)D * D);
+    for (int32_t x = 0; x < D; x++) ht[x] = h->tmul ? h->tmul[x] : 1024;
+    for (int32_t i = 0; i < D * D; i++) {
+      const bool diag = i / D == i % D;
+      hb[i] = diag ? 1 : (h->bw ? h->bw[i] : d->bw);
+      hl[i] = diag ? 0 : (h->lat ? h->lat[i] : d->lat);
+      if (!h->bw && hb[i] > INT32_MAX) return set_error(CEL_E_ARG, "%s: bw above 2^31", fn);
+      if (!h->lat && hl[i] > INT32_MAX) return set_error(CEL_E_ARG, "%s: lat above 2^31", fn);
+    }
+    CEL_HIP(hipMemcpyAsync(tmul_d, ht.data(), sizeof(int64_t) * D, hipMemcpyHostToDevice, s));
+    CEL_HIP(hipMemcpyAsync(lbw, hb.data(), sizeof(int64_t) * D * D, hipMemcpyHostToDevice, s));
+    CEL_HIP(hipMemcpyAsync(llat, hl.data(), sizeof(int64_t) * D * D, hipMemcpyHostToDevice, s));
+    a.obp = cq;
+    a.tmul = tmul_d;
+    a.lbw = lbw;
+    a.llat = llat;
+  }
   if (ins) {
     int32_t *cnt;
     int64_t *goff, *ga, *gb;
@@ -486,17 +645,59 @@ extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, cons
   }
   {
     KTimer kt(s, "k_makespan_model");
-    if (!ins && !tasks) k_makespan_model<false, false><<<(unsigned)K, 64, 0, s>>>(a, st);
-    else if (ins && !tasks) k_makespan_model<true, false><<<(unsigned)K, 64, 0, s>>>(a, st);
-    else if (!ins) k_makespan_model<false, true><<<(unsigned)K, 64, 0, s>>>(a, st);
-    else k_makespan_model<true, true><<<(unsigned)K, 64, 0, s>>>(a, st);
+    const unsigned gk = (unsigned)K;
+    if (het) {
+      if (!ins && !tasks) k_makespan_model<false, false, true><<<gk, 64, 0, s>>>(a, st);
+      else if (ins && !tasks) k_makespan_model<true, false, true><<<gk, 64, 0, s>>>(a, st);
+      else if (!ins) k_makespan_model<false, true, true><<<gk, 64, 0, s>>>(a, st);
+      else k_makespan_model<true, true, true><<<gk, 64, 0, s>>>(a, st);
+    } else {
+      if (!ins && !tasks) k_makespan_model<false, false, false><<<gk, 64, 0, s>>>(a, st);
+      else if (ins && !tasks) k_makespan_model<true, false, false><<<gk, 64, 0, s>>>(a, st);
+      else if (!ins) k_makespan_model<false, true, false><<<gk, 64, 0, s>>>(a, st);
+      else k_makespan_model<true, true, false><<<gk, 64, 0, s>>>(a, st);
+    }
   }
   if (start || finish)
-    k_makespan_out<<<grid_for(Kn, 256, 8192), 256, 0, s>>>(K, n, order, finp, wp, start, finish,
-                                                          st);
+    k_mm_out<<<grid_for(Kn, 256, 8192), 256, 0, s>>>(K, n, order, finp, wp, devp, tmul_d, start,
+                                                    finish, st);
   CEL_HIP(hipGetLastError());
-  Status h;
-  CEL_TRY(read_status(st, &h, s));
-  if (h.err) return status_error(h, fn);
+  Status hs;
+  CEL_TRY(read_status(st, &hs, s));
+  if (hs.err) return status_error(hs, fn);
+  return CEL_OK;
+}
+
+extern "C" int cel_colocate(const cel_graph *g, const int32_t *order, const int32_t *group,
+                            int32_t n_groups, int32_t K, uint8_t *node_dev, hipStream_t s) {
+  const char *fn = "cel_colocate";
+  CEL_TRY(check_host_graph(g, fn));
+  const int32_t n = g->n;
+  if (K < 1 || n_groups < 0 || (n > 0 && (!order || !group || !node_dev)))
+    return set_error(CEL_E_ARG, "%s: NULL argument, K < 1 or n_groups < 0", fn);
+  if (n == 0) return CEL_OK;
+  Scratch sc(s);
+  Status *st;
+  int32_t *tmp, *pos, *lead;
+  CEL_TRY(sc.get(&st, 1));
+  CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
+  CEL_TRY(sc.get(&tmp, n));
+  CEL_TRY(sc.get(&pos, n));
+  CEL_TRY(check_graph(g, 1, 0, false, st, tmp, sc, s));
+  CEL_TRY(check_topo_order(g, order, pos, st, s));
+  if (n_groups > 0) {
+    CEL_TRY(sc.get(&lead, n_groups));
+    k_fill_i32<<<grid_for(n_groups, 256, 1024), 256, 0, s>>>(lead, n_groups, INT32_MAX);
+    k_colo_lead<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, n_groups, group, pos, lead, st);
+    const int gy = K < 1024 ? K : 1024;
+    k_colo_apply<<<dim3(grid_for(n, 256, 1024), gy), 256, 0, s>>>(K, n, group, lead, order,
+                                                                 node_dev, st);
+  } else {
+    k_colo_lead<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, 0, group, pos, nullptr, st);
+  }
+  CEL_HIP(hipGetLastError());
+  Status hs;
+  CEL_TRY(read_status(st, &hs, s));
+  if (hs.err) return status_error(hs, fn);
   return CEL_OK;
 }

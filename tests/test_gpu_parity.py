@@ -780,14 +780,15 @@ def test_order_place_and_ccr_transformer96():
 MODELS = (0, cel.MODEL_INSERT, cel.MODEL_COMM_TASKS, cel.MODEL_INSERT | cel.MODEL_COMM_TASKS)
 
 
-def check_model(wl, order, P, models=MODELS):
+def check_model(wl, order, P, models=MODELS, **het):
     g, d = up(wl)
     o = tt(order, np.int32)
     Pt = tt(P, np.uint8)
     for m in models:
-        ref = O.makespan_model(wl, order, P, m)
-        print(f"[model] n={wl.n} D={wl.D} K={1 if P.ndim == 1 else P.shape[0]} model={m}", flush=True)
-        ms, st, fi = cel.makespan_model(g, d, o, Pt, m, want_times=True)
+        ref = O.makespan_model(wl, order, P, m, **het)
+        print(f"[model] n={wl.n} D={wl.D} K={1 if P.ndim == 1 else P.shape[0]} model={m} "
+              f"het={sorted(k for k, v in het.items() if v is not None)}", flush=True)
+        ms, st, fi = cel.makespan_model(g, d, o, Pt, m, want_times=True, **het)
         assert np.array_equal(np_(ms), ref[0]), m
         assert np.array_equal(np_(fi), ref[2]), m
         assert np.array_equal(np_(st), ref[1]), m
@@ -801,9 +802,11 @@ def test_model_hand_fixtures():
         wl = from_edges(case["n"], case["edges"], case["w"], case["ob"], case["D"], case["cap"],
                         case["bw"], case["lat"])
         g, d = up(wl)
+        het = dict(tmul=case.get("tmul"), bw=case.get("bw_matrix"), lat=case.get("lat_matrix"))
         for m, e in case["models"].items():
             ms, st, fi = cel.makespan_model(g, d, tt(case["order"], np.int32),
-                                            tt(case["dev"], np.uint8), int(m), want_times=True)
+                                            tt(case["dev"], np.uint8), int(m), want_times=True,
+                                            **het)
             assert np_(st)[0].tolist() == e["start"], (case["name"], m)
             assert np_(fi)[0].tolist() == e["finish"] and int(np_(ms)[0]) == e["makespan"]
 
@@ -918,3 +921,102 @@ def test_model_transformer96():
     lev, oid, lp, L = O.topo_levels(wl)
     _, _, pr, _ = O.blevel(wl, lev, oid)
     check_model(wl, pr, P)
+
+
+
+# ------------------------------------------- heterogeneous devices, co-location
+
+
+def rand_het(rng, wl, parts=("tmul", "bw", "lat")):
+    D = wl.D
+    het = dict(tmul=None, bw=None, lat=None)
+    if "tmul" in parts:
+        het["tmul"] = rng.integers(200, 5000, D)
+    if "bw" in parts:
+        het["bw"] = rng.integers(1, 4 * int(wl.bw) + 2, (D, D))
+    if "lat" in parts:
+        het["lat"] = rng.integers(0, 3 * int(wl.lat) + 5, (D, D))
+    return het
+
+
+def test_hetero_random_dags():
+    rng = np.random.default_rng(51)
+    parts = [("tmul", "bw", "lat"), ("tmul",), ("bw",), ("lat", "bw")]
+    for s in range(12):
+        n = 5 + (s * 151) % 1200
+        D = [2, 3, 8, 64, 5, 17][s % 6]
+        wl = make_random_dag(8100 + s, n, p_edge=min(0.6, (2.0 + 20.0 * (s % 4 == 0)) / n), D=D,
+                             multi=(s % 3 == 0), zero_frac=0.2 if s % 2 else 0.0)
+        order = random_topo_order(wl, rng)
+        P = rng.integers(0, D, (2, n)).astype(np.uint8)
+        check_model(wl, order, P, **rand_het(rng, wl, parts[s % 4]))
+
+
+def test_hetero_configs_and_overflow():
+    wl, rt, rb = config(3, 0)
+    rng = np.random.default_rng(52)
+    cid, C, _ = O.cluster(wl, rb[2], 200, -1)
+    P = np.concatenate([O.place(wl, cid, C)[1][None, :], random_placements(wl, 1, 3)])
+    check_model(wl, rb[2], P, **rand_het(rng, wl))
+    big = from_edges(2, [(0, 1)], [2 ** 50, 1], [0, 0], 2, [5, 5], 1, 0)
+    g, d = up(big)
+    o, dv = tt([0, 1], np.int32), tt([0, 1], np.uint8)
+    with pytest.raises(cel.CelError) as ei:  # link latencies must stay below 2^31
+        cel.makespan_model(g, d, o, dv, 0, tmul=[65536, 1024], bw=[[1, 1], [1, 1]],
+                           lat=[[0, 2 ** 31], [0, 0]])
+    assert ei.value.code == -1
+    ms, _, _ = cel.makespan_model(g, d, o, dv, 0, tmul=[65536, 1024])  # 2^50 x 64 = 2^56 fits
+    assert int(np_(ms)[0]) == int(O.makespan_model(big, [0, 1], [0, 1], 0, tmul=[65536, 1024])[0][0])
+    huge = from_edges(2, [(0, 1)], [2 ** 57, 1], [0, 0], 2, [5, 5], 1, 0)
+    g, d = up(huge)
+    with pytest.raises(cel.CelError) as ei:  # 2^57 x 64 = 2^63: rejected like the oracle
+        cel.makespan_model(g, d, o, dv, 1, tmul=[65536, 1024])
+    assert ei.value.code == -3
+    with pytest.raises(O.OracleError):
+        O.makespan_model(huge, [0, 1], [0, 1], 1, tmul=[65536, 1024])
+
+
+def test_hetero_transformer96():
+    """Full size: two device speeds, faster links inside pairs of devices."""
+    wl = make_config(4, 0)
+    D = wl.D
+    tmul = [1024 if x < D // 2 else 2048 for x in range(D)]
+    bw = [[2 * wl.bw if x // 2 == y // 2 else wl.bw for y in range(D)] for x in range(D)]
+    lat = [[wl.lat // 2 if x // 2 == y // 2 else wl.lat for y in range(D)] for x in range(D)]
+    ocpd = oracle_cpd(wl)
+    cid, C, _ = O.cluster(wl, ocpd, 200, -1)
+    lev, oid, lp, L = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    check_model(wl, pr, O.place(wl, cid, C)[1], tmul=tmul, bw=bw, lat=lat)
+
+
+def check_colocate(wl, order, grp, G, P):
+    ref = O.colocate(wl, order, grp, G, P)
+    g, _ = up(wl)
+    got = tt(P, np.uint8)
+    cel.colocate(g, tt(order, np.int32), tt(grp, np.int32), G, got)
+    assert np.array_equal(np_(got), ref)
+
+
+def test_colocate():
+    import json
+    import os
+    case = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                       "colocate_hand.json")))["cases"][0]
+    wl = from_edges(case["n"], case["edges"], [1] * case["n"], [0] * case["n"], 4, [9] * 4, 1, 0)
+    g, _ = up(wl)
+    nd = tt(case["dev_in"], np.uint8)
+    cel.colocate(g, tt(case["order"], np.int32), tt(case["group"], np.int32), case["n_groups"], nd)
+    assert np_(nd).tolist() == case["dev_out"]
+    rng = np.random.default_rng(53)
+    for cfg in (1, 3):
+        wl, rt, rb = config(cfg, 0)
+        for G in (1, 37, wl.n // 3):
+            grp = rng.integers(-1, G, wl.n).astype(np.int32)
+            check_colocate(wl, rb[2], grp, G, random_placements(wl, 3, G))
+    check_colocate(wl, rb[2], np.full(wl.n, -1, np.int32), 0, random_placements(wl, 1, 1))
+    g, _ = up(wl)
+    with pytest.raises(cel.CelError) as ei:
+        cel.colocate(g, tt(rb[2], np.int32), tt(np.full(wl.n, 5, np.int32), np.int32), 5,
+                     tt(random_placements(wl, 1, 1), np.uint8))
+    assert ei.value.code == -1
