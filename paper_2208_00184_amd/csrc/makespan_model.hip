@@ -6,28 +6,34 @@
 // holds one of its successors, in increasing device order, occupying the
 // producer device's send channel and the target device's receive channel.
 //
-// Under either model a node's start depends on everything placed before it in
-// the order, so a placement is a sequential walk.  One wave walks one
+// Under either model a node's start depends on everything placed before it on
+// its device, so a placement is a walk in order.  One wave walks one
 // placement, 64 consecutive positions (a window) at a time:
 //  A. lane j folds slot j's inputs from before the window (finish times, or
 //     arrivals of transfers: final by now) into a partial ready time, marks
 //     its in-window predecessors in a 64-bit mask, and loads its own w, c,
 //     device and destination-device mask.  Rows with many inputs are folded
 //     by the whole wave.
-//  B. the wave steps through the slots with uniform control flow: a slot's
-//     values and its in-window inputs come from other lanes by readlane;
-//     device d's state (free time or end of its last task, idle-gap count,
-//     channel free times) lives in lane d.  Only the gap search and the
-//     transfer arrivals touch memory.
+//  B. the window splits into segments, runs of consecutive slots with no
+//     edge among them, taken in order.  A segment's slots add their inputs
+//     from earlier segments (shuffles), then are placed: with FIFO devices
+//     by one segmented max-plus scan over the slots sorted by (device,
+//     position); with insertion by lane d for device d's slots, in order.
+//     Device d's state (free time or end of its last task, gap count and
+//     ring head, channel free times) lives in lane d.  The segment's
+//     transfers are then issued in slot order.
 //  C. the window's finish times are stored.
 //
 // Idle gaps: device d keeps the idle intervals before its last task, sorted,
-// in its own segment of a per-placement array (a task adds at most one gap,
-// so the segment holds as many entries as d has nodes).  A node ready at or
-// after the last gap's end goes after the device's last task with no search;
-// otherwise the wave loads 64 gaps at a time, walking back from the end to the
-// first gap that ends after the ready time, and takes the first gap from
-// there that holds the node (ballot), then shrinks, splits or empties it.
+// in its segment of a per-placement global array (a task adds at most one gap,
+// so the segment holds as many entries as d has nodes), and its newest 64
+// again in an LDS ring (written through to the array).  A node ready at or
+// after the last gap's end goes after the device's last task with no search.
+// Otherwise the wave reads the ring, one gap per lane, and takes the first gap
+// that holds the node (ballot); only when the ring's oldest gap already ends
+// after the ready time can an older gap hold it, and then the wave walks the
+// global segment first, 64 gaps per round trip.  The chosen gap shrinks,
+// splits or empties.
 // Transfers: a producer's destination devices form a mask; its arrivals sit
 // in a pool at off[p] + (rank of the device in the mask).
 // Heterogeneous devices (HET): device d runs a node of w in ceil(w tmul[d] /
@@ -139,106 +145,266 @@ __device__ inline void fold_inputs(const MmArgs &a, const uint8_t *dev, const in
   }
 }
 
-// First-fit slot of a node (w > 0, ready r) on device dj, whose gap segment
-// starts at A / B; L, G, gl are the device's last end, gap count and last
-// gap end (uniform), updated in place.  Returns the start.
-__device__ inline int64_t insert_slot(int64_t *A, int64_t *B, int64_t r, int64_t w, int64_t &L,
-                                      int32_t &G, int64_t &gl, int lane) {
+constexpr int kTail = 64;  // most recent idle gaps of each device kept in LDS
+
+// Device d's idle gaps: the full sorted list in global memory (A / B [0, G),
+// written through), and its newest t = min(G, kTail) entries again in an LDS
+// ring (ta / tb), logical tail index i at slot (h + i) mod kTail.
+
+// Appends the idle gap [a, b) after the G gaps.
+__device__ inline void gap_append(int64_t *A, int64_t *B, int64_t *ta, int64_t *tb, int32_t G,
+                                  int32_t &h, int64_t a, int64_t b, int lane) {
+  const int32_t slot = G < kTail ? G : h;  // a full ring overwrites its oldest gap
+  if (lane == 0) {
+    A[G] = a;
+    B[G] = b;
+    ta[slot] = a;
+    tb[slot] = b;
+  }
+  if (G >= kTail) h = (h + 1) & (kTail - 1);
+  lds_order();
+}
+
+// First-fit slot of a node (w > 0, ready r); L, G, gl, h are the device's
+// last end, gap count, last gap end and ring head (uniform), updated in
+// place.  Returns the start.
+__device__ inline int64_t insert_slot(int64_t *A, int64_t *B, int64_t *ta, int64_t *tb, int64_t r,
+                                      int64_t w, int64_t &L, int32_t &G, int64_t &gl, int32_t &h,
+                                      int lane) {
   if (G == 0 || r >= gl) {  // no idle gap ends after r: go after the last task
     const int64_t s = r > L ? r : L;
     if (s > L) {
-      if (lane == 0) {
-        A[G] = L;
-        B[G] = s;
-      }
+      gap_append(A, B, ta, tb, G, h, L, s, lane);
       G++;
       gl = s;
     }
     L = s + w;
     return s;
   }
-  // gaps stored by earlier steps must be visible to this wave's loads
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
-  // walk back to the chunk holding the first gap that ends after r
-  int32_t lo = G > 64 ? G - 64 : 0;
-  int64_t ca, cb;
-  for (;;) {
-    const int32_t i = lo + lane;
-    ca = cb = 0;
-    if (i < G) {
-      ca = A[i];
-      cb = B[i];
-    }
-    if (lo == 0 || !(__builtin_amdgcn_readfirstlane((int32_t)(cb > r)))) break;
-    lo = lo > 64 ? lo - 64 : 0;
+  const int32_t t = G < kTail ? G : kTail, g0 = G - t;
+  int64_t ca = 0, cb = 0;  // the tail in logical order, one gap per lane
+  if (lane < t) {
+    const int slot = (h + lane) & (kTail - 1);
+    ca = ta[slot];
+    cb = tb[slot];
   }
-  // scan forward from there for the first gap that holds [max(start, r), + w)
   int32_t q = -1;
   int64_t qa = 0, qb = 0;
-  for (;;) {
-    const int32_t i = lo + lane;
-    const int64_t t = ca > r ? ca : r;
-    const uint64_t fit = __ballot(i < G && cb > r && t + w <= cb);
-    if (fit) {
-      const int l = __builtin_ctzll(fit);
-      q = lo + l;
-      qa = readlane64(ca, l);
-      qb = readlane64(cb, l);
-      break;
+  bool glob = false;
+  if (g0 > 0 && readlane64(cb, 0) > r) {
+    // the tail's oldest gap ends after r: an older one may hold the node.
+    // Gaps stored by earlier steps must be visible here.
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+    CEL_TCOUNT(5);
+    int32_t lo = g0 > 64 ? g0 - 64 : 0;
+    int64_t ga_ = 0, gb_ = 0;
+    for (;;) {  // walk back to the chunk holding the first gap that ends after r
+      const int32_t i = lo + lane;
+      ga_ = gb_ = 0;
+      if (i < g0) {
+        ga_ = A[i];
+        gb_ = B[i];
+      }
+      if (lo == 0 || !(__builtin_amdgcn_readfirstlane((int32_t)(gb_ > r)))) break;
+      lo = lo > 64 ? lo - 64 : 0;
+      CEL_TCOUNT(6);
     }
-    lo += 64;
-    if (lo >= G) break;
-    ca = cb = 0;
-    if (lo + lane < G) {
-      ca = A[lo + lane];
-      cb = B[lo + lane];
+    for (;;) {  // scan forward, over the gaps older than the tail, for one that holds it
+      const int32_t i = lo + lane;
+      const int64_t x = ga_ > r ? ga_ : r;
+      const uint64_t fit = __ballot(i < g0 && gb_ > r && x + w <= gb_);
+      if (fit) {
+        const int l = __builtin_ctzll(fit);
+        q = lo + l;
+        qa = readlane64(ga_, l);
+        qb = readlane64(gb_, l);
+        glob = true;
+        break;
+      }
+      lo += 64;
+      if (lo >= g0) break;
+      CEL_TCOUNT(7);
+      ga_ = gb_ = 0;
+      if (lo + lane < g0) {
+        ga_ = A[lo + lane];
+        gb_ = B[lo + lane];
+      }
+    }
+  }
+  if (q < 0) {  // the tail
+    const int64_t x = ca > r ? ca : r;
+    const uint64_t fit = __ballot(lane < t && cb > r && x + w <= cb);
+    if (fit) {
+      q = __builtin_ctzll(fit);
+      qa = readlane64(ca, q);
+      qb = readlane64(cb, q);
     }
   }
   if (q < 0) {  // none holds it: after the last task (r < gl <= L)
+    CEL_TCOUNT(10);
     const int64_t s = L;
     L = s + w;
     return s;
   }
   const int64_t s = qa > r ? qa : r, e = s + w;
   const bool left = s > qa, right = e < qb;
-  if (left && right) {  // split: move gaps q+1 .. G-1 up by one, top chunk first
-    for (int32_t hi = G; hi > q + 1;) {
-      const int32_t l0 = hi - 64 > q + 1 ? hi - 64 : q + 1;
-      const int32_t i = l0 + lane;
-      int64_t xa = 0, xb = 0;
-      if (i < hi) {
-        xa = A[i];
-        xb = B[i];
+  if (glob) {  // a gap older than the tail (global only)
+    if (left && right) {  // split: move gaps q+1 .. G-1 up by one, top chunk first
+      for (int32_t hi = G; hi > q + 1;) {
+        const int32_t l0 = hi - 64 > q + 1 ? hi - 64 : q + 1;
+        const int32_t i = l0 + lane;
+        int64_t xa = 0, xb = 0;
+        if (i < hi) {
+          xa = A[i];
+          xb = B[i];
+        }
+        if (i < hi) {
+          A[i + 1] = xa;
+          B[i + 1] = xb;
+        }
+        hi = l0;
+        CEL_TCOUNT(9);
       }
-      if (i < hi) {
-        A[i + 1] = xa;
-        B[i + 1] = xb;
+      if (lane == 0) {
+        B[q] = s;
+        A[q + 1] = e;
+        B[q + 1] = qb;
       }
-      hi = l0;
+      G++;  // the newest t gaps, and so the ring, are unchanged
+      CEL_TCOUNT(8);
+    } else if (left) {
+      if (lane == 0) B[q] = s;
+    } else if (right) {
+      if (lane == 0) A[q] = e;
+    } else {  // filled exactly: leave an empty gap [qb, qb)
+      if (lane == 0) A[q] = qb;
     }
-    if (lane == 0) {
-      B[q] = s;
-      A[q + 1] = e;
-      B[q + 1] = qb;
+    return s;
+  }
+  if (left && right) {  // split inside the tail: t + 1 gaps, the oldest leaves a full ring
+    const int drop = t == kTail ? 1 : 0;
+    const int k = lane + drop;  // lane i takes gap k of the new sequence (global g0 + k)
+    const int src = k < q ? k : k - 1;
+    const int64_t xa = __shfl(ca, src < 0 ? 0 : src), xb = __shfl(cb, src < 0 ? 0 : src);
+    int64_t na = xa, nb = xb;
+    if (k == q) {
+      na = qa;
+      nb = s;
+    } else if (k == q + 1) {
+      na = e;
+      nb = qb;
     }
+    const int32_t h2 = (h + drop) & (kTail - 1);
+    if (lane < t + 1 - drop) {
+      const int slot = (h2 + lane) & (kTail - 1);
+      ta[slot] = na;
+      tb[slot] = nb;
+      if (k >= q) {  // write the changed part through
+        A[g0 + k] = na;
+        B[g0 + k] = nb;
+      }
+    }
+    if (drop && q == 0 && lane == 0) {  // the dropped gap is the split's first part
+      A[g0] = qa;
+      B[g0] = s;
+    }
+    lds_order();
+    h = h2;
     G++;
-  } else if (left) {  // the node ends the gap
-    if (lane == 0) B[q] = s;
-    if (q == G - 1) gl = s;
-  } else if (right) {  // the node starts the gap
-    if (lane == 0) A[q] = e;
-  } else {  // filled exactly: leave an empty gap [qb, qb)
-    if (lane == 0) A[q] = qb;
+    CEL_TCOUNT(8);
+  } else {
+    const int slot = (h + q) & (kTail - 1);
+    if (left) {  // the node ends the gap
+      if (lane == 0) {
+        tb[slot] = s;
+        B[g0 + q] = s;
+      }
+      if (q == t - 1) gl = s;
+    } else if (right) {  // the node starts the gap
+      if (lane == 0) {
+        ta[slot] = e;
+        A[g0 + q] = e;
+      }
+    } else {  // filled exactly: leave an empty gap [qb, qb)
+      if (lane == 0) {
+        ta[slot] = qb;
+        A[g0 + q] = qb;
+      }
+    }
+    lds_order();
   }
   return s;
+}
+
+// First fit run by the lane that holds the device (its own state, its own
+// gap segment and ring).  Returns false, leaving everything unchanged, when
+// the whole wave must place the node: a split, which moves the ring, or a
+// ring whose oldest gap already ends after r, so that an older gap may hold it.
+__device__ inline bool lane_insert(int64_t *A, int64_t *B, int64_t *ta, int64_t *tb, int64_t r,
+                                   int64_t w, int64_t &L, int32_t &G, int64_t &gl, int32_t &h,
+                                   int64_t &s) {
+  if (w == 0) {
+    s = r;
+    return true;
+  }
+  if (G == 0 || r >= gl) {  // after the last task, maybe leaving a new gap
+    s = r > L ? r : L;
+    if (s > L) {
+      const int32_t slot = G < kTail ? G : h;
+      A[G] = L;
+      B[G] = s;
+      ta[slot] = L;
+      tb[slot] = s;
+      if (G >= kTail) h = (h + 1) & (kTail - 1);
+      G++;
+      gl = s;
+    }
+    L = s + w;
+    return true;
+  }
+  const int32_t t = G < kTail ? G : kTail, g0 = G - t;
+  if (g0 > 0 && tb[h] > r) return false;
+  int32_t lo = 0, hi = t - 1;  // first gap of the ring that ends after r (the last one does)
+  while (lo < hi) {
+    const int32_t mid = (lo + hi) >> 1;
+    if (tb[(h + mid) & (kTail - 1)] > r) hi = mid;
+    else lo = mid + 1;
+  }
+  for (int32_t i = lo; i < t; i++) {
+    const int sl = (h + i) & (kTail - 1);
+    const int64_t ga = ta[sl], gb = tb[sl], x = ga > r ? ga : r, e = x + w;
+    if (e > gb) continue;
+    const bool left = x > ga, right = e < gb;
+    if (left && right) return false;
+    if (left) {  // the node ends the gap
+      tb[sl] = x;
+      B[g0 + i] = x;
+      if (i == t - 1) gl = x;
+    } else if (right) {  // the node starts the gap
+      ta[sl] = e;
+      A[g0 + i] = e;
+    } else {  // filled exactly: an empty gap [gb, gb)
+      ta[sl] = gb;
+      A[g0 + i] = gb;
+    }
+    s = x;
+    return true;
+  }
+  s = L;  // none holds it: after the last task
+  L = s + w;
+  return true;
 }
 
 template <bool INS, bool TASKS, bool HET>
 __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
   __shared__ int64_t s_T[TASKS ? 64 * 64 : 1];  // arrival of slot j's output on device b
   __shared__ int32_t s_bw[HET ? kHetD * kHetD : 1], s_lat[HET ? kHetD * kHetD : 1];
+  __shared__ int64_t s_ta[INS ? 64 * kTail : 1], s_tb[INS ? 64 * kTail : 1];  // gap tails
+  __shared__ unsigned long long s_lst[64];  // slots of the segment by device
+  __shared__ int64_t s_fin[64];             // finish of the segment's slots
   if (failed(st)) return;
   const int lane = threadIdx.x;
+  s_lst[lane] = 0;
   int64_t tmr = 1024;  // device `lane`'s time multiplier
   if (HET) {
     for (int i = lane; i < a.D * a.D; i += 64) {
@@ -260,6 +426,7 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
   int32_t gcnt = 0;   // idle gaps stored
   int64_t glast = 0;  // end of the last stored gap
   int64_t gbase = INS && lane < a.D ? a.goff[k * a.D + lane] : 0;
+  int32_t ghead = 0;  // ring head of the gap tail
   int64_t snd = 0, rcv = 0, tcur = 0;
   int64_t span = 0;
   uint32_t bad = 0;
@@ -267,6 +434,7 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
     const int32_t nw = n - P0 < 64 ? n - P0 : 64;
     const int32_t p = P0 + lane;
     const bool act = lane < nw;
+    CEL_TSTAMP(t_a);
     int32_t dv = 0, i0 = 0, i1 = 0;
     int64_t w = 0, c = 0, ext = 0, myoff = 0;
     uint64_t msk = 0, mydm = 0;
@@ -303,46 +471,131 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
         msk = mk;
       }
     }
-    // B: the slots in order
+    // B: segments of consecutive slots with no edge among them, in order.
+    // Inside a segment every slot's ready time is known once the earlier
+    // segments are placed, and devices are independent but for the transfer
+    // channels: lane d places device d's slots of the segment in order, then
+    // the segment's transfers are issued in slot order.
+    CEL_TSTAMP(t_b);
+    CEL_TADD(0, t_a, t_b);
     int64_t finw = 0;
-    for (int j = 0; j < nw; j++) {
-      const int32_t dj = __builtin_amdgcn_readlane(dv, j);
-      const int64_t wj = HET ? dur_on(readlane64(w, j), readlane64(tmr, dj)) : readlane64(w, j);
-      int64_t r = readlane64(ext, j);
-      for (uint64_t mj = (uint64_t)readlane64((int64_t)msk, j); mj; mj &= mj - 1) {
-        const int q = __builtin_ctzll(mj);
-        const int32_t dq = __builtin_amdgcn_readlane(dv, q);
-        const int64_t fq = readlane64(finw, q);
-        int64_t t;
-        if (dq == dj) t = fq;
-        else if (TASKS) t = s_T[q * 64 + dj];
-        else if (HET) t = fq + link_c(readlane64(c, q), s_bw[dq * kHetD + dj], s_lat[dq * kHetD + dj]);
-        else t = fq + readlane64(c, q);
-        r = t > r ? t : r;
+    const int64_t wd = HET ? dur_on(w, __shfl(tmr, dv)) : w;  // slot duration on its device
+    for (int32_t s0 = 0; s0 < nw;) {
+      const uint64_t cut = __ballot(lane > s0 && lane < nw && (msk & ~below(s0)) != 0);
+      const int32_t s1 = cut ? __builtin_ctzll(cut) : nw;
+      const bool inseg = lane >= s0 && lane < s1;
+      CEL_TCOUNT(11);
+      int64_t r = ext;  // + inputs from the earlier segments of this window
+      for (uint64_t mm = inseg ? msk : 0; __ballot(mm != 0);) {
+        const bool has = mm != 0;
+        const int q = has ? __builtin_ctzll(mm) : lane;
+        mm &= mm - 1;
+        const int64_t fq = __shfl(finw, q), xq = __shfl(c, q);
+        const int32_t dq = __shfl(dv, q);
+        int64_t t = fq;
+        if (dq != dv) {
+          if (TASKS) t = s_T[q * 64 + dv];
+          else if (HET) t = fq + link_c(xq, s_bw[dq * kHetD + dv], s_lat[dq * kHetD + dv]);
+          else t = fq + xq;
+        }
+        if (has && t > r) r = t;
       }
-      int64_t s;
+      if (inseg) atomicOr(&s_lst[dv], 1ull << lane);
+      wave_lds_sync();
+      uint64_t mine = lane < a.D ? s_lst[lane] : 0;
       if (!INS) {
-        const int64_t L = readlane64(last, dj);
-        s = r > L ? r : L;
-        last = setlane<int64_t>(last, s + wj, dj);
-      } else if (wj == 0) {
-        s = r;
+        // FIFO devices: a device's chain last' = max(r, last) + w composes
+        // maps x -> max(r + w, x + w); with the segment's slots sorted by
+        // (device, position), one segmented max-plus scan places them all.
+        const int32_t cnt = __builtin_popcountll(mine);
+        int32_t inc = cnt;
+        for (int off = 1; off < 64; off <<= 1) {
+          const int32_t o = __shfl_up(inc, off);
+          if (lane >= off) inc += o;
+        }
+        const int32_t first = inc - cnt;  // lane d: where device d's slots start
+        int32_t rank = 0;
+        const int32_t fd = __shfl(first, dv);
+        if (inseg) {
+          rank = fd + __builtin_popcountll(s_lst[dv] & below(lane));
+          s_fin[rank] = lane;  // sorted position -> slot (s_fin reused as scratch)
+        }
+        wave_lds_sync();
+        const int32_t ns = s1 - s0;
+        const int32_t jj = lane < ns ? (int32_t)s_fin[lane] : lane;
+        const int32_t dd = __shfl(dv, jj);
+        const int64_t rr = __shfl(r, jj), ww = __shfl(wd, jj), l0 = __shfl(last, dd);
+        const int32_t dprev = __shfl_up(dd, 1);
+        int64_t ma = kNeg, mb = 0;
+        int32_t fl = 1;
+        if (lane < ns) {
+          ma = rr + ww;
+          mb = ww;
+          fl = lane == 0 || dprev != dd;
+        }
+        wave_seg_scan_dpp(ma, mb, fl);
+        const int64_t fs = ma > l0 + mb ? ma : l0 + mb;  // finish of sorted slot `lane`
+        const int64_t nl = __shfl(fs, cnt > 0 ? inc - 1 : 0);  // device `lane`'s last finish
+        if (lane < a.D && cnt > 0) last = nl;
+        const int64_t myf = __shfl(fs, rank);
+        if (inseg) finw = myf;
+        lds_order();
+        s_lst[lane] = 0;
+        mine = 0;
       } else {
-        int64_t L = readlane64(last, dj), gl = readlane64(glast, dj);
-        int32_t G = __builtin_amdgcn_readlane(gcnt, dj);
-        const int64_t base = readlane64(gbase, dj);
-        s = insert_slot(a.ga + base, a.gb + base, r, wj, L, G, gl, lane);
-        last = setlane<int64_t>(last, L, dj);
-        glast = setlane<int64_t>(glast, gl, dj);
-        gcnt = setlane<int32_t>(gcnt, G, dj);
+        lds_order();
+        s_lst[lane] = 0;
       }
-      const int64_t f = s + wj;
-      finw = setlane<int64_t>(finw, f, j);
-      span = f > span ? f : span;
-      if (TASKS) {
-        const uint64_t dmj = (uint64_t)readlane64((int64_t)mydm, j);
-        if (dmj) {
-          const int64_t cj = readlane64(c, j);
+      while (__ballot(mine != 0)) {
+        const bool has = mine != 0;
+        const int j = has ? __builtin_ctzll(mine) : lane;
+        mine &= mine - 1;
+        const int64_t rj = __shfl(r, j), wj = __shfl(wd, j);
+        CEL_TCOUNT(12);
+        int64_t f = 0;
+        bool done = true;
+        if (has) {
+          if (!INS) {
+            last = (rj > last ? rj : last) + wj;
+            f = last;
+          } else {
+            int64_t s_;
+            done = lane_insert(a.ga + gbase, a.gb + gbase, s_ta + lane * kTail,
+                               s_tb + lane * kTail, rj, wj, last, gcnt, glast, ghead, s_);
+            f = s_ + wj;
+          }
+        }
+        if (INS) {
+          lds_order();
+          for (uint64_t dl = __ballot(has && !done); dl; dl &= dl - 1) {  // the whole wave
+            const int d = __builtin_ctzll(dl);
+            CEL_TCOUNT(13);
+            const int64_t rr = readlane64(rj, d), ww = readlane64(wj, d);
+            int64_t L = readlane64(last, d), gl = readlane64(glast, d);
+            int32_t G = __builtin_amdgcn_readlane(gcnt, d), hd = __builtin_amdgcn_readlane(ghead, d);
+            const int64_t base = readlane64(gbase, d);
+            const int64_t s_ = insert_slot(a.ga + base, a.gb + base, s_ta + d * kTail,
+                                           s_tb + d * kTail, rr, ww, L, G, gl, hd, lane);
+            last = setlane<int64_t>(last, L, d);
+            glast = setlane<int64_t>(glast, gl, d);
+            gcnt = setlane<int32_t>(gcnt, G, d);
+            ghead = setlane<int32_t>(ghead, hd, d);
+            f = setlane<int64_t>(f, s_ + ww, d);
+          }
+        }
+        if (has) s_fin[j] = f;
+      }
+      if (INS) {
+        wave_lds_sync();
+        if (inseg) finw = s_fin[lane];
+        lds_order();
+      }
+      if (TASKS) {  // the segment's transfers in slot order
+        for (uint64_t pm = __ballot(inseg && mydm != 0); pm; pm &= pm - 1) {
+          const int j = __builtin_ctzll(pm);
+          const int32_t dj = __builtin_amdgcn_readlane(dv, j);
+          const int64_t f = readlane64(finw, j), cj = readlane64(c, j);
+          const uint64_t dmj = (uint64_t)readlane64((int64_t)mydm, j);
           int64_t sf = readlane64(snd, dj);
           for (uint64_t x = dmj; x; x &= x - 1) {
             const int b = __builtin_ctzll(x);
@@ -361,11 +614,22 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
           lds_order();
         }
       }
+      s0 = s1;
     }
+    if (act) span = finw > span ? finw : span;
     // C: finish times of the window
+    CEL_TSTAMP(t_c);
+    CEL_TADD(1, t_b, t_c);
     if (act) fin[p] = finw;
     // the next window reads these finish times and arrivals
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+    CEL_TSTAMP(t_d);
+    CEL_TADD(2, t_c, t_d);
+    CEL_TCOUNT(3);
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const int64_t o = __shfl_xor(span, off);
+    span = o > span ? o : span;
   }
   if (lane == 0) a.makespan[k] = span;
   if (bad) raise_err(st, bad);
@@ -667,6 +931,8 @@ extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, cons
   if (hs.err) return status_error(hs, fn);
   return CEL_OK;
 }
+
+CEL_PHASE_READER(cel_debug_phases_model)
 
 extern "C" int cel_colocate(const cel_graph *g, const int32_t *order, const int32_t *group,
                             int32_t n_groups, int32_t K, uint8_t *node_dev, hipStream_t s) {
