@@ -292,6 +292,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-models", action="store_true",
+                    help="skip the device-model rows (insertion, transfers as tasks, "
+                         "heterogeneous devices, co-location)")
     ap.add_argument("--no-batch", action="store_true",
                     help="skip the 1,024-candidate scoring row on the 200k-node DAG")
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
@@ -412,8 +415,10 @@ def main() -> int:
                   "k_tlevel_sweep_ms": ks_t.get("k_tlevel_sweep", (1, float("nan")))[1]}
 
     cpd_row, ndev_cpd = cpd_compare(cel, torch, g, d, bl_t, tl_t, pr_t, lev, lp, L)
-    print("[bench] device models", file=sys.stderr, flush=True)
-    model_row = models_row(cel, torch, g, d, pr_t, ndev_cpd, args.seed)
+    model_row = None
+    if not args.no_models:
+        print("[bench] device models", file=sys.stderr, flush=True)
+        model_row = models_row(cel, torch, g, d, pr_t, ndev_cpd, args.seed)
 
     batch5 = None if args.no_batch else batched_row(cel, torch, dev, args)
 
