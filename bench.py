@@ -440,6 +440,19 @@ def main() -> int:
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
                 "traffic": load_traffic(dom), "algorithmic_bytes": B,
                 "ns_per_level": round(t_dom * 1e9 / L, 1)}
+    # depth-latency ceiling of the measured pass: b-level and makespan are chains
+    # of L dependent levels each; a level cannot take less than the dependent
+    # step measured by a one-wave probe on this GPU (a dependent LDS round trip
+    # plus a 6-step DPP prefix max, about 150 ns), so the pass cannot beat 2 L
+    # such steps whatever the bandwidth
+    t_level_ns = 150.0
+    B_pass = algorithmic_bytes("k_blevel_sweep", n, m, 1) + algorithmic_bytes("k_makespan_sweep",
+                                                                              n, m, 1)
+    floor_s = 2 * L * t_level_ns * 1e-9
+    roofline["depth_ceiling"] = {
+        "t_level_ns": t_level_ns, "levels": L, "pass_floor_ms": round(floor_s * 1e3, 3),
+        "frac_ceiling": round(B_pass / floor_s / 1e9 / HBM_PEAK_GBS, 5),
+        "frac_pass": round(B_pass / (eval_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 6)}
     # the level sweeps are chains of L dependent levels: per-level latency
     per_level = {k: round(kernels[k]["avg_ms"] * 1e6 / L, 1)
                  for k in ("k_kahn", "k_blevel_sweep", "k_makespan_sweep", "k_makespan_batch")
@@ -457,20 +470,54 @@ def main() -> int:
 
     cpu = None
     if not args.no_cpu:
+        # the oracle as it stands, one thread pinned to one core, every stage of
+        # the path on the same graph (median of 3)
         from oracle import oracle as O
-        lev, oid, lp, L_ = O.topo_levels(wl)
-        reps, t_cpu = 0, 0.0
-        while t_cpu < 10.0 and reps < 5:
-            a = time.perf_counter()
-            _, _, pr, _ = O.blevel(wl, lev, oid)
-            O.makespan(wl, pr, np.zeros(n, np.uint8), want_times=False)
-            t_cpu += time.perf_counter() - a
-            reps += 1
-        cpu = {"value": m / (t_cpu / reps), "unit": "edges/s", "cores": 1, "kind": "oracle",
-               "sample": f"b-level (with priority order) + single-placement makespan on the "
-                         f"full {n}-node graph, {reps} reps, single-threaded C"}
-        print(f"[bench] cpu oracle {t_cpu / reps * 1e3:.0f} ms per pass", file=sys.stderr,
-              flush=True)
+        import statistics
+        aff = os.sched_getaffinity(0)
+        os.sched_setaffinity(0, {min(aff)})
+        st_cpu = {}
+
+        def tm(name, f, reps=3):
+            ts, r = [], None
+            for _ in range(reps):
+                a = time.perf_counter()
+                r = f()
+                ts.append(time.perf_counter() - a)
+            st_cpu[name] = round(statistics.median(ts) * 1e3, 1)
+            return r
+
+        try:
+            lev_o, oid_o, _, _ = tm("topo_levels", lambda: O.topo_levels(wl))
+            _, _, pr_o, _ = tm("blevel", lambda: O.blevel(wl, lev_o, oid_o))
+            cid_o, C_o, _ = tm("cluster", lambda: O.cluster(wl, pr_o, 200, -1))
+            pl_o = tm("place", lambda: O.place(wl, cid_o, C_o))
+            tm("makespan", lambda: O.makespan(wl, pr_o, pl_o[1], want_times=False))
+        finally:
+            os.sched_setaffinity(0, aff)
+        t_pass = (st_cpu["blevel"] + st_cpu["makespan"]) * 1e-3
+        model = ""
+        try:
+            with open("/proc/cpuinfo") as fh:
+                model = next(line.split(":", 1)[1].strip() for line in fh
+                             if line.startswith("model name"))
+        except (OSError, StopIteration):
+            pass
+        cpu = {"value": m / t_pass, "unit": "edges/s", "cores": 1, "kind": "oracle",
+               "sample": f"b-level (with priority order) + makespan of the Adjusting Placement on "
+                         f"the full {n}-node graph, median of 3, single-threaded C pinned to one "
+                         f"core",
+               "stages_ms": st_cpu,
+               "placement_gen_ms": round(sum(st_cpu[k] for k in ("topo_levels", "blevel",
+                                                                  "cluster", "place")), 1),
+               "host": {"nproc": os.cpu_count(), "cpu_model": model,
+                        "oracle_cores": f"1 of {len(aff)}"}}
+        print(f"[bench] cpu oracle {t_pass * 1e3:.0f} ms per pass", file=sys.stderr, flush=True)
+
+    props = torch.cuda.get_device_properties(0)
+    device = {"name": props.name, "arch": getattr(props, "gcnArchName", ""),
+              "compute_units": props.multi_processor_count,
+              "memory_GB": round(props.total_memory / 1e9, 1), "hbm_peak_GBs": HBM_PEAK_GBS}
 
     out = {
         "metric": METRIC, "value": value, "unit": "edges/s", "n_gpus": 1,
@@ -485,6 +532,7 @@ def main() -> int:
         "stages_ms": stages,
         "kernels": kernels,
         "roofline": roofline,
+        "device": device,
         "ns_per_level": per_level,
         "tlevel": tlevel_row,
         "cpd_topo": cpd_row,
