@@ -137,7 +137,7 @@ __global__ void k_place_combine(int32_t C, const int32_t *boff, const uint64_t *
 }
 
 constexpr int kPlaceBlk = 5120;  // busy blocks held in LDS, shared evenly by the devices
-constexpr int kPlaceLds = 6144;  // clusters whose Fin and device are kept in LDS too
+constexpr int kPlaceLds = 8192;  // clusters whose Fin and device are kept in LDS too (161,792 B of LDS in all)
 
 __device__ inline void argmax_i64(int64_t &v, int32_t &i) {  // wave: largest v, then smallest i
   for (int off = 32; off > 0; off >>= 1) {

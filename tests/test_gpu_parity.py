@@ -556,7 +556,7 @@ def test_place_many_clusters_and_devices():
     share and the device choice takes the wave reductions."""
     wl, rt, rb = config(3, 0)
     cid, C, _ = O.cluster(wl, rb[2], 4, -1)
-    assert C > 6144
+    assert C > 8192
     check_place(wl, cid, C)
     for D in (80, 200):
         wl2 = make_random_dag(77 + D, 3000, p_edge=4.0 / 3000, D=D, cap_frac=(1, 3))
@@ -564,6 +564,15 @@ def test_place_many_clusters_and_devices():
         _, _, pr2, _ = O.blevel(wl2, lev2, oid2)
         cid2, C2, _ = O.cluster(wl2, pr2, 2, -1)
         check_place(wl2, cid2, C2)
+
+
+def test_place_cpd_transformer96():
+    """Full size: the CPD-TOPO clustering of transformer-96 (6,284 clusters), the
+    largest cluster counts whose finish times and devices stay in LDS."""
+    wl = make_config(4, 0)
+    cid, C, _ = O.cluster(wl, oracle_cpd(wl), 200, -1)
+    assert 6144 < C <= 8192
+    check_place(wl, cid, C)
 
 
 def test_place_rejects_bad_clusters():
