@@ -1029,3 +1029,16 @@ def test_colocate():
         cel.colocate(g, tt(rb[2], np.int32), tt(np.full(wl.n, 5, np.int32), np.int32), 5,
                      tt(random_placements(wl, 1, 1), np.uint8))
     assert ei.value.code == -1
+
+
+def test_model_many_placements():
+    """More placements than compute units in one call (K = 300, one wave each),
+    64 devices, every model; and K = 257 on config 1."""
+    rng = np.random.default_rng(61)
+    wl = make_random_dag(9100, 1500, p_edge=3.0 / 1500, D=64, multi=True, zero_frac=0.1)
+    order = random_topo_order(wl, rng)
+    P = rng.integers(0, 64, (300, wl.n)).astype(np.uint8)
+    check_model(wl, order, P)
+    wl, rt, rb = config(1, 0)
+    check_model(wl, rb[2], random_placements(wl, 257, 8), models=(cel.MODEL_INSERT,
+                                                                  cel.MODEL_COMM_TASKS))
