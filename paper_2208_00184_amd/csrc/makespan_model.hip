@@ -65,6 +65,7 @@ struct MmArgs {
   const int64_t *obp;          // ob by position (HET)
   const int64_t *tmul;         // [D] time multipliers, 1/1024 (HET)
   const int64_t *lbw, *llat;   // [D][D] links (HET)
+  const int4 *ipre;            // first 4 inputs of each position (-1 past the row's end)
 };
 
 constexpr int kHetD = 64;  // link table stride
@@ -93,6 +94,58 @@ __device__ inline uint64_t below(int b) { return (uint64_t(1) << b) - 1; }
 // on another device contributes f + c (contention-free) or, with transfers,
 // the arrival of its output on dv: pool[off + rank of dv in its mask].
 template <bool TASKS, bool HET>
+__device__ inline void fold_batch(const MmArgs &a, const uint8_t *dev, const int64_t *fin,
+                                  const uint64_t *dm, const int64_t *of, const int32_t *s_bw,
+                                  const int32_t *s_lat, int32_t P0, const int32_t (&q)[4],
+                                  int32_t dv, int64_t &ext, uint64_t &msk, uint32_t &bad) {
+  int64_t f[4], x[4];
+  int32_t dq[4];
+#pragma unroll
+  for (int u = 0; u < 4; u++) {  // first round: all loads that need only q
+    dq[u] = dv;
+    f[u] = x[u] = 0;
+    if (q[u] >= 0 && q[u] < P0) {
+      dq[u] = dev[q[u]];
+      f[u] = fin[q[u]];
+      if (TASKS) {  // -1: dv missing from the mask (CSR and CSC disagree)
+        const uint64_t mq = dm[q[u]];
+        x[u] = (mq >> dv) & 1 ? of[q[u]] + __builtin_popcountll(mq & below(dv)) : -1;
+      } else {
+        x[u] = HET ? a.obp[q[u]] : a.cq[q[u]];
+      }
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < 4; u++) {  // second round: arrivals of transfers
+    if (q[u] < 0) continue;
+    if (q[u] >= P0) {
+      msk |= uint64_t(1) << (q[u] - P0);
+      continue;
+    }
+    int64_t t;
+    if (dq[u] == dv) {
+      t = f[u];
+    } else if (TASKS) {
+      if (x[u] < 0) {
+        bad |= EB_ARG;
+        continue;
+      }
+      t = a.pool[x[u]];
+    } else if (HET) {
+      t = f[u] + link_c(x[u], s_bw[dq[u] * kHetD + dv], s_lat[dq[u] * kHetD + dv]);
+    } else {
+      t = f[u] + x[u];
+    }
+    ext = t > ext ? t : ext;
+  }
+}
+
+// Ready-time contribution of the inputs iidx[e] for e = e0, e0 + step, ...
+// < e1 of a node on device dv: inputs before the window (position < P0) are
+// folded into ext, the others marked in msk (bit = position - P0).  An input
+// on another device contributes f + c (contention-free) or, with transfers,
+// the arrival of its output on dv: pool[off + rank of dv in its mask].
+template <bool TASKS, bool HET>
 __device__ inline void fold_inputs(const MmArgs &a, const uint8_t *dev, const int64_t *fin,
                                    const uint64_t *dm, const int64_t *of, const int32_t *s_bw,
                                    const int32_t *s_lat, int32_t P0, int32_t e0, int32_t e1,
@@ -102,46 +155,7 @@ __device__ inline void fold_inputs(const MmArgs &a, const uint8_t *dev, const in
     int32_t q[4];
 #pragma unroll
     for (int u = 0; u < 4; u++) q[u] = e + u * step < e1 ? a.iidx[e + u * step] : -1;
-    int64_t f[4], x[4];
-    int32_t dq[4];
-#pragma unroll
-    for (int u = 0; u < 4; u++) {  // first round: all loads that need only q
-      dq[u] = dv;
-      f[u] = x[u] = 0;
-      if (q[u] >= 0 && q[u] < P0) {
-        dq[u] = dev[q[u]];
-        f[u] = fin[q[u]];
-        if (TASKS) {  // -1: dv missing from the mask (CSR and CSC disagree)
-          const uint64_t mq = dm[q[u]];
-          x[u] = (mq >> dv) & 1 ? of[q[u]] + __builtin_popcountll(mq & below(dv)) : -1;
-        } else {
-          x[u] = HET ? a.obp[q[u]] : a.cq[q[u]];
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 4; u++) {  // second round: arrivals of transfers
-      if (q[u] < 0) continue;
-      if (q[u] >= P0) {
-        msk |= uint64_t(1) << (q[u] - P0);
-        continue;
-      }
-      int64_t t;
-      if (dq[u] == dv) {
-        t = f[u];
-      } else if (TASKS) {
-        if (x[u] < 0) {
-          bad |= EB_ARG;
-          continue;
-        }
-        t = a.pool[x[u]];
-      } else if (HET) {
-        t = f[u] + link_c(x[u], s_bw[dq[u] * kHetD + dv], s_lat[dq[u] * kHetD + dv]);
-      } else {
-        t = f[u] + x[u];
-      }
-      ext = t > ext ? t : ext;
-    }
+    fold_batch<TASKS, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, q, dv, ext, msk, bad);
   }
 }
 
@@ -430,29 +444,55 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
   int64_t snd = 0, rcv = 0, tcur = 0;
   int64_t span = 0;
   uint32_t bad = 0;
+  // A slot's own values and its first 4 inputs depend on nothing computed
+  // here: they are loaded for the next window while this one is placed.
+  int32_t nx_dv = 0, nx_i0 = 0, nx_i1 = 0, nx_q[4] = {-1, -1, -1, -1};
+  int64_t nx_w = 0, nx_c = 0, nx_off = 0;
+  uint64_t nx_dm = 0;
+  auto load_own = [&](int32_t P) {
+    const int32_t q = P + lane;
+    nx_dv = nx_i0 = nx_i1 = 0;
+    nx_w = nx_c = nx_off = 0;
+    nx_dm = 0;
+    nx_q[0] = nx_q[1] = nx_q[2] = nx_q[3] = -1;
+    if (q < n) {
+      nx_dv = dev[q];
+      nx_w = a.wp[q];
+      nx_c = HET ? a.obp[q] : a.cq[q];  // ob under HET: the comm depends on the link
+      nx_i0 = a.iptr[q];
+      nx_i1 = a.iptr[q + 1];
+      const int4 f4 = a.ipre[q];
+      nx_q[0] = f4.x;
+      nx_q[1] = f4.y;
+      nx_q[2] = f4.z;
+      nx_q[3] = f4.w;
+      if (TASKS) {
+        nx_dm = dm[q];
+        nx_off = of[q];
+      }
+    }
+  };
+  load_own(0);
   for (int32_t P0 = 0; P0 < n; P0 += 64) {
     const int32_t nw = n - P0 < 64 ? n - P0 : 64;
     const int32_t p = P0 + lane;
     const bool act = lane < nw;
     CEL_TSTAMP(t_a);
-    int32_t dv = 0, i0 = 0, i1 = 0;
-    int64_t w = 0, c = 0, ext = 0, myoff = 0;
-    uint64_t msk = 0, mydm = 0;
-    if (act) {
-      dv = dev[p];
-      w = a.wp[p];
-      c = HET ? a.obp[p] : a.cq[p];  // ob under HET: the comm depends on the link
-      i0 = a.iptr[p];
-      i1 = a.iptr[p + 1];
-      if (TASKS) {
-        mydm = dm[p];
-        myoff = of[p];
-      }
-    }
+    const int32_t dv = nx_dv, i0 = nx_i0, i1 = nx_i1;
+    const int64_t w = nx_w, c = nx_c, myoff = nx_off;
+    const uint64_t mydm = nx_dm;
+    int32_t q4[4];
+#pragma unroll
+    for (int u = 0; u < 4; u++) q4[u] = nx_q[u];
+    int64_t ext = 0;
+    uint64_t msk = 0;
     // A: inputs from before the window
     const bool heavy = i1 - i0 > kMmLight;
-    if (!heavy)
-      fold_inputs<TASKS, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, i0, i1, 1, dv, ext, msk, bad);
+    if (!heavy) {
+      fold_batch<TASKS, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, q4, dv, ext, msk, bad);
+      fold_inputs<TASKS, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, i0 + 4, i1, 1, dv, ext, msk,
+                              bad);
+    }
     for (uint64_t hv = __ballot(heavy); hv; hv &= hv - 1) {
       const int h = __builtin_ctzll(hv);
       const int32_t e0 = __builtin_amdgcn_readlane(i0, h), e1 = __builtin_amdgcn_readlane(i1, h);
@@ -478,6 +518,7 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
     // the segment's transfers are issued in slot order.
     CEL_TSTAMP(t_b);
     CEL_TADD(0, t_a, t_b);
+    load_own(P0 + 64);
     int64_t finw = 0;
     const int64_t wd = HET ? dur_on(w, __shfl(tmr, dv)) : w;  // slot duration on its device
     for (int32_t s0 = 0; s0 < nw;) {
@@ -633,6 +674,19 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
   }
   if (lane == 0) a.makespan[k] = span;
   if (bad) raise_err(st, bad);
+}
+
+// First 4 inputs of each position (position space, -1 past the row's end),
+// so that a window's inputs load with its other per-slot values.
+__global__ void k_mm_ipre(int32_t n, const int32_t *iptr, const int32_t *iidx, int4 *ipre,
+                          const Status *st) {
+  if (failed(st)) return;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t e0 = iptr[p], e1 = iptr[p + 1];
+    ipre[p] = make_int4(e0 < e1 ? iidx[e0] : -1, e0 + 1 < e1 ? iidx[e0 + 1] : -1,
+                        e0 + 2 < e1 ? iidx[e0 + 2] : -1, e0 + 3 < e1 ? iidx[e0 + 3] : -1);
+  }
 }
 
 // Per placement, nodes per device (gap segment sizes); blocks take chunks of
@@ -839,7 +893,11 @@ extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, cons
                                                     het ? 0 : d->lat, wp, cq, st);
   const int gx = grid_for(n, 256, 1024), gy = K < 1024 ? K : 1024;
   k_dev_gather<<<dim3(gx, gy), 256, 0, s>>>(K, n, order, node_dev, D, devp, st);
+  int4 *ipre;
+  CEL_TRY(sc.get(&ipre, n));
+  k_mm_ipre<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, iptr, iidx, ipre, st);
   MmArgs a{};
+  a.ipre = ipre;
   a.n = n;
   a.D = D;
   a.iptr = iptr;
