@@ -9,8 +9,9 @@
 //
 // The recurrence is sequential in j.  One workgroup runs it in blocks of 64
 // targets, one lane per target:
-//  * the candidates below the block ("old" ones, at most R) are split in
-//    chunks of 64 over waves 1..NW-1; each wave sweeps its candidates in
+//  * the candidates below the block ("old" ones, at most R) are split evenly
+//    over waves 1..NW-1 (about 16 each, up to 15 waves), in chunks of at most
+//    64; each wave sweeps its candidates in
 //    descending order, merging the block's edge list (sorted by source,
 //    descending), so that every lane keeps the running Int of its own target
 //    and a running (min, argmin); per-wave offsets are added afterwards;
@@ -203,7 +204,7 @@ __global__ void __launch_bounds__(64)
 constexpr int kRing = 8192;  // LDS ring of H over positions (window R + 64 <= 4160)
 constexpr int kEC = 1024;    // staged edges of one block
 constexpr int kPF = 4;       // prefetched edges per thread of waves 1..NW-1
-constexpr int kMaxW = 7;     // candidate waves
+constexpr int kMaxW = 15;    // candidate waves
 
 __device__ inline int32_t rl32(int32_t v, int32_t l) { return __builtin_amdgcn_readlane(v, l); }
 __device__ inline int64_t rl64(int64_t v, int32_t l) {
@@ -553,7 +554,7 @@ __device__ inline void dp_inblock_runs(int64_t &best, uint64_t runs, int32_t j0,
 
 // The blocked DP.  blockDim = 64 * NW: wave 0 runs the in-block steps, waves
 // 1..NW-1 the candidates below the block.
-__global__ void __launch_bounds__(512)
+__global__ void __launch_bounds__(1024)
     k_cluster_dp(int32_t n, int32_t nb, const int32_t *lo, const int32_t *boff, const int32_t *eq,
                  const int32_t *et, const int64_t *ec, const int64_t *eE, const int64_t *PO,
                  int32_t *P, Status *st) {
@@ -663,12 +664,14 @@ __global__ void __launch_bounds__(512)
       const int w = wave - 1;
       int64_t best = kKeyInf, accS = 0;
       if (j0 > 0) {
+        // the candidates [lo0, j0), split evenly: wave w takes the w-th range
+        // from the top, in chunks of at most 64
         const int32_t lo0 = s_lo[buf][0];
-        const int32_t K = (j0 - lo0 + 63) >> 6;
-        const int32_t ka = w * K / W, kb = (w + 1) * K / W;
-        if (ka < kb) {
-          const int32_t top = j0 - 1 - 64 * ka;
-          const int32_t bot = j0 - 64 * kb > lo0 ? j0 - 64 * kb : lo0;
+        const int32_t Nc = j0 - lo0;
+        const int32_t sa = (int32_t)((int64_t)w * Nc / W), sb = (int32_t)((int64_t)(w + 1) * Nc / W);
+        if (sa < sb) {
+          const int32_t top = j0 - 1 - sa;
+          const int32_t bot = j0 - sb;
           int32_t kk = first_le(Q, cnt, top, lane);
           for (int32_t ct = top; ct >= bot; ct -= 64) {
             const int32_t cb = ct - 63 > bot ? ct - 63 : bot;
@@ -864,7 +867,7 @@ static int dp_blocked(int32_t n, int32_t m, int32_t R, const int32_t *lo, const 
     k_dp_fill<<<nb < 65535 ? nb : 65535, 256, 0, s>>>(n, nb, pptr, pidx, lo, cq, boff, eq, et, ec,
                                                       eE, st);
   }
-  const int32_t K = (R + 63) / 64;
+  const int32_t K = (R + 15) / 16;  // about 16 candidates per wave
   const int NW = 1 + (K < kMaxW ? K : kMaxW);
   {
     KTimer kt(s, "k_cluster_dp");
