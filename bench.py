@@ -15,9 +15,14 @@ the per-level latency of the level sweeps (a single placement of a graph
 10^4 levels deep is bound by it, not by HBM), the t-level pass (an optional
 output, timed apart), batched scoring of 1,024 perturbed placements of the
 200k-node layered DAG in one call (the bandwidth-bound regime), and the CPU
-oracle (one core) on the same 1.07M-node graph.
+oracle (one pinned core, every stage) on the same 1.07M-node graph.  Further
+rows: the CPD-TOPO order against the priority order, the CCR before and
+after fusion, Order-Place against Adjusting Placement, and the makespan under
+the device models (first-fit insertion, transfers as tasks, heterogeneous
+devices, co-location).
 
 Usage: python bench.py [--gpus 1] [--steps 5] [--warmup 2] [--no-cpu] [--no-batch]
+                       [--no-models]
 """
 from __future__ import annotations
 
