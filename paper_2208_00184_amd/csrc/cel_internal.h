@@ -336,8 +336,10 @@ int check_host_devices(const cel_devices *d, const char *fn);
 // (launchers; defined in common.hip)
 
 // Validates the graph arrays and, when `bound` is set, the overflow bound
-// sum(w) + sum over edges of c[src] < 2^62.  Fills indeg_scratch (n ints)
-// with in-degrees counted from the CSR.  Raises EB_ARG / EB_OVERFLOW in st.
+// sum(w) + sum over edges of c[src] < 2^62.  CSR and CSC must hold the same
+// edge multiset (compared by a hash total of the (source, target) pairs).
+// Fills indeg_scratch (n ints) with the in-degrees.  Raises EB_ARG /
+// EB_OVERFLOW in st.
 int check_graph(const cel_graph *g, int64_t bw, int64_t lat, bool bound, Status *st,
                 int32_t *indeg_scratch, Scratch &sc, hipStream_t s);
 

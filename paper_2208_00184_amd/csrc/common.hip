@@ -192,50 +192,81 @@ __device__ inline uint64_t mix64(uint64_t x) {  // SplitMix64 finaliser
   return x ^ (x >> 31);
 }
 
-// CSR pass over edge-balanced blocks: counts in-degrees and a per-target sum
-// of hashed source ids.
-__global__ void k_check_csr(cel_graph g, Status *st, int32_t *indeg, uint64_t *hsum) {
+// CSR and CSC must hold the same edge multiset.  Each side adds a 64-bit hash
+// of every (source, target) pair into one total (block sums, one atomic per
+// block); equal multisets give equal totals, and any difference is caught with
+// overwhelming probability.  The CSC pass also writes each node's in-degree.
+__device__ inline uint64_t pair_hash(int32_t u, int32_t v) {
+  return mix64(((uint64_t)(uint32_t)u << 32) | (uint32_t)v);
+}
+
+// failed(st) read once per block, so that every thread of the block returns
+// or none does (the kernels below reach block-wide barriers)
+__device__ inline bool block_failed(const Status *st, int *flag) {
+  if (threadIdx.x == 0) *flag = failed(st) ? 1 : 0;
+  __syncthreads();
+  return *flag != 0;
+}
+
+__device__ inline void block_add_u64(unsigned long long *dst, uint64_t x, uint64_t *red) {
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_down(x, off);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t t = 0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); i++) t += red[i];
+    if (t) atomicAdd(dst, (unsigned long long)t);
+  }
+}
+
+// CSR pass over edge-balanced blocks: target ranges and the pair-hash total.
+__global__ void k_check_csr(cel_graph g, Status *st, unsigned long long *hs) {
   __shared__ int32_t ptr[kRowsPB + 1], su[2];
-  if (failed(st)) return;  // row pointers not validated
+  __shared__ uint64_t red[16];
+  __shared__ int s_f;
+  if (block_failed(st, &s_f)) return;  // row pointers not validated
   const int32_t n = g.n;
   uint32_t bad = 0;
+  uint64_t acc = 0;
   for_edges_balanced(g.out_ptr, n, g.m, ptr, su, [&](int32_t u, int32_t e) {
     const int32_t t = g.out_idx[e];
     if (t < 0 || t >= n) {
       bad |= EB_ARG;
       return;
     }
-    atomicAdd(&indeg[t], 1);
-    atomicAdd((unsigned long long *)&hsum[t], (unsigned long long)mix64((uint64_t)u));
+    acc += pair_hash(u, t);
   });
   if (bad) raise_err(st, bad);
+  block_add_u64(&hs[0], acc, red);
 }
 
-// CSC pass: in-degree and hashed-source sum of every node must match the CSR's
-// (equal edge multisets give equal sums; a mismatch is caught with
-// overwhelming probability).
-__global__ void k_check_csc(cel_graph g, Status *st, const int32_t *indeg, const uint64_t *hsum) {
-  if (failed(st)) return;
+// CSC pass: source ranges, in-degrees and the pair-hash total.
+__global__ void k_check_csc(cel_graph g, Status *st, int32_t *indeg, unsigned long long *hs) {
+  __shared__ uint64_t red[16];
+  __shared__ int s_f;
+  if (block_failed(st, &s_f)) return;
   uint32_t bad = 0;
+  uint64_t acc = 0;
   for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < g.n;
        v += (int64_t)gridDim.x * blockDim.x) {
     const int32_t k0 = g.in_ptr[v], k1 = g.in_ptr[v + 1];
-    if (indeg[v] != k1 - k0) {
-      bad |= EB_ARG;
-      continue;
-    }
-    uint64_t h = 0;
+    indeg[v] = k1 - k0;
     for (int32_t k = k0; k < k1; k++) {
       const int32_t s = g.in_idx[k];
       if (s < 0 || s >= g.n) {
         bad |= EB_ARG;
         break;
       }
-      h += mix64((uint64_t)s);
+      acc += pair_hash(s, (int32_t)v);
     }
-    if (h != hsum[v]) bad |= EB_ARG;
   }
   if (bad) raise_err(st, bad);
+  block_add_u64(&hs[1], acc, red);
+}
+
+__global__ void k_check_pairs(const unsigned long long *hs, Status *st) {
+  if (failed(st)) return;
+  if (hs[0] != hs[1]) raise_err(st, EB_ARG);
 }
 
 // one block: saturating sum of the per-block partials
@@ -262,12 +293,12 @@ int check_graph(const cel_graph *g, int64_t bw, int64_t lat, bool bound, Status 
   CEL_TRY(sc.get(&part, nbk));
   k_check_nodes<<<nbk, B, 0, s>>>(*g, bw, lat, st, part);
   if (g->n > 0) {
-    uint64_t *hsum;
-    CEL_TRY(sc.get(&hsum, g->n));
-    CEL_HIP(hipMemsetAsync(indeg, 0, sizeof(int32_t) * (size_t)g->n, s));
-    CEL_HIP(hipMemsetAsync(hsum, 0, sizeof(uint64_t) * (size_t)g->n, s));
-    k_check_csr<<<edge_blocks(g->m), B, 0, s>>>(*g, st, indeg, hsum);
-    k_check_csc<<<grid_for(g->n, B, 4096), B, 0, s>>>(*g, st, indeg, hsum);
+    unsigned long long *hs;
+    CEL_TRY(sc.get(&hs, 2));
+    CEL_HIP(hipMemsetAsync(hs, 0, 2 * sizeof(unsigned long long), s));
+    k_check_csr<<<edge_blocks(g->m), B, 0, s>>>(*g, st, hs);
+    k_check_csc<<<grid_for(g->n, B, 4096), B, 0, s>>>(*g, st, indeg, hs);
+    k_check_pairs<<<1, 1, 0, s>>>(hs, st);
   }
   if (bound) k_finish_overflow<<<1, B, 0, s>>>(part, nbk, st);
   CEL_HIP(hipGetLastError());
