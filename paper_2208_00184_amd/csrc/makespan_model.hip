@@ -10,10 +10,11 @@
 // its device, so a placement is a walk in order.  One wave walks one
 // placement, 64 consecutive positions (a window) at a time:
 //  A. lane j folds slot j's inputs from before the window (finish times, or
-//     arrivals of transfers: final by now) into a partial ready time, marks
-//     its in-window predecessors in a 64-bit mask, and loads its own w, c,
-//     device and destination-device mask.  Rows with many inputs are folded
-//     by the whole wave.
+//     arrivals of transfers: final by now) into a partial ready time and
+//     marks its in-window predecessors in a 64-bit mask.  Its own w, c,
+//     device, row and first four inputs (a per-position table) were loaded
+//     during the previous window.  Rows with many inputs are folded by the
+//     whole wave.
 //  B. the window splits into segments, runs of consecutive slots with no
 //     edge among them, taken in order.  A segment's slots add their inputs
 //     from earlier segments (shuffles), then are placed: with FIFO devices
@@ -29,11 +30,11 @@
 // so the segment holds as many entries as d has nodes), and its newest 64
 // again in an LDS ring (written through to the array).  A node ready at or
 // after the last gap's end goes after the device's last task with no search.
-// Otherwise the wave reads the ring, one gap per lane, and takes the first gap
-// that holds the node (ballot); only when the ring's oldest gap already ends
-// after the ready time can an older gap hold it, and then the wave walks the
-// global segment first, 64 gaps per round trip.  The chosen gap shrinks,
-// splits or empties.
+// Otherwise lane d binary-searches its device's ring for the first gap that
+// holds the node and shrinks or empties it.  A split (which moves the ring),
+// or a ring whose oldest gap already ends after the ready time (an older gap
+// may hold the node), goes to the whole wave: the ring one gap per lane with
+// a ballot, after walking the global segment, 64 gaps per round trip.
 // Transfers: a producer's destination devices form a mask; its arrivals sit
 // in a pool at off[p] + (rank of the device in the mask).
 // Heterogeneous devices (HET): device d runs a node of w in ceil(w tmul[d] /
