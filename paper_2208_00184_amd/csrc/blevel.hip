@@ -491,24 +491,29 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
   CEL_TRY(relabel_csr(n, g->m, order_id, pos, g->out_ptr, g->out_idx, sptr, sidx, sc, s, st));
   k_node_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order_id, g->w, g->ob, d->bw, d->lat,
                                                      (flags & CEL_COMM_OFF) ? 1 : 0, wp, wcp, st);
-  {
-    KTimer kt(s, "k_blevel_sweep");
-    k_level_sweep<true><<<1, kSweepB, 0, s>>>(n, L, level_ptr, sptr, sidx, wp, wcp, blp, st);
-  }
-  k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, blp, blevel, st, &st->s0);
+  // The t-level (eq. 2) needs no b-level: its relabelling and sweep run on a
+  // side stream, so the two single-workgroup sweeps overlap on two CUs.
+  SideFork fk;
   if (tlevel && n > 0) {
     int32_t *pptr, *pidx;
     int64_t *tlp;
     CEL_TRY(sc.get(&pptr, (int64_t)n + 1));
     CEL_TRY(sc.get(&pidx, g->m));
     CEL_TRY(sc.get(&tlp, n));
-    CEL_TRY(relabel_csr(n, g->m, order_id, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
+    CEL_TRY(fk.start(s));
+    const hipStream_t t = fk.side();
+    CEL_TRY(relabel_csr(n, g->m, order_id, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, t, st));
     {
-      KTimer kt(s, "k_tlevel_sweep");
-      k_level_sweep<false><<<1, kSweepB, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, wcp, tlp, st);
+      KTimer kt(t, "k_tlevel_sweep");
+      k_level_sweep<false><<<1, kSweepB, 0, t>>>(n, L, level_ptr, pptr, pidx, wp, wcp, tlp, st);
     }
-    k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, tlp, tlevel, st, &st->s1);
+    k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, t>>>(n, order_id, tlp, tlevel, st, &st->s1);
   }
+  {
+    KTimer kt(s, "k_blevel_sweep");
+    k_level_sweep<true><<<1, kSweepB, 0, s>>>(n, L, level_ptr, sptr, sidx, wp, wcp, blp, st);
+  }
+  k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, blp, blevel, st, &st->s0);
   if (prio_order && n > 0) {
     uint64_t *keys;
     CEL_TRY(sc.get(&keys, n));
@@ -517,6 +522,7 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
     CEL_TRY(segmented_sort(keys, ids, level_ptr, L, n, sc, s, st));
   }
   CEL_HIP(hipGetLastError());
+  CEL_TRY(fk.join());
   Status h;
   CEL_TRY(read_status(st, &h, s));
   if (h.err) return status_error(h, fn);

@@ -388,6 +388,30 @@ __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v);  // common.hip
 // Copies the status block to the host (synchronising the stream).
 int read_status(const Status *dst, Status *host, hipStream_t s);
 
+// Fork/join onto a second stream of the current device (created once, at the
+// default priority, non-blocking, kept until the process ends), for two
+// independent single-workgroup kernels that would each leave the chip idle.
+// start() orders the side stream after the work already on `s`; join()
+// orders `s` after the work put on the side stream since.  The destructor
+// joins if join() was not called, so an early error return still leaves
+// every later use of `s` (scratch reuse included) behind the side work, and
+// it waits for the join before releasing its events.
+class SideFork {
+ public:
+  SideFork() = default;
+  ~SideFork();
+  SideFork(const SideFork &) = delete;
+  SideFork &operator=(const SideFork &) = delete;
+  int start(hipStream_t s);
+  int join();
+  hipStream_t side() const { return side_; }
+
+ private:
+  hipStream_t s_ = nullptr, side_ = nullptr;
+  hipEvent_t fork_ = nullptr, join_ = nullptr;
+  bool joined_ = true;
+};
+
 // Translates device error bits into an API error code with a message.
 int status_error(const Status &h, const char *fn);
 

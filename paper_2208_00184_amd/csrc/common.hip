@@ -136,6 +136,46 @@ int read_status(const Status *dst, Status *host, hipStream_t s) {
   return CEL_OK;
 }
 
+// ------------------------------------------------------------ side stream
+
+static std::mutex g_side_mu;
+static std::map<int, hipStream_t> g_side;
+
+int SideFork::start(hipStream_t s) {
+  int dev = 0;
+  CEL_HIP(hipGetDevice(&dev));
+  {
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    hipStream_t &t = g_side[dev];
+    if (!t) CEL_HIP(hipStreamCreateWithFlags(&t, hipStreamNonBlocking));
+    side_ = t;
+  }
+  CEL_HIP(hipEventCreateWithFlags(&fork_, hipEventDisableTiming));
+  CEL_HIP(hipEventCreateWithFlags(&join_, hipEventDisableTiming));
+  CEL_HIP(hipEventRecord(fork_, s));
+  CEL_HIP(hipStreamWaitEvent(side_, fork_, 0));
+  s_ = s;
+  joined_ = false;
+  return CEL_OK;
+}
+
+int SideFork::join() {
+  if (joined_) return CEL_OK;
+  joined_ = true;
+  CEL_HIP(hipEventRecord(join_, side_));
+  CEL_HIP(hipStreamWaitEvent(s_, join_, 0));
+  return CEL_OK;
+}
+
+SideFork::~SideFork() {
+  if (!joined_ && join() != CEL_OK) (void)hipStreamSynchronize(side_);
+  if (join_) {
+    (void)hipEventSynchronize(join_);
+    (void)hipEventDestroy(join_);
+  }
+  if (fork_) (void)hipEventDestroy(fork_);
+}
+
 // ------------------------------------------------------------- validation
 
 // saturating add for the overflow bound
