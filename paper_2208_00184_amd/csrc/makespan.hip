@@ -104,6 +104,28 @@ __device__ inline void wave_seg_scan_maxplus_z(int64_t &a, int64_t &b, int32_t &
   segz_step<0x142, 0xA>(a, b, f);  // row_bcast:15 into rows 1 and 3
   segz_step<0x143, 0xC>(a, b, f);  // row_bcast:31 into rows 2 and 3
 }
+
+// The same scan over one segment (no start flags): every lane combines.
+template <int CTRL, int ROWMASK>
+__device__ inline void mpz_step(int64_t &a, int64_t &b) {
+  const int32_t alo = __builtin_amdgcn_update_dpp(0, (int32_t)a, CTRL, ROWMASK, 0xF, true);
+  const int32_t ahi = __builtin_amdgcn_update_dpp(0, (int32_t)(a >> 32), CTRL, ROWMASK, 0xF, true);
+  const int32_t blo = __builtin_amdgcn_update_dpp(0, (int32_t)b, CTRL, ROWMASK, 0xF, true);
+  const int32_t bhi = __builtin_amdgcn_update_dpp(0, (int32_t)(b >> 32), CTRL, ROWMASK, 0xF, true);
+  const int64_t ua = (int64_t)(((uint64_t)(uint32_t)ahi << 32) | (uint32_t)alo);
+  const int64_t ub = (int64_t)(((uint64_t)(uint32_t)bhi << 32) | (uint32_t)blo);
+  const int64_t c = ua + b;
+  a = c <= a ? a : c;
+  b = ub + b;
+}
+__device__ inline void wave_scan_maxplus_z(int64_t &a, int64_t &b) {
+  mpz_step<0x111, 0xF>(a, b);
+  mpz_step<0x112, 0xF>(a, b);
+  mpz_step<0x114, 0xF>(a, b);
+  mpz_step<0x118, 0xF>(a, b);
+  mpz_step<0x142, 0xA>(a, b);
+  mpz_step<0x143, 0xC>(a, b);
+}
 constexpr int kBatchWide = 384;  // batches up to this size get one CU-sized window per placement
 constexpr int kWideLevels = 256;  // mean level width from which batches skip the windows
 
@@ -271,49 +293,70 @@ __global__ void __launch_bounds__(B)
                 ww = s_w[i];
                 aa = s_pm[i] + ww;
               }
-              // slot in device-grouped order (devices ascending, positions
-              // ascending): ballots over the device id's bits, high to low
-              const uint64_t actm = __ballot(act);
-              uint32_t eql = (uint32_t)actm, eqh = (uint32_t)(actm >> 32), ltl = 0, lth = 0;
-              for (int bit = dbits - 1; bit >= 0; bit--) {
-                const uint32_t on = (dv >> bit) & 1;
-                const uint64_t bb = __ballot(on) & actm;
-                const uint32_t bl = (uint32_t)bb, bh = (uint32_t)(bb >> 32);
-                const uint32_t keep0 = on - 1u;  // ~0 when the bit is 0, else 0
-                ltl |= (eql & ~bl) & ~keep0;     // equal so far, bit 0 there, 1 here
-                lth |= (eqh & ~bh) & ~keep0;
-                eql &= bl ^ keep0;
-                eqh &= bh ^ keep0;
-              }
-              const uint64_t eq = ((uint64_t)eqh << 32) | eql;
-              const int below = __popcll(eq & lanemask_lt);
-              const int q = act ? __popc(ltl) + __popc(lth) + below : lane;  // a permutation
-              const int head = act && below == 0;                // first of its device
-              const int tail = act && (eq >> lane) == 1ull;      // last of its device
-              const int addr = q << 2;
-              const int64_t ash = aa + kShift;  // shifted: the scan identity is all zero
-              const int32_t meta = dv | (head << 8) | (tail << 9) | ((int)act << 10);
-              const int32_t pa_lo = __builtin_amdgcn_ds_permute(addr, (int32_t)ash);
-              const int32_t pa_hi = __builtin_amdgcn_ds_permute(addr, (int32_t)(ash >> 32));
-              const int32_t pb_lo = __builtin_amdgcn_ds_permute(addr, (int32_t)ww);
-              const int32_t pb_hi = __builtin_amdgcn_ds_permute(addr, (int32_t)(ww >> 32));
-              const int32_t pm = __builtin_amdgcn_ds_permute(addr, meta);
-              const int32_t pj = __builtin_amdgcn_ds_permute(addr, i);
-              const bool pact = (pm >> 10) & 1;
-              const int dq = pm & 255;
-              int64_t sa = pact ? (int64_t)(((uint64_t)(uint32_t)pa_hi << 32) | (uint32_t)pa_lo) : 0;
-              int64_t sb = pact ? (int64_t)(((uint64_t)(uint32_t)pb_hi << 32) | (uint32_t)pb_lo) : 0;
-              int32_t f = pact ? ((pm >> 8) & 1) : 1;
-              wave_seg_scan_maxplus_z(sa, sb, f);
-              sa -= kShift;
-              if (pact) {
-                const int64_t viafree = s_avail[dq] + sb;
-                const int64_t fin = viafree > sa ? viafree : sa;
-                s_f[pj] = fin;
-                fk[P0 + pj] = fin;
-                mk = fin > mk ? fin : mk;
+              // Rows whose nodes all sit on one device (nearly every row of
+              // a clustered placement): device-grouped order is lane order
+              // and the row is one segment, so no permutation is needed.
+              const int dv0 = __builtin_amdgcn_readfirstlane(dv);  // lane 0 is active
+              if (__ballot(act && dv != dv0) == 0) {
+                int64_t sa = act ? aa + kShift : 0, sb = act ? ww : 0;
+                wave_scan_maxplus_z(sa, sb);
+                sa -= kShift;
+                int64_t fin = 0;
+                if (act) {
+                  const int64_t viafree = s_avail[dv0] + sb;
+                  fin = viafree > sa ? viafree : sa;
+                  s_f[i] = fin;
+                  fk[P0 + i] = fin;
+                  mk = fin > mk ? fin : mk;
+                }
                 lds_order();  // every lane's read of s_avail precedes the update
-                if ((pm >> 9) & 1) s_avail[dq] = fin;
+                if (lane == cnt2 - 1) s_avail[dv0] = fin;
+              } else {
+                // slot in device-grouped order (devices ascending, positions
+                // ascending): ballots over the device id's bits, high to low
+                const uint64_t actm = __ballot(act);
+                uint32_t eql = (uint32_t)actm, eqh = (uint32_t)(actm >> 32), ltl = 0, lth = 0;
+                for (int bit = dbits - 1; bit >= 0; bit--) {
+                  const uint32_t on = (dv >> bit) & 1;
+                  const uint64_t bb = __ballot(on) & actm;
+                  const uint32_t bl = (uint32_t)bb, bh = (uint32_t)(bb >> 32);
+                  const uint32_t keep0 = on - 1u;  // ~0 when the bit is 0, else 0
+                  ltl |= (eql & ~bl) & ~keep0;     // equal so far, bit 0 there, 1 here
+                  lth |= (eqh & ~bh) & ~keep0;
+                  eql &= bl ^ keep0;
+                  eqh &= bh ^ keep0;
+                }
+                const uint64_t eq = ((uint64_t)eqh << 32) | eql;
+                const int below = __popcll(eq & lanemask_lt);
+                const int q = act ? __popc(ltl) + __popc(lth) + below : lane;  // a permutation
+                const int head = act && below == 0;                // first of its device
+                const int tail = act && (eq >> lane) == 1ull;      // last of its device
+                const int addr = q << 2;
+                const int64_t ash = aa + kShift;  // shifted: the scan identity is all zero
+                const int32_t meta = dv | (head << 8) | (tail << 9) | ((int)act << 10);
+                const int32_t pa_lo = __builtin_amdgcn_ds_permute(addr, (int32_t)ash);
+                const int32_t pa_hi = __builtin_amdgcn_ds_permute(addr, (int32_t)(ash >> 32));
+                const int32_t pb_lo = __builtin_amdgcn_ds_permute(addr, (int32_t)ww);
+                const int32_t pb_hi = __builtin_amdgcn_ds_permute(addr, (int32_t)(ww >> 32));
+                const int32_t pm = __builtin_amdgcn_ds_permute(addr, meta);
+                const int32_t pj = __builtin_amdgcn_ds_permute(addr, i);
+                const bool pact = (pm >> 10) & 1;
+                const int dq = pm & 255;
+                int64_t sa = pact ? (int64_t)(((uint64_t)(uint32_t)pa_hi << 32) | (uint32_t)pa_lo) : 0;
+                int64_t sb = pact ? (int64_t)(((uint64_t)(uint32_t)pb_hi << 32) | (uint32_t)pb_lo) : 0;
+                int32_t f = pact ? ((pm >> 8) & 1) : 1;
+                wave_seg_scan_maxplus_z(sa, sb, f);
+                sa -= kShift;
+                if (pact) {
+                  const int64_t viafree = s_avail[dq] + sb;
+                  const int64_t fin = viafree > sa ? viafree : sa;
+                  s_f[pj] = fin;
+                  fk[P0 + pj] = fin;
+                  mk = fin > mk ? fin : mk;
+                  lds_order();  // every lane's read of s_avail precedes the update
+                  if ((pm >> 9) & 1) s_avail[dq] = fin;
+                }
+
               }
               lds_order();
             }
