@@ -302,6 +302,45 @@ int orc_cpd_topo(const orc_graph *g, const int64_t *blevel, const int64_t *tleve
   return out == n ? ORC_OK : ORC_E_CYCLE;
 }
 
+/* DFS-TOPO order (Section 4.2.2): a queue Q holds every node with no
+ * remaining in-edge, sources first in increasing id; the head of Q is removed
+ * and output, its out-edges removed, and the successors that this leaves with
+ * no in-edge go to the head of Q, the lowest id in front.  Q is held as an
+ * array whose end is the head. */
+int orc_dfs_topo(const orc_graph *g, int32_t *dfs_order) {
+  int rc = check_graph(g);
+  if (rc) return rc;
+  int32_t n = g->n;
+  if (n > 0 && !dfs_order) return ORC_E_ARG;
+  int32_t *indeg = calloc((size_t)n + 1, sizeof(int32_t));
+  int32_t *q = malloc(sizeof(int32_t) * ((size_t)n + 1));
+  for (int32_t e = 0; e < g->m; e++) indeg[g->out_idx[e]]++;
+  int32_t head = 0; /* q[0 .. head-1]; q[head-1] is the head of Q */
+  for (int32_t v = n - 1; v >= 0; v--)
+    if (indeg[v] == 0) q[head++] = v;
+  int32_t out = 0;
+  while (head > 0) {
+    int32_t v = q[--head];
+    dfs_order[out++] = v;
+    /* the successors freed now, in decreasing id, so the lowest ends in front */
+    int32_t first = head;
+    for (int32_t e = g->out_ptr[v]; e < g->out_ptr[v + 1]; e++) {
+      int32_t s = g->out_idx[e];
+      if (--indeg[s] == 0) {
+        int32_t k = head++;
+        while (k > first && q[k - 1] < s) {
+          q[k] = q[k - 1];
+          k--;
+        }
+        q[k] = s;
+      }
+    }
+  }
+  free(indeg);
+  free(q);
+  return out == n ? ORC_OK : ORC_E_CYCLE;
+}
+
 /* ------------------------------------------------- CCR and Order-Place */
 
 /* eq. 1: CCR = sum over edges of c_{i,j} / sum over nodes of w_i; fusion keeps

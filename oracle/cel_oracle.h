@@ -69,6 +69,13 @@ int orc_blevel(const orc_graph *g, const orc_devices *d, const int32_t *level,
 int orc_cpd_topo(const orc_graph *g, const int64_t *blevel, const int64_t *tlevel,
                  int32_t *cpd_order);
 
+/* DFS-TOPO order (Section 4.2.2): a queue starts with the sources, lowest id
+ * at the head; the head node is removed and output, its out-edges removed,
+ * and the successors left with no in-edge are put at the head of the queue,
+ * the lowest id in front, so a freed child is output before anything older.
+ * dfs_order[k] = k-th node output. */
+int orc_dfs_topo(const orc_graph *g, int32_t *dfs_order);
+
 /* Contiguous clustering of a topological order (Section 5.1.3, eq. 4-6):
  * DP over breakpoints minimising inter-cluster comm with cluster length <= R
  * and cluster memory <= M (a single node may exceed M).  M = -1 selects

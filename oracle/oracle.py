@@ -58,6 +58,7 @@ def lib():
         L.orc_makespan.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), _P32, C.c_int32,
                                    _PU8, _P64, _P64, _P64]
         L.orc_cpd_topo.argtypes = [C.POINTER(_Graph), _P64, _P64, _P32]
+        L.orc_dfs_topo.argtypes = [C.POINTER(_Graph), _P32]
         L.orc_comm_sums.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), _P32,
                                     C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
         L.orc_order_place.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), _P32, C.c_int32,
@@ -67,7 +68,7 @@ def lib():
                                          _P64, _P64, _P64]
         L.orc_colocate.argtypes = [C.POINTER(_Graph), _P32, _P32, C.c_int32, C.c_int32, _PU8]
         for f in (L.orc_topo_levels, L.orc_blevel, L.orc_cluster, L.orc_place, L.orc_makespan,
-                  L.orc_cpd_topo, L.orc_comm_sums, L.orc_order_place, L.orc_makespan_model,
+                  L.orc_cpd_topo, L.orc_dfs_topo, L.orc_comm_sums, L.orc_order_place, L.orc_makespan_model,
                   L.orc_colocate):
             f.restype = C.c_int
         _lib = L
@@ -143,6 +144,15 @@ def cpd_topo(wl, blevel, tlevel):
     out = np.zeros(max(n, 1), np.int32)
     _check(lib().orc_cpd_topo(C.byref(k.g), _ptr(bl, _P64), _ptr(tl, _P64), _ptr(out, _P32)),
            "orc_cpd_topo")
+    return out[:n]
+
+
+def dfs_topo(wl):
+    """DFS-TOPO order (Section 4.2.2) -> int32[n] node ids."""
+    k = _Keep(wl)
+    n = int(wl.n)
+    out = np.zeros(max(n, 1), np.int32)
+    _check(lib().orc_dfs_topo(C.byref(k.g), _ptr(out, _P32)), "orc_dfs_topo")
     return out[:n]
 
 

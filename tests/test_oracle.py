@@ -576,6 +576,86 @@ def test_cpd_small_dags_and_edge_cases():
         O.cpd_topo(wl, np.zeros(3, np.int64), np.zeros(3, np.int64))
 
 
+# ------------------------------------------------------------- DFS-TOPO order
+
+
+def dfs_by_freed_step(wl):
+    """DFS-TOPO restated without a queue: the next node is the ready one freed
+    most recently (sources count as freed before the first step), the lowest
+    id among those freed by the same step.  Brute force, O(n^2)."""
+    n = wl.n
+    indeg = np.zeros(n, np.int64)
+    us, vs = wl.edges()
+    succ = [[] for _ in range(n)]
+    for u, v in zip(us, vs):
+        indeg[int(v)] += 1
+        succ[int(u)].append(int(v))
+    freed = {v: -1 for v in range(n) if indeg[v] == 0}
+    out = []
+    for step in range(n):
+        v = min(freed, key=lambda x: (-freed[x], x))
+        del freed[v]
+        out.append(v)
+        for s in succ[v]:
+            indeg[s] -= 1
+            if indeg[s] == 0:
+                freed[s] = step
+    return out
+
+
+def test_dfs_two_chains_keeps_chains_whole():
+    # two chains with interleaved ids: level order alternates between them,
+    # DFS-TOPO finishes one chain before starting the other
+    wl = from_edges(8, [(0, 2), (2, 4), (4, 6), (1, 3), (3, 5), (5, 7)], [1] * 8, [0] * 8, 2,
+                    [10 ** 9] * 2, 1, 0)
+    order = list(O.dfs_topo(wl))
+    assert order == [0, 2, 4, 6, 1, 3, 5, 7]
+    _, kahn, _, _ = O.topo_levels(wl)
+    assert list(kahn) == list(range(8))
+
+    def cut(order):  # edges between the two halves of the order
+        half = set(order[:4])
+        return sum((int(u) in half) != (int(v) in half) for u, v in zip(*wl.edges()))
+    assert cut(order) == 0 and cut(list(kahn)) == 2
+
+
+def test_dfs_matches_freed_step_brute_force():
+    for wl in small_dags():
+        assert list(O.dfs_topo(wl)) == dfs_by_freed_step(wl)
+    rng = np.random.default_rng(5)
+    for _ in range(40):
+        n = int(rng.integers(1, 60))
+        edges = sorted({(int(a), int(b)) for a, b in rng.integers(0, n, (2 * n, 2)) if a < b})
+        perm = rng.permutation(n)  # ids not in topological order
+        edges = [(int(perm[a]), int(perm[b])) for a, b in edges]
+        wl = from_edges(n, edges, [1] * n, [0] * n, 2, [10 ** 9] * 2, 1, 0)
+        assert list(O.dfs_topo(wl)) == dfs_by_freed_step(wl)
+
+
+def test_dfs_forest_is_preorder_and_cpd_with_equal_cpath():
+    rng = np.random.default_rng(22)
+    for _ in range(20):
+        n = 1 + int(rng.integers(1, 200))
+        parent = [-1 if (v == 0 or rng.random() < 0.1) else int(rng.integers(0, v))
+                  for v in range(n)]
+        wl = from_edges(n, [(p, v) for v, p in enumerate(parent) if p >= 0], [1] * n, [0] * n, 2,
+                        [10 ** 9] * 2, 1, 0)
+        assert list(O.dfs_topo(wl)) == preorder(wl, np.zeros(n, np.int64))
+    for cfg in (1, 2):  # CPD-TOPO with every cpath equal is DFS-TOPO
+        wl = make_config(cfg, 0)
+        z = np.zeros(wl.n, np.int64)
+        assert np.array_equal(O.dfs_topo(wl), O.cpd_topo(wl, z, z))
+
+
+def test_dfs_edge_cases():
+    assert len(O.dfs_topo(from_edges(0, [], [], [], 2, [5, 5], 3, 1))) == 0
+    wl = from_edges(5, [], [1] * 5, [0] * 5, 2, [5, 5], 1, 0)
+    assert list(O.dfs_topo(wl)) == list(range(5))  # isolated nodes by id
+    wl = from_edges(3, [(0, 1), (1, 2), (2, 0)], [1] * 3, [0] * 3, 2, [5, 5], 1, 0)
+    with pytest.raises(O.OracleError):
+        O.dfs_topo(wl)
+
+
 # ------------------------------------------------------- CCR and Order-Place
 
 
