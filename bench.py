@@ -16,7 +16,7 @@ the per-level latency of the level sweeps (a single placement of a graph
 output, timed apart), batched scoring of 1,024 perturbed placements of the
 200k-node layered DAG in one call (the bandwidth-bound regime), and the CPU
 oracle (one pinned core, every stage) on the same 1.07M-node graph.  Further
-rows: the CPD-TOPO order against the priority order, the CCR before and
+rows: the CPD-TOPO order against the priority and DFS-TOPO orders, the CCR before and
 after fusion, Order-Place against Adjusting Placement, and the makespan under
 the device models (first-fit insertion, transfers as tasks, heterogeneous
 devices, co-location).
@@ -213,13 +213,16 @@ def _timed(torch, f, reps=3):
 def cpd_compare(cel, torch, g, d, bl, tl, prio, lev, lp, L):
     """CPD-TOPO order (host walk over GPU b-/t-levels) and what it changes
     downstream: DP clustering (R = 200) on it against the level-monotone
-    priority order; for each, the CCR before and after fusion (eq. 1, as in
-    the paper's CCR table) and the makespan of Order-Place against Adjusting
-    Placement on the same clusters (as in its placement comparison)."""
+    priority order and the DFS-TOPO order; for each, the CCR before and after
+    fusion (eq. 1, as in the paper's CCR table) and the makespan of Order-Place
+    against Adjusting Placement on the same clusters (as in its placement
+    comparison)."""
     cpd, cpd_ms = _timed(torch, lambda: cel.cpd_order(g, bl, tl))
+    dfs, dfs_ms = _timed(torch, lambda: cel.dfs_order(g))
     (ec0, ws), ccr_ms = _timed(torch, lambda: cel.comm_sums(g, d))
-    row = {"cpd_order_ms": cpd_ms, "comm_sums_ms": ccr_ms, "n": g.n, "ccr": ec0 / ws}
-    for name, order in (("priority", prio), ("cpd", cpd)):
+    row = {"cpd_order_ms": cpd_ms, "dfs_order_ms": dfs_ms, "comm_sums_ms": ccr_ms, "n": g.n,
+           "ccr": ec0 / ws}
+    for name, order in (("priority", prio), ("dfs", dfs), ("cpd", cpd)):
         cid, C, cut = cel.cluster(g, d, order, 200, -1)
         ec, _ = cel.comm_sums(g, d, cid)
         _, ndev, cms, be = cel.place(g, d, cid, C)

@@ -6,6 +6,7 @@
  *   cel_topo_levels  level-synchronous topological ordering      (Section 4.2.2)
  *   cel_blevel       b-level / t-level / critical path, priority  (Section 5.1.3, eq. 2-3)
  *   cel_cpd_order    CPD-TOPO critical-path depth-first order    (Section 5.1.3, Algorithm 1)
+ *   cel_dfs_order    DFS-TOPO depth-first topological order      (Section 4.2.2)
  *   cel_cluster      memory-capped contiguous clustering (DP)     (Section 5.1.3, eq. 4-6)
  *   cel_place        coarse graph + Adjusting Placement           (Section 5.2, eq. 7-9, Alg. 2)
  *   cel_makespan     makespan of one or K placements              (Section 5.2, eq. 7)
@@ -124,6 +125,18 @@ int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_t *level,
  * Errors: CEL_E_ARG (NULL or a malformed CSR), CEL_E_CYCLE, CEL_E_HIP. */
 int cel_cpd_order(const cel_graph *g, const int64_t *blevel, const int64_t *tlevel,
                   int32_t *cpd_order, hipStream_t stream);
+
+/* DFS-TOPO order (Section 4.2.2), the depth-first topological order that
+ * CPD-TOPO refines.  A queue starts with the sources, the lowest id at its
+ * head; the head node is removed and output, its out-edges removed, and the
+ * successors left with no in-edge are put at the head of the queue, the
+ * lowest id in front, so a freed child comes before every older entry.
+ * Only the CSR half of the graph is read.  Output: dfs_order [n], the node
+ * ids in DFS-TOPO order (a topological order, which cel_cluster accepts).
+ * Like cel_cpd_order it walks on the host over a copy of the successor
+ * lists and synchronises `stream`.
+ * Errors: CEL_E_ARG (NULL or a malformed CSR), CEL_E_CYCLE, CEL_E_HIP. */
+int cel_dfs_order(const cel_graph *g, int32_t *dfs_order, hipStream_t stream);
 
 /* Contiguous clustering of a topological order (Section 5.1.3, eq. 4-6;
  * clusters are runs of consecutive positions, which keeps the coarse graph

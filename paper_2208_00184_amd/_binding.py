@@ -20,7 +20,7 @@ OK, E_ARG, E_CYCLE, E_OVERFLOW, E_HIP, E_NOMEM, E_ORDER = 0, -1, -2, -3, -4, -5,
 COMM_OFF = 1
 CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
-EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_cluster", "cel_place", "cel_makespan",
+EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_dfs_order", "cel_cluster", "cel_place", "cel_makespan",
            "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_colocate", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
@@ -66,12 +66,13 @@ def lib() -> C.CDLL:
         L.cel_place.argtypes = [G, Dv, vp, i32, vp, vp, vp, C.POINTER(i64), C.POINTER(i32), vp]
         L.cel_makespan.argtypes = [G, Dv, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]
         L.cel_cpd_order.argtypes = [G, vp, vp, vp, vp]
+        L.cel_dfs_order.argtypes = [G, vp, vp]
         L.cel_order_place.argtypes = [G, Dv, vp, i32, vp, vp, C.POINTER(i32), vp]
         L.cel_comm_sums.argtypes = [G, Dv, vp, C.POINTER(i64), C.POINTER(i64), vp]
         L.cel_makespan_model.argtypes = [G, Dv, C.POINTER(_Hetero), vp, i32, vp, i32, vp, vp, vp, vp]
         L.cel_colocate.argtypes = [G, vp, vp, i32, i32, vp, vp]
         for f in ("cel_topo_levels", "cel_blevel", "cel_cluster", "cel_place", "cel_makespan",
-                  "cel_cpd_order", "cel_order_place", "cel_comm_sums", "cel_makespan_model",
+                  "cel_cpd_order", "cel_dfs_order", "cel_order_place", "cel_comm_sums", "cel_makespan_model",
                   "cel_colocate", "cel_version"):
             getattr(L, f).restype = C.c_int
         L.cel_last_error.argtypes = []
@@ -206,6 +207,15 @@ def cpd_order(g: Graph, blevel_, tlevel_):
     out = _empty(n, torch.int32, g.device)
     gc = g._c()
     _check(lib().cel_cpd_order(C.byref(gc), _p(blevel_), _p(tlevel_), _p(out), _stream()))
+    return out[:n]
+
+
+def dfs_order(g: Graph):
+    """DFS-TOPO order (Section 4.2.2) -> int32[n] node ids."""
+    n = g.n
+    out = _empty(n, torch.int32, g.device)
+    gc = g._c()
+    _check(lib().cel_dfs_order(C.byref(gc), _p(out), _stream()))
     return out[:n]
 
 

@@ -675,6 +675,43 @@ def test_cluster_on_cpd_order(cfg):
     assert np.array_equal(np_(cid), ref[0])
 
 
+# ------------------------------------------------------------- DFS-TOPO order
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_dfs_order_configs(cfg):
+    wl = make_config(cfg, 0) if cfg == 4 else config(cfg, 0)[0]
+    g, _ = up(wl)
+    assert np.array_equal(np_(cel.dfs_order(g)), O.dfs_topo(wl))
+
+
+def test_dfs_order_random_and_edge_cases():
+    for s in range(12):
+        wl = make_random_dag(700 + s, 20 + 41 * s, p_edge=min(0.5, 3.0 / (20 + 41 * s)),
+                             D=2 + s % 4, multi=(s % 2 == 0), zero_frac=0.2 if s % 3 == 0 else 0)
+        g, _ = up(wl)
+        assert np.array_equal(np_(cel.dfs_order(g)), O.dfs_topo(wl)), s
+    g, _ = up(from_edges(0, [], [], [], 2, [5, 5], 3, 1))
+    assert np_(cel.dfs_order(g)).size == 0
+    g, _ = up(from_edges(8, [(0, 2), (2, 4), (4, 6), (1, 3), (3, 5), (5, 7)], [1] * 8, [0] * 8, 2,
+                         [10 ** 9] * 2, 1, 0))
+    assert np_(cel.dfs_order(g)).tolist() == [0, 2, 4, 6, 1, 3, 5, 7]
+    g, _ = up(from_edges(3, [(0, 1), (1, 2), (2, 0)], [1] * 3, [0] * 3, 2, [5, 5], 1, 0))
+    with pytest.raises(cel.CelError) as ei:
+        cel.dfs_order(g)
+    assert ei.value.code == -2
+
+
+def test_cluster_and_place_on_dfs_order():
+    wl, _, _ = config(3, 0)
+    g, d = up(wl)
+    order = cel.dfs_order(g)
+    ref = O.cluster(wl, O.dfs_topo(wl), 200, -1)
+    cid, C, cut = cel.cluster(g, d, order, 200, -1)
+    assert C == ref[1] and cut == ref[2]
+    assert np.array_equal(np_(cid), ref[0])
+
+
 # ----------------------------------------- Order-Place and the CCR parts
 
 
