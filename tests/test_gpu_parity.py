@@ -89,6 +89,34 @@ def test_blevel_comm_off(cfg):
     assert np.array_equal(np_(bl), ref[0]) and np.array_equal(np_(pr), ref[2])
 
 
+def test_blevel_tlevel_on_caller_streams():
+    """The t-level sweep runs on a side stream joined back into the caller's
+    stream: results must be complete when the call returns, on the default
+    stream and on user streams used in turn (the side stream is shared)."""
+    outs = []
+    for cfg in (1, 3):
+        wl, rt, rb = config(cfg, 0)
+        lev, oid, lp, L = rt
+        g, d = up(wl)
+        args = (tt(lev, np.int32), tt(lp, np.int32), tt(oid, np.int32), L)
+        torch.cuda.synchronize()
+        s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+        for stream in (None, s1, s2, s1):
+            if stream is None:
+                bl, tl, pr, cp = cel.blevel(g, d, *args, want_tlevel=True)
+            else:
+                with torch.cuda.stream(stream):
+                    bl, tl, pr, cp = cel.blevel(g, d, *args, want_tlevel=True)
+                    tl_host = tl.to("cpu", non_blocking=False)  # ordered on `stream`
+                assert np.array_equal(tl_host.numpy(), rb[1])
+            torch.cuda.synchronize()
+            assert cp == rb[3]
+            assert np.array_equal(np_(bl), rb[0]) and np.array_equal(np_(tl), rb[1])
+            assert np.array_equal(np_(pr), rb[2])
+        outs.append(cfg)
+    assert outs == [1, 3]
+
+
 def random_placements(wl, K, seed):
     rng = np.random.default_rng([77, seed])
     return rng.integers(0, wl.D, (K, wl.n)).astype(np.uint8)
