@@ -51,7 +51,7 @@ def algorithmic_bytes(kernel: str, n: int, m: int, K: int) -> float | None:
         return 32.0 * n + 12.0 * m
     if kernel == "k_tlevel_sweep":
         return 32.0 * n + 12.0 * m
-    if kernel == "k_makespan_sweep":    # per node: order 4, ptr 4, w 8, c 8, dev 1, fin 8; per edge: idx 4, fin 8, dev 1, c 8
+    if kernel == "k_makespan_one":    # per node: order 4, ptr 4, w 8, c 8, dev 1, fin 8; per edge: idx 4, fin 8, dev 1, c 8
         return 33.0 * n + 21.0 * m
     if kernel == "k_makespan_batch":    # shared structure once + per placement dev, fin write, dev/fin gathers
         return 24.0 * n + 12.0 * m + K * (9.0 * n + 9.0 * m)
@@ -65,7 +65,7 @@ TRAFFIC_FILES = [os.path.join(ROOT, "profiles", f) for f in
 CSRC = os.path.join(ROOT, "paper_2208_00184_amd", "csrc")
 # kernels the bench names, their symbols in rocprofv3 output and their sources
 PMC_KERNELS = {
-    "k_makespan_sweep": ("cel::k_makespan_one<", ["makespan.hip", "cel_internal.h"]),
+    "k_makespan_one": ("cel::k_makespan_one<", ["makespan.hip", "cel_internal.h"]),
     "k_blevel_sweep": ("cel::k_level_sweep<true>", ["blevel.hip", "cel_internal.h"]),
     "k_tlevel_sweep": ("cel::k_level_sweep<false>", ["blevel.hip", "cel_internal.h"]),
     "k_makespan_batch": ("cel::k_makespan_sweep<256, 1024, 4096>", ["makespan.hip", "cel_internal.h"]),
@@ -189,6 +189,19 @@ def batched_row(cel, torch, dev, args):
     call_ms = float(np.mean(times))
     print(f"[bench] 200k-node scoring of {BATCH5} placements: {call_ms:.2f} ms per call",
           file=sys.stderr, flush=True)
+    parity = None
+    if not args.no_cpu:
+        # 16 rows spread over the batch against the oracle, whose inputs (order,
+        # clustering, placement, perturbation) it derives on its own
+        from oracle import oracle as O
+        lev_o, oid_o, _, _ = O.topo_levels(wl)
+        _, _, pr_o, _ = O.blevel(wl, lev_o, oid_o)
+        cid_o, C_o, _ = O.cluster(wl, pr_o, 200, -1)
+        cdev_o, _, _, _ = O.place(wl, cid_o, C_o)
+        rows = np.linspace(0, BATCH5 - 1, 16).astype(np.int64)
+        cand_o = perturb_placements(cdev_o, wl.D, BATCH5, args.seed)[rows][:, cid_o]
+        ref, _, _ = O.makespan(wl, pr_o, cand_o, want_times=False)
+        parity = {"makespan_rows": bool(np.array_equal(ms.cpu().numpy()[rows], ref))}
     return {"workload": f"layered-200k: 400 x 500 layered DAG, {BATCH5} placements (5% of the "
                         f"clusters of the Adjusting Placement moved at random)",
             "n": wl.n, "m": wl.m, "levels": L, "K": BATCH5, "call_ms": call_ms,
@@ -196,7 +209,8 @@ def batched_row(cel, torch, dev, args):
             "algorithmic_bytes": B, "achieved_GBs": round(B / (kms * 1e-3) / 1e9, 2),
             "frac": round(B / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS, 5),
             "traffic": load_traffic("k_makespan_batch_wide"),
-            "makespan_min_ns": int(ms.min().item()), "makespan_max_ns": int(ms.max().item())}
+            "makespan_min_ns": int(ms.min().item()), "makespan_max_ns": int(ms.max().item()),
+            "parity": parity}
 
 
 def _timed(torch, f, reps=3):
@@ -234,6 +248,91 @@ def cpd_compare(cel, torch, g, d, bl, tl, prio, lev, lp, L):
                      "order_place": {"makespan_ns": int(ms_o[0].item()), "best_effort": be_o,
                                      "ms": op_ms}}
     return row, ndev
+
+
+def check_parity(pairs: dict) -> dict:
+    """{name: (gpu, oracle)} -> {name: equal}; arrays compare element by element."""
+    return {k: bool(np.array_equal(np.asarray(a), np.asarray(b))) for k, (a, b) in pairs.items()}
+
+
+def config_rows(cel, torch, dev, args):
+    """The smaller graphs, stage by stage: Kahn levels, b-level with the
+    priority order, DP clustering (R = 200), Adjusting Placement and the
+    makespan of the placement, each timed with HIP events (median of 5 after 2
+    warm-ups), beside the oracle's time per stage on one core (median of 3) and
+    a check of every result against the oracle's."""
+    from workloads import make_config
+    rows = {}
+    for cfg in (1, 2, 3):
+        wl = make_config(cfg, args.seed)
+        g = cel.Graph.from_arrays(wl, dev)
+        d = cel.Devices.from_arrays(wl)
+        stream = torch.cuda.current_stream()
+        names = ["topo_levels", "blevel", "cluster", "place", "makespan"]
+        rec = {k: [] for k in names}
+        out = None
+        for it in range(7):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+            ev[0].record(stream)
+            lev, oid, lp, L = cel.topo_levels(g)
+            ev[1].record(stream)
+            bl, _, pr, cp = cel.blevel(g, d, lev, lp, oid, L)
+            ev[2].record(stream)
+            cid, C, cut = cel.cluster(g, d, pr, 200, -1)
+            ev[3].record(stream)
+            cdev, ndev, cms, be = cel.place(g, d, cid, C)
+            ev[4].record(stream)
+            ms, st, fi = cel.makespan(g, d, pr, lev, lp, L, ndev, want_times=True)
+            ev[5].record(stream)
+            torch.cuda.synchronize()
+            if it >= 2:
+                for i, k in enumerate(names):
+                    rec[k].append(ev[i].elapsed_time(ev[i + 1]))
+            out = (lev, oid, lp, L, bl, pr, cp, cid, C, cut, ndev, cms, be, ms, fi)
+        stages = {k: round(float(np.median(v)), 3) for k, v in rec.items()}
+        lev, oid, lp, L, bl, pr, cp, cid, C, cut, ndev, cms, be, ms, fi = out
+        row = {"workload": wl.name, "n": wl.n, "m": wl.m, "levels": L, "D": wl.D,
+               "stages_ms": stages,
+               "placement_gen_ms": round(sum(stages[k] for k in names[:4]), 3),
+               "edges_per_s": wl.m / ((stages["blevel"] + stages["makespan"]) * 1e-3)}
+        if not args.no_cpu:
+            from oracle import oracle as O
+            import statistics
+            st_cpu = {}
+
+            def tm(name, f, reps=3):
+                ts, r = [], None
+                for _ in range(reps):
+                    a = time.perf_counter()
+                    r = f()
+                    ts.append(time.perf_counter() - a)
+                st_cpu[name] = round(statistics.median(ts) * 1e3, 3)
+                return r
+
+            aff = os.sched_getaffinity(0)
+            os.sched_setaffinity(0, {min(aff)})
+            try:
+                r_lev, r_oid, r_lp, r_L = tm("topo_levels", lambda: O.topo_levels(wl))
+                r_bl, _, r_pr, r_cp = tm("blevel", lambda: O.blevel(wl, r_lev, r_oid))
+                r_cid, r_C, r_cut = tm("cluster", lambda: O.cluster(wl, r_pr, 200, -1))
+                r_pl = tm("place", lambda: O.place(wl, r_cid, r_C))
+                r_ms, _, r_fi = tm("makespan", lambda: O.makespan(wl, r_pr, r_pl[1]))
+            finally:
+                os.sched_setaffinity(0, aff)
+            row["oracle_stages_ms"] = st_cpu
+            row["oracle_edges_per_s"] = wl.m / ((st_cpu["blevel"] + st_cpu["makespan"]) * 1e-3)
+            row["parity"] = check_parity({
+                "level": (lev.cpu().numpy(), r_lev), "order_id": (oid.cpu().numpy(), r_oid),
+                "level_ptr": (lp.cpu().numpy(), r_lp), "blevel": (bl.cpu().numpy(), r_bl),
+                "prio_order": (pr.cpu().numpy(), r_pr), "critical_path_ns": (cp, int(r_cp)),
+                "cluster_id": (cid.cpu().numpy(), r_cid), "cut_cost_ns": (cut, int(r_cut)),
+                "node_dev": (ndev.cpu().numpy(), r_pl[1]), "coarse_makespan_ns": (cms, int(r_pl[2])),
+                "best_effort": (be, int(r_pl[3])), "finish": (fi.cpu().numpy(), r_fi),
+                "makespan_ns": (ms.cpu().numpy(), r_ms)})
+        rows[f"config{cfg}"] = row
+        print(f"[bench] {wl.name}: placement-gen {row['placement_gen_ms']:.2f} ms", file=sys.stderr,
+              flush=True)
+    return rows
 
 
 MODEL_NAMES = {0: "fifo", 1: "insert", 2: "comm_tasks", 3: "insert+comm_tasks"}
@@ -303,6 +402,8 @@ def main() -> int:
     ap.add_argument("--no-models", action="store_true",
                     help="skip the device-model rows (insertion, transfers as tasks, "
                          "heterogeneous devices, co-location)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-stage rows of the 2k-, 20k- and 55k-node graphs")
     ap.add_argument("--no-batch", action="store_true",
                     help="skip the 1,024-candidate scoring row on the 200k-node DAG")
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
@@ -388,7 +489,7 @@ def main() -> int:
             for i, nm in enumerate(names):
                 record.setdefault(nm, []).append(ev[i].elapsed_time(ev[i + 1]))
         state.update(L=L, C=C, cp=cp, cut=cut, cms=cms, be=be, ms1=int(ms1[0].item()),
-                     msK=msK.cpu().numpy())
+                     msK=msK.cpu().numpy(), cid=cid, ndev=ndev, pr=pr)
 
     for _ in range(args.warmup):
         step()
@@ -444,7 +545,7 @@ def main() -> int:
                kstats.items()}
 
     # roofline of the dominant kernel of the measured (b-level + makespan) pass
-    dom = max(("k_blevel_sweep", "k_makespan_sweep"), key=lambda k: kernels[k]["avg_ms"])
+    dom = max(("k_blevel_sweep", "k_makespan_one"), key=lambda k: kernels[k]["avg_ms"])
     B = algorithmic_bytes(dom, n, m, 1)
     t_dom = kernels[dom]["avg_ms"] * 1e-3
     achieved = B / t_dom / 1e9
@@ -455,20 +556,23 @@ def main() -> int:
                 "ns_per_level": round(t_dom * 1e9 / L, 1)}
     # depth-latency ceiling of the measured pass: b-level and makespan are chains
     # of L dependent levels each; a level cannot take less than the dependent
-    # step measured by a one-wave probe on this GPU (a dependent LDS round trip
-    # plus a 6-step DPP prefix max, about 150 ns), so the pass cannot beat 2 L
-    # such steps whatever the bandwidth
-    t_level_ns = 150.0
-    B_pass = algorithmic_bytes("k_blevel_sweep", n, m, 1) + algorithmic_bytes("k_makespan_sweep",
+    # step the library's probe measures on this GPU right now (one wave: LDS
+    # gather -> 64-bit segmented max-plus DPP scan -> LDS write), so the pass
+    # cannot beat 2 L such steps whatever the bandwidth
+    probe = {name: round(cel.step_latency(v, 200000), 1)
+             for v, name in ((0, "wave_lds_ns"), (1, "block_barrier_ns"), (2, "wave_l2_ns"))}
+    t_level_ns = probe["wave_lds_ns"]
+    B_pass = algorithmic_bytes("k_blevel_sweep", n, m, 1) + algorithmic_bytes("k_makespan_one",
                                                                               n, m, 1)
     floor_s = 2 * L * t_level_ns * 1e-9
     roofline["depth_ceiling"] = {
-        "t_level_ns": t_level_ns, "levels": L, "pass_floor_ms": round(floor_s * 1e3, 3),
+        "t_level_ns": t_level_ns, "probe": probe, "levels": L,
+        "pass_floor_ms": round(floor_s * 1e3, 3),
         "frac_ceiling": round(B_pass / floor_s / 1e9 / HBM_PEAK_GBS, 5),
         "frac_pass": round(B_pass / (eval_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 6)}
     # the level sweeps are chains of L dependent levels: per-level latency
     per_level = {k: round(kernels[k]["avg_ms"] * 1e6 / L, 1)
-                 for k in ("k_kahn", "k_blevel_sweep", "k_makespan_sweep", "k_makespan_batch")
+                 for k in ("k_kahn", "k_blevel_sweep", "k_makespan_one", "k_makespan_batch")
                  if k in kernels}
     for k, v in kernels.items():
         b_ = algorithmic_bytes(k, n, m, BATCH if k == "k_makespan_batch" else 1)
@@ -482,6 +586,8 @@ def main() -> int:
                "achieved_GBs": round(Bk / tk / 1e9, 2), "frac": round(Bk / tk / 1e9 / HBM_PEAK_GBS, 5)}
 
     cpu = None
+    parity = None
+    cfg_rows = None if args.no_configs else config_rows(cel, torch, dev, args)
     if not args.no_cpu:
         # the oracle as it stands, one thread pinned to one core, every stage of
         # the path on the same graph (median of 3)
@@ -502,12 +608,21 @@ def main() -> int:
 
         try:
             lev_o, oid_o, _, _ = tm("topo_levels", lambda: O.topo_levels(wl))
-            _, _, pr_o, _ = tm("blevel", lambda: O.blevel(wl, lev_o, oid_o))
-            cid_o, C_o, _ = tm("cluster", lambda: O.cluster(wl, pr_o, 200, -1))
+            _, _, pr_o, cp_o = tm("blevel", lambda: O.blevel(wl, lev_o, oid_o))
+            cid_o, C_o, cut_o = tm("cluster", lambda: O.cluster(wl, pr_o, 200, -1))
             pl_o = tm("place", lambda: O.place(wl, cid_o, C_o))
-            tm("makespan", lambda: O.makespan(wl, pr_o, pl_o[1], want_times=False))
+            ms_o = tm("makespan", lambda: O.makespan(wl, pr_o, pl_o[1], want_times=False))
         finally:
             os.sched_setaffinity(0, aff)
+        # self-check: the timed GPU results against the oracle's on the same graph
+        parity = check_parity({
+            "critical_path_ns": (state["cp"], int(cp_o)), "clusters": (state["C"], int(C_o)),
+            "cut_cost_ns": (state["cut"], int(cut_o)),
+            "coarse_makespan_ns": (state["cms"], int(pl_o[2])),
+            "best_effort": (state["be"], int(pl_o[3])), "makespan_ns": (state["ms1"], int(ms_o[0][0])),
+            "prio_order": (state["pr"].cpu().numpy(), pr_o),
+            "cluster_id": (state["cid"].cpu().numpy(), cid_o),
+            "node_dev": (state["ndev"].cpu().numpy(), pl_o[1])})
         t_pass = (st_cpu["blevel"] + st_cpu["makespan"]) * 1e-3
         model = ""
         try:
@@ -553,12 +668,19 @@ def main() -> int:
         "batched_makespan": batched,
         "batched_scoring_200k": batch5,
         "cpu_baseline": cpu,
+        "parity": parity,
+        "configs": cfg_rows,
         "results": {"critical_path_ns": state["cp"], "clusters": state["C"],
                     "cut_cost_ns": state["cut"], "coarse_makespan_ns": state["cms"],
                     "best_effort": state["be"], "makespan_ns": state["ms1"],
                     "batch_makespan_min_ns": int(state["msK"].min())},
     }
     print(json.dumps(out))
+    bad = [k for r in [parity] + [(c or {}).get("parity") for c in (cfg_rows or {}).values()] +
+           [(batch5 or {}).get("parity")] if r for k, v in r.items() if v is False]
+    if bad:
+        print(f"[bench] PARITY MISMATCH against the oracle: {bad}", file=sys.stderr, flush=True)
+        return 1
     return 0
 
 

@@ -269,6 +269,19 @@ int cel_colocate(const cel_graph *g, const int32_t *order, const int32_t *group,
 int cel_timing(int enable);
 int cel_kernel_stats(char *buf, int buflen, int reset);
 
+/* Diagnostics: the dependent step that bounds a level-synchronous sweep
+ * (each level of the b-level recursion, eq. 3, and of the makespan, eq. 7,
+ * waits for the previous one).  Runs `steps` dependent iterations of gather
+ * -> 64-bit segmented max-plus wave scan -> write, each iteration's gather
+ * index taken from the previous result, and returns the time per iteration
+ * in *ns_per_step (host).  variant 0: one wave, gather from LDS; 1: a
+ * workgroup of 1024 threads, gather from LDS and a barrier after the write;
+ * 2: one wave, gather from a global array resident in L2.  Two launches of
+ * steps/8 and steps iterations are timed with HIP events and differenced, so
+ * launch overhead cancels.  1 <= steps <= 2^24.  Synchronises `stream`.
+ * Errors: CEL_E_ARG, CEL_E_HIP, CEL_E_NOMEM. */
+int cel_step_latency(int32_t variant, int32_t steps, double *ns_per_step, hipStream_t stream);
+
 /* Message describing the calling thread's last error ("" if none). */
 const char *cel_last_error(void);
 

@@ -21,7 +21,7 @@ COMM_OFF = 1
 CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
 EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_dfs_order", "cel_cluster", "cel_place", "cel_makespan",
-           "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_colocate", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
+           "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_colocate", "cel_step_latency", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
 class CelError(RuntimeError):
@@ -77,6 +77,8 @@ def lib() -> C.CDLL:
             getattr(L, f).restype = C.c_int
         L.cel_last_error.argtypes = []
         L.cel_last_error.restype = C.c_char_p
+        L.cel_step_latency.argtypes = [i32, i32, C.POINTER(C.c_double), vp]
+        L.cel_step_latency.restype = C.c_int
         L.cel_timing.argtypes = [C.c_int]
         L.cel_timing.restype = C.c_int
         L.cel_kernel_stats.argtypes = [C.c_char_p, C.c_int, C.c_int]
@@ -87,6 +89,14 @@ def lib() -> C.CDLL:
 
 def version() -> int:
     return lib().cel_version()
+
+
+def step_latency(variant: int = 0, steps: int = 200000) -> float:
+    """ns per dependent gather -> wave scan -> write step (variant 0: one wave
+    over LDS; 1: 1024 threads with a barrier; 2: one wave gathering from L2)."""
+    ns = C.c_double(0.0)
+    _check(lib().cel_step_latency(int(variant), int(steps), C.byref(ns), _stream()))
+    return ns.value
 
 
 def timing(enable: bool) -> bool:

@@ -1413,7 +1413,7 @@ extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int3
     k_runs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, level_ptr, level, gorder, devp, wx, sx, meta,
                                                  st);
     {
-      KTimer kt(s, "k_makespan_sweep");
+      KTimer kt(s, "k_makespan_one");
       k_makespan_one<1024, 1792, 5120><<<1, 1024, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq, devp,
                                                           sx, meta, finp, makespan, st);
     }

@@ -45,7 +45,7 @@ def test_traffic_only_while_the_sources_match(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "TRAFFIC_FILES", [str(p)])
     assert bench.load_traffic("k_kahn") == 12345.0
     assert bench.load_traffic("k_place") is None          # stale hash
-    assert bench.load_traffic("k_makespan_sweep") is None  # no row
+    assert bench.load_traffic("k_makespan_one") is None  # no row
     assert bench.load_traffic("not_a_kernel") is None
 
 
@@ -64,6 +64,6 @@ def test_stats_summary_orders_by_total(tmp_path):
 def test_algorithmic_bytes():
     n, m = 1000, 3000
     assert bench.algorithmic_bytes("k_blevel_sweep", n, m, 1) == 32 * n + 12 * m
-    assert bench.algorithmic_bytes("k_makespan_sweep", n, m, 1) == 33 * n + 21 * m
+    assert bench.algorithmic_bytes("k_makespan_one", n, m, 1) == 33 * n + 21 * m
     assert bench.algorithmic_bytes("k_makespan_batch", n, m, 5) == 24 * n + 12 * m + 5 * (9 * n + 9 * m)
     assert bench.algorithmic_bytes("k_kahn", n, m, 1) is None

@@ -164,12 +164,64 @@ def test_makespan_large_batches():
     cdev5, _, _, _ = O.place(wl5, cid5, C5)
     P5 = perturb_placements(cdev5, wl5.D, 1024, 0)[:, cid5]
     g5, d5 = up(wl5)
-    ms5, _, _ = cel.makespan(g5, d5, tt(pr5, np.int32), tt(lev5, np.int32), tt(lp5, np.int32), L5,
-                             tt(P5, np.uint8))
+    ms5, st5, fi5 = cel.makespan(g5, d5, tt(pr5, np.int32), tt(lev5, np.int32),
+                                 tt(lp5, np.int32), L5, tt(P5, np.uint8), want_times=True)
     ms5 = np_(ms5)
-    rows = [0, 1, 511, 777, 1022, 1023]
-    ref5, _, _ = O.makespan(wl5, pr5, P5[rows], want_times=False)
-    assert np.array_equal(ms5[rows], ref5)
+    # every one of the 1,024 makespans (the oracle's rows are independent, so
+    # slices of them run on host threads: ctypes releases the GIL)
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(8) as ex:
+        parts = list(ex.map(lambda a: O.makespan(wl5, pr5, P5[a:a + 64], want_times=False)[0],
+                            range(0, 1024, 64)))
+    assert np.array_equal(ms5, np.concatenate(parts))
+    # full start and finish arrays of rows spread over the batch
+    rows = [0, 1, 255, 256, 511, 777, 1022, 1023]
+    _, ref_st, ref_fi = O.makespan(wl5, pr5, P5[rows])
+    ridx = torch.tensor(rows, device=DEV)
+    assert np.array_equal(np_(fi5.index_select(0, ridx)), ref_fi)
+    assert np.array_equal(np_(st5.index_select(0, ridx)), ref_st)
+
+
+def _all_placements(n, D):
+    """Every device assignment of n nodes to D devices, [D**n, n] uint8 (row k
+    reads k in base D, node 0 the most significant digit)."""
+    k = np.arange(D ** n, dtype=np.int64)
+    digits = [(k // D ** (n - 1 - i)) % D for i in range(n)]
+    return np.stack(digits, axis=1).astype(np.uint8)
+
+
+@pytest.mark.parametrize("n,D,seed", [(10, 4, 0), (10, 2, 1), (9, 3, 2), (8, 4, 3), (6, 5, 4),
+                                      (1, 4, 5)])
+def test_makespan_brute_force_batch(n, D, seed):
+    """Every one of the D^n placements of a DAG of at most 10 nodes in ONE
+    batched call (up to 4^10 = 1,048,576 rows), row by row against the oracle;
+    the optimum over all placements lies between the lower bound max(CP0,
+    ceil(sum w / D)) and the makespan of Adjusting Placement's placement."""
+    wl = make_random_dag(950 + seed, n, p_edge=0.35, D=D, cap_frac=(1, 1),
+                         multi=(seed % 2 == 0))
+    lev, oid, lp, L = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid, want_tlevel=False)
+    P = _all_placements(n, D)
+    K = P.shape[0]
+    ref, _, _ = O.makespan(wl, pr, P, want_times=False)
+    g, d = up(wl)
+    ms, _, fi = cel.makespan(g, d, tt(pr, np.int32), tt(lev, np.int32), tt(lp, np.int32), L,
+                             tt(P, np.uint8), want_times=(K <= 4096))
+    got = np_(ms)
+    assert got.shape == (K,) and np.array_equal(got, ref)
+    if fi is not None:
+        assert np.array_equal(np_(fi), O.makespan(wl, pr, P)[2])
+    opt = int(got.min())
+    _, _, _, cp0 = O.blevel(wl, lev, oid, comm_off=True, want_tlevel=False)
+    assert opt >= max(int(cp0), -(-int(wl.w.sum()) // D))
+    cid = np.empty(n, np.int32)
+    cid[pr] = np.arange(n)  # every node its own cluster, in priority order
+    _, ndev, _, _ = cel.place(g, d, tt(cid, np.int32), n)
+    ms_p, _, _ = cel.makespan(g, d, tt(pr, np.int32), tt(lev, np.int32), tt(lp, np.int32), L, ndev)
+    assert opt <= int(np_(ms_p)[0])
+    # the row of Adjusting Placement's devices is that same value
+    row = int(sum(int(x) * D ** (n - 1 - i) for i, x in enumerate(np_(ndev))))
+    assert got[row] == int(np_(ms_p)[0])
 
 
 def _wide_layered(seed, widths, max_fanin, D):
@@ -637,8 +689,16 @@ def test_full_path_large(cfg):
     rm = O.makespan(wl, rb[2], P)
     ms, st, fi = cel.makespan(g, d, gb[2], gt[0], gt[2], gt[3], tt(P, np.uint8), want_times=True)
     assert np.array_equal(np_(ms), rm[0]) and np.array_equal(np_(fi), rm[2])
-    ms1, _, _ = cel.makespan(g, d, gb[2], gt[0], gt[2], gt[3], ndev)
+    # the single-placement path (device-grouped sweep) on Adjusting Placement's
+    # devices: every start and finish time of the 1.07M nodes, element by element
+    ms1, st1, fi1 = cel.makespan(g, d, gb[2], gt[0], gt[2], gt[3], ndev, want_times=True)
     assert np_(ms1)[0] == rm[0][0]
+    assert np.array_equal(np_(fi1)[0], rm[2][0]) and np.array_equal(np_(st1)[0], rm[1][0])
+    for k in (1, 3):  # random placements through the same path
+        msk, stk, fik = cel.makespan(g, d, gb[2], gt[0], gt[2], gt[3], tt(P[k], np.uint8),
+                                     want_times=True)
+        assert np_(msk)[0] == rm[0][k]
+        assert np.array_equal(np_(fik)[0], rm[2][k]) and np.array_equal(np_(stk)[0], rm[1][k])
 
 
 # ------------------------------------------------------------- CPD-TOPO order
@@ -1107,3 +1167,16 @@ def test_model_many_placements():
     wl, rt, rb = config(1, 0)
     check_model(wl, rb[2], random_placements(wl, 257, 8), models=(cel.MODEL_INSERT,
                                                                   cel.MODEL_COMM_TASKS))
+
+
+# ------------------------------------------------------------ diagnostics
+
+
+def test_step_latency_probe():
+    """The dependent-step probe behind the bench's depth ceiling returns a
+    plausible time per step for each variant (a few ns to a few us)."""
+    for v in (0, 1, 2):
+        ns = cel.step_latency(v, 20000)
+        assert 5.0 < ns < 5000.0, (v, ns)
+    with pytest.raises(cel.CelError):
+        cel.step_latency(3, 100)
