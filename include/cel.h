@@ -214,6 +214,26 @@ int cel_makespan(const cel_graph *g, const cel_devices *d, const int32_t *order,
                  int32_t K, const uint8_t *node_dev, int64_t *start, int64_t *finish,
                  int64_t *makespan, hipStream_t stream);
 
+/* cel_makespan for callers that cannot allocate device memory: code being
+ * captured into a HIP graph, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, outputs and results as cel_makespan; the call
+ * makes no hipMalloc, hipFree or other allocating call.  Its scratch is one
+ * fixed array of CEL_NOALLOC_SCRATCH_BYTES per GPU, created with the
+ * library's code object on that GPU and held until the process ends; it keeps
+ * the last call's contents (each call clears what it needs).  Inputs whose
+ * scratch bound, 65536 + 136 (n + 1) + 4 m + 9 K n bytes, exceeds that size
+ * are rejected with CEL_E_ARG before any work is queued (about 870k nodes
+ * with m = 2n at K = 1; 32 placements of a 200k-node graph).  Calls
+ * through this entry point take turns on a process-wide lock and return
+ * after their results are complete, so they never overlap; anything else
+ * that wrote the same array at the same time would race with them.
+ * Errors: as cel_makespan. */
+#define CEL_NOALLOC_SCRATCH_BYTES (128ull << 20)
+int cel_makespan_noalloc(const cel_graph *g, const cel_devices *d, const int32_t *order,
+                         const int32_t *level, const int32_t *level_ptr, int32_t n_levels,
+                         int32_t K, const uint8_t *node_dev, int64_t *start, int64_t *finish,
+                         int64_t *makespan, hipStream_t stream);
+
 /* Heterogeneous devices for cel_makespan_model (host arrays; a NULL member
  * keeps the homogeneous value): device x runs a node of compute time w in
  * ceil(w * tmul[x] / 1024) (1024 = the reference speed, 1 <= tmul <= 65536);

@@ -20,7 +20,7 @@ OK, E_ARG, E_CYCLE, E_OVERFLOW, E_HIP, E_NOMEM, E_ORDER = 0, -1, -2, -3, -4, -5,
 COMM_OFF = 1
 CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
-EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_dfs_order", "cel_cluster", "cel_place", "cel_makespan",
+EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_dfs_order", "cel_cluster", "cel_place", "cel_makespan", "cel_makespan_noalloc",
            "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_colocate", "cel_step_latency", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
@@ -65,6 +65,7 @@ def lib() -> C.CDLL:
         L.cel_cluster.argtypes = [G, Dv, vp, i32, i64, i32, vp, C.POINTER(i32), C.POINTER(i64), vp]
         L.cel_place.argtypes = [G, Dv, vp, i32, vp, vp, vp, C.POINTER(i64), C.POINTER(i32), vp]
         L.cel_makespan.argtypes = [G, Dv, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]
+        L.cel_makespan_noalloc.argtypes = [G, Dv, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]
         L.cel_cpd_order.argtypes = [G, vp, vp, vp, vp]
         L.cel_dfs_order.argtypes = [G, vp, vp]
         L.cel_order_place.argtypes = [G, Dv, vp, i32, vp, vp, C.POINTER(i32), vp]
@@ -72,6 +73,7 @@ def lib() -> C.CDLL:
         L.cel_makespan_model.argtypes = [G, Dv, C.POINTER(_Hetero), vp, i32, vp, i32, vp, vp, vp, vp]
         L.cel_colocate.argtypes = [G, vp, vp, i32, i32, vp, vp]
         for f in ("cel_topo_levels", "cel_blevel", "cel_cluster", "cel_place", "cel_makespan",
+                  "cel_makespan_noalloc",
                   "cel_cpd_order", "cel_dfs_order", "cel_order_place", "cel_comm_sums", "cel_makespan_model",
                   "cel_colocate", "cel_version"):
             getattr(L, f).restype = C.c_int
@@ -325,8 +327,11 @@ def comm_sums(g: Graph, d: Devices, cluster_id=None):
     return ec.value, ws.value
 
 
-def makespan(g: Graph, d: Devices, order, level, level_ptr, n_levels, node_dev, want_times=False):
-    """node_dev uint8 [n] or [K, n] -> (makespan int64[K], start, finish) ([K, n] or None)"""
+def makespan(g: Graph, d: Devices, order, level, level_ptr, n_levels, node_dev, want_times=False,
+             noalloc=False):
+    """node_dev uint8 [n] or [K, n] -> (makespan int64[K], start, finish) ([K, n] or None).
+    noalloc=True calls cel_makespan_noalloc (the library allocates nothing;
+    the outputs are still allocated here by torch)."""
     n = g.n
     nd = node_dev.contiguous()
     K = 1 if nd.dim() == 1 else nd.shape[0]
@@ -334,8 +339,9 @@ def makespan(g: Graph, d: Devices, order, level, level_ptr, n_levels, node_dev, 
     st = torch.empty((K, max(n, 1)), dtype=torch.int64, device=g.device) if want_times else None
     fi = torch.empty((K, max(n, 1)), dtype=torch.int64, device=g.device) if want_times else None
     gc, dc = g._c(), d._c()
-    _check(lib().cel_makespan(C.byref(gc), C.byref(dc), _p(order), _p(level), _p(level_ptr),
-                              int(n_levels), int(K), _p(nd), _p(st), _p(fi), _p(ms), _stream()))
+    f = lib().cel_makespan_noalloc if noalloc else lib().cel_makespan
+    _check(f(C.byref(gc), C.byref(dc), _p(order), _p(level), _p(level_ptr), int(n_levels), int(K),
+             _p(nd), _p(st), _p(fi), _p(ms), _stream()))
     if want_times:
         st, fi = st[:, :n], fi[:, :n]
     return ms, st, fi

@@ -13,6 +13,7 @@ namespace cel {
 constexpr int64_t kLim = int64_t(1) << 62;  // every sum the path forms stays below this
 constexpr int64_t kInf = INT64_MAX;         // comparison sentinel only
 constexpr int kMaxD = 255;
+constexpr uint64_t kNoAllocScratchBytes = CEL_NOALLOC_SCRATCH_BYTES;  // cel_makespan_noalloc's array
 
 // error bits raised by device-side checks (Status::err)
 enum : uint32_t { EB_ARG = 1u, EB_CYCLE = 2u, EB_OVERFLOW = 4u, EB_ORDER = 8u };
@@ -284,11 +285,16 @@ int set_error(int code, const char *fmt, ...);
 // arena is held for the object's lifetime, so calls on one stream from
 // several host threads take turns; calls on different streams use different
 // arenas.  Pointers stay valid until the object dies.
+// The second form bumps through a fixed device range [base, base + cap) that
+// the caller owns and never allocates: a request beyond `cap` fails with
+// CEL_E_ARG.
 struct Arena;
 class Scratch {
  public:
   explicit Scratch(hipStream_t s);
+  Scratch(hipStream_t s, char *base, size_t cap) : s_(s), base_(base), cap_(cap) {}
   ~Scratch();
+  size_t used() const { return off_; }
   Scratch(const Scratch &) = delete;
   Scratch &operator=(const Scratch &) = delete;
   // allocate `count` elements of T (count may be 0: a 1-element block is taken)
@@ -302,6 +308,8 @@ class Scratch {
   hipStream_t s_;
   Arena *a_ = nullptr;
   int err_ = CEL_OK;
+  char *base_ = nullptr;  // fixed range (second form), else null
+  size_t cap_ = 0, off_ = 0;
 };
 
 // Launch-configuration helpers

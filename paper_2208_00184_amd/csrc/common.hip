@@ -106,6 +106,14 @@ Scratch::Scratch(hipStream_t s) : s_(s) {
 int Scratch::raw(void **out, size_t bytes) {
   if (err_ != CEL_OK) return err_;
   const size_t sz = (bytes + kAlign - 1) / kAlign * kAlign;
+  if (base_) {  // fixed range: bump, never allocate
+    if (sz > cap_ - off_)
+      return err_ = set_error(CEL_E_ARG, "the call needs more than the %zu bytes of fixed scratch",
+                              cap_);
+    *out = base_ + off_;
+    off_ += sz;
+    return CEL_OK;
+  }
   a_->need += sz;
   while (a_->blk < a_->blocks.size() && a_->off + sz > a_->blocks[a_->blk].second) {
     a_->blk++;

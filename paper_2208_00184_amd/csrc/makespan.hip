@@ -17,6 +17,8 @@
 //
 // One workgroup evaluates one placement; a batch of K placements runs K
 // independent workgroups that share the graph structure through L2/MALL.
+#include <map>
+#include <mutex>
 #include <type_traits>
 
 #include "cel_internal.h"
@@ -1348,18 +1350,26 @@ using namespace cel;
 
 CEL_PHASE_READER(cel_debug_phases_makespan)
 
-extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int32_t *order,
-                            const int32_t *level, const int32_t *level_ptr, int32_t L, int32_t K,
-                            const uint8_t *node_dev, int64_t *start, int64_t *finish,
-                            int64_t *makespan, hipStream_t s) {
-  const char *fn = "cel_makespan";
+static int check_makespan_args(const char *fn, const cel_graph *g, const cel_devices *d,
+                               const int32_t *order, const int32_t *level,
+                               const int32_t *level_ptr, int32_t L, int32_t K,
+                               const uint8_t *node_dev, const int64_t *makespan) {
   CEL_TRY(check_host_graph(g, fn));
   CEL_TRY(check_host_devices(d, fn));
   const int32_t n = g->n;
   if (!makespan || !level_ptr || K < 1 || (n > 0 && (!order || !level || !node_dev)))
     return set_error(CEL_E_ARG, "%s: NULL argument or K < 1", fn);
   if (L < 0 || L > n || (n > 0 && L == 0)) return set_error(CEL_E_ARG, "%s: n_levels out of range", fn);
-  Scratch sc(s);
+  return CEL_OK;
+}
+
+// The whole call on scratch from `sc` (the arena, or the fixed array of
+// cel_makespan_noalloc).
+static int makespan_impl(const char *fn, const cel_graph *g, const cel_devices *d,
+                         const int32_t *order, const int32_t *level, const int32_t *level_ptr,
+                         int32_t L, int32_t K, const uint8_t *node_dev, int64_t *start,
+                         int64_t *finish, int64_t *makespan, Scratch &sc, hipStream_t s) {
+  const int32_t n = g->n;
   Status *st;
   int32_t *tmp, *pos, *pptr, *pidx;
   int64_t *wp, *cq, *finp;
@@ -1458,4 +1468,77 @@ extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int3
   CEL_TRY(read_status(st, &h, s));
   if (h.err) return status_error(h, fn);
   return CEL_OK;
+}
+
+extern "C" int cel_makespan(const cel_graph *g, const cel_devices *d, const int32_t *order,
+                            const int32_t *level, const int32_t *level_ptr, int32_t L, int32_t K,
+                            const uint8_t *node_dev, int64_t *start, int64_t *finish,
+                            int64_t *makespan, hipStream_t s) {
+  const char *fn = "cel_makespan";
+  CEL_TRY(check_makespan_args(fn, g, d, order, level, level_ptr, L, K, node_dev, makespan));
+  Scratch sc(s);
+  return makespan_impl(fn, g, d, order, level, level_ptr, L, K, node_dev, start, finish, makespan,
+                       sc, s);
+}
+
+// ----------------------------------------------- the allocation-free variant
+//
+// Its scratch is one fixed device array per GPU, a module-scope __device__
+// variable: the runtime creates it when it loads the library's code object on
+// a device and keeps it until the process ends.  Host code may not use the
+// array's name as a device address; the address comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+namespace {
+std::mutex g_fixed_mu;               // one call at a time per process (the array is shared)
+std::map<int, char *> g_fixed_ptr;   // device ordinal -> address of that device's array
+}  // namespace
+
+static int fixed_scratch(char **out) {  // g_fixed_mu held
+  int dev = 0;
+  CEL_HIP(hipGetDevice(&dev));
+  auto it = g_fixed_ptr.find(dev);
+  if (it == g_fixed_ptr.end()) {
+    void *p = nullptr;
+    CEL_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return set_error(CEL_E_HIP, "hipGetSymbolAddress returned NULL for the fixed scratch");
+    it = g_fixed_ptr.emplace(dev, (char *)p).first;
+  }
+  *out = it->second;
+  return CEL_OK;
+}
+
+// A bound on the scratch one call takes: per node at most 136 bytes (position
+// maps, relabelled CSR rows, costs, the device-grouped order and its sort
+// buffers, per-level tile lists, for K = 1), 4 bytes per edge (relabelled
+// in-edges), 9 bytes per node and placement (devices and finish times), and
+// 64 KiB for block partials and 256-byte rounding.
+static uint64_t makespan_scratch_bound(int64_t n, int64_t m, int64_t K) {
+  return 65536ull + 136ull * (uint64_t)(n + 1) + 4ull * (uint64_t)m + 9ull * (uint64_t)K * (uint64_t)n;
+}
+
+extern "C" int cel_makespan_noalloc(const cel_graph *g, const cel_devices *d, const int32_t *order,
+                                    const int32_t *level, const int32_t *level_ptr, int32_t L,
+                                    int32_t K, const uint8_t *node_dev, int64_t *start,
+                                    int64_t *finish, int64_t *makespan, hipStream_t s) {
+  const char *fn = "cel_makespan_noalloc";
+  CEL_TRY(check_makespan_args(fn, g, d, order, level, level_ptr, L, K, node_dev, makespan));
+  const uint64_t need = makespan_scratch_bound(g->n, g->m, K);
+  if (need > kNoAllocScratchBytes)
+    return set_error(CEL_E_ARG,
+                     "%s: n = %d, m = %d, K = %d may need %llu bytes of scratch, above the fixed "
+                     "%llu (use cel_makespan)",
+                     fn, g->n, g->m, K, (unsigned long long)need,
+                     (unsigned long long)kNoAllocScratchBytes);
+  std::lock_guard<std::mutex> lk(g_fixed_mu);
+  char *base = nullptr;
+  CEL_TRY(fixed_scratch(&base));
+  Scratch sc(s, base, kNoAllocScratchBytes);
+  const int rc = makespan_impl(fn, g, d, order, level, level_ptr, L, K, node_dev, start, finish,
+                               makespan, sc, s);
+  // a failed call may leave kernels queued that use the array: drain them
+  // before the next call may take it
+  if (rc != CEL_OK) (void)hipStreamSynchronize(s);
+  return rc;
 }
