@@ -752,7 +752,15 @@ int orc_makespan(const orc_graph *g, const orc_devices *d, const int32_t *order,
  *   order they are issued: start = max(fin[u], send free[a], receive free[b]).
  *   A successor on b is ready for u's output when that transfer ends; outputs
  *   consumed on their own device need no transfer.  Compute never waits for a
- *   channel other than through its inputs. */
+ *   channel other than through its inputs.
+ * ORC_MODEL_COMM_BLOCK (alone; FIFO devices): the same transfers, one per
+ *   (producer, other device holding a successor) in increasing device order,
+ *   are operations on the devices themselves (Section 6.1 places a transfer
+ *   node on every device that sends or receives).  Each enters the compute
+ *   queue of both its sending and its receiving device right after its
+ *   producer, starts when both devices are free and holds both for c[u]:
+ *   start = max(free[a], free[b]), then free[a] = free[b] = start + c[u].
+ *   A successor on b is ready for u's output when that transfer ends. */
 /* Heterogeneous devices: node v takes ceil(w[v] * tmul[x] / 1024) on device x,
  * and its output takes ceil(ob[v] / bw[a][b]) + lat[a][b] from device a to b.
  * h == NULL, or a NULL member, means the homogeneous value (1024, d->bw,
@@ -822,7 +830,9 @@ int orc_makespan_model(const orc_graph *g, const orc_devices *d, const orc_heter
   if ((rc = check_devices(d))) return rc;
   if ((rc = check_hetero(g, d, h))) return rc;
   int32_t n = g->n, D = d->D;
-  if (K < 1 || !makespan || (n > 0 && !node_dev) || (model & ~3)) return ORC_E_ARG;
+  /* COMM_BLOCK replaces both other bits: transfers on the compute queues */
+  if (K < 1 || !makespan || (n > 0 && !node_dev) || (model & ~7) || ((model & 4) && (model & 3)))
+    return ORC_E_ARG;
   for (int64_t i = 0; i < (int64_t)K * n; i++)
     if (node_dev[i] >= D) return ORC_E_ARG;
   int32_t *pos = malloc(sizeof(int32_t) * (size_t)(n + 1));
@@ -830,13 +840,14 @@ int orc_makespan_model(const orc_graph *g, const orc_devices *d, const orc_heter
   free(pos);
   if (rc) return rc;
   const int insert = model & ORC_MODEL_INSERT, tasks = model & ORC_MODEL_COMM_TASKS;
+  const int block = model & ORC_MODEL_COMM_BLOCK;
   int64_t *c = malloc(sizeof(int64_t) * (size_t)(n + 1));
   for (int32_t v = 0; v < n; v++) c[v] = comm_of(g->ob[v], d->bw, d->lat);
   int64_t *fin = malloc(sizeof(int64_t) * (size_t)(n + 1));
   int64_t *avail = malloc(sizeof(int64_t) * (size_t)D);
   int64_t *snd = malloc(sizeof(int64_t) * (size_t)D), *rcv = malloc(sizeof(int64_t) * (size_t)D);
   /* arrival of u's output on device b (transfers only) */
-  int64_t *arr = tasks ? malloc(sizeof(int64_t) * ((size_t)n * D + 1)) : NULL;
+  int64_t *arr = tasks || block ? malloc(sizeof(int64_t) * ((size_t)n * D + 1)) : NULL;
   char *wants = malloc((size_t)D);
   /* busy intervals per device, sorted by start (insertion only) */
   int64_t *bs = insert ? malloc(sizeof(int64_t) * ((size_t)n + 1)) : NULL;
@@ -857,7 +868,7 @@ int orc_makespan_model(const orc_graph *g, const orc_devices *d, const orc_heter
         int32_t u = g->in_idx[e];
         int64_t r;
         if (dev[u] == dv) r = fin[u];
-        else if (tasks) r = arr[(int64_t)u * D + dv];
+        else if (tasks || block) r = arr[(int64_t)u * D + dv];
         else r = fin[u] + (h ? link_comm(h, d, g->ob[u], dev[u], dv) : c[u]);
         if (r > ready) ready = r;
       }
@@ -903,6 +914,21 @@ int orc_makespan_model(const orc_graph *g, const orc_devices *d, const orc_heter
           int64_t cv = h ? link_comm(h, d, g->ob[v], dv, b) : c[v];
           arr[(int64_t)v * D + b] = t0 + cv;
           snd[dv] = rcv[b] = t0 + cv;
+        }
+      }
+      if (block) {
+        /* each transfer is a task on both devices' compute queues, entered
+         * right after its producer: it starts when both devices are free
+         * (the sender's queue already ends at or after fin[v]) and holds
+         * both until it ends */
+        for (int32_t x = 0; x < D; x++) wants[x] = 0;
+        for (int32_t e = g->out_ptr[v]; e < g->out_ptr[v + 1]; e++) wants[dev[g->out_idx[e]]] = 1;
+        for (int32_t b = 0; b < D; b++) {
+          if (b == dv || !wants[b]) continue;
+          int64_t t0 = avail[dv] > avail[b] ? avail[dv] : avail[b];
+          int64_t cv = h ? link_comm(h, d, g->ob[v], dv, b) : c[v];
+          arr[(int64_t)v * D + b] = t0 + cv;
+          avail[dv] = avail[b] = t0 + cv;
         }
       }
     }

@@ -116,9 +116,13 @@ int orc_makespan(const orc_graph *g, const orc_devices *d, const int32_t *order,
  * node into its device's busy intervals (eq. 7's slot rule at node level).
  * COMM_TASKS: transfers are tasks on per-device send and receive channels,
  * one per (producer, other device holding a successor), issued in increasing
- * device order (Section 6.1's runtime model).  `order` is any topological
- * order; start/finish ([K][n], by node id) may be NULL. */
-enum { ORC_MODEL_INSERT = 1, ORC_MODEL_COMM_TASKS = 2 };
+ * device order (Section 6.1's runtime model).  COMM_BLOCK (alone, with FIFO
+ * devices): each such transfer is instead a task on the compute queues of
+ * both the sending and the receiving device (Section 6.1's transfer
+ * operations on the devices that send or receive), entered into both queues
+ * right after its producer and starting when both are free.  `order` is any
+ * topological order; start/finish ([K][n], by node id) may be NULL. */
+enum { ORC_MODEL_INSERT = 1, ORC_MODEL_COMM_TASKS = 2, ORC_MODEL_COMM_BLOCK = 4 };
 /* Heterogeneous devices (NULL members: homogeneous): tmul[D] scales compute
  * time by tmul / 1024 (rounded up, 1 <= tmul <= 65536); bw[D*D], lat[D*D]
  * give the link from device a to b at [a * D + b] (diagonal unused). */

@@ -229,7 +229,7 @@ def makespan(wl, order, node_dev, want_times=True):
     return ms, st, fi
 
 
-MODEL_INSERT, MODEL_COMM_TASKS = 1, 2
+MODEL_INSERT, MODEL_COMM_TASKS, MODEL_COMM_BLOCK = 1, 2, 4
 
 
 class _Hetero(C.Structure):
@@ -237,8 +237,8 @@ class _Hetero(C.Structure):
 
 
 def makespan_model(wl, order, node_dev, model, want_times=True, tmul=None, bw=None, lat=None):
-    """Makespan under the device models (bits MODEL_INSERT, MODEL_COMM_TASKS; 0 is
-    makespan()'s schedule) -> (makespan int64[K], start, finish) ([K, n] or None).
+    """Makespan under the device models (bits MODEL_INSERT, MODEL_COMM_TASKS, or
+    MODEL_COMM_BLOCK alone; 0 is makespan()'s schedule) -> (makespan int64[K], start, finish) ([K, n] or None).
     tmul [D] (compute time x tmul / 1024), bw / lat [D, D] (link a -> b): heterogeneous
     devices; all None = homogeneous."""
     k = _Keep(wl)

@@ -146,3 +146,52 @@ def makespan_augmented(wl, order, dev):
 
 def all_placements(n, D):
     return itertools.product(range(D), repeat=n)
+
+
+def makespan_blocking_transfers(wl, order, dev):
+    """Makespan when every transfer occupies the compute queues of both the
+    sending and the receiving device, as a longest path in a task DAG.
+
+    Tasks: the nodes, plus one transfer task (u, b) of length c[u] for each
+    producer u and each other device b holding a successor of u.  Walking
+    ``order``, each node is appended to its device's queue, then its transfer
+    tasks (increasing b) to the queues of both its device and b.  Edges: u ->
+    (u, b) -> every successor of u on b; u -> successors on u's own device;
+    consecutive tasks of each device queue.  A task finishes at its length
+    plus the latest finish among its predecessors (0 if none): a formulation
+    independent of the oracle's time-stepping.  Returns (makespan, finish by
+    node id).
+    """
+    c = comm(wl)
+    S = succs(wl)
+    queue = {}  # device -> list of tasks in queue order
+    length = {}
+    preds_of = {}
+    for v in order:
+        v = int(v)
+        d = int(dev[v])
+        length[("n", v)] = int(wl.w[v])
+        queue.setdefault(d, []).append(("n", v))
+        for b in sorted({int(dev[s]) for s in S[v]} - {d}):
+            t = ("t", v, b)
+            length[t] = c[v]
+            preds_of.setdefault(t, set()).add(("n", v))
+            queue[d].append(t)
+            queue.setdefault(b, []).append(t)
+    for v in range(wl.n):
+        for s in S[v]:
+            src = ("n", v) if dev[s] == dev[v] else ("t", v, int(dev[s]))
+            preds_of.setdefault(("n", int(s)), set()).add(src)
+    for q in queue.values():
+        for a, b in zip(q, q[1:]):
+            preds_of.setdefault(b, set()).add(a)
+
+    import sys
+    sys.setrecursionlimit(max(10000, 8 * len(length) + 100))
+
+    @lru_cache(maxsize=None)
+    def fin(t):
+        return length[t] + max([fin(p) for p in preds_of.get(t, ())] + [0])
+
+    f = [fin(("n", v)) for v in range(wl.n)]
+    return (max(f) if f else 0), f

@@ -843,11 +843,47 @@ def test_model_comm_tasks_properties():
     assert int(ms[0]) == sum(range(1, n + 1)) + (n - 1) * (2 + 1)  # c = ceil(3/2) + 1
 
 
+def test_model_comm_block_task_dag():
+    """Transfers occupying both devices' compute queues: every finish time
+    equals the longest path of an explicit task DAG (nodes, one transfer task
+    per producer and other consuming device, device queue edges) built in
+    tests/brute.py; and, elementwise, finish(model 4) >= finish(model 2) >=
+    finish(model 0): the blocking model keeps every constraint of the
+    channel model (a device's queue serialises its sends and receives, and
+    compute too), which keeps every constraint of contention-free comm."""
+    rng = np.random.default_rng(77)
+    for s in range(40):
+        n = 2 + (s * 7) % 40
+        wl = make_random_dag(6000 + s, n, p_edge=min(0.5, 3.0 / n), D=1 + s % 6,
+                             multi=(s % 4 == 0), zero_frac=0.2 if s % 3 == 0 else 0.0)
+        order = _rand_topo(wl, rng)
+        dev = rng.integers(0, wl.D, n).astype(np.uint8)
+        ms4, st4, fi4 = O.makespan_model(wl, order, dev, O.MODEL_COMM_BLOCK)
+        ref_ms, ref_fi = B.makespan_blocking_transfers(wl, order, dev)
+        assert fi4[0].tolist() == ref_fi and int(ms4[0]) == ref_ms, s
+        assert np.array_equal(st4[0], fi4[0] - np.asarray(wl.w, np.int64))
+        _, _, fi2 = O.makespan_model(wl, order, dev, O.MODEL_COMM_TASKS)
+        _, _, fi0 = O.makespan_model(wl, order, dev, 0)
+        assert np.all(fi4[0] >= fi2[0]) and np.all(fi2[0] >= fi0[0]), s
+        one = np.zeros(n, np.uint8)  # one device: no transfers at all
+        a = O.makespan_model(wl, order, one, 0)
+        b = O.makespan_model(wl, order, one, O.MODEL_COMM_BLOCK)
+        assert all(np.array_equal(x, y) for x, y in zip(a, b))
+    # a chain alternating two devices never finds a device busy: sum w + sum c
+    n = 9
+    wl = from_edges(n, [(i, i + 1) for i in range(n - 1)], list(range(1, n + 1)), [3] * n, 2,
+                    [100, 100], 2, 1)
+    dev = np.array([i % 2 for i in range(n)], np.uint8)
+    ms, _, _ = O.makespan_model(wl, np.arange(n, dtype=np.int32), dev, O.MODEL_COMM_BLOCK)
+    assert int(ms[0]) == sum(range(1, n + 1)) + (n - 1) * (2 + 1)
+
+
 def test_model_rejects_bad_inputs():
     wl = from_edges(3, [(0, 1), (1, 2)], [1, 1, 1], [0, 0, 0], 2, [5, 5], 1, 0)
     dev = np.zeros(3, np.uint8)
-    with pytest.raises(RuntimeError):
-        O.makespan_model(wl, np.array([0, 1, 2], np.int32), dev, 4)
+    for bad in (5, 6, 7, 8):  # the blocking model combines with no other bit
+        with pytest.raises(RuntimeError):
+            O.makespan_model(wl, np.array([0, 1, 2], np.int32), dev, bad)
     with pytest.raises(RuntimeError):
         O.makespan_model(wl, np.array([1, 0, 2], np.int32), dev, 1)
     with pytest.raises(RuntimeError):
