@@ -335,7 +335,7 @@ def config_rows(cel, torch, dev, args):
     return rows
 
 
-MODEL_NAMES = {0: "fifo", 1: "insert", 2: "comm_tasks", 3: "insert+comm_tasks"}
+MODEL_NAMES = {0: "fifo", 1: "insert", 2: "comm_tasks", 3: "insert+comm_tasks", 4: "comm_block"}
 
 
 def models_row(cel, torch, g, d, prio, ndev, seed, K=64):

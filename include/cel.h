@@ -59,7 +59,8 @@ enum { CEL_COMM_OFF = 1 /* treat every c[v] as 0 (compute-only critical path) */
 /* cel_makespan_model model bits */
 enum {
   CEL_MODEL_INSERT = 1,     /* first-fit insertion into each device's idle slots */
-  CEL_MODEL_COMM_TASKS = 2  /* transfers as tasks on per-device send/receive channels */
+  CEL_MODEL_COMM_TASKS = 2, /* transfers as tasks on per-device send/receive channels */
+  CEL_MODEL_COMM_BLOCK = 4  /* transfers as operations on both devices' compute queues */
 };
 
 /* cel_cluster modes */
@@ -258,11 +259,17 @@ typedef struct {
  * holding a successor of p, in increasing device order, each taking c[p] and
  * holding p's device's send channel and the target's receive channel:
  * start = max(finish of p, both channels' previous transfer end).
+ * CEL_MODEL_COMM_BLOCK (alone, FIFO devices): the same transfers are
+ * operations on the devices themselves (Section 6.1 adds a transfer node on
+ * every device that sends or receives): each enters the compute queue of the
+ * sending and of the receiving device right after its producer, starts when
+ * both are free and holds both for its duration.
  * h: heterogeneous devices (cel_hetero; node durations and link costs follow
  * it), or NULL.
  * Inputs: order [n] any topological order (permutation with pos[u] < pos[v]
  * on every edge); K >= 1; node_dev [K][n] uint8, each < D; D <= 64; model a
- * combination of the CEL_MODEL_* bits.
+ * combination of CEL_MODEL_INSERT and CEL_MODEL_COMM_TASKS, or
+ * CEL_MODEL_COMM_BLOCK alone.
  * Outputs: start, finish [K][n] by node id, or NULL; makespan [K] (device).
  * Errors: CEL_E_ARG (also D > 64), CEL_E_ORDER, CEL_E_OVERFLOW, CEL_E_HIP,
  * CEL_E_NOMEM. */

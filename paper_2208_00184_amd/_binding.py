@@ -271,7 +271,7 @@ def order_place(g: Graph, d: Devices, cluster_id, n_clusters):
     return cdev[:n_clusters], ndev[:n], be.value
 
 
-MODEL_INSERT, MODEL_COMM_TASKS = 1, 2
+MODEL_INSERT, MODEL_COMM_TASKS, MODEL_COMM_BLOCK = 1, 2, 4
 
 
 def makespan_model(g: Graph, d: Devices, order, node_dev, model, want_times=False, tmul=None,

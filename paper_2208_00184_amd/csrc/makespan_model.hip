@@ -410,9 +410,13 @@ __device__ inline bool lane_insert(int64_t *A, int64_t *B, int64_t *ta, int64_t 
   return true;
 }
 
-template <bool INS, bool TASKS, bool HET>
+template <bool INS, bool TASKS, bool HET, bool BLOCK = false>
 __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
-  __shared__ int64_t s_T[TASKS ? 64 * 64 : 1];  // arrival of slot j's output on device b
+  // transfers whose arrivals the inputs read: on channels (TASKS) or on the
+  // devices' compute queues (BLOCK)
+  constexpr bool ARR = TASKS || BLOCK;
+  static_assert(!(BLOCK && (INS || TASKS)), "the blocking model combines with no other bit");
+  __shared__ int64_t s_T[ARR ? 64 * 64 : 1];  // arrival of slot j's output on device b
   __shared__ int32_t s_bw[HET ? kHetD * kHetD : 1], s_lat[HET ? kHetD * kHetD : 1];
   __shared__ int64_t s_ta[INS ? 64 * kTail : 1], s_tb[INS ? 64 * kTail : 1];  // gap tails
   __shared__ unsigned long long s_lst[64];  // slots of the segment by device
@@ -434,8 +438,8 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
   const int32_t n = a.n;
   const uint8_t *dev = a.devp + k * n;
   int64_t *fin = a.finp + k * n;
-  const uint64_t *dm = TASKS ? a.dmask + k * n : nullptr;
-  const int64_t *of = TASKS ? a.aoff + k * n : nullptr;
+  const uint64_t *dm = ARR ? a.dmask + k * n : nullptr;
+  const int64_t *of = ARR ? a.aoff + k * n : nullptr;
   // device `lane`'s state
   int64_t last = 0;   // free time (FIFO) or end of the last task (insertion)
   int32_t gcnt = 0;   // idle gaps stored
@@ -467,7 +471,7 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
       nx_q[1] = f4.y;
       nx_q[2] = f4.z;
       nx_q[3] = f4.w;
-      if (TASKS) {
+      if (ARR) {
         nx_dm = dm[q];
         nx_off = of[q];
       }
@@ -490,9 +494,9 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
     // A: inputs from before the window
     const bool heavy = i1 - i0 > kMmLight;
     if (!heavy) {
-      fold_batch<TASKS, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, q4, dv, ext, msk, bad);
-      fold_inputs<TASKS, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, i0 + 4, i1, 1, dv, ext, msk,
-                              bad);
+      fold_batch<ARR, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, q4, dv, ext, msk, bad);
+      fold_inputs<ARR, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, i0 + 4, i1, 1, dv, ext, msk,
+                            bad);
     }
     for (uint64_t hv = __ballot(heavy); hv; hv &= hv - 1) {
       const int h = __builtin_ctzll(hv);
@@ -500,8 +504,8 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
       const int32_t dh = __builtin_amdgcn_readlane(dv, h);
       int64_t mx = 0;
       uint64_t mk = 0;
-      fold_inputs<TASKS, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, e0 + lane, e1, 64, dh, mx, mk,
-                              bad);
+      fold_inputs<ARR, HET>(a, dev, fin, dm, of, s_bw, s_lat, P0, e0 + lane, e1, 64, dh, mx, mk,
+                            bad);
       for (int off = 32; off > 0; off >>= 1) {
         const int64_t o = __shfl_xor(mx, off);
         mx = o > mx ? o : mx;
@@ -536,11 +540,45 @@ __global__ void __launch_bounds__(64) k_makespan_model(MmArgs a, Status *st) {
         const int32_t dq = __shfl(dv, q);
         int64_t t = fq;
         if (dq != dv) {
-          if (TASKS) t = s_T[q * 64 + dv];
+          if (ARR) t = s_T[q * 64 + dv];
           else if (HET) t = fq + link_c(xq, s_bw[dq * kHetD + dv], s_lat[dq * kHetD + dv]);
           else t = fq + xq;
         }
         if (has && t > r) r = t;
+      }
+      if (BLOCK) {
+        // Transfers sit on the compute queues: a slot's transfers delay the
+        // devices of later slots of the segment, so its slots are placed one
+        // at a time, in order, each followed by its transfers (one per
+        // destination device, increasing), from device states held in lanes
+        for (uint64_t sm = __ballot(inseg); sm; sm &= sm - 1) {
+          const int j = __builtin_ctzll(sm);
+          CEL_TCOUNT(14);
+          const int32_t dj = __builtin_amdgcn_readlane(dv, j);
+          const int64_t rj = readlane64(r, j), wj = readlane64(wd, j);
+          const int64_t lj = readlane64(last, dj);
+          const int64_t f = (rj > lj ? rj : lj) + wj;
+          int64_t qe = f;  // end of the sending device's queue
+          const uint64_t dmj = (uint64_t)readlane64((int64_t)mydm, j);
+          const int64_t cj = readlane64(c, j);
+          for (uint64_t x = dmj; x; x &= x - 1) {
+            const int b = __builtin_ctzll(x);
+            const int64_t lb = readlane64(last, b);
+            const int64_t t0 = qe > lb ? qe : lb;
+            qe = t0 + (HET ? link_c(cj, s_bw[dj * kHetD + b], s_lat[dj * kHetD + b]) : cj);
+            last = setlane<int64_t>(last, qe, b);
+            tcur = setlane<int64_t>(tcur, qe, b);
+          }
+          last = setlane<int64_t>(last, qe, dj);
+          finw = setlane<int64_t>(finw, f, j);
+          if ((dmj >> lane) & 1) {
+            s_T[j * 64 + lane] = tcur;
+            a.pool[readlane64(myoff, j) + __builtin_popcountll(dmj & below(lane))] = tcur;
+          }
+          lds_order();
+        }
+        s0 = s1;
+        continue;
       }
       if (inseg) atomicOr(&s_lst[dv], 1ull << lane);
       wave_lds_sync();
@@ -845,10 +883,13 @@ extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, cons
   const int32_t n = g->n, D = d->D;
   if (!makespan || K < 1 || (n > 0 && (!order || !node_dev)))
     return set_error(CEL_E_ARG, "%s: NULL argument or K < 1", fn);
-  if (model & ~(CEL_MODEL_INSERT | CEL_MODEL_COMM_TASKS))
+  if (model & ~(CEL_MODEL_INSERT | CEL_MODEL_COMM_TASKS | CEL_MODEL_COMM_BLOCK))
     return set_error(CEL_E_ARG, "%s: unknown model bits 0x%x", fn, model);
+  if ((model & CEL_MODEL_COMM_BLOCK) && (model & (CEL_MODEL_INSERT | CEL_MODEL_COMM_TASKS)))
+    return set_error(CEL_E_ARG, "%s: CEL_MODEL_COMM_BLOCK combines with no other bit", fn);
   if (D > 64) return set_error(CEL_E_ARG, "%s: D = %d above 64", fn, D);
   const bool ins = model & CEL_MODEL_INSERT, tasks = model & CEL_MODEL_COMM_TASKS;
+  const bool block = model & CEL_MODEL_COMM_BLOCK;
   const bool het = h && (h->tmul || h->bw || h->lat);
   int64_t bwmin = d->bw, latmax = d->lat, tmax = 1024;
   if (het) {
@@ -945,7 +986,7 @@ extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, cons
     a.ga = ga;
     a.gb = gb;
   }
-  if (tasks) {
+  if (tasks || block) {
     uint64_t *dmask;
     int64_t *pc, *aoff, *pool;
     CEL_TRY(sc.get(&dmask, Kn));
@@ -969,7 +1010,10 @@ extern "C" int cel_makespan_model(const cel_graph *g, const cel_devices *d, cons
   {
     KTimer kt(s, "k_makespan_model");
     const unsigned gk = (unsigned)K;
-    if (het) {
+    if (block) {
+      if (het) k_makespan_model<false, false, true, true><<<gk, 64, 0, s>>>(a, st);
+      else k_makespan_model<false, false, false, true><<<gk, 64, 0, s>>>(a, st);
+    } else if (het) {
       if (!ins && !tasks) k_makespan_model<false, false, true><<<gk, 64, 0, s>>>(a, st);
       else if (ins && !tasks) k_makespan_model<true, false, true><<<gk, 64, 0, s>>>(a, st);
       else if (!ins) k_makespan_model<false, true, true><<<gk, 64, 0, s>>>(a, st);

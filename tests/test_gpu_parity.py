@@ -911,7 +911,8 @@ def test_order_place_and_ccr_transformer96():
 
 # ------------------------------------ makespan under device models (insertion, transfers)
 
-MODELS = (0, cel.MODEL_INSERT, cel.MODEL_COMM_TASKS, cel.MODEL_INSERT | cel.MODEL_COMM_TASKS)
+MODELS = (0, cel.MODEL_INSERT, cel.MODEL_COMM_TASKS, cel.MODEL_INSERT | cel.MODEL_COMM_TASKS,
+          cel.MODEL_COMM_BLOCK)
 
 
 def check_model(wl, order, P, models=MODELS, **het):
@@ -1028,9 +1029,10 @@ def test_model_edge_cases_and_errors():
     wl = from_edges(3, [(0, 1), (1, 2)], [1, 2, 3], [4, 5, 6], 2, [10, 10], 2, 1)
     g, d = up(wl)
     o = tt([0, 1, 2], np.int32)
-    with pytest.raises(cel.CelError) as ei:  # unknown model bit
-        cel.makespan_model(g, d, o, tt([0, 1, 0], np.uint8), 4)
-    assert ei.value.code == -1
+    for bad in (8, 5, 6, 7):  # an unknown bit; the blocking model combined with another
+        with pytest.raises(cel.CelError) as ei:
+            cel.makespan_model(g, d, o, tt([0, 1, 0], np.uint8), bad)
+        assert ei.value.code == -1
     with pytest.raises(cel.CelError) as ei:  # device out of range
         cel.makespan_model(g, d, o, tt([0, 2, 0], np.uint8), 2)
     assert ei.value.code == -1
@@ -1166,7 +1168,8 @@ def test_model_many_placements():
     check_model(wl, order, P)
     wl, rt, rb = config(1, 0)
     check_model(wl, rb[2], random_placements(wl, 257, 8), models=(cel.MODEL_INSERT,
-                                                                  cel.MODEL_COMM_TASKS))
+                                                                  cel.MODEL_COMM_TASKS,
+                                                                  cel.MODEL_COMM_BLOCK))
 
 
 # ------------------------------------------------------------ diagnostics
