@@ -940,6 +940,236 @@ int orc_makespan_model(const orc_graph *g, const orc_devices *d, const orc_heter
   return ORC_OK;
 }
 
+typedef struct {
+  int64_t key; /* (a << 32) | b */
+  int64_t c, ob, cnt;
+} xedge;
+
+static int cmp_xedge(const void *x, const void *y) {
+  int64_t a = ((const xedge *)x)->key, b = ((const xedge *)y)->key;
+  return (a > b) - (a < b);
+}
+
+/* Adjusting Placement with heterogeneous devices and links and with
+ * co-location groups inside the algorithm (Section 5.2's Algorithm 2 with the
+ * generality of Sections 4.1 and 6.1).  The steps are orc_place's, with:
+ *  - Device speeds: cluster t takes W_x[t] = sum over its members v of
+ *    ceil(w[v] * tmul[x] / 1024) on device x (each member at device x's
+ *    speed, as in orc_makespan_model), both for its first-fit slot and for
+ *    its finish time.  Devices are compared, and the move test of eq. 9 is
+ *    made, on the earliest finish time, slot + W_x[t]: with identical
+ *    devices W_x[t] is the same on every device, so the ordering and the
+ *    differences are those of eq. 7's start times.
+ *  - Links: with per-link tables, the coarse edge a -> b is charged, on the
+ *    link from device y to device x, ceil(OB / bw[y][x]) + N * lat[y][x],
+ *    where OB is the sum of ob[u] over its N member edges u -> v: the
+ *    members' tensors cross the link together, each edge paying the link's
+ *    latency.  pre_t on device x (eq. 7) uses the link from each
+ *    predecessor's device to x.  back_cost (eq. 8) is the largest charge of
+ *    t's outgoing coarse edges on the link from the best device d_1 back to
+ *    the previous cluster's device d_k, the link t's outputs would take if t
+ *    moved away from d_k.  Without link tables every coarse edge costs the sum
+ *    of c[u] exactly as in orc_place.
+ *  - Co-location: a group's leading cluster is the smallest cluster id among
+ *    its members (the first of them Algorithm 2 places); every member runs on
+ *    that cluster's device.  A member outside the leading cluster (a
+ *    follower) is charged to that device's memory when its own cluster is
+ *    placed, before the devices are compared; the cluster's memory test and
+ *    its own device's charge count only its other members (MEM_own).  The
+ *    coarse schedule keeps every member's compute in its cluster.
+ * h == NULL and group == NULL give orc_place's result. */
+int orc_place_ext(const orc_graph *g, const orc_devices *d, const orc_hetero *h,
+                  const int32_t *group, int32_t n_groups, const int32_t *cluster_id,
+                  int32_t n_clusters, uint8_t *cluster_dev, uint8_t *node_dev,
+                  int64_t *cluster_fin, int64_t *coarse_makespan, int32_t *best_effort_count) {
+  int rc = check_graph(g);
+  if (rc) return rc;
+  if ((rc = check_devices(d))) return rc;
+  if ((rc = check_hetero(g, d, h))) return rc;
+  int32_t n = g->n, C = n_clusters, D = d->D;
+  if (C < 0 || !coarse_makespan || !best_effort_count || n_groups < 0) return ORC_E_ARG;
+  if ((n > 0 && (!cluster_id || !node_dev || C < 1)) || (C > 0 && !cluster_dev)) return ORC_E_ARG;
+  if (n_groups > 0 && !group) return ORC_E_ARG;
+  for (int32_t v = 0; v < n; v++) {
+    if (cluster_id[v] < 0 || cluster_id[v] >= C) return ORC_E_ARG;
+    if (group && (group[v] < -1 || group[v] >= n_groups)) return ORC_E_ARG;
+  }
+  const int links = h && (h->bw || h->lat);
+  /* leading cluster of each group */
+  int32_t *lead = malloc(sizeof(int32_t) * ((size_t)n_groups + 1));
+  for (int32_t x = 0; x < n_groups; x++) lead[x] = INT32_MAX;
+  for (int32_t v = 0; v < n; v++)
+    if (group && group[v] >= 0 && cluster_id[v] < lead[group[v]]) lead[group[v]] = cluster_id[v];
+  /* coarse nodes: duration per device, own memory; followers by cluster */
+  int64_t *Wx = calloc((size_t)C * D + 1, sizeof(int64_t));
+  int64_t *MEM = calloc((size_t)C + 1, sizeof(int64_t));
+  int32_t *fp = calloc((size_t)C + 2, sizeof(int32_t)), *fv = malloc(sizeof(int32_t) * ((size_t)n + 1));
+  for (int32_t v = 0; v < n; v++) {
+    int32_t t = cluster_id[v];
+    for (int32_t x = 0; x < D; x++) Wx[(int64_t)t * D + x] += dur_on(h, g->w[v], x);
+    int follower = group && group[v] >= 0 && lead[group[v]] < t;
+    if (follower) fp[t + 1]++;
+    else MEM[t] += g->mem[v];
+  }
+  for (int32_t t = 0; t < C; t++) fp[t + 1] += fp[t];
+  {
+    int32_t *fill = malloc(sizeof(int32_t) * ((size_t)C + 1));
+    memcpy(fill, fp, sizeof(int32_t) * (size_t)(C + 1));
+    for (int32_t v = 0; v < n; v++)
+      if (group && group[v] >= 0 && lead[group[v]] < cluster_id[v]) fv[fill[cluster_id[v]]++] = v;
+    free(fill);
+  }
+  /* coarse edges, one per distinct (a, b): sum of c[u], sum of ob[u], count */
+  xedge *xe = malloc(sizeof(xedge) * ((size_t)g->m + 1));
+  int32_t ne = 0;
+  for (int32_t u = 0; u < n; u++) {
+    int64_t cu = comm_of(g->ob[u], d->bw, d->lat);
+    for (int32_t e = g->out_ptr[u]; e < g->out_ptr[u + 1]; e++) {
+      int32_t a = cluster_id[u], b = cluster_id[g->out_idx[e]];
+      if (a == b) continue;
+      if (a > b) {
+        free(lead); free(Wx); free(MEM); free(fp); free(fv); free(xe);
+        return ORC_E_ORDER;
+      }
+      xe[ne].key = ((int64_t)a << 32) | b;
+      xe[ne].c = cu;
+      xe[ne].ob = g->ob[u];
+      xe[ne].cnt = 1;
+      ne++;
+    }
+  }
+  qsort(xe, (size_t)ne, sizeof(xedge), cmp_xedge);
+  int32_t k = 0;
+  for (int32_t i = 0; i < ne; i++) {
+    if (k > 0 && xe[k - 1].key == xe[i].key) {
+      xe[k - 1].c += xe[i].c;
+      xe[k - 1].ob += xe[i].ob;
+      xe[k - 1].cnt += xe[i].cnt;
+    } else {
+      xe[k++] = xe[i];
+    }
+  }
+  ne = k;
+  /* predecessor lists (by target) and successor lists (by source) */
+  int32_t *pp = calloc((size_t)C + 2, sizeof(int32_t)), *sp = calloc((size_t)C + 2, sizeof(int32_t));
+  int32_t *pe = malloc(sizeof(int32_t) * ((size_t)ne + 1)), *se = malloc(sizeof(int32_t) * ((size_t)ne + 1));
+  for (int32_t i = 0; i < ne; i++) {
+    pp[(xe[i].key & 0xffffffff) + 1]++;
+    sp[(xe[i].key >> 32) + 1]++;
+  }
+  for (int32_t t = 0; t < C; t++) pp[t + 1] += pp[t], sp[t + 1] += sp[t];
+  {
+    int32_t *fa = malloc(sizeof(int32_t) * ((size_t)C + 1)), *fb = malloc(sizeof(int32_t) * ((size_t)C + 1));
+    memcpy(fa, pp, sizeof(int32_t) * (size_t)(C + 1));
+    memcpy(fb, sp, sizeof(int32_t) * (size_t)(C + 1));
+    for (int32_t i = 0; i < ne; i++) {
+      pe[fa[xe[i].key & 0xffffffff]++] = i;
+      se[fb[xe[i].key >> 32]++] = i;
+    }
+    free(fa); free(fb);
+  }
+  /* device state */
+  int64_t *Ava = malloc(sizeof(int64_t) * (size_t)D);
+  int32_t *nbusy = calloc((size_t)D, sizeof(int32_t));
+  int64_t **bs = malloc(sizeof(int64_t *) * (size_t)D), **bf = malloc(sizeof(int64_t *) * (size_t)D);
+  for (int32_t i = 0; i < D; i++) {
+    Ava[i] = d->cap[i];
+    bs[i] = malloc(sizeof(int64_t) * (size_t)(C + 1));
+    bf[i] = malloc(sizeof(int64_t) * (size_t)(C + 1));
+  }
+  int64_t *Fin = malloc(sizeof(int64_t) * (size_t)(C + 1));
+  int64_t *EST = malloc(sizeof(int64_t) * (size_t)D), *slot = malloc(sizeof(int64_t) * (size_t)D);
+  int32_t be = 0;
+  int64_t span = 0;
+  for (int32_t t = 0; t < C; t++) {
+    /* followers take memory on their leading cluster's device */
+    for (int32_t i = fp[t]; i < fp[t + 1]; i++) {
+      int32_t v = fv[i];
+      Ava[cluster_dev[lead[group[v]]]] -= g->mem[v];
+    }
+    for (int32_t x = 0; x < D; x++) {
+      int64_t pre = 0;
+      for (int32_t q = pp[t]; q < pp[t + 1]; q++) {
+        const xedge *ed = &xe[pe[q]];
+        int32_t a = (int32_t)(ed->key >> 32), y = cluster_dev[a];
+        int64_t cost = 0;
+        if (y != x) {
+          if (links) {
+            int64_t bw = h->bw ? h->bw[y * D + x] : d->bw, lat = h->lat ? h->lat[y * D + x] : d->lat;
+            cost = (ed->ob + bw - 1) / bw + ed->cnt * lat;
+          } else {
+            cost = ed->c;
+          }
+        }
+        if (Fin[a] + cost > pre) pre = Fin[a] + cost;
+      }
+      int64_t s = pre, wx = Wx[(int64_t)t * D + x];
+      if (wx > 0) {
+        for (int32_t q = 0; q < nbusy[x]; q++) {
+          if (bf[x][q] <= s) continue;
+          if (bs[x][q] < s + wx) s = bf[x][q];
+          else break;
+        }
+      }
+      slot[x] = s;
+      EST[x] = Ava[x] < MEM[t] ? INF : s + wx; /* the earliest finish time */
+    }
+    int32_t dk = t == 0 ? 0 : cluster_dev[t - 1];
+    int32_t d1 = 0;
+    for (int32_t x = 1; x < D; x++)
+      if (EST[x] < EST[d1]) d1 = x;
+    int32_t pick;
+    if (EST[d1] == INF) {
+      pick = 0;
+      for (int32_t x = 1; x < D; x++)
+        if (Ava[x] > Ava[pick]) pick = x;
+      be++;
+    } else if (EST[dk] == INF) {
+      pick = d1;
+    } else {
+      /* back_cost (eq. 8): largest charge of t's outgoing coarse edges, on the
+       * link d_1 -> d_k under link tables */
+      int64_t back = 0;
+      for (int32_t q = sp[t]; q < sp[t + 1]; q++) {
+        const xedge *ed = &xe[se[q]];
+        int64_t cost = ed->c;
+        if (links && d1 != dk) {
+          int64_t bw = h->bw ? h->bw[d1 * D + dk] : d->bw, lat = h->lat ? h->lat[d1 * D + dk] : d->lat;
+          cost = (ed->ob + bw - 1) / bw + ed->cnt * lat;
+        }
+        if (cost > back) back = cost;
+      }
+      pick = EST[dk] - EST[d1] > back ? d1 : dk;
+    }
+    cluster_dev[t] = (uint8_t)pick;
+    int64_t wp = Wx[(int64_t)t * D + pick];
+    Fin[t] = slot[pick] + wp;
+    if (Fin[t] > span) span = Fin[t];
+    Ava[pick] -= MEM[t];
+    if (wp > 0) {
+      int32_t q = nbusy[pick];
+      while (q > 0 && bs[pick][q - 1] > slot[pick]) {
+        bs[pick][q] = bs[pick][q - 1];
+        bf[pick][q] = bf[pick][q - 1];
+        q--;
+      }
+      bs[pick][q] = slot[pick];
+      bf[pick][q] = Fin[t];
+      nbusy[pick]++;
+    }
+  }
+  for (int32_t v = 0; v < n; v++)
+    node_dev[v] = group && group[v] >= 0 ? cluster_dev[lead[group[v]]] : cluster_dev[cluster_id[v]];
+  if (cluster_fin)
+    for (int32_t t = 0; t < C; t++) cluster_fin[t] = Fin[t];
+  *coarse_makespan = span;
+  *best_effort_count = be;
+  for (int32_t i = 0; i < D; i++) { free(bs[i]); free(bf[i]); }
+  free(bs); free(bf); free(nbusy); free(Ava); free(Fin); free(EST); free(slot);
+  free(lead); free(Wx); free(MEM); free(fp); free(fv); free(xe); free(pp); free(sp); free(pe); free(se);
+  return ORC_OK;
+}
+
 /* Co-location groups (Section 6.1, as in Baechi): every node of a group runs
  * on the device of the group's first node in `order`; nodes with group -1
  * keep theirs.  node_dev is [K][n], rewritten in place. */

@@ -135,6 +135,21 @@ int orc_makespan_model(const orc_graph *g, const orc_devices *d, const orc_heter
                        const int32_t *order, int32_t K, const uint8_t *node_dev, int32_t model,
                        int64_t *start, int64_t *finish, int64_t *makespan);
 
+/* Adjusting Placement with heterogeneous devices and links (h, or NULL) and
+ * co-location groups decided inside the algorithm (group [n] in [-1,
+ * n_groups), or NULL): clusters take W_x = sum of their members' durations on
+ * device x, and devices are compared on the earliest finish time (the start
+ * of eq. 7 plus W_x, the same ordering with identical devices); under link tables a coarse edge costs ceil(OB / bw) + N lat on
+ * the link used (OB = its members' summed ob, N = their count), in eq. 7 from
+ * each predecessor's device and in eq. 8 from the best device back to the
+ * previous one; a group follows its smallest cluster, whose device is charged
+ * with the followers' memory when their clusters are placed.  h == NULL and
+ * group == NULL give orc_place's result. */
+int orc_place_ext(const orc_graph *g, const orc_devices *d, const orc_hetero *h,
+                  const int32_t *group, int32_t n_groups, const int32_t *cluster_id,
+                  int32_t n_clusters, uint8_t *cluster_dev, uint8_t *node_dev,
+                  int64_t *cluster_fin, int64_t *coarse_makespan, int32_t *best_effort_count);
+
 /* Co-location groups: nodes with group[v] >= 0 take the device of their
  * group's first node in `order` (a topological order); node_dev [K][n] in
  * place. */

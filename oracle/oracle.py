@@ -67,9 +67,12 @@ def lib():
                                          C.POINTER(_Hetero), _P32, C.c_int32, _PU8, C.c_int32,
                                          _P64, _P64, _P64]
         L.orc_colocate.argtypes = [C.POINTER(_Graph), _P32, _P32, C.c_int32, C.c_int32, _PU8]
+        L.orc_place_ext.argtypes = [C.POINTER(_Graph), C.POINTER(_Devices), C.POINTER(_Hetero),
+                                    _P32, C.c_int32, _P32, C.c_int32, _PU8, _PU8, _P64,
+                                    C.POINTER(C.c_int64), C.POINTER(C.c_int32)]
         for f in (L.orc_topo_levels, L.orc_blevel, L.orc_cluster, L.orc_place, L.orc_makespan,
                   L.orc_cpd_topo, L.orc_dfs_topo, L.orc_comm_sums, L.orc_order_place, L.orc_makespan_model,
-                  L.orc_colocate):
+                  L.orc_colocate, L.orc_place_ext):
             f.restype = C.c_int
         _lib = L
     return _lib
@@ -209,6 +212,34 @@ def place(wl, cluster_id, n_clusters, want_fin=False):
                            C.byref(span), C.byref(be)), "orc_place")
     out = (cdev[:n_clusters], ndev[:n], span.value, be.value)
     return out + (fin[:n_clusters],) if want_fin else out
+
+
+def place_ext(wl, cluster_id, n_clusters, tmul=None, bw=None, lat=None, group=None,
+              n_groups=0):
+    """Adjusting Placement with heterogeneous devices/links (tmul [D], bw / lat
+    [D, D]) and co-location groups (group [n] in [-1, n_groups)) inside the
+    algorithm -> (cluster_dev, node_dev, coarse_makespan, best_effort_count,
+    cluster_fin)."""
+    k = _Keep(wl)
+    het = None
+    if tmul is not None or bw is not None or lat is not None:
+        arrs = [None if a is None else np.ascontiguousarray(a, np.int64).reshape(-1)
+                for a in (tmul, bw, lat)]
+        k.het_arrays = arrs
+        het = _Hetero(*[_ptr(a, _P64) for a in arrs])
+    n = int(wl.n)
+    cid = np.ascontiguousarray(cluster_id, np.int32)
+    grp = None if group is None else np.ascontiguousarray(group, np.int32)
+    cdev = np.zeros(max(n_clusters, 1), np.uint8)
+    ndev = np.zeros(max(n, 1), np.uint8)
+    fin = np.zeros(max(n_clusters, 1), np.int64)
+    span = C.c_int64(0)
+    be = C.c_int32(0)
+    _check(lib().orc_place_ext(C.byref(k.g), C.byref(k.d), None if het is None else C.byref(het),
+                               _ptr(grp, _P32), int(n_groups), _ptr(cid, _P32), int(n_clusters),
+                               _ptr(cdev, _PU8), _ptr(ndev, _PU8), _ptr(fin, _P64),
+                               C.byref(span), C.byref(be)), "orc_place_ext")
+    return cdev[:n_clusters], ndev[:n], span.value, be.value, fin[:n_clusters]
 
 
 def makespan(wl, order, node_dev, want_times=True):

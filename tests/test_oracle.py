@@ -1022,3 +1022,129 @@ def test_colocate_hand_and_properties():
         O.colocate(wl, [0, 1], [0, 2], 2, np.zeros(2, np.uint8))
     with pytest.raises(RuntimeError):
         O.colocate(wl, [1, 0], [0, 0], 1, np.zeros(2, np.uint8))
+
+
+# ------------- Adjusting Placement with heterogeneous devices/links and co-location
+
+
+@pytest.mark.parametrize("case", load("place_ext_hand.json")["cases"], ids=lambda c: c["name"])
+def test_place_ext_hand_cases(case):
+    wl = from_edges(case["n"], case["edges"], case["w"], case["ob"], case["D"], case["cap"],
+                    case["bw"], case["lat"])
+    for v in case["variants"]:
+        cdev, ndev, span, be, fin = O.place_ext(
+            wl, case["cluster_id"], case["C"], tmul=v.get("tmul"), bw=v.get("bw_matrix"),
+            lat=v.get("lat_matrix"), group=v.get("group"), n_groups=v.get("n_groups", 0))
+        assert cdev.tolist() == v["cluster_dev"] and ndev.tolist() == v["node_dev"], case["name"]
+        assert fin.tolist() == v["fin"] and span == v["span"] and be == v["be"], case["name"]
+
+
+def _clustered(wl, seed, R=None):
+    lev, oid, _, _ = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    R = R if R is not None else 1 + seed % 9
+    cid, C, _ = O.cluster(wl, pr, R, -1, seed % 2)
+    return pr, cid, C
+
+
+def test_place_ext_reduces_to_place():
+    """No descriptor and no groups: Algorithm 2 as orc_place computes it (a
+    separately pinned function); singleton groups change nothing either."""
+    for s in range(30):
+        n = 3 + (s * 37) % 300
+        wl = make_random_dag(8800 + s, n, p_edge=min(0.5, 4.0 / n), D=1 + s % 7,
+                             cap_frac=(1, 1 + s % 5), multi=(s % 3 == 0),
+                             zero_frac=0.2 if s % 4 == 0 else 0.0)
+        _, cid, C = _clustered(wl, s)
+        ref = O.place(wl, cid, C, want_fin=True)
+        got = O.place_ext(wl, cid, C)
+        single = O.place_ext(wl, cid, C, group=np.arange(n, dtype=np.int32), n_groups=n)
+        for r in (got, single):
+            assert np.array_equal(r[0], ref[0]) and np.array_equal(r[1], ref[1]), s
+            assert r[2] == ref[2] and r[3] == ref[3] and np.array_equal(r[4], ref[4]), s
+
+
+def test_place_ext_uniform_descriptors():
+    """Uniform descriptors reduce to the homogeneous placement: tmul = 2048 on
+    every device with no comm doubles every time (the same devices as orc_place
+    on the graph with w doubled, the same finish times); link tables repeating
+    (bw, lat) with every ob a multiple of bw give exactly the summed c[u] of the
+    coarse edges (ceil(OB / bw) + N lat = sum of ceil(ob / bw) + lat)."""
+    for s in range(20):
+        n = 5 + (s * 53) % 250
+        D = 2 + s % 5
+        wl = make_random_dag(8900 + s, n, p_edge=min(0.5, 4.0 / n), D=D, cap_frac=(1, 2 + s % 3),
+                             multi=(s % 2 == 0), bw=3, lat=0)
+        wl.ob = np.zeros(n, np.int64)  # no comm: c = 0 everywhere
+        _, cid, C = _clustered(wl, s)
+        got = O.place_ext(wl, cid, C, tmul=[2048] * D)
+        wl2 = make_random_dag(8900 + s, n, p_edge=min(0.5, 4.0 / n), D=D, cap_frac=(1, 2 + s % 3),
+                              multi=(s % 2 == 0), bw=3, lat=0)
+        wl2.ob = np.zeros(n, np.int64)
+        wl2.w = 2 * np.asarray(wl.w, np.int64)
+        ref = O.place(wl2, cid, C, want_fin=True)
+        assert np.array_equal(got[0], ref[0]) and np.array_equal(got[4], ref[4]), s
+        # link tables equal to the homogeneous link, ob multiples of bw
+        wl3 = make_random_dag(9000 + s, n, p_edge=min(0.5, 4.0 / n), D=D, cap_frac=(1, 3),
+                              multi=(s % 2 == 1), bw=4, lat=3)
+        wl3.ob = 4 * (np.asarray(wl3.ob, np.int64) // 4)
+        wl3.mem = 2 * wl3.ob
+        _, cid3, C3 = _clustered(wl3, s)
+        ref3 = O.place(wl3, cid3, C3, want_fin=True)
+        got3 = O.place_ext(wl3, cid3, C3, bw=np.full((D, D), 4), lat=np.full((D, D), 3))
+        for a, b in zip(got3, (ref3[0], ref3[1], ref3[2], ref3[3], ref3[4])):
+            assert np.array_equal(np.asarray(a), np.asarray(b)), s
+
+
+def test_place_ext_colocation_memory_and_devices():
+    """Co-location inside the algorithm, checked from the outputs alone: every
+    group member runs on its leading cluster's device (the smallest cluster
+    id among the members); replaying Algorithm 2's memory bookkeeping (the
+    followers charged to that device when their own cluster is placed, then
+    the cluster's other members to its device), a cluster not placed by best
+    effort always fitted its device's remaining memory; with best effort 0,
+    every device ends within its cap unless followers overfilled it."""
+    rng = np.random.default_rng(8)
+    for s in range(25):
+        n = 10 + (s * 61) % 400
+        D = 2 + s % 6
+        wl = make_random_dag(9100 + s, n, p_edge=min(0.5, 4.0 / n), D=D, cap_frac=(1, 1 + s % 4),
+                             multi=(s % 3 == 0))
+        _, cid, C = _clustered(wl, s)
+        G = max(1, n // (3 + s % 5))
+        grp = rng.integers(-1, G, n).astype(np.int32)
+        het = dict(tmul=rng.integers(512, 3000, D)) if s % 2 else {}
+        cdev, ndev, span, be, fin = O.place_ext(wl, cid, C, group=grp, n_groups=G, **het)
+        lead = np.full(G, C, np.int64)
+        np.minimum.at(lead, grp[grp >= 0], cid[grp >= 0])
+        member = grp >= 0
+        assert np.array_equal(ndev[member], cdev[lead[grp[member]]])
+        assert np.array_equal(ndev[~member], cdev[cid[~member]])
+        follower = member & (lead[np.where(member, grp, 0)] < cid)
+        mem = np.asarray(wl.mem, np.int64)
+        ava = np.asarray(wl.cap, np.int64).copy()
+        over = False
+        n_be = 0
+        for t in range(C):
+            for v in np.nonzero(follower & (cid == t))[0]:
+                ava[cdev[lead[grp[v]]]] -= mem[v]
+            over |= bool((ava < 0).any())
+            own = mem[(cid == t) & ~follower].sum()
+            if (ava >= own).any():        # some device fits: the pick must fit
+                assert ava[cdev[t]] >= own, (s, t)
+            else:
+                n_be += 1
+            ava[cdev[t]] -= own
+        assert n_be == be
+        if be == 0 and not over:
+            assert (ava >= 0).all()
+
+
+def test_place_ext_rejects_bad_inputs():
+    wl = from_edges(3, [(0, 1), (1, 2)], [1, 1, 1], [0, 0, 0], 2, [5, 5], 1, 0)
+    with pytest.raises(RuntimeError):  # group id out of range
+        O.place_ext(wl, [0, 1, 2], 3, group=[0, 1, 2], n_groups=2)
+    with pytest.raises(RuntimeError):  # bad time multiplier
+        O.place_ext(wl, [0, 1, 2], 3, tmul=[0, 1024])
+    with pytest.raises(RuntimeError):  # clusters against the edges
+        O.place_ext(wl, [2, 1, 0], 3)
