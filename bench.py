@@ -247,7 +247,7 @@ def cpd_compare(cel, torch, g, d, bl, tl, prio, lev, lp, L):
                      "coarse_makespan_ns": cms, "best_effort": be, "makespan_ns": int(ms[0].item()),
                      "order_place": {"makespan_ns": int(ms_o[0].item()), "best_effort": be_o,
                                      "ms": op_ms}}
-    return row, ndev
+    return row, ndev, cid, C
 
 
 def check_parity(pairs: dict) -> dict:
@@ -338,7 +338,7 @@ def config_rows(cel, torch, dev, args):
 MODEL_NAMES = {0: "fifo", 1: "insert", 2: "comm_tasks", 3: "insert+comm_tasks", 4: "comm_block"}
 
 
-def models_row(cel, torch, g, d, prio, ndev, seed, K=64):
+def models_row(cel, torch, g, d, prio, ndev, seed, K=64, cid=None, C=0):
     """The makespan under each device model (first-fit insertion, transfers as
     tasks) of Adjusting Placement's placement (K = 1) and of K placements in one
     call (that one first, the rest random), on the priority order."""
@@ -389,6 +389,29 @@ def models_row(cel, torch, g, d, prio, ndev, seed, K=64):
     row["colocate"] = {"groups": G, "group_size": 4, "K": K, "call_ms": round(colo_ms, 2),
                        "makespan_ns_after": int(ms_c[0].item()),
                        "makespan_ns_before": row["fifo"]["K1"]["makespan_ns"]}
+    # the optimiser itself under the same devices and groups: Adjusting
+    # Placement with per-device durations, per-link costs and co-location
+    # inside the algorithm, against the homogeneous placement made
+    # co-located afterwards, both scored under the heterogeneous model
+    if cid is not None:
+        (cd_x, nd_x, cms_x, be_x, _), px_ms = _timed(
+            torch, lambda: cel.place_ext(g, d, cid, C, group=grp_t, n_groups=G, **het), reps=3)
+        cel.kernel_stats(reset=True)
+        cel.timing(True)
+        cel.place_ext(g, d, cid, C, group=grp_t, n_groups=G, **het)
+        cel.timing(False)
+        kx = cel.kernel_stats(reset=True).get("k_place_ext", (1, float("nan")))
+        (ms_x, _, _), _ = _timed(torch, lambda: cel.makespan_model(g, d, prio, nd_x, 0, **het),
+                                 reps=1)
+        nd_h = ndev.clone()
+        cel.colocate(g, prio, grp_t, G, nd_h)
+        (ms_h, _, _), _ = _timed(torch, lambda: cel.makespan_model(g, d, prio, nd_h, 0, **het),
+                                 reps=1)
+        row["place_ext"] = {"clusters": C, "groups": G, "call_ms": round(px_ms, 2),
+                            "k_place_ext_ms": round(kx[1] / kx[0], 2),
+                            "coarse_makespan_ns": cms_x, "best_effort": be_x,
+                            "makespan_ns_hetero_model": int(ms_x[0].item()),
+                            "homogeneous_place_then_colocate_ns": int(ms_h[0].item())}
     return row
 
 
@@ -528,11 +551,11 @@ def main() -> int:
     launches, tot = ks_t.get("k_tlevel_sweep", (1, float("nan")))
     tlevel_row = {"blevel_with_tlevel_ms": sorted(t_ms)[1], "k_tlevel_sweep_ms": tot / max(launches, 1)}
 
-    cpd_row, ndev_cpd = cpd_compare(cel, torch, g, d, bl_t, tl_t, pr_t, lev, lp, L)
+    cpd_row, ndev_cpd, cid_cpd, C_cpd = cpd_compare(cel, torch, g, d, bl_t, tl_t, pr_t, lev, lp, L)
     model_row = None
     if not args.no_models:
         print("[bench] device models", file=sys.stderr, flush=True)
-        model_row = models_row(cel, torch, g, d, pr_t, ndev_cpd, args.seed)
+        model_row = models_row(cel, torch, g, d, pr_t, ndev_cpd, args.seed, cid=cid_cpd, C=C_cpd)
 
     batch5 = None if args.no_batch else batched_row(cel, torch, dev, args)
 

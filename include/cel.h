@@ -175,6 +175,40 @@ int cel_place(const cel_graph *g, const cel_devices *d, const int32_t *cluster_i
               int64_t *cluster_fin, int64_t *coarse_makespan, int32_t *best_effort_count,
               hipStream_t stream);
 
+/* Adjusting Placement (Section 5.2, eq. 7-9, Algorithm 2) with the device
+ * generality of Section 4.1 and the co-location groups of Section 6.1 decided
+ * inside the algorithm.  As cel_place, except:
+ *  - h (heterogeneous devices and links, or NULL): cluster t takes W_x = the
+ *    sum of its members' durations ceil(w * tmul[x] / 1024) on device x, and
+ *    devices are compared, and the move test of eq. 9 made, on the earliest
+ *    finish time (first-fit start + W_x), which orders identical devices as
+ *    eq. 7's start times do.  With link tables (h->bw or h->lat) a coarse edge
+ *    whose N member edges carry OB output bytes in total costs
+ *    ceil(OB / bw[y][x]) + N * lat[y][x] on the link y -> x: in pre_t from each
+ *    predecessor's device y (eq. 7), and in back_cost on the link from the best
+ *    device back to the previous cluster's (eq. 8); without them a coarse edge
+ *    costs the sum of its members' c[u] as in cel_place.
+ *  - group [n] (device, in [-1, n_groups), or NULL): a group's leading
+ *    cluster is the smallest cluster id among its members and every member
+ *    runs on that cluster's device; a member in a later cluster (a follower)
+ *    is charged to that device's memory when its own cluster is placed, before
+ *    the devices are compared, and its cluster's memory test and charge count
+ *    only the other members.  The coarse schedule keeps every member's
+ *    compute in its own cluster.
+ * h == NULL and group == NULL give cel_place's results.
+ * Inputs: as cel_place; D <= 64; tmul in [1, 65536], link bw in [1, 2^31) and
+ * lat in [0, 2^31).  Outputs: cluster_dev [C]; node_dev [n] (group members on
+ * their leading cluster's device); cluster_fin [C] or NULL; coarse_makespan
+ * and best_effort_count (host).
+ * Errors: CEL_E_ARG (also D > 64 or a bad group id), CEL_E_ORDER,
+ * CEL_E_OVERFLOW, CEL_E_HIP, CEL_E_NOMEM. */
+typedef struct cel_hetero cel_hetero;
+int cel_place_ext(const cel_graph *g, const cel_devices *d, const cel_hetero *h,
+                  const int32_t *group, int32_t n_groups, const int32_t *cluster_id,
+                  int32_t n_clusters, uint8_t *cluster_dev, uint8_t *node_dev,
+                  int64_t *cluster_fin, int64_t *coarse_makespan, int32_t *best_effort_count,
+                  hipStream_t stream);
+
 /* Order-Place, the baseline placement of Sections 5.2 and 6.2.2: clusters are taken in
  * index order and filled onto device 0 until the next cluster's MEM (sum of
  * its members' mem) no longer fits that device's remaining cap, then onto
@@ -240,11 +274,11 @@ int cel_makespan_noalloc(const cel_graph *g, const cel_devices *d, const int32_t
  * ceil(w * tmul[x] / 1024) (1024 = the reference speed, 1 <= tmul <= 65536);
  * node u's output takes ceil(ob[u] / bw[a*D + b]) + lat[a*D + b] from device
  * a to device b (1 <= bw < 2^31, 0 <= lat < 2^31; the diagonal is unused). */
-typedef struct {
+struct cel_hetero {
   const int64_t *tmul; /* (host) [D] */
   const int64_t *bw;   /* (host) [D*D] bytes per ns */
   const int64_t *lat;  /* (host) [D*D] ns */
-} cel_hetero;
+};
 
 /* Makespan of K placements under richer device models (Section 5.2's slot
  * rule, eq. 7, at node level; Section 6.1's transfers as tasks).  Nodes are

@@ -20,7 +20,7 @@ OK, E_ARG, E_CYCLE, E_OVERFLOW, E_HIP, E_NOMEM, E_ORDER = 0, -1, -2, -3, -4, -5,
 COMM_OFF = 1
 CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
-EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_dfs_order", "cel_cluster", "cel_place", "cel_makespan", "cel_makespan_noalloc",
+EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_dfs_order", "cel_cluster", "cel_place", "cel_place_ext", "cel_makespan", "cel_makespan_noalloc",
            "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_colocate", "cel_step_latency", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
@@ -64,6 +64,8 @@ def lib() -> C.CDLL:
         L.cel_blevel.argtypes = [G, Dv, vp, vp, vp, i32, i32, vp, vp, vp, C.POINTER(i64), vp]
         L.cel_cluster.argtypes = [G, Dv, vp, i32, i64, i32, vp, C.POINTER(i32), C.POINTER(i64), vp]
         L.cel_place.argtypes = [G, Dv, vp, i32, vp, vp, vp, C.POINTER(i64), C.POINTER(i32), vp]
+        L.cel_place_ext.argtypes = [G, Dv, C.POINTER(_Hetero), vp, i32, vp, i32, vp, vp, vp,
+                                    C.POINTER(i64), C.POINTER(i32), vp]
         L.cel_makespan.argtypes = [G, Dv, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]
         L.cel_makespan_noalloc.argtypes = [G, Dv, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]
         L.cel_cpd_order.argtypes = [G, vp, vp, vp, vp]
@@ -72,7 +74,8 @@ def lib() -> C.CDLL:
         L.cel_comm_sums.argtypes = [G, Dv, vp, C.POINTER(i64), C.POINTER(i64), vp]
         L.cel_makespan_model.argtypes = [G, Dv, C.POINTER(_Hetero), vp, i32, vp, i32, vp, vp, vp, vp]
         L.cel_colocate.argtypes = [G, vp, vp, i32, i32, vp, vp]
-        for f in ("cel_topo_levels", "cel_blevel", "cel_cluster", "cel_place", "cel_makespan",
+        for f in ("cel_topo_levels", "cel_blevel", "cel_cluster", "cel_place", "cel_place_ext",
+                  "cel_makespan",
                   "cel_makespan_noalloc",
                   "cel_cpd_order", "cel_dfs_order", "cel_order_place", "cel_comm_sums", "cel_makespan_model",
                   "cel_colocate", "cel_version"):
@@ -274,22 +277,48 @@ def order_place(g: Graph, d: Devices, cluster_id, n_clusters):
 MODEL_INSERT, MODEL_COMM_TASKS, MODEL_COMM_BLOCK = 1, 2, 4
 
 
+def _hetero(tmul, bw, lat, keep):
+    """cel_hetero over host copies (kept alive in `keep`), or None."""
+    if tmul is None and bw is None and lat is None:
+        return None
+    ptrs = []
+    for a in (tmul, bw, lat):
+        if a is None:
+            ptrs.append(None)
+            continue
+        arr = (C.c_int64 * int(np.asarray(a).size))(*[int(x) for x in np.asarray(a).reshape(-1)])
+        keep.append(arr)
+        ptrs.append(C.cast(arr, C.POINTER(C.c_int64)))
+    return _Hetero(*ptrs)
+
+
+def place_ext(g: Graph, d: Devices, cluster_id, n_clusters, tmul=None, bw=None, lat=None,
+              group=None, n_groups=0):
+    """Adjusting Placement with heterogeneous devices/links (host tmul [D], bw / lat
+    [D, D]) and co-location groups (device int32 [n] in [-1, n_groups)) inside the
+    algorithm -> (cluster_dev, node_dev, coarse_makespan, best_effort_count, cluster_fin)."""
+    keep = []
+    het = _hetero(tmul, bw, lat, keep)
+    n = g.n
+    cdev = _empty(n_clusters, torch.uint8, g.device)
+    ndev = _empty(n, torch.uint8, g.device)
+    fin = _empty(n_clusters, torch.int64, g.device)
+    span = C.c_int64(0)
+    be = C.c_int32(0)
+    gc, dc = g._c(), d._c()
+    _check(lib().cel_place_ext(C.byref(gc), C.byref(dc), None if het is None else C.byref(het),
+                               _p(group), int(n_groups), _p(cluster_id), int(n_clusters), _p(cdev),
+                               _p(ndev), _p(fin), C.byref(span), C.byref(be), _stream()))
+    return cdev[:n_clusters], ndev[:n], span.value, be.value, fin[:n_clusters]
+
+
 def makespan_model(g: Graph, d: Devices, order, node_dev, model, want_times=False, tmul=None,
                    bw=None, lat=None):
     """Makespan under the device models (MODEL_* bits; 0 = FIFO devices, contention-free
     comm). node_dev uint8 [n] or [K, n] -> (makespan int64[K], start, finish) ([K, n] or None).
     tmul [D], bw / lat [D, D]: heterogeneous devices (host values, time x tmul / 1024)."""
-    het, keep = None, []
-    if tmul is not None or bw is not None or lat is not None:
-        ptrs = []
-        for a in (tmul, bw, lat):
-            if a is None:
-                ptrs.append(None)
-                continue
-            arr = (C.c_int64 * int(np.asarray(a).size))(*[int(x) for x in np.asarray(a).reshape(-1)])
-            keep.append(arr)
-            ptrs.append(C.cast(arr, C.POINTER(C.c_int64)))
-        het = _Hetero(*ptrs)
+    keep = []
+    het = _hetero(tmul, bw, lat, keep)
     n = g.n
     nd = node_dev.contiguous()
     K = 1 if nd.dim() == 1 else nd.shape[0]

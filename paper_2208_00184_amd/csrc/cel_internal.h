@@ -392,6 +392,13 @@ __global__ void k_makespan_out(int32_t K, int32_t n, const int32_t *order, const
                                const Status *st);
 __global__ void k_fill_i64(int64_t *p, int64_t n, int64_t v);
 __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v);  // common.hip
+// makespan_model.hip: a heterogeneous descriptor's ranges, its slowest
+// multiplier, smallest bandwidth and largest latency; lead[g] = smallest
+// pos[v] over the members v of group g (INT32_MAX before)
+int check_hetero(const cel_hetero *h, const cel_devices *d, const char *fn, int64_t *bwmin,
+                 int64_t *latmax, int64_t *tmax);
+__global__ void k_colo_lead(int32_t n, int32_t G, const int32_t *group, const int32_t *pos,
+                            int32_t *lead, Status *st);
 
 // Copies the status block to the host (synchronising the stream).
 int read_status(const Status *dst, Status *host, hipStream_t s);

@@ -840,8 +840,8 @@ using namespace cel;
 
 // Host checks of a heterogeneous descriptor; fills the worst link (smallest
 // bandwidth, largest latency) and the largest multiplier.
-static int check_hetero(const cel_hetero *h, const cel_devices *d, const char *fn, int64_t *bwmin,
-                        int64_t *latmax, int64_t *tmax) {
+int cel::check_hetero(const cel_hetero *h, const cel_devices *d, const char *fn, int64_t *bwmin,
+                      int64_t *latmax, int64_t *tmax) {
   const int32_t D = d->D;
   *bwmin = d->bw;
   *latmax = d->lat;

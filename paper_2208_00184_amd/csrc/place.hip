@@ -458,6 +458,284 @@ __global__ void __launch_bounds__(64)
   }
 }
 
+// ----------------------------------- extended placement: devices, links, groups
+//
+// Algorithm 2 with per-device cluster durations, per-link coarse-edge costs
+// and co-location groups (cel_place_ext).  Cluster t's duration on device x
+// is the sum of its members' durations there; devices are compared on the
+// earliest finish time (start + duration: the order of eq. 7's start times
+// when devices are identical).  Under link tables a coarse edge (OB = summed
+// ob of its N member edges) costs ceil(OB / bw[y][x]) + N lat[y][x] on the
+// link y -> x: in pre_t from each predecessor's device, in back_cost (eq. 8)
+// on the link from the best device back to the previous cluster's.  A group
+// follows its smallest cluster; its other members' memory is charged to that
+// cluster's device when their own cluster is placed.
+
+__device__ inline int64_t dur_tm(int64_t w, int64_t tm) {  // ceil(w * tm / 1024)
+  return (w >> 10) * tm + (((w & 1023) * tm + 1023) >> 10);
+}
+
+// Per node: the cluster's duration on every device (atomics into W2[t][x]),
+// its own memory (followers excluded) and follower counts per cluster.
+__global__ void k_pe_nodes(int32_t n, int32_t C, int32_t D, const int32_t *cid, const int64_t *w,
+                           const int64_t *mem, const int32_t *group, const int32_t *lead,
+                           const int64_t *tmul, uint64_t *W2, uint64_t *MEMo, int32_t *fcnt,
+                           Status *st) {
+  if (failed(st)) return;
+  uint32_t bad = 0;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t c = cid[v];
+    if (c < 0 || c >= C) {
+      bad |= EB_ARG;
+      continue;
+    }
+    const int64_t wv = w[v];
+    for (int32_t x = 0; x < D; x++)
+      atomicAdd((unsigned long long *)&W2[(int64_t)c * D + x],
+                (unsigned long long)(tmul ? dur_tm(wv, tmul[x]) : wv));
+    const int32_t gv = group ? group[v] : -1;
+    if (gv >= 0 && lead[gv] < c) atomicAdd(&fcnt[c], 1);
+    else atomicAdd((unsigned long long *)&MEMo[c], (unsigned long long)mem[v]);
+  }
+  if (bad) raise_err(st, bad);
+}
+
+// Follower entries (leading cluster, mem) in their own cluster's slice.
+__global__ void k_pe_followers(int32_t n, const int32_t *cid, const int64_t *mem,
+                               const int32_t *group, const int32_t *lead, const int32_t *foff,
+                               int32_t *fill, int32_t *fl, int64_t *fm, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t gv = group[v], c = cid[v];
+    if (gv < 0 || lead[gv] >= c) continue;
+    const int32_t k = foff[c] + atomicAdd(&fill[c], 1);
+    fl[k] = lead[gv];
+    fm[k] = mem[v];
+  }
+}
+
+// Per edge id: the source's output bytes and a count of one (summed per
+// coarse edge by k_place_combine into OB and N).
+__global__ void k_pe_edge_ob(cel_graph g, int64_t *eob, int64_t *eone, const Status *st) {
+  __shared__ int32_t ptr[kRowsPB + 1], su[2];
+  if (failed(st)) return;
+  for_edges_balanced(g.out_ptr, g.n, g.m, ptr, su, [&](int32_t u, int32_t e) {
+    eob[e] = g.ob[u];
+    eone[e] = 1;
+  });
+}
+
+// Successor lists of the coarse graph (by source cluster) from the
+// predecessor buckets: PASS 0 counts, PASS 1 writes (OB, N).
+template <int PASS>
+__global__ void k_pe_succ(int32_t C, const int32_t *boff, const int32_t *ncp, const int32_t *ca,
+                          const int64_t *cob, const int64_t *cnum, int32_t *scnt,
+                          const int32_t *soff, int64_t *sob, int64_t *snum, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t b = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; b < C;
+       b += (int64_t)gridDim.x * blockDim.x) {
+    for (int32_t k = boff[b]; k < boff[b] + ncp[b]; k++) {
+      const int32_t a = ca[k];
+      if (PASS == 0) {
+        atomicAdd(&scnt[a], 1);
+      } else {
+        const int32_t q = soff[a] + atomicAdd(&scnt[a], 1);
+        sob[q] = cob[k];
+        snum[q] = cnum[k];
+      }
+    }
+  }
+}
+
+struct PeArgs {
+  int32_t C, D;
+  bool links;                      // per-link tables given
+  const int64_t *cap;              // [D]
+  const uint64_t *W2, *MEMo;       // [C][D] durations, [C] own memory
+  const int32_t *boff, *ncp, *ca;  // coarse in-edges (bucket start, count, source)
+  const int64_t *cc, *cob, *cnum;  // their summed c, ob and member count
+  const uint64_t *back;            // max summed c over out-edges (no link tables)
+  const int32_t *soff;             // [C + 1] out-edges (link tables): OB, N
+  const int64_t *sob, *snum;
+  const int32_t *foff, *fl;        // [C + 1] followers: leading cluster, memory
+  const int64_t *fm;
+  const int64_t *lbw, *llat;       // [D][D] link tables
+  uint8_t *cdev;
+  int64_t *Fin, *bs, *bf;          // busy lists [D][bcap]
+  int32_t bcap;
+};
+
+constexpr int kPeLds = 8192;  // clusters whose Fin and device stay in LDS too
+
+__device__ inline int64_t link_cost(int64_t ob, int64_t cnt, int32_t bw, int32_t lat) {
+  return (int64_t)(((uint64_t)ob + (uint64_t)bw - 1) / (uint64_t)bw) + cnt * lat;
+}
+
+// One wave; device x's free memory, busy-list size and last end sit in lane
+// x (D <= 64), its busy blocks in its global list, which only lane x reads
+// and writes.
+template <bool LDSF>
+__global__ void __launch_bounds__(64) k_place_ext(PeArgs a, Status *st) {
+  __shared__ int32_t s_bw[64 * 64], s_lat[64 * 64];
+  __shared__ int64_t s_fin[LDSF ? kPeLds : 1];
+  __shared__ uint8_t s_cd[LDSF ? kPeLds : 1];
+  if (failed(st)) return;
+  const int lane = threadIdx.x;
+  const int32_t C = a.C, D = a.D;
+  const bool mine = lane < D;
+  if (a.links)
+    for (int i = lane; i < D * D; i += 64) {
+      s_bw[i] = (int32_t)a.lbw[i];
+      s_lat[i] = (int32_t)a.llat[i];
+    }
+  lds_order();
+  wave_lds_sync();
+  int64_t ava = mine ? a.cap[lane] : 0;
+  int32_t nb = 0;
+  int64_t lastb = 0;
+  int64_t *xs = a.bs + (int64_t)(mine ? lane : 0) * a.bcap, *xf = a.bf + (int64_t)(mine ? lane : 0) * a.bcap;
+  int32_t prev = 0, be = 0;
+  int64_t span = 0;
+  auto finof = [&](int32_t c) -> int64_t { return LDSF ? s_fin[c] : a.Fin[c]; };
+  auto devof = [&](int32_t c) -> int32_t { return LDSF ? (int32_t)s_cd[c] : (int32_t)a.cdev[c]; };
+  for (int32_t t = 0; t < C; t++) {
+    // followers of earlier groups: their memory on their leading device
+    const int32_t f0 = a.foff[t], f1 = a.foff[t + 1];
+    for (int32_t k0 = f0; k0 < f1; k0 += 64) {
+      const int32_t k = k0 + lane;
+      int32_t fd = -1;
+      int64_t fmv = 0;
+      if (k < f1) {
+        fd = devof(a.fl[k]);
+        fmv = a.fm[k];
+      }
+      const int nk = f1 - k0 < 64 ? f1 - k0 : 64;
+      for (int j = 0; j < nk; j++) {
+        const int32_t dj = __builtin_amdgcn_readlane(fd, j);
+        const int64_t mj = readlane64(fmv, j);
+        if (lane == dj) ava -= mj;
+      }
+    }
+    const int64_t Mt = (int64_t)a.MEMo[t];
+    const int64_t Wx = mine ? (int64_t)a.W2[(int64_t)t * D + lane] : 0;
+    // pre_t on device `lane` (eq. 7)
+    int64_t pre = 0;
+    const int32_t b0 = a.boff[t], np = a.ncp[t];
+    for (int32_t k0 = 0; k0 < np; k0 += 64) {
+      const int32_t k = k0 + lane;
+      int64_t pf = 0, pc = 0, po = 0, pn = 0;
+      int32_t pd = 0;
+      if (k < np) {
+        const int32_t pa = a.ca[b0 + k];
+        pf = finof(pa);
+        pd = devof(pa);
+        pc = a.cc[b0 + k];
+        if (a.links) {
+          po = a.cob[b0 + k];
+          pn = a.cnum[b0 + k];
+        }
+      }
+      const int nk = np - k0 < 64 ? np - k0 : 64;
+      for (int j = 0; j < nk; j++) {
+        const int64_t fj = readlane64(pf, j);
+        const int32_t dj = __builtin_amdgcn_readlane(pd, j);
+        int64_t cost = 0;
+        if (dj != lane) {
+          if (a.links)
+            cost = link_cost(readlane64(po, j), readlane64(pn, j), s_bw[dj * D + (mine ? lane : 0)],
+                             s_lat[dj * D + (mine ? lane : 0)]);
+          else
+            cost = readlane64(pc, j);
+        }
+        pre = fj + cost > pre ? fj + cost : pre;
+      }
+    }
+    // first fit on device `lane`
+    int64_t sv = pre;
+    if (mine && Wx > 0 && nb > 0 && sv < lastb)
+      for (int32_t q = blocks_ending_by(xf, nb, sv); q < nb && xs[q] < sv + Wx; q++) sv = xf[q];
+    const int64_t eft = (mine && ava >= Mt) ? sv + Wx : kInf;
+    // best device (lowest id on ties)
+    int64_t ev = eft;
+    int32_t ei = lane;
+    for (int off = 32; off > 0; off >>= 1) {
+      const int64_t ov = __shfl_xor((long long)ev, off);
+      const int32_t oi = __shfl_xor(ei, off);
+      if (ov < ev || (ov == ev && oi < ei)) {
+        ev = ov;
+        ei = oi;
+      }
+    }
+    const int32_t dk = t == 0 ? 0 : prev;
+    const int64_t edk = readlane64(eft, dk);
+    int32_t pick;
+    if (ev == kInf) {  // every device full: most remaining memory (best effort)
+      int64_t av = mine ? ava : INT64_MIN;
+      int32_t ai = mine ? lane : INT32_MAX;
+      argmax_i64(av, ai);
+      pick = ai;
+      be++;
+    } else if (edk == kInf || ei == dk) {
+      pick = ei;
+    } else {
+      int64_t bk = 0;  // back_cost (eq. 8)
+      if (!a.links) {
+        bk = (int64_t)a.back[t];
+      } else {
+        const int32_t bw = s_bw[ei * D + dk], lt = s_lat[ei * D + dk];
+        for (int32_t k = a.soff[t] + lane; k < a.soff[t + 1]; k += 64) {
+          const int64_t c = link_cost(a.sob[k], a.snum[k], bw, lt);
+          bk = c > bk ? c : bk;
+        }
+        for (int off = 32; off > 0; off >>= 1) {
+          const int64_t o = __shfl_xor((long long)bk, off);
+          bk = o > bk ? o : bk;
+        }
+      }
+      pick = edk - ev > bk ? ei : dk;
+    }
+    const int64_t s0 = readlane64(sv, pick), wp = readlane64(Wx, pick), f = s0 + wp;
+    span = f > span ? f : span;
+    prev = pick;
+    if (lane == pick) {
+      if (wp > 0) lastb = busy_insert(xs, xf, nb, a.bcap, s0, f, st);
+      ava -= Mt;
+    }
+    if (lane == 0) {  // later steps of this wave read these back, in program order
+      a.cdev[t] = (uint8_t)pick;
+      a.Fin[t] = f;
+      if (LDSF) {
+        s_fin[t] = f;
+        s_cd[t] = (uint8_t)pick;
+      }
+    }
+    if (LDSF) lds_order();
+  }
+  if (lane == 0) {
+    st->s0 = span;
+    st->i0 = be;
+  }
+}
+
+// node_dev: a group member takes its leading cluster's device, every other
+// node its own cluster's; cluster finish times out.
+__global__ void k_pe_out(int32_t n, int32_t C, const int32_t *cid, const int32_t *group,
+                         const int32_t *lead, const uint8_t *cdev, uint8_t *node_dev,
+                         const int64_t *Fin, int64_t *fin_out, const Status *st) {
+  if (failed(st)) return;
+  const int64_t tot = n > C ? n : C;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < tot;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    if (i < n) {
+      const int32_t gv = group ? group[i] : -1;
+      node_dev[i] = cdev[gv >= 0 ? lead[gv] : cid[i]];
+    }
+    if (fin_out && i < C) fin_out[i] = Fin[i];
+  }
+}
+
 __global__ void k_place_out(int32_t n, int32_t C, const int32_t *cid, const uint8_t *cdev,
                             uint8_t *node_dev, const int64_t *Fin, int64_t *fin_out,
                             const Status *st) {
@@ -694,5 +972,210 @@ extern "C" int cel_order_place(const cel_graph *g, const cel_devices *d, const i
   CEL_TRY(read_status(st, &h, s));
   if (h.err) return status_error(h, fn);
   *best_effort_count = h.i0;
+  return CEL_OK;
+}
+
+extern "C" int cel_place_ext(const cel_graph *g, const cel_devices *d, const cel_hetero *h,
+                             const int32_t *group, int32_t n_groups, const int32_t *cluster_id,
+                             int32_t C, uint8_t *cluster_dev, uint8_t *node_dev,
+                             int64_t *cluster_fin, int64_t *coarse_makespan,
+                             int32_t *best_effort_count, hipStream_t s) {
+  const char *fn = "cel_place_ext";
+  CEL_TRY(check_host_graph(g, fn));
+  CEL_TRY(check_host_devices(d, fn));
+  const int32_t n = g->n, D = d->D;
+  if (!coarse_makespan || !best_effort_count || (n > 0 && (!cluster_id || !node_dev)) ||
+      (C > 0 && !cluster_dev) || n_groups < 0 || (n_groups > 0 && n > 0 && !group))
+    return set_error(CEL_E_ARG, "%s: NULL argument or n_groups < 0", fn);
+  if (C < 0 || (n > 0 && C < 1) || C > (n > 0 ? n : 0))
+    return set_error(CEL_E_ARG, "%s: n_clusters = %d out of range", fn, C);
+  if (D > 64) return set_error(CEL_E_ARG, "%s: D = %d above 64", fn, D);
+  const bool het = h && (h->tmul || h->bw || h->lat);
+  const bool links = het && (h->bw || h->lat);
+  int64_t bwmin = d->bw, latmax = d->lat, tmax = 1024;
+  if (het) {
+    CEL_TRY(check_hetero(h, d, fn, &bwmin, &latmax, &tmax));
+    // overflow bound with the slowest device and the worst link: every time
+    // is a sum of cluster durations and coarse-edge costs along one chain,
+    // each coarse cost at most the sum of its member edges' worst-link c
+    cel_devices worst = *d;
+    worst.bw = bwmin;
+    worst.lat = latmax;
+    int64_t ec = 0, ws = 0;
+    CEL_TRY(cel_comm_sums(g, &worst, nullptr, &ec, &ws, s));
+    const __int128 tot = (__int128)ws * ((tmax + 1023) / 1024) + ec;
+    if (tot >= ((__int128)1 << 62))
+      return set_error(CEL_E_OVERFLOW, "%s: times could reach 2^62", fn);
+  }
+  Scratch sc(s);
+  Status *st;
+  int32_t *tmp;
+  CEL_TRY(sc.get(&st, 1));
+  CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
+  CEL_TRY(sc.get(&tmp, n));
+  CEL_TRY(check_graph(g, d->bw, d->lat, true, st, tmp, sc, s));
+  if (C == 0) {
+    Status hs;
+    CEL_TRY(read_status(st, &hs, s));
+    if (hs.err) return status_error(hs, fn);
+    *coarse_makespan = 0;
+    *best_effort_count = 0;
+    return CEL_OK;
+  }
+  const bool grp = n_groups > 0;
+  const int64_t m = g->m, bcap = C;
+  uint64_t *W2, *MEMo, *back, *keys;
+  int32_t *cnt, *boff, *ca, *ncp, *lead, *fcnt, *foff, *fl, *soff, *scnt;
+  int64_t *ecost, *eob, *eone, *cc, *cob, *cnum, *Fin, *bs, *bf, *dcap, *tm_d = nullptr, *fm;
+  int64_t *sob = nullptr, *snum = nullptr, *lbw = nullptr, *llat = nullptr;
+  uint32_t *ids;
+  CEL_TRY(sc.get(&W2, (int64_t)C * D));
+  CEL_TRY(sc.get(&MEMo, C));
+  CEL_TRY(sc.get(&back, C));
+  CEL_TRY(sc.get(&cnt, C));
+  CEL_TRY(sc.get(&boff, (int64_t)C + 1));
+  CEL_TRY(sc.get(&ncp, C));
+  CEL_TRY(sc.get(&Fin, C));
+  CEL_TRY(sc.get(&dcap, D));
+  CEL_TRY(sc.get(&bs, D * bcap));
+  CEL_TRY(sc.get(&bf, D * bcap));
+  CEL_TRY(sc.get(&lead, grp ? n_groups : 1));
+  CEL_TRY(sc.get(&fcnt, C));
+  CEL_TRY(sc.get(&foff, (int64_t)C + 1));
+  CEL_TRY(sc.get(&soff, (int64_t)C + 1));
+  CEL_TRY(sc.get(&scnt, C));
+  CEL_HIP(hipMemsetAsync(W2, 0, sizeof(uint64_t) * C * D, s));
+  CEL_HIP(hipMemsetAsync(MEMo, 0, sizeof(uint64_t) * C, s));
+  CEL_HIP(hipMemsetAsync(back, 0, sizeof(uint64_t) * C, s));
+  CEL_HIP(hipMemsetAsync(cnt, 0, sizeof(int32_t) * C, s));
+  CEL_HIP(hipMemsetAsync(fcnt, 0, sizeof(int32_t) * C, s));
+  CEL_HIP(hipMemcpyAsync(dcap, d->cap, sizeof(int64_t) * D, hipMemcpyHostToDevice, s));
+  std::vector<int64_t> ht, hb, hl;
+  if (het && h->tmul) {
+    CEL_TRY(sc.get(&tm_d, D));
+    ht.assign(h->tmul, h->tmul + D);
+    CEL_HIP(hipMemcpyAsync(tm_d, ht.data(), sizeof(int64_t) * D, hipMemcpyHostToDevice, s));
+  }
+  if (links) {
+    CEL_TRY(sc.get(&lbw, (int64_t)D * D));
+    CEL_TRY(sc.get(&llat, (int64_t)D * D));
+    hb.resize((size_t)D * D);
+    hl.resize((size_t)D * D);
+    for (int32_t i = 0; i < D * D; i++) {
+      const bool diag = i / D == i % D;
+      hb[i] = diag ? 1 : (h->bw ? h->bw[i] : d->bw);
+      hl[i] = diag ? 0 : (h->lat ? h->lat[i] : d->lat);
+      if (hb[i] < 1 || hb[i] > INT32_MAX || hl[i] < 0 || hl[i] > INT32_MAX)
+        return set_error(CEL_E_ARG, "%s: link %d: bw in [1, 2^31) and lat in [0, 2^31) needed", fn, i);
+    }
+    CEL_HIP(hipMemcpyAsync(lbw, hb.data(), sizeof(int64_t) * D * D, hipMemcpyHostToDevice, s));
+    CEL_HIP(hipMemcpyAsync(llat, hl.data(), sizeof(int64_t) * D * D, hipMemcpyHostToDevice, s));
+  }
+  if (group && n > 0) {  // group ids checked even when there are no groups
+    if (grp) k_fill_i32<<<grid_for(n_groups, 256, 1024), 256, 0, s>>>(lead, n_groups, INT32_MAX);
+    k_colo_lead<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, n_groups, group, cluster_id,
+                                                      grp ? lead : nullptr, st);
+  }
+  k_pe_nodes<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, C, D, cluster_id, g->w, g->mem,
+                                                    grp ? group : nullptr, lead, tm_d, W2, MEMo,
+                                                    fcnt, st);
+  CEL_TRY(exclusive_scan_i32(fcnt, foff, C, sc, s));
+  const unsigned eb = edge_blocks(g->m);
+  k_place_edges<0><<<eb, 256, 0, s>>>(*g, d->bw, d->lat, cluster_id, cnt, nullptr, nullptr,
+                                      nullptr, nullptr, st);
+  CEL_TRY(exclusive_scan_i32(cnt, boff, C, sc, s));
+  Status hs;
+  CEL_TRY(read_status(st, &hs, s));
+  if (hs.err) return status_error(hs, fn);
+  int32_t counts[2];  // coarse-edge slots, followers
+  CEL_HIP(hipMemcpyAsync(&counts[0], boff + C, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  CEL_HIP(hipMemcpyAsync(&counts[1], foff + C, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  CEL_HIP(hipStreamSynchronize(s));
+  const int64_t ncross = counts[0], nfol = counts[1];
+  CEL_TRY(sc.get(&keys, ncross));
+  CEL_TRY(sc.get(&ids, ncross));
+  CEL_TRY(sc.get(&ca, ncross));
+  CEL_TRY(sc.get(&cc, ncross));
+  CEL_TRY(sc.get(&ecost, m));
+  CEL_TRY(sc.get(&fl, nfol));
+  CEL_TRY(sc.get(&fm, nfol));
+  if (nfol > 0) {
+    CEL_HIP(hipMemsetAsync(fcnt, 0, sizeof(int32_t) * C, s));
+    k_pe_followers<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, cluster_id, g->mem, group, lead, foff,
+                                                          fcnt, fl, fm, st);
+  }
+  CEL_HIP(hipMemsetAsync(cnt, 0, sizeof(int32_t) * C, s));
+  k_place_edges<1><<<eb, 256, 0, s>>>(*g, d->bw, d->lat, cluster_id, cnt, boff, keys, ids, ecost,
+                                      st);
+  CEL_TRY(segmented_sort(keys, ids, boff, C, ncross, sc, s, st));
+  const int cg = grid_for((int64_t)C * 64, 256, 8192);
+  k_place_combine<<<cg, 256, 0, s>>>(C, boff, keys, ids, ecost, ca, cc, ncp, back, st);
+  cob = cnum = nullptr;
+  if (links) {
+    int32_t *ca2, *ncp2;
+    uint64_t *back2;
+    CEL_TRY(sc.get(&eob, m));
+    CEL_TRY(sc.get(&eone, m));
+    CEL_TRY(sc.get(&cob, ncross));
+    CEL_TRY(sc.get(&cnum, ncross));
+    CEL_TRY(sc.get(&ca2, ncross));
+    CEL_TRY(sc.get(&ncp2, C));
+    CEL_TRY(sc.get(&back2, C));
+    CEL_TRY(sc.get(&sob, ncross));
+    CEL_TRY(sc.get(&snum, ncross));
+    k_pe_edge_ob<<<eb, 256, 0, s>>>(*g, eob, eone, st);
+    // the same runs summed over ob and over a count of one (their sources
+    // and run counts are those of the first pass)
+    k_place_combine<<<cg, 256, 0, s>>>(C, boff, keys, ids, eob, ca2, cob, ncp2, back2, st);
+    k_place_combine<<<cg, 256, 0, s>>>(C, boff, keys, ids, eone, ca2, cnum, ncp2, back2, st);
+    CEL_HIP(hipMemsetAsync(scnt, 0, sizeof(int32_t) * C, s));
+    k_pe_succ<0><<<grid_for(C, 256, 4096), 256, 0, s>>>(C, boff, ncp, ca, cob, cnum, scnt, nullptr,
+                                                       nullptr, nullptr, st);
+    CEL_TRY(exclusive_scan_i32(scnt, soff, C, sc, s));
+    CEL_HIP(hipMemsetAsync(scnt, 0, sizeof(int32_t) * C, s));
+    k_pe_succ<1><<<grid_for(C, 256, 4096), 256, 0, s>>>(C, boff, ncp, ca, cob, cnum, scnt, soff,
+                                                       sob, snum, st);
+  }
+  PeArgs pa{};
+  pa.C = C;
+  pa.D = D;
+  pa.links = links;
+  pa.cap = dcap;
+  pa.W2 = W2;
+  pa.MEMo = MEMo;
+  pa.boff = boff;
+  pa.ncp = ncp;
+  pa.ca = ca;
+  pa.cc = cc;
+  pa.cob = cob;
+  pa.cnum = cnum;
+  pa.back = back;
+  pa.soff = soff;
+  pa.sob = sob;
+  pa.snum = snum;
+  pa.foff = foff;
+  pa.fl = fl;
+  pa.fm = fm;
+  pa.lbw = lbw;
+  pa.llat = llat;
+  pa.cdev = cluster_dev;
+  pa.Fin = Fin;
+  pa.bs = bs;
+  pa.bf = bf;
+  pa.bcap = (int32_t)bcap;
+  {
+    KTimer kt(s, "k_place_ext");
+    if (C <= kPeLds) k_place_ext<true><<<1, 64, 0, s>>>(pa, st);
+    else k_place_ext<false><<<1, 64, 0, s>>>(pa, st);
+  }
+  k_pe_out<<<grid_for(n > C ? n : C, 256, 4096), 256, 0, s>>>(n, C, cluster_id,
+                                                             grp ? group : nullptr, lead,
+                                                             cluster_dev, node_dev, Fin,
+                                                             cluster_fin, st);
+  CEL_HIP(hipGetLastError());
+  CEL_TRY(read_status(st, &hs, s));
+  if (hs.err) return status_error(hs, fn);
+  *coarse_makespan = hs.s0;
+  *best_effort_count = hs.i0;
   return CEL_OK;
 }

@@ -1183,3 +1183,122 @@ def test_step_latency_probe():
         assert 5.0 < ns < 5000.0, (v, ns)
     with pytest.raises(cel.CelError):
         cel.step_latency(3, 100)
+
+
+# ------------- Adjusting Placement with heterogeneous devices/links and co-location
+
+
+def check_place_ext(wl, cid, C, het=None, grp=None, G=0):
+    het = het or {}
+    ref = O.place_ext(wl, cid, C, group=grp, n_groups=G, **het)
+    g, d = up(wl)
+    print(f"[place_ext] n={wl.n} C={C} D={wl.D} het={sorted(het)} groups={G}", flush=True)
+    got = cel.place_ext(g, d, tt(cid, np.int32), C, group=None if grp is None else tt(grp, np.int32),
+                        n_groups=G, **het)
+    assert np.array_equal(np_(got[0]), ref[0]) and np.array_equal(np_(got[1]), ref[1])
+    assert got[2] == ref[2] and got[3] == ref[3] and np.array_equal(np_(got[4]), ref[4])
+    return ref
+
+
+def test_place_ext_hand_fixtures():
+    import json
+    import os
+    gold = os.path.join(os.path.dirname(__file__), "golden", "place_ext_hand.json")
+    for case in json.load(open(gold))["cases"]:
+        wl = from_edges(case["n"], case["edges"], case["w"], case["ob"], case["D"], case["cap"],
+                        case["bw"], case["lat"])
+        g, d = up(wl)
+        for v in case["variants"]:
+            grp = v.get("group")
+            cdev, ndev, span, be, fin = cel.place_ext(
+                g, d, tt(case["cluster_id"], np.int32), case["C"], tmul=v.get("tmul"),
+                bw=v.get("bw_matrix"), lat=v.get("lat_matrix"),
+                group=None if grp is None else tt(grp, np.int32), n_groups=v.get("n_groups", 0))
+            assert np_(cdev).tolist() == v["cluster_dev"] and np_(ndev).tolist() == v["node_dev"]
+            assert np_(fin).tolist() == v["fin"] and span == v["span"] and be == v["be"]
+
+
+def test_place_ext_without_extras_is_place():
+    for cfg in (1, 3):
+        wl, rt, rb = config(cfg, 0)
+        cid, C, _ = O.cluster(wl, rb[2], 200, -1)
+        ref = check_place_ext(wl, cid, C)
+        g, d = up(wl)
+        cdev, ndev, span, be = cel.place(g, d, tt(cid, np.int32), C)
+        assert np.array_equal(np_(cdev), ref[0]) and span == ref[2] and be == ref[3]
+
+
+def test_place_ext_random():
+    rng = np.random.default_rng(71)
+    for s in range(24):
+        n = 5 + (s * 97) % 700
+        D = [1, 2, 3, 5, 8, 16, 64, 33][s % 8]
+        wl = make_random_dag(9300 + s, n, p_edge=min(0.5, 4.0 / n), D=D,
+                             cap_frac=(1, 1 + s % 5), multi=(s % 3 == 0),
+                             zero_frac=0.2 if s % 4 == 0 else 0.0)
+        order = random_topo_order(wl, rng)
+        cid, C, _ = O.cluster(wl, order, int(rng.integers(1, 40)), -1, s % 2)
+        parts = [("tmul", "bw", "lat"), ("tmul",), ("bw",), ("lat",), ()][s % 5]
+        het = {k: v for k, v in rand_het(rng, wl, parts).items() if v is not None}
+        G = 0 if s % 3 == 0 else max(1, n // (2 + s % 7))
+        grp = rng.integers(-1, G, n).astype(np.int32) if G else None
+        check_place_ext(wl, cid, C, het, grp, G)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 5])
+def test_place_ext_configs(cfg):
+    wl, rt, rb = config(cfg, 0)
+    rng = np.random.default_rng(72 + cfg)
+    cid, C, _ = O.cluster(wl, rb[2], 200, -1)
+    G = wl.n // 40
+    grp = np.full(wl.n, -1, np.int32)
+    pick = rng.permutation(wl.n)[:4 * G]
+    grp[pick] = np.repeat(np.arange(G, dtype=np.int32), 4)
+    check_place_ext(wl, cid, C, {k: v for k, v in rand_het(rng, wl).items()}, grp, G)
+    check_place_ext(wl, cid, C, {"tmul": rand_het(rng, wl, ("tmul",))["tmul"]})
+
+
+def test_place_ext_many_clusters():
+    """More clusters than the placement keeps in LDS (config 3, R = 4)."""
+    wl, rt, rb = config(3, 0)
+    rng = np.random.default_rng(74)
+    cid, C, _ = O.cluster(wl, rb[2], 4, -1)
+    assert C > 8192
+    grp = rng.integers(-1, 500, wl.n).astype(np.int32)
+    check_place_ext(wl, cid, C, {k: v for k, v in rand_het(rng, wl).items()}, grp, 500)
+
+
+def test_place_ext_transformer96():
+    """Full size: the CPD-TOPO clustering of transformer-96 (6,284 clusters, 16
+    devices) with two device speeds, faster links inside device pairs and
+    26,765 co-location groups of 4 nodes."""
+    wl = make_config(4, 0)
+    D = wl.D
+    het = dict(tmul=[1024 if x < D // 2 else 2048 for x in range(D)],
+               bw=[[2 * wl.bw if x // 2 == y // 2 else wl.bw for y in range(D)] for x in range(D)],
+               lat=[[wl.lat // 2 if x // 2 == y // 2 else wl.lat for y in range(D)]
+                    for x in range(D)])
+    rng = np.random.default_rng(75)
+    G = wl.n // 40
+    grp = np.full(wl.n, -1, np.int32)
+    grp[rng.permutation(wl.n)[:4 * G]] = np.repeat(np.arange(G, dtype=np.int32), 4)
+    cid, C, _ = O.cluster(wl, oracle_cpd(wl), 200, -1)
+    check_place_ext(wl, cid, C, het, grp, G)
+
+
+def test_place_ext_errors():
+    wl, rt, rb = config(1, 0)
+    cid, C, _ = O.cluster(wl, rb[2], 200, -1)
+    g, d = up(wl)
+    c = tt(cid, np.int32)
+    with pytest.raises(cel.CelError) as ei:  # group id beyond n_groups
+        cel.place_ext(g, d, c, C, group=tt(np.full(wl.n, 3, np.int32), np.int32), n_groups=3)
+    assert ei.value.code == -1
+    with pytest.raises(cel.CelError) as ei:  # a time multiplier out of range
+        cel.place_ext(g, d, c, C, tmul=[0] * wl.D)
+    assert ei.value.code == -1
+    wl2 = make_random_dag(5, 80, p_edge=0.05, D=65)
+    g2, d2 = up(wl2)
+    with pytest.raises(cel.CelError) as ei:  # more than 64 devices
+        cel.place_ext(g2, d2, tt(np.zeros(80, np.int32), np.int32), 1)
+    assert ei.value.code == -1
