@@ -13,8 +13,33 @@ namespace cel {
 constexpr int kKahnB = 1024;
 constexpr int kKahnNW = kKahnB / 64;
 constexpr int kKahnA = 4;         // successors carried with a frontier entry
-constexpr int kKahnCap = 2048;    // frontier entries mirrored in LDS
+constexpr int kKahnCap = 1024;    // frontier entries mirrored in LDS
 constexpr int kKahnE = 4;         // edges per thread whose loads and atomics go out together
+constexpr int kKahnCW = 16384;    // LDS words of packed in-degree counters (64 KB)
+
+// Remaining in-edges of every node from non-sources (a source is removed in
+// the first round and nothing waits on it: an edge from a source never needs
+// its decrement), and the largest such count.
+__global__ void k_kahn_cnt(int32_t n, const int32_t *in_ptr, const int32_t *in_idx, int32_t *cnt,
+                           int32_t *cmax, const Status *st) {
+  if (failed(st)) return;
+  int32_t mx = 0;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    int32_t c = 0;
+    for (int32_t e = in_ptr[v]; e < in_ptr[v + 1]; e++) {
+      const int32_t u = in_idx[e];
+      c += in_ptr[u + 1] > in_ptr[u] ? 1 : 0;
+    }
+    cnt[v] = c;
+    mx = c > mx ? c : mx;
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const int32_t o = __shfl_xor(mx, off);
+    mx = o > mx ? o : mx;
+  }
+  if ((threadIdx.x & 63) == 0 && mx > 0) atomicMax(cmax, mx);
+}
 
 // Per node: first out-edge and out-degree, and its first kKahnA successors
 // (-1 past the end), so that a node that becomes ready brings its adjacency
@@ -60,38 +85,83 @@ __device__ inline void kahn_append(bool want, int32_t v, const int2 &d, const in
   }
 }
 
-// Level-synchronous Kahn in one workgroup.  A frontier node of degree at most
-// kKahnA removes its in-edge from each successor with a global atomic; the
-// successor's degree and first successors are loaded in the same round, so
-// the node that the last removal makes ready joins the next frontier with its
-// adjacency.  Nodes of higher degree are listed and their edges then spread
-// over the whole block (flattened by a prefix sum of the degrees).
-__global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, const int2 *deg,
-                                                 const int4 *adj, int32_t *F, int32_t *level,
-                                                 int32_t *lstart, Status *st) {
+// Level-synchronous Kahn in one workgroup.  The sources form level 0 and
+// their out-edges are never counted (k_kahn_cnt); the nodes whose in-edges
+// all come from sources form level 1.  From there a frontier node of degree
+// at most kKahnA removes its in-edge from each successor; the successor's
+// degree and first successors are loaded in the same round, so the node that
+// the last removal makes ready joins the next frontier with its adjacency.
+// Nodes of higher degree are listed and their edges then spread over the
+// whole block (flattened by a prefix sum of the degrees).
+// In-degree counters live in LDS when they fit: b-bit fields (b = 2, 4 or 8,
+// the smallest that holds the largest count) packed 32 / b to a word, each
+// removal one LDS atomic subtract of 1 << field offset that returns the old
+// word (a field only ever counts down to zero, so no borrow crosses fields).
+// Otherwise they stay in global memory (one returning atomic per removal).
+__global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, const int32_t *cmax,
+                                                 const int2 *deg, const int4 *adj, int32_t *F,
+                                                 int32_t *level, int32_t *lstart, Status *st) {
   __shared__ int32_t s_tail, s_nh[3];  // s_nh: listed nodes, counters used by passes in turn
   __shared__ int32_t s_fv[2][kKahnCap];
   __shared__ int2 s_fd[2][kKahnCap];  // first out-edge, out-degree
   __shared__ int4 s_fa[2][kKahnCap];
   __shared__ int32_t s_hd[kKahnB], s_he[kKahnB], s_hp[kKahnB + 1];
   __shared__ int32_t s_wt[kKahnNW];
+  __shared__ uint32_t s_cnt[kKahnCW];
   if (failed(st)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t n = g.n;
+  // counter layout: b bits per node, 32 / b nodes per word
+  const int32_t cm = *cmax;
+  const int32_t cb = cm < 4 ? 2 : (cm < 16 ? 4 : 8);
+  const int32_t lper = cb == 2 ? 4 : (cb == 4 ? 3 : 2);  // log2(32 / b)
+  const uint32_t fmask = (1u << cb) - 1u;
+  const bool ldsc = cm < 256 && (((int64_t)n << 5 >> lper) <= (int64_t)kKahnCW * 32);
   if (tid == 0) {
     s_tail = 0;
     s_nh[0] = s_nh[1] = s_nh[2] = 0;
   }
-  __syncthreads();
-  for (int32_t v0 = 0; v0 < n; v0 += kKahnB) {  // sources
-    const int32_t v = v0 + tid;
-    const bool src = v < n && cnt[v] == 0;
-    const int2 d = src ? deg[v] : make_int2(0, 0);
-    const int4 a = src ? adj[v] : make_int4(-1, -1, -1, -1);
-    kahn_append(src, v, d, a, F, &s_tail, 0, s_fv[0], s_fd[0], s_fa[0]);
+  if (ldsc) {
+    const int32_t per = 1 << lper, nw = (n + per - 1) >> lper;
+    for (int32_t wd = tid; wd < nw; wd += kKahnB) {
+      uint32_t x = 0;
+      for (int32_t j = 0; j < per; j++) {
+        const int32_t v = (wd << lper) + j;
+        if (v < n) x |= (uint32_t)cnt[v] << (j * cb);
+      }
+      s_cnt[wd] = x;
+    }
   }
   __syncthreads();
-  int32_t fb = 0, fe = s_tail, lvl = 0, cur = 0, pp = 0;
+  // the count of t before this removal
+  auto remove_edge = [&](int32_t t) -> int32_t {
+    if (ldsc) {
+      const int32_t sh = (t & ((1 << lper) - 1)) * cb;
+      const uint32_t old = atomicSub(&s_cnt[t >> lper], 1u << sh);
+      return (int32_t)((old >> sh) & fmask);
+    }
+    return atomicSub(&cnt[t], 1);
+  };
+  for (int32_t v0 = 0; v0 < n; v0 += kKahnB) {  // level 0: the sources
+    const int32_t v = v0 + tid;
+    const bool src = v < n && g.in_ptr[v + 1] == g.in_ptr[v];
+    kahn_append(src, v, make_int2(0, 0), make_int4(-1, -1, -1, -1), F, &s_tail, 0, s_fv[0],
+                s_fd[0], s_fa[0]);
+  }
+  __syncthreads();
+  const int32_t nsrc = s_tail;
+  if (tid == 0) lstart[0] = 0;
+  __syncthreads();
+  for (int32_t v0 = 0; v0 < n; v0 += kKahnB) {  // level 1: every in-edge from a source
+    const int32_t v = v0 + tid;
+    const bool one = v < n && g.in_ptr[v + 1] > g.in_ptr[v] && cnt[v] == 0;
+    const int2 d = one ? deg[v] : make_int2(0, 0);
+    const int4 a = one ? adj[v] : make_int4(-1, -1, -1, -1);
+    kahn_append(one, v, d, a, F, &s_tail, nsrc, s_fv[1], s_fd[1], s_fa[1]);
+  }
+  for (int32_t i = tid; i < nsrc; i += kKahnB) level[F[i]] = 0;
+  __syncthreads();
+  int32_t fb = nsrc, fe = s_tail, lvl = nsrc > 0 ? 1 : 0, cur = 1, pp = 0;
   while (fb < fe) {
     if (tid == 0) lstart[lvl] = fb;
     int32_t *nv = s_fv[cur ^ 1];
@@ -132,9 +202,9 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
           td[q] = make_int2(0, 0);
           ta[q] = make_int4(-1, -1, -1, -1);
           if (light && q < d.y) {
-            c[q] = atomicSub(&cnt[t], 1);
             td[q] = deg[t];
             ta[q] = adj[t];
+            c[q] = remove_edge(t);
           }
         }
 #pragma unroll
@@ -193,9 +263,9 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
             td[q] = make_int2(0, 0);
             ta[q] = make_int4(-1, -1, -1, -1);
             if (v[q] >= 0) {
-              c[q] = atomicSub(&cnt[v[q]], 1);
               td[q] = deg[v[q]];
               ta[q] = adj[v[q]];
+              c[q] = remove_edge(v[q]);
             }
           }
 #pragma unroll
@@ -245,13 +315,18 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
   CEL_TRY(check_graph(g, 1, 0, /*bound=*/false, st, cnt, sc, s));
   int2 *deg;
   int4 *adj;
+  int32_t *cmax;
   CEL_TRY(sc.get(&deg, n));
   CEL_TRY(sc.get(&adj, n));
-  if (n > 0)
+  CEL_TRY(sc.get(&cmax, 1));
+  CEL_HIP(hipMemsetAsync(cmax, 0, sizeof(int32_t), s));
+  if (n > 0) {
     k_kahn_prep<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, g->out_ptr, g->out_idx, deg, adj, st);
+    k_kahn_cnt<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, g->in_ptr, g->in_idx, cnt, cmax, st);
+  }
   {
     KTimer kt(s, "k_kahn");
-    k_kahn<<<1, kKahnB, 0, s>>>(*g, cnt, deg, adj, order_id, level, level_ptr, st);
+    k_kahn<<<1, kKahnB, 0, s>>>(*g, cnt, cmax, deg, adj, order_id, level, level_ptr, st);
   }
   CEL_HIP(hipGetLastError());
   Status h;
