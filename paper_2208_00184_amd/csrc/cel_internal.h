@@ -16,7 +16,7 @@ constexpr int kMaxD = 255;
 constexpr uint64_t kNoAllocScratchBytes = CEL_NOALLOC_SCRATCH_BYTES;  // cel_makespan_noalloc's array
 
 // error bits raised by device-side checks (Status::err)
-enum : uint32_t { EB_ARG = 1u, EB_CYCLE = 2u, EB_OVERFLOW = 4u, EB_ORDER = 8u };
+enum : uint32_t { EB_ARG = 1u, EB_CYCLE = 2u, EB_OVERFLOW = 4u, EB_ORDER = 8u, EB_WAIT = 16u };
 
 // Per-call device status block.  Kernels after a failed check read `err` and
 // return without touching data addressed by unchecked indices.
@@ -392,6 +392,12 @@ __global__ void k_makespan_out(int32_t K, int32_t n, const int32_t *order, const
                                const Status *st);
 __global__ void k_fill_i64(int64_t *p, int64_t n, int64_t v);
 __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v);  // common.hip
+// sweep.hip: one level sweep of eq. 3 (rev: b-level over successors) or eq. 2
+// (t-level over predecessors) in position space; out[p] = the value at p
+int level_sweep(bool rev, int32_t n, int32_t m, int32_t L, const int32_t *lp,
+                const int32_t *order, const int32_t *level, const int32_t *rptr,
+                const int32_t *ridx, const int64_t *wp, const int64_t *wcp, int64_t *out,
+                class Scratch &sc, hipStream_t s, Status *st, const char *timer);
 // makespan_model.hip: a heterogeneous descriptor's ranges, its slowest
 // multiplier, smallest bandwidth and largest latency; lead[g] = smallest
 // pos[v] over the members v of group g (INT32_MAX before)

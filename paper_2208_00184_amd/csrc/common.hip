@@ -32,6 +32,8 @@ int status_error(const Status &h, const char *fn) {
     return set_error(CEL_E_OVERFLOW, "%s: sum(w) + sum over edges of c[src] reaches 2^62", fn);
   if (h.err & EB_ORDER)
     return set_error(CEL_E_ORDER, "%s: order/level/cluster arrays inconsistent with the graph", fn);
+  if (h.err & EB_WAIT)
+    return set_error(CEL_E_HIP, "%s: a bounded wait between waves of a sweep timed out", fn);
   return CEL_OK;
 }
 

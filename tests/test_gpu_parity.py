@@ -365,6 +365,46 @@ def test_heavy_window_nodes():
     assert np_(ms1)[0] == ref_ms[1] and np.array_equal(np_(fi1)[0], ref_fi[1])
 
 
+def test_sweep_many_near_neighbours():
+    """Narrow levels (1..150 nodes) where about one node in 20 has 9..300
+    successors or predecessors within the next few levels: the b-level and
+    t-level sweeps gather those along slot lists instead of pull records, and
+    rows mixing such nodes with ordinary ones, or ending mid-row, take every
+    gather width."""
+    rng = np.random.default_rng(21)
+    widths = [int(x) for x in rng.integers(1, 151, 120)]
+    starts = np.concatenate([[0], np.cumsum(widths)])
+    n = int(starts[-1])
+    edges = set()
+    for li in range(len(widths) - 1):
+        for v in range(int(starts[li]), int(starts[li + 1])):
+            hi = int(starts[min(li + 4, len(widths))])
+            lo = int(starts[li + 1])
+            k = int(rng.integers(1, 4))
+            if rng.random() < 0.05:
+                k = int(rng.integers(9, 301))
+            for u in rng.integers(lo, hi, k):
+                edges.add((v, int(u)))
+        # a node of the next level with many predecessors
+        if rng.random() < 0.3:
+            t = int(rng.integers(starts[li + 1], starts[li + 2]))
+            lo = int(starts[max(0, li - 3)])
+            for u in rng.integers(lo, int(starts[li + 1]), int(rng.integers(9, 301))):
+                edges.add((int(u), t))
+    # every node but the first level's keeps its level: one edge from the level below
+    for li in range(1, len(widths)):
+        for v in range(int(starts[li]), int(starts[li + 1])):
+            edges.add((int(rng.integers(starts[li - 1], starts[li])), v))
+    edges = sorted(edges)
+    wl = from_edges(n, edges, rng.integers(1, 50, n), rng.integers(0, 900, n), 4,
+                    [10 ** 12] * 4, 4, 2)
+    rt = O.topo_levels(wl)
+    assert rt[3] == len(widths)
+    rb = O.blevel(wl, rt[0], rt[1])
+    g, d, gt, gb = run_topo_blevel(wl)
+    assert_topo_blevel(wl, rt, rb, gt, gb)
+
+
 # -------------------------------------------------------------- edge cases
 
 
