@@ -97,23 +97,30 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
   k_node_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order_id, g->w, g->ob, d->bw, d->lat,
                                                      (flags & CEL_COMM_OFF) ? 1 : 0, wp, wcp, st);
   // The t-level (eq. 2) needs no b-level: its relabelling and sweep run on a
-  // side stream, so the two single-workgroup sweeps overlap on two CUs.
+  // side stream, so the two single-workgroup sweeps overlap on two CUs.  Both
+  // preparations are queued before either plan is read back.
   SideFork fk;
+  SweepPlan pt, pb;
+  int64_t *tlp = nullptr;
   if (tlevel && n > 0) {
     int32_t *pptr, *pidx;
-    int64_t *tlp;
     CEL_TRY(sc.get(&pptr, (int64_t)n + 1));
     CEL_TRY(sc.get(&pidx, g->m));
     CEL_TRY(sc.get(&tlp, n));
     CEL_TRY(fk.start(s));
     const hipStream_t t = fk.side();
     CEL_TRY(relabel_csr(n, g->m, order_id, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, t, st));
-    CEL_TRY(level_sweep(false, n, g->m, L, level_ptr, order_id, level, pptr, pidx, wp, wcp, tlp,
-                        sc, t, st, "k_tlevel_sweep"));
+    CEL_TRY(sweep_prepare(pt, false, n, g->m, L, level_ptr, order_id, level, pptr, pidx, wp, wcp,
+                          tlp, sc, t, st));
+  }
+  CEL_TRY(sweep_prepare(pb, true, n, g->m, L, level_ptr, order_id, level, sptr, sidx, wp, wcp, blp,
+                        sc, s, st));
+  if (tlp) {
+    const hipStream_t t = fk.side();
+    CEL_TRY(sweep_run(pt, t, st, "k_tlevel_sweep"));
     k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, t>>>(n, order_id, tlp, tlevel, st, &st->s1);
   }
-  CEL_TRY(level_sweep(true, n, g->m, L, level_ptr, order_id, level, sptr, sidx, wp, wcp, blp, sc,
-                      s, st, "k_blevel_sweep"));
+  CEL_TRY(sweep_run(pb, s, st, "k_blevel_sweep"));
   k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, blp, blevel, st, &st->s0);
   if (prio_order && n > 0) {
     uint64_t *keys;

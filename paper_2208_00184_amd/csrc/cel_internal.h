@@ -392,12 +392,35 @@ __global__ void k_makespan_out(int32_t K, int32_t n, const int32_t *order, const
                                const Status *st);
 __global__ void k_fill_i64(int64_t *p, int64_t n, int64_t v);
 __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v);  // common.hip
-// sweep.hip: one level sweep of eq. 3 (rev: b-level over successors) or eq. 2
-// (t-level over predecessors) in position space; out[p] = the value at p
-int level_sweep(bool rev, int32_t n, int32_t m, int32_t L, const int32_t *lp,
-                const int32_t *order, const int32_t *level, const int32_t *rptr,
-                const int32_t *ridx, const int64_t *wp, const int64_t *wcp, int64_t *out,
-                class Scratch &sc, hipStream_t s, Status *st, const char *timer);
+// sweep.hip: level sweeps of eq. 3 (rev: b-level over successors) or eq. 2
+// (t-level over predecessors) in position space; out[p] = the value at p.
+struct SweepArgs {
+  int32_t n, L;
+  const int32_t *lp;              // [L + 1] level starts (positions)
+  const int32_t *rptr, *ridx;     // neighbours (positions): successors (rev) or predecessors
+  const int64_t *cst;             // [n] w (sink) / w + c
+  const uint4 *rec;               // [n] pull records
+  const int32_t *fptr, *fidx;     // far neighbours
+  const int32_t *hptr, *hidx;     // slot lists of positions with many near neighbours
+  const int32_t *seg;             // [segments + 1] first level of each segment
+  const int32_t *wide;            // [L] levels out of ring mode
+  int64_t *gx;                    // [n] pull values, -1 until written
+  int64_t *out;                   // [n] results (== gx for rev)
+};
+constexpr int kPlanHead = 2, kPlanRec = 3, kPlanFirst = 64;  // plan table layout (ints)
+struct SweepPlan {
+  bool rev = false;
+  SweepArgs a{};
+  const int32_t *gkp = nullptr;   // [n + 1] chunk offsets of split rows in grid levels
+  int32_t *tab = nullptr;         // the plan table on the device
+};
+// sweep_prepare queues the preparation on s; sweep_run reads the plan table
+// back (synchronising s) and queues the sweep's kernels on s.
+int sweep_prepare(SweepPlan &pl, bool rev, int32_t n, int32_t m, int32_t L, const int32_t *lp,
+                  const int32_t *order, const int32_t *level, const int32_t *rptr,
+                  const int32_t *ridx, const int64_t *wp, const int64_t *wcp, int64_t *out,
+                  class Scratch &sc, hipStream_t s, Status *st);
+int sweep_run(SweepPlan &pl, hipStream_t s, Status *st, const char *timer);
 // makespan_model.hip: a heterogeneous descriptor's ranges, its slowest
 // multiplier, smallest bandwidth and largest latency; lead[g] = smallest
 // pos[v] over the members v of group g (INT32_MAX before)

@@ -27,7 +27,11 @@
 // sweep.  Levels wider than kWideW, or holding a node with more than kHeavyDeg
 // neighbours, are run by the whole workgroup straight from global memory
 // (block mode), between barriers; they split the narrow levels into runs
-// (segments) that each start with an empty ring.
+// (segments) that each start with an empty ring.  A level with at least
+// kGridE edges or kGridW nodes (a DNN graph's sources: weights and inputs) is
+// more work than one CU should do: it is a grid level, run by kernels over the
+// whole GPU between launches of the ring kernel.  The host learns where the
+// grid levels are from a small table the preparation writes.
 #include "cel_internal.h"
 
 namespace cel {
@@ -42,6 +46,11 @@ constexpr int kNF = kRing / kStage;     // staging flags in the ring
 constexpr int kNear = 8;                // near neighbours held in a pull record
 constexpr int kBP = 8;                  // positions per thread and pass in block mode
 static_assert(kWideW + kStage < kRing, "a narrow level and a staging task fit the ring");
+constexpr int kGridE = 16384;           // a level of this many edges or nodes is a grid level
+constexpr int kGridW = 16384;
+constexpr int kGridRow = 64;            // grid levels: larger rows are split into chunks
+constexpr int kGridChunk = 4096;        // edges per workgroup of a split row
+constexpr int kGridB = 256;
 constexpr uint32_t kZeroSlot = kRing;   // ring slot that always reads 0
 constexpr int kHeavyNear = 15;          // count field: more near neighbours than kNear
 
@@ -52,20 +61,6 @@ constexpr int kHeavyNear = 15;          // count field: more near neighbours tha
 // array (hidx, from hptr[p]).  Every record thus names in-range slots only.
 __device__ inline uint32_t rec_count(const uint4 &r) { return (r.x >> 12) & 15u; }
 
-struct SweepArgs {
-  int32_t n, L;
-  const int32_t *lp;              // [L + 1] level starts (positions)
-  const int32_t *rptr, *ridx;     // neighbours (positions): successors (REVERSE) or predecessors
-  const int64_t *cst;             // [n] w (sink) / w + c
-  const uint4 *rec;               // [n] pull records
-  const int32_t *fptr, *fidx;     // far neighbours
-  const int32_t *hptr, *hidx;     // slot lists of positions with many near neighbours
-  const int32_t *seg;             // [nseg + 1] first level of each segment
-  const int32_t *nseg;            // device scalar
-  const int32_t *wide;            // [L] block-mode levels
-  int64_t *gx;                    // [n] pull values, -1 until written
-  int64_t *out;                   // [n] results (== gx for REVERSE)
-};
 
 __device__ inline int64_t ld_coherent(const int64_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -107,15 +102,20 @@ __device__ inline void ld_many(int64_t (&x)[N], const int32_t (&q)[N], const int
 
 // -------------------------------------------------------------- preparation
 
-// Levels in block mode: wider than kWideW, or holding a node with more than
-// kHeavyDeg neighbours.
+// Levels out of ring mode (wide[l] = 1): wider than kWideW, holding a node
+// with more than kHeavyDeg neighbours, or grid levels (grid[l] = 1: at least
+// kGridE edges or kGridW nodes).
 __global__ void k_sw_wide(int32_t n, int32_t L, const int32_t *lp, const int32_t *rptr,
                           const int32_t *order, const int32_t *level, int32_t *wide,
-                          const Status *st) {
+                          int32_t *grid, const Status *st) {
   if (failed(st)) return;
   const int64_t i0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x, step = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t l = i0; l < L; l += step)
-    if (lp[l + 1] - lp[l] > kWideW) wide[l] = 1;
+  for (int64_t l = i0; l < L; l += step) {
+    const int32_t w = lp[l + 1] - lp[l], e = rptr[lp[l + 1]] - rptr[lp[l]];
+    const bool g = w >= kGridW || e >= kGridE;
+    grid[l] = g ? 1 : 0;
+    if (g || w > kWideW) wide[l] = 1;
+  }
   for (int64_t p = i0; p < n; p += step)
     if (rptr[p + 1] - rptr[p] > kHeavyDeg) wide[level[order[p]]] = 1;
 }
@@ -146,20 +146,25 @@ __global__ void k_sw_segfill(int32_t L, const int32_t *flag, const int32_t *pre,
 
 // Per position: its pull record, its cost term, and how many far neighbours
 // and (past kNear) near neighbours it has.  PASS 1 fills the far lists and the
-// long slot lists.  Positions of block-mode levels get neither.
+// long slot lists.  Positions of block-mode levels get neither; those of grid
+// levels with more than kGridRow neighbours count their chunks (gk).
 template <bool REV, int PASS>
 __global__ void k_sw_prep(int32_t n, const int32_t *lp, const int32_t *rptr, const int32_t *ridx,
                           const int32_t *order, const int32_t *level, const int32_t *wide,
-                          const int32_t *seg, const int32_t *segid, const int64_t *wp,
-                          const int64_t *wcp, uint4 *rec, int64_t *cst, int32_t *fcnt,
-                          int32_t *hcnt, const int32_t *fptr, int32_t *fidx, const int32_t *hptr,
-                          int32_t *hidx, int32_t *rmax, const Status *st) {
+                          const int32_t *grid, const int32_t *seg, const int32_t *segid,
+                          const int64_t *wp, const int64_t *wcp, uint4 *rec, int64_t *cst,
+                          int32_t *fcnt, int32_t *hcnt, int32_t *gk, const int32_t *fptr,
+                          int32_t *fidx, const int32_t *hptr, int32_t *hidx, int32_t *rmax,
+                          const Status *st) {
   if (failed(st)) return;
   for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
        p += (int64_t)gridDim.x * blockDim.x) {
     const int32_t l = level[order[p]];
     const int32_t e0 = rptr[p], e1 = rptr[p + 1];
-    if (PASS == 0) cst[p] = (REV && e0 == e1) ? wp[p] : wcp[p];
+    if (PASS == 0) {
+      cst[p] = (REV && e0 == e1) ? wp[p] : wcp[p];
+      gk[p] = (grid[l] && e1 - e0 > kGridRow) ? (e1 - e0 + kGridChunk - 1) / kGridChunk : 0;
+    }
     if (wide[l]) {
       if (PASS == 0) {
         rec[p] = make_uint4(kZeroSlot | kZeroSlot << 16, kZeroSlot | kZeroSlot << 16,
@@ -221,6 +226,141 @@ __global__ void k_sw_rowmark(int32_t n, const int32_t *lp, const int32_t *order,
     const int32_t l = level[order[p]];
     if (wide[l] || (((int32_t)p - lp[l]) & 63) != 0) continue;
     rec[p].x = (rec[p].x & 0x0FFFFFFFu) | (uint32_t)rmax[p] << 28;
+  }
+}
+
+// The plan the host reads back: tab[0] = segments, tab[1] = grid levels G,
+// then per grid level (ascending) its segment, width and chunk count.
+__global__ void k_sw_gtab(int32_t L, const int32_t *lp, const int32_t *grid, const int32_t *gpre,
+                          const int32_t *segid, const int32_t *nseg, const int32_t *gkp,
+                          int32_t *tab, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t l = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; l < L;
+       l += (int64_t)gridDim.x * blockDim.x) {
+    if (grid[l]) {
+      int32_t *t = tab + kPlanHead + kPlanRec * gpre[l];
+      t[0] = segid[l];
+      t[1] = lp[l + 1] - lp[l];
+      t[2] = gkp[lp[l + 1]] - gkp[lp[l]];
+    }
+    if (l == L - 1) {
+      tab[0] = *nseg;
+      tab[1] = gpre[l] + grid[l];
+    }
+  }
+}
+
+// ------------------------------------------------------------- grid levels
+//
+// A grid level [S0, S1) of segment g: every neighbour lies in another level
+// and is final (written by an earlier kernel).  k_sw_grid_rows computes the
+// rows of at most kGridRow neighbours and zeroes the others' accumulators;
+// k_sw_grid_split takes the larger rows in chunks of kGridChunk edges, one
+// workgroup each, and folds each chunk's maximum into the accumulator (gx) by
+// an atomic maximum; k_sw_grid_fin turns the accumulators into values.
+
+__device__ inline void grid_level(const SweepArgs &a, int32_t g, int32_t *S0, int32_t *S1) {
+  const int32_t l = a.seg[g];
+  *S0 = a.lp[l];
+  *S1 = a.lp[l + 1];
+}
+
+template <bool REV>
+__global__ void __launch_bounds__(kGridB) k_sw_grid_rows(SweepArgs a, int32_t g, Status *st) {
+  if (failed(st)) return;
+  int32_t S0, S1;
+  grid_level(a, g, &S0, &S1);
+  bool bad = false;
+  for (int64_t p = S0 + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < S1;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t e0 = a.rptr[p], e1 = a.rptr[p + 1];
+    if (e1 - e0 > kGridRow) {
+      a.gx[p] = 0;
+      continue;
+    }
+    int64_t m = 0;
+    for (int32_t e = e0; e < e1; e += 4) {
+      int32_t q[4];
+#pragma unroll
+      for (int j = 0; j < 4; j++) q[j] = e + j < e1 ? a.ridx[e + j] : -1;
+      int64_t x[4];
+#pragma unroll
+      for (int j = 0; j < 4; j++) x[j] = q[j] >= 0 ? a.gx[q[j]] : 0;
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        bad |= x[j] < 0;
+        m = x[j] > m ? x[j] : m;
+      }
+    }
+    const int64_t c = a.cst[p];
+    const int64_t o = REV ? c + m : m;
+    a.gx[p] = REV ? o : o + c;
+    if (!REV) a.out[p] = o;
+  }
+  // a neighbour without its value would be a broken invariant
+  if (bad) raise_err(st, EB_WAIT);
+}
+
+template <bool REV>
+__global__ void __launch_bounds__(kGridB) k_sw_grid_split(SweepArgs a, int32_t g,
+                                                          const int32_t *gkp, Status *st) {
+  __shared__ int32_t s_p;
+  __shared__ int64_t s_red[kGridB / 64];
+  if (failed(st)) return;
+  int32_t S0, S1;
+  grid_level(a, g, &S0, &S1);
+  const int32_t i0 = gkp[S0], i1 = gkp[S1];
+  const int tid = threadIdx.x, lane = tid & 63;
+  constexpr int kPer = kGridChunk / kGridB;
+  for (int32_t i = i0 + blockIdx.x; i < i1; i += gridDim.x) {
+    // the row holding chunk i: last p in [S0, S1) with gkp[p] <= i
+    if (tid < 64) {
+      const int32_t u = wave_row_of(gkp + S0, S1 - S0, i, lane);
+      if (lane == 0) s_p = S0 + u;
+    }
+    __syncthreads();
+    const int32_t p = s_p;
+    const int32_t r1 = a.rptr[p + 1];
+    const int32_t e0 = a.rptr[p] + (i - gkp[p]) * kGridChunk;
+    const int32_t e1 = e0 + kGridChunk < r1 ? e0 + kGridChunk : r1;
+    int32_t q[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; j++) q[j] = e0 + tid + j * kGridB < e1 ? a.ridx[e0 + tid + j * kGridB] : -1;
+    int64_t m = 0;
+    bool bad = false;
+#pragma unroll
+    for (int j = 0; j < kPer; j++) {
+      const int64_t x = q[j] >= 0 ? a.gx[q[j]] : 0;
+      bad |= x < 0;
+      m = x > m ? x : m;
+    }
+    if (bad) raise_err(st, EB_WAIT);
+    for (int off = 32; off > 0; off >>= 1) {
+      const int64_t o = __shfl_xor((long long)m, off);
+      m = o > m ? o : m;
+    }
+    if (lane == 0) s_red[tid >> 6] = m;
+    __syncthreads();
+    if (tid == 0) {
+      for (int w = 1; w < kGridB / 64; w++) m = s_red[w] > m ? s_red[w] : m;
+      atomicMax((unsigned long long *)&a.gx[p], (unsigned long long)m);
+    }
+    __syncthreads();
+  }
+}
+
+template <bool REV>
+__global__ void __launch_bounds__(kGridB) k_sw_grid_fin(SweepArgs a, int32_t g, Status *st) {
+  if (failed(st)) return;
+  int32_t S0, S1;
+  grid_level(a, g, &S0, &S1);
+  for (int64_t p = S0 + blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < S1;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    if (a.rptr[p + 1] - a.rptr[p] <= kGridRow) continue;
+    const int64_t m = a.gx[p], c = a.cst[p];
+    const int64_t o = REV ? c + m : m;
+    a.gx[p] = REV ? o : o + c;
+    if (!REV) a.out[p] = o;
   }
 }
 
@@ -336,8 +476,10 @@ __device__ inline void flush_ring(const SweepArgs &a, int32_t q0, int32_t q1, in
   }
 }
 
+// Segments [k_lo, k_hi) (none a grid level), in sweep order.
 template <bool REV>
-__global__ void __launch_bounds__(kSwB) k_ring_sweep(SweepArgs a, Status *st) {
+__global__ void __launch_bounds__(kSwB) k_ring_sweep(SweepArgs a, int32_t k_lo, int32_t k_hi,
+                                                     Status *st) {
   __shared__ int64_t s_x[kRing + 1];
   __shared__ int64_t s_base[kRing], s_cst[kRing];
   __shared__ uint4 s_rec[kRing];
@@ -365,9 +507,8 @@ __global__ void __launch_bounds__(kSwB) k_ring_sweep(SweepArgs a, Status *st) {
     raise_err(st, EB_WAIT);
     __hip_atomic_store(&s_abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   };
-  const int32_t NS = *a.nseg;
-  for (int32_t kk = 0; kk < NS; kk++) {
-    const int32_t k = REV ? NS - 1 - kk : kk;
+  for (int32_t kk = k_lo; kk < k_hi; kk++) {
+    const int32_t k = REV ? k_hi - 1 - (kk - k_lo) : kk;
     const int32_t l0 = a.seg[k], l1 = a.seg[k + 1];
     const int32_t S0 = a.lp[l0], S1 = a.lp[l1];
     if (tid < kNF) s_flag[tid] = -1;
@@ -651,15 +792,20 @@ __global__ void __launch_bounds__(kSwB) k_ring_sweep(SweepArgs a, Status *st) {
 
 CEL_PHASE_READER(cel_debug_phases_sweep)
 
-int level_sweep(bool rev, int32_t n, int32_t m, int32_t L, const int32_t *lp,
-                const int32_t *order, const int32_t *level, const int32_t *rptr,
-                const int32_t *ridx, const int64_t *wp, const int64_t *wcp, int64_t *out,
-                Scratch &sc, hipStream_t s, Status *st, const char *timer) {
+int sweep_prepare(SweepPlan &pl, bool rev, int32_t n, int32_t m, int32_t L, const int32_t *lp,
+                  const int32_t *order, const int32_t *level, const int32_t *rptr,
+                  const int32_t *ridx, const int64_t *wp, const int64_t *wcp, int64_t *out,
+                  Scratch &sc, hipStream_t s, Status *st) {
+  pl = SweepPlan{};
+  pl.rev = rev;
   if (n == 0) return CEL_OK;
-  int32_t *wide, *flag, *pre, *seg, *segid, *nseg, *fcnt, *fptr, *fidx, *hcnt, *hptr, *hidx, *rmax;
+  int32_t *wide, *grid, *gpre, *flag, *pre, *seg, *segid, *nseg, *fcnt, *fptr, *fidx, *hcnt,
+      *hptr, *hidx, *rmax, *gk, *gkp, *tab;
   int64_t *cst, *gx;
   uint4 *rec;
   CEL_TRY(sc.get(&wide, L));
+  CEL_TRY(sc.get(&grid, L));
+  CEL_TRY(sc.get(&gpre, (int64_t)L + 1));
   CEL_TRY(sc.get(&flag, L));
   CEL_TRY(sc.get(&pre, (int64_t)L + 1));
   CEL_TRY(sc.get(&seg, (int64_t)L + 1));
@@ -669,41 +815,51 @@ int level_sweep(bool rev, int32_t n, int32_t m, int32_t L, const int32_t *lp,
   CEL_TRY(sc.get(&fptr, (int64_t)n + 1));
   CEL_TRY(sc.get(&hcnt, n));
   CEL_TRY(sc.get(&hptr, (int64_t)n + 1));
+  CEL_TRY(sc.get(&gk, n));
+  CEL_TRY(sc.get(&gkp, (int64_t)n + 1));
   CEL_TRY(sc.get(&fidx, m));
   CEL_TRY(sc.get(&hidx, m));
   CEL_TRY(sc.get(&cst, n));
   CEL_TRY(sc.get(&rec, n));
   CEL_TRY(sc.get(&rmax, n));
+  CEL_TRY(sc.get(&tab, kPlanHead + (int64_t)kPlanRec * L));
   gx = out;
   if (!rev) CEL_TRY(sc.get(&gx, n));
   k_fill_i32<<<grid_for(L, 256, 1024), 256, 0, s>>>(wide, L, 0);
+  k_fill_i32<<<1, 64, 0, s>>>(tab, kPlanHead, 0);
   k_fill_i64<<<grid_for(n, 256, 4096), 256, 0, s>>>(gx, n, -1);
   k_fill_i32<<<grid_for(n, 256, 4096), 256, 0, s>>>(rmax, n, 0);
   const int gn = grid_for(n, 256, 4096), gl = grid_for(L, 256, 1024);
-  k_sw_wide<<<gn, 256, 0, s>>>(n, L, lp, rptr, order, level, wide, st);
+  k_sw_wide<<<gn, 256, 0, s>>>(n, L, lp, rptr, order, level, wide, grid, st);
   k_sw_segflag<<<gl, 256, 0, s>>>(L, wide, flag, st);
   CEL_TRY(exclusive_scan_i32(flag, pre, L, sc, s));
+  CEL_TRY(exclusive_scan_i32(grid, gpre, L, sc, s));
   k_sw_segfill<<<gl, 256, 0, s>>>(L, flag, pre, seg, segid, nseg, st);
   if (rev) {
-    k_sw_prep<true, 0><<<gn, 256, 0, s>>>(n, lp, rptr, ridx, order, level, wide, seg, segid, wp,
-                                          wcp, rec, cst, fcnt, hcnt, nullptr, nullptr, nullptr,
-                                          nullptr, rmax, st);
+    k_sw_prep<true, 0><<<gn, 256, 0, s>>>(n, lp, rptr, ridx, order, level, wide, grid, seg, segid,
+                                          wp, wcp, rec, cst, fcnt, hcnt, gk, nullptr, nullptr,
+                                          nullptr, nullptr, rmax, st);
   } else {
-    k_sw_prep<false, 0><<<gn, 256, 0, s>>>(n, lp, rptr, ridx, order, level, wide, seg, segid, wp,
-                                           wcp, rec, cst, fcnt, hcnt, nullptr, nullptr, nullptr,
-                                           nullptr, rmax, st);
+    k_sw_prep<false, 0><<<gn, 256, 0, s>>>(n, lp, rptr, ridx, order, level, wide, grid, seg, segid,
+                                           wp, wcp, rec, cst, fcnt, hcnt, gk, nullptr, nullptr,
+                                           nullptr, nullptr, rmax, st);
   }
   CEL_TRY(exclusive_scan_i32(fcnt, fptr, n, sc, s));
   CEL_TRY(exclusive_scan_i32(hcnt, hptr, n, sc, s));
+  CEL_TRY(exclusive_scan_i32(gk, gkp, n, sc, s));
   if (rev) {
-    k_sw_prep<true, 1><<<gn, 256, 0, s>>>(n, lp, rptr, ridx, order, level, wide, seg, segid, wp,
-                                          wcp, rec, cst, fcnt, hcnt, fptr, fidx, hptr, hidx, rmax, st);
+    k_sw_prep<true, 1><<<gn, 256, 0, s>>>(n, lp, rptr, ridx, order, level, wide, grid, seg, segid,
+                                          wp, wcp, rec, cst, fcnt, hcnt, gk, fptr, fidx, hptr, hidx,
+                                          rmax, st);
   } else {
-    k_sw_prep<false, 1><<<gn, 256, 0, s>>>(n, lp, rptr, ridx, order, level, wide, seg, segid, wp,
-                                           wcp, rec, cst, fcnt, hcnt, fptr, fidx, hptr, hidx, rmax, st);
+    k_sw_prep<false, 1><<<gn, 256, 0, s>>>(n, lp, rptr, ridx, order, level, wide, grid, seg, segid,
+                                           wp, wcp, rec, cst, fcnt, hcnt, gk, fptr, fidx, hptr, hidx,
+                                           rmax, st);
   }
   k_sw_rowmark<<<gn, 256, 0, s>>>(n, lp, order, level, wide, rmax, rec, st);
-  SweepArgs a{};
+  k_sw_gtab<<<gl, 256, 0, s>>>(L, lp, grid, gpre, segid, nseg, gkp, tab, st);
+  CEL_HIP(hipGetLastError());
+  SweepArgs &a = pl.a;
   a.n = n;
   a.L = L;
   a.lp = lp;
@@ -716,14 +872,82 @@ int level_sweep(bool rev, int32_t n, int32_t m, int32_t L, const int32_t *lp,
   a.hptr = hptr;
   a.hidx = hidx;
   a.seg = seg;
-  a.nseg = nseg;
   a.wide = wide;
   a.gx = gx;
   a.out = out;
-  {
-    KTimer kt(s, timer);
-    if (rev) k_ring_sweep<true><<<1, kSwB, 0, s>>>(a, st);
-    else k_ring_sweep<false><<<1, kSwB, 0, s>>>(a, st);
+  pl.gkp = gkp;
+  pl.tab = tab;
+  return CEL_OK;
+}
+
+int sweep_run(SweepPlan &pl, hipStream_t s, Status *st, const char *timer) {
+  const SweepArgs &a = pl.a;
+  if (a.n == 0) return CEL_OK;
+  // the plan: segments, grid levels and, per grid level, segment, width, chunks
+  std::vector<int32_t> tab(kPlanFirst);
+  CEL_HIP(hipMemcpyAsync(tab.data(), pl.tab, sizeof(int32_t) * kPlanFirst, hipMemcpyDeviceToHost, s));
+  CEL_HIP(hipStreamSynchronize(s));
+  const int32_t NS = tab[0], G = tab[1];
+  // a failed preparation (the status block holds its error) leaves NS = 0
+  if (NS <= 0 || NS > a.L || G < 0 || G > NS) return CEL_OK;
+  const int64_t len = kPlanHead + (int64_t)kPlanRec * G;
+  if (len > kPlanFirst) {
+    tab.resize(len);
+    CEL_HIP(hipMemcpyAsync(tab.data() + kPlanFirst, pl.tab + kPlanFirst,
+                           sizeof(int32_t) * (len - kPlanFirst), hipMemcpyDeviceToHost, s));
+    CEL_HIP(hipStreamSynchronize(s));
+  }
+  auto ring = [&](int32_t lo, int32_t hi) {
+    if (lo >= hi) return;
+    if (pl.rev) k_ring_sweep<true><<<1, kSwB, 0, s>>>(a, lo, hi, st);
+    else k_ring_sweep<false><<<1, kSwB, 0, s>>>(a, lo, hi, st);
+  };
+  auto gridlev = [&](int32_t j) {
+    const int32_t *t = &tab[kPlanHead + kPlanRec * j];
+    const int32_t g = t[0], w = t[1], chunks = t[2];
+    const int gw = grid_for(w, kGridB, 8192);
+    if (pl.rev) k_sw_grid_rows<true><<<gw, kGridB, 0, s>>>(a, g, st);
+    else k_sw_grid_rows<false><<<gw, kGridB, 0, s>>>(a, g, st);
+    if (chunks > 0) {
+      const int gc = chunks < 8192 ? chunks : 8192;
+      if (pl.rev) k_sw_grid_split<true><<<gc, kGridB, 0, s>>>(a, g, pl.gkp, st);
+      else k_sw_grid_split<false><<<gc, kGridB, 0, s>>>(a, g, pl.gkp, st);
+      if (pl.rev) k_sw_grid_fin<true><<<gw, kGridB, 0, s>>>(a, g, st);
+      else k_sw_grid_fin<false><<<gw, kGridB, 0, s>>>(a, g, st);
+    }
+  };
+  for (int32_t j = 0; j < G; j++) {
+    const int32_t g = tab[kPlanHead + kPlanRec * j];
+    const int32_t prev = j > 0 ? tab[kPlanHead + kPlanRec * (j - 1)] : -1;
+    if (g <= prev || g >= NS) {
+      // only an error raised while the plan was written (on this stream or
+      // the other sweep's) leaves it inconsistent: the status reports it
+      Status h;
+      CEL_TRY(read_status(st, &h, s));
+      if (h.err) return CEL_OK;
+      return set_error(CEL_E_HIP, "level sweep: inconsistent plan of grid levels");
+    }
+  }
+  KTimer kt(s, timer);
+  if (pl.rev) {
+    // segments from the top: the part above each grid level, then the level
+    int32_t hi = NS;
+    for (int32_t j = G - 1; j >= 0; j--) {
+      const int32_t g = tab[kPlanHead + kPlanRec * j];
+      ring(g + 1, hi);
+      gridlev(j);
+      hi = g;
+    }
+    ring(0, hi);
+  } else {
+    int32_t lo = 0;
+    for (int32_t j = 0; j < G; j++) {
+      const int32_t g = tab[kPlanHead + kPlanRec * j];
+      ring(lo, g);
+      gridlev(j);
+      lo = g + 1;
+    }
+    ring(lo, NS);
   }
   CEL_HIP(hipGetLastError());
   return CEL_OK;

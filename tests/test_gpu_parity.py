@@ -405,6 +405,63 @@ def test_sweep_many_near_neighbours():
     assert_topo_blevel(wl, rt, rb, gt, gb)
 
 
+def _grid_level_dag(seed):
+    """Levels of widths 20000 (sources), 50, 30, 40, 10 (hubs), 60, 12000, 80,
+    2000, 5 (collectors), 70, 30, 20000: one source has 24,375 successors (every
+    node of the levels between and half the sinks), each hub 3,000..9,000
+    successors in the next four levels, each collector 5,000 predecessors
+    below it."""
+    rng = np.random.default_rng(seed)
+    widths = [20000, 50, 30, 40, 10, 60, 12000, 80, 2000, 5, 70, 30, 20000]
+    starts = np.concatenate([[0], np.cumsum(widths)]).astype(np.int64)
+    n = int(starts[-1])
+    nl = len(widths)
+    src, dst = [], []
+
+    def add(u, v):
+        src.append(np.asarray(u, np.int64).ravel())
+        dst.append(np.asarray(v, np.int64).ravel())
+
+    for li in range(1, nl):
+        v = np.arange(starts[li], starts[li + 1])
+        add(rng.integers(starts[li - 1], starts[li], v.size), v)
+    for li in range(nl - 1):
+        u = np.arange(starts[li], starts[li + 1])
+        k = rng.integers(1, 4, u.size)
+        uu = np.repeat(u, k)
+        add(uu, rng.integers(starts[li + 1], starts[min(li + 4, nl)], uu.size))
+    add(np.zeros(n - widths[0] - widths[-1] + widths[-1] // 2, np.int64),
+        np.concatenate([np.arange(starts[1], starts[nl - 1]),
+                        np.arange(starts[nl - 1], starts[nl - 1] + widths[-1] // 2)]))
+    for h in range(starts[4], starts[5]):
+        t = rng.choice(np.arange(starts[5], starts[9]), int(rng.integers(3000, 9001)), replace=False)
+        add(np.full(t.size, h), t)
+    for c in range(starts[9], starts[10]):
+        u = rng.choice(np.arange(0, starts[9]), 5000, replace=False)
+        add(u, np.full(u.size, c))
+    e = np.unique(np.stack([np.concatenate(src), np.concatenate(dst)], 1), axis=0)
+    edges = [(int(a), int(b)) for a, b in e]
+    wl = from_edges(n, edges, rng.integers(1, 50, n), rng.integers(0, 900, n), 4,
+                    [10 ** 12] * 4, 4, 2)
+    return wl, nl
+
+
+def test_sweep_grid_levels():
+    """Levels of at least 16,384 nodes or edges run on the whole GPU between
+    single-workgroup segments, in both sweep directions; rows of more than 64
+    neighbours there are split over workgroups (the 24,375-successor source in
+    6 chunks of 4,096 edges)."""
+    wl, nl = _grid_level_dag(31)
+    rt = O.topo_levels(wl)
+    assert rt[3] == nl
+    rb = O.blevel(wl, rt[0], rt[1])
+    g, d, gt, gb = run_topo_blevel(wl)
+    assert_topo_blevel(wl, rt, rb, gt, gb)
+    # again without the t-level (the b-level alone on the caller's stream)
+    bl, tl, pr, cp = cel.blevel(g, d, gt[0], gt[2], gt[1], gt[3], want_tlevel=False)
+    assert tl is None and cp == rb[3] and np.array_equal(np_(bl), rb[0])
+
+
 # -------------------------------------------------------------- edge cases
 
 
