@@ -392,6 +392,71 @@ __global__ void k_makespan_out(int32_t K, int32_t n, const int32_t *order, const
                                const Status *st);
 __global__ void k_fill_i64(int64_t *p, int64_t n, int64_t v);
 __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v);  // common.hip
+// Segmented prefix maximum over a wave (makespan.hip, ms_ring.hip).
+// One step of the segmented prefix max: take the value of the lane selected
+// by CTRL when `ok` (that lane lies in the same run); lanes the DPP move does
+// not reach read the identity.
+template <int CTRL, int ROWMASK>
+__device__ inline void pmax_step(int64_t &y, bool ok) {
+  const int32_t lo = __builtin_amdgcn_update_dpp((int32_t)kNeg, (int32_t)y, CTRL, ROWMASK, 0xF, false);
+  const int32_t hi =
+      __builtin_amdgcn_update_dpp((int32_t)(kNeg >> 32), (int32_t)(y >> 32), CTRL, ROWMASK, 0xF, false);
+  const int64_t u = (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+  y = (ok && u > y) ? u : y;
+}
+
+// Inclusive prefix max over the run of every lane inside the wave's 64 lanes;
+// hd = distance from the lane's slot to its run's first slot.
+__device__ inline int64_t wave_seg_pmax(int64_t y, int32_t hd, int lane) {
+  pmax_step<0x111, 0xF>(y, hd >= 1);               // row_shr:1
+  pmax_step<0x112, 0xF>(y, hd >= 2);               // row_shr:2
+  pmax_step<0x114, 0xF>(y, hd >= 4);               // row_shr:4
+  pmax_step<0x118, 0xF>(y, hd >= 8);               // row_shr:8
+  pmax_step<0x142, 0xA>(y, hd >= (lane & 15) + 1);  // row_bcast:15 into rows 1 and 3
+  pmax_step<0x143, 0xC>(y, hd >= lane - 31);        // row_bcast:31 into rows 2 and 3
+  return y;
+}
+
+// Device-coherent access to values that waves of other workgroups, or of
+// this one, write during the same kernel (sweep.hip, ms_ring.hip).
+__device__ inline int64_t ld_coherent(const int64_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void st_coherent(int64_t *p, int64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+constexpr int32_t kSpin = 1 << 21;  // polls before a wait gives up (far longer than any real wait)
+
+// A pull value written earlier by this kernel, read again until it is
+// visible.  A wait that outlasts kSpin polls raises EB_WAIT and sets the
+// workgroup's abort flag (a broken invariant, never a slow run); the value
+// returned then is 0 and the results are discarded by the error.
+__device__ inline int64_t ld_final(const int64_t *p, int32_t *s_abort, Status *st) {
+  int64_t v = ld_coherent(p);
+  for (int32_t i = 0; v < 0; i++) {
+    if (i == kSpin || __hip_atomic_load(s_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) {
+      raise_err(st, EB_WAIT);
+      __hip_atomic_store(s_abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      return 0;
+    }
+    __builtin_amdgcn_s_sleep(1);
+    v = ld_coherent(p);
+  }
+  return v;
+}
+
+// Values of the positions q[j] (q < 0: 0), every load issued before the first
+// use; one not yet visible is read again by ld_final (rare).
+template <int N>
+__device__ inline void ld_many(int64_t (&x)[N], const int32_t (&q)[N], const int64_t *gx,
+                               int32_t *s_abort, Status *st) {
+#pragma unroll
+  for (int j = 0; j < N; j++) x[j] = q[j] >= 0 ? ld_coherent(&gx[q[j]]) : 0;
+#pragma unroll
+  for (int j = 0; j < N; j++)
+    if (x[j] < 0) x[j] = ld_final(&gx[q[j]], s_abort, st);
+}
+
 // sweep.hip: level sweeps of eq. 3 (rev: b-level over successors) or eq. 2
 // (t-level over predecessors) in position space; out[p] = the value at p.
 struct SweepArgs {
@@ -421,6 +486,17 @@ int sweep_prepare(SweepPlan &pl, bool rev, int32_t n, int32_t m, int32_t L, cons
                   const int32_t *ridx, const int64_t *wp, const int64_t *wcp, int64_t *out,
                   class Scratch &sc, hipStream_t s, Status *st);
 int sweep_run(SweepPlan &pl, hipStream_t s, Status *st, const char *timer);
+// segment starts of the level sweeps (sweep.hip), also used by ms_ring.hip
+__global__ void k_sw_segflag(int32_t L, const int32_t *wide, int32_t *flag, const Status *st);
+__global__ void k_sw_segfill(int32_t L, const int32_t *flag, const int32_t *pre, int32_t *seg,
+                             int32_t *segid, int32_t *nseg, const Status *st);
+// ms_ring.hip: finish times of one placement over the device-grouped order
+// (slots), levels run by one wave from an LDS ring; finp holds 2n int64 (the
+// finish times, then finish + c), makespan one
+int ms_ring(int32_t n, int32_t m, int32_t L, const int32_t *lp, const int32_t *gorder,
+            const int32_t *level, const int32_t *pptr, const int32_t *pidx, const int64_t *wp,
+            const int64_t *cq, const uint8_t *devp, const int64_t *sxp, const int32_t *metap,
+            int64_t *finp, int64_t *makespan, class Scratch &sc, hipStream_t s, Status *st);
 // makespan_model.hip: a heterogeneous descriptor's ranges, its slowest
 // multiplier, smallest bandwidth and largest latency; lead[g] = smallest
 // pos[v] over the members v of group g (INT32_MAX before)

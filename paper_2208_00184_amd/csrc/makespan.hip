@@ -511,131 +511,10 @@ __global__ void __launch_bounds__(B)
 }
 
 // ---------------------------------------------------------------------------
-// Single placement (K = 1) over the device-grouped order.
-//
-// Inside every level the nodes are sorted by device, priority order kept
-// within a device, so each device's FIFO chain in a level is one run of
-// consecutive slots.  With S(i) the sum of w over the run up to and including
-// slot i and Sx(i) = S(i) - w(i), the chain x -> max(ready + w, x + w)
-// unrolls to
-//   fin(i) = S(i) + max(free(d) - Sx(h), max over h <= j <= i of (ready(j) - Sx(j)))
-// where h is the run's first slot in the window and free(d) the device's
-// free time before it: a segmented prefix maximum.  k_runs precomputes Sx,
-// the distance from each slot to its run's first slot and the run ends, so
-// the sweep needs neither a partition nor a scan of maps.
-//
-// Windows of up to NC consecutive slots (EC in-edges, kMsL levels) are staged
-// into LDS.  Predecessors before the window are final and are folded into a
-// partial ready time per slot.  Predecessors inside the window are counted
-// per slot with an LDS atomic: the first kPull form the slot's pull list
-// (predecessor slot, bit 12 = devices differ), so ready() is a few
-// independent LDS gathers and a max, unrolled to the largest pull count of
-// the row; the rest (rare) are applied per level beforehand by an
-// edge-parallel atomic max.  A level part of at most kNarrow slots is run
-// by wave 0 in rows of 64 without workgroup barriers, the prefix maximum of a
-// run that crosses rows carried in from lane 63; wider parts use the block.
-constexpr int kPull = 8;
-constexpr int kNarrow = 256;
-
-// One step of the segmented prefix max: take the value of the lane selected
-// by CTRL when `ok` (that lane lies in the same run); lanes the DPP move does
-// not reach read the identity.
-template <int CTRL, int ROWMASK>
-__device__ inline void pmax_step(int64_t &y, bool ok) {
-  const int32_t lo = __builtin_amdgcn_update_dpp((int32_t)kNeg, (int32_t)y, CTRL, ROWMASK, 0xF, false);
-  const int32_t hi =
-      __builtin_amdgcn_update_dpp((int32_t)(kNeg >> 32), (int32_t)(y >> 32), CTRL, ROWMASK, 0xF, false);
-  const int64_t u = (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
-  y = (ok && u > y) ? u : y;
-}
-
-// Inclusive prefix max over the run of every lane inside the wave's 64 lanes;
-// hd = distance from the lane's slot to its run's first slot.
-__device__ inline int64_t wave_seg_pmax(int64_t y, int32_t hd, int lane) {
-  pmax_step<0x111, 0xF>(y, hd >= 1);               // row_shr:1
-  pmax_step<0x112, 0xF>(y, hd >= 2);               // row_shr:2
-  pmax_step<0x114, 0xF>(y, hd >= 4);               // row_shr:4
-  pmax_step<0x118, 0xF>(y, hd >= 8);               // row_shr:8
-  pmax_step<0x142, 0xA>(y, hd >= (lane & 15) + 1);  // row_bcast:15 into rows 1 and 3
-  pmax_step<0x143, 0xC>(y, hd >= lane - 31);        // row_bcast:31 into rows 2 and 3
-  return y;
-}
-
-// max of r and the first K pull gathers (finish + comm if the devices differ);
-// pw holds 8 16-bit words, two per register
-template <int K>
-__device__ inline int64_t ms_pull(int64_t r, const uint32_t (&pw)[4], const int64_t *s_f,
-                                  const int64_t *s_c) {
-  int64_t f[K], c[K];
-#pragma unroll
-  for (int k = 0; k < K; k++) {
-    const int32_t j = (pw[k >> 1] >> (16 * (k & 1))) & 0xFFF;
-    f[k] = s_f[j];
-    c[k] = s_c[j];
-  }
-  // every gather is issued before the first use (the compiler would
-  // otherwise chain the cases of the caller's switch into serial round trips)
-  asm volatile("" ::: "memory");
-#pragma unroll
-  for (int k = 0; k < K; k++) {
-    const bool cross = (pw[k >> 1] >> (16 * (k & 1) + 12)) & 1;
-    const int64_t x = f[k] + (cross ? c[k] : 0);
-    r = x > r ? x : r;
-  }
-  return r;
-}
-
-// Rows form of ms_pull: pulls K0 .. K0 + K - 1 of NR rows (row u's packed
-// list in cur[u].pw), all gathers issued before the first use.
-template <int NR, int K, int K0, class RP>
-__device__ inline void ms_pull_rows(int64_t (&r)[NR], const RP (&cur)[NR], const int64_t *s_f,
-                                    const int64_t *s_c) {
-  int64_t f[NR][K], c[NR][K];
-#pragma unroll
-  for (int u = 0; u < NR; u++)
-#pragma unroll
-    for (int k = 0; k < K; k++) {
-      const int kk = K0 + k;
-      const int32_t j = (cur[u].pw[kk >> 1] >> (16 * (kk & 1))) & 0xFFF;
-      f[u][k] = s_f[j];
-      c[u][k] = s_c[j];
-    }
-  asm volatile("" ::: "memory");
-#pragma unroll
-  for (int u = 0; u < NR; u++)
-#pragma unroll
-    for (int k = 0; k < K; k++) {
-      const int kk = K0 + k;
-      const bool cross = (cur[u].pw[kk >> 1] >> (16 * (kk & 1) + 12)) & 1;
-      const int64_t x = f[u][k] + (cross ? c[u][k] : 0);
-      r[u] = x > r[u] ? x : r[u];
-    }
-}
-
-// Pulls K0 .. kmax - 1 of NR rows in batches small enough for the registers.
-template <int NR, int K0, class RP>
-__device__ inline void ms_pull_from(int kmax, int64_t (&r)[NR], const RP (&cur)[NR],
-                                    const int64_t *s_f, const int64_t *s_c) {
-  constexpr int KB = NR == 1 ? 8 : 4;
-  if constexpr (K0 < 8) {
-    const int left = kmax - K0;
-    if (left <= 0) return;
-    if (left >= KB) {
-      ms_pull_rows<NR, KB, K0>(r, cur, s_f, s_c);
-      ms_pull_from<NR, K0 + KB>(kmax, r, cur, s_f, s_c);
-      return;
-    }
-    switch (left) {
-      case 1: ms_pull_rows<NR, 1, K0>(r, cur, s_f, s_c); break;
-      case 2: if constexpr (KB > 2) ms_pull_rows<NR, 2, K0>(r, cur, s_f, s_c); break;
-      case 3: if constexpr (KB > 3) ms_pull_rows<NR, 3, K0>(r, cur, s_f, s_c); break;
-      case 4: if constexpr (KB > 4) ms_pull_rows<NR, 4, K0>(r, cur, s_f, s_c); break;
-      case 5: if constexpr (KB > 5) ms_pull_rows<NR, 5, K0>(r, cur, s_f, s_c); break;
-      case 6: if constexpr (KB > 6) ms_pull_rows<NR, 6, K0>(r, cur, s_f, s_c); break;
-      default: if constexpr (KB > 7) ms_pull_rows<NR, 7, K0>(r, cur, s_f, s_c); break;
-    }
-  }
-}
+// Single placement (K = 1) over the device-grouped order: inside every level
+// the nodes are sorted by device, priority order kept within a device, so each
+// device's FIFO chain in a level is one run of consecutive slots.  k_runs
+// precomputes the run data; the sweep itself is ms_ring (ms_ring.hip).
 
 // Run structure of the device-grouped order, per slot s: sx = exclusive sum
 // of w over the slot's run, meta = device | run ends here << 8 |
@@ -658,445 +537,6 @@ __global__ void k_runs(int32_t n, const int32_t *lp, const int32_t *level, const
     const int32_t hd = s - a < 32767 ? s - a : 32767;
     const int tl = (s + 1 == hi) || gdev[s + 1] != d;
     meta[s] = d | (tl << 8) | (hd << 16);
-  }
-}
-
-template <int B, int NC, int EC>
-__global__ void __launch_bounds__(B)
-    k_makespan_one(int32_t n, int32_t L, const int32_t *lp, const int32_t *pptr,
-                   const int32_t *pidx, const int64_t *wp, const int64_t *cq, const uint8_t *devp,
-                   const int64_t *sxp, const int32_t *metap, int64_t *finp, int64_t *makespan,
-                   const Status *st) {
-  constexpr int NW = B / 64;
-  constexpr int F = kPull;
-  static_assert(NC < 4095 && EC < 32768, "slot fields are 12 bits");
-  constexpr int32_t kNoop = (NC << 16) | NC;  // overflow word that changes nothing
-  constexpr uint32_t kPw2 = ((uint32_t)NC << 16) | NC;  // two dummy pull words
-  static_assert(kPull == 8, "a pull list is one 16-byte LDS word");
-  __shared__ int32_t s_lv[kMsL + 2];
-  __shared__ int32_t s_rp[NC + 1];
-  __shared__ int16_t s_own[EC];  // owner slot of each edge (-1: past kOwnFill of its row)
-  __shared__ int32_t s_epk[EC + 1];
-  __shared__ int64_t s_pm[NC + 1], s_f[NC + 1], s_w[NC + 1], s_c[NC + 1], s_sx[NC + 1];
-  __shared__ int32_t s_meta[NC + 1];
-  __shared__ uint4 s_pw[NC + 1];  // pull lists: F = 8 words of 16 bits per slot
-  __shared__ int32_t s_pc[NC + 1];
-  // per level of the window: first slot | end slot << 12 | window ends in
-  // it << 24 | has overflow words << 25, and its in-edge range ea | eb << 15
-  __shared__ int32_t s_ld[kMsL], s_le[kMsL];
-  static_assert(EC < 32768, "edge range fields are 15 bits");
-  __shared__ int64_t s_avail[256];
-  __shared__ int64_t s_wy[2][NW], s_cy[2];
-  __shared__ int64_t s_red[NW];
-  __shared__ int32_t s_cut;
-  if (failed(st)) return;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const bool wave0 = tid < 64;
-  for (int i = tid; i < 256; i += B) s_avail[i] = 0;
-  if (tid == 0) {
-    s_epk[EC] = kNoop;
-    s_pm[NC] = 0;
-    s_f[NC] = 0;
-    s_w[NC] = 0;
-    s_c[NC] = 0;
-    s_sx[NC] = 0;
-    s_meta[NC] = 0;
-    s_pc[NC] = 0;
-    s_pw[NC] = make_uint4(kPw2, kPw2, kPw2, kPw2);
-  }
-  // a row's structure: costs, run data, in-window predecessor count, pull list
-  struct RowPre {
-    int64_t w, sx;
-    int32_t meta, pc;
-    uint32_t pw[4];
-  };
-  auto row_pre = [&](int32_t si) {
-    RowPre p;
-    p.w = s_w[si];
-    p.sx = s_sx[si];
-    p.meta = s_meta[si];
-    p.pc = s_pc[si];
-    const uint4 q = s_pw[si];
-    p.pw[0] = q.x;
-    p.pw[1] = q.y;
-    p.pw[2] = q.z;
-    p.pw[3] = q.w;
-    return p;
-  };
-  // the largest pull count of the wave's lanes (wave-uniform)
-  auto row_kmax = [&](int32_t pc) {
-    const int32_t c = pc < F ? pc : F;
-    int kmax = 0;
-    while (kmax < F && __ballot(c > kmax)) kmax++;
-    return kmax;
-  };
-  // ready() of a slot: partial from before the window, then the pull
-  // gathers; returns the value ready - Sx of the prefix max (the device's
-  // free time folded in at a run's first slot)
-  auto row_value = [&](int32_t si, const RowPre &p, int kmax) {
-    const int64_t pm = s_pm[si];
-    const int64_t av = s_avail[p.meta & 255];
-    int64_t r;
-    switch (kmax) {
-      case 0: r = pm; break;
-      case 1: r = ms_pull<1>(pm, p.pw, s_f, s_c); break;
-      case 2: r = ms_pull<2>(pm, p.pw, s_f, s_c); break;
-      case 3: r = ms_pull<3>(pm, p.pw, s_f, s_c); break;
-      case 4: r = ms_pull<4>(pm, p.pw, s_f, s_c); break;
-      case 5: r = ms_pull<5>(pm, p.pw, s_f, s_c); break;
-      case 6: r = ms_pull<6>(pm, p.pw, s_f, s_c); break;
-      case 7: r = ms_pull<7>(pm, p.pw, s_f, s_c); break;
-      default: r = ms_pull<8>(pm, p.pw, s_f, s_c); break;
-    }
-    int64_t y = r - p.sx;
-    const int64_t viafree = av - p.sx;
-    if ((p.meta >> 16) == 0 && viafree > y) y = viafree;
-    return y;
-  };
-  int64_t mk = 0;
-  int32_t P0 = 0, lcur = 0;
-  int32_t E0 = 0;                       // edge offset of P0, pptr[P0]
-  int32_t prev_lo = 0;                  // the previous window [prev_lo, P0), still in LDS
-  const int32_t m = pptr[n];
-  constexpr int NU = (NC + B - 1) / B;  // candidate positions per thread
-  constexpr int EU = (EC + B - 1) / B;  // candidate edges per thread
-  // NR (1 or 2) rows of a narrow level starting at slot r0 (slots from b0
-  // idle), run by wave 0; carry: the run value at the end of the previous row
-  auto narrow_rows = [&](auto nrc, int32_t r0, int32_t b0, int64_t &carry) {
-    constexpr int NR = decltype(nrc)::value;
-    RowPre cur[NR];
-    int32_t si[NR];
-    int32_t cmax = 0;
-#pragma unroll
-    for (int u = 0; u < NR; u++) {
-      const int32_t s = r0 + lane + 64 * u;
-      si[u] = s < b0 ? s : NC;
-      cur[u] = row_pre(si[u]);
-      cmax = cur[u].pc > cmax ? cur[u].pc : cmax;
-    }
-    const int kmax = row_kmax(cmax);
-    int64_t r[NR], av[NR];
-#pragma unroll
-    for (int u = 0; u < NR; u++) {
-      r[u] = s_pm[si[u]];
-      av[u] = s_avail[cur[u].meta & 255];  // free times as of the level's start
-    }
-    ms_pull_from<NR, 0>(kmax, r, cur, s_f, s_c);
-    int64_t y[NR];
-#pragma unroll
-    for (int u = 0; u < NR; u++) {
-      y[u] = r[u] - cur[u].sx;
-      const int64_t viafree = av[u] - cur[u].sx;
-      if ((cur[u].meta >> 16) == 0 && viafree > y[u]) y[u] = viafree;
-      y[u] = wave_seg_pmax(y[u], cur[u].meta >> 16, lane);
-    }
-#pragma unroll
-    for (int u = 0; u < NR; u++) {  // a run that began in an earlier row
-      if ((cur[u].meta >> 16) > lane && carry > y[u]) y[u] = carry;
-      if (u + 1 < NR || r0 + 64 * NR < b0) carry = readlane64(y[u], 63);
-    }
-#pragma unroll
-    for (int u = 0; u < NR; u++) {
-      const int32_t s = r0 + lane + 64 * u;
-      if (s < b0) {
-        const int64_t fin = cur[u].sx + cur[u].w + y[u];
-        s_f[s] = fin;
-        finp[P0 + s] = fin;
-        mk = fin > mk ? fin : mk;
-        if (cur[u].meta & 256) s_avail[cur[u].meta & 255] = fin;
-      }
-    }
-  };
-  while (P0 < n) {
-    CEL_TSTAMP(t0);
-    CEL_TCOUNT(6);
-    const int32_t Pc1 = P0 + NC < n ? P0 + NC : n;
-    // P0 and its edge offset are fixed, so every global load the staging
-    // needs that does not depend on the cut is issued before the first wait:
-    // the candidate positions [P0, Pc1) and the candidate edges
-    // [E0, E0 + EC), which hold the edges of any window that is not a single
-    // heavy node
-    const int32_t efar = pptr[Pc1];  // uniform
-    constexpr int NRW = (NC + 1 + B - 1) / B;
-    int32_t rpv[NRW];
-#pragma unroll
-    for (int k = 0; k < NRW; k++) {
-      const int32_t t = tid + k * B;
-      rpv[k] = t <= Pc1 - P0 ? pptr[P0 + t] : 0;
-    }
-    const int32_t Elim = E0 + EC < m ? E0 + EC : m;
-    int32_t qq[EU];
-#pragma unroll
-    for (int u = 0; u < EU; u++) {
-      const int32_t e = E0 + tid + u * B;
-      qq[u] = (u * B + tid < EC && e < Elim) ? pidx[e] : P0;  // P0: in-window, nothing gathered
-    }
-    int32_t cmt[NU];
-    int64_t cwv[NU], ccv[NU], csx[NU];
-#pragma unroll
-    for (int k = 0; k < NU; k++) {
-      const int32_t p = P0 + tid + k * B;
-      const bool ok = k * B + tid < NC && p < Pc1;
-      cmt[k] = ok ? metap[p] : 0;
-      cwv[k] = ok ? wp[p] : 0;
-      ccv[k] = ok ? cq[p] : 0;
-      csx[k] = ok ? sxp[p] : 0;
-    }
-    static_assert(kMsL + 2 <= B, "one level bound per thread");
-    int32_t lvv = 0;
-    if (tid <= kMsL + 1) {
-      const int32_t l = lcur + tid;  // level lcur + k is [s_lv[k], s_lv[k+1])
-      lvv = lp[l > L ? L : l];
-    }
-    for (int t = tid; t < EC; t += B) s_own[t] = -1;
-    if (tid == 0) s_cut = 0;
-#pragma unroll
-    for (int k = 0; k < NRW; k++) {
-      const int32_t t = tid + k * B;
-      if (t <= Pc1 - P0) s_rp[t] = rpv[k];
-    }
-    if (tid <= kMsL + 1) s_lv[tid] = lvv;
-    // predecessors before the window are final: finish time, device and
-    // transfer cost of those in the previous window are read from its LDS
-    // copy before the node staging below overwrites it; older ones are
-    // gathered, in flight across the barriers (edges past the candidate
-    // positions' own, e >= efar, are skipped)
-    int64_t fq[EU], cqq[EU];
-    int32_t dq[EU];
-#pragma unroll
-    for (int u = 0; u < EU; u++) {
-      const int32_t q = qq[u];
-      const bool cand = E0 + tid + u * B < efar;
-      fq[u] = 0;
-      dq[u] = 0;
-      cqq[u] = 0;
-      if (cand && q < prev_lo) {
-        fq[u] = finp[q];
-        dq[u] = devp[q];
-        cqq[u] = cq[q];
-      } else if (cand && q < P0) {
-        const int32_t j = q - prev_lo;
-        fq[u] = s_f[j];
-        dq[u] = s_meta[j] & 255;
-        cqq[u] = s_c[j];
-      }
-    }
-    __syncthreads();
-    int32_t cnt = 0;
-    for (int t = tid; t < Pc1 - P0; t += B) cnt += (s_rp[t + 1] - s_rp[0] <= EC) ? 1 : 0;
-    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
-    if (lane == 0 && cnt) atomicAdd(&s_cut, cnt);
-    __syncthreads();
-    int32_t P1 = P0 + s_cut;
-    const int32_t lvcap = (lcur + kMsL < L) ? s_lv[kMsL] : n;
-    if (P1 > lvcap) P1 = lvcap;
-    const bool heavy = (P1 == P0);  // one node with more than EC predecessors
-    if (heavy) P1 = P0 + 1;
-    const int32_t NN = P1 - P0;
-    const int32_t E1 = s_rp[NN];
-#pragma unroll
-    for (int k = 0; k < NU; k++) {
-      const int32_t i = tid + k * B;
-      if (i >= NN) continue;
-      const int32_t mt = cmt[k];
-      int32_t hd = mt >> 16;
-      hd = hd < i ? hd : i;  // the window's first slot starts a run part ...
-      const int32_t tl = ((mt >> 8) & 1) | (i == NN - 1);  // ... and its last slot ends one
-      s_meta[i] = (mt & 255) | (tl << 8) | (hd << 16);
-      s_w[i] = cwv[k];
-      s_c[i] = ccv[k];
-      s_sx[i] = csx[k];
-      s_pm[i] = 0;
-      s_pc[i] = 0;
-      s_pw[i] = make_uint4(kPw2, kPw2, kPw2, kPw2);  // rows gather past a short list
-      if (!heavy) {  // owners of the row's first kOwnFill edges
-        const int32_t k0 = s_rp[i] - E0, k1 = s_rp[i + 1] - E0;
-        const int32_t kc = k1 - k0 < kOwnFill ? k1 : k0 + kOwnFill;
-        for (int32_t q = k0; q < kc; q++) s_own[q] = (int16_t)i;
-      }
-    }
-    for (int32_t k = tid; k < kMsL; k += B) {
-      const int32_t lb = s_lv[k], le = s_lv[k + 1];
-      int32_t a = lb < P0 ? P0 : (lb > P1 ? P1 : lb);
-      const int32_t b = le < P0 ? P0 : (le > P1 ? P1 : le);
-      if (a > b) a = b;
-      s_ld[k] = (a - P0) | ((b - P0) << 12) | ((int32_t)(le >= P1) << 24);
-      s_le[k] = heavy ? 0 : (s_rp[a - P0] - E0) | ((s_rp[b - P0] - E0) << 15);
-    }
-    __syncthreads();
-    CEL_TSTAMP(t1);
-    CEL_TADD(0, t0, t1);
-    // in-edges: pull lists and overflow words; predecessors before the window
-    // are final and are folded into the owner's partial ready time
-    if (!heavy) {
-      auto stage_edge = [&](int32_t e, int32_t q, int64_t fqv, int32_t dqv, int64_t cqv) {
-        const int32_t own = owner_of(s_rp, NN, s_own[e - E0], e);
-        const int dvo = s_meta[own] & 255;
-        int32_t word = kNoop;
-        if (q >= P0) {
-          const int32_t j = q - P0;
-          const int32_t pwd = j | ((int32_t)((s_meta[j] & 255) != dvo) << 12);
-          const int32_t kk = atomicAdd(&s_pc[own], 1);
-          if (kk < F) {
-            reinterpret_cast<uint16_t *>(&s_pw[own])[kk] = (uint16_t)pwd;
-          } else {
-            word = pwd | (own << 16);
-            int32_t lo = 0, hi = kMsL - 1;  // the owner's level: last k with s_lv[k] <= P0 + own
-            while (lo < hi) {
-              const int32_t mid = (lo + hi + 1) >> 1;
-              if (s_lv[mid] <= P0 + own) lo = mid;
-              else hi = mid - 1;
-            }
-            atomicOr(&s_ld[lo], 1 << 25);
-          }
-        } else {
-          const int64_t x = fqv + (dqv != dvo ? cqv : 0);
-          atomicMax((long long *)&s_pm[own], (long long)x);
-        }
-        s_epk[e - E0] = word;
-      };
-#pragma unroll
-      for (int u = 0; u < EU; u++) {
-        const int32_t e = E0 + tid + u * B;
-        if (u * B + tid < EC && e < E1) stage_edge(e, qq[u], fq[u], dq[u], cqq[u]);
-      }
-    } else {  // a single node with more than EC predecessors, all before it
-      const int dv0 = s_meta[0] & 255;
-      const int64_t mx = heavy_max<kHeavyU, B>(
-          E0, E1, tid, [&](int32_t e) { return pidx[e]; },
-          [&](int32_t q) { return finp[q] + (devp[q] != dv0 ? cq[q] : 0); });
-      if (lane == 0 && mx >= 0) atomicMax((long long *)&s_pm[0], (long long)mx);
-    }
-    __syncthreads();
-    CEL_TSTAMP(t2);
-    CEL_TADD(1, t1, t2);
-    // level descriptors in registers, lane l holding levels l, l+64, ...:
-    // first slot | end slot << 12 | window ends here << 24 | overflow << 25
-    int32_t lvm[4];
-#pragma unroll
-    for (int u = 0; u < 4; u++) {
-      const int k = lane + 64 * u;
-      lvm[u] = s_ld[k];
-    }
-    auto level_desc = [&](int32_t kk) {
-      int32_t t;
-      switch (kk >> 6) {  // uniform: pick the register, then read lane kk & 63
-        case 0: t = lvm[0]; break;
-        case 1: t = lvm[1]; break;
-        case 2: t = lvm[2]; break;
-        default: t = lvm[3]; break;
-      }
-      return __builtin_amdgcn_readlane(t, kk & 63);
-    };
-    uint64_t vis[4];  // levels the whole block visits: wide ones and the window's end
-#pragma unroll
-    for (int u = 0; u < 4; u++)
-      vis[u] = __ballot((((lvm[u] >> 12) & 0xFFF) - (lvm[u] & 0xFFF) > kNarrow) || ((lvm[u] >> 24) & 1));
-    CEL_TSTAMP(t3);
-    CEL_TADD(2, t2, t3);
-    for (int32_t k = wave0 ? 0 : next_marked(vis, 0); k < kMsL;
-         k = wave0 ? k + 1 : next_marked(vis, k + 1)) {
-      const int32_t dsc = level_desc(k);
-      const int32_t a0 = dsc & 0xFFF, b0 = (dsc >> 12) & 0xFFF, fl = dsc >> 24;
-      if (a0 < b0) {
-        const int32_t le = (fl & 2) ? s_le[k] : 0, ea = le & 0x7FFF, eb = le >> 15;
-        CEL_TSTAMP(tl0);
-        if (b0 - a0 <= kNarrow) {
-          if (wave0) {
-            if (fl & 2) {  // in-edges past the pull lists
-              for (int32_t e = ea + lane; e < eb; e += 64) {
-                const int32_t wd = s_epk[e];
-                const int32_t j = wd & 0xFFF;
-                const int64_t x = s_f[j] + (((wd >> 12) & 1) ? s_c[j] : 0);
-                atomicMax((long long *)&s_pm[(wd >> 16) & 0xFFF], (long long)x);
-              }
-              lds_order();
-            }
-            // rows in pairs: gathers and scans of the two rows are
-            // independent; only the carry chains the rows
-            int64_t carry = kNeg;
-            for (int32_t r0 = a0; r0 < b0; r0 += 128) {
-              if (b0 - r0 > 64) narrow_rows(std::integral_constant<int, 2>(), r0, b0, carry);
-              else narrow_rows(std::integral_constant<int, 1>(), r0, b0, carry);
-              lds_order();
-            }
-          }
-          CEL_TSTAMP(tl1);
-          CEL_TADD(7, tl0, tl1);
-          CEL_TCOUNT(4);
-        } else {
-          __syncthreads();  // wave 0's narrow levels before this one
-          if (fl & 2) {
-            for (int32_t e = ea + tid; e < eb; e += B) {
-              const int32_t wd = s_epk[e];
-              const int32_t j = wd & 0xFFF;
-              const int64_t x = s_f[j] + (((wd >> 12) & 1) ? s_c[j] : 0);
-              atomicMax((long long *)&s_pm[(wd >> 16) & 0xFFF], (long long)x);
-            }
-            __syncthreads();
-          }
-          if (tid == 0) s_cy[0] = kNeg;
-          int par = 0;
-          for (int32_t base0 = a0; base0 < b0; base0 += B) {
-            const int32_t s = base0 + tid;
-            const bool act = s < b0;
-            const int32_t si = act ? s : NC;
-            const RowPre cur = row_pre(si);
-            int64_t y = row_value(si, cur, row_kmax(cur.pc));
-            const int32_t meta = cur.meta;
-            const int64_t base = cur.sx + cur.w;
-            const int32_t hd = meta >> 16;
-            y = wave_seg_pmax(y, hd, lane);
-            if (lane == 63) s_wy[par][wv] = y;
-            __syncthreads();
-            if (hd > lane) {  // the run began before this wave's row
-              const int32_t hs = s - hd;
-              int64_t cy = kNeg;
-              for (int w2 = wv - 1; w2 >= 0 && base0 + 64 * w2 + 63 >= hs; w2--)
-                cy = s_wy[par][w2] > cy ? s_wy[par][w2] : cy;
-              if (hs < base0 && s_cy[par] > cy) cy = s_cy[par];
-              y = cy > y ? cy : y;
-            }
-            const int64_t fin = base + y;
-            if (act) {
-              s_f[s] = fin;
-              finp[P0 + s] = fin;
-              mk = fin > mk ? fin : mk;
-              if (meta & 256) s_avail[meta & 255] = fin;
-              if (tid == B - 1) s_cy[par ^ 1] = y;
-            }
-            par ^= 1;
-          }
-          __syncthreads();
-          CEL_TSTAMP(tl1);
-          CEL_TADD(8, tl0, tl1);
-          CEL_TCOUNT(5);
-        }
-      }
-      if (fl & 1) break;  // the window ends inside this level
-    }
-    CEL_TSTAMP(t4);
-    CEL_TADD(3, t3, t4);
-    if (P1 < n) {
-      int32_t k = 0;
-      while (k < kMsL && lcur + k + 1 < L && s_lv[k + 1] <= P1) k++;
-      lcur += k;
-    }
-    prev_lo = P0;
-    P0 = P1;
-    E0 = E1;
-    __syncthreads();
-  }
-  for (int off = 32; off > 0; off >>= 1) {
-    const int64_t y = __shfl_xor(mk, off);
-    mk = y > mk ? y : mk;
-  }
-  if (lane == 0) s_red[wv] = mk;
-  __syncthreads();
-  if (tid == 0) {
-    int64_t r = s_red[0];
-    for (int i = 1; i < NW; i++) r = s_red[i] > r ? s_red[i] : r;
-    makespan[0] = r;
   }
 }
 
@@ -1391,7 +831,7 @@ static int makespan_impl(const char *fn, const cel_graph *g, const cel_devices *
   CEL_TRY(sc.get(&wp, n));
   CEL_TRY(sc.get(&cq, n));
   CEL_TRY(sc.get(&devp, (int64_t)K * n));
-  CEL_TRY(sc.get(&finp, (int64_t)K * n));
+  CEL_TRY(sc.get(&finp, (K == 1 ? 2 : (int64_t)K) * n));  // K = 1: fin, then fin + c
   const int gx = grid_for(n, 256, 1024);
   if (K == 1) {
     // Device-grouped order: inside each level, nodes sorted by (device,
@@ -1422,11 +862,8 @@ static int makespan_impl(const char *fn, const cel_graph *g, const cel_devices *
     CEL_TRY(exclusive_scan_i64(wp, wx, n, sc, s));
     k_runs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, level_ptr, level, gorder, devp, wx, sx, meta,
                                                  st);
-    {
-      KTimer kt(s, "k_makespan_one");
-      k_makespan_one<1024, 1792, 5120><<<1, 1024, 0, s>>>(n, L, level_ptr, pptr, pidx, wp, cq, devp,
-                                                          sx, meta, finp, makespan, st);
-    }
+    CEL_TRY(ms_ring(n, g->m, L, level_ptr, gorder, level, pptr, pidx, wp, cq, devp, sx, meta, finp,
+                    makespan, sc, s, st));
     if (start || finish)
       k_makespan_out<<<grid_for(n, 256, 8192), 256, 0, s>>>(1, n, gorder, finp, wp, start, finish,
                                                             st);
@@ -1509,13 +946,15 @@ static int fixed_scratch(char **out) {  // g_fixed_mu held
   return CEL_OK;
 }
 
-// A bound on the scratch one call takes: per node at most 136 bytes (position
+// A bound on the scratch one call takes: per node at most 200 bytes (position
 // maps, relabelled CSR rows, costs, the device-grouped order and its sort
-// buffers, per-level tile lists, for K = 1), 4 bytes per edge (relabelled
-// in-edges), 9 bytes per node and placement (devices and finish times), and
-// 64 KiB for block partials and 256-byte rounding.
+// buffers, per-level tile lists, and for K = 1 the ring sweep's pull records,
+// list offsets, level and segment tables and the second finish array), 16
+// bytes per edge (relabelled in-edges; for K = 1 tagged, far and long lists),
+// 9 bytes per node and placement (devices and finish times), and 64 KiB for
+// block partials and 256-byte rounding.
 static uint64_t makespan_scratch_bound(int64_t n, int64_t m, int64_t K) {
-  return 65536ull + 136ull * (uint64_t)(n + 1) + 4ull * (uint64_t)m + 9ull * (uint64_t)K * (uint64_t)n;
+  return 65536ull + 200ull * (uint64_t)(n + 1) + 16ull * (uint64_t)m + 9ull * (uint64_t)K * (uint64_t)n;
 }
 
 extern "C" int cel_makespan_noalloc(const cel_graph *g, const cel_devices *d, const int32_t *order,

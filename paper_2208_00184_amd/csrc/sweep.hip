@@ -62,44 +62,6 @@ constexpr int kHeavyNear = 15;          // count field: more near neighbours tha
 __device__ inline uint32_t rec_count(const uint4 &r) { return (r.x >> 12) & 15u; }
 
 
-__device__ inline int64_t ld_coherent(const int64_t *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline void st_coherent(int64_t *p, int64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-constexpr int32_t kSpin = 1 << 21;  // polls before a wait gives up (far longer than any real wait)
-
-// A pull value written earlier by this kernel, read again until it is
-// visible.  A wait that outlasts kSpin polls raises EB_WAIT and sets the
-// workgroup's abort flag (a broken invariant, never a slow run); the value
-// returned then is 0 and the results are discarded by the error.
-__device__ inline int64_t ld_final(const int64_t *p, int32_t *s_abort, Status *st) {
-  int64_t v = ld_coherent(p);
-  for (int32_t i = 0; v < 0; i++) {
-    if (i == kSpin || __hip_atomic_load(s_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) {
-      raise_err(st, EB_WAIT);
-      __hip_atomic_store(s_abort, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-      return 0;
-    }
-    __builtin_amdgcn_s_sleep(1);
-    v = ld_coherent(p);
-  }
-  return v;
-}
-
-// Values of the positions q[j] (q < 0: 0), every load issued before the first
-// use; one not yet visible is read again by ld_final (rare).
-template <int N>
-__device__ inline void ld_many(int64_t (&x)[N], const int32_t (&q)[N], const int64_t *gx,
-                               int32_t *s_abort, Status *st) {
-#pragma unroll
-  for (int j = 0; j < N; j++) x[j] = q[j] >= 0 ? ld_coherent(&gx[q[j]]) : 0;
-#pragma unroll
-  for (int j = 0; j < N; j++)
-    if (x[j] < 0) x[j] = ld_final(&gx[q[j]], s_abort, st);
-}
-
 // -------------------------------------------------------------- preparation
 
 // Levels out of ring mode (wide[l] = 1): wider than kWideW, holding a node
