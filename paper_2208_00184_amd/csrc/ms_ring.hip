@@ -186,18 +186,49 @@ __device__ inline int64_t ms_near(int64_t m, const uint4 &r, const int64_t *s_x)
   return g[0] > m ? g[0] : m;
 }
 
+// Maximum of two non-negative int64 values below 2^62 with one v_max_f64:
+// read as IEEE doubles, such bit patterns are finite, non-negative numbers
+// (subnormal below 2^52, which the kernels' f64 denormal mode keeps) whose
+// order is the integers' order, and the maximum returns one operand's bits
+// unchanged.  Every finish time is below 2^62 (the overflow check), so every
+// value of the prefix maximum is.
+__device__ inline int64_t max_nonneg(int64_t a, int64_t b) {
+  int64_t r;
+  asm volatile("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// One step of an unsegmented prefix maximum over each of NR rows (lanes
+// without a source, or outside the DPP rows the step writes, take 0, the
+// identity for non-negative values); the rows' steps are interleaved.
+template <int CTRL, int ROWMASK, int NR>
+__device__ inline void plain_pmax_step(int64_t (&y)[NR]) {
+  int64_t u[NR];
+#pragma unroll
+  for (int k = 0; k < NR; k++) u[k] = dpp64<CTRL, ROWMASK>(y[k], 0);
+#pragma unroll
+  for (int k = 0; k < NR; k++) y[k] = max_nonneg(y[k], u[k]);
+}
+
 // Finish times of the NR rows [r0, r0 + 64 NR) of a narrow level ending at b,
 // by the compute wave from the staged data; carry is the prefix value at the
-// end of the previous row of the level (kNeg before the first).  Lanes past b
+// end of the previous row of the level (0 before the first).  Lanes past b
 // compute from whatever their slots hold (every record names in-range ring
-// indices, every meta an in-range device) and write nothing.
+// indices, every meta an in-range device) and write nothing; being the rows'
+// last lanes, they never feed a valid lane's prefix.
+//
+// The prefix runs over y = max(0, ready - sx), with the free time folded in
+// at a run's first slot and the carry at lane 0 of a row that continues a
+// run: the run's maximum includes the free time, which is never negative, so
+// clamping at 0 changes no maximum.  A row that is one run (almost every row
+// when a level sits on one device) takes the unsegmented scan.
 template <int NR>
 __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane, int64_t &carry,
                                int64_t &mk, int64_t *s_x, const uint4 *s_rec,
                                const int64_t *s_base, const int64_t *s_sx, const int64_t *s_w,
                                const int64_t *s_c, const int32_t *s_meta, int64_t *s_avail) {
   uint4 r[NR];
-  int64_t y[NR], sx[NR], av[NR];
+  int64_t y[NR], sx[NR], av[NR], w[NR], c[NR];
   int32_t mt[NR];
 #pragma unroll
   for (int u = 0; u < NR; u++) {
@@ -206,14 +237,16 @@ __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane,
     y[u] = s_base[s];
     sx[u] = s_sx[s];
     mt[u] = s_meta[s];
+    w[u] = s_w[s];
+    c[u] = s_c[s];
   }
 #pragma unroll
   for (int u = 0; u < NR; u++) av[u] = s_avail[mt[u] & 255];  // free times as of the level's start
   uint32_t cls = 0;
 #pragma unroll
   for (int u = 0; u < NR; u++) {
-    const uint32_t c = ((uint32_t)__builtin_amdgcn_readfirstlane(r[u].x) >> 13) & 7u;
-    cls = c > cls ? c : cls;
+    const uint32_t k = ((uint32_t)__builtin_amdgcn_readfirstlane(r[u].x) >> 13) & 7u;
+    cls = k > cls ? k : cls;
   }
   if (cls == 1) {
 #pragma unroll
@@ -250,31 +283,52 @@ __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane,
 #pragma unroll
     for (int u = 0; u < NR; u++) y[u] = ms_near<kMNear>(y[u], r[u], s_x);
   }
-  // y = ready - sx, the device's free time at the run's first slot, then the
-  // prefix maximum over the run
+  // y = max(0, ready - sx), the free time at a run's first slot; rows with a
+  // run starting past lane 0
+  bool split = false;
 #pragma unroll
   for (int u = 0; u < NR; u++) {
     const int32_t hd = mt[u] >> 16;
     int64_t v = y[u] - sx[u];
-    if (hd == 0) {
-      const int64_t vf = av[u] - sx[u];
-      v = vf > v ? vf : v;
-    }
-    y[u] = wave_seg_pmax(v, hd, lane);
+    v = v < 0 ? 0 : v;
+    if (hd == 0) v = av[u] > v ? av[u] : v;  // sx = 0 at a run's first slot
+    y[u] = v;
+    split |= __ballot(r0 + 64 * u + lane < b && hd < lane) != 0;
   }
+  if (!split) {
+    // every row one run: the carry enters at lane 0, then a plain prefix max
+    if (lane == 0 && (mt[0] >> 16) > 0) y[0] = carry > y[0] ? carry : y[0];
+    plain_pmax_step<0x111, 0xF, NR>(y);  // row_shr:1
+    plain_pmax_step<0x112, 0xF, NR>(y);  // row_shr:2
+    plain_pmax_step<0x114, 0xF, NR>(y);  // row_shr:4
+    plain_pmax_step<0x118, 0xF, NR>(y);  // row_shr:8
+    plain_pmax_step<0x142, 0xA, NR>(y);  // row_bcast:15 into rows 1 and 3
+    plain_pmax_step<0x143, 0xC, NR>(y);  // row_bcast:31 into rows 2 and 3
+    if constexpr (NR == 2) {
+      // the second row takes the first's carry unless a run starts at its lane 0
+      if ((__builtin_amdgcn_readfirstlane(mt[1]) >> 16) > 0) {
+        const int64_t c0 = readlane64(y[0], 63);
+        y[1] = c0 > y[1] ? c0 : y[1];
+      }
+    }
+    carry = readlane64(y[NR - 1], 63);
+  } else {
 #pragma unroll
-  for (int u = 0; u < NR; u++) {  // a run that began in an earlier row
-    if ((mt[u] >> 16) > lane && carry > y[u]) y[u] = carry;
-    carry = readlane64(y[u], 63);
+    for (int u = 0; u < NR; u++) {
+      const int32_t hd = mt[u] >> 16;
+      if (lane == 0 && hd > 0) y[u] = carry > y[u] ? carry : y[u];
+      y[u] = wave_seg_pmax(y[u], hd, lane);
+      carry = readlane64(y[u], 63);
+    }
   }
 #pragma unroll
   for (int u = 0; u < NR; u++) {
     const int32_t p = r0 + 64 * u + lane;
     if (p < b) {
       const int s = p & kMRMask;
-      const int64_t fin = sx[u] + s_w[s] + y[u];
+      const int64_t fin = sx[u] + w[u] + y[u];
       s_x[s] = fin;
-      s_x[kMRing + s] = fin + s_c[s];
+      s_x[kMRing + s] = fin + c[u];
       mk = fin > mk ? fin : mk;
       if (mt[u] & 256) s_avail[mt[u] & 255] = fin;
     }
@@ -467,7 +521,7 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
           // rows of 64 from the level's start, two at a time, in ascending
           // order: a slot's previous position (kMRing back) may still be read
           // by lower slots of the level, which run first
-          int64_t carry = kNeg;
+          int64_t carry = 0;
           int32_t r0 = pa;
           for (; r0 + 64 < pb; r0 += 128)
             ms_rows<2>(a, r0, pb, lane, carry, mk, s_x, s_rec, s_base, s_sx, s_w, s_c, s_meta, s_avail);

@@ -261,6 +261,55 @@ def test_makespan_wide_levels_batch(widths, fanin, D, K):
     assert np.array_equal(np_(st), ref_st) and np.array_equal(np_(fi), ref_fi)
 
 
+def test_makespan_one_run_boundaries():
+    """K = 1: the device runs of a level (consecutive slots of the
+    device-grouped order) start at lane 0 of a row, inside a row, exactly at
+    the second row's lane 0 and in later rows, or a level sits on one device
+    and its run spans up to four rows; predecessors are near (the previous
+    levels) and far (more than 2,048 slots back)."""
+    rng = np.random.default_rng(17)
+    # per level, the sizes of its device runs (device ids ascending)
+    runs = [[64, 64], [1, 127], [127, 1], [128], [63, 65], [65, 63], [200], [64, 64, 64],
+            [30, 34, 64, 2], [256], [17], [64], [129], [1, 1, 1, 61, 64], [192, 64]]
+    runs = runs * 6
+    widths = [sum(r) for r in runs]
+    starts = np.concatenate([[0], np.cumsum(widths)])
+    n = int(starts[-1])
+    D = 6
+    dev = np.zeros(n, np.int64)
+    edges = []
+    for li, rs in enumerate(runs):
+        devs = np.sort(rng.choice(D, len(rs), replace=False))
+        s0 = int(starts[li])
+        for d_, k in zip(devs, rs):
+            dev[s0:s0 + k] = d_
+            s0 += k
+        if li == 0:
+            continue
+        for v in range(int(starts[li]), int(starts[li + 1])):
+            edges.append((int(rng.integers(starts[li - 1], starts[li])), v))
+            for u in rng.integers(0, starts[li], int(rng.integers(0, 4))):
+                edges.append((int(u), v))
+    edges = sorted(set(edges))
+    wl = from_edges(n, edges, rng.integers(1, 5000, n), rng.integers(0, 1 << 20, n), D,
+                    np.full(D, 1 << 40), 7, 300, name="run-boundaries")
+    lev, oid, lp, L = O.topo_levels(wl)
+    assert L == len(runs)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    # the placement puts each level's runs where the sizes say, whatever the
+    # priority order inside the level
+    P = np.zeros((1, n), np.uint8)
+    for li in range(L):
+        nodes = np.asarray(pr[lp[li]:lp[li + 1]])
+        P[0, nodes] = np.sort(dev[starts[li]:starts[li + 1]])
+    ref_ms, ref_st, ref_fi = O.makespan(wl, pr, P)
+    g, d = up(wl)
+    ms, st, fi = cel.makespan(g, d, tt(pr, np.int32), tt(lev, np.int32), tt(lp, np.int32), L,
+                              tt(P[0], np.uint8), want_times=True)
+    assert np_(ms)[0] == ref_ms[0]
+    assert np.array_equal(np_(st)[0], ref_st[0]) and np.array_equal(np_(fi)[0], ref_fi[0])
+
+
 def test_makespan_wide_no_edges_batch():
     """Sources only: one level of 3,000 isolated nodes, 4 placements."""
     n, D = 3000, 5
