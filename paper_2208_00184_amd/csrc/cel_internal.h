@@ -52,6 +52,14 @@ __device__ inline void wave_lds_sync() {
 // the same wave wrote earlier without a wait; the compiler must merely keep
 // the accesses in program order.
 __device__ inline void lds_order() { asm volatile("" ::: "memory"); }
+// A workgroup barrier that orders LDS only: global loads issued before it
+// stay in flight (a full __syncthreads() waits for them too).  Use it where
+// no wave reads another wave's global stores across the barrier.
+__device__ inline void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
 // ------------------------------------------------ wave-level scans with DPP
 // DPP moves read another lane's register inside the VALU (no LDS round trip).

@@ -173,18 +173,6 @@ __global__ void k_ms_rowmark(int32_t n, const int32_t *lp, const int32_t *gorder
 
 // ------------------------------------------------------------------ compute
 
-// max of m and the first K entries' ring values, as a tree
-template <int K>
-__device__ inline int64_t ms_near(int64_t m, const uint4 &r, const int64_t *s_x) {
-  int64_t g[K];
-#pragma unroll
-  for (int j = 0; j < K; j++) g[j] = s_x[ms_entry(r, j)];
-#pragma unroll
-  for (int w = 1; w < K; w <<= 1)
-#pragma unroll
-    for (int j = 0; j + w < K; j += 2 * w) g[j] = g[j + w] > g[j] ? g[j + w] : g[j];
-  return g[0] > m ? g[0] : m;
-}
 
 // Maximum of two non-negative int64 values below 2^62 with one v_max_f64:
 // read as IEEE doubles, such bit patterns are finite, non-negative numbers
@@ -196,6 +184,19 @@ __device__ inline int64_t max_nonneg(int64_t a, int64_t b) {
   int64_t r;
   asm volatile("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
   return r;
+}
+
+// max of m and the first K entries' ring values, as a tree (all non-negative)
+template <int K>
+__device__ inline int64_t ms_near(int64_t m, const uint4 &r, const int64_t *s_x) {
+  int64_t g[K];
+#pragma unroll
+  for (int j = 0; j < K; j++) g[j] = s_x[ms_entry(r, j)];
+#pragma unroll
+  for (int w = 1; w < K; w <<= 1)
+#pragma unroll
+    for (int j = 0; j + w < K; j += 2 * w) g[j] = max_nonneg(g[j], g[j + w]);
+  return max_nonneg(m, g[0]);
 }
 
 // One step of an unsegmented prefix maximum over each of NR rows (lanes
@@ -225,10 +226,10 @@ __device__ inline void plain_pmax_step(int64_t (&y)[NR]) {
 template <int NR>
 __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane, int64_t &carry,
                                int64_t &mk, int64_t *s_x, const uint4 *s_rec,
-                               const int64_t *s_base, const int64_t *s_sx, const int64_t *s_w,
-                               const int64_t *s_c, const int32_t *s_meta, int64_t *s_avail) {
+                               const int64_t *s_base, const int64_t *s_sx, const int64_t *s_sxw,
+                               const int64_t *s_sxwc, const int32_t *s_meta, int64_t *s_avail) {
   uint4 r[NR];
-  int64_t y[NR], sx[NR], av[NR], w[NR], c[NR];
+  int64_t y[NR], sx[NR], av[NR], w[NR], c[NR];  // w: sx + w, c: sx + w + c
   int32_t mt[NR];
 #pragma unroll
   for (int u = 0; u < NR; u++) {
@@ -237,8 +238,8 @@ __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane,
     y[u] = s_base[s];
     sx[u] = s_sx[s];
     mt[u] = s_meta[s];
-    w[u] = s_w[s];
-    c[u] = s_c[s];
+    w[u] = s_sxw[s];
+    c[u] = s_sxwc[s];
   }
 #pragma unroll
   for (int u = 0; u < NR; u++) av[u] = s_avail[mt[u] & 255];  // free times as of the level's start
@@ -276,7 +277,7 @@ __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane,
             const int64_t o = __shfl_xor((long long)mx, off);
             mx = o > mx ? o : mx;
           }
-          if (lane == h) y[u] = mx > y[u] ? mx : y[u];
+          if (lane == h) y[u] = max_nonneg(y[u], mx);
         }
       }
     }
@@ -291,13 +292,13 @@ __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane,
     const int32_t hd = mt[u] >> 16;
     int64_t v = y[u] - sx[u];
     v = v < 0 ? 0 : v;
-    if (hd == 0) v = av[u] > v ? av[u] : v;  // sx = 0 at a run's first slot
+    if (hd == 0) v = max_nonneg(v, av[u]);  // sx = 0 at a run's first slot
     y[u] = v;
     split |= __ballot(r0 + 64 * u + lane < b && hd < lane) != 0;
   }
   if (!split) {
     // every row one run: the carry enters at lane 0, then a plain prefix max
-    if (lane == 0 && (mt[0] >> 16) > 0) y[0] = carry > y[0] ? carry : y[0];
+    if (lane == 0 && (mt[0] >> 16) > 0) y[0] = max_nonneg(y[0], carry);
     plain_pmax_step<0x111, 0xF, NR>(y);  // row_shr:1
     plain_pmax_step<0x112, 0xF, NR>(y);  // row_shr:2
     plain_pmax_step<0x114, 0xF, NR>(y);  // row_shr:4
@@ -307,8 +308,7 @@ __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane,
     if constexpr (NR == 2) {
       // the second row takes the first's carry unless a run starts at its lane 0
       if ((__builtin_amdgcn_readfirstlane(mt[1]) >> 16) > 0) {
-        const int64_t c0 = readlane64(y[0], 63);
-        y[1] = c0 > y[1] ? c0 : y[1];
+        y[1] = max_nonneg(y[1], readlane64(y[0], 63));
       }
     }
     carry = readlane64(y[NR - 1], 63);
@@ -316,7 +316,7 @@ __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane,
 #pragma unroll
     for (int u = 0; u < NR; u++) {
       const int32_t hd = mt[u] >> 16;
-      if (lane == 0 && hd > 0) y[u] = carry > y[u] ? carry : y[u];
+      if (lane == 0 && hd > 0) y[u] = max_nonneg(y[u], carry);
       y[u] = wave_seg_pmax(y[u], hd, lane);
       carry = readlane64(y[u], 63);
     }
@@ -326,10 +326,10 @@ __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane,
     const int32_t p = r0 + 64 * u + lane;
     if (p < b) {
       const int s = p & kMRMask;
-      const int64_t fin = sx[u] + w[u] + y[u];
+      const int64_t fin = w[u] + y[u];
       s_x[s] = fin;
-      s_x[kMRing + s] = fin + c[u];
-      mk = fin > mk ? fin : mk;
+      s_x[kMRing + s] = c[u] + y[u];
+      mk = max_nonneg(mk, fin);
       if (mt[u] & 256) s_avail[mt[u] & 255] = fin;
     }
   }
@@ -348,7 +348,8 @@ __device__ inline void ms_flush(const MsArgs &a, int32_t q0, int32_t q1, int t, 
 __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
   __shared__ int64_t s_x[2 * kMRing + 1];
   __shared__ uint4 s_rec[kMRing];
-  __shared__ int64_t s_base[kMRing], s_sx[kMRing], s_w[kMRing], s_c[kMRing];
+  __shared__ int64_t s_base[kMRing], s_sx[kMRing];
+  __shared__ int64_t s_sxw[kMRing], s_sxwc[kMRing];  // sx + w, sx + w + c
   __shared__ int32_t s_meta[kMRing];
   __shared__ int64_t s_avail[256];
   __shared__ int32_t s_flag[kMNF];
@@ -370,8 +371,8 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
     s_x[kMRing + i] = 0;
     s_base[i] = 0;
     s_sx[i] = 0;
-    s_w[i] = 0;
-    s_c[i] = 0;
+    s_sxw[i] = 0;
+    s_sxwc[i] = 0;
     s_meta[i] = 0;
   }
   for (int i = tid; i < 256; i += kMsB) s_avail[i] = 0;
@@ -402,36 +403,67 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
       // one level [S0, S1), kMsB slots per pass in order: ready times from
       // global memory (rows of more than kMBRow predecessors by the whole
       // block), then the prefix maximum across the pass, carried between
-      // waves and passes through LDS
+      // waves and passes through LDS.  Each pass's per-slot data is loaded
+      // during the pass before; the passes' barriers order LDS only (no wave
+      // reads this level's finish times).
+      struct Pass {
+        int32_t e0, e1, meta;
+        int64_t sx, w, c;
+      };
+      auto load_pass = [&](int32_t q0) {
+        Pass ps;
+        const int32_t p = q0 + tid;
+        const bool act = p < S1;
+        ps.e0 = act ? a.pptr[p] : 0;
+        ps.e1 = act ? a.pptr[p + 1] : 0;
+        ps.meta = act ? a.metap[p] : 0;
+        ps.sx = act ? a.sxp[p] : 0;
+        ps.w = act ? a.wp[p] : 0;
+        ps.c = act ? a.cq[p] : 0;
+        return ps;
+      };
       int par = 0;
       if (tid == 0) s_cy[0] = kNeg;
+      Pass cur = load_pass(S0);
       for (int32_t p0 = S0; p0 < S1; p0 += kMsB) {
         const int32_t p = p0 + tid;
         const bool act = p < S1;
-        const int32_t e0 = act ? a.pptr[p] : 0, e1 = act ? a.pptr[p + 1] : 0;
+        const int32_t e0 = cur.e0, e1 = cur.e1;
+        const bool many = e1 - e0 > kMBRow;
+        // the first 4 predecessors' values, then the next pass's data, in flight together
+        int64_t x[4];
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+          x[j] = (!many && e0 + j < e1) ? ld_coherent(ms_src(a, a.tidx[e0 + j])) : 0;
+        const Pass nxt = load_pass(p0 + kMsB);
         int64_t r = 0;
-        if (e1 - e0 > kMBRow) {
+        if (many) {
           s_hl[atomicAdd(&s_nh, 1)] = tid;
         } else {
-          for (int32_t e = e0; e < e1; e += 4) {
-            int64_t x[4];
+#pragma unroll
+          for (int j = 0; j < 4; j++) {
+            if (x[j] < 0) x[j] = ld_final(ms_src(a, a.tidx[e0 + j]), &s_abort, st);
+            r = x[j] > r ? x[j] : r;
+          }
+          for (int32_t e = e0 + 4; e < e1; e += 4) {
+            int64_t xx[4];
 #pragma unroll
             for (int j = 0; j < 4; j++)
-              x[j] = e + j < e1 ? ld_coherent(ms_src(a, a.tidx[e + j])) : 0;
+              xx[j] = e + j < e1 ? ld_coherent(ms_src(a, a.tidx[e + j])) : 0;
 #pragma unroll
             for (int j = 0; j < 4; j++) {
-              if (x[j] < 0) x[j] = ld_final(ms_src(a, a.tidx[e + j]), &s_abort, st);
-              r = x[j] > r ? x[j] : r;
+              if (xx[j] < 0) xx[j] = ld_final(ms_src(a, a.tidx[e + j]), &s_abort, st);
+              r = xx[j] > r ? xx[j] : r;
             }
           }
         }
-        __syncthreads();
+        lds_barrier();
         const int32_t nh = s_nh;
         for (int32_t i = 0; i < nh; i++) {  // rows of many predecessors: the whole block
           const int32_t t2 = s_hl[i];
           const int32_t p2 = p0 + t2;
-          // every predecessor was stored before an earlier barrier: visible,
-          // so a negative value would mean a broken invariant
+          // every predecessor was stored before an earlier full barrier:
+          // visible, so a negative value would mean a broken invariant
           const int64_t mx = heavy_max<kHeavyU, kMsB>(
               a.pptr[p2], a.pptr[p2 + 1], tid, [&](int32_t e) { return (int32_t)e; },
               [&](int32_t e) {
@@ -440,17 +472,17 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
                 return v;
               });
           if (lane == 0) s_red[wave] = mx;
-          __syncthreads();
+          lds_barrier();
           if (tid == 0) {
             int64_t m2 = 0;
             for (int w = 0; w < kMsB / 64; w++) m2 = s_red[w] > m2 ? s_red[w] : m2;
             s_hr[t2] = m2;
           }
-          __syncthreads();
+          lds_barrier();
         }
-        if (act && e1 - e0 > kMBRow) r = s_hr[tid];
-        const int32_t meta = act ? a.metap[p] : 0;
-        const int64_t sx = act ? a.sxp[p] : 0;
+        if (act && many) r = s_hr[tid];
+        const int32_t meta = cur.meta;
+        const int64_t sx = cur.sx;
         const int32_t hd = meta >> 16;
         int64_t y = r - sx;
         if (hd == 0) {
@@ -459,7 +491,7 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
         }
         y = wave_seg_pmax(y, hd, lane);
         if (lane == 63) s_wy[par][wave] = y;
-        __syncthreads();  // every free time read before any is written below
+        lds_barrier();  // every free time read before any is written below
         if (hd > lane) {  // the run began before this wave's row
           const int32_t hs = p - hd;
           int64_t cy = kNeg;
@@ -469,16 +501,17 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
           y = cy > y ? cy : y;
         }
         if (act) {
-          const int64_t fin = sx + a.wp[p] + y;
+          const int64_t fin = sx + cur.w + y;
           st_coherent(&a.gf[p], fin);
-          st_coherent(&a.gf[(int64_t)a.n + p], fin + a.cq[p]);
+          st_coherent(&a.gf[(int64_t)a.n + p], fin + cur.c);
           mk = fin > mk ? fin : mk;
           if (meta & 256) s_avail[meta & 255] = fin;
         }
         if (tid == kMsB - 1) s_cy[par ^ 1] = y;
         if (tid == 0) s_nh = 0;
         par ^= 1;
-        __syncthreads();
+        cur = nxt;
+        lds_barrier();
       }
       continue;
     }
@@ -503,10 +536,15 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
           // every staging task covering [pa, pb) complete
           const int32_t need = (pb - 1 - S0) / kMStage;
           for (int32_t spin = 0; ready <= need;) {
-            const int32_t f = __hip_atomic_load(&s_flag[ready % kMNF], __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_WORKGROUP);
-            if (f == ready) {
-              ready++;
+            // lanes 0..kMNF-1 look at the next kMNF tasks in one LDS round trip
+            const int32_t tk = ready + lane;
+            const int32_t f = lane < kMNF ? __hip_atomic_load(&s_flag[tk % kMNF], __ATOMIC_RELAXED,
+                                                              __HIP_MEMORY_SCOPE_WORKGROUP)
+                                          : -1;
+            const uint64_t done = __ballot(lane < kMNF && f == tk);
+            const int32_t adv = __builtin_ctzll(~done);  // complete tasks in a row from `ready`
+            if (adv > 0) {
+              ready += adv;
             } else {
               if (++spin == kSpin || aborted()) {
                 give_up();
@@ -524,9 +562,9 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
           int64_t carry = 0;
           int32_t r0 = pa;
           for (; r0 + 64 < pb; r0 += 128)
-            ms_rows<2>(a, r0, pb, lane, carry, mk, s_x, s_rec, s_base, s_sx, s_w, s_c, s_meta, s_avail);
+            ms_rows<2>(a, r0, pb, lane, carry, mk, s_x, s_rec, s_base, s_sx, s_sxw, s_sxwc, s_meta, s_avail);
           if (r0 < pb)
-            ms_rows<1>(a, r0, pb, lane, carry, mk, s_x, s_rec, s_base, s_sx, s_w, s_c, s_meta, s_avail);
+            ms_rows<1>(a, r0, pb, lane, carry, mk, s_x, s_rec, s_base, s_sx, s_sxw, s_sxwc, s_meta, s_avail);
           lds_order();
           // this level's slots may be staged again: its reads are done
           __hip_atomic_store(&s_cur, pb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -642,8 +680,8 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
             s_rec[s] = r[u];
             s_base[s] = m[u];
             s_sx[s] = sx[u];
-            s_w[s] = w[u];
-            s_c[s] = c[u];
+            s_sxw[s] = sx[u] + w[u];
+            s_sxwc[s] = sx[u] + w[u] + c[u];
             s_meta[s] = mt[u];
           }
         }

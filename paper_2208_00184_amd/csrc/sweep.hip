@@ -586,10 +586,15 @@ __global__ void __launch_bounds__(kSwB) k_ring_sweep(SweepArgs a, int32_t k_lo, 
           // every staging task covering [pa, pb) complete
           const int32_t need = (int32_t)((uint32_t)(REV ? S1 - 1 - pa : pb - 1 - S0) / kStage);
           for (int32_t spin = 0; ready <= need;) {
-            const int32_t f = __hip_atomic_load(&s_flag[ready % kNF], __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_WORKGROUP);
-            if (f == ready) {
-              ready++;
+            // lanes 0..kNF-1 look at the next kNF tasks in one LDS round trip
+            const int32_t tk = ready + lane;
+            const int32_t f = lane < kNF ? __hip_atomic_load(&s_flag[tk % kNF], __ATOMIC_RELAXED,
+                                                             __HIP_MEMORY_SCOPE_WORKGROUP)
+                                         : -1;
+            const uint64_t done = __ballot(lane < kNF && f == tk);
+            const int32_t adv = __builtin_ctzll(~done);  // complete tasks in a row from `ready`
+            if (adv > 0) {
+              ready += adv;
             } else {
               CEL_TCOUNT(3);
               if (++spin == kSpin || aborted()) {
