@@ -400,6 +400,18 @@ __global__ void k_makespan_out(int32_t K, int32_t n, const int32_t *order, const
                                const Status *st);
 __global__ void k_fill_i64(int64_t *p, int64_t n, int64_t v);
 __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v);  // common.hip
+// Maximum of two non-negative int64 values below 2^62 with one v_max_f64:
+// read as IEEE doubles, such bit patterns are finite, non-negative numbers
+// (subnormal below 2^52, which the kernels' f64 denormal mode keeps) whose
+// order is the integers' order, and the maximum returns one operand's bits
+// unchanged.  Every finish time, b-level and t-level is below 2^62 (the
+// overflow check of the inputs).
+__device__ inline int64_t max_nonneg(int64_t a, int64_t b) {
+  int64_t r;
+  asm volatile("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 // Segmented prefix maximum over a wave (makespan.hip, ms_ring.hip).
 // One step of the segmented prefix max: take the value of the lane selected
 // by CTRL when `ok` (that lane lies in the same run); lanes the DPP move does

@@ -174,18 +174,6 @@ __global__ void k_ms_rowmark(int32_t n, const int32_t *lp, const int32_t *gorder
 // ------------------------------------------------------------------ compute
 
 
-// Maximum of two non-negative int64 values below 2^62 with one v_max_f64:
-// read as IEEE doubles, such bit patterns are finite, non-negative numbers
-// (subnormal below 2^52, which the kernels' f64 denormal mode keeps) whose
-// order is the integers' order, and the maximum returns one operand's bits
-// unchanged.  Every finish time is below 2^62 (the overflow check), so every
-// value of the prefix maximum is.
-__device__ inline int64_t max_nonneg(int64_t a, int64_t b) {
-  int64_t r;
-  asm volatile("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-  return r;
-}
-
 // max of m and the first K entries' ring values, as a tree (all non-negative)
 template <int K>
 __device__ inline int64_t ms_near(int64_t m, const uint4 &r, const int64_t *s_x) {
@@ -206,7 +194,17 @@ template <int CTRL, int ROWMASK, int NR>
 __device__ inline void plain_pmax_step(int64_t (&y)[NR]) {
   int64_t u[NR];
 #pragma unroll
-  for (int k = 0; k < NR; k++) u[k] = dpp64<CTRL, ROWMASK>(y[k], 0);
+  for (int k = 0; k < NR; k++) {
+    if constexpr (ROWMASK == 0xF) {
+      // every lane is written (bound_ctrl: 0 where the source lane is out of
+      // the row), so no old value has to be set up
+      const int32_t lo = __builtin_amdgcn_mov_dpp((int32_t)y[k], CTRL, 0xF, 0xF, true);
+      const int32_t hi = __builtin_amdgcn_mov_dpp((int32_t)(y[k] >> 32), CTRL, 0xF, 0xF, true);
+      u[k] = (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+    } else {
+      u[k] = dpp64<CTRL, ROWMASK>(y[k], 0);
+    }
+  }
 #pragma unroll
   for (int k = 0; k < NR; k++) y[k] = max_nonneg(y[k], u[k]);
 }
@@ -231,18 +229,22 @@ __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane,
   uint4 r[NR];
   int64_t y[NR], sx[NR], av[NR], w[NR], c[NR];  // w: sx + w, c: sx + w + c
   int32_t mt[NR];
+  // all staged data in one LDS round trip (the free time's address needs meta)
 #pragma unroll
   for (int u = 0; u < NR; u++) {
     const int s = (r0 + 64 * u + lane) & kMRMask;
+    mt[u] = s_meta[s];
     r[u] = s_rec[s];
     y[u] = s_base[s];
     sx[u] = s_sx[s];
-    mt[u] = s_meta[s];
     w[u] = s_sxw[s];
     c[u] = s_sxwc[s];
   }
+  lds_order();
+  // free times as of the level's start, at a run's first slot (slot 256 of
+  // s_avail always holds 0 for the others)
 #pragma unroll
-  for (int u = 0; u < NR; u++) av[u] = s_avail[mt[u] & 255];  // free times as of the level's start
+  for (int u = 0; u < NR; u++) av[u] = s_avail[(mt[u] >> 16) == 0 ? (mt[u] & 255) : 256];
   uint32_t cls = 0;
 #pragma unroll
   for (int u = 0; u < NR; u++) {
@@ -290,10 +292,8 @@ __device__ inline void ms_rows(const MsArgs &a, int32_t r0, int32_t b, int lane,
 #pragma unroll
   for (int u = 0; u < NR; u++) {
     const int32_t hd = mt[u] >> 16;
-    int64_t v = y[u] - sx[u];
-    v = v < 0 ? 0 : v;
-    if (hd == 0) v = max_nonneg(v, av[u]);  // sx = 0 at a run's first slot
-    y[u] = v;
+    // max(0, ready - sx) = max(ready, sx) - sx; sx = 0 at a run's first slot
+    y[u] = max_nonneg(max_nonneg(y[u], sx[u]) - sx[u], av[u]);
     split |= __ballot(r0 + 64 * u + lane < b && hd < lane) != 0;
   }
   if (!split) {
@@ -351,7 +351,7 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
   __shared__ int64_t s_base[kMRing], s_sx[kMRing];
   __shared__ int64_t s_sxw[kMRing], s_sxwc[kMRing];  // sx + w, sx + w + c
   __shared__ int32_t s_meta[kMRing];
-  __shared__ int64_t s_avail[256];
+  __shared__ int64_t s_avail[257];
   __shared__ int32_t s_flag[kMNF];
   __shared__ int32_t s_next, s_cur, s_nh, s_abort;
   __shared__ int32_t s_hl[kMsB];
@@ -375,7 +375,7 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
     s_sxwc[i] = 0;
     s_meta[i] = 0;
   }
-  for (int i = tid; i < 256; i += kMsB) s_avail[i] = 0;
+  for (int i = tid; i < 257; i += kMsB) s_avail[i] = 0;
   auto aborted = [&]() {
     return __hip_atomic_load(&s_abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) != 0;
   };

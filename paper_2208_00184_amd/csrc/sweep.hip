@@ -336,7 +336,8 @@ __device__ inline uint32_t rec_slot(const uint4 &r, int j) {
 }
 
 // Maximum of m and the first K near neighbours' pull values of a record, as a
-// tree (the gathers are independent; the 64-bit maxima form log2 K + 1 steps).
+// tree (the gathers are independent; the maxima form log2 K + 1 steps).  All
+// pull values are non-negative.
 template <int K>
 __device__ inline int64_t near_max(int64_t m, const uint4 &r, const int64_t *s_x) {
   if constexpr (K == 0) {
@@ -348,8 +349,8 @@ __device__ inline int64_t near_max(int64_t m, const uint4 &r, const int64_t *s_x
 #pragma unroll
     for (int w = 1; w < K; w <<= 1)
 #pragma unroll
-      for (int j = 0; j + w < K; j += 2 * w) g[j] = g[j + w] > g[j] ? g[j + w] : g[j];
-    return g[0] > m ? g[0] : m;
+      for (int j = 0; j + w < K; j += 2 * w) g[j] = max_nonneg(g[j], g[j + w]);
+    return max_nonneg(m, g[0]);
   }
 }
 
