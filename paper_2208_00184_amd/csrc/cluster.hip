@@ -201,7 +201,9 @@ __global__ void __launch_bounds__(64)
 }
 
 // ------------------------------------------------------------ blocked DP
-constexpr int kRing = 8192;  // LDS ring of H over positions (window R + 64 <= 4160)
+constexpr int kRingBig = 8192;  // LDS ring of H over positions (window R + 64 <= 4160)
+constexpr int kRingSmall = 2048;  // the same for R + 64 <= 2048, with room for the in-block table
+constexpr int kTS = 65;  // row stride of the in-block table (int64; odd: rows start in other banks)
 constexpr int kEC = 1024;    // staged edges of one block
 constexpr int kPF = 4;       // prefetched edges per thread of waves 1..NW-1
 constexpr int kMaxW = 15;    // candidate waves
@@ -212,7 +214,8 @@ __device__ inline int64_t rl64(int64_t v, int32_t l) {
   const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int32_t)(v >> 32), l);
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
-__device__ inline int rmod(int32_t p) { return p & (kRing - 1); }
+template <int RING>
+__device__ inline int rmod(int32_t p) { return p & (RING - 1); }
 
 // first k in [0, cnt) with q[k] <= thr (q descending), cnt if none; wave-uniform
 __device__ inline int32_t first_le(const int32_t *q, int32_t cnt, int32_t thr, int lane) {
@@ -399,7 +402,7 @@ __device__ inline int64_t relabel(int64_t key, int32_t s) {
 // descending): add the edge to the lanes above its target, evaluate its
 // segment.  A segment evaluated before its last edge only overestimates.
 // H moves to the next block.  FULL: every target may use every candidate.
-template <bool FULL>
+template <bool FULL, int RING>
 __device__ inline void dp_chunk(int32_t ct, int32_t cb, int32_t base, int32_t lo_t, int32_t *hist,
                                 int64_t *H, const int32_t *Q, const int32_t *T, const int64_t *C,
                                 const int64_t *E, int32_t cnt, int32_t &kk, int64_t &best,
@@ -419,7 +422,7 @@ __device__ inline void dp_chunk(int32_t ct, int32_t cb, int32_t base, int32_t lo
   const int32_t ecnt = hist[lane];
   hist[lane] = 0;
   const int32_t i = ct - lane;
-  const int64_t h = lane < nc ? H[rmod(i)] : 0;
+  const int64_t h = lane < nc ? H[rmod<RING>(i)] : 0;
   int64_t sx = lane < nc ? (int64_t)((uint64_t)h << kIdxBits) + (i - base) : kKeyInf;
   const uint64_t F = __ballot(ecnt > 0) | 1ull;
   wave_segmin(sx, (int32_t)((F >> lane) & 1));
@@ -469,7 +472,7 @@ __device__ inline void dp_chunk(int32_t ct, int32_t cb, int32_t base, int32_t lo
   kk = k1;
   // H(i) for the next block: minus the comm of the block's edges with source >= i
   const int32_t kl = k0 + wave_incl_sum32(ecnt);
-  if (lane < nc) H[rmod(i)] = h - E[kl];
+  if (lane < nc) H[rmod<RING>(i)] = h - E[kl];
 }
 
 // In-block steps, one target at a time: lane t takes candidate j0 + s at step
@@ -506,6 +509,74 @@ __device__ inline void dp_inblock(int64_t &best, int64_t RS, int32_t smin, int32
       }
       nsrc = ke >= 0 ? rl32(qb, ke - kbase) - j0 : 64;
     }
+  }
+}
+
+// In-block table (SMALL kernel): tab[s * kTS + t] = the comm, shifted by
+// kIdxBits, of the block's edges whose source offset is at least s and whose
+// target offset is below t: Int(j0 + s, j0 + t) over sources inside the
+// block, what the in-block step s subtracts for target t.  Built by one wave
+// from the block's in-block edges (the first ein of the list): scatter each
+// edge's comm at (source, target), an exclusive prefix over targets per row
+// (lane = row), then a suffix over rows per column (lane = column).
+__device__ inline void dp_table(int64_t *tab, int32_t j0, int32_t ein, const int32_t *Q,
+                                const int32_t *T, const int64_t *C, int lane) {
+  uint4 *z = reinterpret_cast<uint4 *>(tab);
+  for (int k = lane; k < 64 * kTS / 2; k += 64) z[k] = make_uint4(0, 0, 0, 0);
+  for (int32_t k = lane; k < ein; k += 64)
+    atomicAdd((unsigned long long *)&tab[(Q[k] - j0) * kTS + T[k]],
+              (unsigned long long)C[k] << kIdxBits);
+  // 16 entries at a time: every load of a chunk is issued before the first
+  // use, so the running sum does not wait on one LDS round trip per entry
+  int64_t run = 0;
+  for (int t0 = 0; t0 < 64; t0 += 16) {
+    int64_t a[16];
+#pragma unroll
+    for (int k = 0; k < 16; k++) a[k] = tab[lane * kTS + t0 + k];
+#pragma unroll
+    for (int k = 0; k < 16; k++) {
+      tab[lane * kTS + t0 + k] = run;
+      run += a[k];
+    }
+  }
+  run = 0;
+  for (int s0 = 63; s0 >= 0; s0 -= 16) {
+    int64_t a[16];
+#pragma unroll
+    for (int k = 0; k < 16; k++) a[k] = tab[(s0 - k) * kTS + lane];
+#pragma unroll
+    for (int k = 0; k < 16; k++) {
+      run += a[k];
+      tab[(s0 - k) * kTS + lane] = run;
+    }
+  }
+}
+
+// In-block steps from the table: lane t takes candidate j0 + s at step s (s <
+// t, and j0 + s >= lo when GEN) at its key less tab[s][t].  The steps form
+// one dependent chain through the candidates' keys; the table rows are read
+// eight steps ahead.
+template <bool GEN>
+__device__ inline void dp_inblock_tab(int64_t &best, int32_t smin, const int64_t *tab, int lane) {
+  int32_t lv = lane;
+  asm volatile("" : "+v"(lv));  // keeps the per-step lane tests inside the loop
+  const uint32_t len = (uint32_t)(lv - smin);
+  int64_t row[8], nrow[8];
+#pragma unroll
+  for (int k = 0; k < 8; k++) row[k] = tab[k * kTS + lane];
+#pragma unroll
+  for (int s8 = 0; s8 < 64; s8 += 8) {
+#pragma unroll
+    for (int k = 0; k < 8; k++) nrow[k] = s8 + 8 < 64 ? tab[(s8 + 8 + k) * kTS + lane] : 0;
+#pragma unroll
+    for (int k = 0; k < 8; k++) {
+      const int s = s8 + k;
+      const int64_t kv = relabel(rl64(best, s), s) - row[k];
+      const bool valid = GEN ? ((uint32_t)(s - smin) < len) : (lv > s);
+      if (valid && kv < best) best = kv;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; k++) row[k] = nrow[k];
   }
 }
 
@@ -553,12 +624,18 @@ __device__ inline void dp_inblock_runs(int64_t &best, uint64_t runs, int32_t j0,
 }
 
 // The blocked DP.  blockDim = 64 * NW: wave 0 runs the in-block steps, waves
-// 1..NW-1 the candidates below the block.
+// 1..NW-1 the candidates below the block.  SMALL (R + 64 <= kRingSmall): a
+// smaller ring of H, and blocks whose in-block steps cannot go by runs take
+// them from the in-block table, which wave 0 builds while the candidate waves
+// work.
+template <bool SMALL>
 __global__ void __launch_bounds__(1024)
     k_cluster_dp(int32_t n, int32_t nb, const int32_t *lo, const int32_t *boff, const int32_t *eq,
                  const int32_t *et, const int64_t *ec, const int64_t *eE, const int64_t *PO,
                  int32_t *P, Status *st) {
-  __shared__ int64_t s_h[kRing];
+  constexpr int RING = SMALL ? kRingSmall : kRingBig;
+  __shared__ int64_t s_h[RING];
+  __shared__ __align__(16) int64_t s_tab[SMALL ? 64 * kTS + 1 : 2];
   __shared__ int32_t s_eq[2][kEC];
   __shared__ int32_t s_et[2][kEC];
   __shared__ int64_t s_ec[2][kEC];
@@ -659,6 +736,8 @@ __global__ void __launch_bounds__(1024)
       const int32_t ks = ein - (wave_incl_sum32(sc) - sc);                 // edges with q >= j0 + t
       Nt = E[ks];
       runs = (__ballot(hc > 0) << 1) | 1ull;  // a run starts after each in-block edge target
+      if (SMALL && (lo_hi > j0 || ein > 64 || __popcll(runs) > kMaxRuns))
+        dp_table(s_tab, j0, ein, Q, T, Cc, lane);
     } else {
       // candidates below the block: chunks [ka, kb) of 64, descending
       const int w = wave - 1;
@@ -676,11 +755,11 @@ __global__ void __launch_bounds__(1024)
           for (int32_t ct = top; ct >= bot; ct -= 64) {
             const int32_t cb = ct - 63 > bot ? ct - 63 : bot;
             if (lo_hi <= cb)
-              dp_chunk<true>(ct, cb, base, lo_t, s_hist[w], s_h, Q, T, Cc, E, cnt, kk, best, accS,
-                             lane);
+              dp_chunk<true, RING>(ct, cb, base, lo_t, s_hist[w], s_h, Q, T, Cc, E, cnt, kk, best,
+                                   accS, lane);
             else
-              dp_chunk<false>(ct, cb, base, lo_t, s_hist[w], s_h, Q, T, Cc, E, cnt, kk, best, accS,
-                              lane);
+              dp_chunk<false, RING>(ct, cb, base, lo_t, s_hist[w], s_h, Q, T, Cc, E, cnt, kk, best,
+                                    accS, lane);
           }
         }
       }
@@ -710,7 +789,17 @@ __global__ void __launch_bounds__(1024)
       }
       const int32_t smin = lo_t - j0 > 0 ? lo_t - j0 : 0;
       CEL_TSTAMP(tq0);
-      if (lo_hi > j0) {
+      if (SMALL && lo_hi > j0) {
+        dp_inblock_tab<true>(best, smin, s_tab, lane);
+        CEL_TSTAMP(tq1);
+        CEL_TADD(14, tq0, tq1);
+        CEL_TCOUNT(15);
+      } else if (SMALL && (ein > 64 || __popcll(runs) > kMaxRuns)) {
+        dp_inblock_tab<false>(best, smin, s_tab, lane);
+        CEL_TSTAMP(tq1);
+        CEL_TADD(18, tq0, tq1);
+        CEL_TCOUNT(19);
+      } else if (lo_hi > j0) {
         dp_inblock<true>(best, XS, smin, j0, ein, Q, T, Cc, lane);
         CEL_TSTAMP(tq1);
         CEL_TADD(14, tq0, tq1);
@@ -728,7 +817,7 @@ __global__ void __launch_bounds__(1024)
       }
       const int64_t G = best >> kIdxBits;
       if (j >= 1 && j <= n) P[j] = (int32_t)(best & kIdxMask) + base;
-      if (j < n) s_h[rmod(j)] = G - Nt;
+      if (j < n) s_h[rmod<RING>(j)] = G - Nt;
       if (j == n) st->s0 = PO[n] + G;
     } else if (more) {
       // stage block b + 1
@@ -871,7 +960,10 @@ static int dp_blocked(int32_t n, int32_t m, int32_t R, const int32_t *lo, const 
   const int NW = 1 + (K < kMaxW ? K : kMaxW);
   {
     KTimer kt(s, "k_cluster_dp");
-    k_cluster_dp<<<1, 64 * NW, 0, s>>>(n, nb, lo, boff, eq, et, ec, eE, PO, P, st);
+    if (R + 64 <= kRingSmall)
+      k_cluster_dp<true><<<1, 64 * NW, 0, s>>>(n, nb, lo, boff, eq, et, ec, eE, PO, P, st);
+    else
+      k_cluster_dp<false><<<1, 64 * NW, 0, s>>>(n, nb, lo, boff, eq, et, ec, eE, PO, P, st);
   }
   CEL_HIP(hipGetLastError());
   *done = true;
