@@ -65,13 +65,13 @@ TRAFFIC_FILES = [os.path.join(ROOT, "profiles", f) for f in
 CSRC = os.path.join(ROOT, "paper_2208_00184_amd", "csrc")
 # kernels the bench names, their symbols in rocprofv3 output and their sources
 PMC_KERNELS = {
-    "k_makespan_one": ("cel::k_makespan_one<", ["makespan.hip", "cel_internal.h"]),
-    "k_blevel_sweep": ("cel::k_level_sweep<true>", ["blevel.hip", "cel_internal.h"]),
-    "k_tlevel_sweep": ("cel::k_level_sweep<false>", ["blevel.hip", "cel_internal.h"]),
+    "k_makespan_one": ("cel::k_ms_ring(", ["ms_ring.hip", "cel_internal.h"]),
+    "k_blevel_sweep": ("cel::k_ring_sweep<true>", ["sweep.hip", "cel_internal.h"]),
+    "k_tlevel_sweep": ("cel::k_ring_sweep<false>", ["sweep.hip", "cel_internal.h"]),
     "k_makespan_batch": ("cel::k_makespan_sweep<256, 1024, 4096>", ["makespan.hip", "cel_internal.h"]),
     "k_makespan_batch_wide": ("cel::k_makespan_levels<", ["makespan.hip", "cel_internal.h"]),
     "k_kahn": ("cel::k_kahn(", ["topo.hip", "cel_internal.h"]),
-    "k_cluster_dp": ("cel::k_cluster_dp(", ["cluster.hip", "cel_internal.h"]),
+    "k_cluster_dp": ("cel::k_cluster_dp<true>(", ["cluster.hip", "cel_internal.h"]),
     "k_place": ("cel::k_place<", ["place.hip", "cel_internal.h"]),
 }
 
@@ -134,6 +134,23 @@ def stats_summary(stats_csv: str, top: int = 40) -> str:
     rows.sort(key=lambda x: -x[2])
     out = ["| kernel | calls | total ms | avg us |", "|---|---:|---:|---:|"]
     out += [f"| {n} | {c} | {t:.3f} | {a:.1f} |" for n, c, t, a in rows[:top]]
+    return "\n".join(out)
+
+
+def trace_kernel(trace_csv: str, name: str, top: int = 12) -> str:
+    """Dispatch durations of one kernel from a rocprofv3 kernel_trace CSV,
+    largest first (a run mixes graphs of several sizes; the largest
+    dispatches are the transformer-96 ones)."""
+    import csv
+    durs = []
+    with open(trace_csv) as fh:
+        for r in csv.DictReader(fh):
+            if r["Kernel_Name"].removeprefix("void ").startswith(name):
+                durs.append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6)
+    durs.sort(reverse=True)
+    head = durs[:top]
+    out = [f"{name}: {len(durs)} dispatches; the {len(head)} largest (ms): " +
+           ", ".join(f"{d:.3f}" for d in head)]
     return "\n".join(out)
 
 
@@ -440,9 +457,15 @@ def main() -> int:
                     help="restrict --pmc-summary to these kernels")
     ap.add_argument("--stats-summary", metavar="CSV",
                     help="print a rocprofv3 --stats kernel_stats CSV as a table and exit")
+    ap.add_argument("--trace-kernel", nargs=3, metavar=("CSV", "NAME", "TOP"),
+                    help="print the TOP largest dispatch durations of kernel NAME from a "
+                         "rocprofv3 kernel_trace CSV and exit")
     args = ap.parse_args()
     if args.stats_summary:
         print(stats_summary(args.stats_summary))
+        return 0
+    if args.trace_kernel:
+        print(trace_kernel(args.trace_kernel[0], args.trace_kernel[1], int(args.trace_kernel[2])))
         return 0
     if args.pmc_summary:
         if len(args.pmc_summary) < 2 or args.calib_copy <= 0:
