@@ -462,15 +462,11 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
         for (int32_t i = 0; i < nh; i++) {  // rows of many predecessors: the whole block
           const int32_t t2 = s_hl[i];
           const int32_t p2 = p0 + t2;
-          // every predecessor was stored before an earlier full barrier:
-          // visible, so a negative value would mean a broken invariant
+          // predecessors stored by other waves before a barrier: a barrier
+          // does not wait for those stores, so one still in flight is read again
           const int64_t mx = heavy_max<kHeavyU, kMsB>(
               a.pptr[p2], a.pptr[p2 + 1], tid, [&](int32_t e) { return (int32_t)e; },
-              [&](int32_t e) {
-                const int64_t v = ld_coherent(ms_src(a, a.tidx[e]));
-                if (v < 0) raise_err(st, EB_WAIT);
-                return v;
-              });
+              [&](int32_t e) { return ld_final(ms_src(a, a.tidx[e]), &s_abort, st); });
           if (lane == 0) s_red[wave] = mx;
           lds_barrier();
           if (tid == 0) {
@@ -694,6 +690,9 @@ __global__ void __launch_bounds__(kMsB) k_ms_ring(MsArgs a, Status *st) {
     __syncthreads();  // the segment is done: every value in the ring
     // values whose slots were never taken over: the segment's last kMRing
     ms_flush(a, S1 - kMRing > S0 ? S1 - kMRing : S0, S1, tid, kMsB, s_x);
+    // the stores reach L2 before the next segment's barrier (a barrier alone
+    // does not wait for them; readers re-read a value not yet there anyway)
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   }
   for (int off = 32; off > 0; off >>= 1) {
     const int64_t o = __shfl_xor((long long)mk, off);

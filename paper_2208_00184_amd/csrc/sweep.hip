@@ -535,15 +535,11 @@ __global__ void __launch_bounds__(kSwB) k_ring_sweep(SweepArgs a, int32_t k_lo, 
         const int32_t nh = s_nh;
         for (int32_t i = 0; i < nh; i++) {  // nodes of many neighbours: the whole block
           const int32_t p2 = s_hl[i];
-          // every neighbour was stored before an earlier barrier: visible, so
-          // a negative value would mean a broken invariant
+          // neighbours stored by other waves before a barrier: a barrier does
+          // not wait for those stores, so one still in flight is read again
           const int64_t mx = heavy_max<kHeavyU, kSwB>(
               a.rptr[p2], a.rptr[p2 + 1], tid, [&](int32_t e) { return a.ridx[e]; },
-              [&](int32_t qq) {
-                const int64_t v = ld_coherent(&a.gx[qq]);
-                if (v < 0) raise_err(st, EB_WAIT);
-                return v;
-              });
+              [&](int32_t qq) { return ld_final(&a.gx[qq], &s_abort, st); });
           if (lane == 0) s_red[wave] = mx;
           __syncthreads();
           if (tid == 0) {
@@ -753,6 +749,9 @@ __global__ void __launch_bounds__(kSwB) k_ring_sweep(SweepArgs a, int32_t k_lo, 
     // segment's lowest kRing positions; forward: its highest)
     if (REV) flush_ring<REV>(a, S0, S1 < S0 + kRing ? S1 : S0 + kRing, tid, kSwB, s_x, s_cst);
     else flush_ring<REV>(a, S1 - kRing > S0 ? S1 - kRing : S0, S1, tid, kSwB, s_x, s_cst);
+    // the stores reach L2 before the next segment's barrier (a barrier alone
+    // does not wait for them; readers re-read a value not yet there anyway)
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   }
 }
 
