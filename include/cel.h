@@ -256,7 +256,7 @@ int cel_makespan(const cel_graph *g, const cel_devices *d, const int32_t *order,
  * fixed array of CEL_NOALLOC_SCRATCH_BYTES per GPU, created with the
  * library's code object on that GPU and held until the process ends; it keeps
  * the last call's contents (each call clears what it needs).  Inputs whose
- * scratch bound, 65536 + 200 (n + 1) + 16 m + 9 K n bytes, exceeds that size
+ * scratch bound, 65536 + 200 (n + 1) + 16 m + 21 K n bytes, exceeds that size
  * are rejected with CEL_E_ARG before any work is queued (about 870k nodes
  * with m = 2n at K = 1; 32 placements of a 200k-node graph).  Calls
  * through this entry point take turns on a process-wide lock and return

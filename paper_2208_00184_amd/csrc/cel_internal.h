@@ -510,6 +510,13 @@ int sweep_run(SweepPlan &pl, hipStream_t s, Status *st, const char *timer);
 __global__ void k_sw_segflag(int32_t L, const int32_t *wide, int32_t *flag, const Status *st);
 __global__ void k_sw_segfill(int32_t L, const int32_t *flag, const int32_t *pre, int32_t *seg,
                              int32_t *segid, int32_t *nseg, const Status *st);
+// ms_batch.hip: makespans of K placements over the priority order (positions:
+// lp, pptr/pidx, wp, cq by position; devp [K][n]); fin and fc [K][n] each
+// (fin, fin + c), makespan [K]
+int mb_ring(int32_t K, int32_t n, int32_t m, int32_t L, const int32_t *lp, const int32_t *order,
+            const int32_t *level, const int32_t *pptr, const int32_t *pidx, const int64_t *wp,
+            const int64_t *cq, const uint8_t *devp, int64_t *fin, int64_t *fc, int64_t *makespan,
+            class Scratch &sc, hipStream_t s, Status *st);
 // ms_ring.hip: finish times of one placement over the device-grouped order
 // (slots), levels run by one wave from an LDS ring; finp holds 2n int64 (the
 // finish times, then finish + c), makespan one

@@ -831,7 +831,7 @@ static int makespan_impl(const char *fn, const cel_graph *g, const cel_devices *
   CEL_TRY(sc.get(&wp, n));
   CEL_TRY(sc.get(&cq, n));
   CEL_TRY(sc.get(&devp, (int64_t)K * n));
-  CEL_TRY(sc.get(&finp, (K == 1 ? 2 : (int64_t)K) * n));  // K = 1: fin, then fin + c
+  CEL_TRY(sc.get(&finp, 2 * (int64_t)K * n));  // fin, then fin + c (the ring sweeps)
   const int gx = grid_for(n, 256, 1024);
   if (K == 1) {
     // Device-grouped order: inside each level, nodes sorted by (device,
@@ -884,10 +884,8 @@ static int makespan_impl(const char *fn, const cel_graph *g, const cel_devices *
       k_makespan_levels<512, 1, 3><<<(unsigned)K, 512, 0, s>>>(n, L, dbits, level_ptr, pptr, pidx,
                                                               wp, cq, devp, finp, makespan, st);
     } else if (K <= kBatchWide) {
-      KTimer kt(s, "k_makespan_batch");
-      k_makespan_sweep<256, 1024, 4096><<<(unsigned)K, 256, 0, s>>>(n, L, dbits, level_ptr, pptr,
-                                                                    pidx, wp, cq, devp, finp,
-                                                                    makespan, st);
+      CEL_TRY(mb_ring(K, n, g->m, L, level_ptr, order, level, pptr, pidx, wp, cq, devp, finp,
+                      finp + (int64_t)K * n, makespan, sc, s, st));
     } else {
       // more placements than CUs: small windows (about 35 KB of LDS) so that
       // several placements share a CU and hide each other's memory latency
@@ -951,10 +949,10 @@ static int fixed_scratch(char **out) {  // g_fixed_mu held
 // buffers, per-level tile lists, and for K = 1 the ring sweep's pull records,
 // list offsets, level and segment tables and the second finish array), 16
 // bytes per edge (relabelled in-edges; for K = 1 tagged, far and long lists),
-// 9 bytes per node and placement (devices and finish times), and 64 KiB for
-// block partials and 256-byte rounding.
+// 21 bytes per node and placement (devices, finish times, finish + c, level
+// information), and 64 KiB for block partials and 256-byte rounding.
 static uint64_t makespan_scratch_bound(int64_t n, int64_t m, int64_t K) {
-  return 65536ull + 200ull * (uint64_t)(n + 1) + 16ull * (uint64_t)m + 9ull * (uint64_t)K * (uint64_t)n;
+  return 65536ull + 200ull * (uint64_t)(n + 1) + 16ull * (uint64_t)m + 21ull * (uint64_t)K * (uint64_t)n;
 }
 
 extern "C" int cel_makespan_noalloc(const cel_graph *g, const cel_devices *d, const int32_t *order,

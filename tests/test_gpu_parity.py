@@ -310,6 +310,46 @@ def test_makespan_one_run_boundaries():
     assert np.array_equal(np_(st)[0], ref_st[0]) and np.array_equal(np_(fi)[0], ref_fi[0])
 
 
+def test_makespan_batch_level_paths():
+    """K > 1 over the priority order: the run-boundary DAG under four
+    placements at once: the levels' device runs as sized (several devices per
+    row), everything on one device (one-device levels of up to four rows),
+    one device per level (chains continue through free times across
+    levels), and uniform random devices."""
+    rng = np.random.default_rng(23)
+    runs = [[64, 64], [1, 127], [127, 1], [128], [63, 65], [65, 63], [200], [64, 64, 64],
+            [30, 34, 64, 2], [256], [17], [64], [129], [1, 1, 1, 61, 64], [192, 64]] * 4
+    widths = [sum(r) for r in runs]
+    starts = np.concatenate([[0], np.cumsum(widths)])
+    n = int(starts[-1])
+    D = 6
+    edges = []
+    for li in range(1, len(runs)):
+        for v in range(int(starts[li]), int(starts[li + 1])):
+            edges.append((int(rng.integers(starts[li - 1], starts[li])), v))
+            for u in rng.integers(0, starts[li], int(rng.integers(0, 4))):
+                edges.append((int(u), v))
+    edges = sorted(set(edges))
+    wl = from_edges(n, edges, rng.integers(1, 5000, n), rng.integers(0, 1 << 20, n), D,
+                    np.full(D, 1 << 40), 7, 300, name="batch-paths")
+    lev, oid, lp, L = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    P = np.zeros((4, n), np.uint8)
+    for li in range(L):
+        nodes = np.asarray(pr[lp[li]:lp[li + 1]])
+        devs = np.sort(rng.choice(D, len(runs[li]), replace=False))
+        P[0, nodes] = np.repeat(devs, runs[li])  # sized runs, in priority order
+        P[2, nodes] = li % D
+    P[1, :] = 3
+    P[3] = rng.integers(0, D, n)
+    ref_ms, ref_st, ref_fi = O.makespan(wl, pr, P)
+    g, d = up(wl)
+    ms, st, fi = cel.makespan(g, d, tt(pr, np.int32), tt(lev, np.int32), tt(lp, np.int32), L,
+                              tt(P, np.uint8), want_times=True)
+    assert np.array_equal(np_(ms), ref_ms)
+    assert np.array_equal(np_(st), ref_st) and np.array_equal(np_(fi), ref_fi)
+
+
 def test_makespan_wide_no_edges_batch():
     """Sources only: one level of 3,000 isolated nodes, 4 placements."""
     n, D = 3000, 5

@@ -66,7 +66,7 @@ def test_noalloc_matches_makespan_on_shrinking_calls(cases):
 def test_noalloc_rejects_inputs_above_its_scratch():
     wl = make_config(1, 0)
     g, d, args, _, _ = prepared(wl, 1, 0)
-    K = 8000  # bound 65536 + 200 (n + 1) + 16 m + 9 K n > 128 MiB at n = 2048
+    K = 8000  # bound 65536 + 200 (n + 1) + 16 m + 21 K n > 128 MiB at n = 2048
     P = torch.zeros((K, wl.n), dtype=torch.uint8, device=DEV)
     with pytest.raises(cel.CelError) as ei:
         cel.makespan(g, d, *args, P, noalloc=True)
