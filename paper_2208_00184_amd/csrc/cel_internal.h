@@ -517,6 +517,14 @@ int mb_ring(int32_t K, int32_t n, int32_t m, int32_t L, const int32_t *lp, const
             const int32_t *level, const int32_t *pptr, const int32_t *pidx, const int64_t *wp,
             const int64_t *cq, const uint8_t *devp, int64_t *fin, int64_t *fc, int64_t *makespan,
             class Scratch &sc, hipStream_t s, Status *st);
+// ms_wide.hip: makespans of K placements over a level-grouped priority order
+// whose levels are wide (positions as for mb_ring; 1 <= D <= kWDev,
+// n <= kWMaxN); fin [K][n], makespan [K]
+constexpr int kWDev = 16;
+constexpr int32_t kWMaxN = 1 << 27;
+int mw_batch(int32_t K, int32_t n, int32_t L, int32_t D, const int32_t *lp, const int32_t *pptr,
+             const int32_t *pidx, const int64_t *wp, const int64_t *cq, const uint8_t *devp,
+             int64_t *fin, int64_t *makespan, class Scratch &sc, hipStream_t s, Status *st);
 // ms_ring.hip: finish times of one placement over the device-grouped order
 // (slots), levels run by one wave from an LDS ring; finp holds 2n int64 (the
 // finish times, then finish + c), makespan one

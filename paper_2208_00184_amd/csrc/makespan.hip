@@ -42,6 +42,64 @@ __global__ void k_dev_gather(int32_t K, int32_t n, const int32_t *order, const u
   if (bad) raise_err(st, bad);
 }
 
+// The same gather for a batch: one workgroup per placement stages the
+// devices of up to kGRowNodes nodes at a time in LDS (read once, coalesced)
+// and serves the positions whose node lies in that range from there; a
+// direct gather would move one cache line per byte.
+constexpr int kGRowB = 1024;
+constexpr int kGRowNodes = 131072;
+template <bool VEC>
+__global__ void __launch_bounds__(kGRowB) k_dev_rows(int32_t n, const int32_t *order,
+                                                     const uint8_t *node_dev, int32_t D,
+                                                     uint8_t *devp, Status *st) {
+  __shared__ uint32_t s_dev4[kGRowNodes / 4];
+  uint8_t *s_dev = (uint8_t *)s_dev4;
+  if (failed(st)) return;
+  const int64_t koff = (int64_t)blockIdx.x * n;
+  const uint8_t *row = node_dev + koff;
+  uint8_t *out = devp + koff;
+  uint32_t bad = 0;
+  for (int32_t v0 = 0; v0 < n; v0 += kGRowNodes) {
+    const int32_t cnt = n - v0 < kGRowNodes ? n - v0 : kGRowNodes;
+    if (VEC) {  // n, the row and order aligned: words of 4 devices, quads of positions
+      const uint32_t *row4 = (const uint32_t *)(row + v0);
+#pragma unroll 4
+      for (int32_t i = threadIdx.x; i < (cnt >> 2); i += kGRowB) {
+        const uint32_t w = row4[i];
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+          if ((int32_t)((w >> (8 * j)) & 255u) >= D) bad |= EB_ARG;
+        s_dev4[i] = w;
+      }
+      __syncthreads();
+      const int4 *order4 = (const int4 *)order;
+#pragma unroll 2
+      for (int32_t i = threadIdx.x; i < (n >> 2); i += kGRowB) {
+        const int4 o = order4[i];
+        const int32_t v[4] = {o.x - v0, o.y - v0, o.z - v0, o.w - v0};
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+          if ((uint32_t)v[j] < (uint32_t)cnt) out[4 * i + j] = s_dev[v[j]];
+      }
+    } else {
+#pragma unroll 4
+      for (int32_t i = threadIdx.x; i < cnt; i += kGRowB) {
+        const uint8_t dv = row[v0 + i];
+        if (dv >= D) bad |= EB_ARG;
+        s_dev[i] = dv;
+      }
+      __syncthreads();
+#pragma unroll 4
+      for (int32_t p = threadIdx.x; p < n; p += kGRowB) {
+        const int32_t v = order[p] - v0;
+        if ((uint32_t)v < (uint32_t)cnt) out[p] = s_dev[v];
+      }
+    }
+    __syncthreads();
+  }
+  if (bad) raise_err(st, bad);
+}
+
 __global__ void k_pos_costs(int32_t n, const int32_t *order, const int64_t *w, const int64_t *ob,
                             int64_t bw, int64_t lat, int64_t *wp, int64_t *cq, const Status *st) {
   if (failed(st)) return;
@@ -872,14 +930,24 @@ static int makespan_impl(const char *fn, const cel_graph *g, const cel_devices *
     k_pos_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, g->w, g->ob, d->bw, d->lat, wp,
                                                       cq, st);
     {
-      const int gy = K < 1024 ? K : 1024;
       KTimer kt(s, "k_dev_gather");
-      k_dev_gather<<<dim3(gx, gy), 256, 0, s>>>(K, n, order, node_dev, d->D, devp, st);
+      if (K >= 64) {
+        const bool vec = (n & 3) == 0 && ((uintptr_t)order & 15) == 0 &&
+                         ((uintptr_t)node_dev & 3) == 0;
+        if (vec) k_dev_rows<true><<<(unsigned)K, kGRowB, 0, s>>>(n, order, node_dev, d->D, devp, st);
+        else k_dev_rows<false><<<(unsigned)K, kGRowB, 0, s>>>(n, order, node_dev, d->D, devp, st);
+      } else {
+        const int gy = K < 1024 ? K : 1024;
+        k_dev_gather<<<dim3(gx, gy), 256, 0, s>>>(K, n, order, node_dev, d->D, devp, st);
+      }
     }
     const bool wide = (int64_t)n >= (int64_t)kWideLevels * L;  // gathers from global memory
     int dbits = 0;  // bits of the largest device id
     while ((1 << dbits) < d->D) dbits++;
-    if (wide) {
+    if (wide && d->D <= kWDev && n <= kWMaxN) {
+      CEL_TRY(mw_batch(K, n, L, d->D, level_ptr, pptr, pidx, wp, cq, devp, finp, makespan, sc, s,
+                       st));
+    } else if (wide) {
       KTimer kt(s, "k_makespan_batch");
       k_makespan_levels<512, 1, 3><<<(unsigned)K, 512, 0, s>>>(n, L, dbits, level_ptr, pptr, pidx,
                                                               wp, cq, devp, finp, makespan, st);

@@ -370,6 +370,42 @@ def test_makespan_wide_no_edges_batch():
                      tt(P, np.uint8))
 
 
+def test_makespan_batch_rows_gather():
+    """Batches of 64 and more placements stage each placement's devices in LDS
+    before ordering them by position: 80 rows of a 3,000-node DAG (more nodes
+    than one staging pass on a second graph of 140,000 isolated nodes; node
+    counts that are and are not multiples of 4), and a device id out of range
+    is rejected there too."""
+    wl = make_random_dag(77, 3001, p_edge=0.002, D=6)
+    lev, oid, lp, L = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    P = random_placements(wl, 80, 3)
+    ref_ms, _, ref_fi = O.makespan(wl, pr, P)
+    g, d = up(wl)
+    args = (tt(pr, np.int32), tt(lev, np.int32), tt(lp, np.int32), L)
+    ms, _, fi = cel.makespan(g, d, *args, tt(P, np.uint8), want_times=True)
+    assert np.array_equal(np_(ms), ref_ms) and np.array_equal(np_(fi), ref_fi)
+    P[77, 2999] = 6
+    with pytest.raises(cel.CelError):
+        cel.makespan(g, d, *args, tt(P, np.uint8))
+    n, D = 140000, 3
+    rng = np.random.default_rng(8)
+    wl2 = from_edges(n, [], rng.integers(1, 100, n), rng.integers(0, 1000, n), D,
+                     np.full(D, 1 << 40), 3, 10)
+    lev2, oid2, lp2, L2 = O.topo_levels(wl2)
+    _, _, pr2, _ = O.blevel(wl2, lev2, oid2)
+    P2 = random_placements(wl2, 64, 4)
+    ref2, _, _ = O.makespan(wl2, pr2, P2, want_times=False)
+    g2, d2 = up(wl2)
+    ms2, _, _ = cel.makespan(g2, d2, tt(pr2, np.int32), tt(lev2, np.int32), tt(lp2, np.int32),
+                             L2, tt(P2, np.uint8))
+    assert np.array_equal(np_(ms2), ref2)
+    P2[63, 139999] = 200
+    with pytest.raises(cel.CelError):
+        cel.makespan(g2, d2, tt(pr2, np.int32), tt(lev2, np.int32), tt(lp2, np.int32), L2,
+                     tt(P2, np.uint8))
+
+
 # ---------------------------------------------------------- random small DAGs
 
 
