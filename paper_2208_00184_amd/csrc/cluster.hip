@@ -860,32 +860,94 @@ __global__ void __launch_bounds__(1024)
   }
 }
 
-// breakpoints: follow P from n down to 0, flagging cluster starts
-__global__ void k_backtrack(int32_t n, const int32_t *P, int32_t *flag, Status *st) {
+// Cluster starts by following a chain of positions: the DP's backtrack from
+// n down through P (P[j] < j, at least j - R), or the greedy walk from 0 up
+// through gend (gend[s] > s, at most s + R), flagging every start.  The chain
+// is sequential, so one thread walks it, but through LDS: the table is staged
+// in windows of kWalkWin positions, the next window loaded by waves 1-15 (all
+// their loads in flight at once) while thread 0 walks the current one (a
+// step moves at most R <= 4096 positions, so it never skips a window).
+constexpr int kWalkWin = 16384;
+constexpr int kWalkB = 1024;
+constexpr int kWalkPer = (kWalkWin + kWalkB - 64 - 1) / (kWalkB - 64);  // loads per loading thread
+static_assert(kWalkWin > 4096, "a step of at most R = 4096 positions stays in the next window");
+template <bool DOWN>
+__global__ void __launch_bounds__(kWalkB) k_walk(int32_t n, const int32_t *next, int32_t *flag,
+                                                 Status *st) {
+  __shared__ int32_t s_w[2][kWalkWin];
+  __shared__ int32_t s_done[2];  // by window parity: a slow wave may still read the last one
   if (failed(st)) return;
-  int32_t b = n, C = 0;
-  while (b > 0) {
-    const int32_t a = P[b];
-    if (a < 0 || a >= b) {  // cannot happen: every step has a feasible predecessor
-      raise_err(st, EB_ORDER);
-      return;
+  const int tid = threadIdx.x;
+  // entries of the table: DOWN: next[0..n] (next[0] unused), UP: next[0..n-1]
+  const int32_t ne = DOWN ? n + 1 : n;
+  // window w covers [wlo, wlo + kWalkWin) clipped to [0, ne)
+  auto wstart = [&](int32_t w) -> int32_t {
+    return DOWN ? ne - (w + 1) * kWalkWin : w * kWalkWin;  // may be negative when DOWN
+  };
+  auto load = [&](int buf, int32_t w, int t0, int nt) {
+    const int32_t lo = wstart(w);
+    for (int32_t i0 = t0; i0 < kWalkWin; i0 += nt * kWalkPer) {
+      int32_t v[kWalkPer];
+#pragma unroll
+      for (int u = 0; u < kWalkPer; u++) {
+        const int32_t x = lo + i0 + u * nt;
+        v[u] = (x >= 0 && x < ne && i0 + u * nt < kWalkWin) ? next[x] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < kWalkPer; u++)
+        if (i0 + u * nt < kWalkWin) s_w[buf][i0 + u * nt] = v[u];
     }
-    b = a;
-    flag[b] = 1;
-    C++;
+  };
+  if (tid == 0) s_done[0] = s_done[1] = 0;
+  load(0, 0, tid, kWalkB);
+  __syncthreads();
+  int32_t b = DOWN ? n : 0, C = 0;  // thread 0's walk
+  for (int32_t w = 0;; w++) {
+    const int buf = w & 1;
+    int32_t &done = s_done[buf];
+    if (tid >= 64) load(buf ^ 1, w + 1, tid - 64, kWalkB - 64);
+    if (tid == 0) {
+      const int32_t lo = wstart(w);
+      bool moved = false;
+      if (DOWN) {
+        while (b > 0 && b >= lo) {
+          const int32_t a = s_w[buf][b - lo];
+          if (a < 0 || a >= b) {  // cannot happen: every step has a feasible predecessor
+            raise_err(st, EB_ORDER);
+            done = 1;
+            break;
+          }
+          b = a;
+          flag[b] = 1;
+          C++;
+          moved = true;
+        }
+        if (b == 0) done = 1;
+      } else {
+        while (b < n && b < lo + kWalkWin) {
+          flag[b] = 1;
+          C++;
+          const int32_t e = s_w[buf][b - lo];
+          if (e <= b || e > n) {
+            raise_err(st, EB_ORDER);
+            done = 1;
+            break;
+          }
+          b = e;
+          moved = true;
+        }
+        if (b >= n) done = 1;
+      }
+      // a chain that neither ends nor reaches this window (a corrupt table)
+      if (!moved && !done) {
+        raise_err(st, EB_ORDER);
+        done = 1;
+      }
+      if (done) st->i0 = C;
+    }
+    __syncthreads();
+    if (done) break;
   }
-  st->i0 = C;
-}
-
-__global__ void k_greedy_walk(int32_t n, const int32_t *gend, int32_t *flag, Status *st) {
-  if (failed(st)) return;
-  int32_t s = 0, C = 0;
-  while (s < n) {
-    flag[s] = 1;
-    C++;
-    s = gend[s];
-  }
-  st->i0 = C;
 }
 
 // cluster_id[order[p]] = (number of cluster starts at or before p) - 1
@@ -1044,9 +1106,9 @@ extern "C" int cel_cluster(const cel_graph *g, const cel_devices *d, const int32
     else if (R <= 1024) launch_dp<16>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
     else if (R <= 2048) launch_dp<32>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
     else launch_dp<64>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
-    k_backtrack<<<1, 1, 0, s>>>(n, P, flag, st);
+    k_walk<true><<<1, kWalkB, 0, s>>>(n, P, flag, st);
   } else {
-    k_greedy_walk<<<1, 1, 0, s>>>(n, gend, flag, st);
+    k_walk<false><<<1, kWalkB, 0, s>>>(n, gend, flag, st);
   }
   CEL_TRY(exclusive_scan_i32(flag, incl, n, sc, s));
   k_label<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, incl, cluster_id, st);
