@@ -206,7 +206,7 @@ constexpr int kRingSmall = 2048;  // the same for R + 64 <= 2048, with room for 
 constexpr int kTS = 65;  // row stride of the in-block table (int64; odd: rows start in other banks)
 constexpr int kEC = 1024;    // staged edges of one block
 constexpr int kPF = 4;       // prefetched edges per thread of waves 1..NW-1
-constexpr int kMaxW = 15;    // candidate waves
+constexpr int kMaxW = 15;    // candidate waves (with wave 0: 16 values in the minimum tree)
 
 __device__ inline int32_t rl32(int32_t v, int32_t l) { return __builtin_amdgcn_readlane(v, l); }
 __device__ inline int64_t rl64(int64_t v, int32_t l) {
@@ -665,6 +665,10 @@ __global__ void __launch_bounds__(1024)
     if (tid < 64) s_lo[0][tid] = tid == 0 ? 0 : lo[tid <= n ? tid : n];
     for (int k = tid; k < (kMaxW + 1) * 64; k += blockDim.x) (&s_hist[0][0])[k] = 0;
     if (tid < 64) s_hc[tid] = 0;
+    for (int k = W * 64 + tid; k < kMaxW * 64; k += blockDim.x) {  // rows of absent waves
+      (&s_wb[0][0])[k] = kKeyInf;
+      (&s_wa[0][0])[k] = 0;
+    }
   }
 
 #ifdef CEL_PHASE_TIMERS
@@ -782,13 +786,30 @@ __global__ void __launch_bounds__(1024)
       const int32_t j = j0 + lane;
       int64_t best = j == 0 ? (int64_t)kBaseOff : kKeyInf;  // S(0) = 0
       int64_t off = XS;
-      for (int w = 0; w < W; w++) {
-        const int64_t kv = s_wb[w][lane] - off;
-        best = kv < best ? kv : best;
-        off += s_wa[w][lane];
+      // every wave's results read at once (rows past W: kKeyInf and 0)
+      int64_t wb[kMaxW], wa[kMaxW];
+#pragma unroll
+      for (int w = 0; w < kMaxW; w++) {
+        wb[w] = s_wb[w][lane];
+        wa[w] = s_wa[w][lane];
       }
+      // key of wave w's best relative to the offset of the waves above it: a
+      // prefix sum of the offsets, then a minimum tree
+      int64_t kv[16];
+#pragma unroll
+      for (int w = 0; w < kMaxW; w++) {
+        kv[w] = wb[w] - off;  // rows past W: kKeyInf - off, above every real key
+        off += wa[w];
+      }
+      kv[15] = best;
+#pragma unroll
+      for (int h = 8; h > 0; h >>= 1)
+#pragma unroll
+        for (int w = 0; w < h; w++) kv[w] = kv[w + h] < kv[w] ? kv[w + h] : kv[w];
+      best = kv[0];
       const int32_t smin = lo_t - j0 > 0 ? lo_t - j0 : 0;
       CEL_TSTAMP(tq0);
+      CEL_TADD(20, tp_b, tq0);
       if (SMALL && lo_hi > j0) {
         dp_inblock_tab<true>(best, smin, s_tab, lane);
         CEL_TSTAMP(tq1);
