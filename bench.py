@@ -68,8 +68,8 @@ PMC_KERNELS = {
     "k_makespan_one": ("cel::k_ms_ring(", ["ms_ring.hip", "cel_internal.h"]),
     "k_blevel_sweep": ("cel::k_ring_sweep<true>", ["sweep.hip", "cel_internal.h"]),
     "k_tlevel_sweep": ("cel::k_ring_sweep<false>", ["sweep.hip", "cel_internal.h"]),
-    "k_makespan_batch": ("cel::k_makespan_sweep<256, 1024, 4096>", ["makespan.hip", "cel_internal.h"]),
-    "k_makespan_batch_wide": ("cel::k_makespan_levels<", ["makespan.hip", "cel_internal.h"]),
+    "k_makespan_batch": ("cel::k_mb_ring(", ["ms_batch.hip", "cel_internal.h"]),
+    "k_makespan_batch_wide": ("cel::(anonymous namespace)::k_mw_batch(", ["ms_wide.hip", "cel_internal.h"]),
     "k_kahn": ("cel::k_kahn(", ["topo.hip", "cel_internal.h"]),
     "k_cluster_dp": ("cel::k_cluster_dp<true>(", ["cluster.hip", "cel_internal.h"]),
     "k_place": ("cel::k_place<", ["place.hip", "cel_internal.h"]),

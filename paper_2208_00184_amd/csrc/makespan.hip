@@ -931,7 +931,7 @@ static int makespan_impl(const char *fn, const cel_graph *g, const cel_devices *
                                                       cq, st);
     {
       KTimer kt(s, "k_dev_gather");
-      if (K >= 64) {
+      if (K >= 64 && n <= 2 * kGRowNodes) {  // rows staged in at most two passes
         const bool vec = (n & 3) == 0 && ((uintptr_t)order & 15) == 0 &&
                          ((uintptr_t)node_dev & 3) == 0;
         if (vec) k_dev_rows<true><<<(unsigned)K, kGRowB, 0, s>>>(n, order, node_dev, d->D, devp, st);
