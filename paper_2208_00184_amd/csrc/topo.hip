@@ -66,9 +66,10 @@ __device__ inline int32_t int4_at(const int4 &a, int q) {
 // first kKahnCap entries of the one being built (fe: its first index).
 __device__ inline void kahn_append(bool want, int32_t v, const int2 &d, const int4 &a, int32_t *F,
                                    int32_t *s_tail, int32_t fe, int32_t *s_fv, int2 *s_fd,
-                                   int4 *s_fa) {
+                                   int4 *s_fa, int32_t *s_hv) {
   const uint64_t m = __ballot(want);
   if (m == 0) return;
+  if (__ballot(want && d.y > kKahnA) != 0 && (int)(threadIdx.x & 63) == 0) *s_hv = 1;
   const int leader = __builtin_ctzll(m);
   int32_t base = 0;
   if ((int)(threadIdx.x & 63) == leader) base = atomicAdd(s_tail, __popcll(m));
@@ -107,6 +108,9 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
   __shared__ int4 s_fa[2][kKahnCap];
   __shared__ int32_t s_hd[kKahnB], s_he[kKahnB], s_hp[kKahnB + 1];
   __shared__ int32_t s_wt[kKahnNW];
+  // per mirror: the frontier holds a node of more than kKahnA successors;
+  // the state wave 0 leaves after a run of narrow levels
+  __shared__ int32_t s_hv[2], s_state[4];
   __shared__ uint32_t s_cnt[kKahnCW];
   if (failed(st)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -120,6 +124,7 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
   if (tid == 0) {
     s_tail = 0;
     s_nh[0] = s_nh[1] = s_nh[2] = 0;
+    s_hv[0] = s_hv[1] = 0;
   }
   if (ldsc) {
     const int32_t per = 1 << lper, nw = (n + per - 1) >> lper;
@@ -146,7 +151,7 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
     const int32_t v = v0 + tid;
     const bool src = v < n && g.in_ptr[v + 1] == g.in_ptr[v];
     kahn_append(src, v, make_int2(0, 0), make_int4(-1, -1, -1, -1), F, &s_tail, 0, s_fv[0],
-                s_fd[0], s_fa[0]);
+                s_fd[0], s_fa[0], &s_hv[0]);
   }
   __syncthreads();
   const int32_t nsrc = s_tail;
@@ -157,12 +162,93 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
     const bool one = v < n && g.in_ptr[v + 1] > g.in_ptr[v] && cnt[v] == 0;
     const int2 d = one ? deg[v] : make_int2(0, 0);
     const int4 a = one ? adj[v] : make_int4(-1, -1, -1, -1);
-    kahn_append(one, v, d, a, F, &s_tail, nsrc, s_fv[1], s_fd[1], s_fa[1]);
+    kahn_append(one, v, d, a, F, &s_tail, nsrc, s_fv[1], s_fd[1], s_fa[1], &s_hv[1]);
   }
   for (int32_t i = tid; i < nsrc; i += kKahnB) level[F[i]] = 0;
   __syncthreads();
   int32_t fb = nsrc, fe = s_tail, lvl = nsrc > 0 ? 1 : 0, cur = 1, pp = 0;
   while (fb < fe) {
+    if (fe - fb <= 64 && s_hv[cur] == 0) {
+      // Narrow levels (at most 64 nodes, none of more than kKahnA
+      // successors): wave 0 runs them alone, one node per lane, with no
+      // workgroup barrier; the other waves wait for the next wide level.
+      if (wave == 0) {
+        int32_t tail = fe, cu = cur, lv = lvl;
+        bool hv = false;
+        while (true) {
+          if (lane == 0) lstart[lv] = fb;
+          const int32_t i = fb + lane;
+          const bool act = i < fe;
+          int32_t u = 0;
+          int2 d = make_int2(0, 0);
+          int4 a = make_int4(-1, -1, -1, -1);
+          if (act) {
+            u = s_fv[cu][i - fb];
+            d = s_fd[cu][i - fb];
+            a = s_fa[cu][i - fb];
+            level[u] = lv;
+          }
+          int32_t c[kKahnA];
+          int2 td[kKahnA];
+          int4 ta[kKahnA];
+#pragma unroll
+          for (int q = 0; q < kKahnA; q++) {
+            const int32_t t = int4_at(a, q);
+            c[q] = 0;
+            td[q] = make_int2(0, 0);
+            ta[q] = make_int4(-1, -1, -1, -1);
+            if (act && q < d.y) {
+              td[q] = deg[t];
+              ta[q] = adj[t];
+              c[q] = remove_edge(t);
+            }
+          }
+          // appends: slots by ballot, the tail in a scalar register
+          int32_t *nv = s_fv[cu ^ 1];
+          int2 *nd = s_fd[cu ^ 1];
+          int4 *na = s_fa[cu ^ 1];
+          hv = false;
+#pragma unroll
+          for (int q = 0; q < kKahnA; q++) {
+            const bool want = c[q] == 1;
+            const uint64_t m = __ballot(want);
+            if (want) {
+              const int32_t k = tail + (int32_t)__builtin_amdgcn_mbcnt_hi(
+                                           (uint32_t)(m >> 32),
+                                           __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+              const int32_t t = int4_at(a, q);
+              F[k] = t;
+              nv[k - fe] = t;  // at most 4 * 64 entries: all in the mirror
+              nd[k - fe] = td[q];
+              na[k - fe] = ta[q];
+            }
+            tail += __popcll(m);
+            hv = hv || __ballot(want && td[q].y > kKahnA) != 0;
+          }
+          lv++;
+          cu ^= 1;
+          fb = fe;
+          fe = tail;
+          if (fe == fb || fe - fb > 64 || hv) break;
+        }
+        if (lane == 0) {
+          s_state[0] = fb;
+          s_state[1] = fe;
+          s_state[2] = lv;
+          s_state[3] = cu;
+          s_tail = tail;
+          s_hv[cu] = hv ? 1 : 0;
+          s_hv[cu ^ 1] = 0;
+        }
+      }
+      __syncthreads();
+      fb = s_state[0];
+      fe = s_state[1];
+      lvl = s_state[2];
+      cur = s_state[3];
+      __syncthreads();  // everyone has read the state before it can change again
+      continue;
+    }
     if (tid == 0) lstart[lvl] = fb;
     int32_t *nv = s_fv[cur ^ 1];
     int2 *nd = s_fd[cur ^ 1];
@@ -209,13 +295,17 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
         }
 #pragma unroll
         for (int q = 0; q < kKahnA; q++)
-          kahn_append(c[q] == 1, int4_at(a, q), td[q], ta[q], F, &s_tail, fe, nv, nd, na);
+          kahn_append(c[q] == 1, int4_at(a, q), td[q], ta[q], F, &s_tail, fe, nv, nd, na,
+                      &s_hv[cur ^ 1]);
       }
       __syncthreads();
       const int32_t nh = s_nh[pp];
       // the counter of the pass after next: last read in the previous pass,
       // before this pass's barrier, and next counted after the next pass's
-      if (tid == 0) s_nh[pp == 0 ? 2 : pp - 1] = 0;
+      if (tid == 0) {
+        s_nh[pp == 0 ? 2 : pp - 1] = 0;
+        s_hv[cur] = 0;  // read by every wave at the top of this level; the next frontier but one
+      }
       if (nh > 0) {
         // exclusive prefix of the listed nodes' degrees (by wave 0 alone when
         // they fit one wave)
@@ -270,7 +360,8 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
           }
 #pragma unroll
           for (int q = 0; q < kKahnE; q++)
-            kahn_append(c[q] == 1, v[q], td[q], ta[q], F, &s_tail, fe, nv, nd, na);
+            kahn_append(c[q] == 1, v[q], td[q], ta[q], F, &s_tail, fe, nv, nd, na,
+                        &s_hv[cur ^ 1]);
         }
         __syncthreads();
       }
