@@ -258,18 +258,22 @@ __device__ inline bool block_failed(const Status *st, int *flag) {
   return *flag != 0;
 }
 
-__device__ inline void block_add_u64(unsigned long long *dst, uint64_t x, uint64_t *red) {
+// the block's sum of x into *dst (one plain store per block: blocks write
+// their own partials, which one small kernel adds up, so no address takes
+// thousands of atomics)
+__device__ inline void block_sum_u64(unsigned long long *dst, uint64_t x, uint64_t *red) {
   for (int off = 32; off > 0; off >>= 1) x += __shfl_down(x, off);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
   __syncthreads();
   if (threadIdx.x == 0) {
     uint64_t t = 0;
     for (int i = 0; i < (int)(blockDim.x >> 6); i++) t += red[i];
-    if (t) atomicAdd(dst, (unsigned long long)t);
+    *dst = (unsigned long long)t;
   }
 }
 
-// CSR pass over edge-balanced blocks: target ranges and the pair-hash total.
+// CSR pass over edge-balanced blocks: target ranges and the pair-hash total
+// (hs[block]: the block's part).
 __global__ void k_check_csr(cel_graph g, Status *st, unsigned long long *hs) {
   __shared__ int32_t ptr[kRowsPB + 1], su[2];
   __shared__ uint64_t red[16];
@@ -287,10 +291,10 @@ __global__ void k_check_csr(cel_graph g, Status *st, unsigned long long *hs) {
     acc += pair_hash(u, t);
   });
   if (bad) raise_err(st, bad);
-  block_add_u64(&hs[0], acc, red);
+  block_sum_u64(&hs[blockIdx.x], acc, red);
 }
 
-// CSC pass: source ranges, in-degrees and the pair-hash total.
+// CSC pass: source ranges, in-degrees and the pair-hash total (hs[block]).
 __global__ void k_check_csc(cel_graph g, Status *st, int32_t *indeg, unsigned long long *hs) {
   __shared__ uint64_t red[16];
   __shared__ int s_f;
@@ -311,12 +315,34 @@ __global__ void k_check_csc(cel_graph g, Status *st, int32_t *indeg, unsigned lo
     }
   }
   if (bad) raise_err(st, bad);
-  block_add_u64(&hs[1], acc, red);
+  block_sum_u64(&hs[blockIdx.x], acc, red);
 }
 
-__global__ void k_check_pairs(const unsigned long long *hs, Status *st) {
+// the two totals from the blocks' parts: [0, na) for the CSR side, then nb
+// for the CSC side (a failed earlier check leaves parts unwritten: skipped)
+__global__ void k_check_pairs(const unsigned long long *hs, int na, int nb, Status *st) {
+  __shared__ uint64_t red[2][4];
   if (failed(st)) return;
-  if (hs[0] != hs[1]) raise_err(st, EB_ARG);
+  uint64_t a = 0, b = 0;
+  for (int i = threadIdx.x; i < na; i += blockDim.x) a += hs[i];
+  for (int i = threadIdx.x; i < nb; i += blockDim.x) b += hs[na + i];
+  for (int off = 32; off > 0; off >>= 1) {
+    a += __shfl_down(a, off);
+    b += __shfl_down(b, off);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = a;
+    red[1][threadIdx.x >> 6] = b;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t ta = 0, tb = 0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); i++) {
+      ta += red[0][i];
+      tb += red[1][i];
+    }
+    if (ta != tb) raise_err(st, EB_ARG);
+  }
 }
 
 // one block: saturating sum of the per-block partials
@@ -343,12 +369,12 @@ int check_graph(const cel_graph *g, int64_t bw, int64_t lat, bool bound, Status 
   CEL_TRY(sc.get(&part, nbk));
   k_check_nodes<<<nbk, B, 0, s>>>(*g, bw, lat, st, part);
   if (g->n > 0) {
+    const int na = (int)edge_blocks(g->m), nc = grid_for(g->n, B, 4096);
     unsigned long long *hs;
-    CEL_TRY(sc.get(&hs, 2));
-    CEL_HIP(hipMemsetAsync(hs, 0, 2 * sizeof(unsigned long long), s));
-    k_check_csr<<<edge_blocks(g->m), B, 0, s>>>(*g, st, hs);
-    k_check_csc<<<grid_for(g->n, B, 4096), B, 0, s>>>(*g, st, indeg, hs);
-    k_check_pairs<<<1, 1, 0, s>>>(hs, st);
+    CEL_TRY(sc.get(&hs, (int64_t)na + nc));
+    k_check_csr<<<na, B, 0, s>>>(*g, st, hs);
+    k_check_csc<<<nc, B, 0, s>>>(*g, st, indeg, hs + na);
+    k_check_pairs<<<1, B, 0, s>>>(hs, na, nc, st);
   }
   if (bound) k_finish_overflow<<<1, B, 0, s>>>(part, nbk, st);
   CEL_HIP(hipGetLastError());
@@ -361,7 +387,9 @@ __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
     p[i] = v;
 }
 
-// pos[order[p]] = p, duplicates and out-of-range ids raise EB_ORDER
+// pos[order[p]] = p; out-of-range ids raise EB_ORDER.  Duplicates are found
+// by k_perm_verify: two positions naming one id leave pos[id] at one of them,
+// and the other no longer reads itself back.
 __global__ void k_inverse_perm(int32_t n, const int32_t *order, int32_t *pos, Status *st) {
   uint32_t bad = 0;
   for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
@@ -371,8 +399,17 @@ __global__ void k_inverse_perm(int32_t n, const int32_t *order, int32_t *pos, St
       bad |= EB_ORDER;
       continue;
     }
-    if (atomicCAS(&pos[v], -1, (int32_t)p) != -1) bad |= EB_ORDER;
+    pos[v] = (int32_t)p;
   }
+  if (bad) raise_err(st, bad);
+}
+
+__global__ void k_perm_verify(int32_t n, const int32_t *order, const int32_t *pos, Status *st) {
+  if (failed(st)) return;  // ids not in range
+  uint32_t bad = 0;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+       p += (int64_t)gridDim.x * blockDim.x)
+    if (pos[order[p]] != (int32_t)p) bad |= EB_ORDER;
   if (bad) raise_err(st, bad);
 }
 
@@ -433,6 +470,7 @@ int check_level_order(const cel_graph *g, const int32_t *order, const int32_t *l
   if (n > 0) {
     k_fill_i32<<<grid_for(n, B, 4096), B, 0, s>>>(pos, n, -1);
     k_inverse_perm<<<grid_for(n, B, 4096), B, 0, s>>>(n, order, pos, st);
+    k_perm_verify<<<grid_for(n, B, 4096), B, 0, s>>>(n, order, pos, st);
   }
   k_check_levels_nodes<<<grid_for((int64_t)n + 1, B, 4096), B, 0, s>>>(n, order, level, level_ptr,
                                                                        L, st);
@@ -448,6 +486,7 @@ int check_topo_order(const cel_graph *g, const int32_t *order, int32_t *pos, Sta
   if (n > 0) {
     k_fill_i32<<<grid_for(n, B, 4096), B, 0, s>>>(pos, n, -1);
     k_inverse_perm<<<grid_for(n, B, 4096), B, 0, s>>>(n, order, pos, st);
+    k_perm_verify<<<grid_for(n, B, 4096), B, 0, s>>>(n, order, pos, st);
     k_check_topo_edges<<<edge_blocks(g->m), B, 0, s>>>(*g, pos, st);
   }
   CEL_HIP(hipGetLastError());
