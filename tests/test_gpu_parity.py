@@ -243,6 +243,7 @@ def _wide_layered(seed, widths, max_fanin, D):
 
 @pytest.mark.parametrize("widths,fanin,D,K", [
     ([700, 1300, 900], 10, 200, 3),     # passes of 512 nodes, tail in-edges, 8-bit devices
+    ([700, 1300, 900], 10, 12, 3),      # the LDS-ring kernel (D <= 16) with in-edges past three
     ([257, 513, 1025, 300], 3, 16, 5),  # ragged chunks
     ([600, 600], 1, 1, 2),              # one device
 ])
@@ -342,6 +343,38 @@ def test_makespan_batch_level_paths():
         P[2, nodes] = li % D
     P[1, :] = 3
     P[3] = rng.integers(0, D, n)
+    ref_ms, ref_st, ref_fi = O.makespan(wl, pr, P)
+    g, d = up(wl)
+    ms, st, fi = cel.makespan(g, d, tt(pr, np.int32), tt(lev, np.int32), tt(lp, np.int32), L,
+                              tt(P, np.uint8), want_times=True)
+    assert np.array_equal(np_(ms), ref_ms)
+    assert np.array_equal(np_(st), ref_st) and np.array_equal(np_(fi), ref_fi)
+
+
+def test_makespan_wide_far_predecessors_batch():
+    """Wide levels whose nodes take up to 7 parents from the previous four
+    levels of 3,000: predecessors more than 8,192 positions back (read from the
+    placement's finish times in global memory, ahead or one by one past the
+    third in-edge) beside near ones (from the LDS ring), D = 9, 70 placements
+    (the LDS-staged device gather as well)."""
+    rng = np.random.default_rng(44)
+    widths = [3000] * 7
+    starts = np.concatenate([[0], np.cumsum(widths)])
+    n = int(starts[-1])
+    edges = []
+    for li in range(1, len(widths)):
+        lo = int(starts[max(0, li - 4)])
+        for v in range(int(starts[li]), int(starts[li + 1])):
+            k = int(rng.integers(1, 8))
+            ps = {int(rng.integers(starts[li - 1], starts[li]))}  # one parent in the level below
+            ps.update(int(u) for u in rng.integers(lo, starts[li], k - 1))
+            edges += [(u, v) for u in sorted(ps)]
+    wl = from_edges(n, edges, rng.integers(1, 5000, n), rng.integers(0, 1 << 20, n), 9,
+                    np.full(9, 1 << 40), 7, 300, name="wide-far")
+    lev, oid, lp, L = O.topo_levels(wl)
+    assert wl.n >= 256 * L
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    P = random_placements(wl, 70, 9)
     ref_ms, ref_st, ref_fi = O.makespan(wl, pr, P)
     g, d = up(wl)
     ms, st, fi = cel.makespan(g, d, tt(pr, np.int32), tt(lev, np.int32), tt(lp, np.int32), L,
