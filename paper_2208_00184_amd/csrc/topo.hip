@@ -41,18 +41,33 @@ __global__ void k_kahn_cnt(int32_t n, const int32_t *in_ptr, const int32_t *in_i
   if ((threadIdx.x & 63) == 0 && mx > 0) atomicMax(cmax, mx);
 }
 
+// A successor entry of a node's record: the id, bit 31 set when that
+// successor has exactly one in-edge from a non-source (this one: it becomes
+// ready without a counter).
+constexpr int32_t kOneBit = int32_t(0x80000000u);
+__device__ inline int32_t succ_id(int32_t e) { return e & 0x7FFFFFFF; }
+__device__ inline bool succ_one(int32_t e) { return e < 0; }
+
 // Per node: first out-edge and out-degree, and its first kKahnA successors
-// (-1 past the end), so that a node that becomes ready brings its adjacency
-// along with it.
+// (-1 past the end; count-one successors flagged), so that a node that
+// becomes ready brings its adjacency along with it.
 __global__ void k_kahn_prep(int32_t n, const int32_t *out_ptr, const int32_t *out_idx,
-                            int2 *deg, int4 *adj, const Status *st) {
+                            const int32_t *cnt, int2 *deg, int4 *adj, const Status *st) {
   if (failed(st)) return;
   for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
        v += (int64_t)gridDim.x * blockDim.x) {
     const int32_t e0 = out_ptr[v], d = out_ptr[v + 1] - e0;
     deg[v] = make_int2(e0, d);
-    adj[v] = make_int4(d > 0 ? out_idx[e0] : -1, d > 1 ? out_idx[e0 + 1] : -1,
-                       d > 2 ? out_idx[e0 + 2] : -1, d > 3 ? out_idx[e0 + 3] : -1);
+    int32_t s[kKahnA];
+#pragma unroll
+    for (int q = 0; q < kKahnA; q++) {
+      s[q] = -1;
+      if (q < d) {
+        const int32_t t = out_idx[e0 + q];
+        s[q] = cnt[t] == 1 ? (t | kOneBit) : t;
+      }
+    }
+    adj[v] = make_int4(s[0], s[1], s[2], s[3]);
   }
 }
 
@@ -83,6 +98,44 @@ __device__ inline void kahn_append(bool want, int32_t v, const int2 &d, const in
     s_fv[k - fe] = v;
     s_fd[k - fe] = d;
     s_fa[k - fe] = a;
+  }
+}
+
+// The same for N candidates per lane (want[q], v[q], ...): one LDS atomic
+// reserves the slots of all N ballots of the wave at once.
+template <int N>
+__device__ inline void kahn_append_n(const bool (&want)[N], const int32_t (&v)[N],
+                                     const int2 (&d)[N], const int4 (&a)[N], int32_t *F,
+                                     int32_t *s_tail, int32_t fe, int32_t *s_fv, int2 *s_fd,
+                                     int4 *s_fa, int32_t *s_hv) {
+  uint64_t m[N];
+  int32_t off[N], tot = 0;
+  bool hv = false;
+#pragma unroll
+  for (int q = 0; q < N; q++) {
+    m[q] = __ballot(want[q]);
+    off[q] = tot;
+    tot += __popcll(m[q]);
+    hv = hv || __ballot(want[q] && d[q].y > kKahnA) != 0;
+  }
+  if (tot == 0) return;
+  const int lane = (int)(threadIdx.x & 63);
+  if (hv && lane == 0) *s_hv = 1;
+  int32_t base = 0;
+  if (lane == 0) base = atomicAdd(s_tail, tot);
+  base = __builtin_amdgcn_readfirstlane(base);
+#pragma unroll
+  for (int q = 0; q < N; q++) {
+    if (!want[q]) continue;
+    const int32_t k = base + off[q] +
+                      (int32_t)__builtin_amdgcn_mbcnt_hi(
+                          (uint32_t)(m[q] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m[q], 0u));
+    F[k] = v[q];
+    if (k - fe < kKahnCap) {
+      s_fv[k - fe] = v[q];
+      s_fd[k - fe] = d[q];
+      s_fa[k - fe] = a[q];
+    }
   }
 }
 
@@ -193,14 +246,14 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
           int4 ta[kKahnA];
 #pragma unroll
           for (int q = 0; q < kKahnA; q++) {
-            const int32_t t = int4_at(a, q);
+            const int32_t e = int4_at(a, q), t = succ_id(e);
             c[q] = 0;
             td[q] = make_int2(0, 0);
             ta[q] = make_int4(-1, -1, -1, -1);
             if (act && q < d.y) {
               td[q] = deg[t];
               ta[q] = adj[t];
-              c[q] = remove_edge(t);
+              c[q] = succ_one(e) ? 1 : remove_edge(t);
             }
           }
           // appends: slots by ballot, the tail in a scalar register
@@ -216,7 +269,7 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
               const int32_t k = tail + (int32_t)__builtin_amdgcn_mbcnt_hi(
                                            (uint32_t)(m >> 32),
                                            __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-              const int32_t t = int4_at(a, q);
+              const int32_t t = succ_id(int4_at(a, q));
               F[k] = t;
               nv[k - fe] = t;  // at most 4 * 64 entries: all in the mirror
               nd[k - fe] = td[q];
@@ -283,20 +336,24 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
         int4 ta[kKahnA];
 #pragma unroll
         for (int q = 0; q < kKahnA; q++) {
-          const int32_t t = int4_at(a, q);
+          const int32_t e = int4_at(a, q), t = succ_id(e);
           c[q] = 0;
           td[q] = make_int2(0, 0);
           ta[q] = make_int4(-1, -1, -1, -1);
           if (light && q < d.y) {
             td[q] = deg[t];
             ta[q] = adj[t];
-            c[q] = remove_edge(t);
+            c[q] = succ_one(e) ? 1 : remove_edge(t);
           }
         }
+        bool want[kKahnA];
+        int32_t tv[kKahnA];
 #pragma unroll
-        for (int q = 0; q < kKahnA; q++)
-          kahn_append(c[q] == 1, int4_at(a, q), td[q], ta[q], F, &s_tail, fe, nv, nd, na,
-                      &s_hv[cur ^ 1]);
+        for (int q = 0; q < kKahnA; q++) {
+          want[q] = c[q] == 1;
+          tv[q] = succ_id(int4_at(a, q));
+        }
+        kahn_append_n<kKahnA>(want, tv, td, ta, F, &s_tail, fe, nv, nd, na, &s_hv[cur ^ 1]);
       }
       __syncthreads();
       const int32_t nh = s_nh[pp];
@@ -358,10 +415,10 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
               c[q] = remove_edge(v[q]);
             }
           }
+          bool want[kKahnE];
 #pragma unroll
-          for (int q = 0; q < kKahnE; q++)
-            kahn_append(c[q] == 1, v[q], td[q], ta[q], F, &s_tail, fe, nv, nd, na,
-                        &s_hv[cur ^ 1]);
+          for (int q = 0; q < kKahnE; q++) want[q] = c[q] == 1;
+          kahn_append_n<kKahnE>(want, v, td, ta, F, &s_tail, fe, nv, nd, na, &s_hv[cur ^ 1]);
         }
         __syncthreads();
       }
@@ -412,8 +469,9 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
   CEL_TRY(sc.get(&cmax, 1));
   CEL_HIP(hipMemsetAsync(cmax, 0, sizeof(int32_t), s));
   if (n > 0) {
-    k_kahn_prep<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, g->out_ptr, g->out_idx, deg, adj, st);
     k_kahn_cnt<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, g->in_ptr, g->in_idx, cnt, cmax, st);
+    k_kahn_prep<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, g->out_ptr, g->out_idx, cnt, deg, adj,
+                                                      st);
   }
   {
     KTimer kt(s, "k_kahn");
