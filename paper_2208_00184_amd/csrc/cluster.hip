@@ -632,7 +632,8 @@ template <bool SMALL>
 __global__ void __launch_bounds__(1024)
     k_cluster_dp(int32_t n, int32_t nb, const int32_t *lo, const int32_t *boff, const int32_t *eq,
                  const int32_t *et, const int64_t *ec, const int64_t *eE, const int64_t *PO,
-                 int32_t *P, Status *st) {
+                 const int32_t *pptr, const int32_t *pidx, const int64_t *cq, int32_t *P,
+                 Status *st) {
   constexpr int RING = SMALL ? kRingSmall : kRingBig;
   __shared__ int64_t s_h[RING];
   __shared__ __align__(16) int64_t s_tab[SMALL ? 64 * kTS + 1 : 2];
@@ -645,6 +646,7 @@ __global__ void __launch_bounds__(1024)
   __shared__ int64_t s_wa[kMaxW][64];  // per wave: comm (shifted) of its edges counted by the lane
   __shared__ int32_t s_hist[kMaxW + 1][64];
   __shared__ int64_t s_hc[64];
+  __shared__ int64_t s_bm[16];  // per wave: the minimum key of a dense block's target
   if (failed(st)) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -653,7 +655,7 @@ __global__ void __launch_bounds__(1024)
   // block 0 staged by everyone; histograms cleared
   int32_t o0 = 0, o1 = boff[1 < nb ? 1 : nb], o2 = boff[2 < nb ? 2 : nb];
   {
-    const int32_t c0 = o1;
+    const int32_t c0 = o1 <= kEC ? o1 : 0;  // a dense block 0 is not staged
     for (int32_t k = tid; k < c0; k += blockDim.x) {
       s_eq[0][k] = eq[k];
       s_et[0][k] = et[k];
@@ -688,6 +690,72 @@ __global__ void __launch_bounds__(1024)
     const int32_t cnt = o1 - o0;
     const int32_t o3 = boff[b + 3 < nb ? b + 3 : nb];
     const bool more = b + 1 < nb;
+    if (cnt > kEC) {
+      // A dense block (more window edges than the staging holds): its targets
+      // one at a time by the whole workgroup, straight from the in-edge lists.
+      // Before target j, H(i) = V_j(i); S(j) takes the smallest key over the
+      // candidates [lo(j), j); then H(j) = S(j) - PO[j] and every candidate i
+      // loses the comm of j's in-edges from sources at or after i.
+      const int nwv = (int)(blockDim.x >> 6);
+      for (int t = 0; t < 64; t++) {
+        const int32_t j = j0 + t;
+        if (j > n) break;
+        const int32_t loj = j == 0 ? 0 : lo[j];
+        int64_t key = j == 0 ? (int64_t)kBaseOff : kKeyInf;  // S(0) = 0
+        for (int32_t i = loj + tid; i < j; i += blockDim.x) {
+          const int64_t kv = (int64_t)((uint64_t)s_h[rmod<RING>(i)] << kIdxBits) + (i - base);
+          key = kv < key ? kv : key;
+        }
+        for (int off = 32; off > 0; off >>= 1) {
+          const int64_t o = __shfl_xor((long long)key, off);
+          key = o < key ? o : key;
+        }
+        if (lane == 0) s_bm[wave] = key;
+        __syncthreads();
+        key = s_bm[0];
+        for (int w = 1; w < nwv; w++) key = s_bm[w] < key ? s_bm[w] : key;
+        const int64_t G = key >> kIdxBits;
+        if (tid == 0) {
+          if (j >= 1) P[j] = (int32_t)(key & kIdxMask) + base;
+          if (j == n) st->s0 = PO[n] + G;
+        }
+        if (j < n) {
+          const int32_t e0 = pptr[j], e1 = pptr[j + 1];
+          for (int32_t i = loj + tid; i < j; i += blockDim.x) {
+            int64_t d = 0;
+            for (int32_t e = e0; e < e1; e++) {
+              const int32_t q = pidx[e];
+              if (q >= i) d += cq[q];
+            }
+            if (d) s_h[rmod<RING>(i)] -= d;
+          }
+          if (tid == 0) s_h[rmod<RING>(j)] = G;
+        }
+        __syncthreads();  // H and s_bm settled before the next target
+      }
+      // stage block b + 1 (unless it is dense too)
+      const int nbuf = buf ^ 1;
+      const int32_t c1 = o2 - o1;
+      if (more && c1 <= kEC) {
+        for (int32_t k = tid; k < c1; k += blockDim.x) {
+          const int32_t e = o1 + k;
+          s_eq[nbuf][k] = eq[e];
+          s_et[nbuf][k] = et[e];
+          s_ec[nbuf][k] = ec[e];
+          s_eE[nbuf][k] = eE[e];
+          if (k == c1 - 1) s_eE[nbuf][c1] = eE[e] + ec[e];
+        }
+        if (tid == 0 && c1 == 0) s_eE[nbuf][0] = 0;
+      }
+      if (more && tid < 64) {
+        const int32_t jj = j0 + 64 + tid;
+        s_lo[nbuf][tid] = lo[jj <= n ? jj : n];
+      }
+      o0 = o1;
+      o1 = o2;
+      o2 = o3;
+      continue;
+    }
     const int32_t *Q = s_eq[buf];
     const int32_t *T = s_et[buf];
     const int64_t *Cc = s_ec[buf];
@@ -841,10 +909,10 @@ __global__ void __launch_bounds__(1024)
       if (j < n) s_h[rmod<RING>(j)] = G - Nt;
       if (j == n) st->s0 = PO[n] + G;
     } else if (more) {
-      // stage block b + 1
+      // stage block b + 1 (a dense one is not staged: it reads global memory)
       const int nbuf = buf ^ 1;
       const int x = tid - 64;
-      const int32_t c1 = o2 - o1;
+      const int32_t c1 = o2 - o1 <= kEC ? o2 - o1 : 0;
 #pragma unroll
       for (int r = 0; r < kPF; r++) {
         const int32_t k = x + r * NT;
@@ -1023,12 +1091,10 @@ static int dp_blocked(int32_t n, int32_t m, int32_t R, const int32_t *lo, const 
                                                                      mx, st);
   }
   CEL_TRY(exclusive_scan_i32(bcnt, boff, nb, sc, s));
-  int32_t hm[1] = {0};
   int64_t total = 0;
-  CEL_HIP(hipMemcpyAsync(hm, mx, sizeof hm, hipMemcpyDeviceToHost, s));
   CEL_HIP(hipMemcpyAsync(&total, PO + n, sizeof total, hipMemcpyDeviceToHost, s));
   CEL_HIP(hipStreamSynchronize(s));
-  if (hm[0] > kEC || total >= kPackLim) return CEL_OK;  // step-wise kernel
+  if (total >= kPackLim) return CEL_OK;  // step-wise kernel (keys need values below 2^48)
   int32_t *eq, *et;
   int64_t *ec, *eE;
   CEL_TRY(sc.get(&eq, m));
@@ -1044,9 +1110,11 @@ static int dp_blocked(int32_t n, int32_t m, int32_t R, const int32_t *lo, const 
   {
     KTimer kt(s, "k_cluster_dp");
     if (R + 64 <= kRingSmall)
-      k_cluster_dp<true><<<1, 64 * NW, 0, s>>>(n, nb, lo, boff, eq, et, ec, eE, PO, P, st);
+      k_cluster_dp<true><<<1, 64 * NW, 0, s>>>(n, nb, lo, boff, eq, et, ec, eE, PO, pptr, pidx, cq,
+                                              P, st);
     else
-      k_cluster_dp<false><<<1, 64 * NW, 0, s>>>(n, nb, lo, boff, eq, et, ec, eE, PO, P, st);
+      k_cluster_dp<false><<<1, 64 * NW, 0, s>>>(n, nb, lo, boff, eq, et, ec, eE, PO, pptr, pidx,
+                                               cq, P, st);
   }
   CEL_HIP(hipGetLastError());
   *done = true;

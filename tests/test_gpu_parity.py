@@ -746,13 +746,13 @@ def _cluster_with_kernels(wl, order, R, M):
 # sides of the blocked kernel's staging size (1024 window edges per block of 64
 # targets): many edges per candidate and inside one block, several edge
 # batches, the prefetch remainder (R <= 64: one candidate wave), and blocks too
-# dense for staging (step-wise kernel).
+# dense for staging (taken target by target inside the blocked kernel).
 DENSE_CASES = [
     (4, 600, 0.12, 20, 130, -1, "k_cluster_dp"),
     (6, 2000, 0.02, 30, 1000, -1, "k_cluster_dp"),
     (7, 800, 0.1, 12, 60, -1, "k_cluster_dp"),
-    (6, 2000, 0.02, 30, 1000, 10 ** 15, "k_cluster_dp_step"),
-    (1, 400, 0.5, 400, 200, -1, "k_cluster_dp_step"),
+    (6, 2000, 0.02, 30, 1000, 10 ** 15, "k_cluster_dp"),
+    (1, 400, 0.5, 400, 200, -1, "k_cluster_dp"),
     (8, 800, 0.2, 16, 40, -1, "k_cluster_dp"),
     (10, 1000, 0.3, 10, 30, -1, "k_cluster_dp"),
 ]
