@@ -22,8 +22,10 @@
 // the next block by subtracting the comm of the block's edges whose source is
 // at or after i.  Only edges whose source lies in the window can change a
 // candidate, so each block's list holds only those; it is built and sorted by
-// a parallel pass and staged one block ahead.  Graphs whose blocks exceed the
-// staging sizes take a step-wise kernel that keeps the window in registers.
+// a parallel pass and staged one block ahead.  A block whose list exceeds the
+// staging size is taken target by target by the whole workgroup from the
+// in-edge lists; totals of comm too large for the packed keys take a
+// step-wise kernel that keeps the window in registers.
 //
 // The memory bound lo(j) comes from a prefix sum of the memory in order
 // (binary search), the greedy mode from the same prefix sums.
