@@ -330,6 +330,27 @@ int cel_colocate(const cel_graph *g, const int32_t *order, const int32_t *group,
 int cel_timing(int enable);
 int cel_kernel_stats(char *buf, int buflen, int reset);
 
+/* Diagnostics: how the calling thread's last cel_makespan or
+ * cel_makespan_noalloc call evaluated its schedule.  *path = 0: K = 1 by
+ * relaxation over the edges between different devices (each device's FIFO
+ * chain makes edges inside one device redundant), exact after *rounds rounds,
+ * the last of which changed nothing; 1: K = 1 by the level sweep, after
+ * *rounds rounds of relaxation that did not converge within their budget (0
+ * when the relaxation could not be launched); 2: K > 1 (level sweeps of the
+ * batch), *rounds = 0.
+ * Outputs: path, rounds (host).
+ * Errors: CEL_E_ARG (NULL argument). */
+int cel_makespan_info(int32_t *path, int32_t *rounds);
+
+/* Diagnostics: which K = 1 path the calling thread's cel_makespan and
+ * cel_makespan_noalloc calls take.  mode 0: the level sweep directly (path 1
+ * without relaxation rounds); 1 (the default): the relaxation first, on as
+ * many workgroups as the GPU holds at once; m >= 2: the relaxation first, on
+ * at most m workgroups (more slots per thread; for tests and tuning).  Every
+ * mode gives the same results.  Returns the previous mode (CEL_E_ARG for a
+ * negative mode). */
+int cel_makespan_relax(int mode);
+
 /* Diagnostics: the dependent step that bounds a level-synchronous sweep
  * (each level of the b-level recursion, eq. 3, and of the makespan, eq. 7,
  * waits for the previous one).  Runs `steps` dependent iterations of gather

@@ -21,7 +21,7 @@ COMM_OFF = 1
 CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
 EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_dfs_order", "cel_cluster", "cel_place", "cel_place_ext", "cel_makespan", "cel_makespan_noalloc",
-           "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_colocate", "cel_step_latency", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
+           "cel_makespan_info", "cel_makespan_relax", "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_colocate", "cel_step_latency", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
 class CelError(RuntimeError):
@@ -88,6 +88,10 @@ def lib() -> C.CDLL:
         L.cel_timing.restype = C.c_int
         L.cel_kernel_stats.argtypes = [C.c_char_p, C.c_int, C.c_int]
         L.cel_kernel_stats.restype = C.c_int
+        L.cel_makespan_info.argtypes = [C.POINTER(i32), C.POINTER(i32)]
+        L.cel_makespan_info.restype = C.c_int
+        L.cel_makespan_relax.argtypes = [C.c_int]
+        L.cel_makespan_relax.restype = C.c_int
         _lib = L
     return _lib
 
@@ -102,6 +106,29 @@ def step_latency(variant: int = 0, steps: int = 200000) -> float:
     ns = C.c_double(0.0)
     _check(lib().cel_step_latency(int(variant), int(steps), C.byref(ns), _stream()))
     return ns.value
+
+
+MS_PATH_RELAX, MS_PATH_SWEEP, MS_PATH_BATCH = 0, 1, 2
+
+
+def makespan_info() -> tuple:
+    """(path, rounds) of the calling thread's last makespan call: path 0 =
+    relaxation over cross-device edges (exact after `rounds` rounds), 1 = the
+    level sweep (after `rounds` relaxation rounds that did not converge), 2 =
+    a batch (K > 1)."""
+    path, rounds = C.c_int32(0), C.c_int32(0)
+    _check(lib().cel_makespan_info(C.byref(path), C.byref(rounds)))
+    return path.value, rounds.value
+
+
+def makespan_relax(mode: int) -> int:
+    """K = 1 makespan path of the calling thread: 0 = the level sweep, 1 = the
+    relaxation first (default), m >= 2 = the relaxation on at most m
+    workgroups; returns the previous mode."""
+    r = lib().cel_makespan_relax(int(mode))
+    if r < 0:
+        _check(r)
+    return r
 
 
 def timing(enable: bool) -> bool:

@@ -311,6 +311,14 @@ class Scratch {
     return raw(reinterpret_cast<void **>(out), sizeof(T) * (size_t)(count > 0 ? count : 1));
   }
   int raw(void **out, size_t bytes);
+  // A bump position, and a return to it: the space handed out since the mark
+  // is taken again by later requests (for work queued after the work that
+  // used it, on the same stream).
+  struct Mark {
+    size_t blk, off;
+  };
+  Mark mark() const;
+  void release(const Mark &m);
 
  private:
   hipStream_t s_;
@@ -532,6 +540,17 @@ int ms_ring(int32_t n, int32_t m, int32_t L, const int32_t *lp, const int32_t *g
             const int32_t *level, const int32_t *pptr, const int32_t *pidx, const int64_t *wp,
             const int64_t *cq, const uint8_t *devp, const int64_t *sxp, const int32_t *metap,
             int64_t *finp, int64_t *makespan, class Scratch &sc, hipStream_t s, Status *st);
+// ms_relax.hip: finish times of one placement by relaxation over the
+// cross-device edges (devp = devices by position).  Queues the preparation
+// and one cooperative kernel on s and sets *launched; st->i3 = 1 once the
+// kernel has converged (start, finish and makespan[0] are then written) and
+// st->i2 = the rounds it ran.  *launched stays false when the grid cannot be
+// co-resident (the caller runs the level sweep).  max_groups > 0 caps the
+// workgroups (more tiles per thread).
+int ms_relax(const cel_graph *g, const cel_devices *d, int32_t L, const int32_t *order,
+             const uint8_t *node_dev, const uint8_t *devp, int64_t *start, int64_t *finish,
+             int64_t *makespan, int max_groups, class Scratch &sc, hipStream_t s, Status *st,
+             bool *launched);
 // makespan_model.hip: a heterogeneous descriptor's ranges, its slowest
 // multiplier, smallest bandwidth and largest latency; lead[g] = smallest
 // pos[v] over the members v of group g (INT32_MAX before)

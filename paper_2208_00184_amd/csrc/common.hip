@@ -134,6 +134,23 @@ int Scratch::raw(void **out, size_t bytes) {
   return CEL_OK;
 }
 
+Scratch::Mark Scratch::mark() const {
+  if (base_ || !a_) return Mark{0, off_};
+  return Mark{a_->blk, a_->off};
+}
+
+void Scratch::release(const Mark &m) {
+  if (err_ != CEL_OK) return;
+  if (base_ || !a_) {
+    off_ = m.off;
+    return;
+  }
+  // `need` keeps counting every request: it sizes the single block that
+  // replaces a spilled chain, and a bound from above is enough there
+  a_->blk = m.blk;
+  a_->off = m.off;
+}
+
 Scratch::~Scratch() {
   if (!a_) return;
   if (a_->blocks.size() > 1) a_->grow_to = a_->need;

@@ -861,6 +861,27 @@ static int check_makespan_args(const char *fn, const cel_graph *g, const cel_dev
   return CEL_OK;
 }
 
+// How the calling thread's last makespan call ran (cel_makespan_info).
+struct MsInfo {
+  int32_t path, rounds;
+};
+static thread_local MsInfo t_ms_info{2, 0};
+static thread_local int t_ms_relax = 1;
+
+extern "C" int cel_makespan_relax(int mode) {
+  if (mode < 0) return set_error(CEL_E_ARG, "cel_makespan_relax: negative mode");
+  const int was = t_ms_relax;
+  t_ms_relax = mode;
+  return was;
+}
+
+extern "C" int cel_makespan_info(int32_t *path, int32_t *rounds) {
+  if (!path || !rounds) return set_error(CEL_E_ARG, "cel_makespan_info: NULL argument");
+  *path = t_ms_info.path;
+  *rounds = t_ms_info.rounds;
+  return CEL_OK;
+}
+
 // The whole call on scratch from `sc` (the arena, or the fixed array of
 // cel_makespan_noalloc).
 static int makespan_impl(const char *fn, const cel_graph *g, const cel_devices *d,
@@ -892,25 +913,43 @@ static int makespan_impl(const char *fn, const cel_graph *g, const cel_devices *
   CEL_TRY(sc.get(&finp, 2 * (int64_t)K * n));  // fin, then fin + c (the ring sweeps)
   const int gx = grid_for(n, 256, 1024);
   if (K == 1) {
+    uint8_t *dev0;
+    CEL_TRY(sc.get(&dev0, n));
+    {
+      KTimer kt(s, "k_dev_gather");
+      k_dev_gather<<<dim3(gx, 1), 256, 0, s>>>(1, n, order, node_dev, d->D, dev0, st);
+    }
+    // First the relaxation over cross-device edges; it converges in a few
+    // rounds unless the placement changes device along most long paths.
+    const Scratch::Mark mk = sc.mark();
+    bool launched = false;
+    if (t_ms_relax > 0)
+      CEL_TRY(ms_relax(g, d, L, order, node_dev, dev0, start, finish, makespan,
+                       t_ms_relax > 1 ? t_ms_relax : 0, sc, s, st, &launched));
+    if (launched) {
+      Status h;
+      CEL_TRY(read_status(st, &h, s));
+      if (h.err) return status_error(h, fn);
+      t_ms_info = {0, h.i2};
+      if (h.i3) return CEL_OK;
+      t_ms_info = {1, h.i2};
+    } else {
+      t_ms_info = {1, 0};
+    }
+    sc.release(mk);
     // Device-grouped order: inside each level, nodes sorted by (device,
     // position in `order`).  Every device keeps its FIFO order, so the
     // makespan is unchanged, and each device's chain in a level is one run.
-    uint8_t *dev0;
     uint64_t *keys;
     uint32_t *sig;
     int32_t *gorder, *meta;
     int64_t *wx, *sx;
-    CEL_TRY(sc.get(&dev0, n));
     CEL_TRY(sc.get(&keys, n));
     CEL_TRY(sc.get(&sig, n));
     CEL_TRY(sc.get(&gorder, n));
     CEL_TRY(sc.get(&meta, n));
     CEL_TRY(sc.get(&wx, (int64_t)n + 1));
     CEL_TRY(sc.get(&sx, n));
-    {
-      KTimer kt(s, "k_dev_gather");
-      k_dev_gather<<<dim3(gx, 1), 256, 0, s>>>(1, n, order, node_dev, d->D, dev0, st);
-    }
     k_dev_keys<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, dev0, keys, sig, st);
     CEL_TRY(segmented_sort(keys, sig, level_ptr, L, n, sc, s, st));
     k_grouped<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, sig, dev0, gorder, pos, devp, st);
@@ -926,6 +965,7 @@ static int makespan_impl(const char *fn, const cel_graph *g, const cel_devices *
       k_makespan_out<<<grid_for(n, 256, 8192), 256, 0, s>>>(1, n, gorder, finp, wp, start, finish,
                                                             st);
   } else {
+    t_ms_info = {2, 0};
     CEL_TRY(relabel_csr(n, g->m, order, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
     k_pos_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order, g->w, g->ob, d->bw, d->lat, wp,
                                                       cq, st);

@@ -117,13 +117,22 @@ def test_blevel_tlevel_on_caller_streams():
     assert outs == [1, 3]
 
 
+@pytest.fixture(params=[1, 0], ids=["relax", "sweep"])
+def ms_path(request):
+    """K = 1 makespans by the relaxation over cross-device edges (falling back
+    to the level sweep when it does not converge) or by the level sweep."""
+    was = cel.makespan_relax(request.param)
+    yield request.param
+    cel.makespan_relax(was)
+
+
 def random_placements(wl, K, seed):
     rng = np.random.default_rng([77, seed])
     return rng.integers(0, wl.D, (K, wl.n)).astype(np.uint8)
 
 
 @pytest.mark.parametrize("cfg,seed", [(1, 0), (2, 0), (3, 1), (5, 0)])
-def test_makespan_configs(cfg, seed):
+def test_makespan_configs(cfg, seed, ms_path):
     wl, rt, rb = config(cfg, seed)
     lev, oid, lp, L = rt
     pr = rb[2]
@@ -262,7 +271,7 @@ def test_makespan_wide_levels_batch(widths, fanin, D, K):
     assert np.array_equal(np_(st), ref_st) and np.array_equal(np_(fi), ref_fi)
 
 
-def test_makespan_one_run_boundaries():
+def test_makespan_one_run_boundaries(ms_path):
     """K = 1: the device runs of a level (consecutive slots of the
     device-grouped order) start at lane 0 of a row, inside a row, exactly at
     the second row's lane 0 and in later rows, or a level sits on one device
@@ -442,7 +451,7 @@ def test_makespan_batch_rows_gather():
 # ---------------------------------------------------------- random small DAGs
 
 
-def test_random_dags():
+def test_random_dags(ms_path):
     for s in range(40):
         n = 1 + (s * 37) % 300
         wl = make_random_dag(1000 + s, n, p_edge=min(0.5, 4.0 / max(n, 1)), D=1 + s % 7,
@@ -456,9 +465,14 @@ def test_random_dags():
         ms, st, fi = cel.makespan(g, d, gb[2], gt[0], gt[2], gt[3], tt(P, np.uint8),
                                   want_times=True)
         assert np.array_equal(np_(ms), ref[0]) and np.array_equal(np_(fi), ref[2])
+        ms1, st1, fi1 = cel.makespan(g, d, gb[2], gt[0], gt[2], gt[3], tt(P[s % 3], np.uint8),
+                                     want_times=True)
+        assert np_(ms1)[0] == ref[0][s % 3]
+        assert np.array_equal(np_(fi1)[0], ref[2][s % 3])
+        assert np.array_equal(np_(st1)[0], ref[1][s % 3])
 
 
-def test_wide_levels_and_many_devices():
+def test_wide_levels_and_many_devices(ms_path):
     """Levels wider than a workgroup (ragged chunks) and D = 255."""
     rng = np.random.default_rng(5)
     n0, n1 = 3000, 2500
@@ -494,7 +508,7 @@ def test_heavy_fanout_node():
     assert_topo_blevel(wl, rt, rb, gt, gb)
 
 
-def test_heavy_window_nodes():
+def test_heavy_window_nodes(ms_path):
     """Nodes with more neighbours than a sweep window holds edges: a source with
     9,999 successors (b-level), a sink with 10,000 predecessors (t-level and
     makespan), both between ordinary levels, for every sweep and both
@@ -623,7 +637,7 @@ def test_sweep_grid_levels():
 # -------------------------------------------------------------- edge cases
 
 
-def test_empty_and_single():
+def test_empty_and_single(ms_path):
     wl = from_edges(0, [], [], [], 2, [5, 5], 3, 1)
     g, d = up(wl)
     lev, oid, lp, L = cel.topo_levels(g)
@@ -944,12 +958,20 @@ def test_full_path_large(cfg):
     rm = O.makespan(wl, rb[2], P)
     ms, st, fi = cel.makespan(g, d, gb[2], gt[0], gt[2], gt[3], tt(P, np.uint8), want_times=True)
     assert np.array_equal(np_(ms), rm[0]) and np.array_equal(np_(fi), rm[2])
-    # the single-placement path (device-grouped sweep) on Adjusting Placement's
-    # devices: every start and finish time of the 1.07M nodes, element by element
-    ms1, st1, fi1 = cel.makespan(g, d, gb[2], gt[0], gt[2], gt[3], ndev, want_times=True)
-    assert np_(ms1)[0] == rm[0][0]
-    assert np.array_equal(np_(fi1)[0], rm[2][0]) and np.array_equal(np_(st1)[0], rm[1][0])
-    for k in (1, 3):  # random placements through the same path
+    # the single-placement paths on Adjusting Placement's devices: every start
+    # and finish time of the 1.07M nodes, element by element, by the
+    # relaxation (which converges in a few rounds here) and by the level sweep
+    for mode in (1, 0):
+        was = cel.makespan_relax(mode)
+        try:
+            ms1, st1, fi1 = cel.makespan(g, d, gb[2], gt[0], gt[2], gt[3], ndev, want_times=True)
+            path, rounds = cel.makespan_info()
+        finally:
+            cel.makespan_relax(was)
+        assert (path, rounds > 0) == ((0, True) if mode else (1, False))
+        assert np_(ms1)[0] == rm[0][0]
+        assert np.array_equal(np_(fi1)[0], rm[2][0]) and np.array_equal(np_(st1)[0], rm[1][0])
+    for k in (1, 3):  # random placements (the relaxation gives up on them: the sweep)
         msk, stk, fik = cel.makespan(g, d, gb[2], gt[0], gt[2], gt[3], tt(P[k], np.uint8),
                                      want_times=True)
         assert np_(msk)[0] == rm[0][k]
