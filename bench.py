@@ -46,10 +46,12 @@ BATCH5 = 1024  # candidates of the 200k-node batched-scoring row
 
 
 def algorithmic_bytes(kernel: str, n: int, m: int, K: int) -> float | None:
-    """Bytes each kernel must move per launch (int32 indices, int64 times, u8 devices)."""
-    if kernel == "k_blevel_sweep":      # per node: order 4, ptr 4, w 8, c 8, write 8; per edge: idx 4, gather 8
+    """Bytes each kernel must move per launch (int32 indices, int64 times, u8
+    devices): what one pass of the operation needs, whatever the kernel's
+    method (policy iteration and relaxation rounds re-read more)."""
+    if kernel in ("k_blevel_sweep", "k_blevel_policy"):  # per node: order 4, ptr 4, w 8, c 8, write 8; per edge: idx 4, gather 8
         return 32.0 * n + 12.0 * m
-    if kernel == "k_tlevel_sweep":
+    if kernel in ("k_tlevel_sweep", "k_tlevel_policy"):
         return 32.0 * n + 12.0 * m
     if kernel == "k_makespan_one":    # per node: order 4, ptr 4, w 8, c 8, dev 1, fin 8; per edge: idx 4, fin 8, dev 1, c 8
         return 33.0 * n + 21.0 * m
@@ -65,7 +67,10 @@ TRAFFIC_FILES = [os.path.join(ROOT, "profiles", f) for f in
 CSRC = os.path.join(ROOT, "paper_2208_00184_amd", "csrc")
 # kernels the bench names, their symbols in rocprofv3 output and their sources
 PMC_KERNELS = {
-    "k_makespan_one": ("cel::k_ms_ring(", ["ms_ring.hip", "cel_internal.h"]),
+    "k_makespan_one": ("cel::k_rx_relax<", ["ms_relax.hip", "cel_internal.h"]),
+    "k_makespan_sweep_one": ("cel::k_ms_ring(", ["ms_ring.hip", "cel_internal.h"]),
+    "k_blevel_policy": ("cel::k_lp_policy<false>", ["lp_policy.hip", "cel_internal.h"]),
+    "k_tlevel_policy": ("cel::k_lp_policy<true>", ["lp_policy.hip", "cel_internal.h"]),
     "k_blevel_sweep": ("cel::k_ring_sweep<true>", ["sweep.hip", "cel_internal.h"]),
     "k_tlevel_sweep": ("cel::k_ring_sweep<false>", ["sweep.hip", "cel_internal.h"]),
     "k_makespan_batch": ("cel::k_mb_ring(", ["ms_batch.hip", "cel_internal.h"]),
@@ -518,8 +523,10 @@ def main() -> int:
         ev[3].record(stream)
         cdev, ndev, cms, be = cel.place(g, d, cid, C)
         ev[4].record(stream)
+        bl_info = cel.blevel_info()
         ms1, _, _ = cel.makespan(g, d, pr, lev, lp, L, ndev)
         ev[5].record(stream)
+        ms_info = cel.makespan_info()
         if "cand" not in state:  # input prep for the batched row (random draws)
             cand = perturb_placements(cdev.cpu().numpy(), wl.D, BATCH, args.seed)
             candt = torch.from_numpy(cand).to(dev)
@@ -534,6 +541,11 @@ def main() -> int:
             names = ["topo_levels", "blevel", "cluster", "place", "makespan", "makespan_batch"]
             for i, nm in enumerate(names):
                 record.setdefault(nm, []).append(ev[i].elapsed_time(ev[i + 1]))
+        paths = ("policy iteration", "level sweep", "none", "batch")
+        state["passes"] = {
+            "blevel": {"path": paths[bl_info[0][0]], "iterations": bl_info[0][1]},
+            "makespan": {"path": "relaxation" if ms_info[0] == 0 else paths[ms_info[0]],
+                         "rounds": ms_info[1]}}
         state.update(L=L, C=C, cp=cp, cut=cut, cms=cms, be=be, ms1=int(ms1[0].item()), cdev=cdev.cpu().numpy(),
                      msK=msK.cpu().numpy(), cid=cid, ndev=ndev, pr=pr)
 
@@ -571,8 +583,12 @@ def main() -> int:
         t_ms.append(e0.elapsed_time(e1))
     cel.timing(False)
     ks_t = cel.kernel_stats(reset=True)
-    launches, tot = ks_t.get("k_tlevel_sweep", (1, float("nan")))
-    tlevel_row = {"blevel_with_tlevel_ms": sorted(t_ms)[1], "k_tlevel_sweep_ms": tot / max(launches, 1)}
+    tk = "k_tlevel_policy" if "k_tlevel_policy" in ks_t else "k_tlevel_sweep"
+    launches, tot = ks_t.get(tk, (1, float("nan")))
+    (pb_, ib_), (pt_, it_) = cel.blevel_info()
+    tlevel_row = {"blevel_with_tlevel_ms": sorted(t_ms)[1], "kernel": tk,
+                  "kernel_ms": tot / max(launches, 1),
+                  "iterations": {"blevel": ib_ if pb_ == 0 else None, "tlevel": it_ if pt_ == 0 else None}}
 
     cpd_row, ndev_cpd, cid_cpd, C_cpd = cpd_compare(cel, torch, g, d, bl_t, tl_t, pr_t, lev, lp, L)
     model_row = None
@@ -591,7 +607,8 @@ def main() -> int:
                kstats.items()}
 
     # roofline of the dominant kernel of the measured (b-level + makespan) pass
-    dom = max(("k_blevel_sweep", "k_makespan_one"), key=lambda k: kernels[k]["avg_ms"])
+    dom = max((k for k in ("k_blevel_policy", "k_blevel_sweep", "k_makespan_one") if k in kernels),
+              key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches_per_step"])
     B = algorithmic_bytes(dom, n, m, 1)
     t_dom = kernels[dom]["avg_ms"] * 1e-3
     achieved = B / t_dom / 1e9
@@ -599,27 +616,29 @@ def main() -> int:
     roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 3),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
                 "traffic": load_traffic(dom), "algorithmic_bytes": B,
-                "ns_per_level": round(t_dom * 1e9 / L, 1)}
-    # depth-latency ceiling of the measured pass: b-level and makespan are chains
-    # of L dependent levels each; a level cannot take less than the dependent
-    # step the library's probe measures on this GPU right now (one wave: LDS
-    # gather -> 64-bit segmented max-plus DPP scan -> LDS write), so the pass
-    # cannot beat 2 L such steps whatever the bandwidth
+                "launch_ms": round(t_dom * 1e3, 4)}
+    # how the pass ran: policy iterations of the b-level, relaxation rounds of
+    # the makespan (each a few whole-GPU passes), against the floor of any
+    # level-synchronous method: b-level and makespan as chains of L dependent
+    # levels each, a level no faster than the dependent step the library's
+    # probe measures on this GPU right now (one wave: LDS gather -> 64-bit
+    # segmented max-plus DPP scan -> LDS write)
+    roofline["passes"] = state.get("passes")
     probe = {name: round(cel.step_latency(v, 200000), 1)
              for v, name in ((0, "wave_lds_ns"), (1, "block_barrier_ns"), (2, "wave_l2_ns"))}
     t_level_ns = probe["wave_lds_ns"]
     B_pass = algorithmic_bytes("k_blevel_sweep", n, m, 1) + algorithmic_bytes("k_makespan_one",
                                                                               n, m, 1)
     floor_s = 2 * L * t_level_ns * 1e-9
-    roofline["depth_ceiling"] = {
+    roofline["level_sync_floor"] = {
         "t_level_ns": t_level_ns, "probe": probe, "levels": L,
         "pass_floor_ms": round(floor_s * 1e3, 3),
         "frac_ceiling": round(B_pass / floor_s / 1e9 / HBM_PEAK_GBS, 5),
+        "eval_ms": round(eval_ms, 3),
         "frac_pass": round(B_pass / (eval_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 6)}
     # the level sweeps are chains of L dependent levels: per-level latency
     per_level = {k: round(kernels[k]["avg_ms"] * 1e6 / L, 1)
-                 for k in ("k_kahn", "k_blevel_sweep", "k_makespan_one", "k_makespan_batch")
-                 if k in kernels}
+                 for k in ("k_kahn", "k_blevel_sweep", "k_makespan_batch") if k in kernels}
     for k, v in kernels.items():
         b_ = algorithmic_bytes(k, n, m, BATCH if k == "k_makespan_batch" else 1)
         if b_ is not None:

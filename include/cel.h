@@ -342,6 +342,23 @@ int cel_kernel_stats(char *buf, int buflen, int reset);
  * Errors: CEL_E_ARG (NULL argument). */
 int cel_makespan_info(int32_t *path, int32_t *rounds);
 
+/* Diagnostics: how the calling thread's last cel_blevel call found its
+ * longest paths.  info[0] = 0: the b-level by policy iteration (each node
+ * follows one successor; pointer jumping sums the chains; nodes switch to a
+ * successor of larger value until none can), exact after info[1] iterations;
+ * 1: by the level sweep (after info[1] iterations that did not converge
+ * within their budget, or 0 when policy iteration was not tried).  info[2],
+ * info[3]: the same for the t-level (info[2] = 2: not requested).
+ * Outputs: info [4] (host).
+ * Errors: CEL_E_ARG (NULL argument). */
+int cel_blevel_info(int32_t *info);
+
+/* Diagnostics: cel_blevel_policy(0) makes the calling thread's cel_blevel
+ * calls take the level sweeps directly; 1 (the default) tries policy
+ * iteration first.  Both give the same results.  Returns the previous mode
+ * (CEL_E_ARG for a negative mode). */
+int cel_blevel_policy(int mode);
+
 /* Diagnostics: which K = 1 path the calling thread's cel_makespan and
  * cel_makespan_noalloc calls take.  mode 0: the level sweep directly (path 1
  * without relaxation rounds); 1 (the default): the relaxation first, on as

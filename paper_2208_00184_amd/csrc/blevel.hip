@@ -2,10 +2,13 @@
 // priority order (Section 5.1.3).
 //
 // Nodes are first relabelled into the positions of the level order, so each
-// level is a contiguous range and per-node data is read coalesced.  The sweep
-// over levels (level_sweep, in sweep.hip) pulls, at every node, the values of
-// its successors (b-level, reverse sweep) or predecessors (t-level, forward
-// sweep): no atomics, so the result is exact and independent of scheduling.
+// level is a contiguous range and per-node data is read coalesced.  The
+// longest paths are found by policy iteration (lp_policy.hip), which needs
+// about ten pointer-jumping passes where the levels are many; when it does
+// not converge within its budget, the sweep over levels (sweep.hip) pulls, at
+// every node, the values of its successors (b-level, reverse sweep) or
+// predecessors (t-level, forward sweep).  Both are exact and independent of
+// scheduling.
 #include "cel_internal.h"
 
 namespace cel {
@@ -22,6 +25,16 @@ __global__ void k_node_costs(int32_t n, const int32_t *order, const int64_t *w, 
     wp[p] = wv;
     wcp[p] = comm_off ? wv : wv + comm_of(ob[v], bw, lat);
   }
+}
+
+// per position: the weight of the longest-path recurrences, w + c when the
+// node has successors, w for a sink
+__global__ void k_lp_weights(int32_t n, const int32_t *sptr, const int64_t *wp, const int64_t *wcp,
+                             int64_t *wv, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+       p += (int64_t)gridDim.x * blockDim.x)
+    wv[p] = sptr[p + 1] > sptr[p] ? wcp[p] : wp[p];
 }
 
 // out[order[p]] = val[p] (out may be NULL); *maxout = max val
@@ -66,6 +79,29 @@ using namespace cel;
 
 CEL_PHASE_READER(cel_debug_phases_blevel)
 
+// How the calling thread's last cel_blevel call found its longest paths.
+struct BlInfo {
+  int32_t path_b, iters_b, path_t, iters_t;
+};
+static thread_local BlInfo t_bl_info{1, 0, 2, 0};
+static thread_local int t_lp_mode = 1;
+
+extern "C" int cel_blevel_info(int32_t *info) {
+  if (!info) return set_error(CEL_E_ARG, "cel_blevel_info: NULL argument");
+  info[0] = t_bl_info.path_b;
+  info[1] = t_bl_info.iters_b;
+  info[2] = t_bl_info.path_t;
+  info[3] = t_bl_info.iters_t;
+  return CEL_OK;
+}
+
+extern "C" int cel_blevel_policy(int mode) {
+  if (mode < 0) return set_error(CEL_E_ARG, "cel_blevel_policy: negative mode");
+  const int was = t_lp_mode;
+  t_lp_mode = mode;
+  return was;
+}
+
 extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_t *level,
                           const int32_t *level_ptr, const int32_t *order_id, int32_t L,
                           int32_t flags, int64_t *blevel, int64_t *tlevel, int32_t *prio_order,
@@ -96,31 +132,61 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
   CEL_TRY(relabel_csr(n, g->m, order_id, pos, g->out_ptr, g->out_idx, sptr, sidx, sc, s, st));
   k_node_costs<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order_id, g->w, g->ob, d->bw, d->lat,
                                                      (flags & CEL_COMM_OFF) ? 1 : 0, wp, wcp, st);
-  // The t-level (eq. 2) needs no b-level: its relabelling and sweep run on a
-  // side stream, so the two single-workgroup sweeps overlap on two CUs.  Both
-  // preparations are queued before either plan is read back.
-  SideFork fk;
-  SweepPlan pt, pb;
-  int64_t *tlp = nullptr;
+  // Policy iteration first (b-level, then t-level), whole-GPU kernels one
+  // after the other; what does not converge takes the level sweep.
+  int32_t *pptr = nullptr, *pidx = nullptr;
+  int64_t *tlp = nullptr, *wv;
+  CEL_TRY(sc.get(&wv, n));
+  k_lp_weights<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, sptr, wp, wcp, wv, st);
   if (tlevel && n > 0) {
-    int32_t *pptr, *pidx;
     CEL_TRY(sc.get(&pptr, (int64_t)n + 1));
     CEL_TRY(sc.get(&pidx, g->m));
     CEL_TRY(sc.get(&tlp, n));
+    CEL_TRY(relabel_csr(n, g->m, order_id, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
+  }
+  bool lb = false, lt = false;
+  if (t_lp_mode > 0) {
+    CEL_TRY(lp_policy(n, g->m, L, sptr, sidx, wv, false, blp, &st->i0, "k_blevel_policy", sc, s,
+                      st, &lb));
+    if (tlp)
+      CEL_TRY(lp_policy(n, g->m, L, pptr, pidx, wv, true, tlp, &st->i2, "k_tlevel_policy", sc, s,
+                        st, &lt));
+  }
+  bool sweep_b = true, sweep_t = tlp != nullptr;
+  t_bl_info = {1, 0, tlp ? 1 : 2, 0};
+  if (lb || lt) {
+    Status h;
+    CEL_TRY(read_status(st, &h, s));
+    if (h.err) return status_error(h, fn);
+    if (lb) {
+      sweep_b = !h.i0;
+      t_bl_info.path_b = h.i0 ? 0 : 1;
+      t_bl_info.iters_b = h.i1;
+    }
+    if (lt) {
+      sweep_t = !h.i2;
+      t_bl_info.path_t = h.i2 ? 0 : 1;
+      t_bl_info.iters_t = h.i3;
+    }
+  }
+  // The level sweeps: the t-level (eq. 2) needs no b-level, so its sweep runs
+  // on a side stream and the two single-workgroup sweeps overlap on two CUs.
+  // Both preparations are queued before either plan is read back.
+  SideFork fk;
+  SweepPlan pt, pb;
+  if (sweep_t) {
     CEL_TRY(fk.start(s));
-    const hipStream_t t = fk.side();
-    CEL_TRY(relabel_csr(n, g->m, order_id, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, t, st));
     CEL_TRY(sweep_prepare(pt, false, n, g->m, L, level_ptr, order_id, level, pptr, pidx, wp, wcp,
-                          tlp, sc, t, st));
+                          tlp, sc, fk.side(), st));
   }
-  CEL_TRY(sweep_prepare(pb, true, n, g->m, L, level_ptr, order_id, level, sptr, sidx, wp, wcp, blp,
-                        sc, s, st));
-  if (tlp) {
-    const hipStream_t t = fk.side();
-    CEL_TRY(sweep_run(pt, t, st, "k_tlevel_sweep"));
-    k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, t>>>(n, order_id, tlp, tlevel, st, &st->s1);
-  }
-  CEL_TRY(sweep_run(pb, s, st, "k_blevel_sweep"));
+  if (sweep_b)
+    CEL_TRY(sweep_prepare(pb, true, n, g->m, L, level_ptr, order_id, level, sptr, sidx, wp, wcp,
+                          blp, sc, s, st));
+  if (sweep_t) CEL_TRY(sweep_run(pt, fk.side(), st, "k_tlevel_sweep"));
+  if (tlp)
+    k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, sweep_t ? fk.side() : s>>>(n, order_id, tlp,
+                                                                              tlevel, st, &st->s1);
+  if (sweep_b) CEL_TRY(sweep_run(pb, s, st, "k_blevel_sweep"));
   k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, blp, blevel, st, &st->s0);
   if (prio_order && n > 0) {
     uint64_t *keys;

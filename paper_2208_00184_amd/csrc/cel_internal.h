@@ -485,6 +485,87 @@ __device__ inline void ld_many(int64_t (&x)[N], const int32_t (&q)[N], const int
     if (x[j] < 0) x[j] = ld_final(&gx[q[j]], s_abort, st);
 }
 
+// ---------------------------------------------- grid-wide barrier (cooperative)
+// bar: [0] the released barrier (k << 1 | OR of the bits), [1] abort flag,
+// [2 + b] workgroup b's arrival (k << 1 | its bit); zero before the launch.
+constexpr int32_t kGridSpin = 1 << 20;  // polls of a grid barrier wait before it gives up
+__device__ inline int32_t ld32(const int32_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void st32(int32_t *p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Grid barrier number k (1, 2, ...; all workgroups are co-resident, by
+// cooperative launch) that also ORs one bit over the workgroups.  Thread 0 of
+// workgroup b releases the block's stores (each wave has waited for its own)
+// and publishes (k << 1 | bit) in its own arrival word; workgroup 0 waits
+// until every arrival carries k, ORs the bits and publishes the release word;
+// the others wait for it.  No two workgroups write one word.  Every wait is
+// bounded: one that gives up, or an abort raised anywhere, returns false in
+// every thread of every workgroup.  *bit_out = the OR.
+__device__ inline bool grid_sync(int32_t *bar, int32_t k, int32_t bit, int32_t *s_ok, int32_t *s_bit,
+                                 Status *st, int32_t *bit_out) {
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's stores are complete
+  const int32_t G = (int32_t)gridDim.x;
+  const int32_t mine = (k << 1) | bit;
+  if (blockIdx.x == 0) {
+    __syncthreads();
+    int32_t ok = 1, orb = bit;
+    for (int32_t i = threadIdx.x + 1; i < G; i += (int32_t)blockDim.x) {
+      int32_t v = ld32(&bar[2 + i]);
+      for (int32_t t = 0; (v >> 1) < k; t++) {
+        if (t == kGridSpin || ld32(&bar[1]) != 0) {
+          ok = 0;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        v = ld32(&bar[2 + i]);
+      }
+      if (!ok) break;
+      orb |= v & 1;
+    }
+    ok = __syncthreads_and(ok);
+    orb = __syncthreads_or(orb);
+    if (threadIdx.x == 0) {
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      if (ok) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        st32(&bar[0], (k << 1) | orb);
+      } else {
+        raise_err(st, EB_WAIT);
+        st32(&bar[1], 1);
+      }
+      *s_ok = ok;
+      *s_bit = orb;
+    }
+  } else {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      st32(&bar[2 + blockIdx.x], mine);
+      int32_t ok = 1;
+      int32_t v = ld32(&bar[0]);
+      for (int32_t t = 0; (v >> 1) < k; t++) {
+        if (t == kGridSpin || ld32(&bar[1]) != 0) {
+          raise_err(st, EB_WAIT);
+          st32(&bar[1], 1);
+          ok = 0;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        v = ld32(&bar[0]);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      *s_ok = ok;
+      *s_bit = v & 1;
+    }
+  }
+  __syncthreads();
+  *bit_out = *s_bit;
+  return *s_ok != 0;
+}
+
 // sweep.hip: level sweeps of eq. 3 (rev: b-level over successors) or eq. 2
 // (t-level over predecessors) in position space; out[p] = the value at p.
 struct SweepArgs {
@@ -540,6 +621,13 @@ int ms_ring(int32_t n, int32_t m, int32_t L, const int32_t *lp, const int32_t *g
             const int32_t *level, const int32_t *pptr, const int32_t *pidx, const int64_t *wp,
             const int64_t *cq, const uint8_t *devp, const int64_t *sxp, const int32_t *metap,
             int64_t *finp, int64_t *makespan, class Scratch &sc, hipStream_t s, Status *st);
+// lp_policy.hip: val(p) = wv(p) + max over q in aptr/aidx rows of val(q) by
+// policy iteration on a cooperative grid; out = val (- wv when sub_wv).
+// res[0] = 1 once converged (out written), res[1] = iterations; *launched
+// false when the grid cannot be launched (the caller runs the level sweep).
+int lp_policy(int32_t n, int32_t m, int32_t L, const int32_t *aptr, const int32_t *aidx,
+              const int64_t *wv, bool sub_wv, int64_t *out, int32_t *res, const char *timer,
+              class Scratch &sc, hipStream_t s, Status *st, bool *launched);
 // ms_relax.hip: finish times of one placement by relaxation over the
 // cross-device edges (devp = devices by position).  Queues the preparation
 // and one cooperative kernel on s and sets *launched; st->i3 = 1 once the

@@ -1,0 +1,369 @@
+// Longest paths of a DAG by policy iteration: the b-level (eq. 3) over
+// successors and the t-level (eq. 2) over predecessors, both of the form
+//   val(p) = wv(p) + max over q in adj(p) of val(q)   (wv(p) when adj(p) is empty)
+// with wv(p) = w(p) + c(p) for a node with successors, w(p) for a sink
+// (b-level: val = b-level; t-level: val = t-level + wv).
+//
+// A policy picks one neighbour per node, or none.  Its values are the sums of
+// wv along the chosen pointers until a node without one; pointer jumping finds
+// them all in ceil(log2(longest pointer chain)) + 1 parallel rounds.  Then
+// every node switches to a neighbour of strictly larger value, if it has one,
+// and the next policy is evaluated.  Each policy's values are lengths of real
+// paths, so no value exceeds the longest path; a switch never lowers a value;
+// when no node can switch, every value equals wv plus the largest neighbour
+// value, the recurrence whose solution on a DAG is unique: the values are
+// exact.  A node h hops above the sinks (b-level) is exact after at most h + 1
+// iterations, and on the transformer graphs about ten suffice where the level
+// sweeps need one dependent step per level (10,565 on transformer-96).
+//
+// One cooperative kernel runs everything; grid barriers (grid_sync) separate
+// the phases.  Neighbour lists of more than kLpLight entries are split into
+// chunks of kLpChunk, each taken by one wave, and combined after a barrier.
+#include <map>
+#include <mutex>
+
+#include "cel_internal.h"
+
+namespace cel {
+
+constexpr int kLpB = 1024;        // threads per workgroup
+constexpr int kLpLight = 64;      // longer neighbour lists are split into chunks
+constexpr int kLpChunk = 4096;    // entries of a chunk (one wave)
+constexpr int kLpU = 4;           // nodes per thread with loads in flight together
+
+struct LpE {       // one node's state during pointer jumping
+  int64_t v;       // sum of wv from the node up to (not including) nxt
+  int32_t nxt;     // next node on the pointer chain, -1 at its end
+  int32_t pad;
+};
+
+struct LpArgs {
+  int32_t n, cap, max_rounds;
+  const int32_t *aptr, *aidx;     // adjacency (positions)
+  const int64_t *wv;              // [n]
+  const int32_t *hoff;            // [n + 1] first chunk of each node (chunks only for long lists)
+  const int32_t *hnode;           // [H] node of each chunk
+  int32_t *pol;                   // [n] the policy
+  LpE *e0, *e1;                   // [n] each
+  int64_t *hval;                  // [H] best value of each chunk
+  int32_t *hidx;                  // [H] ... and its neighbour
+  int32_t *bar;                   // grid barrier words [2 + gridDim]
+  int64_t *out;                   // [n] results
+  Status *st;
+  int32_t *res;                   // [0] converged, [1] iterations
+};
+
+// larger value first, then the smaller neighbour index
+__device__ inline bool lp_better(int64_t v, int32_t q, int64_t bv, int32_t bq) {
+  return v > bv || (v == bv && q < bq);
+}
+
+__global__ void k_lp_heavy_count(int32_t n, const int32_t *aptr, int32_t *hcnt, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t d = aptr[p + 1] - aptr[p];
+    hcnt[p] = d > kLpLight ? (d + kLpChunk - 1) / kLpChunk : 0;
+  }
+}
+
+__global__ void k_lp_heavy_fill(int32_t n, const int32_t *hoff, int32_t *hnode, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+       p += (int64_t)gridDim.x * blockDim.x)
+    for (int32_t c = hoff[p]; c < hoff[p + 1]; c++) hnode[c] = (int32_t)p;
+}
+
+// SUB: out = val - wv (the t-level); a template parameter so that the two
+// directions are told apart in profiles
+template <bool SUB>
+__global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
+  __shared__ int32_t s_ok, s_bit;
+  Status *st = a.st;
+  if (failed(st)) return;
+  const int32_t n = a.n;
+  const int64_t gsz = (int64_t)gridDim.x * kLpB;
+  const int64_t gid = (int64_t)blockIdx.x * kLpB + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int32_t H = a.hoff[n];
+  int32_t bar = 0, bit;
+  // the empty policy: every node alone
+  for (int64_t p = gid; p < n; p += gsz) {
+    a.e0[p] = LpE{a.wv[p], -1, 0};
+    a.pol[p] = -1;
+  }
+  if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
+  LpE *cur = a.e0, *oth = a.e1;
+  int32_t it = 0;
+  bool done = false;
+  for (; it < a.cap; it++) {
+    // ---- improvement: the best neighbour under the current values
+    // chunks of long lists, one wave each
+    const int64_t wid = gid >> 6, nw = gsz >> 6;
+    for (int64_t c = wid; c < H; c += nw) {
+      const int32_t p = a.hnode[c];
+      const int32_t e0 = a.aptr[p] + (int32_t)(c - a.hoff[p]) * kLpChunk;
+      const int32_t e1 = min(a.aptr[p + 1], e0 + kLpChunk);
+      int64_t bv = -1;
+      int32_t bq = INT32_MAX;
+      for (int32_t e = e0 + lane; e < e1; e += 64) {
+        const int32_t q = a.aidx[e];
+        const int64_t v = ld_coherent(&cur[q].v);
+        if (lp_better(v, q, bv, bq)) {
+          bv = v;
+          bq = q;
+        }
+      }
+      for (int o = 32; o > 0; o >>= 1) {
+        const int64_t v = __shfl_xor((long long)bv, o);
+        const int32_t q = __shfl_xor(bq, o);
+        if (lp_better(v, q, bv, bq)) {
+          bv = v;
+          bq = q;
+        }
+      }
+      if (lane == 0) {
+        st_coherent(&a.hval[c], bv);
+        a.hidx[c] = bq;
+      }
+    }
+    int32_t chg = 0;
+    // short lists, one thread per node, kLpU nodes with loads in flight
+    for (int64_t p0 = gid; p0 < n; p0 += kLpU * gsz) {
+      int32_t b0[kLpU], b1[kLpU], pq[kLpU];
+#pragma unroll
+      for (int u = 0; u < kLpU; u++) {
+        const int64_t p = p0 + u * gsz;
+        b0[u] = b1[u] = 0;
+        pq[u] = -1;
+        if (p < n) {
+          b0[u] = a.aptr[p];
+          b1[u] = a.aptr[p + 1];
+          pq[u] = a.pol[p];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kLpU; u++) {
+        const int64_t p = p0 + u * gsz;
+        const int32_t d = b1[u] - b0[u];
+        if (p >= n || d == 0 || d > kLpLight) continue;
+        int64_t bv = -1;
+        int32_t bq = INT32_MAX;
+        for (int32_t e = b0[u]; e < b1[u]; e++) {
+          const int32_t q = a.aidx[e];
+          const int64_t v = ld_coherent(&cur[q].v);
+          if (lp_better(v, q, bv, bq)) {
+            bv = v;
+            bq = q;
+          }
+        }
+        const int64_t cv = pq[u] >= 0 ? ld_coherent(&cur[pq[u]].v) : -1;
+        if (bv > cv) {
+          a.pol[p] = bq;
+          chg = 1;
+        }
+      }
+    }
+    if (H > 0) {  // combine the chunks of each long list
+      if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
+      for (int64_t c = gid; c < H; c += gsz) {
+        const int32_t p = a.hnode[c];
+        if (c != a.hoff[p]) continue;  // the node's first chunk combines
+        int64_t bv = -1;
+        int32_t bq = INT32_MAX;
+        for (int32_t k = (int32_t)c; k < a.hoff[p + 1]; k++) {
+          const int64_t v = ld_coherent(&a.hval[k]);
+          const int32_t q = a.hidx[k];
+          if (lp_better(v, q, bv, bq)) {
+            bv = v;
+            bq = q;
+          }
+        }
+        const int32_t pq = a.pol[p];
+        const int64_t cv = pq >= 0 ? ld_coherent(&cur[pq].v) : -1;
+        if (bv > cv) {
+          a.pol[p] = bq;
+          chg = 1;
+        }
+      }
+    }
+    chg = __syncthreads_or(chg);
+    if (!grid_sync(a.bar, ++bar, chg, &s_ok, &s_bit, st, &bit)) return;
+    if (!bit) {
+      done = true;
+      break;
+    }
+    // ---- evaluation of the new policy by pointer jumping; the first round
+    // reads the policy itself (cur is free: nothing reads it any more)
+    int32_t more = 0;
+    for (int64_t p0 = gid; p0 < n; p0 += kLpU * gsz) {
+      int32_t q[kLpU];
+#pragma unroll
+      for (int u = 0; u < kLpU; u++) {
+        const int64_t p = p0 + u * gsz;
+        q[u] = p < n ? a.pol[p] : -1;
+      }
+      int64_t wq[kLpU];
+      int32_t nq[kLpU];
+#pragma unroll
+      for (int u = 0; u < kLpU; u++) {
+        wq[u] = q[u] >= 0 ? a.wv[q[u]] : 0;
+        nq[u] = q[u] >= 0 ? a.pol[q[u]] : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < kLpU; u++) {
+        const int64_t p = p0 + u * gsz;
+        if (p >= n) continue;
+        more |= nq[u] >= 0;
+        cur[p] = LpE{a.wv[p] + wq[u], nq[u], 0};
+      }
+    }
+    more = __syncthreads_or(more);
+    if (!grid_sync(a.bar, ++bar, more, &s_ok, &s_bit, st, &bit)) return;
+    int32_t r = 1;
+    while (bit) {
+      if (r == a.max_rounds) {  // a pointer cycle: the input is not a DAG
+        raise_err(st, EB_CYCLE);
+        return;  // every workgroup takes this branch: bit and r are uniform
+      }
+      more = 0;
+      for (int64_t p0 = gid; p0 < n; p0 += kLpU * gsz) {
+        LpE x[kLpU];
+#pragma unroll
+        for (int u = 0; u < kLpU; u++) {
+          const int64_t p = p0 + u * gsz;
+          x[u] = p < n ? cur[p] : LpE{0, -1, 0};
+        }
+        LpE y[kLpU];
+#pragma unroll
+        for (int u = 0; u < kLpU; u++) y[u] = x[u].nxt >= 0 ? cur[x[u].nxt] : LpE{0, -1, 0};
+#pragma unroll
+        for (int u = 0; u < kLpU; u++) {
+          const int64_t p = p0 + u * gsz;
+          if (p >= n) continue;
+          const LpE z = x[u].nxt >= 0 ? LpE{x[u].v + y[u].v, y[u].nxt, 0} : x[u];
+          more |= z.nxt >= 0;
+          oth[p] = z;
+        }
+      }
+      more = __syncthreads_or(more);
+      if (!grid_sync(a.bar, ++bar, more, &s_ok, &s_bit, st, &bit)) return;
+      LpE *t = cur;
+      cur = oth;
+      oth = t;
+      r++;
+    }
+  }
+  if (!done) {  // not converged: the caller runs the level sweep
+    if (gid == 0) {
+      a.res[0] = 0;
+      a.res[1] = it;
+    }
+    return;
+  }
+  for (int64_t p = gid; p < n; p += gsz) a.out[p] = cur[p].v - (SUB ? a.wv[p] : 0);
+  if (gid == 0) {
+    a.res[0] = 1;
+    a.res[1] = it + 1;
+  }
+}
+
+// ------------------------------------------------------------------- host
+
+namespace {
+std::mutex g_lp_mu;
+std::map<int, int> g_lp_cus;  // device -> co-resident workgroups of k_lp_policy (one per CU at most)
+
+int lp_groups(int *out) {
+  int dev = 0;
+  CEL_HIP(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lk(g_lp_mu);
+  auto it = g_lp_cus.find(dev);
+  if (it == g_lp_cus.end()) {
+    int cus = 0, coop = 0, nb = 0;
+    CEL_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    CEL_HIP(hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev));
+    if (coop)
+      CEL_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)k_lp_policy<false>,
+                                                           kLpB, 0));
+    it = g_lp_cus.emplace(dev, coop ? cus * (nb < 1 ? nb : 1) : 0).first;
+  }
+  *out = it->second;
+  return CEL_OK;
+}
+}  // namespace
+
+int lp_policy(int32_t n, int32_t m, int32_t L, const int32_t *aptr, const int32_t *aidx,
+              const int64_t *wv, bool sub_wv, int64_t *out, int32_t *res, const char *timer,
+              Scratch &sc, hipStream_t s, Status *st, bool *launched) {
+  *launched = false;
+  if (n <= 0) return CEL_OK;
+  int gmax = 0;
+  CEL_TRY(lp_groups(&gmax));
+  if (gmax < 1) return CEL_OK;
+  const int G = (int)((int64_t)n + kLpB - 1) / kLpB < gmax ? (int)(((int64_t)n + kLpB - 1) / kLpB)
+                                                          : gmax;
+  // pointer chains are at most L nodes long (one per level)
+  int32_t max_rounds = 2;
+  while ((int64_t(1) << (max_rounds - 2)) < L) max_rounds++;
+  // Iterations allowed before the level sweep is cheaper: an iteration costs
+  // about max_rounds barriers and passes over 48 bytes per node, plus one pass
+  // over the neighbour lists; the sweep about 0.6 us per level after 0.5 ms.
+  const double it_us = max_rounds * (5.0 + 48.0 * n / 4.0e6) + 12.0 * m / 4.0e6;
+  const double sweep_us = 500.0 + 0.6 * L;
+  int32_t cap = (int32_t)(sweep_us / it_us);
+  if (cap < 2) cap = 2;
+  int32_t *hcnt, *hoff, *hnode, *pol, *hidx, *bar;
+  LpE *e0, *e1;
+  int64_t *hval;
+  CEL_TRY(sc.get(&hcnt, n));
+  CEL_TRY(sc.get(&hoff, (int64_t)n + 1));
+  k_lp_heavy_count<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, aptr, hcnt, st);
+  CEL_TRY(exclusive_scan_i32(hcnt, hoff, n, sc, s));
+  // chunks: at most m / kLpChunk + (nodes with long lists) <= m / kLpChunk + m / kLpLight
+  const int64_t hmax = (int64_t)m / kLpChunk + (int64_t)m / kLpLight + 1;
+  CEL_TRY(sc.get(&hnode, hmax));
+  CEL_TRY(sc.get(&hval, hmax));
+  CEL_TRY(sc.get(&hidx, hmax));
+  CEL_TRY(sc.get(&pol, n));
+  CEL_TRY(sc.get(&e0, n));
+  CEL_TRY(sc.get(&e1, n));
+  CEL_TRY(sc.get(&bar, 2 + (int64_t)G));
+  k_lp_heavy_fill<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, hoff, hnode, st);
+  k_fill_i32<<<1, 256, 0, s>>>(bar, 2 + (int64_t)G, 0);
+  k_fill_i32<<<1, 64, 0, s>>>(res, 2, 0);
+  CEL_HIP(hipGetLastError());
+  LpArgs a{};
+  a.n = n;
+  a.cap = cap;
+  a.max_rounds = max_rounds;
+  a.aptr = aptr;
+  a.aidx = aidx;
+  a.wv = wv;
+  a.hoff = hoff;
+  a.hnode = hnode;
+  a.pol = pol;
+  a.e0 = e0;
+  a.e1 = e1;
+  a.hval = hval;
+  a.hidx = hidx;
+  a.bar = bar;
+  a.out = out;
+  a.st = st;
+  a.res = res;
+  void *args[] = {&a};
+  hipError_t e;
+  {
+    KTimer kt(s, timer);
+    const void *k = sub_wv ? (const void *)k_lp_policy<true> : (const void *)k_lp_policy<false>;
+    e = hipLaunchCooperativeKernel(k, dim3(G), dim3(kLpB), args, 0, s);
+  }
+  if (e != hipSuccess) {  // not launched: the caller takes the level sweep
+    (void)hipGetLastError();
+    return CEL_OK;
+  }
+  *launched = true;
+  return CEL_OK;
+}
+
+}  // namespace cel

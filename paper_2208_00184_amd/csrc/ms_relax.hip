@@ -52,7 +52,6 @@ constexpr int kRxW = kRxB / 64;
 constexpr int kRxCB = 1024;      // positions per block of the counting sort
 constexpr int kRxGroup = 4;      // tiles whose gathers are in flight together
 constexpr int kRxHeavy = 8;      // more predecessors: the whole wave gathers them
-constexpr int32_t kRxSpin = 1 << 20;  // polls of a grid barrier wait before it gives up
 
 __device__ inline uint64_t lanemask_le(int lane) {
   return lane == 63 ? ~0ull : ((1ull << (lane + 1)) - 1);
@@ -181,83 +180,6 @@ struct RxArgs {
                           // [2 + b] workgroup b's arrival (k << 1 | its bit)
   int64_t *start, *finish, *makespan;
 };
-
-__device__ inline int32_t ld32(const int32_t *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline void st32(int32_t *p, int32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Grid barrier number k (1, 2, ...; all workgroups are co-resident, by
-// cooperative launch) that also ORs one bit over the workgroups.  Thread 0 of
-// workgroup b releases the block's stores (each wave has waited for its own)
-// and publishes (k << 1 | bit) in its own arrival word; workgroup 0 waits
-// until every arrival carries k, ORs the bits and publishes the release word;
-// the others wait for it.  No two workgroups write one word.  Every wait is
-// bounded: one that gives up, or an abort raised anywhere, returns false in
-// every thread of every workgroup.  *bit_out = the OR.
-__device__ inline bool rx_grid_sync(const RxArgs &a, int32_t k, int32_t bit, int32_t *s_ok,
-                                    int32_t *s_bit, Status *st, int32_t *bit_out) {
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's stores are complete
-  const int32_t G = (int32_t)gridDim.x;
-  const int32_t mine = (k << 1) | bit;
-  if (blockIdx.x == 0) {
-    __syncthreads();
-    int32_t ok = 1, orb = bit;
-    for (int32_t i = threadIdx.x + 1; i < G; i += kRxB) {
-      int32_t v = ld32(&a.bar[2 + i]);
-      for (int32_t t = 0; (v >> 1) < k; t++) {
-        if (t == kRxSpin || ld32(&a.bar[1]) != 0) {
-          ok = 0;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-        v = ld32(&a.bar[2 + i]);
-      }
-      if (!ok) break;
-      orb |= v & 1;
-    }
-    ok = __syncthreads_and(ok);
-    orb = __syncthreads_or(orb);
-    if (threadIdx.x == 0) {
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      if (ok) {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        st32(&a.bar[0], (k << 1) | orb);
-      } else {
-        raise_err(st, EB_WAIT);
-        st32(&a.bar[1], 1);
-      }
-      *s_ok = ok;
-      *s_bit = orb;
-    }
-  } else {
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-      st32(&a.bar[2 + blockIdx.x], mine);
-      int32_t ok = 1;
-      int32_t v = ld32(&a.bar[0]);
-      for (int32_t t = 0; (v >> 1) < k; t++) {
-        if (t == kRxSpin || ld32(&a.bar[1]) != 0) {
-          raise_err(st, EB_WAIT);
-          st32(&a.bar[1], 1);
-          ok = 0;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-        v = ld32(&a.bar[0]);
-      }
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      *s_ok = ok;
-      *s_bit = v & 1;
-    }
-  }
-  __syncthreads();
-  *bit_out = *s_bit;
-  return *s_ok != 0;
-}
 
 template <int NT>
 __global__ void __launch_bounds__(kRxB) k_rx_relax(RxArgs a, Status *st) {
@@ -401,7 +323,7 @@ __global__ void __launch_bounds__(kRxB) k_rx_relax(RxArgs a, Status *st) {
       wc[k] = q < n ? a.wxc[q] : 0;
     }
     int32_t any;
-    if (!rx_grid_sync(a, ++bar, 0, &s_ok, &s_bit, st, &any)) return;
+    if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &any)) return;
     // carry from the earlier blocks of the chain through lo
     int64_t carry = kNeg;
     if (sb >= 0) {
@@ -438,7 +360,7 @@ __global__ void __launch_bounds__(kRxB) k_rx_relax(RxArgs a, Status *st) {
     if (__ballot(chg) && lane == 0) s_chg = 1;  // LDS store; read after the barrier's __syncthreads
     __syncthreads();
     const int32_t mychg = s_chg;
-    if (!rx_grid_sync(a, ++bar, mychg, &s_ok, &s_bit, st, &any)) return;
+    if (!grid_sync(a.bar, ++bar, mychg, &s_ok, &s_bit, st, &any)) return;
     if (tid == 0) s_chg = 0;  // the next round's flag (read only after two more barriers)
     if (!any) break;
   }

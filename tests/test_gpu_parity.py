@@ -69,16 +69,25 @@ def assert_topo_blevel(wl, ref_t, ref_b, got_t, got_b):
 # ------------------------------------------------------------ configs 1-3, 5
 
 
+@pytest.fixture(params=[1, 0], ids=["policy", "sweep"])
+def bl_path(request):
+    """b-level and t-level by policy iteration (falling back to the level
+    sweeps when it does not converge) or by the level sweeps."""
+    was = cel.blevel_policy(request.param)
+    yield request.param
+    cel.blevel_policy(was)
+
+
 @pytest.mark.parametrize("cfg,seed", [(1, 0), (1, 1), (1, 2), (2, 0), (2, 1), (3, 0), (3, 2),
                                       (5, 0)])
-def test_topo_blevel_configs(cfg, seed):
+def test_topo_blevel_configs(cfg, seed, bl_path):
     wl, rt, rb = config(cfg, seed)
     _, _, gt, gb = run_topo_blevel(wl)
     assert_topo_blevel(wl, rt, rb, gt, gb)
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3])
-def test_blevel_comm_off(cfg):
+def test_blevel_comm_off(cfg, bl_path):
     wl, rt, _ = config(cfg, 0)
     lev, oid, lp, L = rt
     ref = O.blevel(wl, lev, oid, comm_off=True)
@@ -89,7 +98,7 @@ def test_blevel_comm_off(cfg):
     assert np.array_equal(np_(bl), ref[0]) and np.array_equal(np_(pr), ref[2])
 
 
-def test_blevel_tlevel_on_caller_streams():
+def test_blevel_tlevel_on_caller_streams(bl_path):
     """The t-level sweep runs on a side stream joined back into the caller's
     stream: results must be complete when the call returns, on the default
     stream and on user streams used in turn (the side stream is shared)."""
@@ -451,7 +460,7 @@ def test_makespan_batch_rows_gather():
 # ---------------------------------------------------------- random small DAGs
 
 
-def test_random_dags(ms_path):
+def test_random_dags(ms_path, bl_path):
     for s in range(40):
         n = 1 + (s * 37) % 300
         wl = make_random_dag(1000 + s, n, p_edge=min(0.5, 4.0 / max(n, 1)), D=1 + s % 7,
@@ -508,7 +517,7 @@ def test_heavy_fanout_node():
     assert_topo_blevel(wl, rt, rb, gt, gb)
 
 
-def test_heavy_window_nodes(ms_path):
+def test_heavy_window_nodes(ms_path, bl_path):
     """Nodes with more neighbours than a sweep window holds edges: a source with
     9,999 successors (b-level), a sink with 10,000 predecessors (t-level and
     makespan), both between ordinary levels, for every sweep and both
@@ -537,7 +546,7 @@ def test_heavy_window_nodes(ms_path):
     assert np_(ms1)[0] == ref_ms[1] and np.array_equal(np_(fi1)[0], ref_fi[1])
 
 
-def test_sweep_many_near_neighbours():
+def test_sweep_many_near_neighbours(bl_path):
     """Narrow levels (1..150 nodes) where about one node in 20 has 9..300
     successors or predecessors within the next few levels: the b-level and
     t-level sweeps gather those along slot lists instead of pull records, and
@@ -618,7 +627,7 @@ def _grid_level_dag(seed):
     return wl, nl
 
 
-def test_sweep_grid_levels():
+def test_sweep_grid_levels(bl_path):
     """Levels of at least 16,384 nodes or edges run on the whole GPU between
     single-workgroup segments, in both sweep directions; rows of more than 64
     neighbours there are split over workgroups (the 24,375-successor source in
@@ -948,6 +957,14 @@ def test_full_path_large(cfg):
     rb = O.blevel(wl, rt[0], rt[1])
     g, d, gt, gb = run_topo_blevel(wl)
     assert_topo_blevel(wl, rt, rb, gt, gb)
+    assert [p for p, _ in cel.blevel_info()] == [0, 0]  # both by policy iteration
+    was = cel.blevel_policy(0)  # and by the level sweeps
+    try:
+        gb0 = cel.blevel(g, d, gt[0], gt[2], gt[1], gt[3], want_tlevel=True)
+        assert cel.blevel_info() == ((1, 0), (1, 0))
+    finally:
+        cel.blevel_policy(was)
+    assert_topo_blevel(wl, rt, rb, gt, gb0)
     rc = O.cluster(wl, rb[2], 200, -1)
     cid, C, cut = cel.cluster(g, d, gb[2], 200, -1)
     assert C == rc[1] and cut == rc[2] and np.array_equal(np_(cid), rc[0])

@@ -1,0 +1,96 @@
+"""GPU parity of the b-level (eq. 3) and t-level (eq. 2) by policy iteration
+(cel_blevel), against the CPU oracle, tolerance 0, with the path each call
+took (cel_blevel_info)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU, skipped there
+    pytest.skip("needs a ROCm GPU", allow_module_level=True)
+
+import paper_2208_00184_amd as cel  # noqa: E402
+from oracle import oracle as O  # noqa: E402
+from workloads import from_edges, make_config  # noqa: E402
+
+DEV = "cuda:0"
+
+
+def np_(t):
+    return t.detach().cpu().numpy()
+
+
+def tt(a, dt):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=dt)).to(DEV)
+
+
+def run(wl, comm_off=False):
+    lev, oid, lp, L = O.topo_levels(wl)
+    ref = O.blevel(wl, lev, oid, comm_off=comm_off)
+    g, d = cel.Graph.from_arrays(wl, DEV), cel.Devices.from_arrays(wl)
+    bl, tl, pr, cp = cel.blevel(g, d, tt(lev, np.int32), tt(lp, np.int32), tt(oid, np.int32), L,
+                                comm_off=comm_off, want_tlevel=True)
+    info = cel.blevel_info()
+    assert cp == ref[3]
+    assert np.array_equal(np_(bl), ref[0]) and np.array_equal(np_(tl), ref[1])
+    assert np.array_equal(np_(pr), ref[2])
+    return L, info
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_policy_converges_on_configs(cfg):
+    """Both longest paths by policy iteration, exact; a node h hops from the
+    end of its paths is exact after h + 1 iterations, so at most L + 1 run."""
+    L, info = run(make_config(cfg, 0))
+    for path, iters in info:
+        assert path == 0 and 1 <= iters <= L + 1
+
+
+def test_policy_budget_then_sweep():
+    """Layered-200k (196 levels, parents from up to 8 levels back) needs more
+    iterations than its budget: the level sweeps give the exact values."""
+    L, info = run(make_config(5, 0))
+    for path, iters in info:
+        assert path in (0, 1) and iters >= 1
+
+
+def test_policy_ties_and_zero_costs():
+    """Many equal values: zero compute and comm everywhere but a few nodes,
+    a diamond lattice of equal-length paths (values spread one level per
+    iteration here, so the budget may run out before the sweep's cost: either
+    path, exact)."""
+    n, W = 4000, 40
+    edges = []
+    for v in range(W, n):
+        lvl, j = divmod(v, W)
+        edges.append(((lvl - 1) * W + j, v))
+        edges.append(((lvl - 1) * W + (j + 1) % W, v))
+    rng = np.random.default_rng(4)
+    w = np.zeros(n, np.int64)
+    w[rng.choice(n, 10, replace=False)] = 5
+    wl = from_edges(n, edges, w, np.zeros(n, np.int64), 2, [10 ** 9] * 2, 1, 0)
+    L, info = run(wl)
+    for path, iters in info:
+        assert path in (0, 1) and 1 <= iters <= L + 1
+    run(wl, comm_off=True)
+
+
+def test_policy_long_lists_both_ways():
+    """A source with 20,000 successors (five chunks of the b-level's long-list
+    path) and a sink with 12,000 predecessors (the t-level's), between chains."""
+    rng = np.random.default_rng(8)
+    n = 33000
+    edges = [(0, j) for j in range(1, 20001)]
+    edges += [(j, 32999) for j in range(20001, 32999)]
+    edges += [(j, 20001 + int(rng.integers(0, 12998))) for j in range(1, 20001)]
+    edges += [(j, j + 1) for j in range(20001, 32998, 7)]
+    edges = sorted(set((u, v) for u, v in edges if u < v))
+    wl = from_edges(n, edges, rng.integers(1, 90, n), rng.integers(0, 3000, n), 4,
+                    [10 ** 12] * 4, 5, 3)
+    L, info = run(wl)
+    for path, iters in info:
+        assert path == 0 and iters <= L + 1
