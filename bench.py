@@ -69,8 +69,9 @@ CSRC = os.path.join(ROOT, "paper_2208_00184_amd", "csrc")
 PMC_KERNELS = {
     "k_makespan_one": ("cel::k_rx_relax<", ["ms_relax.hip", "cel_internal.h"]),
     "k_makespan_sweep_one": ("cel::k_ms_ring(", ["ms_ring.hip", "cel_internal.h"]),
-    "k_blevel_policy": ("cel::k_lp_policy<false>", ["lp_policy.hip", "cel_internal.h"]),
-    "k_tlevel_policy": ("cel::k_lp_policy<true>", ["lp_policy.hip", "cel_internal.h"]),
+    "k_blevel_policy": ("cel::k_lp_policy<0>", ["lp_policy.hip", "cel_internal.h"]),
+    "k_tlevel_policy": ("cel::k_lp_policy<1>", ["lp_policy.hip", "cel_internal.h"]),
+    "k_levels_policy": ("cel::k_lp_policy<2>", ["lp_policy.hip", "cel_internal.h"]),
     "k_blevel_sweep": ("cel::k_ring_sweep<true>", ["sweep.hip", "cel_internal.h"]),
     "k_tlevel_sweep": ("cel::k_ring_sweep<false>", ["sweep.hip", "cel_internal.h"]),
     "k_makespan_batch": ("cel::k_mb_ring(", ["ms_batch.hip", "cel_internal.h"]),

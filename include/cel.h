@@ -353,11 +353,21 @@ int cel_makespan_info(int32_t *path, int32_t *rounds);
  * Errors: CEL_E_ARG (NULL argument). */
 int cel_blevel_info(int32_t *info);
 
-/* Diagnostics: cel_blevel_policy(0) makes the calling thread's cel_blevel
- * calls take the level sweeps directly; 1 (the default) tries policy
- * iteration first.  Both give the same results.  Returns the previous mode
- * (CEL_E_ARG for a negative mode). */
-int cel_blevel_policy(int mode);
+/* Diagnostics: how the calling thread's last cel_topo_levels call found the
+ * levels.  info[0] = 0: by policy iteration over the predecessors (graphs of
+ * 16,384 nodes and more), exact after info[1] iterations; 1: by Kahn's
+ * level-synchronous kernel (after info[1] iterations that did not converge
+ * within their budget of 12, or 0 when policy iteration was not tried).
+ * Outputs: info [2] (host).
+ * Errors: CEL_E_ARG (NULL argument). */
+int cel_topo_levels_info(int32_t *info);
+
+/* Diagnostics: cel_policy_iteration(0) makes the calling thread's
+ * cel_topo_levels and cel_blevel calls take Kahn's kernel and the level
+ * sweeps directly; 1 (the default) tries policy iteration first.  Both give
+ * the same results.  Returns the previous mode (CEL_E_ARG for a negative
+ * mode). */
+int cel_policy_iteration(int mode);
 
 /* Diagnostics: which K = 1 path the calling thread's cel_makespan and
  * cel_makespan_noalloc calls take.  mode 0: the level sweep directly (path 1

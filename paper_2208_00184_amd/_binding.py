@@ -21,7 +21,8 @@ COMM_OFF = 1
 CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
 EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_dfs_order", "cel_cluster", "cel_place", "cel_place_ext", "cel_makespan", "cel_makespan_noalloc",
-           "cel_makespan_info", "cel_makespan_relax", "cel_blevel_info", "cel_blevel_policy",
+           "cel_makespan_info", "cel_makespan_relax", "cel_blevel_info", "cel_policy_iteration",
+           "cel_topo_levels_info",
            "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_colocate", "cel_step_latency", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
@@ -95,8 +96,10 @@ def lib() -> C.CDLL:
         L.cel_makespan_relax.restype = C.c_int
         L.cel_blevel_info.argtypes = [C.POINTER(i32)]
         L.cel_blevel_info.restype = C.c_int
-        L.cel_blevel_policy.argtypes = [C.c_int]
-        L.cel_blevel_policy.restype = C.c_int
+        L.cel_policy_iteration.argtypes = [C.c_int]
+        L.cel_policy_iteration.restype = C.c_int
+        L.cel_topo_levels_info.argtypes = [C.POINTER(i32)]
+        L.cel_topo_levels_info.restype = C.c_int
         _lib = L
     return _lib
 
@@ -148,10 +151,19 @@ def blevel_info() -> tuple:
     return (info[0], info[1]), (info[2], info[3])
 
 
-def blevel_policy(mode: int) -> int:
-    """b-/t-level path of the calling thread: 0 = the level sweeps, 1 = policy
-    iteration first (default); returns the previous mode."""
-    r = lib().cel_blevel_policy(int(mode))
+def topo_levels_info() -> tuple:
+    """(path, iterations) of the calling thread's last topo_levels call: path
+    0 = policy iteration, 1 = Kahn's level-synchronous kernel."""
+    info = (C.c_int32 * 2)()
+    _check(lib().cel_topo_levels_info(info))
+    return info[0], info[1]
+
+
+def policy_iteration(mode: int) -> int:
+    """Levels, b-level and t-level path of the calling thread: 0 = Kahn's
+    kernel and the level sweeps, 1 = policy iteration first (default);
+    returns the previous mode."""
+    r = lib().cel_policy_iteration(int(mode))
     if r < 0:
         _check(r)
     return r

@@ -86,6 +86,10 @@ struct BlInfo {
 static thread_local BlInfo t_bl_info{1, 0, 2, 0};
 static thread_local int t_lp_mode = 1;
 
+namespace cel {
+bool policy_iteration_on() { return t_lp_mode > 0; }
+}  // namespace cel
+
 extern "C" int cel_blevel_info(int32_t *info) {
   if (!info) return set_error(CEL_E_ARG, "cel_blevel_info: NULL argument");
   info[0] = t_bl_info.path_b;
@@ -95,8 +99,8 @@ extern "C" int cel_blevel_info(int32_t *info) {
   return CEL_OK;
 }
 
-extern "C" int cel_blevel_policy(int mode) {
-  if (mode < 0) return set_error(CEL_E_ARG, "cel_blevel_policy: negative mode");
+extern "C" int cel_policy_iteration(int mode) {
+  if (mode < 0) return set_error(CEL_E_ARG, "cel_policy_iteration: negative mode");
   const int was = t_lp_mode;
   t_lp_mode = mode;
   return was;
@@ -145,11 +149,11 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
     CEL_TRY(relabel_csr(n, g->m, order_id, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
   }
   bool lb = false, lt = false;
-  if (t_lp_mode > 0) {
-    CEL_TRY(lp_policy(n, g->m, L, sptr, sidx, wv, false, blp, &st->i0, "k_blevel_policy", sc, s,
+  if (policy_iteration_on()) {
+    CEL_TRY(lp_policy(n, g->m, L, 0, sptr, sidx, wv, 0, blp, &st->i0, "k_blevel_policy", sc, s,
                       st, &lb));
     if (tlp)
-      CEL_TRY(lp_policy(n, g->m, L, pptr, pidx, wv, true, tlp, &st->i2, "k_tlevel_policy", sc, s,
+      CEL_TRY(lp_policy(n, g->m, L, 0, pptr, pidx, wv, 1, tlp, &st->i2, "k_tlevel_policy", sc, s,
                         st, &lt));
   }
   bool sweep_b = true, sweep_t = tlp != nullptr;

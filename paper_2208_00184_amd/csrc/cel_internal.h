@@ -622,12 +622,18 @@ int ms_ring(int32_t n, int32_t m, int32_t L, const int32_t *lp, const int32_t *g
             const int64_t *cq, const uint8_t *devp, const int64_t *sxp, const int32_t *metap,
             int64_t *finp, int64_t *makespan, class Scratch &sc, hipStream_t s, Status *st);
 // lp_policy.hip: val(p) = wv(p) + max over q in aptr/aidx rows of val(q) by
-// policy iteration on a cooperative grid; out = val (- wv when sub_wv).
-// res[0] = 1 once converged (out written), res[1] = iterations; *launched
-// false when the grid cannot be launched (the caller runs the level sweep).
-int lp_policy(int32_t n, int32_t m, int32_t L, const int32_t *aptr, const int32_t *aidx,
-              const int64_t *wv, bool sub_wv, int64_t *out, int32_t *res, const char *timer,
-              class Scratch &sc, hipStream_t s, Status *st, bool *launched);
+// policy iteration on a cooperative grid; out = val (- wv for kind 1, the
+// t-level; kind 0 is the b-level, 2 the levels: they differ only there).  L
+// bounds the pointer chains (nodes); at most cap iterations (cap <= 0: as
+// many as are cheaper than a level sweep of L levels).  res[0] = 1 once
+// converged (out written), res[1] = iterations; *launched false when the
+// grid cannot be launched (the caller runs the level sweep).
+int lp_policy(int32_t n, int32_t m, int32_t L, int32_t cap, const int32_t *aptr,
+              const int32_t *aidx, const int64_t *wv, int kind, int64_t *out, int32_t *res,
+              const char *timer, class Scratch &sc, hipStream_t s, Status *st, bool *launched);
+// whether the calling thread's cel_topo_levels and cel_blevel calls try
+// policy iteration first (cel_policy_iteration)
+bool policy_iteration_on();
 // ms_relax.hip: finish times of one placement by relaxation over the
 // cross-device edges (devp = devices by position).  Queues the preparation
 // and one cooperative kernel on s and sets *launched; st->i3 = 1 once the

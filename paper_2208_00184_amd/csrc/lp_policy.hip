@@ -74,9 +74,9 @@ __global__ void k_lp_heavy_fill(int32_t n, const int32_t *hoff, int32_t *hnode, 
     for (int32_t c = hoff[p]; c < hoff[p + 1]; c++) hnode[c] = (int32_t)p;
 }
 
-// SUB: out = val - wv (the t-level); a template parameter so that the two
-// directions are told apart in profiles
-template <bool SUB>
+// KIND: 0 the b-level, 1 the t-level (out = val - wv), 2 the levels of Kahn's
+// ordering; a template parameter so that profiles tell the three apart
+template <int KIND>
 __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
   __shared__ int32_t s_ok, s_bit;
   Status *st = a.st;
@@ -261,7 +261,7 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
     }
     return;
   }
-  for (int64_t p = gid; p < n; p += gsz) a.out[p] = cur[p].v - (SUB ? a.wv[p] : 0);
+  for (int64_t p = gid; p < n; p += gsz) a.out[p] = cur[p].v - (KIND == 1 ? a.wv[p] : 0);
   if (gid == 0) {
     a.res[0] = 1;
     a.res[1] = it + 1;
@@ -284,8 +284,8 @@ int lp_groups(int *out) {
     CEL_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
     CEL_HIP(hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev));
     if (coop)
-      CEL_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)k_lp_policy<false>,
-                                                           kLpB, 0));
+      CEL_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)k_lp_policy<0>, kLpB,
+                                                           0));
     it = g_lp_cus.emplace(dev, coop ? cus * (nb < 1 ? nb : 1) : 0).first;
   }
   *out = it->second;
@@ -293,9 +293,9 @@ int lp_groups(int *out) {
 }
 }  // namespace
 
-int lp_policy(int32_t n, int32_t m, int32_t L, const int32_t *aptr, const int32_t *aidx,
-              const int64_t *wv, bool sub_wv, int64_t *out, int32_t *res, const char *timer,
-              Scratch &sc, hipStream_t s, Status *st, bool *launched) {
+int lp_policy(int32_t n, int32_t m, int32_t L, int32_t cap, const int32_t *aptr,
+              const int32_t *aidx, const int64_t *wv, int kind, int64_t *out, int32_t *res,
+              const char *timer, Scratch &sc, hipStream_t s, Status *st, bool *launched) {
   *launched = false;
   if (n <= 0) return CEL_OK;
   int gmax = 0;
@@ -306,13 +306,16 @@ int lp_policy(int32_t n, int32_t m, int32_t L, const int32_t *aptr, const int32_
   // pointer chains are at most L nodes long (one per level)
   int32_t max_rounds = 2;
   while ((int64_t(1) << (max_rounds - 2)) < L) max_rounds++;
-  // Iterations allowed before the level sweep is cheaper: an iteration costs
-  // about max_rounds barriers and passes over 48 bytes per node, plus one pass
-  // over the neighbour lists; the sweep about 0.6 us per level after 0.5 ms.
-  const double it_us = max_rounds * (5.0 + 48.0 * n / 4.0e6) + 12.0 * m / 4.0e6;
-  const double sweep_us = 500.0 + 0.6 * L;
-  int32_t cap = (int32_t)(sweep_us / it_us);
-  if (cap < 2) cap = 2;
+  // Iterations allowed (cap <= 0: before the level sweep is cheaper): an
+  // iteration costs about max_rounds barriers and passes over 48 bytes per
+  // node, plus one pass over the neighbour lists; the sweep about 0.6 us per
+  // level after 0.5 ms.
+  if (cap <= 0) {
+    const double it_us = max_rounds * (5.0 + 48.0 * n / 4.0e6) + 12.0 * m / 4.0e6;
+    const double sweep_us = 500.0 + 0.6 * L;
+    cap = (int32_t)(sweep_us / it_us);
+    if (cap < 2) cap = 2;
+  }
   int32_t *hcnt, *hoff, *hnode, *pol, *hidx, *bar;
   LpE *e0, *e1;
   int64_t *hval;
@@ -355,7 +358,9 @@ int lp_policy(int32_t n, int32_t m, int32_t L, const int32_t *aptr, const int32_
   hipError_t e;
   {
     KTimer kt(s, timer);
-    const void *k = sub_wv ? (const void *)k_lp_policy<true> : (const void *)k_lp_policy<false>;
+    const void *k = kind == 1   ? (const void *)k_lp_policy<1>
+                    : kind == 2 ? (const void *)k_lp_policy<2>
+                                : (const void *)k_lp_policy<0>;
     e = hipLaunchCooperativeKernel(k, dim3(G), dim3(kLpB), args, 0, s);
   }
   if (e != hipSuccess) {  // not launched: the caller takes the level sweep

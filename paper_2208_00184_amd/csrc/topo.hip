@@ -1,4 +1,13 @@
-// cel_topo_levels: level-synchronous Kahn ordering (Section 4.2.2).
+// cel_topo_levels: the levels of Kahn's ordering (Section 4.2.2).
+//
+// The level of a node is the length (in edges) of the longest path into it,
+// 0 for a source: the level at which Kahn's algorithm frees it.  On graphs of
+// at least kTopoPolicyN nodes the levels are first found by policy iteration
+// (lp_policy.hip; each node follows one predecessor, pointer jumping counts the
+// chains, nodes switch to a deeper predecessor until none can), which takes
+// about ten whole-GPU iterations where the levels are many; the nodes are then
+// bucketed by level and each bucket sorted by id.  Within kTopoPolicyIt
+// iterations or not at all, the level-synchronous Kahn kernel runs instead:
 //
 // One workgroup runs all levels: a level costs dependent L2 round trips, so
 // keeping the whole loop in one workgroup with workgroup barriers is far
@@ -436,6 +445,49 @@ __global__ void __launch_bounds__(kKahnB) k_kahn(cel_graph g, int32_t *cnt, cons
   }
 }
 
+constexpr int32_t kTopoPolicyN = 16384;  // smaller graphs take Kahn's kernel directly
+constexpr int32_t kTopoPolicyIt = 12;    // policy iterations before Kahn's kernel takes over
+
+// wv = 1 for a node with predecessors, 0 for a source
+__global__ void k_topo_wv(int32_t n, const int32_t *in_ptr, int64_t *wv, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
+       v += (int64_t)gridDim.x * blockDim.x)
+    wv[v] = in_ptr[v + 1] > in_ptr[v] ? 1 : 0;
+}
+
+// level[v] = val[v]; st->i0 = number of levels (largest level + 1), counts of
+// nodes per level in cnt (zeroed before)
+__global__ void k_topo_count(int32_t n, const int64_t *val, int32_t *level, int32_t *cnt,
+                             Status *st) {
+  if (failed(st)) return;
+  int32_t mx = 0;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t l = (int32_t)val[v];
+    level[v] = l;
+    atomicAdd(&cnt[l], 1);
+    mx = l > mx ? l : mx;
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const int32_t o = __shfl_xor(mx, off);
+    mx = o > mx ? o : mx;
+  }
+  if ((threadIdx.x & 63) == 0) atomicMax(&st->i0, mx + 1);
+}
+
+// order_id: the nodes of each level at level_ptr[l] onwards, in any order
+// (cur counts down from the level's size)
+__global__ void k_topo_scatter(int32_t n, const int32_t *level, const int32_t *lp, int32_t *cur,
+                               int32_t *order_id, const Status *st) {
+  if (failed(st)) return;
+  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t l = level[v];
+    order_id[lp[l] + atomicSub(&cur[l], 1) - 1] = (int32_t)v;
+  }
+}
+
 __global__ void k_zero_u64(uint64_t *p, int64_t n) {
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
@@ -445,6 +497,19 @@ __global__ void k_zero_u64(uint64_t *p, int64_t n) {
 }  // namespace cel
 
 using namespace cel;
+
+// How the calling thread's last cel_topo_levels call found the levels.
+struct TopoInfo {
+  int32_t path, iters;
+};
+static thread_local TopoInfo t_topo_info{1, 0};
+
+extern "C" int cel_topo_levels_info(int32_t *info) {
+  if (!info) return set_error(CEL_E_ARG, "cel_topo_levels_info: NULL argument");
+  info[0] = t_topo_info.path;
+  info[1] = t_topo_info.iters;
+  return CEL_OK;
+}
 
 extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *order_id,
                                int32_t *level_ptr, int32_t *n_levels, hipStream_t s) {
@@ -461,6 +526,48 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
   CEL_TRY(sc.get(&cnt, n));
   CEL_HIP(hipMemsetAsync(st, 0, sizeof(Status), s));
   CEL_TRY(check_graph(g, 1, 0, /*bound=*/false, st, cnt, sc, s));
+  if (n >= kTopoPolicyN && policy_iteration_on()) {
+    // levels by policy iteration over the predecessors
+    int64_t *wv, *val;
+    int32_t *cnt2;
+    CEL_TRY(sc.get(&wv, n));
+    CEL_TRY(sc.get(&val, n));
+    CEL_TRY(sc.get(&cnt2, (int64_t)n + 1));
+    k_topo_wv<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, g->in_ptr, wv, st);
+    bool launched = false;
+    CEL_TRY(lp_policy(n, g->m, n, kTopoPolicyIt, g->in_ptr, g->in_idx, wv, 2, val, &st->i2,
+                      "k_levels_policy", sc, s, st, &launched));
+    if (launched) {
+      Status h;
+      CEL_TRY(read_status(st, &h, s));
+      if (h.err) return status_error(h, "cel_topo_levels");
+      t_topo_info = {h.i2 ? 0 : 1, h.i3};
+      if (h.i2) {
+        k_fill_i32<<<grid_for((int64_t)n + 1, 256, 4096), 256, 0, s>>>(cnt2, (int64_t)n + 1, 0);
+        k_topo_count<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, val, level, cnt2, st);
+        CEL_TRY(read_status(st, &h, s));
+        if (h.err) return status_error(h, "cel_topo_levels");
+        const int32_t L = h.i0;
+        CEL_TRY(exclusive_scan_i32(cnt2, level_ptr, L, sc, s));
+        k_topo_scatter<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, level, level_ptr, cnt2, order_id,
+                                                             st);
+        uint64_t *keys;
+        CEL_TRY(sc.get(&keys, n));
+        k_zero_u64<<<grid_for(n, 256, 4096), 256, 0, s>>>(keys, n);
+        CEL_TRY(segmented_sort(keys, reinterpret_cast<uint32_t *>(order_id), level_ptr, L, n, sc,
+                               s, st));
+        CEL_HIP(hipGetLastError());
+        CEL_TRY(read_status(st, &h, s));
+        if (h.err) return status_error(h, "cel_topo_levels");
+        *n_levels = L;
+        return CEL_OK;
+      }
+    } else {
+      t_topo_info = {1, 0};
+    }
+  } else {
+    t_topo_info = {1, 0};
+  }
   int2 *deg;
   int4 *adj;
   int32_t *cmax;

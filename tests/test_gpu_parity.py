@@ -73,9 +73,9 @@ def assert_topo_blevel(wl, ref_t, ref_b, got_t, got_b):
 def bl_path(request):
     """b-level and t-level by policy iteration (falling back to the level
     sweeps when it does not converge) or by the level sweeps."""
-    was = cel.blevel_policy(request.param)
+    was = cel.policy_iteration(request.param)
     yield request.param
-    cel.blevel_policy(was)
+    cel.policy_iteration(was)
 
 
 @pytest.mark.parametrize("cfg,seed", [(1, 0), (1, 1), (1, 2), (2, 0), (2, 1), (3, 0), (3, 2),
@@ -958,13 +958,16 @@ def test_full_path_large(cfg):
     g, d, gt, gb = run_topo_blevel(wl)
     assert_topo_blevel(wl, rt, rb, gt, gb)
     assert [p for p, _ in cel.blevel_info()] == [0, 0]  # both by policy iteration
-    was = cel.blevel_policy(0)  # and by the level sweeps
+    assert cel.topo_levels_info()[0] == 0                # the levels too
+    was = cel.policy_iteration(0)  # and by Kahn's kernel and the level sweeps
     try:
-        gb0 = cel.blevel(g, d, gt[0], gt[2], gt[1], gt[3], want_tlevel=True)
+        gt0 = cel.topo_levels(g)
+        assert cel.topo_levels_info() == (1, 0)
+        gb0 = cel.blevel(g, d, gt0[0], gt0[2], gt0[1], gt0[3], want_tlevel=True)
         assert cel.blevel_info() == ((1, 0), (1, 0))
     finally:
-        cel.blevel_policy(was)
-    assert_topo_blevel(wl, rt, rb, gt, gb0)
+        cel.policy_iteration(was)
+    assert_topo_blevel(wl, rt, rb, gt0, gb0)
     rc = O.cluster(wl, rb[2], 200, -1)
     cid, C, cut = cel.cluster(g, d, gb[2], 200, -1)
     assert C == rc[1] and cut == rc[2] and np.array_equal(np_(cid), rc[0])

@@ -94,3 +94,34 @@ def test_policy_long_lists_both_ways():
     L, info = run(wl)
     for path, iters in info:
         assert path == 0 and iters <= L + 1
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 5])
+def test_levels_by_policy_iteration(cfg):
+    """Kahn's levels as longest paths over the predecessors: the level of
+    every node, the level-sorted order (ids ascending within a level) and the
+    level starts equal the oracle's; layered-200k may exceed the budget of
+    12 iterations and take Kahn's kernel."""
+    wl = make_config(cfg, 0)
+    ref = O.topo_levels(wl)
+    g = cel.Graph.from_arrays(wl, DEV)
+    lev, oid, lp, L = cel.topo_levels(g)
+    path, iters = cel.topo_levels_info()
+    assert L == ref[3]
+    assert np.array_equal(np_(lev), ref[0]) and np.array_equal(np_(oid), ref[1])
+    assert np.array_equal(np_(lp), ref[2])
+    assert (path, iters > 0) in ((0, True), (1, True))
+    if cfg in (2, 3):
+        assert path == 0 and iters <= 12
+
+
+def test_levels_policy_cycle_detected():
+    """A cycle in a graph large enough for policy iteration is reported as
+    such (by a pointer cycle, or by Kahn's kernel after the budget)."""
+    n = 20000
+    edges = [(i, i + 1) for i in range(n - 1)] + [(n - 1, n // 2)]
+    wl = from_edges(n, edges, [1] * n, [1] * n, 1, [1], 1, 0)
+    g = cel.Graph.from_arrays(wl, DEV)
+    with pytest.raises(cel.CelError) as ei:
+        cel.topo_levels(g)
+    assert ei.value.code == -2
