@@ -485,7 +485,7 @@ __device__ inline void ld_many(int64_t (&x)[N], const int32_t (&q)[N], const int
     if (x[j] < 0) x[j] = ld_final(&gx[q[j]], s_abort, st);
 }
 
-// ---------------------------------------------- grid-wide barrier (cooperative)
+// ------------------------------------------------------- grid-wide barrier
 // bar: [0] the released barrier (k << 1 | OR of the bits), [1] abort flag,
 // [2 + b] workgroup b's arrival (k << 1 | its bit); zero before the launch.
 constexpr int32_t kGridSpin = 1 << 20;  // polls of a grid barrier wait before it gives up
@@ -496,8 +496,8 @@ __device__ inline void st32(int32_t *p, int32_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Grid barrier number k (1, 2, ...; all workgroups are co-resident, by
-// cooperative launch) that also ORs one bit over the workgroups.  Thread 0 of
+// Grid barrier number k (1, 2, ...; the grid is no larger than what the GPU
+// holds at once) that also ORs one bit over the workgroups.  Thread 0 of
 // workgroup b releases the block's stores (each wave has waited for its own)
 // and publishes (k << 1 | bit) in its own arrival word; workgroup 0 waits
 // until every arrival carries k, ORs the bits and publishes the release word;
@@ -622,7 +622,7 @@ int ms_ring(int32_t n, int32_t m, int32_t L, const int32_t *lp, const int32_t *g
             const int64_t *cq, const uint8_t *devp, const int64_t *sxp, const int32_t *metap,
             int64_t *finp, int64_t *makespan, class Scratch &sc, hipStream_t s, Status *st);
 // lp_policy.hip: val(p) = wv(p) + max over q in aptr/aidx rows of val(q) by
-// policy iteration on a cooperative grid; out = val (- wv for kind 1, the
+// policy iteration on a persistent grid; out = val (- wv for kind 1, the
 // t-level; kind 0 is the b-level, 2 the levels: they differ only there).  L
 // bounds the pointer chains (nodes); at most cap iterations (cap <= 0: as
 // many as are cheaper than a level sweep of L levels).  res[0] = 1 once
@@ -636,7 +636,7 @@ int lp_policy(int32_t n, int32_t m, int32_t L, int32_t cap, const int32_t *aptr,
 bool policy_iteration_on();
 // ms_relax.hip: finish times of one placement by relaxation over the
 // cross-device edges (devp = devices by position).  Queues the preparation
-// and one cooperative kernel on s and sets *launched; st->i3 = 1 once the
+// and one persistent kernel on s and sets *launched; st->i3 = 1 once the
 // kernel has converged (start, finish and makespan[0] are then written) and
 // st->i2 = the rounds it ran.  *launched stays false when the grid cannot be
 // co-resident (the caller runs the level sweep).  max_groups > 0 caps the

@@ -16,7 +16,7 @@
 // iterations, and on the transformer graphs about ten suffice where the level
 // sweeps need one dependent step per level (10,565 on transformer-96).
 //
-// One cooperative kernel runs everything; grid barriers (grid_sync) separate
+// One persistent kernel runs everything; grid barriers (grid_sync) separate
 // the phases.  Neighbour lists of more than kLpLight entries are split into
 // chunks of kLpChunk, each taken by one wave, and combined after a barrier.
 #include <map>
@@ -280,13 +280,10 @@ int lp_groups(int *out) {
   std::lock_guard<std::mutex> lk(g_lp_mu);
   auto it = g_lp_cus.find(dev);
   if (it == g_lp_cus.end()) {
-    int cus = 0, coop = 0, nb = 0;
+    int cus = 0, nb = 0;
     CEL_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-    CEL_HIP(hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev));
-    if (coop)
-      CEL_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)k_lp_policy<0>, kLpB,
-                                                           0));
-    it = g_lp_cus.emplace(dev, coop ? cus * (nb < 1 ? nb : 1) : 0).first;
+    CEL_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)k_lp_policy<0>, kLpB, 0));
+    it = g_lp_cus.emplace(dev, cus * (nb < 1 ? nb : 1)).first;
   }
   *out = it->second;
   return CEL_OK;
@@ -354,19 +351,16 @@ int lp_policy(int32_t n, int32_t m, int32_t L, int32_t cap, const int32_t *aptr,
   a.out = out;
   a.st = st;
   a.res = res;
-  void *args[] = {&a};
-  hipError_t e;
   {
+    // at most one workgroup per CU, within the occupancy calculator's limit:
+    // resident all at once on an idle GPU; the grid barriers' waits are
+    // bounded (kGridSpin), so anything else ends in an error, not a hang
     KTimer kt(s, timer);
-    const void *k = kind == 1   ? (const void *)k_lp_policy<1>
-                    : kind == 2 ? (const void *)k_lp_policy<2>
-                                : (const void *)k_lp_policy<0>;
-    e = hipLaunchCooperativeKernel(k, dim3(G), dim3(kLpB), args, 0, s);
+    if (kind == 1) k_lp_policy<1><<<G, kLpB, 0, s>>>(a);
+    else if (kind == 2) k_lp_policy<2><<<G, kLpB, 0, s>>>(a);
+    else k_lp_policy<0><<<G, kLpB, 0, s>>>(a);
   }
-  if (e != hipSuccess) {  // not launched: the caller takes the level sweep
-    (void)hipGetLastError();
-    return CEL_OK;
-  }
+  CEL_HIP(hipGetLastError());
   *launched = true;
   return CEL_OK;
 }

@@ -30,7 +30,7 @@
 // maximum of V along the chain; the rounds store fin + c (finc) per slot, the
 // value a cross-device successor gathers.
 //
-// One cooperative kernel runs every round.  Workgroup b owns slots
+// One persistent kernel runs every round.  Workgroup b owns slots
 // [b T, (b + 1) T) as NT tiles of kRxB, one slot per thread and tile, and
 // keeps its in-block prefix maxima in registers.  A round: gather the
 // predecessors' finc (every load issued before the first use), per tile a
@@ -428,11 +428,9 @@ int rx_device(RxDev *out) {
   if (it == g_rx_dev.end()) {
     RxDev r;
     CEL_HIP(hipDeviceGetAttribute(&r.cus, hipDeviceAttributeMultiprocessorCount, dev));
-    int coop = 0;
-    CEL_HIP(hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev));
     for (int i = 0; i < kRxNV; i++) {
       int nb = 0;
-      if (coop) CEL_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, rx_kernel(i), kRxB, 0));
+      CEL_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, rx_kernel(i), kRxB, 0));
       r.occ[i] = nb;
     }
     it = g_rx_dev.emplace(dev, r).first;
@@ -464,6 +462,11 @@ int ms_relax(const cel_graph *g, const cel_devices *d, int32_t L, const int32_t 
     }
   }
   if (ti < 0) return CEL_OK;  // too large for one co-resident grid
+  // The grid is at most one workgroup per CU, within what the occupancy
+  // calculator says fits: on an idle GPU every workgroup is resident at once,
+  // which the grid barriers need.  Their waits are bounded (kGridSpin), so a
+  // workgroup kept off the GPU by other work ends the call with an error
+  // instead of hanging it.
   // Rounds allowed before the level sweep is cheaper: a round costs a few
   // microseconds of barriers plus its bytes at a few TB/s; the sweep about
   // 0.85 us per level after some 0.5 ms of preparation.
@@ -524,16 +527,19 @@ int ms_relax(const cel_graph *g, const cel_devices *d, int32_t L, const int32_t 
   a.start = start;
   a.finish = finish;
   a.makespan = makespan;
-  void *args[] = {&a, &st};
-  hipError_t e;
   {
     KTimer kt(s, "k_makespan_one");
-    e = hipLaunchCooperativeKernel(rx_kernel(ti), dim3(G), dim3(kRxB), args, 0, s);
+    switch (ti) {
+      case 0: k_rx_relax<1><<<G, kRxB, 0, s>>>(a, st); break;
+      case 1: k_rx_relax<2><<<G, kRxB, 0, s>>>(a, st); break;
+      case 2: k_rx_relax<3><<<G, kRxB, 0, s>>>(a, st); break;
+      case 3: k_rx_relax<4><<<G, kRxB, 0, s>>>(a, st); break;
+      case 4: k_rx_relax<5><<<G, kRxB, 0, s>>>(a, st); break;
+      case 5: k_rx_relax<6><<<G, kRxB, 0, s>>>(a, st); break;
+      default: k_rx_relax<8><<<G, kRxB, 0, s>>>(a, st); break;
+    }
   }
-  if (e != hipSuccess) {  // not launched: the caller takes the level sweep
-    (void)hipGetLastError();
-    return CEL_OK;
-  }
+  CEL_HIP(hipGetLastError());
   *launched = true;
   return CEL_OK;
 }

@@ -6,7 +6,7 @@
 // (lp_policy.hip; each node follows one predecessor, pointer jumping counts the
 // chains, nodes switch to a deeper predecessor until none can), which takes
 // about ten whole-GPU iterations where the levels are many; the nodes are then
-// bucketed by level and each bucket sorted by id.  Within kTopoPolicyIt
+// sorted by (level, id) and the level starts read off the sorted levels.  Within kTopoPolicyIt
 // iterations or not at all, the level-synchronous Kahn kernel runs instead:
 //
 // One workgroup runs all levels: a level costs dependent L2 round trips, so
@@ -456,19 +456,21 @@ __global__ void k_topo_wv(int32_t n, const int32_t *in_ptr, int64_t *wv, const S
     wv[v] = in_ptr[v + 1] > in_ptr[v] ? 1 : 0;
 }
 
-// level[v] = val[v]; st->i0 = number of levels (largest level + 1), counts of
-// nodes per level in cnt (zeroed before)
-__global__ void k_topo_count(int32_t n, const int64_t *val, int32_t *level, int32_t *cnt,
-                             Status *st) {
+// level[v] = val[v], sort keys (level) and ids (v) in node order, the
+// single segment [0, n) for the sort; st->i0 = number of levels (largest + 1)
+__global__ void k_topo_keys(int32_t n, const int64_t *val, int32_t *level, uint64_t *keys,
+                            uint32_t *ids, int32_t *seg, Status *st) {
   if (failed(st)) return;
   int32_t mx = 0;
   for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
        v += (int64_t)gridDim.x * blockDim.x) {
     const int32_t l = (int32_t)val[v];
     level[v] = l;
-    atomicAdd(&cnt[l], 1);
+    keys[v] = (uint64_t)l;
+    ids[v] = (uint32_t)v;
     mx = l > mx ? l : mx;
   }
+  if (blockIdx.x == 0 && threadIdx.x < 2) seg[threadIdx.x] = threadIdx.x ? n : 0;
   for (int off = 32; off > 0; off >>= 1) {
     const int32_t o = __shfl_xor(mx, off);
     mx = o > mx ? o : mx;
@@ -476,15 +478,15 @@ __global__ void k_topo_count(int32_t n, const int64_t *val, int32_t *level, int3
   if ((threadIdx.x & 63) == 0) atomicMax(&st->i0, mx + 1);
 }
 
-// order_id: the nodes of each level at level_ptr[l] onwards, in any order
-// (cur counts down from the level's size)
-__global__ void k_topo_scatter(int32_t n, const int32_t *level, const int32_t *lp, int32_t *cur,
-                               int32_t *order_id, const Status *st) {
+// level_ptr from the levels sorted ascending: every level up to the largest
+// holds a node (a node of level l has a predecessor of level l - 1)
+__global__ void k_topo_ptr(int32_t n, const uint64_t *keys, int32_t *level_ptr, const Status *st) {
   if (failed(st)) return;
-  for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
-       v += (int64_t)gridDim.x * blockDim.x) {
-    const int32_t l = level[v];
-    order_id[lp[l] + atomicSub(&cur[l], 1) - 1] = (int32_t)v;
+  for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t k = keys[p];
+    if (p == 0 || keys[p - 1] != k) level_ptr[k] = (int32_t)p;
+    if (p == n - 1) level_ptr[k + 1] = n;
   }
 }
 
@@ -529,10 +531,8 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
   if (n >= kTopoPolicyN && policy_iteration_on()) {
     // levels by policy iteration over the predecessors
     int64_t *wv, *val;
-    int32_t *cnt2;
     CEL_TRY(sc.get(&wv, n));
     CEL_TRY(sc.get(&val, n));
-    CEL_TRY(sc.get(&cnt2, (int64_t)n + 1));
     k_topo_wv<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, g->in_ptr, wv, st);
     bool launched = false;
     CEL_TRY(lp_policy(n, g->m, n, kTopoPolicyIt, g->in_ptr, g->in_idx, wv, 2, val, &st->i2,
@@ -543,23 +543,19 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
       if (h.err) return status_error(h, "cel_topo_levels");
       t_topo_info = {h.i2 ? 0 : 1, h.i3};
       if (h.i2) {
-        k_fill_i32<<<grid_for((int64_t)n + 1, 256, 4096), 256, 0, s>>>(cnt2, (int64_t)n + 1, 0);
-        k_topo_count<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, val, level, cnt2, st);
-        CEL_TRY(read_status(st, &h, s));
-        if (h.err) return status_error(h, "cel_topo_levels");
-        const int32_t L = h.i0;
-        CEL_TRY(exclusive_scan_i32(cnt2, level_ptr, L, sc, s));
-        k_topo_scatter<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, level, level_ptr, cnt2, order_id,
-                                                             st);
+        // order_id: the nodes sorted by (level, id), one segment
         uint64_t *keys;
+        int32_t *seg;
         CEL_TRY(sc.get(&keys, n));
-        k_zero_u64<<<grid_for(n, 256, 4096), 256, 0, s>>>(keys, n);
-        CEL_TRY(segmented_sort(keys, reinterpret_cast<uint32_t *>(order_id), level_ptr, L, n, sc,
-                               s, st));
+        CEL_TRY(sc.get(&seg, 2));
+        uint32_t *ids = reinterpret_cast<uint32_t *>(order_id);
+        k_topo_keys<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, val, level, keys, ids, seg, st);
+        CEL_TRY(segmented_sort(keys, ids, seg, 1, n, sc, s, st));
+        k_topo_ptr<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, keys, level_ptr, st);
         CEL_HIP(hipGetLastError());
         CEL_TRY(read_status(st, &h, s));
         if (h.err) return status_error(h, "cel_topo_levels");
-        *n_levels = L;
+        *n_levels = h.i0;
         return CEL_OK;
       }
     } else {
