@@ -497,13 +497,21 @@ __device__ inline void st32(int32_t *p, int32_t v) {
 }
 
 // Grid barrier number k (1, 2, ...; the grid is no larger than what the GPU
-// holds at once) that also ORs one bit over the workgroups.  Thread 0 of
-// workgroup b releases the block's stores (each wave has waited for its own)
-// and publishes (k << 1 | bit) in its own arrival word; workgroup 0 waits
-// until every arrival carries k, ORs the bits and publishes the release word;
-// the others wait for it.  No two workgroups write one word.  Every wait is
-// bounded: one that gives up, or an abort raised anywhere, returns false in
-// every thread of every workgroup.  *bit_out = the OR.
+// holds at once) that also ORs one bit over the workgroups.  Every value that
+// one workgroup writes and another reads inside the kernel goes through
+// agent-scope atomic stores and loads (st_coherent / ld_coherent, st32 /
+// ld32): those are written through to, and read from, the level where all
+// XCDs meet, so they need no L2 write-back or invalidation (an agent-scope
+// fence performs both for the whole XCD's L2, in every workgroup: three
+// quarters of a barrier's time at 256 workgroups).  What the barrier orders
+// is completion: each wave waits for its own stores (vmcnt(0)) before its
+// workgroup arrives, and the loads after the barrier are issued only once the
+// release word has been seen.  Thread 0 of workgroup b publishes (k << 1 |
+// bit) in its own arrival word; workgroup 0 waits until every arrival
+// carries k, ORs the bits and publishes the release word; the others wait
+// for it.  No two workgroups write one word.  Every wait is bounded: one that
+// gives up, or an abort raised anywhere, returns false in every thread of
+// every workgroup.  *bit_out = the OR.
 __device__ inline bool grid_sync(int32_t *bar, int32_t k, int32_t bit, int32_t *s_ok, int32_t *s_bit,
                                  Status *st, int32_t *bit_out) {
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's stores are complete
@@ -528,9 +536,7 @@ __device__ inline bool grid_sync(int32_t *bar, int32_t k, int32_t bit, int32_t *
     ok = __syncthreads_and(ok);
     orb = __syncthreads_or(orb);
     if (threadIdx.x == 0) {
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       if (ok) {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         st32(&bar[0], (k << 1) | orb);
       } else {
         raise_err(st, EB_WAIT);
@@ -542,7 +548,6 @@ __device__ inline bool grid_sync(int32_t *bar, int32_t k, int32_t bit, int32_t *
   } else {
     __syncthreads();
     if (threadIdx.x == 0) {
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
       st32(&bar[2 + blockIdx.x], mine);
       int32_t ok = 1;
       int32_t v = ld32(&bar[0]);
@@ -556,7 +561,6 @@ __device__ inline bool grid_sync(int32_t *bar, int32_t k, int32_t bit, int32_t *
         __builtin_amdgcn_s_sleep(1);
         v = ld32(&bar[0]);
       }
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       *s_ok = ok;
       *s_bit = v & 1;
     }

@@ -34,7 +34,7 @@ constexpr int kLpU = 4;           // nodes per thread with loads in flight toget
 struct LpE {       // one node's state during pointer jumping
   int64_t v;       // sum of wv from the node up to (not including) nxt
   int32_t nxt;     // next node on the pointer chain, -1 at its end
-  int32_t pad;
+  int32_t both;    // 1: the chain has ended and both buffers hold the final entry
 };
 
 struct LpArgs {
@@ -52,6 +52,19 @@ struct LpArgs {
   Status *st;
   int32_t *res;                   // [0] converged, [1] iterations
 };
+
+// Entries, policy pointers and chunk results are written and read by
+// different workgroups inside the kernel: agent-scope atomic accesses (see
+// grid_sync).  An entry is two 64-bit words: v, and nxt with the flag.
+__device__ inline LpE lpe_ld(const LpE *p) {
+  const int64_t w = ld_coherent(reinterpret_cast<const int64_t *>(&p->nxt));
+  return LpE{ld_coherent(&p->v), (int32_t)(uint32_t)w, (int32_t)(w >> 32)};
+}
+__device__ inline void lpe_st(LpE *p, const LpE &x) {
+  st_coherent(&p->v, x.v);
+  st_coherent(reinterpret_cast<int64_t *>(&p->nxt),
+              (int64_t)(((uint64_t)(uint32_t)x.both << 32) | (uint32_t)x.nxt));
+}
 
 // larger value first, then the smaller neighbour index
 __device__ inline bool lp_better(int64_t v, int32_t q, int64_t bv, int32_t bq) {
@@ -89,8 +102,8 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
   int32_t bar = 0, bit;
   // the empty policy: every node alone
   for (int64_t p = gid; p < n; p += gsz) {
-    a.e0[p] = LpE{a.wv[p], -1, 0};
-    a.pol[p] = -1;
+    lpe_st(&a.e0[p], LpE{a.wv[p], -1, 0});
+    st32(&a.pol[p], -1);
   }
   if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
   LpE *cur = a.e0, *oth = a.e1;
@@ -124,7 +137,7 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
       }
       if (lane == 0) {
         st_coherent(&a.hval[c], bv);
-        a.hidx[c] = bq;
+        st32(&a.hidx[c], bq);
       }
     }
     int32_t chg = 0;
@@ -139,7 +152,7 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
         if (p < n) {
           b0[u] = a.aptr[p];
           b1[u] = a.aptr[p + 1];
-          pq[u] = a.pol[p];
+          pq[u] = ld32(&a.pol[p]);
         }
       }
 #pragma unroll
@@ -159,7 +172,7 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
         }
         const int64_t cv = pq[u] >= 0 ? ld_coherent(&cur[pq[u]].v) : -1;
         if (bv > cv) {
-          a.pol[p] = bq;
+          st32(&a.pol[p], bq);
           chg = 1;
         }
       }
@@ -173,16 +186,16 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
         int32_t bq = INT32_MAX;
         for (int32_t k = (int32_t)c; k < a.hoff[p + 1]; k++) {
           const int64_t v = ld_coherent(&a.hval[k]);
-          const int32_t q = a.hidx[k];
+          const int32_t q = ld32(&a.hidx[k]);
           if (lp_better(v, q, bv, bq)) {
             bv = v;
             bq = q;
           }
         }
-        const int32_t pq = a.pol[p];
+        const int32_t pq = ld32(&a.pol[p]);
         const int64_t cv = pq >= 0 ? ld_coherent(&cur[pq].v) : -1;
         if (bv > cv) {
-          a.pol[p] = bq;
+          st32(&a.pol[p], bq);
           chg = 1;
         }
       }
@@ -201,21 +214,21 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
 #pragma unroll
       for (int u = 0; u < kLpU; u++) {
         const int64_t p = p0 + u * gsz;
-        q[u] = p < n ? a.pol[p] : -1;
+        q[u] = p < n ? ld32(&a.pol[p]) : -1;
       }
       int64_t wq[kLpU];
       int32_t nq[kLpU];
 #pragma unroll
       for (int u = 0; u < kLpU; u++) {
         wq[u] = q[u] >= 0 ? a.wv[q[u]] : 0;
-        nq[u] = q[u] >= 0 ? a.pol[q[u]] : -1;
+        nq[u] = q[u] >= 0 ? ld32(&a.pol[q[u]]) : -1;
       }
 #pragma unroll
       for (int u = 0; u < kLpU; u++) {
         const int64_t p = p0 + u * gsz;
         if (p >= n) continue;
         more |= nq[u] >= 0;
-        cur[p] = LpE{a.wv[p] + wq[u], nq[u], 0};
+        lpe_st(&cur[p], LpE{a.wv[p] + wq[u], nq[u], 0});
       }
     }
     more = __syncthreads_or(more);
@@ -232,18 +245,25 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
 #pragma unroll
         for (int u = 0; u < kLpU; u++) {
           const int64_t p = p0 + u * gsz;
-          x[u] = p < n ? cur[p] : LpE{0, -1, 0};
+          x[u] = p < n ? lpe_ld(&cur[p]) : LpE{0, -1, 1};
         }
         LpE y[kLpU];
 #pragma unroll
-        for (int u = 0; u < kLpU; u++) y[u] = x[u].nxt >= 0 ? cur[x[u].nxt] : LpE{0, -1, 0};
+        for (int u = 0; u < kLpU; u++) y[u] = x[u].nxt >= 0 ? lpe_ld(&cur[x[u].nxt]) : LpE{0, -1, 0};
 #pragma unroll
         for (int u = 0; u < kLpU; u++) {
           const int64_t p = p0 + u * gsz;
-          if (p >= n) continue;
-          const LpE z = x[u].nxt >= 0 ? LpE{x[u].v + y[u].v, y[u].nxt, 0} : x[u];
-          more |= z.nxt >= 0;
-          oth[p] = z;
+          if (p >= n || x[u].both) continue;  // ended, and final in both buffers
+          if (x[u].nxt < 0) {
+            // ended last round: the other buffer gets the final entry too
+            // (readers of cur[p] see v and nxt unchanged)
+            lpe_st(&oth[p], LpE{x[u].v, -1, 1});
+            st32(&cur[p].both, 1);
+          } else {
+            const LpE z{x[u].v + y[u].v, y[u].nxt, 0};
+            more |= z.nxt >= 0;
+            lpe_st(&oth[p], z);
+          }
         }
       }
       more = __syncthreads_or(more);
@@ -261,7 +281,8 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
     }
     return;
   }
-  for (int64_t p = gid; p < n; p += gsz) a.out[p] = cur[p].v - (KIND == 1 ? a.wv[p] : 0);
+  for (int64_t p = gid; p < n; p += gsz)
+    a.out[p] = ld_coherent(&cur[p].v) - (KIND == 1 ? a.wv[p] : 0);
   if (gid == 0) {
     a.res[0] = 1;
     a.res[1] = it + 1;
