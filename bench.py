@@ -78,6 +78,7 @@ PMC_KERNELS = {
     "k_makespan_batch_wide": ("cel::(anonymous namespace)::k_mw_batch(", ["ms_wide.hip", "cel_internal.h"]),
     "k_kahn": ("cel::k_kahn(", ["topo.hip", "cel_internal.h"]),
     "k_cluster_dp": ("cel::k_cluster_dp<true>(", ["cluster.hip", "cel_internal.h"]),
+    "k_cluster_policy": ("cel::k_dp_policy(", ["dp_policy.hip", "cel_internal.h"]),
     "k_place": ("cel::k_place<", ["place.hip", "cel_internal.h"]),
 }
 

@@ -362,11 +362,21 @@ int cel_blevel_info(int32_t *info);
  * Errors: CEL_E_ARG (NULL argument). */
 int cel_topo_levels_info(int32_t *info);
 
+/* Diagnostics: how the calling thread's last cel_cluster call ran the DP
+ * (mode CEL_CLUSTER_DP).  info[0] = 0: by policy iteration over the back
+ * pointers (graphs of 16,384 nodes and more), exact after info[1]
+ * iterations; 1: by the blocked sequential DP (after info[1] iterations that
+ * did not converge within their budget, or 0 when policy iteration was not
+ * tried).
+ * Outputs: info [2] (host).
+ * Errors: CEL_E_ARG (NULL argument). */
+int cel_cluster_info(int32_t *info);
+
 /* Diagnostics: cel_policy_iteration(0) makes the calling thread's
- * cel_topo_levels and cel_blevel calls take Kahn's kernel and the level
- * sweeps directly; 1 (the default) tries policy iteration first.  Both give
- * the same results.  Returns the previous mode (CEL_E_ARG for a negative
- * mode). */
+ * cel_topo_levels, cel_blevel and cel_cluster calls take Kahn's kernel, the
+ * level sweeps and the blocked DP directly; 1 (the default) tries policy
+ * iteration first.  Both give the same results.  Returns the previous mode
+ * (CEL_E_ARG for a negative mode). */
 int cel_policy_iteration(int mode);
 
 /* Diagnostics: which K = 1 path the calling thread's cel_makespan and

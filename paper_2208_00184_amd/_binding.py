@@ -22,7 +22,7 @@ CLUSTER_DP, CLUSTER_GREEDY = 0, 1
 
 EXPORTS = ("cel_topo_levels", "cel_blevel", "cel_cpd_order", "cel_dfs_order", "cel_cluster", "cel_place", "cel_place_ext", "cel_makespan", "cel_makespan_noalloc",
            "cel_makespan_info", "cel_makespan_relax", "cel_blevel_info", "cel_policy_iteration",
-           "cel_topo_levels_info",
+           "cel_topo_levels_info", "cel_cluster_info",
            "cel_order_place", "cel_comm_sums", "cel_makespan_model", "cel_colocate", "cel_step_latency", "cel_timing", "cel_kernel_stats", "cel_last_error", "cel_version")
 
 
@@ -100,6 +100,8 @@ def lib() -> C.CDLL:
         L.cel_policy_iteration.restype = C.c_int
         L.cel_topo_levels_info.argtypes = [C.POINTER(i32)]
         L.cel_topo_levels_info.restype = C.c_int
+        L.cel_cluster_info.argtypes = [C.POINTER(i32)]
+        L.cel_cluster_info.restype = C.c_int
         _lib = L
     return _lib
 
@@ -159,10 +161,18 @@ def topo_levels_info() -> tuple:
     return info[0], info[1]
 
 
+def cluster_info() -> tuple:
+    """(path, iterations) of the calling thread's last cluster call (DP mode):
+    path 0 = policy iteration, 1 = the blocked DP."""
+    info = (C.c_int32 * 2)()
+    _check(lib().cel_cluster_info(info))
+    return info[0], info[1]
+
+
 def policy_iteration(mode: int) -> int:
-    """Levels, b-level and t-level path of the calling thread: 0 = Kahn's
-    kernel and the level sweeps, 1 = policy iteration first (default);
-    returns the previous mode."""
+    """Levels, b-level, t-level and clustering-DP path of the calling thread:
+    0 = Kahn's kernel, the level sweeps and the blocked DP, 1 = policy
+    iteration first (default); returns the previous mode."""
     r = lib().cel_policy_iteration(int(mode))
     if r < 0:
         _check(r)

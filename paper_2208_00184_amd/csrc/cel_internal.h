@@ -570,6 +570,42 @@ __device__ inline bool grid_sync(int32_t *bar, int32_t k, int32_t bit, int32_t *
   return *s_ok != 0;
 }
 
+// One node's state during pointer jumping (lp_policy.hip, dp_policy.hip):
+// v the sum along the node's chain up to (not including) nxt, nxt the next
+// node on the chain (-1 at its end), both = 1 once the chain has ended and
+// both buffers hold the final entry.  Read and written by different
+// workgroups of one kernel as two agent-scope 64-bit words.
+struct LpE {
+  int64_t v;       // sum of wv from the node up to (not including) nxt
+  int32_t nxt;     // next node on the pointer chain, -1 at its end
+  int32_t both;    // 1: the chain has ended and both buffers hold the final entry
+};
+__device__ inline LpE lpe_ld(const LpE *p) {
+  const int64_t w = ld_coherent(reinterpret_cast<const int64_t *>(&p->nxt));
+  return LpE{ld_coherent(&p->v), (int32_t)(uint32_t)w, (int32_t)(w >> 32)};
+}
+__device__ inline void lpe_st(LpE *p, const LpE &x) {
+  st_coherent(&p->v, x.v);
+  st_coherent(reinterpret_cast<int64_t *>(&p->nxt),
+              (int64_t)(((uint64_t)(uint32_t)x.both << 32) | (uint32_t)x.nxt));
+}
+
+// Grid barrier with agent-scope fences around the arrival and the release:
+// plain stores before it are visible to plain loads after it, in every
+// workgroup (thread 0's release writes back, and its acquire invalidates, the
+// L2 of its XCD and its CU's L1, shared by the workgroup's waves).
+__device__ inline bool grid_sync_fenced(int32_t *bar, int32_t k, int32_t *s_ok, int32_t *s_bit,
+                                        Status *st) {
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __syncthreads();
+  if (threadIdx.x == 0) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  int32_t bit;
+  const bool ok = grid_sync(bar, k, 0, s_ok, s_bit, st, &bit);
+  if (threadIdx.x == 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  __syncthreads();
+  return ok;
+}
+
 // sweep.hip: level sweeps of eq. 3 (rev: b-level over successors) or eq. 2
 // (t-level over predecessors) in position space; out[p] = the value at p.
 struct SweepArgs {
@@ -638,6 +674,13 @@ int lp_policy(int32_t n, int32_t m, int32_t L, int32_t cap, const int32_t *aptr,
 // whether the calling thread's cel_topo_levels and cel_blevel calls try
 // policy iteration first (cel_policy_iteration)
 bool policy_iteration_on();
+// dp_policy.hip: the clustering DP's back pointers P[1..n] (smallest
+// minimising i) and st->s0 = S(n) by policy iteration, given lo, PO, the comm
+// by position and the successors in positions (sptr / sidx).  st->i2 = 1 once
+// converged, st->i3 = iterations; *launched false when not launched.
+int dp_policy(int32_t n, int32_t m, int32_t R, const int32_t *lo, const int64_t *PO,
+              const int64_t *cq, const int32_t *sptr, const int32_t *sidx, int32_t *P,
+              class Scratch &sc, hipStream_t s, Status *st, bool *launched);
 // ms_relax.hip: finish times of one placement by relaxation over the
 // cross-device edges (devp = devices by position).  Queues the preparation
 // and one persistent kernel on s and sets *launched; st->i3 = 1 once the

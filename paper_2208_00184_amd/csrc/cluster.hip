@@ -1129,6 +1129,21 @@ CEL_PHASE_READER(cel_debug_phases_cluster)
 
 using namespace cel;
 
+constexpr int32_t kDpPolicyN = 16384;  // smaller graphs take the blocked DP directly
+
+// How the calling thread's last cel_cluster call ran its DP.
+struct ClInfo {
+  int32_t path, iters;
+};
+static thread_local ClInfo t_cl_info{1, 0};
+
+extern "C" int cel_cluster_info(int32_t *info) {
+  if (!info) return set_error(CEL_E_ARG, "cel_cluster_info: NULL argument");
+  info[0] = t_cl_info.path;
+  info[1] = t_cl_info.iters;
+  return CEL_OK;
+}
+
 extern "C" int cel_cluster(const cel_graph *g, const cel_devices *d, const int32_t *order,
                            int32_t R, int64_t M, int32_t mode, int32_t *cluster_id,
                            int32_t *n_clusters, int64_t *cut_cost, hipStream_t s) {
@@ -1186,10 +1201,30 @@ extern "C" int cel_cluster(const cel_graph *g, const cel_devices *d, const int32
     CEL_TRY(sc.get(&pidx, g->m));
     CEL_TRY(sc.get(&P, (int64_t)n + 1));
     CEL_TRY(exclusive_scan_i64(outc, PO, n, sc, s));
-    CEL_TRY(relabel_csr(n, g->m, order, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
+    // policy iteration first (graphs of kDpPolicyN nodes and more)
+    bool solved = false;
+    t_cl_info = {1, 0};
+    if (n >= kDpPolicyN && policy_iteration_on()) {
+      int32_t *sptr, *sidx;
+      CEL_TRY(sc.get(&sptr, (int64_t)n + 1));
+      CEL_TRY(sc.get(&sidx, g->m));
+      CEL_TRY(relabel_csr(n, g->m, order, pos, g->out_ptr, g->out_idx, sptr, sidx, sc, s, st));
+      bool launched = false;
+      CEL_TRY(dp_policy(n, g->m, R, lo, PO, cq, sptr, sidx, P, sc, s, st, &launched));
+      if (launched) {
+        Status h;
+        CEL_TRY(read_status(st, &h, s));
+        if (h.err) return status_error(h, fn);
+        solved = h.i2 != 0;
+        t_cl_info = {solved ? 0 : 1, h.i3};
+      }
+    }
     bool blocked = false;
-    CEL_TRY(dp_blocked(n, g->m, R, lo, pptr, pidx, cq, PO, P, st, sc, s, &blocked));
-    if (blocked) {
+    if (!solved) {
+      CEL_TRY(relabel_csr(n, g->m, order, pos, g->in_ptr, g->in_idx, pptr, pidx, sc, s, st));
+      CEL_TRY(dp_blocked(n, g->m, R, lo, pptr, pidx, cq, PO, P, st, sc, s, &blocked));
+    }
+    if (solved || blocked) {
     } else if (R <= 64) launch_dp<1>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
     else if (R <= 128) launch_dp<2>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
     else if (R <= 256) launch_dp<4>(n, R, lo, pptr, pidx, cq, PO, P, st, s);

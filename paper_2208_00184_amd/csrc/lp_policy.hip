@@ -31,11 +31,7 @@ constexpr int kLpLight = 64;      // longer neighbour lists are split into chunk
 constexpr int kLpChunk = 4096;    // entries of a chunk (one wave)
 constexpr int kLpU = 4;           // nodes per thread with loads in flight together
 
-struct LpE {       // one node's state during pointer jumping
-  int64_t v;       // sum of wv from the node up to (not including) nxt
-  int32_t nxt;     // next node on the pointer chain, -1 at its end
-  int32_t both;    // 1: the chain has ended and both buffers hold the final entry
-};
+
 
 struct LpArgs {
   int32_t n, cap, max_rounds;
@@ -55,16 +51,7 @@ struct LpArgs {
 
 // Entries, policy pointers and chunk results are written and read by
 // different workgroups inside the kernel: agent-scope atomic accesses (see
-// grid_sync).  An entry is two 64-bit words: v, and nxt with the flag.
-__device__ inline LpE lpe_ld(const LpE *p) {
-  const int64_t w = ld_coherent(reinterpret_cast<const int64_t *>(&p->nxt));
-  return LpE{ld_coherent(&p->v), (int32_t)(uint32_t)w, (int32_t)(w >> 32)};
-}
-__device__ inline void lpe_st(LpE *p, const LpE &x) {
-  st_coherent(&p->v, x.v);
-  st_coherent(reinterpret_cast<int64_t *>(&p->nxt),
-              (int64_t)(((uint64_t)(uint32_t)x.both << 32) | (uint32_t)x.nxt));
-}
+// grid_sync, and lpe_ld / lpe_st).
 
 // larger value first, then the smaller neighbour index
 __device__ inline bool lp_better(int64_t v, int32_t q, int64_t bv, int32_t bq) {

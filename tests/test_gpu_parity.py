@@ -725,7 +725,7 @@ def gpu_cluster(wl, order, R, M, mode):
 
 @pytest.mark.parametrize("cfg,seed", [(1, 0), (2, 0), (3, 0), (5, 1)])
 @pytest.mark.parametrize("mode", [0, 1])
-def test_cluster_configs(cfg, seed, mode):
+def test_cluster_configs(cfg, seed, mode, bl_path):
     wl, rt, rb = config(cfg, seed)
     pr = rb[2]
     for R, M in ((200, -1), (37, -1), (300, int(wl.cap.min()) // 9)):

@@ -125,3 +125,69 @@ def test_levels_policy_cycle_detected():
     with pytest.raises(cel.CelError) as ei:
         cel.topo_levels(g)
     assert ei.value.code == -2
+
+
+def gpu_cluster(wl, order, R, M):
+    g, d = cel.Graph.from_arrays(wl, DEV), cel.Devices.from_arrays(wl)
+    cid, C, cut = cel.cluster(g, d, tt(order, np.int32), R, M, cel.CLUSTER_DP)
+    return np_(cid), C, cut, cel.cluster_info()
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 5])
+def test_cluster_dp_by_policy_iteration(cfg):
+    """The DP of eq. 4-6 as a shortest path over breakpoints, by policy
+    iteration: clusters, their number and the cut cost equal the oracle's
+    sequential DP (ties to the smallest start) for several windows and caps."""
+    wl = make_config(cfg, 0)
+    lev, oid, lp, L = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    avg = int(wl.mem.sum()) // wl.n
+    for R, M in ((200, -1), (37, -1), (1, -1), (1000, avg * 40)):
+        ref = O.cluster(wl, pr, R, M)
+        cid, C, cut, (path, iters) = gpu_cluster(wl, pr, R, M)
+        assert C == ref[1] and cut == ref[2] and np.array_equal(cid, ref[0]), (R, M)
+        assert path in (0, 1) and iters >= 1, (R, M)
+        if cfg in (2, 3) and R == 200:
+            assert path == 0, (R, M)
+
+
+def test_cluster_dp_policy_random_orders():
+    """Random DAGs of 20,000-30,000 nodes (1-3 parents among the previous 500
+    ids, some edges doubled, some costs zero), clustered on random
+    topological orders (not level-monotone)."""
+    import heapq
+    for s in range(3):
+        n = 20000 + 5000 * s
+        rng = np.random.default_rng(900 + s)
+        k = rng.integers(1, 4, n)
+        k[0] = 0
+        dst = np.repeat(np.arange(n), k)
+        src = dst - 1 - (rng.random(dst.size) * np.minimum(dst, 500)).astype(np.int64)
+        edges = list(zip(src.tolist(), dst.tolist()))
+        if s == 1:  # parallel edges
+            edges += edges[::7]
+        w = rng.integers(1, 60, n)
+        ob = rng.integers(0, 300, n)
+        if s == 2:
+            w[rng.random(n) < 0.2] = 0
+            ob[rng.random(n) < 0.2] = 0
+        wl = from_edges(n, edges, w, ob, 3, [int(2 * ob.sum() + n)] * 3, 7, 3)
+        # a random topological order: Kahn with random priorities
+        indeg = np.diff(wl.in_ptr).copy()
+        key = rng.random(n)
+        heap = [(key[v], v) for v in range(n) if indeg[v] == 0]
+        heapq.heapify(heap)
+        order = []
+        while heap:
+            _, u = heapq.heappop(heap)
+            order.append(u)
+            for e in range(wl.out_ptr[u], wl.out_ptr[u + 1]):
+                v = wl.out_idx[e]
+                indeg[v] -= 1
+                if indeg[v] == 0:
+                    heapq.heappush(heap, (key[v], v))
+        order = np.array(order, np.int32)
+        for R in (64, 300):
+            ref = O.cluster(wl, order, R, -1)
+            cid, C, cut, (path, iters) = gpu_cluster(wl, order, R, -1)
+            assert C == ref[1] and cut == ref[2] and np.array_equal(cid, ref[0]), (s, R)
