@@ -93,27 +93,36 @@ def source_hash(files) -> str:
 
 
 def pmc_summary(fetch_csv: str, write_csv: str, calib_mib: int, extra_csvs=(), only=None) -> str:
-    """Markdown summary of rocprofv3 counter CSVs: per-kernel mean per dispatch,
-    FETCH_SIZE / WRITE_SIZE scaled by what they read for a plain copy of
-    calib_mib MiB (the largest __amd_rocclr_copyBuffer dispatch)."""
+    """Markdown summary of rocprofv3 counter CSVs: per kernel, the counters of
+    its first dispatch (in a run with --warmup 0 --steps 1 that is the timed
+    step's; later dispatches of the same kernel belong to other rows, on other
+    graphs or placements), FETCH_SIZE / WRITE_SIZE scaled by what they read
+    for a plain copy of calib_mib MiB (the largest __amd_rocclr_copyBuffer
+    dispatch)."""
     import csv
     from collections import defaultdict
 
-    vals = defaultdict(lambda: defaultdict(list))
+    # kernel -> counter -> {dispatch id: value}
+    vals = defaultdict(lambda: defaultdict(dict))
     for path in (fetch_csv, write_csv, *extra_csvs):
         with open(path) as fh:
             for r in csv.DictReader(fh):
-                vals[r["Kernel_Name"]][r["Counter_Name"]].append(float(r["Counter_Value"]))
+                vals[r["Kernel_Name"]][r["Counter_Name"]][int(r["Dispatch_Id"])] = \
+                    float(r["Counter_Value"])
     copy = [v for k, v in vals.items() if k.startswith("__amd_rocclr_copyBuffer")]
-    cf = max(x for v in copy for x in v.get("FETCH_SIZE", [0]))
-    cw = max(x for v in copy for x in v.get("WRITE_SIZE", [0]))
+    cf = max(x for v in copy for x in v.get("FETCH_SIZE", {0: 0}).values())
+    cw = max(x for v in copy for x in v.get("WRITE_SIZE", {0: 0}).values())
     kib = calib_mib * 1024.0
     ff, fw = kib / cf, kib / cw
     lines = [f"copy calibration: {calib_mib} MiB copied; FETCH_SIZE read {cf:.1f} KiB, "
              f"WRITE_SIZE {cw:.1f} KiB; factors fetch {ff:.4f} write {fw:.4f}", "",
              "| kernel | source | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes (scaled) |"
-             " other counters (mean per dispatch) |",
+             " other counters (first dispatch) |",
              "|---|---|---:|---:|---:|---:|---|"]
+
+    def first(d):
+        return d[min(d)]
+
     for name, (sym, files) in PMC_KERNELS.items():
         if only and name not in only:
             continue
@@ -121,9 +130,8 @@ def pmc_summary(fetch_csv: str, write_csv: str, calib_mib: int, extra_csvs=(), o
         if not hits:
             continue
         v = hits[0]
-        f = sum(v["FETCH_SIZE"]) / len(v["FETCH_SIZE"])
-        w = sum(v["WRITE_SIZE"]) / len(v["WRITE_SIZE"])
-        other = ", ".join(f"{c} {sum(x) / len(x):.0f}" for c, x in sorted(v.items())
+        f, w = first(v["FETCH_SIZE"]), first(v["WRITE_SIZE"])
+        other = ", ".join(f"{c} {first(x):.0f}" for c, x in sorted(v.items())
                           if c not in ("FETCH_SIZE", "WRITE_SIZE"))
         lines.append(f"| {name} | {source_hash(files)} | {len(v['FETCH_SIZE'])} | {f:.1f} | "
                      f"{w:.1f} | {(f * ff + w * fw) * 1024:.0f} | {other} |")

@@ -12,29 +12,33 @@ import bench  # noqa: E402
 
 
 def _counter_csv(path, rows):
+    """rows of (kernel, counter, value, dispatch id)"""
     with open(path, "w", newline="") as fh:
-        w = csv.DictWriter(fh, fieldnames=["Kernel_Name", "Counter_Name", "Counter_Value"])
+        w = csv.DictWriter(fh, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name",
+                                           "Counter_Value"])
         w.writeheader()
-        for k, c, v in rows:
-            w.writerow({"Kernel_Name": k, "Counter_Name": c, "Counter_Value": v})
+        for k, c, v, d in rows:
+            w.writerow({"Dispatch_Id": d, "Kernel_Name": k, "Counter_Name": c,
+                        "Counter_Value": v})
 
 
 def test_pmc_summary_scales_by_the_copy(tmp_path):
     """A 1 MiB copy that reads 512 KiB (FETCH) and writes 1024 KiB (WRITE) gives
-    factors 2 and 1; a kernel's HBM bytes are the scaled sum, mean per dispatch."""
+    factors 2 and 1; a kernel's HBM bytes are the scaled sum of its first
+    dispatch's counters (the timed step's; rows may come in any order)."""
     f, w = tmp_path / "f.csv", tmp_path / "w.csv"
     sym = bench.PMC_KERNELS["k_kahn"][0]
-    _counter_csv(f, [("__amd_rocclr_copyBuffer", "FETCH_SIZE", 512.0),
-                     (sym + "int)", "FETCH_SIZE", 100.0), (sym + "int)", "FETCH_SIZE", 300.0)])
-    _counter_csv(w, [("__amd_rocclr_copyBuffer", "WRITE_SIZE", 1024.0),
-                     (sym + "int)", "WRITE_SIZE", 50.0), (sym + "int)", "WRITE_SIZE", 50.0)])
+    _counter_csv(f, [("__amd_rocclr_copyBuffer", "FETCH_SIZE", 512.0, 1),
+                     (sym + "int)", "FETCH_SIZE", 300.0, 9), (sym + "int)", "FETCH_SIZE", 100.0, 4)])
+    _counter_csv(w, [("__amd_rocclr_copyBuffer", "WRITE_SIZE", 1024.0, 1),
+                     (sym + "int)", "WRITE_SIZE", 70.0, 9), (sym + "int)", "WRITE_SIZE", 50.0, 4)])
     out = bench.pmc_summary(str(f), str(w), 1)
     assert "factors fetch 2.0000 write 1.0000" in out
     row = next(line for line in out.splitlines() if line.startswith("| k_kahn |"))
     cells = [c.strip() for c in row.strip("|").split("|")]
     assert cells[1] == bench.source_hash(bench.PMC_KERNELS["k_kahn"][1])
-    assert cells[2] == "2" and float(cells[3]) == 200.0 and float(cells[4]) == 50.0
-    assert float(cells[5]) == (200.0 * 2 + 50.0 * 1) * 1024
+    assert cells[2] == "2" and float(cells[3]) == 100.0 and float(cells[4]) == 50.0
+    assert float(cells[5]) == (100.0 * 2 + 50.0 * 1) * 1024
 
 
 def test_traffic_only_while_the_sources_match(tmp_path, monkeypatch):
