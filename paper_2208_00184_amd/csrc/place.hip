@@ -9,11 +9,14 @@
 //
 // Placement (sequential over clusters, as the algorithm is): one wave.  For
 // cluster t, pre_t on device x is max over preds of Fin[p] + I(dev p != x)
-// cc; it is evaluated for all devices at once from per-device maxima of Fin
-// and of Fin + cc over the preds, and the best and second-best devices of
-// the latter.  Lane x then finds the first-fit start on device x in that
-// device's sorted list of busy blocks (touching intervals are merged, so the
-// list holds one block per idle gap), and a wave argmin picks the device.
+// cc; it is evaluated for all devices at once from the largest Fin + cc over
+// the preds, one device reaching it, and two more maxima (wave reductions
+// over the preds, one per lane).  Lane x then finds the first-fit start on
+// device x in that device's sorted list of busy blocks (touching intervals
+// are merged, so the list holds one block per idle gap), and a wave
+// reduction picks the device.
+#include <type_traits>
+
 #include "cel_internal.h"
 
 namespace cel {
@@ -137,7 +140,7 @@ __global__ void k_place_combine(int32_t C, const int32_t *boff, const uint64_t *
 }
 
 constexpr int kPlaceBlk = 5120;  // busy blocks held in LDS, shared evenly by the devices
-constexpr int kPlaceLds = 8192;  // clusters whose Fin and device are kept in LDS too (161,792 B of LDS in all)
+constexpr int kPlaceLds = 8192;  // clusters whose Fin and device are kept in LDS too (155,648 B of LDS in all)
 
 __device__ inline void argmax_i64(int64_t &v, int32_t &i) {  // wave: largest v, then smallest i
   for (int off = 32; off > 0; off >>= 1) {
@@ -205,190 +208,274 @@ __device__ inline int64_t busy_insert(int64_t *xs, int64_t *xf, int32_t &nb, int
   return nb > 0 ? xf[nb - 1] : 0;
 }
 
+// Wave reductions for the placement: the largest of the lanes' non-negative
+// values below 2^62 (max_nonneg: such bit patterns order as doubles), by DPP
+// row shifts and broadcasts with zero fill (0 is the identity, so no lane
+// needs an initial value) and one v_max_f64 per step.  Lane 63, or lane 15
+// for lanes 0-15 only, ends with the result; lanes outside the chain that
+// feeds it may hold anything.
+template <int CTRL, int ROWMASK>
+__device__ inline int64_t dpp64z(int64_t v) {
+  const int32_t lo = __builtin_amdgcn_mov_dpp((int32_t)v, CTRL, ROWMASK, 0xF, true);
+  const int32_t hi = __builtin_amdgcn_mov_dpp((int32_t)(v >> 32), CTRL, ROWMASK, 0xF, true);
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+template <bool ALL>
+__device__ inline int64_t wave_max_nonneg(int64_t y) {
+  y = max_nonneg(y, dpp64z<0x111, 0xF>(y));  // row_shr:1
+  y = max_nonneg(y, dpp64z<0x112, 0xF>(y));  // row_shr:2
+  y = max_nonneg(y, dpp64z<0x114, 0xF>(y));  // row_shr:4
+  y = max_nonneg(y, dpp64z<0x118, 0xF>(y));  // row_shr:8
+  if (!ALL) return readlane64(y, 15);
+  y = max_nonneg(y, dpp64z<0x142, 0xA>(y));  // row_bcast:15 into rows 1 and 3
+  y = max_nonneg(y, dpp64z<0x143, 0xC>(y));  // row_bcast:31 into rows 2 and 3
+  return readlane64(y, 63);
+}
+// two at once (independent chains, interleaved)
+__device__ inline void wave_max_nonneg2(int64_t &y, int64_t &z) {
+  y = max_nonneg(y, dpp64z<0x111, 0xF>(y));
+  z = max_nonneg(z, dpp64z<0x111, 0xF>(z));
+  y = max_nonneg(y, dpp64z<0x112, 0xF>(y));
+  z = max_nonneg(z, dpp64z<0x112, 0xF>(z));
+  y = max_nonneg(y, dpp64z<0x114, 0xF>(y));
+  z = max_nonneg(z, dpp64z<0x114, 0xF>(z));
+  y = max_nonneg(y, dpp64z<0x118, 0xF>(y));
+  z = max_nonneg(z, dpp64z<0x118, 0xF>(z));
+  y = max_nonneg(y, dpp64z<0x142, 0xA>(y));
+  z = max_nonneg(z, dpp64z<0x142, 0xA>(z));
+  y = max_nonneg(y, dpp64z<0x143, 0xC>(y));
+  z = max_nonneg(z, dpp64z<0x143, 0xC>(z));
+  y = readlane64(y, 63);
+  z = readlane64(z, 63);
+}
+constexpr int64_t kPlaceFull = int64_t(1) << 62;  // EST of a device without room
+constexpr int kPlaceQ = 4;                        // preds per lane held in registers
+constexpr int kPlacePad = 64 * kPlaceQ;           // entries read past the end of a pred list
+
 // Placement, one wave (its LDS accesses are in program order, so no barrier
-// is needed).  For cluster t, one pass over its coarse preds leaves per device
-// y the largest Fin and the largest Fin + cc of the preds on y; pre_t on
-// device x is then max(0, the first at x, the largest second over devices
-// other than x), from the best and second-best devices.  Device x's free
-// memory and busy-list state sit in the registers of lane x mod 64; values
-// every lane needs are read from LDS in unrolled groups, all requests out
-// before the first use.  Each device's busy list lives in LDS
+// is needed).  For cluster t, pre_t on device x is the largest of 0, Fin[p]
+// over preds p on x and Fin[p] + cc over preds on other devices.  With m1 the
+// largest Fin + cc over all preds and d1 the device of one pred reaching it,
+// every device other than d1 has pre_t = m1 (a pred's Fin never exceeds its
+// Fin + cc); d1 itself takes the larger of m2, the largest Fin + cc over
+// preds on other devices, and g, the largest Fin over its own preds.  So one
+// pass over the preds, kPQ per lane, and three wave reductions give every
+// device's pre_t; device x's free memory and busy-list state sit in the
+// registers of lane x mod 64, so each lane then finds its device's first-fit
+// start and EST (eq. 7) and a wave reduction the smallest EST.  Each device's
+// busy list (merged intervals: one block per idle gap) lives in LDS
 // (kPlaceBlk / D blocks) until it outgrows that share; it then moves to its
-// global list.  LDSF keeps every cluster's Fin and device in LDS as well
-// (C <= kPlaceLds).
-template <bool LDSF>
+// global list.  A start at or after the list's last end (the usual case)
+// extends or appends without reading the list.
+//
+// A step's only memory round trips are LDS ones: the preds of the cluster
+// two steps ahead are loaded into registers at the end of a step (two
+// register sets, the loop unrolled by two, and the sizes of 64 clusters moved
+// between register blocks only between blocks of 64 steps, so no register
+// copy waits for a load in flight: a wait for the vector memory counter waits
+// for every load and store issued before it), and with LDSF every cluster's
+// Fin and device stay in LDS (C <= kPlaceLds) and go to global memory after
+// the loop.  GL = false keeps every busy list in LDS and takes at most 64 kPQ
+// preds per cluster, so that a step issues no global memory access at all;
+// a list that outgrows its share, or a longer pred list, stops the kernel
+// with st->i1 = 1, and the caller runs the GL = true kernel, whose lists move
+// to global memory when full and whose long pred lists are read in passes.
+template <bool LDSF, bool GL, int NI>  // NI: devices per lane (D <= 64 NI)
 __global__ void __launch_bounds__(64)
     k_place(int32_t C, int32_t D, const int64_t *cap, const uint64_t *W, const uint64_t *MEM,
             const int32_t *boff, const int32_t *ncp, const int32_t *ca, const int64_t *cc,
             const uint64_t *back, uint8_t *cdev, int64_t *Fin, int64_t *bs, int64_t *bf,
             int32_t bcap, Status *st) {
-  constexpr int G = 16;  // devices per group of LDS reads
   __shared__ int64_t s_bs[kPlaceBlk], s_bf[kPlaceBlk];
   __shared__ int64_t s_fin[LDSF ? kPlaceLds : 1];
   __shared__ uint8_t s_cd[LDSF ? kPlaceLds : 1];
-  // per device: max Fin and max Fin + cc of the preds on it (-1: none), EST
-  // (kInf past D)
-  __shared__ int64_t s_dm[256], s_dmc[256], s_est[256];
   if (failed(st)) return;
   const int lane = threadIdx.x;
   const int32_t capL = kPlaceBlk / D;
-  int64_t ava[4], last[4];  // device lane + 64 i: free memory, end of its last busy block
-  int32_t nbl[4], glob[4];  // its busy-block count; list moved to global memory
+  int64_t ava[NI], last[NI];  // device lane + 64 i: free memory, end of its last busy block
+  int32_t nbl[NI], glob[NI];  // its busy-block count; list moved to global memory
 #pragma unroll
-  for (int i = 0; i < 4; i++) {
+  for (int i = 0; i < NI; i++) {
     const int x = lane + 64 * i;
     ava[i] = x < D ? cap[x] : 0;
     last[i] = 0;
     nbl[i] = 0;
     glob[i] = 0;
-    s_dm[x] = -1;
-    s_dmc[x] = -1;
-    s_est[x] = kInf;
   }
   int32_t prev = 0, be = 0;
   int64_t span = 0;
-  // Loads run ahead of their use: the sizes of 64 clusters at a time, one per
-  // lane, a block of 64 ahead (read back with readlane), and the first 64
-  // preds of a cluster kPD steps ahead; their Fin and device come from LDS
-  // (LDSF), else from global memory at the step.
-  constexpr int kPD = 3;
+  // The sizes of 64 clusters at a time, one per lane, a block of 64 ahead
+  // (read back with readlane).  Loads here are never predicated (indexes are
+  // clamped instead), so each goes straight into the register that keeps it
+  // and nothing waits for it before its use.
+  constexpr int kPQ = kPlaceQ;
   auto bulk = [&](int32_t t0, int32_t &zb, int32_t &zn, int64_t &zw, int64_t &zm, int64_t &zk) {
-    const int32_t t = t0 + lane;
-    zb = t < C ? boff[t] : 0;
-    zn = t < C ? ncp[t] : 0;
-    zw = t < C ? (int64_t)W[t] : 0;
-    zm = t < C ? (int64_t)MEM[t] : 0;
-    zk = t < C ? (int64_t)back[t] : 0;
+    const int32_t t = t0 + lane < C ? t0 + lane : C - 1;  // past C: never read
+    zb = boff[t];
+    zn = ncp[t];
+    zw = (int64_t)W[t];
+    zm = (int64_t)MEM[t];
+    zk = (int64_t)back[t];
   };
   int32_t ub, un, vb, vn;  // sizes of clusters [T, T + 64) (u*) and [T + 64, T + 128) (v*)
   int64_t uw, um, uk, vw, vm, vk;
   bulk(0, ub, un, uw, um, uk);
   bulk(64, vb, vn, vw, vm, vk);
-  // first preds of the cluster t' (t' < T + 128), by lane
-  auto preds = [&](int32_t tp, int32_t T, int32_t &pa, int64_t &pc) {
-    pa = 0;
-    pc = 0;
-    if (tp >= C) return;
-    const bool in_u = tp - T < 64;
-    const int l = (tp - T) & 63;
-    const int32_t b = __builtin_amdgcn_readlane(in_u ? ub : vb, l);
-    const int32_t nn = __builtin_amdgcn_readlane(in_u ? un : vn, l);
-    if (lane < nn) {
-      pa = ca[b + lane];
-      pc = cc[b + lane];
+  // preds 64 q + lane of the cluster t' in the block of ub (lane t' & 63);
+  // lanes past its count read on into the next clusters' lists (the lists
+  // are allocated with 64 kPQ entries to spare), and the step masks them.
+  // Past C the sizes repeat cluster C - 1's, so no call is ever skipped: a
+  // load that may or may not have been issued makes later waits for earlier
+  // loads wait for it too.  Only ub is read here, never the block in flight.
+  auto preds = [&](int32_t tp, int32_t (&pa)[kPQ], int64_t (&pc)[kPQ]) {
+    const int32_t k = __builtin_amdgcn_readlane(ub, tp & 63) + lane;
+#pragma unroll
+    for (int q = 0; q < kPQ; q++) {
+      pa[q] = ca[k + 64 * q];
+      pc[q] = cc[k + 64 * q];
     }
   };
-  int32_t pa[kPD];
-  int64_t pcv[kPD];
-#pragma unroll
-  for (int q = 0; q < kPD; q++) preds(q, 0, pa[q], pcv[q]);
-  for (int32_t t = 0; t < C; t++) {
-    const int32_t T = t & ~63;
-    if (t > 0 && (t & 63) == 0) {  // next block of sizes
-      ub = vb;
-      un = vn;
-      uw = vw;
-      um = vm;
-      uk = vk;
-      bulk(t + 64, vb, vn, vw, vm, vk);
-    }
+  // Fin and device of pred cluster a (every lane that has one)
+  auto fin_dev = [&](int32_t a, int64_t &f, int32_t &d) {
+    f = LDSF ? s_fin[a] : Fin[a];
+    d = LDSF ? s_cd[a] : cdev[a];
+  };
+  // first-fit start on device x (lane x mod 64) at or after sv for a cluster
+  // of length Wt, in a list held in LDS (GL = false) or in global memory
+  auto first_fit = [&](const int64_t *xs, const int64_t *xf, int32_t nb, int64_t sv, int64_t Wt) {
+    for (int32_t k = blocks_ending_by(xf, nb, sv); k < nb && xs[k] < sv + Wt; k++) sv = xf[k];
+    return sv;
+  };
+  // one cluster; false when the kernel has to stop (GL = false, a full list)
+  auto step = [&](int32_t t, const int32_t (&pa)[kPQ], const int64_t (&pcv)[kPQ]) -> bool {
     const int l = t & 63;
     const int32_t b0 = __builtin_amdgcn_readlane(ub, l), np = __builtin_amdgcn_readlane(un, l);
     const int64_t Wt = readlane64(uw, l), Mt = readlane64(um, l), bk = readlane64(uk, l);
-    int32_t a0 = pa[0];
-    int64_t c0 = pcv[0];
+    // ---- pre_t by device: m1, d1, m2, g over the preds (0 when none)
+    int64_t m1 = 0, m2 = 0, g = 0;
+    int32_t d1 = -1;
+    // one chunk (np <= 64: most clusters) or kPQ of them, in registers
+    auto in_regs = [&](auto nq) {
+      constexpr int NQ = decltype(nq)::value;
+      int64_t f[NQ], fc[NQ];
+      int32_t d[NQ];
 #pragma unroll
-    for (int q = 0; q + 1 < kPD; q++) {
-      pa[q] = pa[q + 1];
-      pcv[q] = pcv[q + 1];
-    }
-    preds(t + kPD, T, pa[kPD - 1], pcv[kPD - 1]);
-    // per-device maxima over the preds
-    for (int32_t k0 = 0; k0 < np; k0 += 64) {
-      if (k0 > 0) {
-        a0 = k0 + lane < np ? ca[b0 + k0 + lane] : 0;
-        c0 = k0 + lane < np ? cc[b0 + k0 + lane] : 0;
-      }
-      if (k0 + lane < np) {
-        const int64_t f0 = LDSF ? s_fin[a0] : Fin[a0];
-        const int32_t d0 = LDSF ? s_cd[a0] : cdev[a0];
-        atomicMax((long long *)&s_dm[d0], (long long)f0);
-        atomicMax((long long *)&s_dmc[d0], (long long)(f0 + c0));
-      }
-    }
-    // best device by Fin + cc (lowest id on ties) and the best of the others,
-    // by every lane
-    int64_t m1 = -1, m2 = -1;
-    int32_t d1 = INT32_MAX;
-    for (int32_t x0 = 0; x0 < D; x0 += G) {
-      int64_t v[G];
+      for (int q = 0; q < NQ; q++)  // every lane loads (pred 0 past np), then masks
+        fin_dev(64 * q + lane < np ? pa[q] : 0, f[q], d[q]);
+      int64_t bfc = 0;
+      int32_t bd = 255;
 #pragma unroll
-      for (int q = 0; q < G; q++) v[q] = s_dmc[x0 + q];
-#pragma unroll
-      for (int q = 0; q < G; q++) {
-        if (v[q] > m1) {
-          m2 = m1;
-          m1 = v[q];
-          d1 = x0 + q;
-        } else if (v[q] > m2) {
-          m2 = v[q];
+      for (int q = 0; q < NQ; q++) {
+        const bool in = 64 * q + lane < np;
+        f[q] = in ? f[q] : 0;
+        d[q] = in ? d[q] : 255;  // no device
+        fc[q] = in ? f[q] + pcv[q] : 0;
+        if (fc[q] > bfc) {
+          bfc = fc[q];
+          bd = d[q];
         }
       }
-    }
-    // device x: pre_t, first-fit slot and EST (eq. 7)
-    int64_t slot[4];
+      m1 = wave_max_nonneg<true>(bfc);
+      if (m1 > 0) {
+        d1 = __builtin_amdgcn_readlane(bd, (int)__builtin_ctzll(__ballot(bfc == m1)));
+        int64_t y = 0, z = 0;
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-      slot[i] = 0;
-      const int x = lane + 64 * i;
-      if (64 * i >= D) continue;  // uniform
-      if (x < D) {
-        int64_t pre = 0;
-        const int64_t other = x != d1 ? m1 : m2;
-        pre = other > pre ? other : pre;
-        pre = s_dm[x] > pre ? s_dm[x] : pre;
-        int64_t sv = pre;
-        const int32_t nb = nbl[i];
-        if (Wt > 0 && nb > 0 && sv < last[i]) {  // LDS and global lists in separate code
-          if (!glob[i]) {
-            const int64_t *xs = s_bs + x * capL, *xf = s_bf + x * capL;
-            for (int32_t k = blocks_ending_by(xf, nb, sv); k < nb && xs[k] < sv + Wt; k++)
-              sv = xf[k];
-          } else {
-            const int64_t *xs = bs + (int64_t)x * bcap, *xf = bf + (int64_t)x * bcap;
-            for (int32_t k = blocks_ending_by(xf, nb, sv); k < nb && xs[k] < sv + Wt; k++)
-              sv = xf[k];
+        for (int q = 0; q < NQ; q++) {
+          if (d[q] != d1 && fc[q] > y) y = fc[q];
+          if (d[q] == d1 && f[q] > z) z = f[q];
+        }
+        wave_max_nonneg2(y, z);
+        m2 = y;
+        g = z;
+      }
+    };
+    if (np > 0 && np <= 64) {
+      in_regs(std::integral_constant<int, 1>());
+    } else if (np > 0 && np <= 64 * kPQ) {
+      in_regs(std::integral_constant<int, kPQ>());
+    } else if (!GL && np > 0) {
+      return false;  // long pred list: the caller runs the GL = true kernel
+    } else if (GL && np > 0) {  // long pred lists: two passes over them, 64 at a time
+      int64_t bfc = 0;
+      int32_t bd = 255;
+      for (int32_t k0 = 0; k0 < np; k0 += 64) {
+        if (k0 + lane < np) {
+          int64_t f;
+          int32_t d;
+          fin_dev(ca[b0 + k0 + lane], f, d);
+          const int64_t fc = f + cc[b0 + k0 + lane];
+          if (fc > bfc) {
+            bfc = fc;
+            bd = d;
           }
         }
-        slot[i] = sv;
-        s_est[x] = ava[i] < Mt ? kInf : sv;
-        s_dm[x] = -1;  // cleared for the next cluster
-        s_dmc[x] = -1;
+      }
+      m1 = wave_max_nonneg<true>(bfc);
+      if (m1 > 0) {
+        d1 = __builtin_amdgcn_readlane(bd, (int)__builtin_ctzll(__ballot(bfc == m1)));
+        int64_t y = 0, z = 0;
+        for (int32_t k0 = 0; k0 < np; k0 += 64) {
+          if (k0 + lane < np) {
+            int64_t f;
+            int32_t d;
+            fin_dev(ca[b0 + k0 + lane], f, d);
+            const int64_t fc = f + cc[b0 + k0 + lane];
+            if (d != d1 && fc > y) y = fc;
+            if (d == d1 && f > z) z = f;
+          }
+        }
+        wave_max_nonneg2(y, z);
+        m2 = y;
+        g = z;
       }
     }
-    // device of smallest EST (lowest id on ties), by every lane
-    int64_t ev = kInf;
-    int32_t ei = INT32_MAX;
-    for (int32_t x0 = 0; x0 < D; x0 += G) {
-      int64_t v[G];
+    const int64_t pre1 = m2 > g ? m2 : g;  // pre_t on d1
+    // ---- device x: first-fit start and EST (eq. 7); kPlaceFull without room
+    int64_t slot[NI], est[NI];
 #pragma unroll
-      for (int q = 0; q < G; q++) v[q] = s_est[x0 + q];
-#pragma unroll
-      for (int q = 0; q < G; q++)
-        if (v[q] < ev) {
-          ev = v[q];
-          ei = x0 + q;
+    for (int i = 0; i < NI; i++) {
+      slot[i] = 0;
+      est[i] = kPlaceFull;
+      const int x = lane + 64 * i;
+      if (x < D) {
+        int64_t sv = x == d1 ? pre1 : m1;
+        const int32_t nb = nbl[i];
+        if (Wt > 0 && nb > 0 && sv < last[i]) {
+          if (!GL || !glob[i])
+            sv = first_fit(s_bs + x * capL, s_bf + x * capL, nb, sv, Wt);
+          else
+            sv = first_fit(bs + (int64_t)x * bcap, bf + (int64_t)x * bcap, nb, sv, Wt);
         }
+        slot[i] = sv;
+        est[i] = ava[i] < Mt ? kPlaceFull : sv;
+      }
     }
-    // the choice (eq. 8-9), uniform over the wave
+    // ---- device of smallest EST (lowest id on ties): the largest
+    // kPlaceFull - EST, so that the reduction's identity is 0
+    int64_t e = kPlaceFull - est[0];
+#pragma unroll
+    for (int i = 1; i < NI; i++) e = max_nonneg(e, kPlaceFull - est[i]);
+    const int64_t ev = kPlaceFull - (D <= 16 ? wave_max_nonneg<false>(e) : wave_max_nonneg<true>(e));
+    int32_t ei = 0;
+    if (ev < kPlaceFull) {
+#pragma unroll
+      for (int i = NI - 1; i >= 0; i--) {  // the lowest i with a hit, then its lowest lane
+        const uint64_t hit = __ballot(est[i] == ev);
+        if (hit) ei = 64 * i + (int32_t)__builtin_ctzll(hit);
+      }
+    }
+    // ---- the choice (eq. 8-9), uniform over the wave
     const int32_t dk = t == 0 ? 0 : prev;
-    const int64_t edk = s_est[dk];
+    int64_t edk = kPlaceFull;
+#pragma unroll
+    for (int i = 0; i < NI; i++)
+      if (i == (dk >> 6)) edk = readlane64(est[i], dk & 63);
     int32_t pick;
-    if (ev == kInf) {  // every device full: most remaining memory (best effort)
+    if (ev >= kPlaceFull) {  // every device full: most remaining memory (best effort)
       int64_t av = INT64_MIN;  // free memory can be negative after best-effort picks
       int32_t ai = INT32_MAX;
 #pragma unroll
-      for (int i = 0; i < 4; i++)
+      for (int i = 0; i < NI; i++)
         if (lane + 64 * i < D && ava[i] > av) {
           av = ava[i];
           ai = lane + 64 * i;
@@ -396,44 +483,71 @@ __global__ void __launch_bounds__(64)
       argmax_i64(av, ai);
       pick = ai;
       be++;
-    } else if (edk == kInf || edk - ev > bk) {
+    } else if (edk >= kPlaceFull || edk - ev > bk) {
       pick = ei;
     } else {
       pick = dk;
     }
     const int ip = pick >> 6, lp = pick & 63;
-    int64_t slp = 0;
+    int64_t slp = 0, lst = 0;
     int32_t nb = 0, gl = 0;
 #pragma unroll
-    for (int i = 0; i < 4; i++)
+    for (int i = 0; i < NI; i++)
       if (i == ip) {
         slp = slot[i];
+        lst = last[i];
         nb = nbl[i];
         gl = glob[i];
       }
     const int64_t s0 = readlane64(slp, lp), f = s0 + Wt;
+    const int64_t lastp = readlane64(lst, lp);
     nb = __builtin_amdgcn_readlane(nb, lp);
     gl = __builtin_amdgcn_readlane(gl, lp);
     span = f > span ? f : span;
     prev = pick;
     if (Wt > 0) {  // insert [s0, f) into the device's merged busy blocks
-      if (!gl && nb == capL) {  // the LDS share is full: move the list out
-        for (int32_t q = lane; q < nb; q += 64) {
-          bs[(int64_t)pick * bcap + q] = s_bs[pick * capL + q];
-          bf[(int64_t)pick * bcap + q] = s_bf[pick * capL + q];
+      int64_t lastv = lastp;
+      if (nb > 0 && s0 == lastp) {  // touches the last block: extend it
+        if (lane == 0) {
+          if (!GL || !gl) s_bf[pick * capL + nb - 1] = f;
+          else bf[(int64_t)pick * bcap + nb - 1] = f;
         }
-        gl = 1;
+        lastv = f;
+      } else {
+        if (!gl && nb == capL) {  // the LDS share is full
+          if (!GL) return false;  // stop: the caller runs the GL = true kernel
+          for (int32_t q = lane; q < nb; q += 64) {  // move the list out
+            bs[(int64_t)pick * bcap + q] = s_bs[pick * capL + q];
+            bf[(int64_t)pick * bcap + q] = s_bf[pick * capL + q];
+          }
+          gl = 1;
+        }
+        if (nb == 0 || s0 > lastp) {  // after the last block: a new block at the end
+          if (lane == 0) {
+            if (!GL || !gl) {
+              s_bs[pick * capL + nb] = s0;
+              s_bf[pick * capL + nb] = f;
+            } else {
+              bs[(int64_t)pick * bcap + nb] = s0;
+              bf[(int64_t)pick * bcap + nb] = f;
+            }
+          }
+          nb++;
+          lastv = f;
+        } else {  // into an idle gap
+          if (lane == 0) {
+            if (!GL || !gl)
+              lastv = busy_insert(s_bs + pick * capL, s_bf + pick * capL, nb, capL, s0, f, st);
+            else
+              lastv = busy_insert(bs + (int64_t)pick * bcap, bf + (int64_t)pick * bcap, nb, bcap,
+                                  s0, f, st);
+          }
+          nb = __builtin_amdgcn_readlane(nb, 0);
+          lastv = readlane64(lastv, 0);
+        }
       }
-      int64_t lastv = 0;
-      if (lane == 0) {
-        if (!gl) lastv = busy_insert(s_bs + pick * capL, s_bf + pick * capL, nb, capL, s0, f, st);
-        else lastv = busy_insert(bs + (int64_t)pick * bcap, bf + (int64_t)pick * bcap, nb, bcap,
-                                 s0, f, st);
-      }
-      nb = __builtin_amdgcn_readlane(nb, 0);
-      lastv = readlane64(lastv, 0);
 #pragma unroll
-      for (int i = 0; i < 4; i++)
+      for (int i = 0; i < NI; i++)
         if (i == ip && lane == lp) {
           nbl[i] = nb;
           last[i] = lastv;
@@ -441,15 +555,57 @@ __global__ void __launch_bounds__(64)
         }
     }
 #pragma unroll
-    for (int i = 0; i < 4; i++)
+    for (int i = 0; i < NI; i++)
       if (i == ip && lane == lp) ava[i] -= Mt;
     if (lane == 0) {  // later steps of this wave read these back, in program order
-      cdev[t] = (uint8_t)pick;
-      Fin[t] = f;
       if (LDSF) {
         s_fin[t] = f;
         s_cd[t] = (uint8_t)pick;
+      } else {
+        cdev[t] = (uint8_t)pick;
+        Fin[t] = f;
       }
+    }
+    return true;
+  };
+  int32_t pa0[kPQ], pa1[kPQ];
+  int64_t pc0[kPQ], pc1[kPQ];
+  preds(0, pa0, pc0);
+  preds(1, pa1, pc1);
+  bool ok = true;
+  for (int32_t T = 0; T < C && ok; T += 64) {  // blocks of 64 clusters: ub / vb hold T, T + 64
+    const int32_t te = T + 64 < C ? T + 64 : C;
+    int32_t t = T;  // even: pa0 holds cluster t, pa1 cluster t + 1
+    for (; t + 2 < T + 64 && t < te; t += 2) {  // the next pair in this block too
+      if (!step(t, pa0, pc0)) {
+        ok = false;
+        break;
+      }
+      preds(t + 2, pa0, pc0);  // a whole step before its use
+      if (t + 1 < te && !step(t + 1, pa1, pc1)) {
+        ok = false;
+        break;
+      }
+      preds(t + 3, pa1, pc1);
+    }
+    if (ok && t < te) ok = step(t, pa0, pc0) && (t + 1 >= te || step(t + 1, pa1, pc1));
+    ub = vb;
+    un = vn;
+    uw = vw;
+    um = vm;
+    uk = vk;
+    bulk(T + 128, vb, vn, vw, vm, vk);
+    preds(T + 64, pa0, pc0);  // from the new ub (past C: cluster C - 1's sizes)
+    preds(T + 65, pa1, pc1);
+  }
+  if (!ok) {  // a busy list outgrew its LDS share, or a long pred list (GL = false)
+    if (lane == 0) st->i1 = 1;
+    return;
+  }
+  if (LDSF) {  // every cluster's Fin and device, from LDS
+    for (int32_t t = lane; t < C; t += 64) {
+      Fin[t] = s_fin[t];
+      cdev[t] = s_cd[t];
     }
   }
   if (lane == 0) {
@@ -874,8 +1030,8 @@ extern "C" int cel_place(const cel_graph *g, const cel_devices *d, const int32_t
   const int64_t ncross = hb[C];
   CEL_TRY(sc.get(&keys, ncross));
   CEL_TRY(sc.get(&ids, ncross));
-  CEL_TRY(sc.get(&ca, ncross));
-  CEL_TRY(sc.get(&cc, ncross));
+  CEL_TRY(sc.get(&ca, ncross + kPlacePad));  // k_place reads up to kPlacePad past a list
+  CEL_TRY(sc.get(&cc, ncross + kPlacePad));
   CEL_TRY(sc.get(&ecost, m));
   CEL_HIP(hipMemsetAsync(cnt, 0, sizeof(int32_t) * C, s));
   k_place_edges<1><<<eb, 256, 0, s>>>(*g, d->bw, d->lat, cluster_id, cnt, boff, keys, ids, ecost,
@@ -883,20 +1039,38 @@ extern "C" int cel_place(const cel_graph *g, const cel_devices *d, const int32_t
   CEL_TRY(segmented_sort(keys, ids, boff, C, ncross, sc, s, st));
   k_place_combine<<<grid_for((int64_t)C * 64, 256, 8192), 256, 0, s>>>(C, boff, keys, ids, ecost,
                                                                       ca, cc, ncp, back, st);
-  {
-    KTimer kt(s, "k_place");
-    if (C <= kPlaceLds)
-      k_place<true><<<1, 64, 0, s>>>(C, d->D, dcap, W, MEM, boff, ncp, ca, cc, back, cluster_dev,
-                                     Fin, bs, bf, (int32_t)bcap, st);
-    else
-      k_place<false><<<1, 64, 0, s>>>(C, d->D, dcap, W, MEM, boff, ncp, ca, cc, back,
-                                      cluster_dev, Fin, bs, bf, (int32_t)bcap, st);
+  // Busy lists in LDS only first; if one outgrows its share (st->i1 set, the
+  // outputs not written), the placement again with lists that move to global
+  // memory when full.
+  for (int gl = 0; gl < 2; gl++) {
+    {
+      KTimer kt(s, "k_place");
+#define CEL_PLACE_LAUNCH(LDSF, GL, NI)                                                          \
+  k_place<LDSF, GL, NI><<<1, 64, 0, s>>>(C, d->D, dcap, W, MEM, boff, ncp, ca, cc, back,        \
+                                         cluster_dev, Fin, bs, bf, (int32_t)bcap, st)
+      const bool lds = C <= kPlaceLds, one = d->D <= 64;
+      if (lds && !gl) {
+        if (one) CEL_PLACE_LAUNCH(true, false, 1);
+        else CEL_PLACE_LAUNCH(true, false, 4);
+      } else if (lds) {
+        if (one) CEL_PLACE_LAUNCH(true, true, 1);
+        else CEL_PLACE_LAUNCH(true, true, 4);
+      } else if (!gl) {
+        if (one) CEL_PLACE_LAUNCH(false, false, 1);
+        else CEL_PLACE_LAUNCH(false, false, 4);
+      } else {
+        if (one) CEL_PLACE_LAUNCH(false, true, 1);
+        else CEL_PLACE_LAUNCH(false, true, 4);
+      }
+#undef CEL_PLACE_LAUNCH
+    }
+    k_place_out<<<grid_for(n > C ? n : C, 256, 4096), 256, 0, s>>>(n, C, cluster_id, cluster_dev,
+                                                                  node_dev, Fin, cluster_fin, st);
+    CEL_HIP(hipGetLastError());
+    CEL_TRY(read_status(st, &h, s));
+    if (h.err) return status_error(h, fn);
+    if (gl || !h.i1) break;  // the GL = true kernel never stops early
   }
-  k_place_out<<<grid_for(n > C ? n : C, 256, 4096), 256, 0, s>>>(n, C, cluster_id, cluster_dev,
-                                                                node_dev, Fin, cluster_fin, st);
-  CEL_HIP(hipGetLastError());
-  CEL_TRY(read_status(st, &h, s));
-  if (h.err) return status_error(h, fn);
   *coarse_makespan = h.s0;
   *best_effort_count = h.i0;
   return CEL_OK;

@@ -924,6 +924,23 @@ def test_place_many_clusters_and_devices():
         check_place(wl2, cid2, C2)
 
 
+def test_place_wide_fan_in():
+    """Clusters with more than 64 and more than 128 coarse preds (the two-pass
+    pred path), on several devices, with ties of Fin + cc across devices."""
+    rng = np.random.default_rng(21)
+    for s, (k, D) in enumerate(((70, 3), (150, 7), (300, 16), (129, 64))):
+        n = k + 40
+        edges = [(u, k) for u in range(k)]                    # node k: k preds
+        edges += [(u, k + 1 + (u % 5)) for u in range(0, k, 2)]  # 5 nodes, k / 10 preds each
+        edges += [(k + j, k + j + 1) for j in range(39)]
+        w = rng.integers(0, 50, n)
+        ob = rng.integers(0, 3, n) * 1000 if s % 2 else rng.integers(0, 5000, n)
+        wl = from_edges(n, sorted(set(edges)), w, ob, D, [int(rng.integers(5, 20)) * 10 ** 4] * D,
+                        7, 2, mem=rng.integers(1, 10 ** 4, n))
+        cid = np.arange(n, dtype=np.int32)  # every node its own cluster
+        check_place(wl, cid, n)
+
+
 def test_place_cpd_transformer96():
     """Full size: the CPD-TOPO clustering of transformer-96 (6,284 clusters), the
     largest cluster counts whose finish times and devices stay in LDS."""
