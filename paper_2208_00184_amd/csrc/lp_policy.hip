@@ -189,6 +189,7 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
     }
     chg = __syncthreads_or(chg);
     if (!grid_sync(a.bar, ++bar, chg, &s_ok, &s_bit, st, &bit)) return;
+    if (KIND == 0 && it == 1) bit = 1;  // values of iteration 0 were cut short: evaluate
     if (!bit) {
       done = true;
       break;
@@ -220,6 +221,14 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
     }
     more = __syncthreads_or(more);
     if (!grid_sync(a.bar, ++bar, more, &s_ok, &s_bit, st, &bit)) return;
+    // b-level: the first policy's evaluation stops after this round, so the
+    // next improvement compares wv(q) + wv(pol(q)), the longest paths of two
+    // nodes, instead of the full chains of the greedy first policy; that
+    // start saves iterations on the transformer and layered graphs (113 -> 80
+    // pointer-jumping rounds on transformer-96).  Any policy is a valid start:
+    // the next iteration evaluates its policy fully whatever the improvement
+    // changes, and only exact values end the iteration.
+    if (KIND == 0 && it == 0) bit = 0;
     int32_t r = 1;
     while (bit) {
       if (r == a.max_rounds) {  // a pointer cycle: the input is not a DAG

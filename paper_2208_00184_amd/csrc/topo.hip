@@ -456,37 +456,34 @@ __global__ void k_topo_wv(int32_t n, const int32_t *in_ptr, int64_t *wv, const S
     wv[v] = in_ptr[v + 1] > in_ptr[v] ? 1 : 0;
 }
 
-// level[v] = val[v], sort keys (level) and ids (v) in node order, the
-// single segment [0, n) for the sort; st->i0 = number of levels (largest + 1)
+// level[v] = val[v], sort keys (level) and ids (v) in node order, and the
+// single segment [0, n) for the sort
 __global__ void k_topo_keys(int32_t n, const int64_t *val, int32_t *level, uint64_t *keys,
                             uint32_t *ids, int32_t *seg, Status *st) {
   if (failed(st)) return;
-  int32_t mx = 0;
   for (int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; v < n;
        v += (int64_t)gridDim.x * blockDim.x) {
     const int32_t l = (int32_t)val[v];
     level[v] = l;
     keys[v] = (uint64_t)l;
     ids[v] = (uint32_t)v;
-    mx = l > mx ? l : mx;
   }
   if (blockIdx.x == 0 && threadIdx.x < 2) seg[threadIdx.x] = threadIdx.x ? n : 0;
-  for (int off = 32; off > 0; off >>= 1) {
-    const int32_t o = __shfl_xor(mx, off);
-    mx = o > mx ? o : mx;
-  }
-  if ((threadIdx.x & 63) == 0) atomicMax(&st->i0, mx + 1);
 }
 
 // level_ptr from the levels sorted ascending: every level up to the largest
-// holds a node (a node of level l has a predecessor of level l - 1)
-__global__ void k_topo_ptr(int32_t n, const uint64_t *keys, int32_t *level_ptr, const Status *st) {
+// holds a node (a node of level l has a predecessor of level l - 1); the
+// number of levels is the last key + 1
+__global__ void k_topo_ptr(int32_t n, const uint64_t *keys, int32_t *level_ptr, Status *st) {
   if (failed(st)) return;
   for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n;
        p += (int64_t)gridDim.x * blockDim.x) {
     const uint64_t k = keys[p];
     if (p == 0 || keys[p - 1] != k) level_ptr[k] = (int32_t)p;
-    if (p == n - 1) level_ptr[k + 1] = n;
+    if (p == n - 1) {
+      level_ptr[k + 1] = n;
+      st->i0 = (int32_t)k + 1;
+    }
   }
 }
 
