@@ -128,10 +128,26 @@ __global__ void __launch_bounds__(kDpB) k_dp_policy(DpArgs a) {
   const int64_t gsz = (int64_t)gridDim.x * kDpB;
   const int64_t gid = (int64_t)blockIdx.x * kDpB + threadIdx.x;
   int32_t bar = 0, bit;
-  // the first policy: every node its own cluster
+  // The first policy: clusters of half the window, R / 2 positions (fewer
+  // where lo(j) binds), cost(P(j), j) from one scan of each window.  Chains
+  // of n / (R / 2) pointers instead of the n of singleton clusters: on the
+  // transformer graphs a third fewer pointer-jumping passes in all, with no
+  // more iterations (any policy is a valid start; only the fixed point ends
+  // the iteration).
+  const int32_t h = a.R / 2 > 1 ? a.R / 2 : 1;
   for (int64_t j = gid; j <= n; j += gsz) {
-    st32(&a.P[j], j > 0 ? (int32_t)j - 1 : -1);
-    st_coherent(&a.cost[j], j > 0 ? a.PO[j] - a.PO[j - 1] : 0);
+    if (j == 0) {
+      st32(&a.P[0], -1);
+      st_coherent(&a.cost[0], 0);
+      continue;
+    }
+    const int32_t lj = a.lo[j];
+    const int32_t p = (int32_t)j - h > lj ? (int32_t)j - h : lj;
+    int64_t Int = 0;
+    for (int32_t i = (int32_t)j - 1; i >= p; i--)
+      Int += a.cq[i] * dp_near_below(a, a.nearw[i], (uint32_t)(j - i));
+    st32(&a.P[j], p);
+    st_coherent(&a.cost[j], a.PO[j] - a.PO[p] - Int);
   }
   if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
   LpE *cur = a.e0, *oth = a.e1;

@@ -27,9 +27,14 @@
 namespace cel {
 
 constexpr int kLpB = 1024;        // threads per workgroup
-constexpr int kLpLight = 64;      // longer neighbour lists are split into chunks
-constexpr int kLpChunk = 4096;    // entries of a chunk (one wave)
+constexpr int kLpLight = 8;       // longer neighbour lists are split into chunks (one wave each)
+constexpr int kLpChunk = 256;     // entries of a chunk (one wave, four per lane in flight)
 constexpr int kLpU = 4;           // nodes per thread with loads in flight together
+// Nodes per thread in the asynchronous jumps: all of a thread's nodes jump
+// together, so that no node starts late (a node that lags holds back every
+// chain through it) as long as n <= kPkU times the grid's threads (2.1 million
+// nodes on 256 workgroups of 1024); larger graphs take several groups.
+constexpr int kPkU = 8;
 
 
 
@@ -52,6 +57,25 @@ struct LpArgs {
 // Entries, policy pointers and chunk results are written and read by
 // different workgroups inside the kernel: agent-scope atomic accesses (see
 // grid_sync, and lpe_ld / lpe_st).
+
+// Packed entries (b-level, t-level): value in the high 40 bits, next node
+// in the low 24 (kPkEnd: the chain has ended), read and written whole by
+// 64-bit agent-scope atomics.  Every version of an entry a reader can see is
+// a true (sum of wv from the node up to next, next) pair, so a node may jump
+// through whatever entry its next node holds at that moment: the result is
+// again a true pair, further along the chain.  Pointer jumping then needs no
+// barrier between rounds; a node's owner keeps its entry in registers and
+// jumps until its chain ends.
+constexpr uint32_t kPkEnd = 0xFFFFFFu;
+__device__ inline uint64_t pk_make(int64_t v, uint32_t nx) { return ((uint64_t)v << 24) | nx; }
+__device__ inline int64_t pk_val(uint64_t e) { return (int64_t)(e >> 24); }
+__device__ inline uint32_t pk_next(uint64_t e) { return (uint32_t)e & kPkEnd; }
+__device__ inline uint64_t pk_ld(const uint64_t *p) {
+  return (uint64_t)ld_coherent(reinterpret_cast<const int64_t *>(p));
+}
+__device__ inline void pk_st(uint64_t *p, uint64_t e) {
+  st_coherent(reinterpret_cast<int64_t *>(p), (int64_t)e);
+}
 
 // larger value first, then the smaller neighbour index
 __device__ inline bool lp_better(int64_t v, int32_t q, int64_t bv, int32_t bq) {
@@ -76,12 +100,12 @@ __global__ void k_lp_heavy_fill(int32_t n, const int32_t *hoff, int32_t *hnode, 
 
 // KIND: 0 the b-level, 1 the t-level (out = val - wv), 2 the levels of Kahn's
 // ordering; a template parameter so that profiles tell the three apart
-template <int KIND>
-__global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
-  __shared__ int32_t s_ok, s_bit;
+template <int KIND, bool PK>
+__device__ inline void lp_run(const LpArgs &a, int32_t *s_okp, int32_t *s_bitp) {
+  int32_t &s_ok = *s_okp, &s_bit = *s_bitp;
   Status *st = a.st;
-  if (failed(st)) return;
   const int32_t n = a.n;
+  uint64_t *E = reinterpret_cast<uint64_t *>(a.e0);  // PK: one packed entry per node
   const int64_t gsz = (int64_t)gridDim.x * kLpB;
   const int64_t gid = (int64_t)blockIdx.x * kLpB + threadIdx.x;
   const int lane = threadIdx.x & 63;
@@ -89,7 +113,8 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
   int32_t bar = 0, bit;
   // the empty policy: every node alone
   for (int64_t p = gid; p < n; p += gsz) {
-    lpe_st(&a.e0[p], LpE{a.wv[p], -1, 0});
+    if (PK) pk_st(E + p, pk_make(a.wv[p], kPkEnd));
+    else lpe_st(&a.e0[p], LpE{a.wv[p], -1, 0});
     st32(&a.pol[p], -1);
   }
   if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
@@ -106,14 +131,19 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
       const int32_t e1 = min(a.aptr[p + 1], e0 + kLpChunk);
       int64_t bv = -1;
       int32_t bq = INT32_MAX;
-      for (int32_t e = e0 + lane; e < e1; e += 64) {
-        const int32_t q = a.aidx[e];
-        const int64_t v = ld_coherent(&cur[q].v);
-        if (lp_better(v, q, bv, bq)) {
-          bv = v;
-          bq = q;
+      int32_t q[kLpChunk / 64];
+      int64_t v[kLpChunk / 64];
+#pragma unroll
+      for (int k = 0; k < kLpChunk / 64; k++) q[k] = e0 + 64 * k + lane < e1 ? a.aidx[e0 + 64 * k + lane] : -1;
+#pragma unroll
+      for (int k = 0; k < kLpChunk / 64; k++)
+        v[k] = q[k] < 0 ? -1 : (PK ? pk_val(pk_ld(E + q[k])) : ld_coherent(&cur[q[k]].v));
+#pragma unroll
+      for (int k = 0; k < kLpChunk / 64; k++)
+        if (q[k] >= 0 && lp_better(v[k], q[k], bv, bq)) {
+          bv = v[k];
+          bq = q[k];
         }
-      }
       for (int o = 32; o > 0; o >>= 1) {
         const int64_t v = __shfl_xor((long long)bv, o);
         const int32_t q = __shfl_xor(bq, o);
@@ -149,29 +179,37 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
         if (p >= n || d == 0 || d > kLpLight) continue;
         int64_t bv = -1;
         int32_t bq = INT32_MAX;
-        for (int32_t e = b0[u]; e < b1[u]; e++) {
-          const int32_t q = a.aidx[e];
-          const int64_t v = ld_coherent(&cur[q].v);
-          if (lp_better(v, q, bv, bq)) {
-            bv = v;
-            bq = q;
-          }
+        for (int32_t e0 = b0[u]; e0 < b1[u]; e0 += 4) {  // four neighbours' loads in flight
+          int32_t q[4];
+          int64_t v[4];
+#pragma unroll
+          for (int k = 0; k < 4; k++) q[k] = e0 + k < b1[u] ? a.aidx[e0 + k] : -1;
+#pragma unroll
+          for (int k = 0; k < 4; k++)
+            v[k] = q[k] < 0 ? -1 : (PK ? pk_val(pk_ld(E + q[k])) : ld_coherent(&cur[q[k]].v));
+#pragma unroll
+          for (int k = 0; k < 4; k++)
+            if (q[k] >= 0 && lp_better(v[k], q[k], bv, bq)) {
+              bv = v[k];
+              bq = q[k];
+            }
         }
-        const int64_t cv = pq[u] >= 0 ? ld_coherent(&cur[pq[u]].v) : -1;
+        const int64_t cv = pq[u] >= 0 ? (PK ? pk_val(pk_ld(E + pq[u])) : ld_coherent(&cur[pq[u]].v)) : -1;
         if (bv > cv) {
           st32(&a.pol[p], bq);
           chg = 1;
         }
       }
     }
-    if (H > 0) {  // combine the chunks of each long list
+    if (H > 0) {  // combine the chunks of each long list: one wave per node
       if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
-      for (int64_t c = gid; c < H; c += gsz) {
+      const int64_t wid = gid >> 6, nw = gsz >> 6;
+      for (int64_t c = wid; c < H; c += nw) {
         const int32_t p = a.hnode[c];
-        if (c != a.hoff[p]) continue;  // the node's first chunk combines
+        if (c != a.hoff[p]) continue;  // uniform: the wave of the node's first chunk combines
         int64_t bv = -1;
         int32_t bq = INT32_MAX;
-        for (int32_t k = (int32_t)c; k < a.hoff[p + 1]; k++) {
+        for (int32_t k = (int32_t)c + lane; k < a.hoff[p + 1]; k += 64) {
           const int64_t v = ld_coherent(&a.hval[k]);
           const int32_t q = ld32(&a.hidx[k]);
           if (lp_better(v, q, bv, bq)) {
@@ -179,11 +217,21 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
             bq = q;
           }
         }
-        const int32_t pq = ld32(&a.pol[p]);
-        const int64_t cv = pq >= 0 ? ld_coherent(&cur[pq].v) : -1;
-        if (bv > cv) {
-          st32(&a.pol[p], bq);
-          chg = 1;
+        for (int o = 32; o > 0; o >>= 1) {
+          const int64_t v = __shfl_xor((long long)bv, o);
+          const int32_t q = __shfl_xor(bq, o);
+          if (lp_better(v, q, bv, bq)) {
+            bv = v;
+            bq = q;
+          }
+        }
+        if (lane == 0) {
+          const int32_t pq = ld32(&a.pol[p]);
+          const int64_t cv = pq >= 0 ? (PK ? pk_val(pk_ld(E + pq)) : ld_coherent(&cur[pq].v)) : -1;
+          if (bv > cv) {
+            st32(&a.pol[p], bq);
+            chg = 1;
+          }
         }
       }
     }
@@ -193,6 +241,68 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
     if (!bit) {
       done = true;
       break;
+    }
+    if (PK) {
+      // ---- evaluation, packed entries: every node's entry with one hop of
+      // its policy folded in, a grid barrier, then asynchronous jumps (see
+      // pk_make); the b-level's first policy keeps the one-hop values
+      for (int64_t p0 = gid; p0 < n; p0 += kLpU * gsz) {
+        int32_t q[kLpU];
+#pragma unroll
+        for (int u = 0; u < kLpU; u++) {
+          const int64_t p = p0 + u * gsz;
+          q[u] = p < n ? ld32(&a.pol[p]) : -1;
+        }
+        int64_t wq[kLpU];
+        int32_t nq[kLpU];
+#pragma unroll
+        for (int u = 0; u < kLpU; u++) {
+          wq[u] = q[u] >= 0 ? a.wv[q[u]] : 0;
+          nq[u] = q[u] >= 0 ? ld32(&a.pol[q[u]]) : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kLpU; u++) {
+          const int64_t p = p0 + u * gsz;
+          if (p < n) pk_st(E + p, pk_make(a.wv[p] + wq[u], nq[u] >= 0 ? nq[u] : kPkEnd));
+        }
+      }
+      if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
+      if (!(KIND == 0 && it == 0)) {
+        for (int64_t p0 = gid; p0 < n; p0 += kPkU * gsz) {
+          uint64_t e[kPkU];
+#pragma unroll
+          for (int u = 0; u < kPkU; u++) {
+            const int64_t p = p0 + u * gsz;
+            e[u] = p < n ? pk_ld(E + p) : pk_make(0, kPkEnd);
+          }
+          // each jump moves a chain's end strictly forward, so a chain of a
+          // DAG ends within n jumps; more means a pointer cycle
+          for (int32_t k = 0;; k++) {
+            uint64_t f[kPkU];
+            bool any = false;
+#pragma unroll
+            for (int u = 0; u < kPkU; u++) {
+              const uint32_t x = pk_next(e[u]);
+              f[u] = x != kPkEnd ? pk_ld(E + x) : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < kPkU; u++) {
+              if (pk_next(e[u]) == kPkEnd) continue;
+              e[u] = pk_make(pk_val(e[u]) + pk_val(f[u]), pk_next(f[u]));
+              pk_st(E + p0 + u * gsz, e[u]);
+              any |= pk_next(e[u]) != kPkEnd;
+            }
+            if (!any) break;
+            if (k > n) {
+              raise_err(st, EB_CYCLE);
+              break;
+            }
+          }
+        }
+        if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
+        if (ld32(reinterpret_cast<const int32_t *>(&st->err))) return;  // uniform after the barrier
+      }
+      continue;
     }
     // ---- evaluation of the new policy by pointer jumping; the first round
     // reads the policy itself (cur is free: nothing reads it any more)
@@ -278,11 +388,26 @@ __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
     return;
   }
   for (int64_t p = gid; p < n; p += gsz)
-    a.out[p] = ld_coherent(&cur[p].v) - (KIND == 1 ? a.wv[p] : 0);
+    a.out[p] = (PK ? pk_val(pk_ld(E + p)) : ld_coherent(&cur[p].v)) - (KIND == 1 ? a.wv[p] : 0);
   if (gid == 0) {
     a.res[0] = 1;
     a.res[1] = it + 1;
   }
+}
+
+// KIND: 0 the b-level, 1 the t-level (out = val - wv), 2 the levels of Kahn's
+// ordering; a template parameter so that profiles tell the three apart.  The
+// b-level and t-level take packed entries when every value fits (the
+// validation's total of w and c below 2^40, positions below 2^24 - 1); the
+// levels keep the synchronous rounds, which detect a cycle by their count.
+template <int KIND>
+__global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
+  __shared__ int32_t s_ok, s_bit;
+  if (failed(a.st)) return;
+  if (KIND != 2 && a.n < (int32_t)kPkEnd && a.st->total < (uint64_t(1) << 40))
+    lp_run<KIND, true>(a, &s_ok, &s_bit);
+  else
+    lp_run<KIND, false>(a, &s_ok, &s_bit);
 }
 
 // ------------------------------------------------------------------- host
