@@ -590,6 +590,31 @@ __device__ inline void lpe_st(LpE *p, const LpE &x) {
               (int64_t)(((uint64_t)(uint32_t)x.both << 32) | (uint32_t)x.nxt));
 }
 
+// Packed entries (policy iteration): value in the high 40 bits, next node
+// in the low 24 (kPkEnd: the chain has ended), read and written whole by
+// 64-bit agent-scope atomics.  Every version of an entry a reader can see is
+// a true (sum of wv from the node up to next, next) pair, so a node may jump
+// through whatever entry its next node holds at that moment: the result is
+// again a true pair, further along the chain.  Pointer jumping then needs no
+// barrier between rounds; a node's owner keeps its entry in registers and
+// jumps until its chain ends.
+constexpr uint32_t kPkEnd = 0xFFFFFFu;
+__device__ inline uint64_t pk_make(int64_t v, uint32_t nx) { return ((uint64_t)v << 24) | nx; }
+__device__ inline int64_t pk_val(uint64_t e) { return (int64_t)(e >> 24); }
+__device__ inline uint32_t pk_next(uint64_t e) { return (uint32_t)e & kPkEnd; }
+__device__ inline uint64_t pk_ld(const uint64_t *p) {
+  return (uint64_t)ld_coherent(reinterpret_cast<const int64_t *>(p));
+}
+__device__ inline void pk_st(uint64_t *p, uint64_t e) {
+  st_coherent(reinterpret_cast<int64_t *>(p), (int64_t)e);
+}
+
+// Nodes per thread in the asynchronous jumps: all of a thread's nodes jump
+// together, so that no node starts late (a node that lags holds back every
+// chain through it) as long as n <= kPkU times the grid's threads (2.1 million
+// nodes on 256 workgroups of 1024); larger graphs take several groups.
+constexpr int kPkU = 8;
+
 // Grid barrier with agent-scope fences around the arrival and the release:
 // plain stores before it are visible to plain loads after it, in every
 // workgroup (thread 0's release writes back, and its acquire invalidates, the

@@ -120,11 +120,12 @@ __device__ inline int32_t dp_near_below(const DpArgs &a, uint64_t w, uint32_t d)
   return k;
 }
 
-__global__ void __launch_bounds__(kDpB) k_dp_policy(DpArgs a) {
-  __shared__ int32_t s_ok, s_bit;
+template <bool PK>
+__device__ inline void dp_run(const DpArgs &a, int32_t *s_okp, int32_t *s_bitp) {
+  int32_t &s_ok = *s_okp, &s_bit = *s_bitp;
   Status *st = a.st;
-  if (failed(st)) return;
   const int32_t n = a.n;
+  uint64_t *E = reinterpret_cast<uint64_t *>(a.e0);  // PK: one packed entry per position
   const int64_t gsz = (int64_t)gridDim.x * kDpB;
   const int64_t gid = (int64_t)blockIdx.x * kDpB + threadIdx.x;
   int32_t bar = 0, bit;
@@ -154,73 +155,132 @@ __global__ void __launch_bounds__(kDpB) k_dp_policy(DpArgs a) {
   int32_t it = 0;
   bool done = false;
   for (; it < a.cap; it++) {
-    // ---- evaluation: S(j) = sum of cost along the back pointers (P(j) = 0 ends a chain)
-    int32_t more = 0;
-    for (int64_t j0 = gid; j0 <= n; j0 += kDpU * gsz) {
-      int32_t q[kDpU];
-#pragma unroll
-      for (int u = 0; u < kDpU; u++) {
-        const int64_t j = j0 + u * gsz;
-        q[u] = j <= n ? ld32(&a.P[j]) : -1;
-      }
-      int64_t cq_[kDpU];
-      int32_t nq[kDpU];
-#pragma unroll
-      for (int u = 0; u < kDpU; u++) {
-        cq_[u] = q[u] > 0 ? ld_coherent(&a.cost[q[u]]) : 0;
-        nq[u] = q[u] > 0 ? ld32(&a.P[q[u]]) : -1;
-      }
-#pragma unroll
-      for (int u = 0; u < kDpU; u++) {
-        const int64_t j = j0 + u * gsz;
-        if (j > n) continue;
-        const int32_t nx = nq[u] > 0 ? nq[u] : -1;
-        more |= nx >= 0;
-        lpe_st(&cur[j], LpE{ld_coherent(&a.cost[j]) + cq_[u], nx, 0});
-      }
-    }
-    more = __syncthreads_or(more);
-    if (!grid_sync(a.bar, ++bar, more, &s_ok, &s_bit, st, &bit)) return;
-    int32_t r = 1;
-    while (bit) {
-      if (r == a.max_rounds) {  // a pointer cycle: cannot happen (P(j) < j)
-        raise_err(st, EB_ORDER);
-        return;  // uniform: bit and r are the same in every workgroup
-      }
-      more = 0;
+    if (PK) {
+      // ---- evaluation, packed entries (see pk_make): one hop folded in,
+      // a grid barrier, then asynchronous jumps; position 0 ends a chain
       for (int64_t j0 = gid; j0 <= n; j0 += kDpU * gsz) {
-        LpE x[kDpU];
+        int32_t q[kDpU];
 #pragma unroll
         for (int u = 0; u < kDpU; u++) {
           const int64_t j = j0 + u * gsz;
-          x[u] = j <= n ? lpe_ld(&cur[j]) : LpE{0, -1, 1};
+          q[u] = j <= n ? ld32(&a.P[j]) : -1;
         }
-        LpE y[kDpU];
+        int64_t cq_[kDpU];
+        int32_t nq[kDpU];
 #pragma unroll
-        for (int u = 0; u < kDpU; u++) y[u] = x[u].nxt >= 0 ? lpe_ld(&cur[x[u].nxt]) : LpE{0, -1, 0};
+        for (int u = 0; u < kDpU; u++) {
+          cq_[u] = q[u] > 0 ? ld_coherent(&a.cost[q[u]]) : 0;
+          nq[u] = q[u] > 0 ? ld32(&a.P[q[u]]) : -1;
+        }
 #pragma unroll
         for (int u = 0; u < kDpU; u++) {
           const int64_t j = j0 + u * gsz;
-          if (j > n || x[u].both) continue;
-          if (x[u].nxt < 0) {
-            lpe_st(&oth[j], LpE{x[u].v, -1, 1});
-            st32(&cur[j].both, 1);
-          } else {
-            const LpE z{x[u].v + y[u].v, y[u].nxt, 0};
-            more |= z.nxt >= 0;
-            lpe_st(&oth[j], z);
+          if (j <= n)
+            pk_st(E + j, pk_make(ld_coherent(&a.cost[j]) + cq_[u], nq[u] > 0 ? (uint32_t)nq[u] : kPkEnd));
+        }
+      }
+      if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
+      for (int64_t j0 = gid; j0 <= n; j0 += kPkU * gsz) {
+        uint64_t e[kPkU];
+#pragma unroll
+        for (int u = 0; u < kPkU; u++) {
+          const int64_t j = j0 + u * gsz;
+          e[u] = j <= n ? pk_ld(E + j) : pk_make(0, kPkEnd);
+        }
+        for (int32_t k = 0;; k++) {  // back pointers decrease: every chain ends
+          uint64_t f[kPkU];
+          bool any = false;
+#pragma unroll
+          for (int u = 0; u < kPkU; u++) {
+            const uint32_t x = pk_next(e[u]);
+            f[u] = x != kPkEnd ? pk_ld(E + x) : 0;
           }
+#pragma unroll
+          for (int u = 0; u < kPkU; u++) {
+            if (pk_next(e[u]) == kPkEnd) continue;
+            e[u] = pk_make(pk_val(e[u]) + pk_val(f[u]), pk_next(f[u]));
+            pk_st(E + j0 + u * gsz, e[u]);
+            any |= pk_next(e[u]) != kPkEnd;
+          }
+          if (!any) break;
+          if (k > n) {  // cannot happen (P(j) < j); bounded all the same
+            raise_err(st, EB_ORDER);
+            break;
+          }
+        }
+      }
+      if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
+      if (ld32(reinterpret_cast<const int32_t *>(&st->err))) return;  // uniform after the barrier
+    } else {
+  // ---- evaluation: S(j) = sum of cost along the back pointers (P(j) = 0 ends a chain)
+      int32_t more = 0;
+      for (int64_t j0 = gid; j0 <= n; j0 += kDpU * gsz) {
+        int32_t q[kDpU];
+#pragma unroll
+        for (int u = 0; u < kDpU; u++) {
+          const int64_t j = j0 + u * gsz;
+          q[u] = j <= n ? ld32(&a.P[j]) : -1;
+        }
+        int64_t cq_[kDpU];
+        int32_t nq[kDpU];
+#pragma unroll
+        for (int u = 0; u < kDpU; u++) {
+          cq_[u] = q[u] > 0 ? ld_coherent(&a.cost[q[u]]) : 0;
+          nq[u] = q[u] > 0 ? ld32(&a.P[q[u]]) : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kDpU; u++) {
+          const int64_t j = j0 + u * gsz;
+          if (j > n) continue;
+          const int32_t nx = nq[u] > 0 ? nq[u] : -1;
+          more |= nx >= 0;
+          lpe_st(&cur[j], LpE{ld_coherent(&a.cost[j]) + cq_[u], nx, 0});
         }
       }
       more = __syncthreads_or(more);
       if (!grid_sync(a.bar, ++bar, more, &s_ok, &s_bit, st, &bit)) return;
-      LpE *t = cur;
-      cur = oth;
-      oth = t;
-      r++;
+      int32_t r = 1;
+      while (bit) {
+        if (r == a.max_rounds) {  // a pointer cycle: cannot happen (P(j) < j)
+          raise_err(st, EB_ORDER);
+          return;  // uniform: bit and r are the same in every workgroup
+        }
+        more = 0;
+        for (int64_t j0 = gid; j0 <= n; j0 += kDpU * gsz) {
+          LpE x[kDpU];
+#pragma unroll
+          for (int u = 0; u < kDpU; u++) {
+            const int64_t j = j0 + u * gsz;
+            x[u] = j <= n ? lpe_ld(&cur[j]) : LpE{0, -1, 1};
+          }
+          LpE y[kDpU];
+#pragma unroll
+          for (int u = 0; u < kDpU; u++) y[u] = x[u].nxt >= 0 ? lpe_ld(&cur[x[u].nxt]) : LpE{0, -1, 0};
+#pragma unroll
+          for (int u = 0; u < kDpU; u++) {
+            const int64_t j = j0 + u * gsz;
+            if (j > n || x[u].both) continue;
+            if (x[u].nxt < 0) {
+              lpe_st(&oth[j], LpE{x[u].v, -1, 1});
+              st32(&cur[j].both, 1);
+            } else {
+              const LpE z{x[u].v + y[u].v, y[u].nxt, 0};
+              more |= z.nxt >= 0;
+              lpe_st(&oth[j], z);
+            }
+          }
+        }
+        more = __syncthreads_or(more);
+        if (!grid_sync(a.bar, ++bar, more, &s_ok, &s_bit, st, &bit)) return;
+        LpE *t = cur;
+        cur = oth;
+        oth = t;
+        r++;
+      }
     }
     // S - PO for the candidates (plain stores, published by a fenced barrier)
-    for (int64_t j = gid; j <= n; j += gsz) a.SP[j] = ld_coherent(&cur[j].v) - a.PO[j];
+    for (int64_t j = gid; j <= n; j += gsz)
+      a.SP[j] = (PK ? pk_val(pk_ld(E + j)) : ld_coherent(&cur[j].v)) - a.PO[j];
     if (!grid_sync_fenced(a.bar, ++bar, &s_ok, &s_bit, st)) return;
     // ---- improvement: the best candidate of every target
     int32_t chg = 0;
@@ -289,6 +349,18 @@ __global__ void __launch_bounds__(kDpB) k_dp_policy(DpArgs a) {
     st->i2 = 1;
     st->i3 = it + 1;
   }
+}
+
+// Packed entries when every value fits: S is at most PO[n], the comm of all
+// edges (every node a cluster of its own), below 2^40, and positions below
+// 2^24 - 1.
+__global__ void __launch_bounds__(kDpB) k_dp_policy(DpArgs a) {
+  __shared__ int32_t s_ok, s_bit;
+  if (failed(a.st)) return;
+  if (a.n < (int32_t)kPkEnd - 1 && a.PO[a.n] < (int64_t(1) << 40))
+    dp_run<true>(a, &s_ok, &s_bit);
+  else
+    dp_run<false>(a, &s_ok, &s_bit);
 }
 
 // ------------------------------------------------------------------- host

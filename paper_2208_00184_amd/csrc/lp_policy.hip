@@ -30,11 +30,6 @@ constexpr int kLpB = 1024;        // threads per workgroup
 constexpr int kLpLight = 8;       // longer neighbour lists are split into chunks (one wave each)
 constexpr int kLpChunk = 256;     // entries of a chunk (one wave, four per lane in flight)
 constexpr int kLpU = 4;           // nodes per thread with loads in flight together
-// Nodes per thread in the asynchronous jumps: all of a thread's nodes jump
-// together, so that no node starts late (a node that lags holds back every
-// chain through it) as long as n <= kPkU times the grid's threads (2.1 million
-// nodes on 256 workgroups of 1024); larger graphs take several groups.
-constexpr int kPkU = 8;
 
 
 
@@ -57,25 +52,6 @@ struct LpArgs {
 // Entries, policy pointers and chunk results are written and read by
 // different workgroups inside the kernel: agent-scope atomic accesses (see
 // grid_sync, and lpe_ld / lpe_st).
-
-// Packed entries (b-level, t-level): value in the high 40 bits, next node
-// in the low 24 (kPkEnd: the chain has ended), read and written whole by
-// 64-bit agent-scope atomics.  Every version of an entry a reader can see is
-// a true (sum of wv from the node up to next, next) pair, so a node may jump
-// through whatever entry its next node holds at that moment: the result is
-// again a true pair, further along the chain.  Pointer jumping then needs no
-// barrier between rounds; a node's owner keeps its entry in registers and
-// jumps until its chain ends.
-constexpr uint32_t kPkEnd = 0xFFFFFFu;
-__device__ inline uint64_t pk_make(int64_t v, uint32_t nx) { return ((uint64_t)v << 24) | nx; }
-__device__ inline int64_t pk_val(uint64_t e) { return (int64_t)(e >> 24); }
-__device__ inline uint32_t pk_next(uint64_t e) { return (uint32_t)e & kPkEnd; }
-__device__ inline uint64_t pk_ld(const uint64_t *p) {
-  return (uint64_t)ld_coherent(reinterpret_cast<const int64_t *>(p));
-}
-__device__ inline void pk_st(uint64_t *p, uint64_t e) {
-  st_coherent(reinterpret_cast<int64_t *>(p), (int64_t)e);
-}
 
 // larger value first, then the smaller neighbour index
 __device__ inline bool lp_better(int64_t v, int32_t q, int64_t bv, int32_t bq) {
@@ -396,15 +372,17 @@ __device__ inline void lp_run(const LpArgs &a, int32_t *s_okp, int32_t *s_bitp) 
 }
 
 // KIND: 0 the b-level, 1 the t-level (out = val - wv), 2 the levels of Kahn's
-// ordering; a template parameter so that profiles tell the three apart.  The
-// b-level and t-level take packed entries when every value fits (the
-// validation's total of w and c below 2^40, positions below 2^24 - 1); the
-// levels keep the synchronous rounds, which detect a cycle by their count.
+// ordering; a template parameter so that profiles tell the three apart.
+// Packed entries when every value fits: positions below 2^24 - 1, and for
+// the b-level and t-level the validation's total of w and c below 2^40 (the
+// levels are at most n).  A pointer cycle (the levels of a graph that is not
+// a DAG) keeps some chain from ending: its node gives up after n jumps with
+// EB_CYCLE.
 template <int KIND>
 __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
   __shared__ int32_t s_ok, s_bit;
   if (failed(a.st)) return;
-  if (KIND != 2 && a.n < (int32_t)kPkEnd && a.st->total < (uint64_t(1) << 40))
+  if (a.n < (int32_t)kPkEnd && (KIND == 2 || a.st->total < (uint64_t(1) << 40)))
     lp_run<KIND, true>(a, &s_ok, &s_bit);
   else
     lp_run<KIND, false>(a, &s_ok, &s_bit);
