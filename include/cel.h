@@ -375,8 +375,10 @@ int cel_cluster_info(int32_t *info);
 /* Diagnostics: cel_policy_iteration(0) makes the calling thread's
  * cel_topo_levels, cel_blevel and cel_cluster calls take Kahn's kernel, the
  * level sweeps and the blocked DP directly; 1 (the default) tries policy
- * iteration first.  Both give the same results.  Returns the previous mode
- * (CEL_E_ARG for a negative mode). */
+ * iteration first, with packed 64-bit entries and asynchronous pointer
+ * jumping where the values fit; 2 tries policy iteration first with 16-byte
+ * entries and synchronous rounds everywhere.  Every mode gives the same
+ * results.  Returns the previous mode (CEL_E_ARG for a negative mode). */
 int cel_policy_iteration(int mode);
 
 /* Diagnostics: which K = 1 path the calling thread's cel_makespan and

@@ -172,7 +172,9 @@ def cluster_info() -> tuple:
 def policy_iteration(mode: int) -> int:
     """Levels, b-level, t-level and clustering-DP path of the calling thread:
     0 = Kahn's kernel, the level sweeps and the blocked DP, 1 = policy
-    iteration first (default); returns the previous mode."""
+    iteration first (default; packed entries and asynchronous pointer jumping
+    where the values fit), 2 = policy iteration first with 16-byte entries and
+    synchronous rounds; returns the previous mode."""
     r = lib().cel_policy_iteration(int(mode))
     if r < 0:
         _check(r)

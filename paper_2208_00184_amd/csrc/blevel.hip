@@ -88,6 +88,7 @@ static thread_local int t_lp_mode = 1;
 
 namespace cel {
 bool policy_iteration_on() { return t_lp_mode > 0; }
+bool policy_iteration_packed() { return t_lp_mode == 1; }
 }  // namespace cel
 
 extern "C" int cel_blevel_info(int32_t *info) {

@@ -699,6 +699,7 @@ int lp_policy(int32_t n, int32_t m, int32_t L, int32_t cap, const int32_t *aptr,
 // whether the calling thread's cel_topo_levels and cel_blevel calls try
 // policy iteration first (cel_policy_iteration)
 bool policy_iteration_on();
+bool policy_iteration_packed();  // packed entries allowed (mode 1), else 16-byte rounds
 // dp_policy.hip: the clustering DP's back pointers P[1..n] (smallest
 // minimising i) and st->s0 = S(n) by policy iteration, given lo, PO, the comm
 // by position and the successors in positions (sptr / sidx).  st->i2 = 1 once

@@ -97,6 +97,7 @@ __global__ void k_dpn_pack(int32_t n, int32_t R, const int32_t *nptr, const uint
 
 struct DpArgs {
   int32_t n, R, cap, max_rounds;
+  int32_t packed;             // packed entries allowed where the values fit
   const int32_t *lo;          // [n + 1] first feasible i of a cluster ending at j
   const int64_t *PO;          // [n + 1]
   const int64_t *cq;          // [n] comm by position
@@ -357,7 +358,7 @@ __device__ inline void dp_run(const DpArgs &a, int32_t *s_okp, int32_t *s_bitp) 
 __global__ void __launch_bounds__(kDpB) k_dp_policy(DpArgs a) {
   __shared__ int32_t s_ok, s_bit;
   if (failed(a.st)) return;
-  if (a.n < (int32_t)kPkEnd - 1 && a.PO[a.n] < (int64_t(1) << 40))
+  if (a.packed && a.n < (int32_t)kPkEnd - 1 && a.PO[a.n] < (int64_t(1) << 40))
     dp_run<true>(a, &s_ok, &s_bit);
   else
     dp_run<false>(a, &s_ok, &s_bit);
@@ -441,6 +442,7 @@ int dp_policy(int32_t n, int32_t m, int32_t R, const int32_t *lo, const int64_t 
   a.R = R;
   a.cap = cap;
   a.max_rounds = max_rounds;
+  a.packed = policy_iteration_packed() ? 1 : 0;
   a.lo = lo;
   a.PO = PO;
   a.cq = cq;

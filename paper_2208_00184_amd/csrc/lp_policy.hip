@@ -35,6 +35,7 @@ constexpr int kLpU = 4;           // nodes per thread with loads in flight toget
 
 struct LpArgs {
   int32_t n, cap, max_rounds;
+  int32_t packed;                 // packed entries allowed where the values fit
   const int32_t *aptr, *aidx;     // adjacency (positions)
   const int64_t *wv;              // [n]
   const int32_t *hoff;            // [n + 1] first chunk of each node (chunks only for long lists)
@@ -382,7 +383,7 @@ template <int KIND>
 __global__ void __launch_bounds__(kLpB) k_lp_policy(LpArgs a) {
   __shared__ int32_t s_ok, s_bit;
   if (failed(a.st)) return;
-  if (a.n < (int32_t)kPkEnd && (KIND == 2 || a.st->total < (uint64_t(1) << 40)))
+  if (a.packed && a.n < (int32_t)kPkEnd && (KIND == 2 || a.st->total < (uint64_t(1) << 40)))
     lp_run<KIND, true>(a, &s_ok, &s_bit);
   else
     lp_run<KIND, false>(a, &s_ok, &s_bit);
@@ -457,6 +458,7 @@ int lp_policy(int32_t n, int32_t m, int32_t L, int32_t cap, const int32_t *aptr,
   a.n = n;
   a.cap = cap;
   a.max_rounds = max_rounds;
+  a.packed = policy_iteration_packed() ? 1 : 0;
   a.aptr = aptr;
   a.aidx = aidx;
   a.wv = wv;

@@ -69,10 +69,12 @@ def assert_topo_blevel(wl, ref_t, ref_b, got_t, got_b):
 # ------------------------------------------------------------ configs 1-3, 5
 
 
-@pytest.fixture(params=[1, 0], ids=["policy", "sweep"])
+@pytest.fixture(params=[1, 2, 0], ids=["policy", "policy-rounds", "sweep"])
 def bl_path(request):
-    """b-level and t-level by policy iteration (falling back to the level
-    sweeps when it does not converge) or by the level sweeps."""
+    """b-level and t-level by policy iteration (packed entries and
+    asynchronous jumps, or 16-byte entries and synchronous rounds; falling
+    back to the level sweeps when it does not converge) or by the level
+    sweeps."""
     was = cel.policy_iteration(request.param)
     yield request.param
     cel.policy_iteration(was)

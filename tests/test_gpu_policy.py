@@ -1,6 +1,7 @@
-"""GPU parity of the b-level (eq. 3) and t-level (eq. 2) by policy iteration
-(cel_blevel), against the CPU oracle, tolerance 0, with the path each call
-took (cel_blevel_info)."""
+"""GPU parity of the longest paths (levels, b-level eq. 3, t-level eq. 2) and
+of the clustering DP (eq. 4-6) by policy iteration, against the CPU oracle,
+tolerance 0, with the path each call took (cel_blevel_info, cel_topo_levels_info,
+cel_cluster_info); every test in both evaluation modes."""
 from __future__ import annotations
 
 import numpy as np
@@ -18,6 +19,15 @@ from oracle import oracle as O  # noqa: E402
 from workloads import from_edges, make_config  # noqa: E402
 
 DEV = "cuda:0"
+
+
+@pytest.fixture(autouse=True, params=[1, 2], ids=["packed", "rounds"])
+def pi_mode(request):
+    """Every test twice: packed entries with asynchronous pointer jumping
+    (where the values fit), and 16-byte entries with synchronous rounds."""
+    was = cel.policy_iteration(request.param)
+    yield request.param
+    cel.policy_iteration(was)
 
 
 def np_(t):
@@ -191,3 +201,23 @@ def test_cluster_dp_policy_random_orders():
             ref = O.cluster(wl, order, R, -1)
             cid, C, cut, (path, iters) = gpu_cluster(wl, order, R, -1)
             assert C == ref[1] and cut == ref[2] and np.array_equal(cid, ref[0]), (s, R)
+
+
+def test_policy_values_beyond_packed_entries():
+    """Transformer-24 with w and output sizes scaled by 2^22: the total of w
+    and c (and the DP's largest S) exceeds the 40 bits of a packed entry, so
+    even the packed mode takes the 16-byte rounds; exact all the same."""
+    import dataclasses
+    wl = make_config(2, 0)
+    wl = dataclasses.replace(wl, w=wl.w << 22, ob=wl.ob << 22)
+    src = np.repeat(np.arange(wl.n), np.diff(wl.out_ptr))
+    c = wl.ob // wl.bw + (wl.ob % wl.bw != 0) + wl.lat
+    assert int(wl.w.sum()) + int(c[src].sum()) >= 2 ** 40
+    L, info = run(wl)
+    for path, iters in info:
+        assert path == 0 and iters >= 1
+    lev, oid, lp, L = O.topo_levels(wl)
+    _, _, pr, _ = O.blevel(wl, lev, oid)
+    ref = O.cluster(wl, pr, 200, -1)
+    cid, C, cut, (path, iters) = gpu_cluster(wl, pr, 200, -1)
+    assert C == ref[1] and cut == ref[2] and np.array_equal(cid, ref[0])
