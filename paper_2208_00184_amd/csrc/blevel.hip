@@ -159,10 +159,42 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
   }
   bool sweep_b = true, sweep_t = tlp != nullptr;
   t_bl_info = {1, 0, tlp ? 1 : 2, 0};
+  // the outputs from the policy-iteration values, queued before the status
+  // is read: one host round trip when the iteration converged (a value that
+  // did not converge is a real path's length, never above the exact one, so
+  // the maxima of the sweep's exact values replace it below)
+  auto outputs = [&](bool b, bool t, hipStream_t sb, hipStream_t stt) -> int {
+    if (t && tlp)
+      k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, stt>>>(n, order_id, tlp, tlevel, st, &st->s1);
+    if (b) {
+      k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, sb>>>(n, order_id, blp, blevel, st, &st->s0);
+      if (prio_order && n > 0) {
+        uint64_t *keys;
+        CEL_TRY(sc.get(&keys, n));
+        uint32_t *ids = reinterpret_cast<uint32_t *>(prio_order);
+        k_prio_keys<<<grid_for(n, 256, 4096), 256, 0, sb>>>(n, order_id, blp, keys, ids, st);
+        CEL_TRY(segmented_sort(keys, ids, level_ptr, L, n, sc, sb, st));
+      }
+    }
+    CEL_HIP(hipGetLastError());
+    return CEL_OK;
+  };
+  if (lb && (lt || !tlp)) {
+    CEL_TRY(outputs(true, true, s, s));
+    Status h;
+    CEL_TRY(read_status(st, &h, s));
+    if (h.err) return status_error(h, fn);
+    if (h.i0 && (!tlp || h.i2)) {
+      t_bl_info = {0, h.i1, tlp ? 0 : 2, tlp ? h.i3 : 0};
+      *cp = h.s0;
+      return CEL_OK;
+    }
+  }
   if (lb || lt) {
     Status h;
     CEL_TRY(read_status(st, &h, s));
     if (h.err) return status_error(h, fn);
+    k_fill_i64<<<1, 64, 0, s>>>(&st->s0, 2, 0);  // s0, s1: the maxima, taken again below
     if (lb) {
       sweep_b = !h.i0;
       t_bl_info.path_b = h.i0 ? 0 : 1;
@@ -188,19 +220,8 @@ extern "C" int cel_blevel(const cel_graph *g, const cel_devices *d, const int32_
     CEL_TRY(sweep_prepare(pb, true, n, g->m, L, level_ptr, order_id, level, sptr, sidx, wp, wcp,
                           blp, sc, s, st));
   if (sweep_t) CEL_TRY(sweep_run(pt, fk.side(), st, "k_tlevel_sweep"));
-  if (tlp)
-    k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, sweep_t ? fk.side() : s>>>(n, order_id, tlp,
-                                                                              tlevel, st, &st->s1);
   if (sweep_b) CEL_TRY(sweep_run(pb, s, st, "k_blevel_sweep"));
-  k_scatter_max<<<grid_for(n, 256, 2048), 256, 0, s>>>(n, order_id, blp, blevel, st, &st->s0);
-  if (prio_order && n > 0) {
-    uint64_t *keys;
-    CEL_TRY(sc.get(&keys, n));
-    uint32_t *ids = reinterpret_cast<uint32_t *>(prio_order);
-    k_prio_keys<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, order_id, blp, keys, ids, st);
-    CEL_TRY(segmented_sort(keys, ids, level_ptr, L, n, sc, s, st));
-  }
-  CEL_HIP(hipGetLastError());
+  CEL_TRY(outputs(true, true, s, sweep_t ? fk.side() : s));
   CEL_TRY(fk.join());
   Status h;
   CEL_TRY(read_status(st, &h, s));

@@ -357,18 +357,14 @@ __device__ inline void lp_run(const LpArgs &a, int32_t *s_okp, int32_t *s_bitp) 
       r++;
     }
   }
-  if (!done) {  // not converged: the caller runs the level sweep
-    if (gid == 0) {
-      a.res[0] = 0;
-      a.res[1] = it;
-    }
-    return;
-  }
+  // The values of the last policy evaluated, exact when converged; otherwise
+  // lengths of real paths (never above the exact values, so levels stay
+  // below n), which callers may use before they read res and replace.
   for (int64_t p = gid; p < n; p += gsz)
     a.out[p] = (PK ? pk_val(pk_ld(E + p)) : ld_coherent(&cur[p].v)) - (KIND == 1 ? a.wv[p] : 0);
   if (gid == 0) {
-    a.res[0] = 1;
-    a.res[1] = it + 1;
+    a.res[0] = done ? 1 : 0;  // not converged: the caller runs the level-synchronous kernel
+    a.res[1] = done ? it + 1 : it;
   }
 }
 

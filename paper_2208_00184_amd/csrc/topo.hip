@@ -535,23 +535,24 @@ extern "C" int cel_topo_levels(const cel_graph *g, int32_t *level, int32_t *orde
     CEL_TRY(lp_policy(n, g->m, n, kTopoPolicyIt, g->in_ptr, g->in_idx, wv, 2, val, &st->i2,
                       "k_levels_policy", sc, s, st, &launched));
     if (launched) {
+      // order_id: the nodes sorted by (level, id), one segment, queued before
+      // the status is read (one host round trip when the iteration
+      // converged; otherwise Kahn's kernel below rewrites every output, and
+      // these values, lengths of real paths, stay below n meanwhile)
+      uint64_t *keys;
+      int32_t *seg;
+      CEL_TRY(sc.get(&keys, n));
+      CEL_TRY(sc.get(&seg, 2));
+      uint32_t *ids = reinterpret_cast<uint32_t *>(order_id);
+      k_topo_keys<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, val, level, keys, ids, seg, st);
+      CEL_TRY(segmented_sort(keys, ids, seg, 1, n, sc, s, st));
+      k_topo_ptr<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, keys, level_ptr, st);
+      CEL_HIP(hipGetLastError());
       Status h;
       CEL_TRY(read_status(st, &h, s));
       if (h.err) return status_error(h, "cel_topo_levels");
       t_topo_info = {h.i2 ? 0 : 1, h.i3};
       if (h.i2) {
-        // order_id: the nodes sorted by (level, id), one segment
-        uint64_t *keys;
-        int32_t *seg;
-        CEL_TRY(sc.get(&keys, n));
-        CEL_TRY(sc.get(&seg, 2));
-        uint32_t *ids = reinterpret_cast<uint32_t *>(order_id);
-        k_topo_keys<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, val, level, keys, ids, seg, st);
-        CEL_TRY(segmented_sort(keys, ids, seg, 1, n, sc, s, st));
-        k_topo_ptr<<<grid_for(n, 256, 4096), 256, 0, s>>>(n, keys, level_ptr, st);
-        CEL_HIP(hipGetLastError());
-        CEL_TRY(read_status(st, &h, s));
-        if (h.err) return status_error(h, "cel_topo_levels");
         *n_levels = h.i0;
         return CEL_OK;
       }
