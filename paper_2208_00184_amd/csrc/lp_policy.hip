@@ -82,7 +82,10 @@ __device__ inline void lp_run(const LpArgs &a, int32_t *s_okp, int32_t *s_bitp) 
   int32_t &s_ok = *s_okp, &s_bit = *s_bitp;
   Status *st = a.st;
   const int32_t n = a.n;
-  uint64_t *E = reinterpret_cast<uint64_t *>(a.e0);  // PK: one packed entry per node
+  // PK: packed entries in two buffers; the improvement reads E and writes
+  // each node's entry for the next policy (wv, new pointer) into En, where
+  // the jumps then run; the buffers swap after every evaluation
+  uint64_t *E = reinterpret_cast<uint64_t *>(a.e0), *En = reinterpret_cast<uint64_t *>(a.e1);
   const int64_t gsz = (int64_t)gridDim.x * kLpB;
   const int64_t gid = (int64_t)blockIdx.x * kLpB + threadIdx.x;
   const int lane = threadIdx.x & 63;
@@ -153,6 +156,7 @@ __device__ inline void lp_run(const LpArgs &a, int32_t *s_okp, int32_t *s_bitp) 
       for (int u = 0; u < kLpU; u++) {
         const int64_t p = p0 + u * gsz;
         const int32_t d = b1[u] - b0[u];
+        if (PK && p < n && d == 0) pk_st(En + p, pk_make(a.wv[p], kPkEnd));
         if (p >= n || d == 0 || d > kLpLight) continue;
         int64_t bv = -1;
         int32_t bq = INT32_MAX;
@@ -176,6 +180,7 @@ __device__ inline void lp_run(const LpArgs &a, int32_t *s_okp, int32_t *s_bitp) 
           st32(&a.pol[p], bq);
           chg = 1;
         }
+        if (PK) pk_st(En + p, pk_make(a.wv[p], bv > cv ? (uint32_t)bq : pq[u] >= 0 ? (uint32_t)pq[u] : kPkEnd));
       }
     }
     if (H > 0) {  // combine the chunks of each long list: one wave per node
@@ -209,6 +214,7 @@ __device__ inline void lp_run(const LpArgs &a, int32_t *s_okp, int32_t *s_bitp) 
             st32(&a.pol[p], bq);
             chg = 1;
           }
+          if (PK) pk_st(En + p, pk_make(a.wv[p], bv > cv ? (uint32_t)bq : pq >= 0 ? (uint32_t)pq : kPkEnd));
         }
       }
     }
@@ -220,37 +226,38 @@ __device__ inline void lp_run(const LpArgs &a, int32_t *s_okp, int32_t *s_bitp) 
       break;
     }
     if (PK) {
-      // ---- evaluation, packed entries: every node's entry with one hop of
-      // its policy folded in, a grid barrier, then asynchronous jumps (see
-      // pk_make); the b-level's first policy keeps the one-hop values
-      for (int64_t p0 = gid; p0 < n; p0 += kLpU * gsz) {
-        int32_t q[kLpU];
+      // ---- evaluation, packed entries: the jumps start from the entries the
+      // improvement wrote (wv, pointer) into En, asynchronously (see pk_make);
+      // the b-level's first policy instead keeps one-hop values (wv(p) +
+      // wv(pol(p)), next pol(pol(p))), folded in one pass
+      if (KIND == 0 && it == 0) {
+        for (int64_t p0 = gid; p0 < n; p0 += kLpU * gsz) {
+          int32_t q[kLpU];
 #pragma unroll
-        for (int u = 0; u < kLpU; u++) {
-          const int64_t p = p0 + u * gsz;
-          q[u] = p < n ? ld32(&a.pol[p]) : -1;
-        }
-        int64_t wq[kLpU];
-        int32_t nq[kLpU];
+          for (int u = 0; u < kLpU; u++) {
+            const int64_t p = p0 + u * gsz;
+            q[u] = p < n ? ld32(&a.pol[p]) : -1;
+          }
+          int64_t wq[kLpU];
+          int32_t nq[kLpU];
 #pragma unroll
-        for (int u = 0; u < kLpU; u++) {
-          wq[u] = q[u] >= 0 ? a.wv[q[u]] : 0;
-          nq[u] = q[u] >= 0 ? ld32(&a.pol[q[u]]) : -1;
-        }
+          for (int u = 0; u < kLpU; u++) {
+            wq[u] = q[u] >= 0 ? a.wv[q[u]] : 0;
+            nq[u] = q[u] >= 0 ? ld32(&a.pol[q[u]]) : -1;
+          }
 #pragma unroll
-        for (int u = 0; u < kLpU; u++) {
-          const int64_t p = p0 + u * gsz;
-          if (p < n) pk_st(E + p, pk_make(a.wv[p] + wq[u], nq[u] >= 0 ? nq[u] : kPkEnd));
+          for (int u = 0; u < kLpU; u++) {
+            const int64_t p = p0 + u * gsz;
+            if (p < n) pk_st(En + p, pk_make(a.wv[p] + wq[u], nq[u] >= 0 ? nq[u] : kPkEnd));
+          }
         }
-      }
-      if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
-      if (!(KIND == 0 && it == 0)) {
+      } else {
         for (int64_t p0 = gid; p0 < n; p0 += kPkU * gsz) {
           uint64_t e[kPkU];
 #pragma unroll
           for (int u = 0; u < kPkU; u++) {
             const int64_t p = p0 + u * gsz;
-            e[u] = p < n ? pk_ld(E + p) : pk_make(0, kPkEnd);
+            e[u] = p < n ? pk_ld(En + p) : pk_make(0, kPkEnd);
           }
           // each jump moves a chain's end strictly forward, so a chain of a
           // DAG ends within n jumps; more means a pointer cycle
@@ -260,13 +267,13 @@ __device__ inline void lp_run(const LpArgs &a, int32_t *s_okp, int32_t *s_bitp) 
 #pragma unroll
             for (int u = 0; u < kPkU; u++) {
               const uint32_t x = pk_next(e[u]);
-              f[u] = x != kPkEnd ? pk_ld(E + x) : 0;
+              f[u] = x != kPkEnd ? pk_ld(En + x) : 0;
             }
 #pragma unroll
             for (int u = 0; u < kPkU; u++) {
               if (pk_next(e[u]) == kPkEnd) continue;
               e[u] = pk_make(pk_val(e[u]) + pk_val(f[u]), pk_next(f[u]));
-              pk_st(E + p0 + u * gsz, e[u]);
+              pk_st(En + p0 + u * gsz, e[u]);
               any |= pk_next(e[u]) != kPkEnd;
             }
             if (!any) break;
@@ -276,9 +283,12 @@ __device__ inline void lp_run(const LpArgs &a, int32_t *s_okp, int32_t *s_bitp) 
             }
           }
         }
-        if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
-        if (ld32(reinterpret_cast<const int32_t *>(&st->err))) return;  // uniform after the barrier
       }
+      if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
+      if (ld32(reinterpret_cast<const int32_t *>(&st->err))) return;  // uniform after the barrier
+      uint64_t *t = E;
+      E = En;
+      En = t;
       continue;
     }
     // ---- evaluation of the new policy by pointer jumping; the first round
