@@ -704,6 +704,10 @@ bool policy_iteration_packed();  // packed entries allowed (mode 1), else 16-byt
 // minimising i) and st->s0 = S(n) by policy iteration, given lo, PO, the comm
 // by position and the successors in positions (sptr / sidx).  st->i2 = 1 once
 // converged, st->i3 = iterations; *launched false when not launched.
+// cluster starts from the DP's back pointers by doubling tables (flag[j] = 1
+// at every start, st->i0 = their number); *launched false: nothing queued
+int chain_marks(int32_t n, const int32_t *P, int32_t *flag, Scratch &sc, hipStream_t s, Status *st,
+                bool *launched);
 int dp_policy(int32_t n, int32_t m, int32_t R, const int32_t *lo, const int64_t *PO,
               const int64_t *cq, const int32_t *sptr, const int32_t *sidx, int32_t *P,
               class Scratch &sc, hipStream_t s, Status *st, bool *launched);

@@ -1232,7 +1232,9 @@ extern "C" int cel_cluster(const cel_graph *g, const cel_devices *d, const int32
     else if (R <= 1024) launch_dp<16>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
     else if (R <= 2048) launch_dp<32>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
     else launch_dp<64>(n, R, lo, pptr, pidx, cq, PO, P, st, s);
-    k_walk<true><<<1, kWalkB, 0, s>>>(n, P, flag, st);
+    bool marked = false;
+    if (policy_iteration_on()) CEL_TRY(chain_marks(n, P, flag, sc, s, st, &marked));
+    if (!marked) k_walk<true><<<1, kWalkB, 0, s>>>(n, P, flag, st);
   } else {
     k_walk<false><<<1, kWalkB, 0, s>>>(n, gend, flag, st);
   }

@@ -364,11 +364,77 @@ __global__ void __launch_bounds__(kDpB) k_dp_policy(DpArgs a) {
     dp_run<false>(a, &s_ok, &s_bit);
 }
 
+// ------------------------------------------------------ cluster starts
+
+// The cluster starts are the chain from n through the final back pointers P
+// (each P(j) < j).  Doubling tables J_0 = P (J_0(0) = 0), J_{k+1} = J_k(J_k)
+// are built until the 2^k-th ancestor of n is position 0; then M = {n}, and
+// for l = k down to 0 every marked position marks J_l of itself: after level
+// l the marks cover every distance along the chain from n that is a sum of
+// distinct powers 2^l .. 2^k, so at the end every chain node is marked and
+// nothing else (a mark another thread sets during a pass only adds ancestors).
+// About 2 log2(C) whole-GPU passes where one thread would follow C pointers.
+struct CmArgs {
+  int32_t n, K;               // K levels allocated in J
+  const int32_t *P;           // [n + 1]
+  int32_t *J;                 // [K][n + 1]
+  int32_t *M;                 // [n + 1]
+  int32_t *flag;              // [n] 1 at the cluster starts
+  int32_t *bar;
+  Status *st;
+};
+
+__global__ void __launch_bounds__(kDpB) k_chain_marks(CmArgs a) {
+  __shared__ int32_t s_ok, s_bit, s_red[kDpB / 64];
+  Status *st = a.st;
+  if (failed(st)) return;
+  const int64_t n1 = (int64_t)a.n + 1;
+  const int64_t gsz = (int64_t)gridDim.x * kDpB;
+  const int64_t gid = (int64_t)blockIdx.x * kDpB + threadIdx.x;
+  int32_t bar = 0, bit;
+  for (int64_t j = gid; j < n1; j += gsz) {
+    const int32_t pj = j > 0 ? a.P[j] : 0;
+    if (j > 0 && (pj < 0 || pj >= j)) raise_err(st, EB_ORDER);  // not a back pointer
+    st32(&a.J[j], j > 0 && pj >= 0 && pj < j ? pj : 0);
+    st32(&a.M[j], j == a.n ? 1 : 0);
+  }
+  if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
+  int32_t k = 0;
+  while (ld32(&a.J[(int64_t)k * n1 + a.n]) != 0 && k + 1 < a.K) {  // uniform after the barrier
+    const int32_t *Jk = a.J + (int64_t)k * n1;
+    int32_t *Jn = a.J + (int64_t)(k + 1) * n1;
+    for (int64_t j = gid; j < n1; j += gsz) st32(&Jn[j], ld32(&Jk[ld32(&Jk[j])]));
+    if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
+    k++;
+  }
+  for (int32_t l = k; l >= 0; l--) {
+    const int32_t *Jl = a.J + (int64_t)l * n1;
+    for (int64_t j = gid; j < n1; j += gsz)
+      if (ld32(&a.M[j])) st32(&a.M[ld32(&Jl[j])], 1);
+    if (!grid_sync(a.bar, ++bar, 0, &s_ok, &s_bit, st, &bit)) return;
+  }
+  int32_t c = 0;
+  for (int64_t j = gid; j < a.n; j += gsz) {
+    const int32_t m = ld32(&a.M[j]);
+    a.flag[j] = m;
+    c += m;
+  }
+  for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
+  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t t = 0;
+    for (int i = 0; i < kDpB / 64; i++) t += s_red[i];
+    atomicAdd(&st->i0, t);
+  }
+}
+
 // ------------------------------------------------------------------- host
 
 namespace {
 std::mutex g_dp_mu;
 std::map<int, int> g_dp_groups;  // device -> co-resident workgroups (one per CU at most)
+std::map<int, int> g_cm_groups;  // the same for k_chain_marks
 }  // namespace
 
 int dp_policy(int32_t n, int32_t m, int32_t R, const int32_t *lo, const int64_t *PO,
@@ -461,6 +527,54 @@ int dp_policy(int32_t n, int32_t m, int32_t R, const int32_t *lo, const int64_t 
     // resident all at once on an idle GPU; the barriers' waits are bounded
     KTimer kt(s, "k_cluster_policy");
     k_dp_policy<<<G, kDpB, 0, s>>>(a);
+  }
+  CEL_HIP(hipGetLastError());
+  *launched = true;
+  return CEL_OK;
+}
+
+int chain_marks(int32_t n, const int32_t *P, int32_t *flag, Scratch &sc, hipStream_t s, Status *st,
+                bool *launched) {
+  *launched = false;
+  if (n <= 0) return CEL_OK;
+  int gmax = 0;
+  {
+    int dev = 0;
+    CEL_HIP(hipGetDevice(&dev));
+    std::lock_guard<std::mutex> lk(g_dp_mu);
+    auto it = g_cm_groups.find(dev);
+    if (it == g_cm_groups.end()) {
+      int cus = 0, nb = 0;
+      CEL_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+      CEL_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)k_chain_marks, kDpB,
+                                                           0));
+      it = g_cm_groups.emplace(dev, cus * (nb < 1 ? nb : 1)).first;
+    }
+    gmax = it->second;
+  }
+  if (gmax < 1) return CEL_OK;
+  const int64_t need = ((int64_t)n + 1 + kDpB - 1) / kDpB;
+  const int G = (int)(need < gmax ? need : gmax);
+  int32_t K = 2;  // 2^(K - 1) > n: enough levels for a chain through every position
+  while ((int64_t(1) << (K - 1)) <= (int64_t)n) K++;
+  int32_t *J, *M, *bar;
+  CEL_TRY(sc.get(&J, (int64_t)K * ((int64_t)n + 1)));
+  CEL_TRY(sc.get(&M, (int64_t)n + 1));
+  CEL_TRY(sc.get(&bar, 2 + (int64_t)G));
+  k_fill_i32<<<1, 256, 0, s>>>(bar, 2 + (int64_t)G, 0);
+  CmArgs a{};
+  a.n = n;
+  a.K = K;
+  a.P = P;
+  a.J = J;
+  a.M = M;
+  a.flag = flag;
+  a.bar = bar;
+  a.st = st;
+  {
+    // at most one workgroup per CU (bounded grid-barrier waits, as k_dp_policy)
+    KTimer kt(s, "k_chain_marks");
+    k_chain_marks<<<G, kDpB, 0, s>>>(a);
   }
   CEL_HIP(hipGetLastError());
   *launched = true;
