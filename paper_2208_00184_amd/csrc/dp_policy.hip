@@ -113,12 +113,14 @@ struct DpArgs {
 };
 
 // successors of a position at offsets below d (1 <= d <= R)
+// (SWAR over the four 16-bit fields: a field b, an offset below 2^12 or the
+// unused 0x3FFF, has bits 14-15 clear, so (0x8000 | d) - (b + 1) neither
+// borrows nor carries across fields and keeps bit 15 exactly when b < d.)
 __device__ inline int32_t dp_near_below(const DpArgs &a, uint64_t w, uint32_t d) {
   if (w & kDpHeavy) return (int32_t)a.hcnt[(int64_t)(uint32_t)w * (a.R + 1) + d];
-  int32_t k = 0;
-#pragma unroll
-  for (int f = 0; f < 4; f++) k += ((uint32_t)(w >> (16 * f)) & kDpOffMask) < d;
-  return k;
+  constexpr uint64_t kOnes = 0x0001000100010001ull, kHigh = 0x8000800080008000ull;
+  const uint64_t t = (((uint64_t)d * kOnes) | kHigh) - (w + kOnes);
+  return __popcll(t & kHigh);
 }
 
 template <bool PK>
